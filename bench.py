@@ -1,0 +1,324 @@
+#!/usr/bin/env python3
+"""Throughput of ACE grouped adapter execution on one MI355X.
+
+A step is one pass of the whole hot path over one batch of synthetic MoE
+routing, for both execution schemes on the same GPU:
+  ace   -- group-keyed permutation (one row per (token, active group)) and the
+           grouped LoRA forward+backward of the gate and up projections at the
+           consolidated rank r_g; the down projection keeps expert-wise LoRA
+           (its input is expert-specific), with its own expert-keyed permutation.
+  lora  -- expert-wise LoRA (rank r per expert) on gate, up and down.
+Metric: routed (token, expert) pairs per second of the ace step (fwd+bwd), the
+speedup over the lora step, and the HBM roofline fraction of the dominant
+kernel.  Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+from paper_2609_06072_amd import workloads as W  # noqa: E402
+
+METRIC = "routed tokens/s, grouped LoRA fwd+bwd; speedup vs expert-wise; % roofline"
+HBM_PEAK_GBS = 8000.0
+
+
+def algo_bytes(shared: bool, T: int, P: int, d_in: int, d_out: int, R: int, b: int):
+    """Bytes the method must move for one projection (each input read once,
+    y and dx read-modify-written, dA/dB written in fp32)."""
+    rows_in = T if shared else P
+    fwd = b * (rows_in * d_in + 2 * P * d_out + R * (d_in + d_out))
+    bwd = b * (P * d_out + 3 * rows_in * d_in) + R * (d_in + d_out) * (b + 4)
+    return fwd, bwd
+
+
+class Proj:
+    def __init__(self, name, mode, im, ranks, x, A, B, dy, y, dx, dA, dB):
+        self.name, self.mode, self.im, self.ranks = name, mode, im, ranks
+        self.x, self.A, self.B, self.dy, self.y, self.dx, self.dA, self.dB = x, A, B, dy, y, dx, dA, dB
+
+
+class Path:
+    """All buffers of one execution scheme; step() runs the hot path once."""
+
+    def __init__(self, ace, cfg, rt, kind, bufs, ws_perm, ws_bwd):
+        import torch
+        self.ace, self.cfg, self.kind = ace, cfg, kind
+        self.ws_perm, self.ws_bwd = ws_perm, ws_bwd
+        dev = "cuda"
+        self.ids = torch.from_numpy(rt.topk_ids).to(dev)
+        self.e2g = torch.from_numpy(rt.expert_to_group).to(dev)
+        self.G = rt.G
+        self.rt_e = ace.Routing(cfg.T, cfg.k, cfg.E)
+        self.rt_g = ace.Routing(cfg.T, cfg.k, rt.G) if kind == "ace" else None
+        self.projs = []
+        for proj in cfg.projections:
+            d_in, d_out, im = cfg.proj_dims(proj)
+            grouped = kind == "ace" and im == W.INPUT_SHARED
+            ranks = [int(r) for r in rt.group_rank] if grouped else [cfg.r_e] * cfg.E
+            b = bufs[proj]
+            mode = ace.ACE_ROWS_GROUP_DEDUP if grouped else ace.ACE_ROWS_EXPERT
+            self.projs.append(Proj(proj, mode, im, ranks, b["x"], b["A"], b["B"], b["dy"], b["y"],
+                                   b["dx"], b["dA"], b["dB"]))
+        self.timer = None   # (proj name, phase) -> list of (start, end) events
+
+    def _fwd(self, p):
+        a = self.ace
+        if p.mode == a.ACE_ROWS_EXPERT:
+            a.ace_expertwise_lora_fwd(p.x, p.A, p.B, self.cfg.E, self.cfg.r_e, self.cfg.alpha,
+                                      self.rt_e, p.y, input_mode=p.im)
+        else:
+            a.ace_grouped_lora_fwd(p.x, p.A, p.B, p.ranks, self.cfg.alpha, self.rt_g, p.y,
+                                   input_mode=p.im)
+
+    def _bwd(self, p):
+        a = self.ace
+        if p.mode == a.ACE_ROWS_EXPERT:
+            a.ace_expertwise_lora_bwd(p.x, p.A, p.B, self.cfg.E, self.cfg.r_e, self.cfg.alpha,
+                                      self.rt_e, p.dy, p.dx, p.dA, p.dB, input_mode=p.im,
+                                      ws=self.ws_bwd)
+        else:
+            a.ace_grouped_lora_bwd(p.x, p.A, p.B, p.ranks, self.cfg.alpha, self.rt_g, p.dy, p.dx,
+                                   p.dA, p.dB, input_mode=p.im, ws=self.ws_bwd)
+
+    def _timed(self, key, fn, *args):
+        import torch
+        if self.timer is None:
+            return fn(*args)
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        fn(*args)
+        e.record()
+        self.timer.setdefault(key, []).append((s, e))
+
+    def step(self):
+        a = self.ace
+        if self.rt_g is not None:
+            self._timed(("permute", "group"), a.ace_group_permute, self.ids, self.cfg.E, self.e2g,
+                        self.G, a.ACE_ROWS_GROUP_DEDUP, self.rt_g, self.ws_perm)
+        if any(p.mode == a.ACE_ROWS_EXPERT for p in self.projs):
+            self._timed(("permute", "expert"), a.ace_group_permute, self.ids, self.cfg.E, None,
+                        self.cfg.E, a.ACE_ROWS_EXPERT, self.rt_e, self.ws_perm)
+        for p in self.projs:
+            self._timed((p.name, "fwd"), self._fwd, p)
+        for p in reversed(self.projs):
+            self._timed((p.name, "bwd"), self._bwd, p)
+
+
+def make_buffers(cfg, rt, seed=0):
+    import torch
+    bufs = {}
+    dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    dx_shared = None
+    for proj in cfg.projections:
+        t = W.make_proj(cfg, proj, [cfg.r_e] * cfg.E, seed=seed, device="cuda")
+        R = cfg.E * cfg.r_e
+        if t.input_mode == W.INPUT_SHARED:
+            if dx_shared is None:
+                dx_shared = torch.zeros_like(t.x)
+            dx = dx_shared
+        else:
+            dx = torch.zeros_like(t.x)
+        bufs[proj] = dict(x=t.x, A=t.A, B=t.B, dy=t.dy,
+                          y=torch.zeros(cfg.P, t.d_out, dtype=dt, device="cuda"), dx=dx,
+                          dA=torch.zeros(R, t.d_in, dtype=torch.float32, device="cuda"),
+                          dB=torch.zeros(R * t.d_out, dtype=torch.float32, device="cuda"))
+    # gate and up read the same token activations
+    if "gate" in bufs and "up" in bufs:
+        bufs["up"]["x"] = bufs["gate"]["x"]
+    return bufs
+
+
+def time_path(path, steps, warmup, repeats):
+    import torch
+    for _ in range(warmup):
+        path.step()
+    torch.cuda.synchronize()
+    per_step = []
+    path.timer = {}
+    for _ in range(repeats):
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        s.record()
+        for _ in range(steps):
+            path.step()
+        e.record()
+        torch.cuda.synchronize()
+        per_step.append(s.elapsed_time(e) / steps)
+    phases = {f"{k[0]}.{k[1]}": statistics.mean(s.elapsed_time(e) for s, e in v)
+              for k, v in path.timer.items()}
+    path.timer = None
+    return per_step, phases
+
+
+def time_plain(path, steps, repeats):
+    """Step time without per-phase events (the events add a little overhead)."""
+    import torch
+    out = []
+    for _ in range(repeats):
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        s.record()
+        for _ in range(steps):
+            path.step()
+        e.record()
+        torch.cuda.synchronize()
+        out.append(s.elapsed_time(e) / steps)
+    return out
+
+
+def cpu_baseline(cfg, rt, budget_s=15.0):
+    """The fp64 oracle (not tuned) on the first T' tokens of the same workload:
+    ACE step = grouped gate/up + expert-wise down, fwd+bwd."""
+    from oracle import ace_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count() or 1
+    rng = np.random.default_rng(0)
+
+    def run(Tp):
+        ids = rt.topk_ids[:Tp].astype(np.int64)
+        t0 = time.perf_counter()
+        for proj in cfg.projections:
+            d_in, d_out, im = cfg.proj_dims(proj)
+            grouped = im == W.INPUT_SHARED
+            ranks = [int(r) for r in rt.group_rank] if grouped else [cfg.r_e] * cfg.E
+            e2g = rt.expert_to_group if grouped else None
+            n_keys = rt.G if grouped else cfg.E
+            R = sum(ranks)
+            rows = Tp if grouped else Tp * cfg.k
+            x = rng.standard_normal((rows, d_in))
+            A = rng.standard_normal((R, d_in)) / np.sqrt(d_in)
+            B = rng.standard_normal(R * d_out) * 0.02
+            dy = rng.standard_normal((Tp * cfg.k, d_out))
+            O.lora_delta(x, A, B, ranks, cfg.alpha, ids, cfg.E, e2g, n_keys, input_mode=im)
+            O.lora_grads(x, A, B, ranks, cfg.alpha, ids, cfg.E, e2g, n_keys, dy, input_mode=im)
+        return time.perf_counter() - t0
+
+    Tp = min(cfg.T, 64)
+    dt = run(Tp)
+    while dt < 1.0 and Tp < cfg.T:
+        Tp = min(cfg.T, Tp * 4)
+        dt = run(Tp)
+    if dt < budget_s and Tp < cfg.T:
+        Tp = min(cfg.T, max(Tp, int(Tp * budget_s / max(dt, 1e-3))))
+        dt = run(Tp)
+    return {"value": Tp * cfg.k / dt, "unit": "routed tokens/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"first {Tp} of {cfg.T} tokens ({Tp * cfg.k} routed pairs), fwd+bwd of "
+                      f"{'/'.join(cfg.projections)} in fp64 numpy, {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--repeats", type=int, default=5)
+    ap.add_argument("--config", default="olmoe_bf16", choices=W.CONFIG_ORDER)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--phases", action="store_true", help="print per-phase times to stderr")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: the hot path is timed on one MI355X's share of "
+              "the work; multi-GPU runs are not part of this build.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_06072_amd import ace
+
+    cfg = W.CONFIGS[args.config]
+    rt = W.make_routing(cfg, args.seed)
+    torch.cuda.set_device(0)
+    bufs = make_buffers(cfg, rt, args.seed)
+    b = 2 if cfg.dtype == "bf16" else 4
+    r_max = max(int(rt.group_rank.max()), cfg.r_e)
+    n_keys = max(cfg.E, rt.G)
+    ws_perm = torch.empty(max(256, ace.ace_workspace_bytes(ace.ACE_OP_PERMUTE, cfg.T, cfg.k, 0, 0,
+                                                            n_keys, 0)), dtype=torch.uint8,
+                          device="cuda")
+    need = 0
+    for proj in cfg.projections:
+        d_in, d_out, _ = cfg.proj_dims(proj)
+        for nk, r in ((rt.G, int(rt.group_rank.max())), (cfg.E, cfg.r_e)):
+            need = max(need, ace.ace_workspace_bytes(ace.ACE_OP_BWD, cfg.T, cfg.k, d_in, d_out, nk, r))
+    ws_bwd = torch.empty(need, dtype=torch.uint8, device="cuda")
+
+    paths = {kind: Path(ace, cfg, rt, kind, bufs, ws_perm, ws_bwd) for kind in ("ace", "lora")}
+    res = {}
+    for kind, path in paths.items():
+        per_step, phases = time_path(path, args.steps, args.warmup, args.repeats)
+        plain = time_plain(path, args.steps, args.repeats)
+        res[kind] = dict(ms=statistics.median(plain), ms_std=statistics.pstdev(plain),
+                         ms_with_events=statistics.median(per_step), phases=phases)
+
+    # algorithmic bytes of a step and of the dominant kernel
+    T, P = cfg.T, cfg.P
+    step_bytes = 0
+    gate_fwd_bytes = None
+    first = cfg.projections[0]
+    for proj in cfg.projections:
+        d_in, d_out, im = cfg.proj_dims(proj)
+        f, bb = algo_bytes(im == W.INPUT_SHARED, T, P, d_in, d_out, cfg.E * cfg.r_e, b)
+        step_bytes += f + bb
+        if proj == first:
+            gate_fwd_bytes = f
+    ace_ms = res["ace"]["ms"]
+    lora_ms = res["lora"]["ms"]
+    kern_ms = res["ace"]["phases"][f"{first}.fwd"]
+    achieved = gate_fwd_bytes / (kern_ms * 1e-3) / 1e9
+    line = {
+        "metric": METRIC,
+        "value": P / (ace_ms * 1e-3),
+        "unit": "routed tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ace_ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic",
+        "config": {
+            "workload": f"{cfg.name}: T={cfg.T} d_model={cfg.d_model} d_ffn={cfg.d_ffn} "
+                        f"E={cfg.E} top-{cfg.k} routing={cfg.routing[0]}({cfg.routing[1]}) "
+                        f"G={rt.G} expert rank {cfg.r_e} -> group ranks "
+                        f"{sorted(set(int(r) for r in rt.group_rank))}; "
+                        f"LoRA on {'/'.join(cfg.projections)}; grouped gate/up, expert-wise down",
+            "routed_pairs": P, "tokens": T, "parallelism": "single GPU",
+        },
+        "speedup_vs_expertwise": lora_ms / ace_ms,
+        "expertwise": {"value": P / (lora_ms * 1e-3), "ms_per_step": lora_ms},
+        "step_roofline": {"bound": "hbm", "algorithmic_bytes": step_bytes,
+                          "frac_ace": step_bytes / (ace_ms * 1e-3) / (HBM_PEAK_GBS * 1e9),
+                          "frac_expertwise": step_bytes / (lora_ms * 1e-3) / (HBM_PEAK_GBS * 1e9)},
+        "roofline": {"bound": "hbm", "kernel": f"lora_fwd_kernel ({first}, grouped)",
+                     "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None},
+        "phases_ms": {k: {"ace": res["ace"]["phases"].get(k), "lora": res["lora"]["phases"].get(k)}
+                      for k in sorted(set(res["ace"]["phases"]) | set(res["lora"]["phases"]))},
+        "ms_std": {"ace": res["ace"]["ms_std"], "lora": res["lora"]["ms_std"]},
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(cfg, rt)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,212 @@
+/*
+ * ace.h -- C-ABI of libace, grouped adapter execution for MoE LoRA on MI355X.
+ *
+ * Method: ACE (Adapter Consolidation across Experts, arXiv 2609.06072).
+ *   Sec. 3.1    expert-wise LoRA: a routed expert e adds p_e * B_e A_e x.
+ *   Sec. 3.3    rank consolidation: a group G_g shares B_g A_g, with
+ *               A_g in R^{r_g x d_in}, B_g in R^{d_out x r_g},
+ *               r_g = sum of its members' ranks (same parameter budget).
+ *   Sec. 3.4    shared adapter updates: expert e uses the adapter of g(e).
+ *   Sec. 3.5    grouped adapter execution: for the active groups
+ *               A(x) = { g(e) : e in R(x) } of a token, c_g(x) = B_g A_g x is
+ *               computed once and handed to every routed expert of g.
+ *   Appendix "Implementation Details": gate/up projections share the token
+ *               input x (grouped execution applies); the down projection
+ *               takes an expert-specific input per routed pair.
+ *
+ * Conventions for every call
+ *   - Pointers marked "device" are HIP device pointers owned by the caller;
+ *     "host" pointers are read during the call only.  The library keeps no
+ *     pointer after it returns and allocates no device memory.
+ *   - Every call that launches work is asynchronous on `stream` (a
+ *     hipStream_t passed as void*, NULL = the null stream) and does not
+ *     synchronise, except ace_routing_check.
+ *   - Errors: arguments are validated on the host before anything is
+ *     launched; a rejected call returns a negative ace_status, writes
+ *     nothing, and ace_last_error() describes why.  A failed launch returns
+ *     ACE_ERR_HIP.  Faults inside kernels surface at the caller's next sync.
+ *   - Element types: ACE_F32 (float) or ACE_BF16 (bfloat16, RNE).  Matrix
+ *     products accumulate in fp32 on the matrix cores.
+ *   - Row alignment: d_in and d_out must be multiples of 8 (bf16) or 4
+ *     (f32), and x, A, y, dy, dx must be 16-byte aligned.
+ *   - Limits: 1 <= k <= 32, number of keys (experts or groups) <= 256,
+ *     1 <= rank <= 256 per key, T*k < 2^31.
+ *
+ * Parameter layout (the caller's adapter tensors)
+ *   Keys q = 0..n_keys-1 (groups for the grouped calls, experts for the
+ *   expert-wise calls) with ranks r_q and rank offsets roff_q = sum_{q'<q} r_q',
+ *   R = sum_q r_q:
+ *     A  : [R, d_in] row-major; rows roff_q .. roff_q + r_q - 1 are A_q.
+ *     B  : R * d_out elements; key q's block B_q in R^{d_out x r_q}, row-major,
+ *          starts at element d_out * roff_q.
+ *   Gradients dA, dB use the same layouts, in fp32.
+ *   The LoRA scale of key q is s_q = alpha / r_q.
+ *
+ * Outputs of the forward (Sec. 3.4 with the router weight optional):
+ *   y[t*k + j, :] += w[t, j] * s_q * B_q (A_q xin(t, j))   for every routed
+ *   pair (t, j) with q = the key of expert topk_ids[t, j];
+ *   xin(t, j) = x[t] (ACE_INPUT_SHARED) or x[t*k + j] (ACE_INPUT_PER_PAIR);
+ *   w = 1 when pair_w is NULL.
+ */
+#ifndef ACE_H_
+#define ACE_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  ACE_OK = 0,
+  ACE_ERR_INVALID_ARG = -1,  /* bad pointer, size, mode or range            */
+  ACE_ERR_UNSUPPORTED = -2,  /* valid but outside the supported limits      */
+  ACE_ERR_WORKSPACE = -3,    /* workspace missing or smaller than required  */
+  ACE_ERR_HIP = -4           /* a HIP runtime call failed                   */
+} ace_status;
+
+typedef enum { ACE_F32 = 0, ACE_BF16 = 1 } ace_dtype;
+
+typedef enum {
+  /* one row per (token, active group): Sec. 3.5 grouped execution            */
+  ACE_ROWS_GROUP_DEDUP = 0,
+  /* one row per routed pair, keyed by its group: shared adapters run with the
+     expert-wise execution pattern (the paper's "w/o grouped execution")      */
+  ACE_ROWS_GROUP_PAIRS = 1,
+  /* one row per routed pair, keyed by its expert: expert-wise LoRA, Sec. 3.1 */
+  ACE_ROWS_EXPERT = 2
+} ace_row_mode;
+
+typedef enum {
+  ACE_INPUT_SHARED = 0,   /* x is [T, d_in]; every routed expert sees x[t]        */
+  ACE_INPUT_PER_PAIR = 1  /* x is [T*k, d_in]; pair (t,j) has its own row t*k+j   */
+} ace_input_mode;
+
+typedef enum {
+  ACE_OP_PERMUTE = 0,
+  ACE_OP_FWD = 1,
+  ACE_OP_BWD = 2
+} ace_op;
+
+/*
+ * Routing rows produced by ace_group_permute.  The caller allocates the
+ * device arrays (sizes below, P = T*k) and keeps the struct alive while the
+ * forward/backward calls that read it are in flight.  The host fields are
+ * written by ace_group_permute and checked by the other calls.
+ *
+ * Rows are sorted by key, then token, then slot.  Row u serves token
+ * row_token[u]; bit j of row_slots[u] is set for every slot j it serves.
+ * offsets[q] .. offsets[q+1] is key q's segment; offsets[n_keys] = U, the
+ * number of rows (U <= P; in ACE_ROWS_GROUP_DEDUP mode U is the number of
+ * distinct (token, group) pairs, Sec. 3.5).
+ */
+typedef struct ace_routing {
+  int32_t* counts;     /* device [n_keys]    rows per key                           */
+  int32_t* offsets;    /* device [n_keys+1]  exclusive prefix of counts             */
+  int32_t* row_token;  /* device [P]         token of each row (entries >= U unused)*/
+  uint32_t* row_slots; /* device [P]         slot mask of each row                  */
+  int32_t* pair_row;   /* device [P]         row that serves pair t*k+j, -1 if dropped */
+  int32_t* n_dropped;  /* device [1]         pairs dropped for an id out of range   */
+  int32_t n_keys;      /* host: set by ace_group_permute                            */
+  int32_t mode;        /* host: ace_row_mode used                                   */
+  int32_t T, k;        /* host: problem size used                                   */
+} ace_routing;
+
+/*
+ * Route expansion and permutation (Sec. 3.5, the active group set A(x)).
+ *   topk_ids        device int32 [T, k]: routed expert of slot j of token t.
+ *                   An id outside [0, E), or whose group is outside [0, G),
+ *                   drops the pair (counted in rt->n_dropped).
+ *   expert_to_group device int32 [E]: g(e); may be NULL iff mode == ACE_ROWS_EXPERT.
+ *   mode            row mode; n_keys = G for the group modes, E for ACE_ROWS_EXPERT.
+ *   ws, ws_bytes    device scratch, at least
+ *                   ace_workspace_bytes(ACE_OP_PERMUTE, T, k, 0, 0, n_keys, 0);
+ *                   needs no initialisation.
+ * Output arrays of rt are overwritten.  Bit-exact and deterministic.
+ */
+ace_status ace_group_permute(const int32_t* topk_ids, int32_t T, int32_t k, int32_t E,
+                             const int32_t* expert_to_group, int32_t G, ace_row_mode mode,
+                             ace_routing* rt, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Grouped LoRA forward (Sec. 3.4 output, Sec. 3.5 execution).
+ *   group_rank  host int32 [G]: r_g, the consolidated rank of each group.
+ *   alpha       LoRA scaling numerator (s_g = alpha / r_g).
+ *   x           device [T, d_in] (shared) or [T*k, d_in] (per pair), dtype.
+ *   A, B        device, packed as described at the top, dtype.
+ *   pair_w      device fp32 [T, k] or NULL (weight 1).
+ *   rt          rows from ace_group_permute in ACE_ROWS_GROUP_DEDUP (requires
+ *               ACE_INPUT_SHARED) or ACE_ROWS_GROUP_PAIRS mode, with n_keys == G.
+ *   y           device [T*k, d_out], dtype: accumulated (+=).
+ *   ws          none needed (ws may be NULL; ws_bytes is ignored).
+ * One persistent launch: per tile of rows of one group, the shrink h = A_g x,
+ * the expand B_g h, the scale and the add into every slot row.
+ */
+ace_status ace_grouped_lora_fwd(ace_dtype dtype, ace_input_mode input_mode, int32_t T,
+                                int32_t k, int32_t d_in, int32_t d_out, int32_t G,
+                                const int32_t* group_rank, float alpha, const void* x,
+                                const void* A, const void* B, const float* pair_w,
+                                const ace_routing* rt, void* y, void* ws, size_t ws_bytes,
+                                void* stream);
+
+/*
+ * Grouped LoRA backward: gradients of L = <dy, y_out> for the forward above
+ * (Sec. 3.1.2 / 3.4: a shared adapter collects every routed pair of its group).
+ *   dy          device [T*k, d_out], dtype.
+ *   dx          device, shape of x, dtype: accumulated (+=).
+ *   dA          device fp32 [R, d_in]: overwritten (a group with no rows gets 0).
+ *   dB          device fp32, layout of B: overwritten.
+ *   ws          device scratch of at least
+ *               ace_workspace_bytes(ACE_OP_BWD, T, k, d_in, d_out, G, max r_g);
+ *               needs no initialisation.
+ * Deterministic: every output element is reduced in a fixed order.
+ */
+ace_status ace_grouped_lora_bwd(ace_dtype dtype, ace_input_mode input_mode, int32_t T,
+                                int32_t k, int32_t d_in, int32_t d_out, int32_t G,
+                                const int32_t* group_rank, float alpha, const void* x,
+                                const void* A, const void* B, const float* pair_w,
+                                const ace_routing* rt, const void* dy, void* dx, float* dA,
+                                float* dB, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Expert-wise LoRA (Sec. 3.1), the baseline that grouped execution replaces:
+ * every expert owns a rank-`rank` adapter (s = alpha / rank), one row per
+ * routed pair.  Arguments as for the grouped calls with n_keys = E; rt must
+ * come from ace_group_permute in ACE_ROWS_EXPERT mode.
+ */
+ace_status ace_expertwise_lora_fwd(ace_dtype dtype, ace_input_mode input_mode, int32_t T,
+                                   int32_t k, int32_t d_in, int32_t d_out, int32_t E,
+                                   int32_t rank, float alpha, const void* x, const void* A,
+                                   const void* B, const float* pair_w, const ace_routing* rt,
+                                   void* y, void* ws, size_t ws_bytes, void* stream);
+
+ace_status ace_expertwise_lora_bwd(ace_dtype dtype, ace_input_mode input_mode, int32_t T,
+                                   int32_t k, int32_t d_in, int32_t d_out, int32_t E,
+                                   int32_t rank, float alpha, const void* x, const void* A,
+                                   const void* B, const float* pair_w, const ace_routing* rt,
+                                   const void* dy, void* dx, float* dA, float* dB, void* ws,
+                                   size_t ws_bytes, void* stream);
+
+/*
+ * Device scratch needed by an op (bytes, rounded up to 256).  n_keys and
+ * r_max bound the packed rank R <= n_keys * r_max; dtype-independent (sized
+ * for fp32).  Pure host computation.
+ */
+size_t ace_workspace_bytes(ace_op op, int32_t T, int32_t k, int32_t d_in, int32_t d_out,
+                           int32_t n_keys, int32_t r_max);
+
+/*
+ * Copies rt->n_dropped to *n_dropped after synchronising `stream`.  For
+ * tests and debugging; the only call that blocks.
+ */
+ace_status ace_routing_check(const ace_routing* rt, int32_t* n_dropped, void* stream);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* ace_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ACE_H_ */

@@ -1,0 +1,230 @@
+"""ctypes binding of libace (include/ace.h).
+
+Argument marshalling only: torch supplies device memory and the current HIP
+stream; every step of the computation runs in the library's HIP kernels.
+Importing this module loads libace.so and raises if it is missing -- there is
+no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libace.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"libace.so not found at {LIB_PATH}; build it with "
+                      "`python -m paper_2609_06072_amd.build`")
+_lib = ctypes.CDLL(LIB_PATH)
+
+ACE_OK, ACE_ERR_INVALID_ARG, ACE_ERR_UNSUPPORTED, ACE_ERR_WORKSPACE, ACE_ERR_HIP = 0, -1, -2, -3, -4
+ACE_F32, ACE_BF16 = 0, 1
+ACE_ROWS_GROUP_DEDUP, ACE_ROWS_GROUP_PAIRS, ACE_ROWS_EXPERT = 0, 1, 2
+ACE_INPUT_SHARED, ACE_INPUT_PER_PAIR = 0, 1
+ACE_OP_PERMUTE, ACE_OP_FWD, ACE_OP_BWD = 0, 1, 2
+
+EXPORTS = ("ace_group_permute", "ace_grouped_lora_fwd", "ace_grouped_lora_bwd",
+           "ace_expertwise_lora_fwd", "ace_expertwise_lora_bwd", "ace_workspace_bytes",
+           "ace_routing_check", "ace_last_error")
+
+
+class AceRouting(ctypes.Structure):
+    _fields_ = [("counts", ctypes.c_void_p), ("offsets", ctypes.c_void_p),
+                ("row_token", ctypes.c_void_p), ("row_slots", ctypes.c_void_p),
+                ("pair_row", ctypes.c_void_p), ("n_dropped", ctypes.c_void_p),
+                ("n_keys", ctypes.c_int32), ("mode", ctypes.c_int32),
+                ("T", ctypes.c_int32), ("k", ctypes.c_int32)]
+
+
+_i32, _f32, _vp, _sz = ctypes.c_int32, ctypes.c_float, ctypes.c_void_p, ctypes.c_size_t
+_R = ctypes.POINTER(AceRouting)
+_lib.ace_group_permute.argtypes = [_vp, _i32, _i32, _i32, _vp, _i32, _i32, _R, _vp, _sz, _vp]
+_lib.ace_group_permute.restype = _i32
+_FWD = [_i32, _i32, _i32, _i32, _i32, _i32, _i32, _vp, _f32, _vp, _vp, _vp, _vp, _R, _vp, _vp, _sz, _vp]
+_BWD = [_i32, _i32, _i32, _i32, _i32, _i32, _i32, _vp, _f32, _vp, _vp, _vp, _vp, _R, _vp, _vp, _vp,
+        _vp, _vp, _sz, _vp]
+_lib.ace_grouped_lora_fwd.argtypes = _FWD
+_lib.ace_grouped_lora_fwd.restype = _i32
+_lib.ace_grouped_lora_bwd.argtypes = _BWD
+_lib.ace_grouped_lora_bwd.restype = _i32
+_EFWD = list(_FWD)
+_EFWD[7] = _i32          # rank instead of group_rank pointer
+_EBWD = list(_BWD)
+_EBWD[7] = _i32
+_lib.ace_expertwise_lora_fwd.argtypes = _EFWD
+_lib.ace_expertwise_lora_fwd.restype = _i32
+_lib.ace_expertwise_lora_bwd.argtypes = _EBWD
+_lib.ace_expertwise_lora_bwd.restype = _i32
+_lib.ace_workspace_bytes.argtypes = [_i32, _i32, _i32, _i32, _i32, _i32, _i32]
+_lib.ace_workspace_bytes.restype = _sz
+_lib.ace_routing_check.argtypes = [_R, ctypes.POINTER(ctypes.c_int32), _vp]
+_lib.ace_routing_check.restype = _i32
+_lib.ace_last_error.argtypes = []
+_lib.ace_last_error.restype = ctypes.c_char_p
+
+
+class AceError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where} failed with status {status}: {ace_last_error()}")
+
+
+def ace_last_error() -> str:
+    return _lib.ace_last_error().decode()
+
+
+def _check(status: int, where: str) -> None:
+    if status != ACE_OK:
+        raise AceError(status, where)
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensors passed to libace must be contiguous")
+    return t.data_ptr() or None
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream or None
+
+
+def _dtype(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return ACE_BF16
+    if t.dtype == torch.float32:
+        return ACE_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def ace_workspace_bytes(op: int, T: int, k: int, d_in: int, d_out: int, n_keys: int,
+                        r_max: int) -> int:
+    n = _lib.ace_workspace_bytes(op, T, k, d_in, d_out, n_keys, r_max)
+    if n == ctypes.c_size_t(-1).value:
+        raise AceError(ACE_ERR_INVALID_ARG, "ace_workspace_bytes")
+    return int(n)
+
+
+class Routing:
+    """Owns the device arrays of an ace_routing (sized for T*k pairs)."""
+
+    def __init__(self, T: int, k: int, n_keys: int, device="cuda"):
+        P = max(1, T * k)
+        i32 = dict(dtype=torch.int32, device=device)
+        self.counts = torch.zeros(n_keys, **i32)
+        self.offsets = torch.zeros(n_keys + 1, **i32)
+        self.row_token = torch.zeros(P, **i32)
+        self.row_slots = torch.zeros(P, **i32)
+        self.pair_row = torch.zeros(P, **i32)
+        self.n_dropped = torch.zeros(1, **i32)
+        self.c = AceRouting(self.counts.data_ptr(), self.offsets.data_ptr(),
+                            self.row_token.data_ptr(), self.row_slots.data_ptr(),
+                            self.pair_row.data_ptr(), self.n_dropped.data_ptr(), n_keys, -1, T, k)
+
+    @property
+    def n_keys(self) -> int:
+        return self.c.n_keys
+
+    @property
+    def mode(self) -> int:
+        return self.c.mode
+
+
+def ace_group_permute(topk_ids: torch.Tensor, E: int, expert_to_group: Optional[torch.Tensor],
+                      G: int, mode: int, routing: Optional[Routing] = None,
+                      ws: Optional[torch.Tensor] = None, stream=None) -> Routing:
+    T, k = topk_ids.shape
+    n_keys = E if mode == ACE_ROWS_EXPERT else G
+    if routing is None:
+        routing = Routing(T, k, n_keys, device=topk_ids.device)
+    need = ace_workspace_bytes(ACE_OP_PERMUTE, T, k, 0, 0, n_keys, 0)
+    if ws is None:
+        ws = torch.empty(max(need, 256), dtype=torch.uint8, device=topk_ids.device)
+    _check(_lib.ace_group_permute(_ptr(topk_ids), T, k, E, _ptr(expert_to_group), G, mode,
+                                  ctypes.byref(routing.c), _ptr(ws), ws.numel(), _stream(stream)),
+           "ace_group_permute")
+    return routing
+
+
+def ace_routing_check(routing: Routing, stream=None) -> int:
+    n = ctypes.c_int32(0)
+    _check(_lib.ace_routing_check(ctypes.byref(routing.c), ctypes.byref(n), _stream(stream)),
+           "ace_routing_check")
+    return int(n.value)
+
+
+def _ranks_arg(ranks: Sequence[int]):
+    arr = (ctypes.c_int32 * len(ranks))(*[int(r) for r in ranks])
+    return arr
+
+
+def _T_of(x: torch.Tensor, input_mode: int, k: int, routing: Routing) -> int:
+    return routing.c.T
+
+
+def ace_grouped_lora_fwd(x, A, B, group_rank: Sequence[int], alpha: float, routing: Routing,
+                         y, pair_w=None, input_mode: int = ACE_INPUT_SHARED, ws=None,
+                         stream=None) -> None:
+    T, k = routing.c.T, routing.c.k
+    d_in, d_out = A.shape[1], y.shape[1]
+    ranks = _ranks_arg(group_rank)
+    _check(_lib.ace_grouped_lora_fwd(_dtype(x), input_mode, T, k, d_in, d_out, len(group_rank),
+                                     ranks, alpha, _ptr(x), _ptr(A), _ptr(B), _ptr(pair_w),
+                                     ctypes.byref(routing.c), _ptr(y), _ptr(ws),
+                                     0 if ws is None else ws.numel(), _stream(stream)),
+           "ace_grouped_lora_fwd")
+
+
+def ace_grouped_lora_bwd(x, A, B, group_rank: Sequence[int], alpha: float, routing: Routing,
+                         dy, dx, dA, dB, pair_w=None, input_mode: int = ACE_INPUT_SHARED,
+                         ws=None, stream=None) -> None:
+    T, k = routing.c.T, routing.c.k
+    d_in, d_out = A.shape[1], dy.shape[1]
+    ranks = _ranks_arg(group_rank)
+    if ws is None:
+        need = ace_workspace_bytes(ACE_OP_BWD, T, k, d_in, d_out, len(group_rank), max(group_rank))
+        ws = torch.empty(max(need, 256), dtype=torch.uint8, device=A.device)
+    _check(_lib.ace_grouped_lora_bwd(_dtype(A), input_mode, T, k, d_in, d_out, len(group_rank),
+                                     ranks, alpha, _ptr(x), _ptr(A), _ptr(B), _ptr(pair_w),
+                                     ctypes.byref(routing.c), _ptr(dy), _ptr(dx), _ptr(dA),
+                                     _ptr(dB), _ptr(ws), ws.numel(), _stream(stream)),
+           "ace_grouped_lora_bwd")
+
+
+def ace_expertwise_lora_fwd(x, A, B, E: int, rank: int, alpha: float, routing: Routing, y,
+                            pair_w=None, input_mode: int = ACE_INPUT_SHARED, ws=None,
+                            stream=None) -> None:
+    T, k = routing.c.T, routing.c.k
+    d_in, d_out = A.shape[1], y.shape[1]
+    _check(_lib.ace_expertwise_lora_fwd(_dtype(x), input_mode, T, k, d_in, d_out, E, rank, alpha,
+                                        _ptr(x), _ptr(A), _ptr(B), _ptr(pair_w),
+                                        ctypes.byref(routing.c), _ptr(y), _ptr(ws),
+                                        0 if ws is None else ws.numel(), _stream(stream)),
+           "ace_expertwise_lora_fwd")
+
+
+def ace_expertwise_lora_bwd(x, A, B, E: int, rank: int, alpha: float, routing: Routing, dy, dx,
+                            dA, dB, pair_w=None, input_mode: int = ACE_INPUT_SHARED, ws=None,
+                            stream=None) -> None:
+    T, k = routing.c.T, routing.c.k
+    d_in, d_out = A.shape[1], dy.shape[1]
+    if ws is None:
+        need = ace_workspace_bytes(ACE_OP_BWD, T, k, d_in, d_out, E, rank)
+        ws = torch.empty(max(need, 256), dtype=torch.uint8, device=A.device)
+    _check(_lib.ace_expertwise_lora_bwd(_dtype(A), input_mode, T, k, d_in, d_out, E, rank, alpha,
+                                        _ptr(x), _ptr(A), _ptr(B), _ptr(pair_w),
+                                        ctypes.byref(routing.c), _ptr(dy), _ptr(dx), _ptr(dA),
+                                        _ptr(dB), _ptr(ws), ws.numel(), _stream(stream)),
+           "ace_expertwise_lora_bwd")
+
+
+def raw_lib() -> ctypes.CDLL:
+    """The loaded library (tests check exports and host-side validation)."""
+    return _lib

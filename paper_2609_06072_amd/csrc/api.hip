@@ -1,0 +1,286 @@
+// C-ABI entry points of libace: argument validation on the host, then the
+// kernel launches of permute.hip, lora_fwd.hip and lora_bwd.hip on the
+// caller's stream.  No call allocates device memory or synchronises (except
+// ace_routing_check).
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <cmath>
+#include <string>
+
+#include "ace_internal.hpp"
+
+namespace ace {
+
+namespace {
+
+thread_local std::string g_err;
+
+ace_status fail(ace_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+ace_status ok() {
+  g_err.clear();
+  return ACE_OK;
+}
+
+ace_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return ok();
+  return fail(ACE_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+size_t round256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+// Shared validation of the forward/backward calls; fills the Problem.
+ace_status check_problem(Problem& p, ace_dtype dtype, ace_input_mode im, int32_t T, int32_t k,
+                         int32_t d_in, int32_t d_out, int32_t n_keys, const int32_t* ranks,
+                         int32_t uniform_rank, float alpha, const void* x, const void* A,
+                         const void* B, const float* pair_w, const ace_routing* rt,
+                         bool expertwise) {
+  if (dtype != ACE_F32 && dtype != ACE_BF16) return fail(ACE_ERR_INVALID_ARG, "unknown dtype %d", (int)dtype);
+  if (im != ACE_INPUT_SHARED && im != ACE_INPUT_PER_PAIR)
+    return fail(ACE_ERR_INVALID_ARG, "unknown input mode %d", (int)im);
+  if (T < 0) return fail(ACE_ERR_INVALID_ARG, "T = %d < 0", T);
+  if (k < 1 || k > kMaxK) return fail(ACE_ERR_UNSUPPORTED, "k = %d outside [1, %d]", k, kMaxK);
+  if ((int64_t)T * k >= (int64_t)1 << 31) return fail(ACE_ERR_UNSUPPORTED, "T*k >= 2^31");
+  const int vec = dtype == ACE_BF16 ? 8 : 4;
+  if (d_in < 1 || d_out < 1) return fail(ACE_ERR_INVALID_ARG, "d_in = %d, d_out = %d", d_in, d_out);
+  if (d_in % vec || d_out % vec)
+    return fail(ACE_ERR_UNSUPPORTED, "d_in (%d) and d_out (%d) must be multiples of %d", d_in,
+                d_out, vec);
+  if (n_keys < 1 || n_keys > kMaxKeys)
+    return fail(ACE_ERR_UNSUPPORTED, "%s count %d outside [1, %d]", expertwise ? "expert" : "group",
+                n_keys, kMaxKeys);
+  if (!expertwise && !ranks) return fail(ACE_ERR_INVALID_ARG, "group_rank is NULL");
+  if (!std::isfinite(alpha)) return fail(ACE_ERR_INVALID_ARG, "alpha is not finite");
+  if (!rt) return fail(ACE_ERR_INVALID_ARG, "routing is NULL");
+  if (!rt->offsets || !rt->counts) return fail(ACE_ERR_INVALID_ARG, "routing arrays are NULL");
+  if (T > 0 && (!rt->row_token || !rt->row_slots))
+    return fail(ACE_ERR_INVALID_ARG, "routing arrays are NULL");
+  if (rt->T != T || rt->k != k)
+    return fail(ACE_ERR_INVALID_ARG, "routing was built for T=%d k=%d, call has T=%d k=%d", rt->T,
+                rt->k, T, k);
+  if (rt->n_keys != n_keys)
+    return fail(ACE_ERR_INVALID_ARG, "routing has %d keys, call has %d", rt->n_keys, n_keys);
+  if (expertwise) {
+    if (rt->mode != ACE_ROWS_EXPERT)
+      return fail(ACE_ERR_INVALID_ARG, "expert-wise calls need ACE_ROWS_EXPERT routing");
+  } else {
+    if (rt->mode == ACE_ROWS_GROUP_DEDUP) {
+      if (im != ACE_INPUT_SHARED)
+        return fail(ACE_ERR_INVALID_ARG, "ACE_ROWS_GROUP_DEDUP needs ACE_INPUT_SHARED");
+    } else if (rt->mode != ACE_ROWS_GROUP_PAIRS) {
+      return fail(ACE_ERR_INVALID_ARG, "grouped calls need group-keyed routing");
+    }
+  }
+  if (!A || !B) return fail(ACE_ERR_INVALID_ARG, "A or B is NULL");
+  if (T > 0 && !x) return fail(ACE_ERR_INVALID_ARG, "x is NULL");
+  if (!aligned(A, 16) || !aligned(B, 16) || !aligned(x, 16))
+    return fail(ACE_ERR_INVALID_ARG, "x, A and B must be 16-byte aligned");
+  if (!aligned(pair_w, 4)) return fail(ACE_ERR_INVALID_ARG, "pair_w misaligned");
+  p.keys = KeyTable{};
+  p.keys.n_keys = n_keys;
+  int R = 0, rmax = 0;
+  for (int q = 0; q < n_keys; ++q) {
+    const int r = expertwise ? uniform_rank : ranks[q];
+    if (r < 1 || r > kMaxRank)
+      return fail(ACE_ERR_UNSUPPORTED, "rank %d of key %d outside [1, %d]", r, q, kMaxRank);
+    p.keys.rank[q] = r;
+    p.keys.roff[q] = R;
+    R += r;
+    rmax = r > rmax ? r : rmax;
+  }
+  p.keys.roff[n_keys] = R;
+  p.keys.R = R;
+  p.r_max = rmax;
+  p.dtype = dtype;
+  p.per_pair = im == ACE_INPUT_PER_PAIR;
+  p.T = T;
+  p.k = k;
+  p.d_in = d_in;
+  p.d_out = d_out;
+  p.alpha = alpha;
+  p.x = x;
+  p.A = A;
+  p.B = B;
+  p.pair_w = pair_w;
+  p.rt = rt;
+  return ok();
+}
+
+ace_status run_fwd(const Problem& p, void* y, void* stream) {
+  if (p.T > 0 && !y) return fail(ACE_ERR_INVALID_ARG, "y is NULL");
+  if (!aligned(y, 16)) return fail(ACE_ERR_INVALID_ARG, "y must be 16-byte aligned");
+  if (p.T == 0) return ok();
+  return hip_status(launch_fwd(p, y, static_cast<hipStream_t>(stream)), "forward launch");
+}
+
+ace_status run_bwd(const Problem& p, const void* dy, void* dx, float* dA, float* dB, void* ws,
+                   size_t ws_bytes, void* stream) {
+  if (p.T > 0 && (!dy || !dx)) return fail(ACE_ERR_INVALID_ARG, "dy or dx is NULL");
+  if (!dA || !dB) return fail(ACE_ERR_INVALID_ARG, "dA or dB is NULL");
+  if (!aligned(dy, 16) || !aligned(dx, 16))
+    return fail(ACE_ERR_INVALID_ARG, "dy and dx must be 16-byte aligned");
+  if (!aligned(dA, 4) || !aligned(dB, 4)) return fail(ACE_ERR_INVALID_ARG, "dA/dB misaligned");
+  const size_t need = bwd_ws_bytes(p.T, p.k, p.d_in, p.d_out, p.keys.R);
+  if (!ws || ws_bytes < need)
+    return fail(ACE_ERR_WORKSPACE, "backward needs %zu workspace bytes, got %zu", need,
+                ws ? ws_bytes : (size_t)0);
+  if (!aligned(ws, 256)) return fail(ACE_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  return hip_status(launch_bwd(p, dy, dx, dA, dB, ws, static_cast<hipStream_t>(stream)),
+                    "backward launch");
+}
+
+}  // namespace
+
+int device_cu_count() {
+  static int cache[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cache[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    cache[dev] = n;
+  }
+  return cache[dev];
+}
+
+}  // namespace ace
+
+using namespace ace;
+
+extern "C" {
+
+ace_status ace_group_permute(const int32_t* topk_ids, int32_t T, int32_t k, int32_t E,
+                             const int32_t* expert_to_group, int32_t G, ace_row_mode mode,
+                             ace_routing* rt, void* ws, size_t ws_bytes, void* stream) {
+  if (!rt) return fail(ACE_ERR_INVALID_ARG, "routing is NULL");
+  if (mode != ACE_ROWS_GROUP_DEDUP && mode != ACE_ROWS_GROUP_PAIRS && mode != ACE_ROWS_EXPERT)
+    return fail(ACE_ERR_INVALID_ARG, "unknown row mode %d", (int)mode);
+  if (T < 0) return fail(ACE_ERR_INVALID_ARG, "T = %d < 0", T);
+  if (k < 1 || k > kMaxK) return fail(ACE_ERR_UNSUPPORTED, "k = %d outside [1, %d]", k, kMaxK);
+  if ((int64_t)T * k >= (int64_t)1 << 31) return fail(ACE_ERR_UNSUPPORTED, "T*k >= 2^31");
+  if (E < 1 || E > kMaxKeys) return fail(ACE_ERR_UNSUPPORTED, "E = %d outside [1, %d]", E, kMaxKeys);
+  int n_keys = E;
+  if (mode != ACE_ROWS_EXPERT) {
+    if (G < 1 || G > kMaxKeys) return fail(ACE_ERR_UNSUPPORTED, "G = %d outside [1, %d]", G, kMaxKeys);
+    if (!expert_to_group) return fail(ACE_ERR_INVALID_ARG, "expert_to_group is NULL");
+    n_keys = G;
+  }
+  if (T > 0 && !topk_ids) return fail(ACE_ERR_INVALID_ARG, "topk_ids is NULL");
+  if (!rt->counts || !rt->offsets || !rt->n_dropped)
+    return fail(ACE_ERR_INVALID_ARG, "routing arrays are NULL");
+  if (T > 0 && (!rt->row_token || !rt->row_slots || !rt->pair_row))
+    return fail(ACE_ERR_INVALID_ARG, "routing arrays are NULL");
+  const size_t need = permute_ws_bytes(T, k, n_keys);
+  if (need > 0 && (!ws || ws_bytes < need))
+    return fail(ACE_ERR_WORKSPACE, "permute needs %zu workspace bytes, got %zu", need,
+                ws ? ws_bytes : (size_t)0);
+  if (!aligned(ws, 4)) return fail(ACE_ERR_WORKSPACE, "workspace misaligned");
+  rt->n_keys = n_keys;
+  rt->mode = mode;
+  rt->T = T;
+  rt->k = k;
+  return hip_status(launch_permute(topk_ids, T, k, E, expert_to_group, G, mode, n_keys, rt, ws,
+                                   static_cast<hipStream_t>(stream)),
+                    "permute launch");
+}
+
+ace_status ace_grouped_lora_fwd(ace_dtype dtype, ace_input_mode input_mode, int32_t T,
+                                int32_t k, int32_t d_in, int32_t d_out, int32_t G,
+                                const int32_t* group_rank, float alpha, const void* x,
+                                const void* A, const void* B, const float* pair_w,
+                                const ace_routing* rt, void* y, void* ws, size_t ws_bytes,
+                                void* stream) {
+  (void)ws;
+  (void)ws_bytes;
+  Problem p;
+  ace_status s = check_problem(p, dtype, input_mode, T, k, d_in, d_out, G, group_rank, 0, alpha,
+                               x, A, B, pair_w, rt, false);
+  if (s != ACE_OK) return s;
+  return run_fwd(p, y, stream);
+}
+
+ace_status ace_grouped_lora_bwd(ace_dtype dtype, ace_input_mode input_mode, int32_t T,
+                                int32_t k, int32_t d_in, int32_t d_out, int32_t G,
+                                const int32_t* group_rank, float alpha, const void* x,
+                                const void* A, const void* B, const float* pair_w,
+                                const ace_routing* rt, const void* dy, void* dx, float* dA,
+                                float* dB, void* ws, size_t ws_bytes, void* stream) {
+  Problem p;
+  ace_status s = check_problem(p, dtype, input_mode, T, k, d_in, d_out, G, group_rank, 0, alpha,
+                               x, A, B, pair_w, rt, false);
+  if (s != ACE_OK) return s;
+  return run_bwd(p, dy, dx, dA, dB, ws, ws_bytes, stream);
+}
+
+ace_status ace_expertwise_lora_fwd(ace_dtype dtype, ace_input_mode input_mode, int32_t T,
+                                   int32_t k, int32_t d_in, int32_t d_out, int32_t E,
+                                   int32_t rank, float alpha, const void* x, const void* A,
+                                   const void* B, const float* pair_w, const ace_routing* rt,
+                                   void* y, void* ws, size_t ws_bytes, void* stream) {
+  (void)ws;
+  (void)ws_bytes;
+  Problem p;
+  ace_status s = check_problem(p, dtype, input_mode, T, k, d_in, d_out, E, nullptr, rank, alpha,
+                               x, A, B, pair_w, rt, true);
+  if (s != ACE_OK) return s;
+  return run_fwd(p, y, stream);
+}
+
+ace_status ace_expertwise_lora_bwd(ace_dtype dtype, ace_input_mode input_mode, int32_t T,
+                                   int32_t k, int32_t d_in, int32_t d_out, int32_t E,
+                                   int32_t rank, float alpha, const void* x, const void* A,
+                                   const void* B, const float* pair_w, const ace_routing* rt,
+                                   const void* dy, void* dx, float* dA, float* dB, void* ws,
+                                   size_t ws_bytes, void* stream) {
+  Problem p;
+  ace_status s = check_problem(p, dtype, input_mode, T, k, d_in, d_out, E, nullptr, rank, alpha,
+                               x, A, B, pair_w, rt, true);
+  if (s != ACE_OK) return s;
+  return run_bwd(p, dy, dx, dA, dB, ws, ws_bytes, stream);
+}
+
+size_t ace_workspace_bytes(ace_op op, int32_t T, int32_t k, int32_t d_in, int32_t d_out,
+                           int32_t n_keys, int32_t r_max) {
+  if (T < 0 || k < 1 || k > kMaxK || n_keys < 1 || n_keys > kMaxKeys) {
+    fail(ACE_ERR_INVALID_ARG, "invalid workspace query");
+    return (size_t)-1;
+  }
+  switch (op) {
+    case ACE_OP_PERMUTE:
+      return round256(permute_ws_bytes(T, k, n_keys));
+    case ACE_OP_FWD:
+      return 0;
+    case ACE_OP_BWD:
+      if (d_in < 1 || d_out < 1 || r_max < 1 || r_max > kMaxRank) {
+        fail(ACE_ERR_INVALID_ARG, "invalid workspace query");
+        return (size_t)-1;
+      }
+      return round256(bwd_ws_bytes(T, k, d_in, d_out, n_keys * r_max));
+  }
+  fail(ACE_ERR_INVALID_ARG, "unknown op %d", (int)op);
+  return (size_t)-1;
+}
+
+ace_status ace_routing_check(const ace_routing* rt, int32_t* n_dropped, void* stream) {
+  if (!rt || !rt->n_dropped || !n_dropped) return fail(ACE_ERR_INVALID_ARG, "NULL argument");
+  hipError_t e = hipStreamSynchronize(static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_status(e, "stream synchronize");
+  return hip_status(hipMemcpy(n_dropped, rt->n_dropped, sizeof(int32_t), hipMemcpyDeviceToHost),
+                    "copy n_dropped");
+}
+
+const char* ace_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,215 @@
+// Route expansion and permutation (Sec. 3.5: the active group set A(x) of each
+// token, one row per (token, active group); or one row per routed pair for the
+// expert-wise and "shared adapter, per-pair" modes).
+//
+// A stable counting sort of the emitted rows by key, in three launches:
+//   count   -- each block owns a chunk of whole tokens (<= 1024 pairs).  The
+//              block's keys go to LDS; each emitted row sets the bit of its
+//              local pair index in a per-key bitmap (LDS, ds_or_b64), and the
+//              per-(key, block) population counts are written key-major.
+//   scan    -- one block: exclusive scan of the key-major counts gives each
+//              (key, block) its first row; counts/offsets/n_dropped written.
+//   scatter -- rebuilds the bitmap; a row's rank inside its (key, block) cell
+//              is the popcount of the lower bits, so rows come out sorted by
+//              (key, token, slot) with no atomics on rows and no sort.
+#include "ace_device.hpp"
+#include "ace_internal.hpp"
+
+namespace ace {
+
+namespace {
+
+constexpr int kPairsPerBlock = 1024;
+constexpr int kWordsPerKey = kPairsPerBlock / 64;
+
+struct PermArgs {
+  const int32_t* ids;
+  const int32_t* e2g;  // null in expert mode
+  int32_t T, k, E, G, mode, n_keys;
+  int32_t tokens_per_block, nblk;
+  int32_t* cell;       // [n_keys * nblk] counts, then (scan) first rows
+  int32_t* drops;      // [nblk]
+  int32_t* counts;
+  int32_t* offsets;
+  int32_t* row_token;
+  uint32_t* row_slots;
+  int32_t* pair_row;
+  int32_t* n_dropped;
+};
+
+// Stage the block's pair keys (-1 = dropped) and mark emitted rows in the
+// per-key bitmaps.  Returns the number of dropped pairs seen by this thread.
+__device__ int stage_and_mark(const PermArgs& a, int p0, int np, int* keys, uint32_t* masks,
+                              unsigned long long* bits) {
+  const int t = threadIdx.x;
+  int drops = 0;
+  for (int i = t; i < a.n_keys * kWordsPerKey; i += kThreads) bits[i] = 0ull;
+  for (int lp = t; lp < np; lp += kThreads) {
+    const int e = a.ids[p0 + lp];
+    int q = -1;
+    if (e >= 0 && e < a.E) {
+      if (a.mode == ACE_ROWS_EXPERT) {
+        q = e;
+      } else {
+        const int g = a.e2g[e];
+        q = (g >= 0 && g < a.G) ? g : -1;
+      }
+    }
+    drops += q < 0;
+    keys[lp] = q;
+  }
+  __syncthreads();
+  const int k = a.k;
+  for (int lp = t; lp < np; lp += kThreads) {
+    const int q = keys[lp];
+    if (q < 0) { masks[lp] = 0u; continue; }
+    uint32_t m = 1u << (lp % k);
+    bool emit = true;
+    if (a.mode == ACE_ROWS_GROUP_DEDUP) {
+      // leader = first slot of the token with this group; mask = all of them
+      const int j = lp % k, tb = lp - j;
+      for (int jj = 0; jj < k; ++jj) {
+        if (keys[tb + jj] != q) continue;
+        if (jj < j) { emit = false; break; }
+        m |= 1u << jj;
+      }
+    }
+    masks[lp] = emit ? m : 0u;
+    if (emit) atomicOr(&bits[q * kWordsPerKey + (lp >> 6)], 1ull << (lp & 63));
+  }
+  __syncthreads();
+  return drops;
+}
+
+__global__ __launch_bounds__(kThreads) void permute_count_kernel(PermArgs a) {
+  extern __shared__ unsigned long long bits[];  // [n_keys * kWordsPerKey]
+  __shared__ int keys[kPairsPerBlock];
+  __shared__ uint32_t masks[kPairsPerBlock];
+  __shared__ int red[kThreads];
+  const int b = blockIdx.x;
+  const int p0 = b * a.tokens_per_block * a.k;
+  const int np = min(a.tokens_per_block * a.k, a.T * a.k - p0);
+  const int d = stage_and_mark(a, p0, np, keys, masks, bits);
+  for (int q = threadIdx.x; q < a.n_keys; q += kThreads) {
+    int c = 0;
+#pragma unroll
+    for (int w = 0; w < kWordsPerKey; ++w) c += __popcll(bits[q * kWordsPerKey + w]);
+    a.cell[q * a.nblk + b] = c;
+  }
+  int total;
+  block_exclusive_scan(d, red, &total);
+  if (threadIdx.x == 0) a.drops[b] = total;
+}
+
+// One block of 1024 threads: exclusive scan over n_keys * nblk cells.
+__global__ __launch_bounds__(1024) void permute_scan_kernel(PermArgs a) {
+  __shared__ int part[1024];
+  const int t = threadIdx.x;
+  const int N = a.n_keys * a.nblk;
+  const int per = (N + 1023) / 1024;
+  const int lo = min(N, t * per), hi = min(N, lo + per);
+  int s = 0;
+  for (int i = lo; i < hi; ++i) s += a.cell[i];
+  part[t] = s;
+  __syncthreads();
+  for (int off = 1; off < 1024; off <<= 1) {
+    const int add = t >= off ? part[t - off] : 0;
+    __syncthreads();
+    part[t] += add;
+    __syncthreads();
+  }
+  int run = part[t] - s;  // exclusive prefix of this thread's range
+  for (int i = lo; i < hi; ++i) {
+    const int c = a.cell[i];
+    a.cell[i] = run;
+    run += c;
+  }
+  __syncthreads();
+  const int U = part[1023];
+  for (int q = t; q < a.n_keys; q += 1024) {
+    const int first = a.nblk > 0 ? a.cell[q * a.nblk] : 0;
+    const int next = (q + 1 < a.n_keys && a.nblk > 0) ? a.cell[(q + 1) * a.nblk] : U;
+    a.offsets[q] = first;
+    a.counts[q] = next - first;
+  }
+  if (t == 0) {
+    a.offsets[a.n_keys] = U;
+    int d = 0;
+    for (int b = 0; b < a.nblk; ++b) d += a.drops[b];
+    *a.n_dropped = d;
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void permute_scatter_kernel(PermArgs a) {
+  extern __shared__ unsigned long long bits[];
+  __shared__ int keys[kPairsPerBlock];
+  __shared__ uint32_t masks[kPairsPerBlock];
+  const int b = blockIdx.x;
+  const int k = a.k;
+  const int p0 = b * a.tokens_per_block * k;
+  const int np = min(a.tokens_per_block * k, a.T * k - p0);
+  stage_and_mark(a, p0, np, keys, masks, bits);
+  for (int lp = threadIdx.x; lp < np; lp += kThreads) {
+    const int q = keys[lp];
+    if (q < 0) {
+      a.pair_row[p0 + lp] = -1;
+      continue;
+    }
+    const uint32_t m = masks[lp];
+    if (m == 0u) continue;  // served by its token's leader slot
+    const unsigned long long* kb = bits + q * kWordsPerKey;
+    const int w = lp >> 6;
+    int rank = __popcll(kb[w] & ((1ull << (lp & 63)) - 1ull));
+    for (int i = 0; i < w; ++i) rank += __popcll(kb[i]);
+    const int row = a.cell[q * a.nblk + b] + rank;
+    const int tok = (p0 + lp) / k;
+    a.row_token[row] = tok;
+    a.row_slots[row] = m;
+    for (uint32_t mm = m; mm; mm &= mm - 1u) a.pair_row[tok * k + __builtin_ctz(mm)] = row;
+  }
+}
+
+}  // namespace
+
+size_t permute_ws_bytes(int T, int k, int n_keys) {
+  const int tpb = permute_tokens_per_block(k);
+  const long nblk = T > 0 ? (T + tpb - 1) / tpb : 0;
+  return (size_t)(nblk * n_keys + nblk) * sizeof(int32_t);
+}
+
+int permute_tokens_per_block(int k) { return k > 0 ? kPairsPerBlock / k : 1; }
+
+hipError_t launch_permute(const int32_t* ids, int T, int k, int E, const int32_t* e2g, int G,
+                          int mode, int n_keys, const ace_routing* rt, void* ws,
+                          hipStream_t stream) {
+  PermArgs a{};
+  a.ids = ids;
+  a.e2g = e2g;
+  a.T = T;
+  a.k = k;
+  a.E = E;
+  a.G = G;
+  a.mode = mode;
+  a.n_keys = n_keys;
+  a.tokens_per_block = permute_tokens_per_block(k);
+  a.nblk = T > 0 ? (T + a.tokens_per_block - 1) / a.tokens_per_block : 0;
+  a.cell = static_cast<int32_t*>(ws);
+  a.drops = a.cell + (size_t)a.nblk * n_keys;
+  a.counts = rt->counts;
+  a.offsets = rt->offsets;
+  a.row_token = rt->row_token;
+  a.row_slots = rt->row_slots;
+  a.pair_row = rt->pair_row;
+  a.n_dropped = rt->n_dropped;
+  const size_t lds = (size_t)n_keys * kWordsPerKey * sizeof(unsigned long long);
+  if (a.nblk > 0) {
+    permute_count_kernel<<<a.nblk, kThreads, lds, stream>>>(a);
+  }
+  permute_scan_kernel<<<1, 1024, 0, stream>>>(a);
+  if (a.nblk > 0) {
+    permute_scatter_kernel<<<a.nblk, kThreads, lds, stream>>>(a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace ace

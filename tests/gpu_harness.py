@@ -1,0 +1,139 @@
+"""Shared helpers of the GPU parity tests: run one projection through the HIP
+library (C-ABI via the ctypes binding) and through the fp64 oracle on the
+same seeded inputs."""
+from __future__ import annotations
+
+import dataclasses
+import sys
+from typing import Optional, Sequence
+
+import numpy as np
+import torch
+
+from oracle import ace_oracle as O
+from paper_2609_06072_amd import workloads as W
+
+TOL = {"bf16": 2e-2, "f32": 1e-5}
+
+PATHS = {
+    # name: (row mode, input mode override (None = projection's), key kind)
+    "grouped": (W.ROWS_GROUP_DEDUP, W.INPUT_SHARED, "group"),
+    "expertwise": (W.ROWS_EXPERT, W.INPUT_SHARED, "expert"),
+    "down_expertwise": (W.ROWS_EXPERT, W.INPUT_PER_PAIR, "expert"),
+    "pairs_shared": (W.ROWS_GROUP_PAIRS, W.INPUT_SHARED, "group"),
+    "pairs_per_pair": (W.ROWS_GROUP_PAIRS, W.INPUT_PER_PAIR, "group"),
+}
+
+
+def say(msg: str) -> None:
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@dataclasses.dataclass
+class Case:
+    cfg: W.MoEConfig
+    rt: W.Routing
+    mode: int
+    input_mode: int
+    ranks: list
+    e2g: Optional[np.ndarray]   # None for expert keys
+    n_keys: int
+    d_in: int
+    d_out: int
+    x: torch.Tensor
+    A: torch.Tensor
+    B: torch.Tensor
+    dy: torch.Tensor
+    pair_w: Optional[torch.Tensor]
+
+
+def make_case(cfg: W.MoEConfig, path: str, seed: int = 0, with_w: bool = False,
+              device: str = "cuda", proj: Optional[str] = None) -> Case:
+    mode, im, kind = PATHS[path]
+    rt = W.make_routing(cfg, seed)
+    if proj is None:
+        if im == W.INPUT_PER_PAIR:
+            proj = "down"
+        else:
+            proj = "gate" if "gate" in cfg.projections else cfg.projections[0]
+    if kind == "group":
+        ranks = [int(r) for r in rt.group_rank]
+        e2g = rt.expert_to_group
+        n_keys = rt.G
+    else:
+        ranks = [cfg.r_e] * cfg.E
+        e2g = None
+        n_keys = cfg.E
+    t = W.make_proj(cfg, proj, ranks, seed=seed, device=device)
+    x = t.x
+    if t.input_mode != im:
+        rows = cfg.T if im == W.INPUT_SHARED else cfg.P
+        x = W.draw_tensor((rows, t.d_in), 1.0, seed, "x" if im == W.INPUT_SHARED else "h",
+                          cfg.dtype, device)
+    pair_w = torch.from_numpy(rt.topk_w).to(device) if with_w else None
+    return Case(cfg, rt, mode, im, ranks, e2g, n_keys, t.d_in, t.d_out, x, t.A, t.B, t.dy, pair_w)
+
+
+def run_gpu(c: Case, fwd: bool = True, bwd: bool = True, y_in=None, dx_in=None):
+    from paper_2609_06072_amd import ace
+    dev = c.x.device
+    ids = torch.from_numpy(c.rt.topk_ids).to(dev)
+    e2g = torch.from_numpy(c.rt.expert_to_group).to(dev)
+    routing = ace.ace_group_permute(ids, c.cfg.E, None if c.mode == W.ROWS_EXPERT else e2g,
+                                    c.rt.G, c.mode)
+    out = {"routing": routing}
+    P = c.cfg.P
+    if fwd:
+        y = torch.zeros(P, c.d_out, dtype=c.x.dtype, device=dev) if y_in is None else y_in.clone()
+        if c.mode == W.ROWS_EXPERT:
+            ace.ace_expertwise_lora_fwd(c.x, c.A, c.B, c.cfg.E, c.cfg.r_e, c.cfg.alpha, routing, y,
+                                        pair_w=c.pair_w, input_mode=c.input_mode)
+        else:
+            ace.ace_grouped_lora_fwd(c.x, c.A, c.B, c.ranks, c.cfg.alpha, routing, y,
+                                     pair_w=c.pair_w, input_mode=c.input_mode)
+        out["y"] = y
+    if bwd:
+        dx = torch.zeros_like(c.x) if dx_in is None else dx_in.clone()
+        R = sum(c.ranks)
+        dA = torch.full((R, c.d_in), float("nan"), dtype=torch.float32, device=dev)
+        dB = torch.full((R * c.d_out,), float("nan"), dtype=torch.float32, device=dev)
+        if c.mode == W.ROWS_EXPERT:
+            ace.ace_expertwise_lora_bwd(c.x, c.A, c.B, c.cfg.E, c.cfg.r_e, c.cfg.alpha, routing,
+                                        c.dy, dx, dA, dB, pair_w=c.pair_w, input_mode=c.input_mode)
+        else:
+            ace.ace_grouped_lora_bwd(c.x, c.A, c.B, c.ranks, c.cfg.alpha, routing, c.dy, dx, dA,
+                                     dB, pair_w=c.pair_w, input_mode=c.input_mode)
+        out.update(dx=dx, dA=dA, dB=dB)
+    torch.cuda.synchronize()
+    return out
+
+
+def f64(t: torch.Tensor) -> np.ndarray:
+    return t.detach().to("cpu", torch.float64).numpy()
+
+
+def oracle_args(c: Case, ids: Optional[np.ndarray] = None, x: Optional[np.ndarray] = None,
+                w: Optional[np.ndarray] = None):
+    ids = c.rt.topk_ids.astype(np.int64) if ids is None else ids
+    x = f64(c.x) if x is None else x
+    if w is None and c.pair_w is not None:
+        w = c.rt.topk_w.astype(np.float64)
+    return (x, f64(c.A), f64(c.B), c.ranks, c.cfg.alpha, ids, c.cfg.E, c.e2g, c.n_keys), w
+
+
+def oracle_fwd(c: Case) -> np.ndarray:
+    a, w = oracle_args(c)
+    return O.lora_delta(*a, input_mode=c.input_mode, pair_w=w)
+
+
+def oracle_bwd(c: Case):
+    a, w = oracle_args(c)
+    return O.lora_grads(*a, f64(c.dy), input_mode=c.input_mode, pair_w=w)
+
+
+def check_rel(name: str, got, ref, tol: float) -> float:
+    e = O.rel_l2(got, ref)
+    assert np.all(np.isfinite(np.asarray(got))), f"{name}: non-finite values"
+    assert e <= tol, f"{name}: rel L2 {e:.3e} > {tol:.1e}"
+    return e

