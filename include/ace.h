@@ -139,9 +139,11 @@ ace_status ace_group_permute(const int32_t* topk_ids, int32_t T, int32_t k, int3
  *   rt          rows from ace_group_permute in ACE_ROWS_GROUP_DEDUP (requires
  *               ACE_INPUT_SHARED) or ACE_ROWS_GROUP_PAIRS mode, with n_keys == G.
  *   y           device [T*k, d_out], dtype: accumulated (+=).
- *   ws          none needed (ws may be NULL; ws_bytes is ignored).
- * One persistent launch: per tile of rows of one group, the shrink h = A_g x,
- * the expand B_g h, the scale and the add into every slot row.
+ *   ws          device scratch of at least
+ *               ace_workspace_bytes(ACE_OP_FWD, T, k, d_in, d_out, G, max r_g)
+ *               (it holds h = (alpha/r_g) A_g x per row); no initialisation.
+ * Two launches: the shrink h once per row of the permutation, then the
+ * expand B_g h added into every slot the row serves.
  */
 ace_status ace_grouped_lora_fwd(ace_dtype dtype, ace_input_mode input_mode, int32_t T,
                                 int32_t k, int32_t d_in, int32_t d_out, int32_t G,
@@ -191,7 +193,7 @@ ace_status ace_expertwise_lora_bwd(ace_dtype dtype, ace_input_mode input_mode, i
 /*
  * Device scratch needed by an op (bytes, rounded up to 256).  n_keys and
  * r_max bound the packed rank R <= n_keys * r_max; dtype-independent (sized
- * for fp32).  Pure host computation.
+ * for fp32).  Pure host computation; (size_t)-1 for invalid arguments.
  */
 size_t ace_workspace_bytes(ace_op op, int32_t T, int32_t k, int32_t d_in, int32_t d_out,
                            int32_t n_keys, int32_t r_max);

@@ -165,8 +165,11 @@ def _ranks_arg(ranks: Sequence[int]):
     return arr
 
 
-def _T_of(x: torch.Tensor, input_mode: int, k: int, routing: Routing) -> int:
-    return routing.c.T
+def _fwd_ws(ws, T, k, d_in, d_out, n_keys, r_max, device):
+    if ws is not None:
+        return ws
+    need = ace_workspace_bytes(ACE_OP_FWD, T, k, d_in, d_out, n_keys, r_max)
+    return torch.empty(max(need, 256), dtype=torch.uint8, device=device)
 
 
 def ace_grouped_lora_fwd(x, A, B, group_rank: Sequence[int], alpha: float, routing: Routing,
@@ -175,6 +178,7 @@ def ace_grouped_lora_fwd(x, A, B, group_rank: Sequence[int], alpha: float, routi
     T, k = routing.c.T, routing.c.k
     d_in, d_out = A.shape[1], y.shape[1]
     ranks = _ranks_arg(group_rank)
+    ws = _fwd_ws(ws, T, k, d_in, d_out, len(group_rank), max(group_rank), A.device)
     _check(_lib.ace_grouped_lora_fwd(_dtype(x), input_mode, T, k, d_in, d_out, len(group_rank),
                                      ranks, alpha, _ptr(x), _ptr(A), _ptr(B), _ptr(pair_w),
                                      ctypes.byref(routing.c), _ptr(y), _ptr(ws),
@@ -203,6 +207,7 @@ def ace_expertwise_lora_fwd(x, A, B, E: int, rank: int, alpha: float, routing: R
                             stream=None) -> None:
     T, k = routing.c.T, routing.c.k
     d_in, d_out = A.shape[1], y.shape[1]
+    ws = _fwd_ws(ws, T, k, d_in, d_out, E, rank, A.device)
     _check(_lib.ace_expertwise_lora_fwd(_dtype(x), input_mode, T, k, d_in, d_out, E, rank, alpha,
                                         _ptr(x), _ptr(A), _ptr(B), _ptr(pair_w),
                                         ctypes.byref(routing.c), _ptr(y), _ptr(ws),

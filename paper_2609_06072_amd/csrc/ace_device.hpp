@@ -6,12 +6,17 @@
 //   fp32: v_mfma_f32_16x16x4f32    -- one 16-byte fragment (4 floats) per lane,
 //                                     consumed by four MFMAs (element i in step i)
 // Lane l = 16*g + c (g = l >> 4 in 0..3, c = l & 15) supplies row/column c of
-// its operand; its fragment covers the PER contraction indices PER*g .. PER*g+PER-1
-// of a K-block of KB = 4*PER (32 for bf16, 16 for fp32).  The accumulator
-// block holds D[4*g + v][c] in element v.  Since a contraction is a sum, any
-// assignment of contraction indices to (g, element) works as long as both
-// operands use the same one; the kernels use that freedom to feed an
-// accumulator straight back in as an operand (see Tr<T>::kmap_acc).
+// its operand; its fragment holds contraction indices PER*g .. PER*g+PER-1 of a
+// K-block of KB = 4*PER (32 for bf16, 16 for fp32).  The accumulator block
+// holds D[4*g + v][c] in element v.
+//
+// Rank permutation.  The shrink H^T = A_q X^T puts rank indices on the rows
+// of D.  Because the rows of the A operand may be any permutation of A_q's
+// rows, the shrink loads row rank_of_row(rb, i) into operand row i of rank
+// block rb; then the accumulators of rank blocks (APF*m .. APF*m+APF-1) of
+// lane group g hold exactly rank indices KB*m + PER*g .. + PER-1: a natural
+// K-block fragment, so H feeds the expand MFMA without any data movement and
+// the expand's weight fragments are plain 16-byte loads.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -47,6 +52,7 @@ struct Tr<float> {
   using frag = f32x4;
   static constexpr int PER = 4;
   static constexpr int KB = 16;
+  static constexpr int APF = 1;  // accumulator blocks per rank K-block
   __device__ static inline f32x4 mma(frag a, frag b, f32x4 c) {
     c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[0], b[0], c, 0, 0, 0);
     c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[1], b[1], c, 0, 0, 0);
@@ -55,24 +61,15 @@ struct Tr<float> {
     return c;
   }
   __device__ static inline frag zero() { return frag{0.f, 0.f, 0.f, 0.f}; }
-  __device__ static inline frag load(const float* p) {
-    return *reinterpret_cast<const f32x4*>(p);
-  }
-  using v4 = f32x4;
-  __device__ static inline v4 load4raw(const float* p) { return *reinterpret_cast<const f32x4*>(p); }
-  // 4 consecutive elements -> 4 floats (p 16-byte aligned)
-  __device__ static inline f32x4 load4(const float* p) { return *reinterpret_cast<const f32x4*>(p); }
-  __device__ static inline void store4(float* p, f32x4 v) { *reinterpret_cast<f32x4*>(p) = v; }
-  // Fragment of the rank-K-block m built from accumulator blocks: block m's
-  // element v of lane group g is index 16*m + 4*g + v, which is exactly the
-  // natural fragment layout of a K-block of 16.
-  static constexpr int ACC_PER_FRAG = 1;
-  __device__ static inline frag from_acc(const f32x4* acc, int m, float s) {
-    return acc[m] * s;
+  __device__ static inline frag load(const float* p) { return *reinterpret_cast<const f32x4*>(p); }
+  __device__ static inline void store(float* p, frag v) { *reinterpret_cast<f32x4*>(p) = v; }
+  __device__ static inline f32x4 lo4(frag f) { return f; }
+  __device__ static inline void to_f32(frag f, float* v) {
+    v[0] = f[0]; v[1] = f[1]; v[2] = f[2]; v[3] = f[3];
   }
   __device__ static inline frag from_f32(const float* v) { return frag{v[0], v[1], v[2], v[3]}; }
-  __device__ static inline float to_f32(float v) { return v; }
-  __device__ static inline float from_float(float v) { return v; }
+  // fragment of rank K-block m from the accumulators (times s)
+  __device__ static inline frag from_acc(const f32x4* acc, int m, float s) { return acc[m] * s; }
 };
 
 template <>
@@ -80,6 +77,7 @@ struct Tr<__bf16> {
   using frag = bf16x8;
   static constexpr int PER = 8;
   static constexpr int KB = 32;
+  static constexpr int APF = 2;
   __device__ static inline f32x4 mma(frag a, frag b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
   }
@@ -90,70 +88,44 @@ struct Tr<__bf16> {
   __device__ static inline frag load(const __bf16* p) {
     return __builtin_bit_cast(frag, *reinterpret_cast<const u32x4*>(p));
   }
-  using v4 = bf16x4;
-  __device__ static inline v4 load4raw(const __bf16* p) {
-    return __builtin_bit_cast(bf16x4, *reinterpret_cast<const u32x2*>(p));
+  __device__ static inline void store(__bf16* p, frag v) {
+    *reinterpret_cast<u32x4*>(p) = __builtin_bit_cast(u32x4, v);
   }
-  __device__ static inline f32x4 load4(const __bf16* p) {
-    bf16x4 v = __builtin_bit_cast(bf16x4, *reinterpret_cast<const u32x2*>(p));
-    return f32x4{(float)v[0], (float)v[1], (float)v[2], (float)v[3]};
-  }
-  __device__ static inline void store4(__bf16* p, f32x4 v) {
-    bf16x4 b = {(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
-    *reinterpret_cast<u32x2*>(p) = __builtin_bit_cast(u32x2, b);
-  }
-  // A rank K-block of 32 covers accumulator blocks 2m and 2m+1: element i of
-  // lane group g is rank index 32*m + 16*(i/4) + 4*g + (i%4).
-  static constexpr int ACC_PER_FRAG = 2;
-  __device__ static inline frag from_acc(const f32x4* acc, int m, float s) {
-    const f32x4 a = acc[2 * m] * s, b = acc[2 * m + 1] * s;
-    return frag{(__bf16)a[0], (__bf16)a[1], (__bf16)a[2], (__bf16)a[3],
-                (__bf16)b[0], (__bf16)b[1], (__bf16)b[2], (__bf16)b[3]};
+  __device__ static inline void to_f32(frag f, float* v) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = (float)f[i];
   }
   __device__ static inline frag from_f32(const float* v) {
     return frag{(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3],
                 (__bf16)v[4], (__bf16)v[5], (__bf16)v[6], (__bf16)v[7]};
   }
-  __device__ static inline float to_f32(__bf16 v) { return (float)v; }
-  __device__ static inline __bf16 from_float(float v) { return (__bf16)v; }
+  __device__ static inline frag from_acc(const f32x4* acc, int m, float s) {
+    const f32x4 a = acc[2 * m] * s, b = acc[2 * m + 1] * s;
+    return frag{(__bf16)a[0], (__bf16)a[1], (__bf16)a[2], (__bf16)a[3],
+                (__bf16)b[0], (__bf16)b[1], (__bf16)b[2], (__bf16)b[3]};
+  }
 };
 
-// Rank index held by element i of lane group g in rank K-block m when the
-// fragment was built from accumulators (Tr<T>::from_acc).
+// Rank index loaded into operand row i (0..15) of rank block rb by the
+// shrink, so that accumulator element v of lane group g in rank block rb
+// holds rank rank_of_row<T>(rb, 4*g + v) and from_acc yields natural order.
 template <typename T>
-__device__ inline int kmap_acc(int m, int g, int i) {
-  if constexpr (Tr<T>::PER == 4) {
-    return 16 * m + 4 * g + i;
-  } else {
-    return 32 * m + 16 * (i >> 2) + 4 * g + (i & 3);
-  }
+__device__ __host__ inline int rank_of_row(int rb, int i) {
+  constexpr int APF = Tr<T>::APF, PER = Tr<T>::PER, KB = Tr<T>::KB;
+  return KB * (rb / APF) + PER * (i >> 2) + 4 * (rb % APF) + (i & 3);
 }
 
-// Loads the operand fragment of one weight row (base = the row's first
-// element, valid columns [0, ncols)) for rank K-block m in the
-// accumulator-derived order (kmap_acc).  Columns >= ncols read as zero.
-// `aligned4` says the row starts on a multiple of 4 elements.
+// PER consecutive elements p[0 .. PER) of which the first nvalid are read
+// (the rest are zero); a full fragment uses one 16-byte load when `vec`.
 template <typename T>
-__device__ inline typename Tr<T>::frag load_acc_order(const T* base, int ncols, int m, int g,
-                                                      bool row_ok, bool aligned4) {
+__device__ inline typename Tr<T>::frag load_frag(const T* p, int nvalid, bool vec) {
+  constexpr int PER = Tr<T>::PER;
+  if (nvalid >= PER && vec) return Tr<T>::load(p);
   typename Tr<T>::frag f = Tr<T>::zero();
-  if (!row_ok) return f;
-  constexpr int CH = Tr<T>::PER / 4;  // 4-element chunks per fragment
+  if (nvalid <= 0) return f;
 #pragma unroll
-  for (int c = 0; c < CH; ++c) {
-    const int r0 = kmap_acc<T>(m, g, 4 * c);
-    if (aligned4 && r0 + 3 < ncols) {
-      const typename Tr<T>::v4 v = Tr<T>::load4raw(base + r0);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) f[4 * c + i] = v[i];
-    } else {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int r = r0 + i;
-        f[4 * c + i] = r < ncols ? base[r] : (T)0.f;
-      }
-    }
-  }
+  for (int e = 0; e < PER; ++e)
+    if (e < nvalid) f[e] = p[e];
   return f;
 }
 
@@ -175,8 +147,8 @@ __device__ inline int block_exclusive_scan(int v, int* lds /* kThreads ints */, 
   return incl - v;
 }
 
-// Tile table of a persistent launch over per-key row segments: tiles of BM
-// rows, key-major.  tstart[q] = first tile of key q, tstart[n_keys] = total.
+// Tile table of a launch over per-key row segments: tiles of BM rows,
+// key-major.  tstart[q] = first tile of key q, tstart[n_keys] = total.
 // seg[q] = offsets[q] (first row of key q), seg[n_keys] = U.
 __device__ inline void build_tile_table(const int32_t* offsets, int n_keys, int BM, int* seg,
                                         int* tstart, int* scan_lds) {
@@ -192,12 +164,41 @@ __device__ inline void build_tile_table(const int32_t* offsets, int n_keys, int 
   __syncthreads();
 }
 
-// Key q with tstart[q] <= tile < tstart[q+1] (binary search; uniform).
-__device__ inline int find_key(const int* tstart, int n_keys, int tile) {
-  int lo = 0, hi = n_keys;  // invariant: tstart[lo] <= tile < tstart[hi]
+// XCD-aware tile table.  Blocks are dispatched to the XCDs round-robin, so
+// block b runs on XCD b % kXcds.  Within a key the rows are sorted by token,
+// so the x-th eighth of a key's tiles covers about the x-th eighth of the
+// tokens; bucket x collects that eighth of every key and is served by the
+// blocks with b % kXcds == x.  Rows that share a token (the same token's rows
+// in other groups) then meet in the same XCD's L2.
+// bstart[q] = first index of key q's tiles inside the bucket, bfirst[q] = the
+// key-local index of that tile, bstart[n_keys] = the bucket's tile count.
+constexpr int kXcds = 8;
+__device__ inline void build_bucket_table(const int32_t* offsets, int n_keys, int BM, int bucket,
+                                          int* seg, int* bstart, int* bfirst, int* scan_lds) {
+  const int t = threadIdx.x;
+  for (int i = t; i <= n_keys; i += kThreads) seg[i] = offsets[i];
+  __syncthreads();
+  int cnt = 0;
+  if (t < n_keys) {
+    const int nq = (seg[t + 1] - seg[t] + BM - 1) / BM;
+    const int j0 = (bucket * nq + kXcds - 1) / kXcds;
+    const int j1 = ((bucket + 1) * nq + kXcds - 1) / kXcds;
+    bfirst[t] = j0;
+    cnt = j1 - j0;
+  }
+  int total;
+  const int ex = block_exclusive_scan(cnt, scan_lds, &total);
+  if (t < n_keys) bstart[t] = ex;
+  if (t == 0) bstart[n_keys] = total;
+  __syncthreads();
+}
+
+// Largest q in [0, n) with arr[q] <= x, for a non-decreasing arr (uniform).
+__device__ inline int upper_index(const int* arr, int n, int x) {
+  int lo = 0, hi = n;  // invariant: arr[lo] <= x < arr[hi] (arr[n] treated as +inf)
   while (hi - lo > 1) {
     const int mid = (lo + hi) >> 1;
-    if (tstart[mid] <= tile) lo = mid; else hi = mid;
+    if (arr[mid] <= x) lo = mid; else hi = mid;
   }
   return lo;
 }

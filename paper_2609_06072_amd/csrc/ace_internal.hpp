@@ -31,9 +31,55 @@ hipError_t launch_permute(const int32_t* ids, int T, int k, int E, const int32_t
                           int mode, int n_keys, const ace_routing* rt, void* ws,
                           hipStream_t stream);
 
-hipError_t launch_fwd(const Problem& p, void* y, hipStream_t stream);
+// Source of the rows of a rank contraction.
+constexpr int kSrcShared = 0;   // x[row_token[u]]
+constexpr int kSrcPerPair = 1;  // x[t*k + j] (the row's single slot)
+constexpr int kSrcGather = 2;   // sum over the row's slots of w_tj * dY[t*k + j]
 
-size_t bwd_ws_bytes(int T, int k, int d_in, int d_out, int R);
+struct ContractArgs {
+  const void* src;            // x or dY, rows of length K
+  const void* W;              // weight row (roff_q + r) at W + (roff_q + r) * ldw
+  int32_t ldw, K, src_mode, k;
+  float alpha;
+  const float* pair_w;
+  const int32_t* offsets;
+  const int32_t* row_token;
+  const uint32_t* row_slots;
+  void* out_row;              // [U][rpad] or null
+  int32_t rpad;
+  void* out_t;                // [R][ldh] (column u - offsets[q]) or null
+  long ldh;
+  void* out_dense;            // [T * kslots][R] or null
+  int32_t kslots;
+  KeyTable keys;
+};
+
+struct ExpandArgs {
+  const void* H;              // [U][rpad], scaled, zero beyond r_q
+  int32_t rpad;
+  const void* W;              // key q's rows start at W + w_key_mul * roff_q
+  int32_t w_key_mul;
+  int32_t w_stride_is_rank;   // row stride r_q (B_q) or R (A^T)
+  const int32_t* offsets;
+  const int32_t* row_token;
+  const uint32_t* row_slots;
+  int32_t k, n_out;
+  void* out;                  // [T*k][n_out], accumulated
+  const float* pair_w;        // or null (weight 1)
+  int32_t nch;                // set by the launcher
+  KeyTable keys;
+};
+
+int rank_blocks(int r_max);
+int rank_pad(int dtype, int r_max);
+hipError_t launch_contract(int dtype, const ContractArgs& a, int r_max, long P,
+                           hipStream_t stream);
+hipError_t launch_expand(int dtype, const ExpandArgs& a, int r_max, long P, hipStream_t stream);
+
+size_t fwd_ws_bytes(int T, int k, int r_max);
+hipError_t launch_fwd(const Problem& p, void* y, void* ws, hipStream_t stream);
+
+size_t bwd_ws_bytes(int T, int k, int d_in, int d_out, int R, int r_max);
 hipError_t launch_bwd(const Problem& p, const void* dy, void* dx, float* dA, float* dB, void* ws,
                       hipStream_t stream);
 

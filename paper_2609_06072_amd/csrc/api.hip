@@ -117,11 +117,16 @@ ace_status check_problem(Problem& p, ace_dtype dtype, ace_input_mode im, int32_t
   return ok();
 }
 
-ace_status run_fwd(const Problem& p, void* y, void* stream) {
+ace_status run_fwd(const Problem& p, void* y, void* ws, size_t ws_bytes, void* stream) {
   if (p.T > 0 && !y) return fail(ACE_ERR_INVALID_ARG, "y is NULL");
   if (!aligned(y, 16)) return fail(ACE_ERR_INVALID_ARG, "y must be 16-byte aligned");
+  const size_t need = fwd_ws_bytes(p.T, p.k, p.r_max);
+  if (need > 0 && (!ws || ws_bytes < need))
+    return fail(ACE_ERR_WORKSPACE, "forward needs %zu workspace bytes, got %zu", need,
+                ws ? ws_bytes : (size_t)0);
+  if (!aligned(ws, 256)) return fail(ACE_ERR_WORKSPACE, "workspace must be 256-byte aligned");
   if (p.T == 0) return ok();
-  return hip_status(launch_fwd(p, y, static_cast<hipStream_t>(stream)), "forward launch");
+  return hip_status(launch_fwd(p, y, ws, static_cast<hipStream_t>(stream)), "forward launch");
 }
 
 ace_status run_bwd(const Problem& p, const void* dy, void* dx, float* dA, float* dB, void* ws,
@@ -131,7 +136,7 @@ ace_status run_bwd(const Problem& p, const void* dy, void* dx, float* dA, float*
   if (!aligned(dy, 16) || !aligned(dx, 16))
     return fail(ACE_ERR_INVALID_ARG, "dy and dx must be 16-byte aligned");
   if (!aligned(dA, 4) || !aligned(dB, 4)) return fail(ACE_ERR_INVALID_ARG, "dA/dB misaligned");
-  const size_t need = bwd_ws_bytes(p.T, p.k, p.d_in, p.d_out, p.keys.R);
+  const size_t need = bwd_ws_bytes(p.T, p.k, p.d_in, p.d_out, p.keys.R, p.r_max);
   if (!ws || ws_bytes < need)
     return fail(ACE_ERR_WORKSPACE, "backward needs %zu workspace bytes, got %zu", need,
                 ws ? ws_bytes : (size_t)0);
@@ -202,13 +207,11 @@ ace_status ace_grouped_lora_fwd(ace_dtype dtype, ace_input_mode input_mode, int3
                                 const void* A, const void* B, const float* pair_w,
                                 const ace_routing* rt, void* y, void* ws, size_t ws_bytes,
                                 void* stream) {
-  (void)ws;
-  (void)ws_bytes;
   Problem p;
   ace_status s = check_problem(p, dtype, input_mode, T, k, d_in, d_out, G, group_rank, 0, alpha,
                                x, A, B, pair_w, rt, false);
   if (s != ACE_OK) return s;
-  return run_fwd(p, y, stream);
+  return run_fwd(p, y, ws, ws_bytes, stream);
 }
 
 ace_status ace_grouped_lora_bwd(ace_dtype dtype, ace_input_mode input_mode, int32_t T,
@@ -229,13 +232,11 @@ ace_status ace_expertwise_lora_fwd(ace_dtype dtype, ace_input_mode input_mode, i
                                    int32_t rank, float alpha, const void* x, const void* A,
                                    const void* B, const float* pair_w, const ace_routing* rt,
                                    void* y, void* ws, size_t ws_bytes, void* stream) {
-  (void)ws;
-  (void)ws_bytes;
   Problem p;
   ace_status s = check_problem(p, dtype, input_mode, T, k, d_in, d_out, E, nullptr, rank, alpha,
                                x, A, B, pair_w, rt, true);
   if (s != ACE_OK) return s;
-  return run_fwd(p, y, stream);
+  return run_fwd(p, y, ws, ws_bytes, stream);
 }
 
 ace_status ace_expertwise_lora_bwd(ace_dtype dtype, ace_input_mode input_mode, int32_t T,
@@ -261,13 +262,17 @@ size_t ace_workspace_bytes(ace_op op, int32_t T, int32_t k, int32_t d_in, int32_
     case ACE_OP_PERMUTE:
       return round256(permute_ws_bytes(T, k, n_keys));
     case ACE_OP_FWD:
-      return 0;
+      if (r_max < 1 || r_max > kMaxRank) {
+        fail(ACE_ERR_INVALID_ARG, "invalid workspace query");
+        return (size_t)-1;
+      }
+      return round256(fwd_ws_bytes(T, k, r_max));
     case ACE_OP_BWD:
       if (d_in < 1 || d_out < 1 || r_max < 1 || r_max > kMaxRank) {
         fail(ACE_ERR_INVALID_ARG, "invalid workspace query");
         return (size_t)-1;
       }
-      return round256(bwd_ws_bytes(T, k, d_in, d_out, n_keys * r_max));
+      return round256(bwd_ws_bytes(T, k, d_in, d_out, n_keys * r_max, r_max));
   }
   fail(ACE_ERR_INVALID_ARG, "unknown op %d", (int)op);
   return (size_t)-1;

@@ -1,0 +1,300 @@
+// Rank contraction over the rows of the permutation: for every row u of key q
+//   out[u][r] = s_q * sum_c W_q[r][c] * src_u[c],   r < r_q,  s_q = alpha / r_q
+// with either
+//   src_u = x[row_token[u]]            (shared input; Sec. 3.5: once per row,
+//                                       i.e. once per (token, active group))
+//   src_u = x[t*k + j]                 (per-pair input, down projection)
+//   src_u = sum_{j in slots(u)} w_tj dY[t*k + j]   (the row's output gradient)
+// and W = A (the shrink h = A_q x of Sec. 3.1.3) or W = B^T (dH = B_q^T G).
+//
+// A block takes a tile of BM rows of one key.  The four waves split the
+// contraction (wave w takes K-blocks w, w+4, ...), so each source row and each
+// weight row is read once per tile, and the partial sums meet in LDS in a
+// fixed order (deterministic).  Results go to any of three layouts:
+//   row-major  [U][rpad]      operand of the expand kernel (zero beyond r_q)
+//   per key    [R][ldh]       column u - offsets[q]: operand of the column pass
+//   dense      [T*kslots][R]  per-token rows: operand of the dense dx GEMM
+#include "ace_device.hpp"
+#include "ace_internal.hpp"
+
+namespace ace {
+
+namespace {
+
+template <int RB>
+struct CGeo {
+  static constexpr int NRB = RB <= 4 ? 4 : (RB == 8 ? 2 : 1);
+  static constexpr int UNROLL = RB <= 8 ? 2 : 1;
+};
+
+template <typename T, int RB>
+__global__ __launch_bounds__(kThreads) void contract_kernel(ContractArgs a) {
+  using F = typename Tr<T>::frag;
+  constexpr int PER = Tr<T>::PER, KB = Tr<T>::KB, APF = Tr<T>::APF;
+  constexpr int NRB = CGeo<RB>::NRB, U = CGeo<RB>::UNROLL;
+  constexpr int BM = 16 * NRB;
+  __shared__ int seg[kMaxKeys + 1];
+  __shared__ int bstart[kMaxKeys + 1];
+  __shared__ int bfirst[kMaxKeys];
+  __shared__ int scan[kThreads];
+  __shared__ f32x4 red[4][NRB][RB][64];
+  const int n_keys = a.keys.n_keys;
+  const int bucket = blockIdx.x % kXcds;
+  build_bucket_table(a.offsets, n_keys, BM, bucket, seg, bstart, bfirst, scan);
+  const int total = bstart[n_keys];
+  const int stride = gridDim.x / kXcds;  // the grid is a multiple of kXcds
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int c16 = lane & 15, g = lane >> 4;
+  const T* S = static_cast<const T*>(a.src);
+  const T* W = static_cast<const T*>(a.W);
+  const int K = a.K, k = a.k, R = a.keys.R;
+  const int nks = (K + KB - 1) / KB, nks_full = K / KB;
+  const bool gather = a.src_mode == kSrcGather;
+
+  for (int idx = blockIdx.x / kXcds; idx < total; idx += stride) {
+    const int q = upper_index(bstart, n_keys, idx);
+    const int lo = seg[q];
+    const int u0 = lo + (bfirst[q] + idx - bstart[q]) * BM;
+    const int u_end = seg[q + 1];
+    const int r_q = a.keys.rank[q], roff = a.keys.roff[q];
+    const int nmb = (r_q + KB - 1) / KB;
+    const int nrb = nmb * APF;  // rank blocks spanned by rank_of_row for r < r_q
+
+    // Source rows.  Rows past the segment read row 0 (never stored); weight
+    // rows past r_q re-read row r_q - 1 (zeroed before any store), so every
+    // load is unconditional and a wave keeps all of them in flight.
+    const T* srow[NRB];
+    int tokv[NRB];
+    uint32_t slv[NRB];
+    bool multi = false;
+#pragma unroll
+    for (int ib = 0; ib < NRB; ++ib) {  // unconditional loads: one round trip
+      const int u = u0 + 16 * ib + c16;
+      const int uc = min(u, u_end - 1);
+      tokv[ib] = a.row_token[uc];
+      slv[ib] = a.row_slots[uc];
+    }
+#pragma unroll
+    for (int ib = 0; ib < NRB; ++ib) {
+      if (u0 + 16 * ib + c16 >= u_end) slv[ib] = 0u;
+      const int j0 = __builtin_ctz(slv[ib] | 0x80000000u) & 31;
+      const int sr = a.src_mode == kSrcShared ? tokv[ib] : tokv[ib] * k + (slv[ib] ? j0 : 0);
+      srow[ib] = S + (size_t)sr * K;
+      multi |= gather && ((slv[ib] & (slv[ib] - 1u)) != 0u || a.pair_w != nullptr);
+    }
+    // a wave takes the weighted/multi-slot path if any of its lanes needs it
+    const bool wave_multi = __ballot(multi) != 0ull;
+    const T* wrow[RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const int r = rank_of_row<T>(rb, c16);
+      wrow[rb] = W + (size_t)(roff + (r < r_q ? r : r_q - 1)) * a.ldw;
+    }
+
+    // The row's operand fragment at contraction offset kof (nv valid
+    // elements): one row, or the weighted sum over the row's slots.
+    auto gather_frag = [&](int ib, int kof, int nv) -> F {
+      float v[PER];
+#pragma unroll
+      for (int e = 0; e < PER; ++e) v[e] = 0.f;
+      for (uint32_t mm = slv[ib]; mm; mm &= mm - 1u) {
+        const int p = tokv[ib] * k + __builtin_ctz(mm);
+        const float w = a.pair_w ? a.pair_w[p] : 1.f;
+        float f[PER];
+        Tr<T>::to_f32(load_frag<T>(S + (size_t)p * K + kof, nv, true), f);
+#pragma unroll
+        for (int e = 0; e < PER; ++e) v[e] += w * f[e];
+      }
+      return Tr<T>::from_f32(v);
+    };
+    auto src_frag = [&](int ib, int kof, int nv, bool full) -> F {
+      if (!wave_multi) return full ? Tr<T>::load(srow[ib] + kof) : load_frag<T>(srow[ib] + kof, nv, true);
+      return gather_frag(ib, kof, nv);
+    };
+
+    f32x4 acc[NRB][RB];
+#pragma unroll
+    for (int ib = 0; ib < NRB; ++ib)
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) acc[ib][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // Main loop over this wave's full stages (U K-blocks each), register
+    // double-buffered: the next stage's loads are in flight while the
+    // matrix cores work on the current one.
+    struct Stage {
+      F sf[U][NRB];
+      F wf[U][RB];
+    };
+    auto load_stage = [&](int ks0, Stage& st) {  // single-row sources (no branches)
+#pragma unroll
+      for (int s = 0; s < U; ++s) {
+        const int kof = (ks0 + 4 * s) * KB + PER * g;
+#pragma unroll
+        for (int ib = 0; ib < NRB; ++ib) st.sf[s][ib] = Tr<T>::load(srow[ib] + kof);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) st.wf[s][rb] = Tr<T>::load(wrow[rb] + kof);
+      }
+    };
+    auto load_stage_gather = [&](int ks0, Stage& st) {
+#pragma unroll
+      for (int s = 0; s < U; ++s) {
+        const int kof = (ks0 + 4 * s) * KB + PER * g;
+#pragma unroll
+        for (int ib = 0; ib < NRB; ++ib) st.sf[s][ib] = gather_frag(ib, kof, PER);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) st.wf[s][rb] = Tr<T>::load(wrow[rb] + kof);
+      }
+    };
+    auto mma_stage = [&](const Stage& st) {
+#pragma unroll
+      for (int s = 0; s < U; ++s)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+          if (rb < nrb) {
+#pragma unroll
+            for (int ib = 0; ib < NRB; ++ib) acc[ib][rb] = Tr<T>::mma(st.wf[s][rb], st.sf[s][ib], acc[ib][rb]);
+          }
+    };
+    // stages of this wave: ks0 = wave + 4*U*i with ks0 + 4*(U-1) < nks_full
+    const int n_main = nks_full > wave + 4 * (U - 1) ? (nks_full - wave - 4 * (U - 1) + 4 * U - 1) / (4 * U) : 0;
+    if (!wave_multi) {
+      Stage SA, SB;
+      if (n_main > 0) load_stage(wave, SA);
+      int i = 0;
+      for (; i + 1 < n_main; i += 2) {
+        load_stage(wave + 4 * U * (i + 1), SB);
+        mma_stage(SA);
+        if (i + 2 < n_main) load_stage(wave + 4 * U * (i + 2), SA);
+        mma_stage(SB);
+      }
+      if (i < n_main) mma_stage(SA);
+    } else {
+      for (int i = 0; i < n_main; ++i) {
+        Stage st;
+        load_stage_gather(wave + 4 * U * i, st);
+        mma_stage(st);
+      }
+    }
+    int ks0 = wave + 4 * U * n_main;
+    for (; ks0 < nks; ks0 += 4) {  // leftover K-blocks of this wave (masked tail)
+      const int kof = ks0 * KB + PER * g;
+      const int nv = K - kof;
+      const int kc = nv > 0 ? kof : 0;
+      F sf[NRB], wf[RB];
+#pragma unroll
+      for (int ib = 0; ib < NRB; ++ib) sf[ib] = nv > 0 ? src_frag(ib, kc, nv, nv >= PER) : Tr<T>::zero();
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) wf[rb] = load_frag<T>(wrow[rb] + kc, nv, true);
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+        if (rb < nrb) {
+#pragma unroll
+          for (int ib = 0; ib < NRB; ++ib) acc[ib][rb] = Tr<T>::mma(wf[rb], sf[ib], acc[ib][rb]);
+        }
+    }
+
+    // ---- partial sums meet in LDS; wave w finishes row block w % NRB
+    __syncthreads();
+#pragma unroll
+    for (int ib = 0; ib < NRB; ++ib)
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) red[wave][ib][rb][lane] = acc[ib][rb];
+    __syncthreads();
+    const int ib = wave % NRB;
+    if (wave >= NRB) continue;  // the other waves' row blocks are done by waves < NRB
+    const int u = u0 + 16 * ib + c16;
+    if (u0 + 16 * ib >= u_end) continue;  // wave-uniform
+    const bool valid = u < u_end;
+    const float s = a.alpha / (float)r_q;
+    f32x4 h[RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      h[rb] = (((red[0][ib][rb][lane] + red[1][ib][rb][lane]) + red[2][ib][rb][lane]) +
+               red[3][ib][rb][lane]) * s;
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        if (rank_of_row<T>(rb, 4 * g + v) >= r_q) h[rb][v] = 0.f;
+    }
+    if (!valid) continue;
+    const int tok = a.row_token[u];
+    const uint32_t slots = a.row_slots[u];
+    if (a.out_row) {
+      T* dst = static_cast<T*>(a.out_row) + (size_t)u * a.rpad;
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        const int r0 = rank_of_row<T>(rb, 4 * g);  // 4 consecutive ranks
+        if (r0 < a.rpad) {
+#pragma unroll
+          for (int v = 0; v < 4; ++v) dst[r0 + v] = (T)h[rb][v];
+        }
+      }
+    }
+    if (a.out_t) {
+      T* dst = static_cast<T*>(a.out_t);
+      const long col = u - lo;
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+        if (rb < nrb) {
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int r = rank_of_row<T>(rb, 4 * g + v);
+            if (r < r_q) dst[(size_t)(roff + r) * a.ldh + col] = (T)h[rb][v];
+          }
+        }
+    }
+    if (a.out_dense) {
+      const int j0 = __builtin_ctz(slots | 0x80000000u) & 31;
+      const size_t drow = (size_t)tok * a.kslots + (a.kslots > 1 ? j0 : 0);
+      T* dst = static_cast<T*>(a.out_dense) + drow * R + roff;
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+        if (rb < nrb) {
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int r = rank_of_row<T>(rb, 4 * g + v);
+            if (r < r_q) dst[r] = (T)h[rb][v];
+          }
+        }
+    }
+  }
+}
+
+template <typename T, int RB>
+hipError_t launch_contract_rb(const ContractArgs& a, long P, hipStream_t stream) {
+  constexpr int BM = 16 * CGeo<RB>::NRB;
+  // tiles per bucket <= (all tiles) / kXcds + n_keys
+  const long per_bucket = P > 0 ? ((P + BM - 1) / BM + a.keys.n_keys) / kXcds + a.keys.n_keys : 0;
+  const long cap = 6L * device_cu_count() / kXcds;
+  const int grid = (int)(per_bucket < cap ? per_bucket : cap) * kXcds;
+  if (grid > 0) contract_kernel<T, RB><<<grid, kThreads, 0, stream>>>(a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int rank_blocks(int r_max) {
+  const int rb = (r_max + 15) / 16;
+  return rb <= 2 ? 2 : rb <= 4 ? 4 : rb <= 8 ? 8 : 16;
+}
+
+int rank_pad(int dtype, int r_max) {
+  // KB * (RB / APF) = 16 * RB for both element types
+  (void)dtype;
+  return 16 * rank_blocks(r_max);
+}
+
+hipError_t launch_contract(int dtype, const ContractArgs& a, int r_max, long P,
+                           hipStream_t stream) {
+  const int rb = rank_blocks(r_max);
+  if (dtype == ACE_BF16) {
+    if (rb == 2) return launch_contract_rb<__bf16, 2>(a, P, stream);
+    if (rb == 4) return launch_contract_rb<__bf16, 4>(a, P, stream);
+    if (rb == 8) return launch_contract_rb<__bf16, 8>(a, P, stream);
+    return launch_contract_rb<__bf16, 16>(a, P, stream);
+  }
+  if (rb == 2) return launch_contract_rb<float, 2>(a, P, stream);
+  if (rb == 4) return launch_contract_rb<float, 4>(a, P, stream);
+  if (rb == 8) return launch_contract_rb<float, 8>(a, P, stream);
+  return launch_contract_rb<float, 16>(a, P, stream);
+}
+
+}  // namespace ace

@@ -2,25 +2,27 @@
 // a shared adapter collects the gradient of every routed pair of its group).
 //
 // With G_u = sum_{j in slots(u)} w_j dY[t*k+j] (the row's output gradient),
-// H_u = A_q x_u and s_q = alpha / r_q:
-//   dH_u  = s_q B_q^T G_u                       (per row, K = d_out)
-//   dB_q  = s_q sum_u G_u H_u^T                 (per key, K = rows of q)
+// s_q = alpha / r_q, Hs_u = s_q A_q x_u and dH_u = s_q B_q^T G_u:
+//   dB_q  = sum_u G_u Hs_u^T                    (per key, K = rows of q)
 //   dA_q  = sum_u dH_u x_u^T                    (per key, K = rows of q)
-//   dx    += sum over the rows that read x      (token-major)
+//   dx    += sum over the rows that read x of A_q^T dH_u
 //
-// Three launches, all deterministic (each output reduced in a fixed order):
-//   prep  -- transposes of the parameters (A^T, B_q^T) into the workspace, so
-//            that every MFMA operand is contiguous along its contraction
-//            index, and zeroes the dense dH buffer used for dx.
-//   row   -- persistent over 64-row tiles of each key's segment: recomputes
-//            H, gathers G, forms dH; stores H^T and dH^T per key (for the
-//            column pass) and either scatters dH into the dense per-token
-//            buffer (shared input) or applies dx_u += dH_u A_q directly
-//            (per-pair input: every row owns its input row).
-//   col   -- one block per output block: dB_q (64 columns of d_out), dA_q (64
-//            columns of d_in), both reducing over the key's rows with the
-//            large operand staged transposed in LDS; and, for shared input,
-//            dx = dHdense A as a dense GEMM over K = R (token-major).
+// Launches, all deterministic (each output is reduced in a fixed order):
+//   prep      -- A^T and B_q^T into the workspace (so every MFMA operand is
+//                contiguous along its contraction index); zeroes the dense
+//                per-token dH buffer used for dx.
+//   contract  -- Hs per row (x against A), stored per key as [r][u].
+//   contract  -- dH per row (gathered G against B^T), stored per key as
+//                [r][u] and either as dense per-token rows (shared input) or
+//                row-major for the expand below (per-pair input).
+//   expand    -- per-pair input only: dx[t*k+j] += A_q^T dH_u (each row owns
+//                its input row).
+//   col       -- one block per output block: dB_q (64 columns of d_out) and
+//                dA_q (64 columns of d_in), reducing over the key's rows in
+//                128-row stages whose large operand (G or x) is staged
+//                transposed in LDS (double buffered, one barrier per stage);
+//                and, for shared input, dx = dHdense A as a dense GEMM over
+//                K = R (token-major).
 #include "ace_device.hpp"
 #include "ace_internal.hpp"
 
@@ -28,30 +30,29 @@ namespace ace {
 
 namespace {
 
-constexpr int kBM = 64;
-constexpr int kNCH = 4;
 constexpr int kTile = 64;   // transpose tile / column block
 constexpr int kMaxJobs = kMaxKeys + 2;
 
 size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 
 struct WsLayout {
-  size_t At, Bt, Ht, dHt, dHf, total;
+  size_t At, Bt, Ht, dHt, dHf, dHrow, total;
 };
 
 // Workspace regions for element size es: At [d_in][R], Bt [R][d_out],
 // Ht/dHt [R][ldh] (column = row index inside the key's segment), dense dH
-// [T*kslots][R].
-WsLayout ws_layout(int T, int k, int d_in, int d_out, int R, size_t es) {
+// [T*kslots][R] (kslots <= k), row-major dH [P][rpad].
+WsLayout ws_layout(int T, int k, int d_in, int d_out, int R, int rpad, size_t es) {
   const size_t P = (size_t)T * k;
   const size_t ldh = (P + 7) & ~(size_t)7;
   WsLayout w{};
   size_t o = 0;
-  w.At = o;  o += align256(es * d_in * R);
-  w.Bt = o;  o += align256(es * (size_t)R * d_out);
-  w.Ht = o;  o += align256(es * (size_t)R * ldh);
-  w.dHt = o; o += align256(es * (size_t)R * ldh);
-  w.dHf = o; o += align256(es * P * R);
+  w.At = o;    o += align256(es * d_in * R);
+  w.Bt = o;    o += align256(es * (size_t)R * d_out);
+  w.Ht = o;    o += align256(es * (size_t)R * ldh);
+  w.dHt = o;   o += align256(es * (size_t)R * ldh);
+  w.dHf = o;   o += align256(es * P * R);
+  w.dHrow = o; o += align256(es * P * rpad);
   w.total = o;
   return w;
 }
@@ -65,7 +66,7 @@ struct PrepArgs {
   void* Bt;
   void* dHf;
   int32_t d_in, d_out, R;
-  long dHf_elems;
+  long dHf_vecs;                    // 16-byte vectors to zero
   int32_t n_jobs;
   int32_t job_start[kMaxJobs + 1];  // block ranges: job 0 = A, 1..n_keys = B_q, last = zero
   int32_t job_cols_tiles[kMaxJobs];
@@ -76,16 +77,16 @@ template <typename T>
 __global__ __launch_bounds__(kThreads) void bwd_prep_kernel(PrepArgs a) {
   __shared__ T tile[kTile][kTile + 1];
   const int b = blockIdx.x;
-  int job = 0;
-  while (job + 1 < a.n_jobs && a.job_start[job + 1] <= b) ++job;
+  const int job = upper_index(a.job_start, a.n_jobs, b);
   const int tb = b - a.job_start[job];
   const int n_keys = a.keys.n_keys;
   if (job == n_keys + 1) {  // zero the dense dH buffer
-    T* d = static_cast<T*>(a.dHf);
-    const long base = (long)tb * kTile * kTile;
-    for (int i = threadIdx.x; i < kTile * kTile; i += kThreads) {
-      const long e = base + i;
-      if (e < a.dHf_elems) d[e] = (T)0.f;
+    u32x4* d = static_cast<u32x4*>(a.dHf);
+    const long base = (long)tb * kThreads * 4;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const long e = base + i * kThreads + threadIdx.x;
+      if (e < a.dHf_vecs) d[e] = u32x4{0u, 0u, 0u, 0u};
     }
     return;
   }
@@ -117,11 +118,10 @@ __global__ __launch_bounds__(kThreads) void bwd_prep_kernel(PrepArgs a) {
   }
 }
 
-// --------------------------------------------------------------- row pass
+// ------------------------------------------------------------ column pass
 
 struct BwdArgs {
   const void* x;
-  const void* A;
   const float* pair_w;
   const void* dy;
   void* dx;
@@ -131,206 +131,27 @@ struct BwdArgs {
   const int32_t* row_token;
   const uint32_t* row_slots;
   int32_t T, k, d_in, d_out, per_pair, kslots;
-  float alpha;
   long ldh;
   const void* At;
-  const void* Bt;
-  void* Ht;
-  void* dHt;
-  void* dHf;
+  const void* Ht;
+  const void* dHt;
+  const void* dHf;
   int32_t nB, nA, nX;      // column-pass item counts
   KeyTable keys;
 };
 
-template <typename T, int RB>
-__global__ __launch_bounds__(kThreads) void bwd_row_kernel(BwdArgs a) {
-  using F = typename Tr<T>::frag;
-  constexpr int APF = Tr<T>::ACC_PER_FRAG;
-  constexpr int NM = RB / APF;
-  constexpr int PER = Tr<T>::PER;
-  __shared__ int seg[kMaxKeys + 1];
-  __shared__ int tstart[kMaxKeys + 1];
-  __shared__ int scan[kThreads];
-  const int n_keys = a.keys.n_keys;
-  build_tile_table(a.offsets, n_keys, kBM, seg, tstart, scan);
-  const int total = tstart[n_keys];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int c16 = lane & 15, g = lane >> 4;
-  const T* X = static_cast<const T*>(a.x);
-  const T* Aw = static_cast<const T*>(a.A);
-  const T* DY = static_cast<const T*>(a.dy);
-  const T* At = static_cast<const T*>(a.At);
-  const T* Bt = static_cast<const T*>(a.Bt);
-  T* Ht = static_cast<T*>(a.Ht);
-  T* dHt = static_cast<T*>(a.dHt);
-  T* dHf = static_cast<T*>(a.dHf);
-  T* DX = static_cast<T*>(a.dx);
-  const int d_in = a.d_in, d_out = a.d_out, k = a.k, R = a.keys.R;
-
-  for (int tile = blockIdx.x; tile < total; tile += gridDim.x) {
-    const int q = find_key(tstart, n_keys, tile);
-    const int lo = seg[q];
-    const int u_begin = lo + (tile - tstart[q]) * kBM + wave * 16;
-    const int u_end = seg[q + 1];
-    if (u_begin >= u_end) continue;
-    const int r_q = a.keys.rank[q], roff = a.keys.roff[q];
-    const int nrb = (r_q + 15) >> 4;
-    const int nmb = (r_q + 16 * APF - 1) / (16 * APF);
-    const int u = u_begin + c16;
-    const bool valid = u < u_end;
-    int tok = 0;
-    uint32_t slots = 0u;
-    if (valid) {
-      tok = a.row_token[u];
-      slots = a.row_slots[u];
-    }
-    const int j0 = __builtin_ctz(slots | 0x80000000u);
-    const int xr = a.per_pair ? tok * k + j0 : tok;
-
-    // ---- H (recomputed): hacc[rb][v] = H[u][16 rb + 4 g + v]
-    f32x4 hacc[RB];
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) hacc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const T* xrow = X + (size_t)xr * d_in;
-    for (int kk = 0; kk < d_in; kk += Tr<T>::KB) {
-      const int kof = kk + PER * g;
-      const bool kok = kof < d_in;
-      const F xf = (valid && kok) ? Tr<T>::load(xrow + kof) : Tr<T>::zero();
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        if (rb < nrb) {
-          const int r = rb * 16 + c16;
-          const F af = (r < r_q && kok) ? Tr<T>::load(Aw + (size_t)(roff + r) * d_in + kof)
-                                        : Tr<T>::zero();
-          hacc[rb] = Tr<T>::mma(af, xf, hacc[rb]);
-        }
-      }
-    }
-
-    // ---- dH: dacc[rb][v] = (B_q^T G_u)[16 rb + 4 g + v]
-    f32x4 dacc[RB];
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) dacc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int kk = 0; kk < d_out; kk += Tr<T>::KB) {
-      const int n = kk + PER * g;
-      const bool nok = n < d_out;
-      float gs[PER];
-#pragma unroll
-      for (int e = 0; e < PER; ++e) gs[e] = 0.f;
-      if (valid && nok) {
-        for (uint32_t mm = slots; mm; mm &= mm - 1u) {
-          const int p = tok * k + __builtin_ctz(mm);
-          const float w = a.pair_w ? a.pair_w[p] : 1.f;
-          const F v = Tr<T>::load(DY + (size_t)p * d_out + n);
-#pragma unroll
-          for (int e = 0; e < PER; ++e) gs[e] += w * (float)v[e];
-        }
-      }
-      const F gf = Tr<T>::from_f32(gs);
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        if (rb < nrb) {
-          const int r = rb * 16 + c16;
-          const F bf = (r < r_q && nok) ? Tr<T>::load(Bt + (size_t)(roff + r) * d_out + n)
-                                        : Tr<T>::zero();
-          dacc[rb] = Tr<T>::mma(bf, gf, dacc[rb]);
-        }
-      }
-    }
-    const float s = a.alpha / (float)r_q;
-
-    // ---- store H^T and dH^T (key block rows, column = u - lo)
-    if (valid) {
-      const long col = u - lo;
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        if (rb < nrb) {
-#pragma unroll
-          for (int v = 0; v < 4; ++v) {
-            const int r = rb * 16 + 4 * g + v;
-            if (r < r_q) {
-              Ht[(size_t)(roff + r) * a.ldh + col] = (T)hacc[rb][v];
-              dHt[(size_t)(roff + r) * a.ldh + col] = (T)(s * dacc[rb][v]);
-            }
-          }
-        }
-      }
-    }
-
-    if (!a.per_pair) {
-      // dense dH row of the token (one column block per key)
-      if (valid) {
-        const size_t drow = (size_t)tok * a.kslots + (a.kslots > 1 ? j0 : 0);
-        T* dst = dHf + drow * R + roff;
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) {
-          if (rb < nrb) {
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-              const int r = rb * 16 + 4 * g + v;
-              if (r < r_q) dst[r] = (T)(s * dacc[rb][v]);
-            }
-          }
-        }
-      }
-    } else {
-      // per-pair input: dx[xr] += dH_u A_q   (C^T = A_q^T dH^T, K = r_q)
-      F df[NM];
-#pragma unroll
-      for (int m = 0; m < NM; ++m) df[m] = Tr<T>::from_acc(dacc, m, s);
-      const bool al4 = (R & 3) == 0 && (roff & 3) == 0;
-      for (int c0 = 0; c0 < d_in; c0 += 16 * kNCH) {
-        f32x4 c[kNCH];
-#pragma unroll
-        for (int ch = 0; ch < kNCH; ++ch) {
-          c[ch] = f32x4{0.f, 0.f, 0.f, 0.f};
-          const int cc = c0 + ch * 16 + c16;
-          const bool cok = cc < d_in;
-#pragma unroll
-          for (int m = 0; m < NM; ++m) {
-            if (m < nmb) {
-              const F wf = load_acc_order<T>(At + (size_t)(cok ? cc : 0) * R + roff, r_q, m, g,
-                                             cok, al4);
-              c[ch] = Tr<T>::mma(wf, df[m], c[ch]);
-            }
-          }
-        }
-        if (valid) {
-          T* drow = DX + (size_t)xr * d_in + c0 + 4 * g;
-          f32x4 old[kNCH];
-#pragma unroll
-          for (int ch = 0; ch < kNCH; ++ch)
-            if (c0 + ch * 16 + 4 * g < d_in) old[ch] = Tr<T>::load4(drow + ch * 16);
-#pragma unroll
-          for (int ch = 0; ch < kNCH; ++ch)
-            if (c0 + ch * 16 + 4 * g < d_in) Tr<T>::store4(drow + ch * 16, old[ch] + c[ch]);
-        }
-      }
-    }
-  }
-}
-
-// ------------------------------------------------------------ column pass
-
-template <typename T>
-__device__ inline typename Tr<T>::frag load_frag_masked(const T* p, int nvalid) {
-  // PER consecutive elements, those at index >= nvalid read as zero
-  constexpr int PER = Tr<T>::PER;
-  if (nvalid >= PER) return Tr<T>::load(p);
-  typename Tr<T>::frag f = Tr<T>::zero();
-#pragma unroll
-  for (int e = 0; e < PER; ++e)
-    if (e < nvalid) f[e] = p[e];
-  return f;
-}
 
 template <typename T, int RB>
 __global__ __launch_bounds__(kThreads) void bwd_col_kernel(BwdArgs a) {
   using F = typename Tr<T>::frag;
   constexpr int PER = Tr<T>::PER;
   constexpr int KB = Tr<T>::KB;
-  constexpr int SLD = KB + PER;  // LDS row stride (elements): 80 bytes
-  __shared__ __attribute__((aligned(16))) T S[kTile * SLD];
+  constexpr int NKB = 4;                 // K-blocks per stage
+  constexpr int KC = NKB * KB;           // rows per stage
+  constexpr int SLD = KC + PER;          // LDS row stride (elements)
+  constexpr int TPR = kTile / PER;       // staging threads per row
+  constexpr int RPP = kThreads / TPR;    // rows per staging pass (= KB)
+  __shared__ __attribute__((aligned(16))) T S[2][kTile * SLD];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int c16 = lane & 15, g = lane >> 4;
   const int d_in = a.d_in, d_out = a.d_out, k = a.k, R = a.keys.R;
@@ -352,63 +173,76 @@ __global__ __launch_bounds__(kThreads) void bwd_col_kernel(BwdArgs a) {
     f32x4 acc[RB];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) acc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    // staging assignment: thread -> (row ul of the K-block, PER columns at cs)
-    constexpr int TPR = kTile / PER;  // threads per staged row
     const int ul = threadIdx.x / TPR, cs = (threadIdx.x % TPR) * PER;
-    for (int u0 = lo; u0 < hi; u0 += KB) {
-      float v[PER];
+    const int cc = col0 + cs;
+    const bool cok = cc < ncol;
+    // staged values of one stage: NKB passes of PER columns
+    float v[NKB][PER];
+    auto load_stage = [&](int u0) {
 #pragma unroll
-      for (int e = 0; e < PER; ++e) v[e] = 0.f;
-      const int u = u0 + ul;
-      const int cc = col0 + cs;
-      if (u < hi && cc < ncol) {
-        const int tok = a.row_token[u];
-        const uint32_t slots = a.row_slots[u];
-        if (isB) {
-          for (uint32_t mm = slots; mm; mm &= mm - 1u) {
-            const int p = tok * k + __builtin_ctz(mm);
-            const float w = a.pair_w ? a.pair_w[p] : 1.f;
-            const F f = Tr<T>::load(DY + (size_t)p * d_out + cc);
+      for (int ps = 0; ps < NKB; ++ps) {
 #pragma unroll
-            for (int e = 0; e < PER; ++e) v[e] += w * (float)f[e];
+        for (int e = 0; e < PER; ++e) v[ps][e] = 0.f;
+        const int u = u0 + ps * RPP + ul;
+        if (u < hi && cok) {
+          const int tok = a.row_token[u];
+          const uint32_t slots = a.row_slots[u];
+          if (isB) {
+            for (uint32_t mm = slots; mm; mm &= mm - 1u) {
+              const int p = tok * k + __builtin_ctz(mm);
+              const float w = a.pair_w ? a.pair_w[p] : 1.f;
+              float f[PER];
+              Tr<T>::to_f32(Tr<T>::load(DY + (size_t)p * d_out + cc), f);
+#pragma unroll
+              for (int e = 0; e < PER; ++e) v[ps][e] += w * f[e];
+            }
+          } else {
+            const int xr = a.per_pair ? tok * k + __builtin_ctz(slots) : tok;
+            Tr<T>::to_f32(Tr<T>::load(X + (size_t)xr * d_in + cc), v[ps]);
           }
-        } else {
-          const int xr = a.per_pair ? tok * k + __builtin_ctz(slots) : tok;
-          const F f = Tr<T>::load(X + (size_t)xr * d_in + cc);
-#pragma unroll
-          for (int e = 0; e < PER; ++e) v[e] = (float)f[e];
         }
       }
+    };
+    int buf = 0;
+    if (lo < hi) load_stage(lo);
+    for (int u0 = lo; u0 < hi; u0 += KC) {
+      T* Sb = S[buf];
 #pragma unroll
-      for (int e = 0; e < PER; ++e) S[(cs + e) * SLD + ul] = (T)v[e];
+      for (int ps = 0; ps < NKB; ++ps)
+#pragma unroll
+        for (int e = 0; e < PER; ++e) Sb[(cs + e) * SLD + ps * RPP + ul] = (T)v[ps][e];
       __syncthreads();
-      const F sf = *reinterpret_cast<const F*>(&S[(16 * wave + c16) * SLD + PER * g]);
-      const int kvalid = hi - (u0 + PER * g);
+      if (u0 + KC < hi) load_stage(u0 + KC);
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        if (rb < nrb) {
-          const int r = rb * 16 + c16;
-          F tf = Tr<T>::zero();
-          if (r < r_q && kvalid > 0)
-            tf = load_frag_masked<T>(small + (size_t)(roff + r) * a.ldh + (u0 - lo) + PER * g,
-                                     kvalid);
-          if (isB) acc[rb] = Tr<T>::mma(sf, tf, acc[rb]);   // D[n][r]
-          else acc[rb] = Tr<T>::mma(tf, sf, acc[rb]);       // D[r][c]
+      for (int kb = 0; kb < NKB; ++kb) {
+        const int ubase = u0 + kb * KB;
+        if (ubase >= hi) break;
+        const F sf = *reinterpret_cast<const F*>(&Sb[(16 * wave + c16) * SLD + kb * KB + PER * g]);
+        const int kvalid = hi - (ubase + PER * g);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          if (rb < nrb) {
+            const int r = rb * 16 + c16;
+            const F tf = (r < r_q)
+                ? load_frag<T>(small + (size_t)(roff + r) * a.ldh + (ubase - lo) + PER * g, kvalid, true)
+                : Tr<T>::zero();
+            if (isB) acc[rb] = Tr<T>::mma(sf, tf, acc[rb]);   // D[n][r]
+            else acc[rb] = Tr<T>::mma(tf, sf, acc[rb]);       // D[r][c]
+          }
         }
       }
-      __syncthreads();
+      buf ^= 1;
     }
     if (isB) {
-      const float s = a.alpha / (float)r_q;
       float* dst = a.dB + (size_t)d_out * roff;
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
         if (rb < nrb) {
           const int r = rb * 16 + c16;
 #pragma unroll
-          for (int v = 0; v < 4; ++v) {
-            const int n = col0 + 16 * wave + 4 * g + v;
-            if (r < r_q && n < d_out) dst[(size_t)n * r_q + r] = s * acc[rb][v];
+          for (int vv = 0; vv < 4; ++vv) {
+            const int n = col0 + 16 * wave + 4 * g + vv;
+            if (r < r_q && n < d_out) dst[(size_t)n * r_q + r] = acc[rb][vv];
           }
         }
       }
@@ -418,9 +252,9 @@ __global__ __launch_bounds__(kThreads) void bwd_col_kernel(BwdArgs a) {
         if (rb < nrb) {
           const int c = col0 + 16 * wave + c16;
 #pragma unroll
-          for (int v = 0; v < 4; ++v) {
-            const int r = rb * 16 + 4 * g + v;
-            if (r < r_q && c < d_in) a.dA[(size_t)(roff + r) * d_in + c] = acc[rb][v];
+          for (int vv = 0; vv < 4; ++vv) {
+            const int r = rb * 16 + 4 * g + vv;
+            if (r < r_q && c < d_in) a.dA[(size_t)(roff + r) * d_in + c] = acc[rb][vv];
           }
         }
       }
@@ -440,51 +274,52 @@ __global__ __launch_bounds__(kThreads) void bwd_col_kernel(BwdArgs a) {
   T* DX = static_cast<T*>(a.dx);
   const int KR = a.kslots * R;
   const bool vec = (R % PER) == 0;
-  f32x4 c[kNCH];
+  constexpr int UX = 4;
+  f32x4 c[4];
 #pragma unroll
-  for (int ch = 0; ch < kNCH; ++ch) c[ch] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int kk = 0; kk < KR; kk += KB) {
-    const int kof = kk + PER * g;
-    F df = Tr<T>::zero();
-    if (tok_ok && kof < KR) {
-      const T* src = dHf + (size_t)t * KR + kof;
-      df = vec ? Tr<T>::load(src) : load_frag_masked<T>(src, KR - kof);
-    }
+  for (int ch = 0; ch < 4; ++ch) c[ch] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int kk0 = 0; kk0 < KR; kk0 += UX * KB) {
+    F df[UX], wf[UX][4];
 #pragma unroll
-    for (int ch = 0; ch < kNCH; ++ch) {
-      const int cc = c0 + ch * 16 + c16;
-      F wf = Tr<T>::zero();
-      if (cc < d_in && kof < KR) {
-        if (vec) {
-          wf = Tr<T>::load(At + (size_t)cc * R + (kof % R));
-        } else {
+    for (int s = 0; s < UX; ++s) {
+      const int kof = kk0 + s * KB + PER * g;
+      df[s] = Tr<T>::zero();
+      if (tok_ok && kof < KR) {
+        const T* src = dHf + (size_t)t * KR + kof;
+        df[s] = load_frag<T>(src, KR - kof, vec);
+      }
 #pragma unroll
-          for (int e = 0; e < PER; ++e)
-            if (kof + e < KR) wf[e] = At[(size_t)cc * R + ((kof + e) % R)];
+      for (int ch = 0; ch < 4; ++ch) {
+        const int cc = c0 + ch * 16 + c16;
+        wf[s][ch] = Tr<T>::zero();
+        if (cc < d_in && kof < KR) {
+          if (vec) {
+            wf[s][ch] = Tr<T>::load(At + (size_t)cc * R + (kof % R));
+          } else {
+#pragma unroll
+            for (int e = 0; e < PER; ++e)
+              if (kof + e < KR) wf[s][ch][e] = At[(size_t)cc * R + ((kof + e) % R)];
+          }
         }
       }
-      c[ch] = Tr<T>::mma(wf, df, c[ch]);   // D[c][t]
     }
+#pragma unroll
+    for (int s = 0; s < UX; ++s)
+#pragma unroll
+      for (int ch = 0; ch < 4; ++ch) c[ch] = Tr<T>::mma(wf[s][ch], df[s], c[ch]);   // D[c][t]
   }
   if (tok_ok) {
     T* drow = DX + (size_t)t * d_in + c0 + 4 * g;
-    f32x4 old[kNCH];
 #pragma unroll
-    for (int ch = 0; ch < kNCH; ++ch)
-      if (c0 + ch * 16 + 4 * g < d_in) old[ch] = Tr<T>::load4(drow + ch * 16);
+    for (int ch = 0; ch < 4; ++ch) {
+      const int cc = c0 + ch * 16 + 4 * g;
+      if (cc < d_in) {
+        T* p = drow + ch * 16;
 #pragma unroll
-    for (int ch = 0; ch < kNCH; ++ch)
-      if (c0 + ch * 16 + 4 * g < d_in) Tr<T>::store4(drow + ch * 16, old[ch] + c[ch]);
+        for (int vv = 0; vv < 4; ++vv) p[vv] = (T)((float)p[vv] + c[ch][vv]);
+      }
+    }
   }
-}
-
-template <typename T, int RB>
-hipError_t launch_bwd_rb(const Problem& p, BwdArgs& a, int row_grid, hipStream_t stream) {
-  if (row_grid > 0) bwd_row_kernel<T, RB><<<row_grid, kThreads, 0, stream>>>(a);
-  const int items = a.nB + a.nA + a.nX;
-  if (items > 0) bwd_col_kernel<T, RB><<<items, kThreads, 0, stream>>>(a);
-  (void)p;
-  return hipGetLastError();
 }
 
 template <typename T>
@@ -492,12 +327,14 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
                         void* ws, hipStream_t stream) {
   const int R = p.keys.R;
   const int n_keys = p.keys.n_keys;
-  const WsLayout L = ws_layout(p.T, p.k, p.d_in, p.d_out, R, sizeof(T));
+  const int rpad = rank_pad(p.dtype, p.r_max);
+  const WsLayout L = ws_layout(p.T, p.k, p.d_in, p.d_out, R, rpad, sizeof(T));
   char* base = static_cast<char*>(ws);
+  const long P = (long)p.T * p.k;
+  const long ldh = (long)((((size_t)P) + 7) & ~(size_t)7);
   // kslots: rows of the dense dH buffer per token (1 when (token, key) is unique)
   const int kslots = (!p.per_pair && p.rt->mode == ACE_ROWS_GROUP_PAIRS) ? p.k : 1;
 
-  // prep: A^T, B_q^T, zero the dense dH buffer
   PrepArgs pa{};
   pa.A = p.A;
   pa.B = p.B;
@@ -507,7 +344,8 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
   pa.d_in = p.d_in;
   pa.d_out = p.d_out;
   pa.R = R;
-  pa.dHf_elems = p.per_pair ? 0 : (long)p.T * kslots * R;
+  const long dHf_bytes = p.per_pair ? 0 : (long)p.T * kslots * R * (long)sizeof(T);
+  pa.dHf_vecs = (dHf_bytes + 15) / 16;   // the region is 256-byte padded
   pa.keys = p.keys;
   pa.n_jobs = n_keys + 2;
   long nb = 0;
@@ -522,13 +360,64 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
   }
   pa.job_start[n_keys + 1] = (int)nb;
   pa.job_cols_tiles[n_keys + 1] = 1;
-  nb += (pa.dHf_elems + kTile * kTile - 1) / (kTile * kTile);
+  nb += (pa.dHf_vecs + 4 * kThreads - 1) / (4 * kThreads);
   pa.job_start[n_keys + 2] = (int)nb;
   if (nb > 0) bwd_prep_kernel<T><<<(int)nb, kThreads, 0, stream>>>(pa);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+
+  ContractArgs c{};
+  c.k = p.k;
+  c.alpha = p.alpha;
+  c.offsets = p.rt->offsets;
+  c.row_token = p.rt->row_token;
+  c.row_slots = p.rt->row_slots;
+  c.rpad = rpad;
+  c.ldh = ldh;
+  c.kslots = kslots;
+  c.keys = p.keys;
+  // Hs = s A x, per key [r][u]
+  c.src = p.x;
+  c.W = p.A;
+  c.ldw = p.d_in;
+  c.K = p.d_in;
+  c.src_mode = p.per_pair ? kSrcPerPair : kSrcShared;
+  c.out_t = base + L.Ht;
+  e = launch_contract(p.dtype, c, p.r_max, P, stream);
+  if (e != hipSuccess) return e;
+  // dH = s B^T G
+  c.src = dy;
+  c.W = base + L.Bt;
+  c.ldw = p.d_out;
+  c.K = p.d_out;
+  c.src_mode = kSrcGather;
+  c.pair_w = p.pair_w;
+  c.out_t = base + L.dHt;
+  c.out_dense = p.per_pair ? nullptr : base + L.dHf;
+  c.out_row = p.per_pair ? base + L.dHrow : nullptr;
+  e = launch_contract(p.dtype, c, p.r_max, P, stream);
+  if (e != hipSuccess) return e;
+  if (p.per_pair) {
+    ExpandArgs x{};
+    x.H = base + L.dHrow;
+    x.rpad = rpad;
+    x.W = base + L.At;
+    x.w_key_mul = 1;
+    x.w_stride_is_rank = 0;
+    x.offsets = p.rt->offsets;
+    x.row_token = p.rt->row_token;
+    x.row_slots = p.rt->row_slots;
+    x.k = p.k;
+    x.n_out = p.d_in;
+    x.out = dx;
+    x.pair_w = nullptr;
+    x.keys = p.keys;
+    e = launch_expand(p.dtype, x, p.r_max, P, stream);
+    if (e != hipSuccess) return e;
+  }
 
   BwdArgs a{};
   a.x = p.x;
-  a.A = p.A;
   a.pair_w = p.pair_w;
   a.dy = dy;
   a.dx = dx;
@@ -543,10 +432,8 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
   a.d_out = p.d_out;
   a.per_pair = p.per_pair;
   a.kslots = kslots;
-  a.alpha = p.alpha;
-  a.ldh = (long)((((size_t)p.T * p.k) + 7) & ~(size_t)7);
+  a.ldh = ldh;
   a.At = base + L.At;
-  a.Bt = base + L.Bt;
   a.Ht = base + L.Ht;
   a.dHt = base + L.dHt;
   a.dHf = base + L.dHf;
@@ -554,21 +441,21 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
   a.nB = n_keys * (int)tiles(p.d_out);
   a.nA = n_keys * (int)tiles(p.d_in);
   a.nX = p.per_pair ? 0 : (int)(tiles(p.T) * tiles(p.d_in));
-  const long P = (long)p.T * p.k;
-  const long bound = P > 0 ? (P + kBM - 1) / kBM + n_keys : 0;
-  const long cap = 4L * device_cu_count();
-  const int row_grid = (int)(bound < cap ? bound : cap);
-  const int rb = (p.r_max + 15) / 16;
-  if (rb <= 2) return launch_bwd_rb<T, 2>(p, a, row_grid, stream);
-  if (rb <= 4) return launch_bwd_rb<T, 4>(p, a, row_grid, stream);
-  if (rb <= 8) return launch_bwd_rb<T, 8>(p, a, row_grid, stream);
-  return launch_bwd_rb<T, 16>(p, a, row_grid, stream);
+  const int items = a.nB + a.nA + a.nX;
+  if (items > 0) {
+    const int rb = rank_blocks(p.r_max);
+    if (rb == 2) bwd_col_kernel<T, 2><<<items, kThreads, 0, stream>>>(a);
+    else if (rb == 4) bwd_col_kernel<T, 4><<<items, kThreads, 0, stream>>>(a);
+    else if (rb == 8) bwd_col_kernel<T, 8><<<items, kThreads, 0, stream>>>(a);
+    else bwd_col_kernel<T, 16><<<items, kThreads, 0, stream>>>(a);
+  }
+  return hipGetLastError();
 }
 
 }  // namespace
 
-size_t bwd_ws_bytes(int T, int k, int d_in, int d_out, int R) {
-  return ws_layout(T, k, d_in, d_out, R, sizeof(float)).total;
+size_t bwd_ws_bytes(int T, int k, int d_in, int d_out, int R, int r_max) {
+  return ws_layout(T, k, d_in, d_out, R, rank_pad(ACE_F32, r_max), sizeof(float)).total;
 }
 
 hipError_t launch_bwd(const Problem& p, const void* dy, void* dx, float* dA, float* dB, void* ws,
