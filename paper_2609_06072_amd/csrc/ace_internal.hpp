@@ -79,7 +79,40 @@ hipError_t launch_expand(int dtype, const ExpandArgs& a, int r_max, long P, hipS
 size_t fwd_ws_bytes(int T, int k, int r_max);
 hipError_t launch_fwd(const Problem& p, void* y, void* ws, hipStream_t stream);
 
-size_t bwd_ws_bytes(int T, int k, int d_in, int d_out, int R, int r_max);
+// Weight gradients dB_q = sum_u G_u Hs_u^T and dA_q = sum_u dH_u x_u^T over
+// the rows of each key (split over chunks of rows, reduced deterministically).
+struct GradArgs {
+  const void* x;              // [T][d_in] (shared) or [T*k][d_in] (per pair)
+  const void* dy;             // [T*k][d_out]
+  const float* pair_w;        // [T*k] or null (weight 1)
+  const void* Ht;             // Hs per key: rank row roff_q + r at Ht + (roff_q + r) * ldh,
+  const void* dHt;            //   column u - offsets[q]; dH likewise
+  long ldh;
+  float* dA;                  // [R][d_in]
+  float* dB;                  // key q: [d_out][r_q] at dB + d_out * roff_q
+  void* part;                 // split partials
+  const int32_t* offsets;
+  const int32_t* row_token;
+  const uint32_t* row_slots;
+  int32_t k, d_in, d_out, per_pair;
+  int32_t multi;              // rows may serve several slots
+  int32_t nbB, nbA;           // column blocks of dB / dA (set by the launcher)
+  KeyTable keys;
+};
+
+// dx[t][c] += sum_K dHf[t][K] At[c][K mod R], K < KR (shared input).
+struct DxArgs {
+  const void* dHf;            // [T][KR]
+  const void* At;             // [d_in][R]
+  void* dx;                   // [T][d_in]
+  int32_t T, d_in, R, KR;
+};
+
+size_t grads_part_bytes(int T, int k, int d_in, int d_out, int n_keys, int r_max);
+hipError_t launch_grads(int dtype, GradArgs g, int r_max, long P, hipStream_t stream);
+hipError_t launch_dx_gemm(int dtype, const DxArgs& d, hipStream_t stream);
+
+size_t bwd_ws_bytes(int T, int k, int d_in, int d_out, int n_keys, int R, int r_max);
 hipError_t launch_bwd(const Problem& p, const void* dy, void* dx, float* dA, float* dB, void* ws,
                       hipStream_t stream);
 

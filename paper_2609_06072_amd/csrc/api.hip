@@ -136,7 +136,7 @@ ace_status run_bwd(const Problem& p, const void* dy, void* dx, float* dA, float*
   if (!aligned(dy, 16) || !aligned(dx, 16))
     return fail(ACE_ERR_INVALID_ARG, "dy and dx must be 16-byte aligned");
   if (!aligned(dA, 4) || !aligned(dB, 4)) return fail(ACE_ERR_INVALID_ARG, "dA/dB misaligned");
-  const size_t need = bwd_ws_bytes(p.T, p.k, p.d_in, p.d_out, p.keys.R, p.r_max);
+  const size_t need = bwd_ws_bytes(p.T, p.k, p.d_in, p.d_out, p.keys.n_keys, p.keys.R, p.r_max);
   if (!ws || ws_bytes < need)
     return fail(ACE_ERR_WORKSPACE, "backward needs %zu workspace bytes, got %zu", need,
                 ws ? ws_bytes : (size_t)0);
@@ -272,7 +272,7 @@ size_t ace_workspace_bytes(ace_op op, int32_t T, int32_t k, int32_t d_in, int32_
         fail(ACE_ERR_INVALID_ARG, "invalid workspace query");
         return (size_t)-1;
       }
-      return round256(bwd_ws_bytes(T, k, d_in, d_out, n_keys * r_max, r_max));
+      return round256(bwd_ws_bytes(T, k, d_in, d_out, n_keys, n_keys * r_max, r_max));
   }
   fail(ACE_ERR_INVALID_ARG, "unknown op %d", (int)op);
   return (size_t)-1;
