@@ -10,7 +10,8 @@ routing, for both execution schemes on the same GPU:
   lora  -- expert-wise LoRA (rank r per expert) on gate, up and down.
 Metric: routed (token, expert) pairs per second of the ace step (fwd+bwd), the
 speedup over the lora step, and the HBM roofline fraction of the dominant
-kernel.  Prints one JSON line.
+call (the library call of the ace step that takes longest, all of its kernels).
+Prints one JSON line.
 """
 from __future__ import annotations
 
@@ -71,6 +72,7 @@ class Path:
             self.projs.append(Proj(proj, mode, im, ranks, b["x"], b["A"], b["B"], b["dy"], b["y"],
                                    b["dx"], b["dA"], b["dB"]))
         self.timer = None   # (proj name, phase) -> list of (start, end) events
+        self.marker = None  # callable(label) run before each phase (traffic pass)
 
     def _fwd(self, p):
         a = self.ace
@@ -93,6 +95,8 @@ class Path:
 
     def _timed(self, key, fn, *args):
         import torch
+        if self.marker is not None:
+            self.marker(f"{self.kind}:{key[0]}.{key[1]}")
         if self.timer is None:
             return fn(*args)
         s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -212,13 +216,204 @@ def cpu_baseline(cfg, rt, budget_s=15.0):
     while dt < 1.0 and Tp < cfg.T:
         Tp = min(cfg.T, Tp * 4)
         dt = run(Tp)
-    if dt < budget_s and Tp < cfg.T:
-        Tp = min(cfg.T, max(Tp, int(Tp * budget_s / max(dt, 1e-3))))
+    if dt < budget_s / 3 and Tp < cfg.T:
+        Tp = min(cfg.T, max(Tp, int(Tp * budget_s / 3 / max(dt, 1e-3))))
         dt = run(Tp)
+    # repeat the sample until about budget_s of work; report the median run
+    times = [dt]
+    while sum(times) < budget_s and len(times) < 9:
+        times.append(run(Tp))
+    dt = statistics.median(times)
     return {"value": Tp * cfg.k / dt, "unit": "routed tokens/s", "cores": int(threads),
             "kind": "oracle",
             "sample": f"first {Tp} of {cfg.T} tokens ({Tp * cfg.k} routed pairs), fwd+bwd of "
-                      f"{'/'.join(cfg.projections)} in fp64 numpy, {dt:.1f} s"}
+                      f"{'/'.join(cfg.projections)} in fp64 numpy; median of {len(times)} runs "
+                      f"({sum(times):.1f} s in total), {dt:.2f} s per run"}
+
+
+# ---------------------------------------------------------------- HBM traffic
+# Traffic is taken from two rocprofv3 counter passes over `--traffic-pass`
+# (FETCH_SIZE, then WRITE_SIZE), summarised by `--pmc-summary` into
+# profiles/traffic_<config>.txt together with a hash of the library sources;
+# the bench line reports it only while the sources still hash the same.
+CALIB_BYTES = 256 << 20          # plain device copy: reads and writes this much
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2609_06072_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith((".hip", ".hpp")):
+            h.update(f.encode())
+            h.update(open(os.path.join(csrc, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def traffic_file(config: str) -> str:
+    return os.path.join(PROFILES, f"traffic_{config}.txt")
+
+
+def traffic_pass(paths, labels_out: str):
+    """One calibration copy and one step of each path, each phase preceded by a
+    one-element fill kernel that marks where its dispatches start."""
+    import torch
+    mark = torch.zeros(1, dtype=torch.int32, device="cuda")
+    labels = []
+
+    def marker(label):
+        labels.append(label)
+        mark.zero_()
+
+    src = torch.randn(CALIB_BYTES // 4, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    for path in paths.values():
+        path.step()                       # warm
+    torch.cuda.synchronize()
+    marker("calib:copy")
+    dst.copy_(src)
+    for path in paths.values():
+        path.marker = marker
+        path.step()
+        path.marker = None
+    torch.cuda.synchronize()
+    with open(labels_out, "w") as f:
+        f.write("\n".join(labels) + "\n")
+
+
+def short_kernel(name: str) -> str:
+    import re
+    m = re.search(r"([a-z_]+_kernel)", name)
+    return m.group(1) if m else name.split("(")[0][:40]
+
+
+def _pmc_by_dispatch(csv_dir: str, counter: str, with_grid: bool = False):
+    import csv
+    import glob
+    files = glob.glob(os.path.join(csv_dir, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {csv_dir}")
+    out = {}
+    for r in csv.DictReader(open(files[0])):
+        if r["Counter_Name"] != counter:
+            continue
+        d = int(r["Dispatch_Id"])
+        name, kib = r["Kernel_Name"], float(r["Counter_Value"])
+        if with_grid:
+            name = (name, int(r["Grid_Size"]))
+        prev = out.get(d, (name, 0.0))
+        out[d] = (name, prev[1] + kib)
+    return [out[d] for d in sorted(out)]
+
+
+def _split_phases(disp, labels):
+    """Dispatches after the warm-up, split at the marker fills (the marker
+    kernel is the only one-element fill in the pass)."""
+    idx = [i for i, (n, _) in enumerate(disp) if "FillFunctor" in (n if isinstance(n, str) else n[0])]
+    idx = idx[-len(labels):]
+    if len(idx) != len(labels):
+        raise SystemExit("marker kernels not found")
+    phases = {}
+    for j, lab in enumerate(labels):
+        end = idx[j + 1] if j + 1 < len(idx) else len(disp)
+        phases[lab] = disp[idx[j] + 1:end]
+    return phases
+
+
+def pmc_summary(fetch_dir, write_dir, labels_path, config, command):
+    labels = [l.strip() for l in open(labels_path) if l.strip()]
+    f = _split_phases(_pmc_by_dispatch(fetch_dir, "FETCH_SIZE"), labels)
+    w = _split_phases(_pmc_by_dispatch(write_dir, "WRITE_SIZE"), labels)
+    cal_f = sum(v for _, v in f["calib:copy"]) * 1024
+    cal_w = sum(v for _, v in w["calib:copy"]) * 1024
+    kf, kw = CALIB_BYTES / cal_f, CALIB_BYTES / cal_w
+    lines = [f"# HBM traffic per call, {config}", f"source_hash {source_hash()}",
+             f"command {command}",
+             f"calibration copy of {CALIB_BYTES} B: FETCH_SIZE {cal_f:.0f} B, WRITE_SIZE {cal_w:.0f} B"
+             f" -> scale fetch {kf:.4f}, write {kw:.4f}",
+             "# phase  fetch_bytes  write_bytes  (scaled)  kernels"]
+    for lab in labels[1:]:
+        fb = sum(v for _, v in f[lab]) * 1024 * kf
+        wb = sum(v for _, v in w[lab]) * 1024 * kw
+        names = ",".join(short_kernel(n) for n, _ in f[lab])
+        lines.append(f"{lab} {fb:.0f} {wb:.0f} {names}")
+    os.makedirs(PROFILES, exist_ok=True)
+    with open(traffic_file(config), "w") as out:
+        out.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def trace_summary(trace_dir, fetch_dir, labels_path, config, command):
+    """Per-call kernel time from a rocprofv3 kernel trace of the bench: the
+    dispatch sequence of one step of each path (names and grid sizes, taken
+    from the marked counter pass) is matched against the trace, and each call's
+    kernel durations are averaged over every matched step."""
+    import csv
+    import glob
+    labels = [l.strip() for l in open(labels_path) if l.strip()]
+    ph = _split_phases(_pmc_by_dispatch(fetch_dir, "FETCH_SIZE", with_grid=True), labels)
+    tf = glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True)[0]
+    rows = sorted(csv.DictReader(open(tf)), key=lambda r: int(r["Dispatch_Id"]))
+    trace = [((r["Kernel_Name"], int(r["Grid_Size_X"])),
+              (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3) for r in rows]
+    keys = [t[0] for t in trace]
+    lines = [f"# kernel time per call, {config} (rocprofv3 kernel trace)", f"source_hash {source_hash()}",
+             f"command {command}"]
+    for kind in ("ace", "lora"):
+        calls = [(lab, [n for n, _ in ph[lab]]) for lab in labels if lab.startswith(kind + ":")]
+        sig = [n for _, ns in calls for n in ns]
+        acc = {lab: [] for lab, _ in calls}
+        per_kernel = {}
+        i, steps = 0, 0
+        while i + len(sig) <= len(keys):
+            if keys[i:i + len(sig)] == sig:
+                j = i
+                for lab, ns in calls:
+                    durs = [trace[j + m][1] for m in range(len(ns))]
+                    acc[lab].append(sum(durs))
+                    for m, n in enumerate(ns):
+                        per_kernel.setdefault((lab, m, short_kernel(n[0]), n[1] // kThreadsGuess), []).append(durs[m])
+                    j += len(ns)
+                steps += 1
+                i += len(sig)
+            else:
+                i += 1
+        lines.append(f"# {kind}: {steps} steps matched; call  kernels_us_avg  [kernel(grid) us_avg ...]")
+        for lab, _ in calls:
+            v = acc[lab]
+            if not v:
+                continue
+            ks = " ".join(f"{k[2]}({k[3]})={statistics.mean(d):.2f}"
+                          for k, d in sorted(per_kernel.items()) if k[0] == lab)
+            lines.append(f"{lab} {statistics.mean(v):.2f} {ks}")
+    sf = glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True)
+    if sf:
+        lines.append("# rocprofv3 --stats: kernel  calls  avg_us  min_us  max_us  percent")
+        for r in csv.DictReader(open(sf[0])):
+            lines.append(f"{short_kernel(r['Name'])} {r['Calls']} {float(r['AverageNs']) / 1e3:.2f} "
+                         f"{float(r['MinNs']) / 1e3:.2f} {float(r['MaxNs']) / 1e3:.2f} {r['Percentage']}")
+    os.makedirs(PROFILES, exist_ok=True)
+    with open(os.path.join(PROFILES, f"kernels_{config}.txt"), "w") as out:
+        out.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+kThreadsGuess = 256   # threads per workgroup of the library's kernels (grid printed in blocks)
+
+
+def read_traffic(config: str):
+    """{phase label: (fetch, write)} if the stored counters were taken on the
+    current sources, else None."""
+    p = traffic_file(config)
+    if not os.path.exists(p):
+        return None
+    rows = [l.split() for l in open(p) if l.strip() and not l.startswith("#")]
+    meta = {r[0]: r[1] for r in rows if r[0] == "source_hash"}
+    if meta.get("source_hash") != source_hash():
+        return None
+    return {r[0]: (float(r[1]), float(r[2])) for r in rows if ":" in r[0] and len(r) >= 3}
 
 
 def main():
@@ -230,8 +425,21 @@ def main():
     ap.add_argument("--config", default="olmoe_bf16", choices=W.CONFIG_ORDER)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--phases", action="store_true", help="print per-phase times to stderr")
+    ap.add_argument("--traffic-pass", metavar="LABELS_OUT",
+                    help="run one marked step of each path for rocprofv3 counter passes")
+    ap.add_argument("--pmc-summary", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "LABELS"),
+                    help="write profiles/traffic_<config>.txt from two counter passes")
+    ap.add_argument("--trace-summary", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "LABELS"),
+                    help="write profiles/kernels_<config>.txt from a kernel trace of the bench")
+    ap.add_argument("--pmc-command", default="", help="command recorded in the summary")
     args = ap.parse_args()
+
+    if args.pmc_summary:
+        pmc_summary(*args.pmc_summary, args.config, args.pmc_command)
+        return
+    if args.trace_summary:
+        trace_summary(*args.trace_summary, args.config, args.pmc_command)
+        return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -260,6 +468,9 @@ def main():
     ws_bwd = torch.empty(need, dtype=torch.uint8, device="cuda")
 
     paths = {kind: Path(ace, cfg, rt, kind, bufs, ws_perm, ws_bwd) for kind in ("ace", "lora")}
+    if args.traffic_pass:
+        traffic_pass(paths, args.traffic_pass)
+        return
     res = {}
     for kind, path in paths.items():
         per_step, phases = time_path(path, args.steps, args.warmup, args.repeats)
@@ -267,21 +478,34 @@ def main():
         res[kind] = dict(ms=statistics.median(plain), ms_std=statistics.pstdev(plain),
                          ms_with_events=statistics.median(per_step), phases=phases)
 
-    # algorithmic bytes of a step and of the dominant kernel
+    # algorithmic bytes of a step and of each call (proj.fwd / proj.bwd)
     T, P = cfg.T, cfg.P
     step_bytes = 0
-    gate_fwd_bytes = None
-    first = cfg.projections[0]
+    call_bytes = {}
     for proj in cfg.projections:
         d_in, d_out, im = cfg.proj_dims(proj)
         f, bb = algo_bytes(im == W.INPUT_SHARED, T, P, d_in, d_out, cfg.E * cfg.r_e, b)
         step_bytes += f + bb
-        if proj == first:
-            gate_fwd_bytes = f
+        call_bytes[f"{proj}.fwd"], call_bytes[f"{proj}.bwd"] = f, bb
     ace_ms = res["ace"]["ms"]
     lora_ms = res["lora"]["ms"]
-    kern_ms = res["ace"]["phases"][f"{first}.fwd"]
-    achieved = gate_fwd_bytes / (kern_ms * 1e-3) / 1e9
+    call_roofline = {
+        kind: {k: call_bytes[k] / (res[kind]["phases"][k] * 1e-3) / (HBM_PEAK_GBS * 1e9)
+               for k in call_bytes}
+        for kind in ("ace", "lora")}
+    # the dominant call of the ace step: the one that takes longest
+    dom = max(call_bytes, key=lambda k: res["ace"]["phases"][k])
+    dom_ms = res["ace"]["phases"][dom]
+    achieved = call_bytes[dom] / (dom_ms * 1e-3) / 1e9
+    proj, phase = dom.split(".")
+    d_in, d_out, im = cfg.proj_dims(proj)
+    grouped = im == W.INPUT_SHARED
+    entry = f"ace_{'grouped' if grouped else 'expertwise'}_lora_{phase}"
+    traffic = read_traffic(cfg.name)
+    dom_traffic = None
+    if traffic is not None and f"ace:{dom}" in traffic:
+        fb, wb = traffic[f"ace:{dom}"]
+        dom_traffic = fb + wb
     line = {
         "metric": METRIC,
         "value": P / (ace_ms * 1e-3),
@@ -308,9 +532,11 @@ def main():
         "step_roofline": {"bound": "hbm", "algorithmic_bytes": step_bytes,
                           "frac_ace": step_bytes / (ace_ms * 1e-3) / (HBM_PEAK_GBS * 1e9),
                           "frac_expertwise": step_bytes / (lora_ms * 1e-3) / (HBM_PEAK_GBS * 1e9)},
-        "roofline": {"bound": "hbm", "kernel": f"lora_fwd_kernel ({first}, grouped)",
+        "roofline": {"bound": "hbm", "kernel": f"{entry} ({proj}): all kernels of one call",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None},
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": dom_traffic,
+                     "algorithmic_bytes": call_bytes[dom], "ms_per_call": dom_ms},
+        "call_roofline_frac": call_roofline,
         "phases_ms": {k: {"ace": res["ace"]["phases"].get(k), "lora": res["lora"]["phases"].get(k)}
                       for k in sorted(set(res["ace"]["phases"]) | set(res["lora"]["phases"]))},
         "ms_std": {"ace": res["ace"]["ms_std"], "lora": res["lora"]["ms_std"]},
