@@ -173,10 +173,12 @@ __device__ inline void build_tile_table(const int32_t* offsets, int n_keys, int 
 // bstart[q] = first index of key q's tiles inside the bucket, bfirst[q] = the
 // key-local index of that tile, bstart[n_keys] = the bucket's tile count.
 constexpr int kXcds = 8;
-__device__ inline void build_bucket_table(const int32_t* offsets, int n_keys, int BM, int bucket,
-                                          int* seg, int* bstart, int* bfirst, int* scan_lds) {
+// With seg_map, the segments are seg_map[offsets[q]] .. seg_map[offsets[q+1]].
+__device__ inline void build_bucket_table(const int32_t* offsets, const int32_t* seg_map,
+                                          int n_keys, int BM, int bucket, int* seg, int* bstart,
+                                          int* bfirst, int* scan_lds) {
   const int t = threadIdx.x;
-  for (int i = t; i <= n_keys; i += kThreads) seg[i] = offsets[i];
+  for (int i = t; i <= n_keys; i += kThreads) seg[i] = seg_map ? seg_map[offsets[i]] : offsets[i];
   __syncthreads();
   int cnt = 0;
   if (t < n_keys) {

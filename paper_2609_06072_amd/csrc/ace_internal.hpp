@@ -32,9 +32,9 @@ hipError_t launch_permute(const int32_t* ids, int T, int k, int E, const int32_t
                           hipStream_t stream);
 
 // Source of the rows of a rank contraction.
-constexpr int kSrcShared = 0;   // x[row_token[u]]
-constexpr int kSrcPerPair = 1;  // x[t*k + j] (the row's single slot)
-constexpr int kSrcGather = 2;   // sum over the row's slots of w_tj * dY[t*k + j]
+constexpr int kSrcShared = 0;    // src[row_token[u]]
+constexpr int kSrcPerPair = 1;   // src[t*k + j] (the row's single slot)
+constexpr int kSrcPairList = 2;  // src[plist[u]], u a pair position (segments from ppos)
 
 struct ContractArgs {
   const void* src;            // x or dY, rows of length K
@@ -42,6 +42,8 @@ struct ContractArgs {
   int32_t ldw, K, src_mode, k;
   float alpha;
   const float* pair_w;
+  int32_t out_w;              // multiply a single-pair row's result by its pair weight
+  const int32_t* plist;       // kSrcPairList: pair at each position
   const int32_t* offsets;
   const int32_t* row_token;
   const uint32_t* row_slots;
@@ -49,6 +51,9 @@ struct ContractArgs {
   int32_t rpad;
   void* out_t;                // [R][ldh] (column u - offsets[q]) or null
   long ldh;
+  int32_t out_t_pairs;        // out_t holds one column per pair (times its weight):
+                              //   column = pair position - first position of the key
+  const int32_t* ppos;        // [U+1] first pair position of each row, or null (one per row)
   void* out_dense;            // [T * kslots][R] or null
   int32_t kslots;
   KeyTable keys;
@@ -79,14 +84,14 @@ hipError_t launch_expand(int dtype, const ExpandArgs& a, int r_max, long P, hipS
 size_t fwd_ws_bytes(int T, int k, int r_max);
 hipError_t launch_fwd(const Problem& p, void* y, void* ws, hipStream_t stream);
 
-// Weight gradients dB_q = sum_u G_u Hs_u^T and dA_q = sum_u dH_u x_u^T over
-// the rows of each key (split over chunks of rows, reduced deterministically).
+// Weight gradients dB_q = sum_p dY[p] Hw_p^T over the pairs of key q and
+// dA_q = sum_u dH_u x_u^T over its rows (split over chunks, reduced in order).
 struct GradArgs {
   const void* x;              // [T][d_in] (shared) or [T*k][d_in] (per pair)
   const void* dy;             // [T*k][d_out]
-  const float* pair_w;        // [T*k] or null (weight 1)
-  const void* Ht;             // Hs per key: rank row roff_q + r at Ht + (roff_q + r) * ldh,
-  const void* dHt;            //   column u - offsets[q]; dH likewise
+  const void* Hw;             // w_p s A x per pair: rank row roff_q + r at Hw + (roff_q + r) * ldh,
+                              //   column = pair position - first pair position of key q
+  const void* dHt;            // dH per row: same layout, column = u - offsets[q]
   long ldh;
   float* dA;                  // [R][d_in]
   float* dB;                  // key q: [d_out][r_q] at dB + d_out * roff_q
@@ -94,8 +99,9 @@ struct GradArgs {
   const int32_t* offsets;
   const int32_t* row_token;
   const uint32_t* row_slots;
+  const int32_t* ppos;        // [U+1] first pair position of each row, or null (one pair per row)
+  const int32_t* plist;       // [P] pair (t*k + j) at each position, or null
   int32_t k, d_in, d_out, per_pair;
-  int32_t multi;              // rows may serve several slots
   int32_t nbB, nbA;           // column blocks of dB / dA (set by the launcher)
   KeyTable keys;
 };

@@ -3,9 +3,12 @@
 // with either
 //   src_u = x[row_token[u]]            (shared input; Sec. 3.5: once per row,
 //                                       i.e. once per (token, active group))
-//   src_u = x[t*k + j]                 (per-pair input, down projection)
-//   src_u = sum_{j in slots(u)} w_tj dY[t*k + j]   (the row's output gradient)
-// and W = A (the shrink h = A_q x of Sec. 3.1.3) or W = B^T (dH = B_q^T G).
+//   src_u = S[t*k + j]                 (the row's single pair: per-pair input of
+//                                       the down projection, or dY)
+//   src_u = S[plist[u]]                (u a pair position: dY of that pair)
+// and W = A (the shrink h = A_q x of Sec. 3.1.3) or W = B^T (dH = B_q^T dY).
+// With out_w, the result of a single-pair row is multiplied by the pair's
+// weight.
 //
 // A block takes a tile of BM rows of one key.  The four waves split the
 // contraction (wave w takes K-blocks w, w+4, ...), so each source row and each
@@ -40,7 +43,8 @@ __global__ __launch_bounds__(kThreads) void contract_kernel(ContractArgs a) {
   __shared__ f32x4 red[4][NRB][RB][64];
   const int n_keys = a.keys.n_keys;
   const int bucket = blockIdx.x % kXcds;
-  build_bucket_table(a.offsets, n_keys, BM, bucket, seg, bstart, bfirst, scan);
+  build_bucket_table(a.offsets, a.src_mode == kSrcPairList ? a.ppos : nullptr, n_keys, BM, bucket,
+                     seg, bstart, bfirst, scan);
   const int total = bstart[n_keys];
   const int stride = gridDim.x / kXcds;  // the grid is a multiple of kXcds
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -49,7 +53,6 @@ __global__ __launch_bounds__(kThreads) void contract_kernel(ContractArgs a) {
   const T* W = static_cast<const T*>(a.W);
   const int K = a.K, k = a.k, R = a.keys.R;
   const int nks = (K + KB - 1) / KB, nks_full = K / KB;
-  const bool gather = a.src_mode == kSrcGather;
 
   for (int idx = blockIdx.x / kXcds; idx < total; idx += stride) {
     const int q = upper_index(bstart, n_keys, idx);
@@ -60,57 +63,36 @@ __global__ __launch_bounds__(kThreads) void contract_kernel(ContractArgs a) {
     const int nmb = (r_q + KB - 1) / KB;
     const int nrb = nmb * APF;  // rank blocks spanned by rank_of_row for r < r_q
 
-    // Source rows.  Rows past the segment read row 0 (never stored); weight
-    // rows past r_q re-read row r_q - 1 (zeroed before any store), so every
-    // load is unconditional and a wave keeps all of them in flight.
+    // Source rows.  Rows past the segment re-read the last row (never
+    // stored); weight rows past r_q re-read row r_q - 1 (zeroed before any
+    // store), so every load is unconditional and a wave keeps all of them in
+    // flight.
     const T* srow[NRB];
-    int tokv[NRB];
+    int sv[NRB];
     uint32_t slv[NRB];
-    bool multi = false;
 #pragma unroll
     for (int ib = 0; ib < NRB; ++ib) {  // unconditional loads: one round trip
-      const int u = u0 + 16 * ib + c16;
-      const int uc = min(u, u_end - 1);
-      tokv[ib] = a.row_token[uc];
-      slv[ib] = a.row_slots[uc];
+      const int uc = min(u0 + 16 * ib + c16, u_end - 1);
+      if (a.src_mode == kSrcPairList) {
+        sv[ib] = a.plist[uc];
+        slv[ib] = 1u;
+      } else {
+        sv[ib] = a.row_token[uc];
+        slv[ib] = a.row_slots[uc];
+      }
     }
 #pragma unroll
     for (int ib = 0; ib < NRB; ++ib) {
-      if (u0 + 16 * ib + c16 >= u_end) slv[ib] = 0u;
       const int j0 = __builtin_ctz(slv[ib] | 0x80000000u) & 31;
-      const int sr = a.src_mode == kSrcShared ? tokv[ib] : tokv[ib] * k + (slv[ib] ? j0 : 0);
+      const int sr = a.src_mode == kSrcPerPair ? sv[ib] * k + j0 : sv[ib];
       srow[ib] = S + (size_t)sr * K;
-      multi |= gather && ((slv[ib] & (slv[ib] - 1u)) != 0u || a.pair_w != nullptr);
     }
-    // a wave takes the weighted/multi-slot path if any of its lanes needs it
-    const bool wave_multi = __ballot(multi) != 0ull;
     const T* wrow[RB];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
       const int r = rank_of_row<T>(rb, c16);
       wrow[rb] = W + (size_t)(roff + (r < r_q ? r : r_q - 1)) * a.ldw;
     }
-
-    // The row's operand fragment at contraction offset kof (nv valid
-    // elements): one row, or the weighted sum over the row's slots.
-    auto gather_frag = [&](int ib, int kof, int nv) -> F {
-      float v[PER];
-#pragma unroll
-      for (int e = 0; e < PER; ++e) v[e] = 0.f;
-      for (uint32_t mm = slv[ib]; mm; mm &= mm - 1u) {
-        const int p = tokv[ib] * k + __builtin_ctz(mm);
-        const float w = a.pair_w ? a.pair_w[p] : 1.f;
-        float f[PER];
-        Tr<T>::to_f32(load_frag<T>(S + (size_t)p * K + kof, nv, true), f);
-#pragma unroll
-        for (int e = 0; e < PER; ++e) v[e] += w * f[e];
-      }
-      return Tr<T>::from_f32(v);
-    };
-    auto src_frag = [&](int ib, int kof, int nv, bool full) -> F {
-      if (!wave_multi) return full ? Tr<T>::load(srow[ib] + kof) : load_frag<T>(srow[ib] + kof, nv, true);
-      return gather_frag(ib, kof, nv);
-    };
 
     f32x4 acc[NRB][RB];
 #pragma unroll
@@ -124,22 +106,12 @@ __global__ __launch_bounds__(kThreads) void contract_kernel(ContractArgs a) {
       F sf[U][NRB];
       F wf[U][RB];
     };
-    auto load_stage = [&](int ks0, Stage& st) {  // single-row sources (no branches)
+    auto load_stage = [&](int ks0, Stage& st) {
 #pragma unroll
       for (int s = 0; s < U; ++s) {
         const int kof = (ks0 + 4 * s) * KB + PER * g;
 #pragma unroll
         for (int ib = 0; ib < NRB; ++ib) st.sf[s][ib] = Tr<T>::load(srow[ib] + kof);
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) st.wf[s][rb] = Tr<T>::load(wrow[rb] + kof);
-      }
-    };
-    auto load_stage_gather = [&](int ks0, Stage& st) {
-#pragma unroll
-      for (int s = 0; s < U; ++s) {
-        const int kof = (ks0 + 4 * s) * KB + PER * g;
-#pragma unroll
-        for (int ib = 0; ib < NRB; ++ib) st.sf[s][ib] = gather_frag(ib, kof, PER);
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) st.wf[s][rb] = Tr<T>::load(wrow[rb] + kof);
       }
@@ -156,7 +128,7 @@ __global__ __launch_bounds__(kThreads) void contract_kernel(ContractArgs a) {
     };
     // stages of this wave: ks0 = wave + 4*U*i with ks0 + 4*(U-1) < nks_full
     const int n_main = nks_full > wave + 4 * (U - 1) ? (nks_full - wave - 4 * (U - 1) + 4 * U - 1) / (4 * U) : 0;
-    if (!wave_multi) {
+    {
       Stage SA, SB;
       if (n_main > 0) load_stage(wave, SA);
       int i = 0;
@@ -167,12 +139,6 @@ __global__ __launch_bounds__(kThreads) void contract_kernel(ContractArgs a) {
         mma_stage(SB);
       }
       if (i < n_main) mma_stage(SA);
-    } else {
-      for (int i = 0; i < n_main; ++i) {
-        Stage st;
-        load_stage_gather(wave + 4 * U * i, st);
-        mma_stage(st);
-      }
     }
     int ks0 = wave + 4 * U * n_main;
     for (; ks0 < nks; ks0 += 4) {  // leftover K-blocks of this wave (masked tail)
@@ -181,7 +147,7 @@ __global__ __launch_bounds__(kThreads) void contract_kernel(ContractArgs a) {
       const int kc = nv > 0 ? kof : 0;
       F sf[NRB], wf[RB];
 #pragma unroll
-      for (int ib = 0; ib < NRB; ++ib) sf[ib] = nv > 0 ? src_frag(ib, kc, nv, nv >= PER) : Tr<T>::zero();
+      for (int ib = 0; ib < NRB; ++ib) sf[ib] = nv > 0 ? load_frag<T>(srow[ib] + kc, nv, true) : Tr<T>::zero();
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) wf[rb] = load_frag<T>(wrow[rb] + kc, nv, true);
 #pragma unroll
@@ -215,8 +181,17 @@ __global__ __launch_bounds__(kThreads) void contract_kernel(ContractArgs a) {
         if (rank_of_row<T>(rb, 4 * g + v) >= r_q) h[rb][v] = 0.f;
     }
     if (!valid) continue;
-    const int tok = a.row_token[u];
-    const uint32_t slots = a.row_slots[u];
+    int tok = 0;
+    uint32_t slots = 1u;
+    if (a.src_mode != kSrcPairList) {
+      tok = a.row_token[u];
+      slots = a.row_slots[u];
+    }
+    if (a.out_w && a.pair_w) {  // single-pair rows: times the pair's weight
+      const float w = a.pair_w[tok * k + (__builtin_ctz(slots | 0x80000000u) & 31)];
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) h[rb] *= w;
+    }
     if (a.out_row) {
       T* dst = static_cast<T*>(a.out_row) + (size_t)u * a.rpad;
 #pragma unroll
@@ -228,7 +203,7 @@ __global__ __launch_bounds__(kThreads) void contract_kernel(ContractArgs a) {
         }
       }
     }
-    if (a.out_t) {
+    if (a.out_t && !a.out_t_pairs) {
       T* dst = static_cast<T*>(a.out_t);
       const long col = u - lo;
 #pragma unroll
@@ -240,6 +215,22 @@ __global__ __launch_bounds__(kThreads) void contract_kernel(ContractArgs a) {
             if (r < r_q) dst[(size_t)(roff + r) * a.ldh + col] = (T)h[rb][v];
           }
         }
+    }
+    if (a.out_t && a.out_t_pairs) {  // one column per pair served, times its weight
+      T* dst = static_cast<T*>(a.out_t);
+      long col = a.ppos ? (long)a.ppos[u] - a.ppos[lo] : (long)(u - lo);
+      for (uint32_t mm = slots; mm; mm &= mm - 1u, ++col) {
+        const float w = a.pair_w ? a.pair_w[tok * k + __builtin_ctz(mm)] : 1.f;
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+          if (rb < nrb) {
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+              const int r = rank_of_row<T>(rb, 4 * g + v);
+              if (r < r_q) dst[(size_t)(roff + r) * a.ldh + col] = (T)(h[rb][v] * w);
+            }
+          }
+      }
     }
     if (a.out_dense) {
       const int j0 = __builtin_ctz(slots | 0x80000000u) & 31;

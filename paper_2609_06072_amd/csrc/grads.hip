@@ -1,22 +1,30 @@
 // Reductions of the backward over the rows of the permutation and over the
 // ranks (Sec. 3.1.2 / 3.4: a shared adapter collects every routed pair of its
 // group):
-//   dB_q[n][r] = sum_u G_u[n] Hs_u[r]          (G_u = sum_{j in slots(u)} w_j dY[t*k+j])
-//   dA_q[r][c] = sum_u dH_u[r] x_u[c]
+//   dB_q[n][r] = sum_p dY[p][n] Hw_p[r]    over the pairs p of key q, where
+//                Hw_p = w_p s_q A_q xin(p) (the contraction of the row serving
+//                p, times the pair's weight)
+//   dA_q[r][c] = sum_u dH_u[r] x_u[c]      over the rows u of key q
 //   dx[t][c]  += sum_K dHdense[t][K] A^T[c][K mod R]   (shared input only)
+// Both weight gradients are gathered-row GEMMs: a list of rows of a large
+// row-major operand L (dY or x) against a small operand S that is contiguous
+// along the contraction index (Hw or dH, stored per key as [r][position]).
 //
-// grad_w_kernel  -- one item = (key, chunk of <= 1024 rows, block of 128
-//   gradient columns, dB or dA).  Items are enumerated from the device-side
-//   segment offsets, so a skewed key is split over several blocks.  The
-//   chunk's row metadata goes to LDS first; then 128-row stages of the large
-//   operand (G or x, 16-byte loads issued one stage ahead into registers) are
-//   written transposed into LDS and multiplied on the matrix cores against the
-//   small operand (Hs or dH, stored per key as [r][u]).  A key of one chunk
-//   writes its gradient directly; otherwise every chunk writes a partial.
-// grad_reduce_kernel -- sums the partials of a (key, column block) in chunk
-//   order (deterministic) and writes the gradient.
-// dx_gemm_kernel -- dense GEMM dx += dHdense A on 128x128 output tiles, the
-//   tile staged through LDS for a coalesced read-modify-write of dx.
+// Items are (key, chunk of <= 1024 contraction indices, 128 gradient columns,
+// dB or dA), enumerated on the device from the segment offsets, so a skewed key
+// is split over several blocks; a key of one chunk writes its gradient
+// directly, otherwise every chunk writes a partial and grad_reduce_kernel sums
+// them in chunk order (deterministic).
+//
+// bf16 (grad_dma_kernel): the chunk's row indices go to LDS; every stage of 64
+// L rows x 128 columns and the matching S slice are copied global -> LDS with
+// global_load_lds_dwordx4 (no register staging), NBUF stages in flight.  L is
+// kept row-major in LDS (16-byte chunks XOR-swizzled by row) and read as MFMA
+// fragments along the contraction index with ds_read_b64_tr_b16: within each
+// 16-lane group, lane i receives element (i & 3) of the 8-byte reads of lanes
+// 4j + (i >> 2), j = 0..3.
+// fp32 (grad_reg_kernel): each thread loads a 4 x 4 block of L, transposes it
+// in registers and writes 16-byte vectors to LDS.
 #include "ace_device.hpp"
 #include "ace_internal.hpp"
 
@@ -25,25 +33,98 @@ namespace ace {
 namespace {
 
 constexpr int kColBlk = 128;     // gradient columns per item
-constexpr int kSplitRows = 1024; // rows per item (split-K chunk)
+constexpr int kSplitRows = 1024; // contraction indices per item (split-K chunk)
 
-// Item table of the weight-gradient pass: key q has ns_q = max(1, ceil(U_q /
-// kSplitRows)) chunks times nb column blocks.  istart[q] = first item of q.
-__device__ inline void build_item_table(const int32_t* offsets, int n_keys, int nb, int* seg,
-                                        int* istart, int* scan_lds) {
+// Item table shared by the gradient kernels.  For key q: rows seg[q] ..
+// seg[q+1], pairs pseg[q] .. pseg[q+1] (positions in pair order; = rows when
+// every row serves one pair).  Items of q: nsB(q) * nbB dB items, then
+// nsA(q) * nbA dA items, ns = max(1, ceil(count / kSplitRows)).
+struct GradTable {
+  int seg[kMaxKeys + 1];
+  int pseg[kMaxKeys + 1];
+  int istart[kMaxKeys + 1];
+};
+
+__device__ inline int n_split(int cnt) { return max(1, (cnt + kSplitRows - 1) / kSplitRows); }
+
+__device__ inline void build_grad_table(const GradArgs& a, GradTable& tb, int* scan_lds) {
   const int t = threadIdx.x;
-  for (int i = t; i <= n_keys; i += kThreads) seg[i] = offsets[i];
+  const int n_keys = a.keys.n_keys;
+  for (int i = t; i <= n_keys; i += kThreads) {
+    const int o = a.offsets[i];
+    tb.seg[i] = o;
+    tb.pseg[i] = a.ppos ? a.ppos[o] : o;
+  }
   __syncthreads();
   int items = 0;
-  if (t < n_keys) {
-    const int cnt = seg[t + 1] - seg[t];
-    items = max(1, (cnt + kSplitRows - 1) / kSplitRows) * nb;
-  }
+  if (t < n_keys)
+    items = n_split(tb.pseg[t + 1] - tb.pseg[t]) * a.nbB + n_split(tb.seg[t + 1] - tb.seg[t]) * a.nbA;
   int total;
   const int ex = block_exclusive_scan(items, scan_lds, &total);
-  if (t < n_keys) istart[t] = ex;
-  if (t == 0) istart[n_keys] = total;
+  if (t < n_keys) tb.istart[t] = ex;
+  if (t == 0) tb.istart[n_keys] = total;
   __syncthreads();
+}
+
+struct Item {
+  int q, s, cb, ns;
+  bool isB;
+  int kbase;   // first contraction index of the key (pair position or row)
+  int k0;      // first index of the chunk, relative to kbase
+  int nk;      // indices in the chunk
+};
+
+__device__ inline Item decode_item(const GradArgs& a, const GradTable& tb, int item) {
+  Item it;
+  const int n_keys = a.keys.n_keys;
+  it.q = upper_index(tb.istart, n_keys, item);
+  int local = item - tb.istart[it.q];
+  const int npB = tb.pseg[it.q + 1] - tb.pseg[it.q];
+  const int nsB = n_split(npB);
+  it.isB = local < nsB * a.nbB;
+  int cnt;
+  if (it.isB) {
+    it.s = local / a.nbB;
+    it.cb = local % a.nbB;
+    it.ns = nsB;
+    it.kbase = tb.pseg[it.q];
+    cnt = npB;
+  } else {
+    local -= nsB * a.nbB;
+    it.s = local / a.nbA;
+    it.cb = local % a.nbA;
+    cnt = tb.seg[it.q + 1] - tb.seg[it.q];
+    it.ns = n_split(cnt);
+    it.kbase = tb.seg[it.q];
+  }
+  it.k0 = it.s * kSplitRows;
+  it.nk = max(0, min(cnt - it.k0, kSplitRows));
+  return it;
+}
+
+// Row of the large operand for contraction index kabs of an item.
+__device__ inline int l_row(const GradArgs& a, bool isB, int kabs) {
+  if (isB) {
+    if (a.plist) return a.plist[kabs];
+    return a.row_token[kabs] * a.k + (__builtin_ctz(a.row_slots[kabs] | 0x80000000u) & 31);
+  }
+  const int tok = a.row_token[kabs];
+  return a.per_pair ? tok * a.k + (__builtin_ctz(a.row_slots[kabs] | 0x80000000u) & 31) : tok;
+}
+
+// Loads the chunk's L row indices into idx[0 .. kSplitRows) (clamped to the
+// chunk's last index; unused when the chunk is empty).
+__device__ inline void load_chunk_rows(const GradArgs& a, const Item& it, int* idx) {
+  if (it.nk <= 0) return;
+  constexpr int MPT = kSplitRows / kThreads;
+  int v[MPT];
+#pragma unroll
+  for (int i = 0; i < MPT; ++i) {
+    const int kabs = it.kbase + it.k0 + min((int)threadIdx.x + i * kThreads, it.nk - 1);
+    v[i] = l_row(a, it.isB, kabs);
+  }
+#pragma unroll
+  for (int i = 0; i < MPT; ++i) idx[threadIdx.x + i * kThreads] = v[i];
 }
 
 // Writes one accumulator fragment of an item's gradient block: element v of
@@ -72,289 +153,17 @@ __device__ inline void store_grad(const GradArgs& a, bool isB, int q, int col0, 
   }
 }
 
-// PER consecutive elements at p (one 16-byte load, always in bounds of the
-// workspace) with the ones from index nvalid on set to zero.
-template <typename T>
-__device__ inline typename Tr<T>::frag load_masked(const T* p, int nvalid) {
-  typename Tr<T>::frag f = Tr<T>::load(p);
-#pragma unroll
-  for (int e = 0; e < Tr<T>::PER; ++e)
-    if (e >= nvalid) f[e] = (T)0.f;
-  return f;
-}
-
-// Transpose of a PER x PER block held as PER row fragments: out[e] holds
-// element e of every row.
-template <typename T>
-__device__ inline void transpose_block(const typename Tr<T>::frag (&in)[Tr<T>::PER],
-                                       typename Tr<T>::frag (&out)[Tr<T>::PER]);
-
-template <>
-__device__ inline void transpose_block<float>(const f32x4 (&in)[4], f32x4 (&out)[4]) {
-#pragma unroll
-  for (int e = 0; e < 4; ++e) out[e] = f32x4{in[0][e], in[1][e], in[2][e], in[3][e]};
-}
-
-template <>
-__device__ inline void transpose_block<__bf16>(const bf16x8 (&in)[8], bf16x8 (&out)[8]) {
-  // word m of row r holds columns 2m (low half) and 2m+1 (high half); word m2
-  // of column e holds rows 2m2 (low half) and 2m2+1 (high half)
-  u32x4 w[8];
-#pragma unroll
-  for (int r = 0; r < 8; ++r) w[r] = __builtin_bit_cast(u32x4, in[r]);
-#pragma unroll
-  for (int m = 0; m < 4; ++m) {
-    u32x4 ev, od;
-#pragma unroll
-    for (int m2 = 0; m2 < 4; ++m2) {
-      const uint32_t a = w[2 * m2][m], b = w[2 * m2 + 1][m];
-      ev[m2] = (a & 0xffffu) | (b << 16);
-      od[m2] = (a >> 16) | (b & 0xffff0000u);
-    }
-    out[2 * m] = __builtin_bit_cast(bf16x8, ev);
-    out[2 * m + 1] = __builtin_bit_cast(bf16x8, od);
-  }
-}
-
-// Stage geometry of the weight-gradient kernel.
-template <typename T>
-struct GradGeo {
-  static constexpr int PER = Tr<T>::PER, KB = Tr<T>::KB;
-  static constexpr int NKB = 4;                      // K-blocks per stage
-  static constexpr int RPS = NKB * KB;               // rows per stage (128 bf16, 64 f32)
-  static constexpr int NI = RPS / PER;               // row groups of PER rows per stage
-  static constexpr int NJ = kColBlk / PER;           // 16-byte column pieces per row
-  static constexpr int NBLK = NI * NJ / kThreads;    // PER x PER blocks per thread (1 bf16, 2 f32)
-  static constexpr int TI = NI / 8;                  // 8 x 8 block tiles along the rows
-  static constexpr int SLD = RPS + PER;              // LDS stride of a transposed column (elements)
-  static constexpr int MPT = kSplitRows / kThreads;
-  static_assert(NBLK >= 1 && NI % 8 == 0, "stage shape");
-};
-
-template <typename T>
-struct GradSmem {
-  int seg[kMaxKeys + 1];
-  int istart[kMaxKeys + 1];
-  __attribute__((aligned(16))) T S[kColBlk * GradGeo<T>::SLD];
-  // per row of the chunk: source row of the first slot (pair for dB, x row
-  // for dA); dB only: pair of the second slot (the first again if none, bit 31
-  // set when there are more) and the weights of the two slots
-  int m0[kSplitRows];
-  int m1[kSplitRows];
-  float mw0[kSplitRows];
-  float mw1[kSplitRows];
-};
-
-// One item: rows r0 .. r0+nrows of key q against gradient columns col0 ..
-// col0+128 of dB_q (ISB) or dA_q.  TWO: rows may serve several slots.
-template <typename T, int RB, bool ISB, bool TWO>
-__device__ __forceinline__ void grad_item(const GradArgs& a, GradSmem<T>& sm, int item, int q, int s,
-                                          int cb, const int (&bi)[GradGeo<T>::NBLK],
-                                          const int (&bj)[GradGeo<T>::NBLK]) {
-  using G = GradGeo<T>;
-  using F = typename Tr<T>::frag;
-  constexpr int PER = G::PER, KB = G::KB, NKB = G::NKB, RPS = G::RPS, NBLK = G::NBLK;
-  constexpr int SLD = G::SLD, MPT = G::MPT;
-  constexpr bool PF = RB <= 2;  // small-operand fragments prefetched a stage ahead
-  constexpr int NKP = PF ? NKB : 1;
-  const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
-  const int c16 = lane & 15, g = lane >> 4;
-  const int k = a.k;
-  const int lo = sm.seg[q], hi = sm.seg[q + 1];
-  const int ns = max(1, (hi - lo + kSplitRows - 1) / kSplitRows);
-  const int r0 = lo + s * kSplitRows;
-  const int nrows = max(0, min(hi, r0 + kSplitRows) - r0);
-  const int ncol = ISB ? a.d_out : a.d_in;
-  const int col0 = cb * kColBlk;
-  const int r_q = a.keys.rank[q], roff = a.keys.roff[q];
-  const int nrb = (r_q + 15) >> 4;
-  const T* small = static_cast<const T*>(ISB ? a.Ht : a.dHt);
-  const T* src = static_cast<const T*>(ISB ? a.dy : a.x);
-  const T* DY = static_cast<const T*>(a.dy);
-  const int lds_src = ISB ? a.d_out : a.d_in;
-  const long hcol0 = (long)(r0 - lo);   // column of the chunk's first row in Ht/dHt
-  const long hmax = a.ldh - PER;
-
-  __syncthreads();  // the previous item's readers of the metadata and S are done
-  if (nrows > 0) {
-    int tv[MPT];
-    uint32_t sv[MPT];
-#pragma unroll
-    for (int i = 0; i < MPT; ++i) {
-      const int u = r0 + min(tid + i * kThreads, nrows - 1);
-      tv[i] = a.row_token[u];
-      sv[i] = a.row_slots[u];
-    }
-    int p0[MPT], p1[MPT];
-#pragma unroll
-    for (int i = 0; i < MPT; ++i) {
-      const uint32_t sl = sv[i] | (sv[i] == 0u ? 1u : 0u);  // rows always serve a slot
-      const uint32_t rest = sl & (sl - 1u);
-      p0[i] = tv[i] * k + __builtin_ctz(sl);
-      p1[i] = tv[i] * k + __builtin_ctz(rest ? rest : sl);
-      sm.m0[tid + i * kThreads] = ISB ? p0[i] : (a.per_pair ? p0[i] : tv[i]);
-      if (ISB) sm.m1[tid + i * kThreads] = p1[i] | ((rest & (rest - 1u)) ? (int)0x80000000 : 0);
-    }
-    if (ISB) {
-      if (a.pair_w) {
-        float w0[MPT], w1[MPT];
-#pragma unroll
-        for (int i = 0; i < MPT; ++i) {
-          w0[i] = a.pair_w[p0[i]];
-          w1[i] = a.pair_w[p1[i]];
-        }
-#pragma unroll
-        for (int i = 0; i < MPT; ++i) {
-          sm.mw0[tid + i * kThreads] = w0[i];
-          sm.mw1[tid + i * kThreads] = w1[i];
-        }
-      } else {
-#pragma unroll
-        for (int i = 0; i < MPT; ++i) {
-          sm.mw0[tid + i * kThreads] = 1.f;
-          sm.mw1[tid + i * kThreads] = 1.f;
-        }
-      }
-    }
-  }
-  __syncthreads();
-
-  f32x4 acc[2][RB];
-#pragma unroll
-  for (int cbi = 0; cbi < 2; ++cbi)
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) acc[cbi][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int nst = (nrows + RPS - 1) / RPS;
-  F v[NBLK][PER];
-  F v2[TWO ? NBLK : 1][PER];
-  F tf[NKP][RB];
-  auto load_small = [&](int st, int kb, F* dst) {
-    const int ul = st * RPS + kb * KB + PER * g;
-    const long hc = min(hcol0 + ul, hmax);   // a clamped fragment is fully masked
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      if (rb < nrb) {
-        // rank rows past r_q repeat row r_q - 1; nothing is stored for them
-        const int rr = min(16 * rb + c16, r_q - 1);
-        dst[rb] = load_masked<T>(small + (size_t)(roff + rr) * a.ldh + hc, nrows - ul);
-      }
-    }
-  };
-  auto load_stage = [&](int st) {
-#pragma unroll
-    for (int x = 0; x < NBLK; ++x) {
-      const int cc = min(col0 + PER * bj[x], ncol - PER);
-#pragma unroll
-      for (int r = 0; r < PER; ++r) {
-        const int row = min(st * RPS + PER * bi[x] + r, nrows - 1);
-        v[x][r] = Tr<T>::load(src + (size_t)sm.m0[row] * lds_src + cc);
-      }
-      if (TWO) {
-#pragma unroll
-        for (int r = 0; r < PER; ++r) {
-          const int row = min(st * RPS + PER * bi[x] + r, nrows - 1);
-          v2[TWO ? x : 0][r] = Tr<T>::load(DY + (size_t)(sm.m1[row] & 0x7fffffff) * a.d_out + cc);
-        }
-      }
-    }
-    if (PF) {
-#pragma unroll
-      for (int kb = 0; kb < NKP; ++kb) load_small(st, kb, tf[kb]);
-    }
-  };
-  auto write_stage = [&](int st) {
-#pragma unroll
-    for (int x = 0; x < NBLK; ++x) {
-      const bool cok = col0 + PER * bj[x] < ncol;
-      if (ISB) {  // G rows: weighted sum of the row's slots, rounded to T
-#pragma unroll
-        for (int r = 0; r < PER; ++r) {
-          const int row = st * RPS + PER * bi[x] + r;
-          const int rowc = min(row, nrows - 1);
-          float f[PER];
-          Tr<T>::to_f32(v[x][r], f);
-          const float w0 = sm.mw0[rowc];
-#pragma unroll
-          for (int e = 0; e < PER; ++e) f[e] *= w0;
-          if (TWO) {
-            const int p1 = sm.m1[rowc];
-            const float w1 = (p1 & 0x7fffffff) != sm.m0[rowc] ? sm.mw1[rowc] : 0.f;
-            float f2[PER];
-            Tr<T>::to_f32(v2[TWO ? x : 0][r], f2);
-#pragma unroll
-            for (int e = 0; e < PER; ++e) f[e] += w1 * f2[e];
-            if (p1 < 0 && row < nrows) {  // third and further slots (rare)
-              const int u = r0 + row;
-              const int tok = a.row_token[u];
-              uint32_t mm = a.row_slots[u];
-              mm &= mm - 1u;
-              mm &= mm - 1u;
-              const int cc = min(col0 + PER * bj[x], ncol - PER);
-              for (; mm; mm &= mm - 1u) {
-                const int p2 = tok * k + __builtin_ctz(mm);
-                const float w = a.pair_w ? a.pair_w[p2] : 1.f;
-                float f3[PER];
-                Tr<T>::to_f32(Tr<T>::load(DY + (size_t)p2 * a.d_out + cc), f3);
-#pragma unroll
-                for (int e = 0; e < PER; ++e) f[e] += w * f3[e];
-              }
-            }
-          }
-          v[x][r] = Tr<T>::from_f32(f);
-        }
-      }
-      // rows past the chunk and columns past the matrix are zero
-#pragma unroll
-      for (int r = 0; r < PER; ++r)
-        if (!(cok && st * RPS + PER * bi[x] + r < nrows)) v[x][r] = Tr<T>::zero();
-      F o[PER];
-      transpose_block<T>(v[x], o);
-#pragma unroll
-      for (int e = 0; e < PER; ++e)
-        *reinterpret_cast<F*>(&sm.S[(PER * bj[x] + e) * SLD + PER * bi[x]]) = o[e];
-    }
-  };
-  if (nst > 0) load_stage(0);
-  for (int st = 0; st < nst; ++st) {
-    write_stage(st);
-    F cur[NKP][RB];
-    if (PF) {
-#pragma unroll
-      for (int kb = 0; kb < NKP; ++kb)
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) cur[kb][rb] = tf[kb][rb];
-    }
-    __syncthreads();
-    if (st + 1 < nst) load_stage(st + 1);
-#pragma unroll
-    for (int kb = 0; kb < NKB; ++kb) {
-      const int ul = st * RPS + kb * KB;  // first row of the K-block (chunk-local)
-      if (ul >= nrows) break;
-      F tl[RB];
-      if (!PF) load_small(st, kb, tl);
-#pragma unroll
-      for (int cbi = 0; cbi < 2; ++cbi) {
-        const F sf = *reinterpret_cast<const F*>(&sm.S[(32 * wave + 16 * cbi + c16) * SLD + kb * KB + PER * g]);
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) {
-          if (rb < nrb) {
-            const F t = PF ? cur[PF ? kb : 0][rb] : tl[rb];
-            if (ISB) acc[cbi][rb] = Tr<T>::mma(sf, t, acc[cbi][rb]);   // D[n][r]
-            else acc[cbi][rb] = Tr<T>::mma(t, sf, acc[cbi][rb]);       // D[r][c]
-          }
-        }
-      }
-    }
-    __syncthreads();  // the next stage overwrites S
-  }
-
-  if (ns == 1) {
+template <int RB>
+__device__ inline void finish_item(const GradArgs& a, const Item& it, int item,
+                                   const f32x4 (&acc)[2][RB]) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int nrb = (a.keys.rank[it.q] + 15) >> 4;
+  if (it.ns == 1) {
 #pragma unroll
     for (int cbi = 0; cbi < 2; ++cbi)
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb)
-        if (rb < nrb) store_grad(a, ISB, q, col0, wave, cbi, rb, lane, acc[cbi][rb]);
+        if (rb < nrb) store_grad(a, it.isB, it.q, it.cb * kColBlk, wave, cbi, rb, lane, acc[cbi][rb]);
   } else {
     f32x4* part = reinterpret_cast<f32x4*>(a.part) + (size_t)item * (4 * 2 * RB * 64);
 #pragma unroll
@@ -364,49 +173,341 @@ __device__ __forceinline__ void grad_item(const GradArgs& a, GradSmem<T>& sm, in
   }
 }
 
-template <typename T, int RB, bool MULTI>
-__global__ __launch_bounds__(kThreads) void grad_w_kernel(GradArgs a) {
-  using G = GradGeo<T>;
-  __shared__ GradSmem<T> sm;
-  const int n_keys = a.keys.n_keys;
-  const int nb = a.nbB + a.nbA;
-  build_item_table(a.offsets, n_keys, nb, sm.seg, sm.istart, reinterpret_cast<int*>(sm.S));
-  const int total = sm.istart[n_keys];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  // Staging: thread block x covers rows PER*bi .. +PER and columns PER*bj ..
-  // +PER of a stage.  Eight consecutive lanes take eight consecutive row
-  // groups of one column piece, so a load instruction reads whole 128-byte
-  // lines and the transposed 16-byte LDS writes of eight lanes are contiguous.
-  int bi[G::NBLK], bj[G::NBLK];
+// ----------------------------------------------------------------- bf16 path
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
+// vmcnt bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8).
+template <int N>
+__device__ inline void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+typedef __attribute__((ext_vector_type(4))) short s16x4;
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+typedef __attribute__((address_space(3))) void lds_void;
+
+template <int RB>
+struct DmaGeo {
+  static constexpr int RS = 64;                     // contraction indices per stage
+  static constexpr int NBUF = RB <= 2 ? 3 : 2;      // stages in LDS
+  static constexpr int LBYTES = RS * 256;           // 64 rows x 128 bf16
+  static constexpr int SROWS = 16 * RB;             // rank rows of the S slice
+  static constexpr int SBYTES = SROWS * RS * 2;     // rank rows x 64 bf16
+  static constexpr int NL = 4;                      // L copies per wave per stage
+  static constexpr int NS = RB / 2;                 // S copies per wave per stage
+};
+
+// 16-byte chunk position of chunk c of L row r (0..63) inside the LDS row:
+// spreads the 16 rows that one transposed read touches over the banks.
+__device__ inline int l_swz(int r) { return 2 * ((r & 3) | (((r >> 3) & 1) << 2)); }
+
+// 16-byte copy global -> LDS: lane l's bytes land at lds_base + 16 * l
+// (lds_base wave-uniform).  Issued as inline assembly so that the compiler does
+// not treat every later LDS read as dependent on it; completion is awaited
+// explicitly with wait_vmcnt before the barrier that publishes a stage.
+__device__ inline void dma16(const void* g, uint32_t lds_base) {
+  asm volatile("global_load_lds_dwordx4 %1, off" ::"{m0}"(lds_base), "v"(g) : "memory");
+}
+
+__device__ inline uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const lds_void*)p;
+}
+
+template <int RB>
+struct DmaSmem {
+  __attribute__((aligned(16))) char L[DmaGeo<RB>::NBUF][DmaGeo<RB>::LBYTES];
+  __attribute__((aligned(16))) char S[DmaGeo<RB>::NBUF][DmaGeo<RB>::SBYTES];
+  int idx[kSplitRows];
+  GradTable tb;
+};
+
+// Loads the chunk's L row indices into idx (clamped to the last index).
+template <bool ISB>
+__device__ inline void load_rows(const GradArgs& a, const Item& it, int* idx) {
+  if (it.nk <= 0) return;
+  constexpr int MPT = kSplitRows / kThreads;
+  int kabs[MPT], v[MPT];
 #pragma unroll
-  for (int x = 0; x < G::NBLK; ++x) {
-    const int tile = wave + 4 * x;
-    bi[x] = (tile % G::TI) * 8 + (lane & 7);
-    bj[x] = (tile / G::TI) * 8 + (lane >> 3);
+  for (int i = 0; i < MPT; ++i)
+    kabs[i] = it.kbase + it.k0 + min((int)threadIdx.x + i * kThreads, it.nk - 1);
+  if (ISB && a.plist) {
+#pragma unroll
+    for (int i = 0; i < MPT; ++i) v[i] = a.plist[kabs[i]];
+  } else {
+    int tok[MPT];
+    uint32_t sl[MPT];
+#pragma unroll
+    for (int i = 0; i < MPT; ++i) {
+      tok[i] = a.row_token[kabs[i]];
+      sl[i] = a.row_slots[kabs[i]];
+    }
+#pragma unroll
+    for (int i = 0; i < MPT; ++i) {
+      const int p = tok[i] * a.k + (__builtin_ctz(sl[i] | 0x80000000u) & 31);
+      v[i] = (ISB || a.per_pair) ? p : tok[i];
+    }
   }
+#pragma unroll
+  for (int i = 0; i < MPT; ++i) idx[threadIdx.x + i * kThreads] = v[i];
+}
+
+template <int RB, bool ISB>
+__device__ __forceinline__ void dma_item(const GradArgs& a, DmaSmem<RB>& sm, const Item& it,
+                                         int item) {
+  using G = DmaGeo<RB>;
+  constexpr int RS = G::RS, NBUF = G::NBUF;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int c16 = lane & 15, g = lane >> 4;
+  const int q = it.q;
+  const int r_q = a.keys.rank[q], roff = a.keys.roff[q];
+  const __bf16* L = static_cast<const __bf16*>(ISB ? a.dy : a.x);
+  const int ldl = ISB ? a.d_out : a.d_in;
+  const __bf16* S = static_cast<const __bf16*>(ISB ? a.Hw : a.dHt);
+  const int col0 = it.cb * kColBlk;
+  const int nst = (it.nk + RS - 1) / RS;
+
+  __syncthreads();  // the previous item is done with idx and the buffers
+  load_rows<ISB>(a, it, sm.idx);
+  __syncthreads();
+
+  const int lrow_in = lane >> 4;   // row inside a 4-row copy
+  const int lpos = lane & 15;      // 16-byte position in the LDS row
+  const int srow_in = lane >> 3;   // rank row inside an 8-row copy
+  const int spos = lane & 7;
+  auto issue = [&](int st) {
+    const int b = st % NBUF;
+#pragma unroll
+    for (int i = 0; i < G::NL; ++i) {
+      const int r0 = 16 * wave + 4 * i;
+      const int r = r0 + lrow_in;                       // row of the stage
+      const int row = sm.idx[min(st * RS + r, it.nk - 1)];
+      const int c = lpos ^ l_swz(r);                    // chunk this lane copies
+      const int col = min(col0 + 8 * c, ldl - 8);
+      dma16(L + (size_t)row * ldl + col,
+            __builtin_amdgcn_readfirstlane(lds_addr(&sm.L[b][r0 * 256])));
+    }
+#pragma unroll
+    for (int i = 0; i < G::NS; ++i) {
+      const int rr0 = 8 * (wave * G::NS + i);
+      const int rr = rr0 + srow_in;                     // rank row of the slice
+      const int c = spos ^ (rr & 7);
+      const long col = min((long)it.k0 + st * RS + 8 * c, a.ldh - 8);
+      dma16(S + (size_t)(roff + min(rr, r_q - 1)) * a.ldh + col,
+            __builtin_amdgcn_readfirstlane(lds_addr(&sm.S[b][rr0 * RS * 2])));
+    }
+  };
+
+  f32x4 acc[2][RB];
+#pragma unroll
+  for (int cbi = 0; cbi < 2; ++cbi)
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) acc[cbi][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+#pragma unroll
+  for (int p = 0; p < NBUF - 1; ++p)
+    if (p < nst) issue(p);
+  for (int st = 0; st < nst; ++st) {
+    // this wave's copies of stage st are done once at most the later stages'
+    // copies are outstanding; the barrier then publishes every wave's copies
+    if (NBUF == 3 && st + 1 < nst) wait_vmcnt<G::NL + G::NS>();
+    else wait_vmcnt<0>();
+    __syncthreads();
+    if (st + NBUF - 1 < nst) issue(st + NBUF - 1);
+    const int b = st % NBUF;
+#pragma unroll
+    for (int kb = 0; kb < RS / 32; ++kb) {
+      const int kk = st * RS + kb * 32;   // chunk-relative index of the K-block
+      if (kk >= it.nk) break;
+      const int nv = it.nk - (kk + 8 * g);
+      bf16x8 sf[RB];
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        const int rr = 16 * rb + c16;
+        const int pos = (kb * 4 + g) ^ (rr & 7);
+        bf16x8 f = *reinterpret_cast<const bf16x8*>(&sm.S[b][rr * RS * 2 + pos * 16]);
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (e >= nv) f[e] = (__bf16)0.f;
+        sf[rb] = f;
+      }
+#pragma unroll
+      for (int cbi = 0; cbi < 2; ++cbi) {
+        const int n0 = 32 * wave + 16 * cbi;
+        s16x4 h2[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int r = kb * 32 + 8 * g + 4 * h + (c16 >> 2);
+          const int c = (n0 >> 3) + ((c16 & 3) >> 1);
+          const int off = r * 256 + ((c ^ l_swz(r)) << 4) + ((c16 & 1) << 3);
+          h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)&sm.L[b][off]);
+        }
+        const bf16x8 lf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(h2[0], h2[1], 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          if (ISB) acc[cbi][rb] = Tr<__bf16>::mma(lf, sf[rb], acc[cbi][rb]);   // D[n][r]
+          else acc[cbi][rb] = Tr<__bf16>::mma(sf[rb], lf, acc[cbi][rb]);       // D[r][c]
+        }
+      }
+    }
+  }
+  finish_item<RB>(a, it, item, acc);
+}
+
+template <int RB>
+__global__ __launch_bounds__(kThreads) void grad_dma_kernel(GradArgs a) {
+  __shared__ DmaSmem<RB> sm;
+  build_grad_table(a, sm.tb, sm.idx);
+  const int total = sm.tb.istart[a.keys.n_keys];
   for (int item = blockIdx.x; item < total; item += gridDim.x) {
-    const int q = upper_index(sm.istart, n_keys, item);
-    const int local = item - sm.istart[q];
-    const int s = local / nb, rem = local % nb;
-    if (rem < a.nbB) grad_item<T, RB, true, MULTI>(a, sm, item, q, s, rem, bi, bj);
-    else grad_item<T, RB, false, false>(a, sm, item, q, s, rem - a.nbB, bi, bj);
+    const Item it = decode_item(a, sm.tb, item);
+    if (it.isB) dma_item<RB, true>(a, sm, it, item);
+    else dma_item<RB, false>(a, sm, it, item);
   }
 }
 
-// One block per (key, column block, dB|dA): sums the chunk partials in order.
+// ----------------------------------------------------------------- fp32 path
+
+template <typename T>
+__device__ inline typename Tr<T>::frag load_masked(const T* p, int nvalid) {
+  typename Tr<T>::frag f = Tr<T>::load(p);
+#pragma unroll
+  for (int e = 0; e < Tr<T>::PER; ++e)
+    if (e >= nvalid) f[e] = (T)0.f;
+  return f;
+}
+
+template <int RB>
+__global__ __launch_bounds__(kThreads) void grad_reg_kernel(GradArgs a) {
+  using F = f32x4;
+  constexpr int PER = 4, KB = 16;
+  constexpr int NKB = 4;                      // K-blocks per stage
+  constexpr int RPS = NKB * KB;               // contraction indices per stage (64)
+  constexpr int NI = RPS / PER;               // row groups of 4 (16)
+  constexpr int NJ = kColBlk / PER;           // 16-byte column pieces (32)
+  constexpr int NBLK = NI * NJ / kThreads;    // 4 x 4 blocks per thread (2)
+  constexpr int TI = NI / 8;
+  constexpr int SLD = RPS + PER;              // LDS stride of a transposed column
+  __shared__ __attribute__((aligned(16))) float Sl[kColBlk * SLD];
+  __shared__ int idx[kSplitRows];
+  __shared__ GradTable tb;
+  build_grad_table(a, tb, idx);
+  const int total = tb.istart[a.keys.n_keys];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int c16 = lane & 15, g = lane >> 4;
+  int bi[NBLK], bj[NBLK];
+#pragma unroll
+  for (int x = 0; x < NBLK; ++x) {
+    const int tile = wave + 4 * x;
+    bi[x] = (tile % TI) * 8 + (lane & 7);
+    bj[x] = (tile / TI) * 8 + (lane >> 3);
+  }
+
+  for (int item = blockIdx.x; item < total; item += gridDim.x) {
+    const Item it = decode_item(a, tb, item);
+    const int q = it.q;
+    const int r_q = a.keys.rank[q], roff = a.keys.roff[q];
+    const int nrb = (r_q + 15) >> 4;
+    const float* L = static_cast<const float*>(it.isB ? a.dy : a.x);
+    const int ldl = it.isB ? a.d_out : a.d_in;
+    const int ncol = ldl;
+    const float* S = static_cast<const float*>(it.isB ? a.Hw : a.dHt);
+    const int col0 = it.cb * kColBlk;
+    const long scol0 = (long)it.kbase - (it.isB ? tb.pseg[q] : tb.seg[q]) + it.k0;
+    const long hmax = a.ldh - PER;
+    const int nst = (it.nk + RPS - 1) / RPS;
+
+    __syncthreads();
+    load_chunk_rows(a, it, idx);
+    __syncthreads();
+
+    f32x4 acc[2][RB];
+#pragma unroll
+    for (int cbi = 0; cbi < 2; ++cbi)
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) acc[cbi][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    F v[NBLK][PER];
+    auto load_stage = [&](int st) {
+#pragma unroll
+      for (int x = 0; x < NBLK; ++x) {
+        const int cc = min(col0 + PER * bj[x], ncol - PER);
+#pragma unroll
+        for (int r = 0; r < PER; ++r) {
+          const int row = idx[min(st * RPS + PER * bi[x] + r, it.nk - 1)];
+          v[x][r] = *reinterpret_cast<const F*>(L + (size_t)row * ldl + cc);
+        }
+      }
+    };
+    auto write_stage = [&](int st) {
+#pragma unroll
+      for (int x = 0; x < NBLK; ++x) {
+        const bool cok = col0 + PER * bj[x] < ncol;
+#pragma unroll
+        for (int e = 0; e < PER; ++e) {
+          F o;
+#pragma unroll
+          for (int r = 0; r < PER; ++r) {
+            const bool ok = cok && st * RPS + PER * bi[x] + r < it.nk;
+            o[r] = ok ? v[x][r][e] : 0.f;
+          }
+          *reinterpret_cast<F*>(&Sl[(PER * bj[x] + e) * SLD + PER * bi[x]]) = o;
+        }
+      }
+    };
+    if (nst > 0) load_stage(0);
+    for (int st = 0; st < nst; ++st) {
+      write_stage(st);
+      __syncthreads();
+      if (st + 1 < nst) load_stage(st + 1);
+#pragma unroll
+      for (int kb = 0; kb < NKB; ++kb) {
+        const int ul = st * RPS + kb * KB;
+        if (ul >= it.nk) break;
+        const int nv = it.nk - (ul + PER * g);
+        const long hc = min(scol0 + ul + PER * g, hmax);
+        F tf[RB];
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          if (rb < nrb) {
+            const int rr = min(16 * rb + c16, r_q - 1);
+            tf[rb] = load_masked<float>(S + (size_t)(roff + rr) * a.ldh + hc, nv);
+          }
+        }
+#pragma unroll
+        for (int cbi = 0; cbi < 2; ++cbi) {
+          const F sf = *reinterpret_cast<const F*>(&Sl[(32 * wave + 16 * cbi + c16) * SLD + kb * KB + PER * g]);
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) {
+            if (rb < nrb) {
+              if (it.isB) acc[cbi][rb] = Tr<float>::mma(sf, tf[rb], acc[cbi][rb]);
+              else acc[cbi][rb] = Tr<float>::mma(tf[rb], sf, acc[cbi][rb]);
+            }
+          }
+        }
+      }
+      __syncthreads();
+    }
+    finish_item<RB>(a, it, item, acc);
+  }
+}
+
+// One block per (key, dB|dA column block): sums the chunk partials in order.
 template <int RB>
 __global__ __launch_bounds__(kThreads) void grad_reduce_kernel(GradArgs a) {
-  __shared__ int seg[kMaxKeys + 1];
-  __shared__ int istart[kMaxKeys + 1];
+  __shared__ GradTable tb;
   __shared__ int scan[kThreads];
-  const int n_keys = a.keys.n_keys;
+  build_grad_table(a, tb, scan);
   const int nb = a.nbB + a.nbA;
-  build_item_table(a.offsets, n_keys, nb, seg, istart, scan);
   const int q = blockIdx.x / nb, rem = blockIdx.x % nb;
-  const int ns = max(1, (seg[q + 1] - seg[q] + kSplitRows - 1) / kSplitRows);
-  if (ns == 1) return;  // written directly by grad_w_kernel
   const bool isB = rem < a.nbB;
   const int cb = isB ? rem : rem - a.nbB;
+  const int nsB = n_split(tb.pseg[q + 1] - tb.pseg[q]);
+  const int ns = isB ? nsB : n_split(tb.seg[q + 1] - tb.seg[q]);
+  if (ns == 1) return;  // written directly by the gradient kernel
+  const int first = tb.istart[q] + (isB ? cb : nsB * a.nbB + cb);
+  const int step = isB ? a.nbB : a.nbA;
   const int nrb = (a.keys.rank[q] + 15) >> 4;
   const f32x4* part = reinterpret_cast<const f32x4*>(a.part);
   constexpr int PER_ITEM = 4 * 2 * RB * 64;
@@ -416,7 +517,7 @@ __global__ __launch_bounds__(kThreads) void grad_reduce_kernel(GradArgs a) {
     const int wc = (e >> 6) / RB;  // wave * 2 + cbi
     if (rb >= nrb) continue;
     f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int c = 0; c < ns; ++c) s += part[(size_t)(istart[q] + c * nb + rem) * PER_ITEM + e];
+    for (int c = 0; c < ns; ++c) s += part[(size_t)(first + c * step) * PER_ITEM + e];
     store_grad(a, isB, q, cb * kColBlk, wc >> 1, wc & 1, rb, lane, s);
   }
 }
@@ -538,15 +639,15 @@ __global__ __launch_bounds__(kThreads) void dx_gemm_kernel(DxArgs a) {
   }
 }
 
-template <typename T, int RB>
-hipError_t launch_grads_rb(const GradArgs& g, long P, hipStream_t stream) {
+template <int RB>
+hipError_t launch_grads_rb(int dtype, const GradArgs& g, long P, hipStream_t stream) {
   const int nb = g.nbB + g.nbA;
   const long items = ((P + kSplitRows - 1) / kSplitRows + g.keys.n_keys) * nb;
   const long cap = 8L * device_cu_count();
   const int grid = (int)(items < cap ? items : cap);
   if (grid > 0) {
-    if (g.multi) grad_w_kernel<T, RB, true><<<grid, kThreads, 0, stream>>>(g);
-    else grad_w_kernel<T, RB, false><<<grid, kThreads, 0, stream>>>(g);
+    if (dtype == ACE_BF16) grad_dma_kernel<RB><<<grid, kThreads, 0, stream>>>(g);
+    else grad_reg_kernel<RB><<<grid, kThreads, 0, stream>>>(g);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -567,16 +668,10 @@ hipError_t launch_grads(int dtype, GradArgs g, int r_max, long P, hipStream_t st
   g.nbB = (g.d_out + kColBlk - 1) / kColBlk;
   g.nbA = (g.d_in + kColBlk - 1) / kColBlk;
   const int rb = rank_blocks(r_max);
-  if (dtype == ACE_BF16) {
-    if (rb == 2) return launch_grads_rb<__bf16, 2>(g, P, stream);
-    if (rb == 4) return launch_grads_rb<__bf16, 4>(g, P, stream);
-    if (rb == 8) return launch_grads_rb<__bf16, 8>(g, P, stream);
-    return launch_grads_rb<__bf16, 16>(g, P, stream);
-  }
-  if (rb == 2) return launch_grads_rb<float, 2>(g, P, stream);
-  if (rb == 4) return launch_grads_rb<float, 4>(g, P, stream);
-  if (rb == 8) return launch_grads_rb<float, 8>(g, P, stream);
-  return launch_grads_rb<float, 16>(g, P, stream);
+  if (rb == 2) return launch_grads_rb<2>(dtype, g, P, stream);
+  if (rb == 4) return launch_grads_rb<4>(dtype, g, P, stream);
+  if (rb == 8) return launch_grads_rb<8>(dtype, g, P, stream);
+  return launch_grads_rb<16>(dtype, g, P, stream);
 }
 
 hipError_t launch_dx_gemm(int dtype, const DxArgs& d, hipStream_t stream) {

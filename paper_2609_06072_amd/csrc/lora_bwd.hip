@@ -8,17 +8,21 @@
 //   dx    += sum over the rows that read x of A_q^T dH_u
 //
 // Launches, all deterministic (each output is reduced in a fixed order):
+//   pairs     -- rows serving several slots only: the position of each row's
+//                first pair in pair order and the pair at each position (two
+//                small launches: per-tile counts, then positions).
 //   prep      -- A^T and B_q^T into the workspace (so every MFMA operand is
 //                contiguous along its contraction index); zeroes the dense
 //                per-token dH buffer used for dx.
-//   contract  -- Hs per row (x against A), stored per key as [r][u].
+//   contract  -- Hs per row (x against A), stored per key and per pair served
+//                as [r][pair position], times the pair's weight (Hw).
 //   contract  -- dH per row (gathered G against B^T), stored per key as
 //                [r][u] and either as dense per-token rows (shared input) or
 //                row-major for the expand below (per-pair input).
 //   expand    -- per-pair input only: dx[t*k+j] += A_q^T dH_u (each row owns
 //                its input row).
-//   grads     -- dB_q and dA_q, reduced over each key's rows (split into
-//                chunks of rows for skewed keys, partials summed in order).
+//   grads     -- dB_q over each key's pairs and dA_q over its rows (split into
+//                chunks for skewed keys, partials summed in order).
 //   dx GEMM   -- shared input only: dx += dHdense A over K = R (token-major).
 #include "ace_device.hpp"
 #include "ace_internal.hpp"
@@ -33,8 +37,10 @@ constexpr int kMaxJobs = kMaxKeys + 2;
 size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 
 struct WsLayout {
-  size_t At, Bt, Ht, dHt, dHf, dHrow, part, total;
+  size_t At, Bt, Ht, dHt, dHf, dHrow, part, ppos, plist, tsum, total;
 };
+
+constexpr int kPairTile = 1024;   // rows per tile of the pair-position launches
 
 // Workspace regions for element size es: At [d_in][R], Bt [R][d_out],
 // Ht/dHt [R][ldh] (column = row index inside the key's segment), dense dH
@@ -55,8 +61,148 @@ WsLayout ws_layout(int T, int k, int d_in, int d_out, int n_keys, int R, int r_m
   w.dHf = o;   o += align256(es * P * R);
   w.dHrow = o; o += align256(es * P * rpad);
   w.part = o;  o += align256(grads_part_bytes(T, k, d_in, d_out, n_keys, r_max));
+  w.ppos = o;  o += align256(4 * (P + 1));
+  w.plist = o; o += align256(4 * P);
+  w.tsum = o;  o += align256(4 * ((P + kPairTile - 1) / kPairTile));
   w.total = o + 256;
   return w;
+}
+
+// ----------------------------------------------------------------- pairs
+
+// Sum of the slot counts of each tile of kPairTile rows.
+__global__ __launch_bounds__(kThreads) void pair_count_kernel(const int32_t* offsets, int n_keys,
+                                                              const uint32_t* row_slots,
+                                                              int32_t* tsum) {
+  __shared__ int red[kThreads];
+  const int U = offsets[n_keys];
+  const int u0 = blockIdx.x * kPairTile;
+  int c = 0;
+#pragma unroll
+  for (int i = 0; i < kPairTile / kThreads; ++i) {
+    const int u = u0 + threadIdx.x + i * kThreads;
+    const uint32_t sl = row_slots[min(u, max(U - 1, 0))];
+    c += u < U ? __builtin_popcount(sl) : 0;
+  }
+  int total;
+  block_exclusive_scan(c, red, &total);
+  if (threadIdx.x == 0) tsum[blockIdx.x] = total;
+}
+
+// ppos[u] = number of pairs served by rows before u (u <= U); plist[ppos[u] +
+// i] = t*k + (i-th slot of row u).  Pairs are thus ordered by key, token, slot.
+__global__ __launch_bounds__(kThreads) void pair_write_kernel(const int32_t* offsets, int n_keys,
+                                                              const int32_t* row_token,
+                                                              const uint32_t* row_slots, int k,
+                                                              const int32_t* tsum, int32_t* ppos,
+                                                              int32_t* plist) {
+  __shared__ int red[kThreads];
+  const int U = offsets[n_keys];
+  const int u0 = blockIdx.x * kPairTile;
+  if (u0 > U) return;
+  int before = 0;
+  for (int b = threadIdx.x; b < (int)blockIdx.x; b += kThreads) before += tsum[b];
+  int base;
+  block_exclusive_scan(before, red, &base);   // base = sum over the earlier tiles
+  constexpr int RPT = kPairTile / kThreads;   // consecutive rows per thread
+  const int ub = u0 + RPT * threadIdx.x;
+  uint32_t sl[RPT];
+  int tok[RPT];
+  int c = 0;
+#pragma unroll
+  for (int i = 0; i < RPT; ++i) {
+    const int u = min(ub + i, max(U - 1, 0));
+    sl[i] = row_slots[u];
+    tok[i] = row_token[u];
+  }
+#pragma unroll
+  for (int i = 0; i < RPT; ++i) {
+    if (ub + i >= U) sl[i] = 0u;
+    c += __builtin_popcount(sl[i]);
+  }
+  int total;
+  int pos = base + block_exclusive_scan(c, red, &total);
+#pragma unroll
+  for (int i = 0; i < RPT; ++i) {
+    const int u = ub + i;
+    if (u < U) ppos[u] = pos;
+    for (uint32_t mm = sl[i]; mm; mm &= mm - 1u) plist[pos++] = tok[i] * k + __builtin_ctz(mm);
+    if (u == U - 1) ppos[U] = pos;
+  }
+  if (U == 0 && blockIdx.x == 0 && threadIdx.x == 0) ppos[0] = 0;
+}
+
+// dH of a row serving several pairs: dH_u = sum_i w_{p_i} dHp[ppos[u] + i]
+// (dHp = s B^T dY per pair position, row-major [P][rpad]); written per key as
+// [r][u - offsets[q]] for the weight gradient and as dense per-token rows for
+// the dx GEMM.  One thread per row.
+struct CombineArgs {
+  const int32_t* offsets;
+  const int32_t* row_token;
+  const int32_t* ppos;
+  const int32_t* plist;
+  const float* pair_w;
+  const void* dHp;
+  int32_t rpad;
+  void* dHt;
+  long ldh;
+  void* dHf;
+  KeyTable keys;
+};
+
+// A block takes 64 consecutive rows; lane l of wave w handles row 64b + l and
+// the rank chunks w, w + 4, ... (PER ranks each), so the transposed stores of
+// a wave cover 64 consecutive columns.  The first two pairs of a row are
+// loaded unconditionally (a missing second pair gets weight 0); further pairs
+// (rare) are added in a loop.
+template <typename T>
+__global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
+  constexpr int PER = Tr<T>::PER;
+  __shared__ int seg[kMaxKeys + 1];
+  const int n_keys = a.keys.n_keys;
+  for (int i = threadIdx.x; i <= n_keys; i += kThreads) seg[i] = a.offsets[i];
+  __syncthreads();
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int U = seg[n_keys];
+  const int u = blockIdx.x * 64 + lane;
+  if (u >= U) return;
+  const int q = upper_index(seg, n_keys, u);
+  const int r_q = a.keys.rank[q], roff = a.keys.roff[q], R = a.keys.R;
+  const long col = u - seg[q];
+  const int tok = a.row_token[u];
+  const int p0 = a.ppos[u], p1 = a.ppos[u + 1];
+  const int pb = min(p0 + 1, p1 - 1);
+  float w0 = 1.f, w1 = p1 - p0 > 1 ? 1.f : 0.f;
+  if (a.pair_w) {
+    const float x0 = a.pair_w[a.plist[p0]], x1 = a.pair_w[a.plist[pb]];
+    w0 = x0;
+    w1 = p1 - p0 > 1 ? x1 : 0.f;
+  }
+  const T* src = static_cast<const T*>(a.dHp);
+  T* dt = static_cast<T*>(a.dHt);
+  T* df = static_cast<T*>(a.dHf) + (size_t)tok * R + roff;
+  for (int r0 = PER * wave; r0 < r_q; r0 += 4 * PER) {
+    float f0[PER], f1[PER];
+    Tr<T>::to_f32(Tr<T>::load(src + (size_t)p0 * a.rpad + r0), f0);
+    Tr<T>::to_f32(Tr<T>::load(src + (size_t)pb * a.rpad + r0), f1);
+    float acc[PER];
+#pragma unroll
+    for (int e = 0; e < PER; ++e) acc[e] = w0 * f0[e] + w1 * f1[e];
+    for (int pos = p0 + 2; pos < p1; ++pos) {
+      const float w = a.pair_w ? a.pair_w[a.plist[pos]] : 1.f;
+      float f[PER];
+      Tr<T>::to_f32(Tr<T>::load(src + (size_t)pos * a.rpad + r0), f);
+#pragma unroll
+      for (int e = 0; e < PER; ++e) acc[e] += w * f[e];
+    }
+#pragma unroll
+    for (int e = 0; e < PER; ++e)
+      if (r0 + e < r_q) {
+        const T v = (T)acc[e];
+        dt[(size_t)(roff + r0 + e) * a.ldh + col] = v;
+        df[r0 + e] = v;
+      }
+  }
 }
 
 // ------------------------------------------------------------------ prep
@@ -107,16 +253,53 @@ __global__ __launch_bounds__(kThreads) void bwd_prep_kernel(PrepArgs a) {
     dst = static_cast<T*>(a.Bt) + (size_t)roff * a.d_out;        // Bt rows roff.. [r_q][d_out]
     rows = a.d_out; cols = r_q; lds = r_q; ldd = a.d_out;
   }
+  using F = typename Tr<T>::frag;
+  constexpr int PER = Tr<T>::PER;
+  constexpr int PPR = kTile / PER;            // 16-byte pieces per tile row
+  constexpr int NP = kTile * PPR / kThreads;  // pieces per thread
   const int ct = a.job_cols_tiles[job];
   const int r0 = (tb / ct) * kTile, c0 = (tb % ct) * kTile;
-  for (int i = threadIdx.x; i < kTile * kTile; i += kThreads) {
-    const int rr = i / kTile, cc = i % kTile;
-    if (r0 + rr < rows && c0 + cc < cols) tile[rr][cc] = src[(size_t)(r0 + rr) * lds + c0 + cc];
+  // 16-byte pieces when rows are aligned; then a piece is either wholly
+  // inside the matrix or wholly outside (cols and rows are multiples of PER)
+  const bool vs = (lds % PER) == 0 && (cols % PER) == 0;
+  const bool vd = (ldd % PER) == 0 && (rows % PER) == 0;
+  if (vs) {
+    F v[NP];
+#pragma unroll
+    for (int i = 0; i < NP; ++i) {
+      const int pc = threadIdx.x + i * kThreads;
+      const int rr = pc / PPR, cc = (pc % PPR) * PER;
+      v[i] = Tr<T>::load(src + (size_t)min(r0 + rr, rows - 1) * lds + min(c0 + cc, cols - PER));
+    }
+#pragma unroll
+    for (int i = 0; i < NP; ++i) {
+      const int pc = threadIdx.x + i * kThreads;
+      const int rr = pc / PPR, cc = (pc % PPR) * PER;
+#pragma unroll
+      for (int e = 0; e < PER; ++e) tile[rr][cc + e] = v[i][e];
+    }
+  } else {
+    for (int i = threadIdx.x; i < kTile * kTile; i += kThreads) {
+      const int rr = i / kTile, cc = i % kTile;
+      if (r0 + rr < rows && c0 + cc < cols) tile[rr][cc] = src[(size_t)(r0 + rr) * lds + c0 + cc];
+    }
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < kTile * kTile; i += kThreads) {
-    const int cc = i / kTile, rr = i % kTile;
-    if (r0 + rr < rows && c0 + cc < cols) dst[(size_t)(c0 + cc) * ldd + r0 + rr] = tile[rr][cc];
+  if (vd) {
+#pragma unroll
+    for (int i = 0; i < NP; ++i) {
+      const int pc = threadIdx.x + i * kThreads;
+      const int cc = pc / PPR, rr = (pc % PPR) * PER;
+      F o;
+#pragma unroll
+      for (int e = 0; e < PER; ++e) o[e] = tile[rr + e][cc];
+      if (c0 + cc < cols && r0 + rr < rows) Tr<T>::store(dst + (size_t)(c0 + cc) * ldd + r0 + rr, o);
+    }
+  } else {
+    for (int i = threadIdx.x; i < kTile * kTile; i += kThreads) {
+      const int cc = i / kTile, rr = i % kTile;
+      if (r0 + rr < rows && c0 + cc < cols) dst[(size_t)(c0 + cc) * ldd + r0 + rr] = tile[rr][cc];
+    }
   }
 }
 
@@ -174,26 +357,72 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
   c.ldh = ldh;
   c.kslots = kslots;
   c.keys = p.keys;
-  // Hs = s A x, per key [r][u]
+  // pair positions (rows that serve several slots)
+  const bool multi = p.rt->mode == ACE_ROWS_GROUP_DEDUP;
+  int32_t* ppos = multi ? reinterpret_cast<int32_t*>(base + L.ppos) : nullptr;
+  int32_t* plist = multi ? reinterpret_cast<int32_t*>(base + L.plist) : nullptr;
+  if (multi && P > 0) {
+    const int tiles = (int)((P + kPairTile - 1) / kPairTile);
+    int32_t* tsum = reinterpret_cast<int32_t*>(base + L.tsum);
+    pair_count_kernel<<<tiles, kThreads, 0, stream>>>(p.rt->offsets, n_keys, p.rt->row_slots, tsum);
+    pair_write_kernel<<<tiles, kThreads, 0, stream>>>(p.rt->offsets, n_keys, p.rt->row_token,
+                                                      p.rt->row_slots, p.k, tsum, ppos, plist);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  // Hw = w s A x, per key and pair [r][pair position]
   c.src = p.x;
   c.W = p.A;
   c.ldw = p.d_in;
   c.K = p.d_in;
   c.src_mode = p.per_pair ? kSrcPerPair : kSrcShared;
+  c.pair_w = p.pair_w;
   c.out_t = base + L.Ht;
+  c.out_t_pairs = 1;
+  c.ppos = ppos;
   e = launch_contract(p.dtype, c, p.r_max, P, stream);
   if (e != hipSuccess) return e;
   // dH = s B^T G
-  c.src = dy;
   c.W = base + L.Bt;
   c.ldw = p.d_out;
   c.K = p.d_out;
-  c.src_mode = kSrcGather;
-  c.pair_w = p.pair_w;
-  c.out_t = base + L.dHt;
-  c.out_dense = p.per_pair ? nullptr : base + L.dHf;
-  c.out_row = p.per_pair ? base + L.dHrow : nullptr;
-  e = launch_contract(p.dtype, c, p.r_max, P, stream);
+  c.src = dy;
+  c.out_t_pairs = 0;
+  c.ppos = nullptr;
+  if (multi) {
+    // per pair position (single dY rows), then summed per row
+    c.src_mode = kSrcPairList;
+    c.plist = plist;
+    c.ppos = ppos;
+    c.out_w = 0;
+    c.out_t = nullptr;
+    c.out_dense = nullptr;
+    c.out_row = base + L.dHrow;
+    e = launch_contract(p.dtype, c, p.r_max, P, stream);
+    if (e != hipSuccess) return e;
+    CombineArgs cb{};
+    cb.offsets = p.rt->offsets;
+    cb.row_token = p.rt->row_token;
+    cb.ppos = ppos;
+    cb.plist = plist;
+    cb.pair_w = p.pair_w;
+    cb.dHp = base + L.dHrow;
+    cb.rpad = rpad;
+    cb.dHt = base + L.dHt;
+    cb.ldh = ldh;
+    cb.dHf = base + L.dHf;
+    cb.keys = p.keys;
+    const int blocks = (int)((P + 63) / 64);
+    if (blocks > 0) combine_kernel<T><<<blocks, kThreads, 0, stream>>>(cb);
+    e = hipGetLastError();
+  } else {
+    c.src_mode = kSrcPerPair;
+    c.out_w = 1;
+    c.out_t = base + L.dHt;
+    c.out_dense = p.per_pair ? nullptr : base + L.dHf;
+    c.out_row = p.per_pair ? base + L.dHrow : nullptr;
+    e = launch_contract(p.dtype, c, p.r_max, P, stream);
+  }
   if (e != hipSuccess) return e;
   if (p.per_pair) {
     ExpandArgs x{};
@@ -217,9 +446,10 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
   GradArgs gr{};
   gr.x = p.x;
   gr.dy = dy;
-  gr.pair_w = p.pair_w;
-  gr.Ht = base + L.Ht;
+  gr.Hw = base + L.Ht;
   gr.dHt = base + L.dHt;
+  gr.ppos = ppos;
+  gr.plist = plist;
   gr.ldh = ldh;
   gr.dA = dA;
   gr.dB = dB;
@@ -231,7 +461,6 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
   gr.d_in = p.d_in;
   gr.d_out = p.d_out;
   gr.per_pair = p.per_pair;
-  gr.multi = p.rt->mode == ACE_ROWS_GROUP_DEDUP;
   gr.keys = p.keys;
   e = launch_grads(p.dtype, gr, p.r_max, P, stream);
   if (e != hipSuccess || p.per_pair) return e;
