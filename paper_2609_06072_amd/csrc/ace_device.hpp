@@ -205,4 +205,28 @@ __device__ inline int upper_index(const int* arr, int n, int x) {
   return lo;
 }
 
+// ---- direct global -> LDS copies (gfx950 global_load_lds_dwordx4)
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+__device__ inline uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const lds_void*)p;
+}
+
+// 16-byte copy global -> LDS: lane l's bytes land at lds_base + 16 * l
+// (lds_base wave-uniform).  Issued as inline assembly so that the compiler does
+// not treat every later LDS read as dependent on it; completion is awaited
+// explicitly with wait_vmcnt before the barrier that publishes the data.
+__device__ inline void dma16(const void* g, uint32_t lds_base) {
+  asm volatile("global_load_lds_dwordx4 %1, off" ::"{m0}"(lds_base), "v"(g) : "memory");
+}
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
+// vmcnt bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8).
+template <int N>
+__device__ inline void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
 }  // namespace ace

@@ -17,12 +17,89 @@
 //   row-major  [U][rpad]      operand of the expand kernel (zero beyond r_q)
 //   per key    [R][ldh]       column u - offsets[q]: operand of the column pass
 //   dense      [T*kslots][R]  per-token rows: operand of the dense dx GEMM
+#include <type_traits>
+
 #include "ace_device.hpp"
 #include "ace_internal.hpp"
 
 namespace ace {
 
 namespace {
+
+// Writes row u's result h (scaled, zero past r_q) to the requested outputs.
+template <typename T, int RB>
+__device__ inline void contract_store(const ContractArgs& a, int q, int lo, int u, f32x4 (&h)[RB]) {
+  constexpr int KB = Tr<T>::KB, APF = Tr<T>::APF;
+  const int k = a.k, R = a.keys.R;
+  const int r_q = a.keys.rank[q], roff = a.keys.roff[q];
+  const int nrb = ((r_q + KB - 1) / KB) * APF;
+  const int g = (threadIdx.x & 63) >> 4;
+  int tok = 0;
+  uint32_t slots = 1u;
+  if (a.src_mode != kSrcPairList) {
+    tok = a.row_token[u];
+    slots = a.row_slots[u];
+  }
+  if (a.out_w && a.pair_w) {  // single-pair rows: times the pair's weight
+    const float w = a.pair_w[tok * k + (__builtin_ctz(slots | 0x80000000u) & 31)];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) h[rb] *= w;
+  }
+  if (a.out_row) {
+    T* dst = static_cast<T*>(a.out_row) + (size_t)u * a.rpad;
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const int r0 = rank_of_row<T>(rb, 4 * g);  // 4 consecutive ranks
+      if (r0 < a.rpad) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) dst[r0 + v] = (T)h[rb][v];
+      }
+    }
+  }
+  if (a.out_t && !a.out_t_pairs) {
+    T* dst = static_cast<T*>(a.out_t);
+    const long col = u - lo;
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+      if (rb < nrb) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int r = rank_of_row<T>(rb, 4 * g + v);
+          if (r < r_q) dst[(size_t)(roff + r) * a.ldh + col] = (T)h[rb][v];
+        }
+      }
+  }
+  if (a.out_t && a.out_t_pairs) {  // one column per pair served, times its weight
+    T* dst = static_cast<T*>(a.out_t);
+    long col = a.ppos ? (long)a.ppos[u] - a.ppos[lo] : (long)(u - lo);
+    for (uint32_t mm = slots; mm; mm &= mm - 1u, ++col) {
+      const float w = a.pair_w ? a.pair_w[tok * k + __builtin_ctz(mm)] : 1.f;
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+        if (rb < nrb) {
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int r = rank_of_row<T>(rb, 4 * g + v);
+            if (r < r_q) dst[(size_t)(roff + r) * a.ldh + col] = (T)(h[rb][v] * w);
+          }
+        }
+    }
+  }
+  if (a.out_dense) {
+    const int j0 = __builtin_ctz(slots | 0x80000000u) & 31;
+    const size_t drow = (size_t)tok * a.kslots + (a.kslots > 1 ? j0 : 0);
+    T* dst = static_cast<T*>(a.out_dense) + drow * R + roff;
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+      if (rb < nrb) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int r = rank_of_row<T>(rb, 4 * g + v);
+          if (r < r_q) dst[r] = (T)h[rb][v];
+        }
+      }
+  }
+}
 
 template <int RB>
 struct CGeo {
@@ -51,7 +128,7 @@ __global__ __launch_bounds__(kThreads) void contract_kernel(ContractArgs a) {
   const int c16 = lane & 15, g = lane >> 4;
   const T* S = static_cast<const T*>(a.src);
   const T* W = static_cast<const T*>(a.W);
-  const int K = a.K, k = a.k, R = a.keys.R;
+  const int K = a.K, k = a.k;
   const int nks = (K + KB - 1) / KB, nks_full = K / KB;
 
   for (int idx = blockIdx.x / kXcds; idx < total; idx += stride) {
@@ -181,71 +258,173 @@ __global__ __launch_bounds__(kThreads) void contract_kernel(ContractArgs a) {
         if (rank_of_row<T>(rb, 4 * g + v) >= r_q) h[rb][v] = 0.f;
     }
     if (!valid) continue;
-    int tok = 0;
-    uint32_t slots = 1u;
-    if (a.src_mode != kSrcPairList) {
-      tok = a.row_token[u];
-      slots = a.row_slots[u];
+    contract_store<T, RB>(a, q, lo, u, h);
+  }
+}
+
+// ------------------------------------------------------------- bf16 path
+//
+// A block takes a tile of 64 rows of one key; wave w owns rows 16w .. 16w+15
+// for every rank over the whole contraction, so no cross-wave reduction is
+// needed.  Stages of KC contraction indices of the 64 source rows and of the
+// key's weight rows are copied global -> LDS (global_load_lds_dwordx4, row
+// pieces with 16-byte chunks XOR-swizzled by row), NBUF stages in flight;
+// MFMA fragments are plain 16-byte LDS reads.  Only the weight rows below r_q
+// (rounded up to a copy) are copied.
+template <int RB>
+struct CDma {
+  static constexpr int KC = 64;                  // contraction indices per stage
+  static constexpr int NBUF = 3;                 // at most 4 (see the waits)
+  static constexpr int CPR = KC / 8;             // 16-byte chunks per row piece
+  static constexpr int RPI = 64 / CPR;           // row pieces per copy instruction
+  static constexpr int SBYTES = 64 * KC * 2;     // 64 source rows x KC bf16
+  static constexpr int WROWS = 16 * RB;
+  static constexpr int WBYTES = WROWS * KC * 2;  // weight rows x KC bf16
+  static constexpr int NS = 16 / RPI;            // source copies per wave per stage
+  static constexpr int NW = WROWS / RPI / 4;     // weight copies per wave per stage (at most)
+  static constexpr int LDS = NBUF * (SBYTES + WBYTES);
+  // LDS per CU is 160 KiB; the tile tables take about 4 KiB more per block
+  static constexpr int BLOCKS_PER_CU = (160 * 1024) / (LDS + 4 * 1024 + 512) < 1 ? 1 : (160 * 1024) / (LDS + 4 * 1024 + 512);
+};
+
+// s_waitcnt vmcnt(n) for a wave-uniform 0 <= n <= N
+template <int N>
+__device__ inline void wait_vmcnt_upto(int n) {
+  if constexpr (N > 0) {
+    if (n >= N) {
+      wait_vmcnt<N>();
+      return;
     }
-    if (a.out_w && a.pair_w) {  // single-pair rows: times the pair's weight
-      const float w = a.pair_w[tok * k + (__builtin_ctz(slots | 0x80000000u) & 31)];
+    wait_vmcnt_upto<N - 1>(n);
+  } else {
+    (void)n;
+    wait_vmcnt<0>();
+  }
+}
+
+template <int RB>
+__global__ __launch_bounds__(kThreads) void contract_dma_kernel(ContractArgs a) {
+  using G = CDma<RB>;
+  constexpr int KC = G::KC, NBUF = G::NBUF, KB = Tr<__bf16>::KB;
+  constexpr int CPR = G::CPR, RPI = G::RPI;
+  __shared__ __attribute__((aligned(16))) char Sb[NBUF][G::SBYTES];
+  __shared__ __attribute__((aligned(16))) char Wb[NBUF][G::WBYTES];
+  __shared__ int seg[kMaxKeys + 1];
+  __shared__ int bstart[kMaxKeys + 1];
+  __shared__ int bfirst[kMaxKeys];
+  __shared__ int scan[kThreads];
+  const int n_keys = a.keys.n_keys;
+  const int bucket = blockIdx.x % kXcds;
+  build_bucket_table(a.offsets, a.src_mode == kSrcPairList ? a.ppos : nullptr, n_keys, 64, bucket,
+                     seg, bstart, bfirst, scan);
+  const int total = bstart[n_keys];
+  const int stride = gridDim.x / kXcds;  // the grid is a multiple of kXcds
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int c16 = lane & 15, g = lane >> 4;
+  const __bf16* S = static_cast<const __bf16*>(a.src);
+  const __bf16* W = static_cast<const __bf16*>(a.W);
+  const int K = a.K, k = a.k;
+  const int nst = (K + KC - 1) / KC;
+  const int cpos = lane & (CPR - 1), crow = lane / CPR;   // 16-byte position / row inside a copy
+
+  for (int idx = blockIdx.x / kXcds; idx < total; idx += stride) {
+    const int q = upper_index(bstart, n_keys, idx);
+    const int lo = seg[q];
+    const int u0 = lo + (bfirst[q] + idx - bstart[q]) * 64;
+    const int u_end = seg[q + 1];
+    const int r_q = a.keys.rank[q], roff = a.keys.roff[q];
+    // weight copies this wave issues per stage (rows below r_q only)
+    const int wcopies = (r_q + RPI - 1) / RPI;
+    const int nw = min(G::NW, max(0, wcopies - wave * G::NW));
+
+    // source rows this lane copies (rows past the segment re-read the last
+    // one) and the chunk of the row piece it copies
+    const __bf16* sptr[G::NS];
+    int scol[G::NS];
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb) h[rb] *= w;
+    for (int i = 0; i < G::NS; ++i) {
+      const int uc = min(u0 + 16 * wave + RPI * i + crow, u_end - 1);
+      int sr;
+      if (a.src_mode == kSrcPairList) {
+        sr = a.plist[uc];
+      } else {
+        const int tok = a.row_token[uc];
+        sr = a.src_mode == kSrcPerPair ? tok * k + (__builtin_ctz(a.row_slots[uc] | 0x80000000u) & 31) : tok;
+      }
+      sptr[i] = S + (size_t)sr * K;
+      scol[i] = 8 * (cpos ^ ((16 * wave + RPI * i + crow) & (CPR - 1)));
     }
-    if (a.out_row) {
-      T* dst = static_cast<T*>(a.out_row) + (size_t)u * a.rpad;
+    const __bf16* wptr[G::NW];
+    int wcol[G::NW];
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        const int r0 = rank_of_row<T>(rb, 4 * g);  // 4 consecutive ranks
-        if (r0 < a.rpad) {
+    for (int i = 0; i < G::NW; ++i) {
+      const int rl = RPI * (wave * G::NW + i) + crow;  // weight row of the tile (rank)
+      wptr[i] = W + (size_t)(roff + min(rl, r_q - 1)) * a.ldw;
+      wcol[i] = 8 * (cpos ^ (rl & (CPR - 1)));
+    }
+    // copies of stage st (columns past K are clamped; masked at the reads)
+    auto issue = [&](int st) {
+      const int b = st % NBUF;
+      const int k0 = st * KC;
 #pragma unroll
-          for (int v = 0; v < 4; ++v) dst[r0 + v] = (T)h[rb][v];
+      for (int i = 0; i < G::NS; ++i)
+        dma16(sptr[i] + min(k0 + scol[i], K - 8),
+              __builtin_amdgcn_readfirstlane(lds_addr(&Sb[b][(16 * wave + RPI * i) * KC * 2])));
+#pragma unroll
+      for (int i = 0; i < G::NW; ++i)
+        if (i < nw)
+          dma16(wptr[i] + min(k0 + wcol[i], K - 8),
+                __builtin_amdgcn_readfirstlane(lds_addr(&Wb[b][RPI * (wave * G::NW + i) * KC * 2])));
+    };
+    const int per_stage = G::NS + nw;   // copies per stage of this wave
+
+    __syncthreads();  // the previous tile is done with the buffers
+    f32x4 acc[RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) acc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int p = 0; p < NBUF - 1; ++p)
+      if (p < nst) issue(p);
+    for (int st = 0; st < nst; ++st) {
+      // this wave's copies of stage st are done once at most those of the
+      // stages issued after it are outstanding; the barrier publishes them
+      wait_vmcnt_upto<(NBUF - 2) * (G::NS + G::NW)>(min(NBUF - 2, nst - 1 - st) * per_stage);
+      __syncthreads();
+      if (st + NBUF - 1 < nst) issue(st + NBUF - 1);
+      const int b = st % NBUF;
+#pragma unroll
+      for (int kb = 0; kb < KC / KB; ++kb) {
+        const int kk = st * KC + kb * KB;
+        if (kk >= K) break;
+        const int chunk = kb * 4 + g;
+        const int rl = 16 * wave + c16;
+        bf16x8 sf = *reinterpret_cast<const bf16x8*>(&Sb[b][rl * KC * 2 + ((chunk ^ (rl & (CPR - 1))) << 4)]);
+        const int nv = K - (kk + 8 * g);
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (e >= nv) sf[e] = (__bf16)0.f;
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          // weight rows at or past r_q were not copied: their results are zeroed below
+          const int wr = rank_of_row<__bf16>(rb, c16);
+          const bf16x8 wf = *reinterpret_cast<const bf16x8*>(&Wb[b][wr * KC * 2 + ((chunk ^ (wr & (CPR - 1))) << 4)]);
+          acc[rb] = Tr<__bf16>::mma(wf, sf, acc[rb]);   // D[rank][row]
         }
       }
     }
-    if (a.out_t && !a.out_t_pairs) {
-      T* dst = static_cast<T*>(a.out_t);
-      const long col = u - lo;
+
+    const int u = u0 + 16 * wave + c16;
+    if (u0 + 16 * wave >= u_end || u >= u_end) continue;
+    const float s = a.alpha / (float)r_q;
+    f32x4 h[RB];
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
-        if (rb < nrb) {
+    for (int rb = 0; rb < RB; ++rb) {
+      h[rb] = acc[rb] * s;
 #pragma unroll
-          for (int v = 0; v < 4; ++v) {
-            const int r = rank_of_row<T>(rb, 4 * g + v);
-            if (r < r_q) dst[(size_t)(roff + r) * a.ldh + col] = (T)h[rb][v];
-          }
-        }
+      for (int v = 0; v < 4; ++v)
+        if (rank_of_row<__bf16>(rb, 4 * g + v) >= r_q) h[rb][v] = 0.f;
     }
-    if (a.out_t && a.out_t_pairs) {  // one column per pair served, times its weight
-      T* dst = static_cast<T*>(a.out_t);
-      long col = a.ppos ? (long)a.ppos[u] - a.ppos[lo] : (long)(u - lo);
-      for (uint32_t mm = slots; mm; mm &= mm - 1u, ++col) {
-        const float w = a.pair_w ? a.pair_w[tok * k + __builtin_ctz(mm)] : 1.f;
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
-          if (rb < nrb) {
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-              const int r = rank_of_row<T>(rb, 4 * g + v);
-              if (r < r_q) dst[(size_t)(roff + r) * a.ldh + col] = (T)(h[rb][v] * w);
-            }
-          }
-      }
-    }
-    if (a.out_dense) {
-      const int j0 = __builtin_ctz(slots | 0x80000000u) & 31;
-      const size_t drow = (size_t)tok * a.kslots + (a.kslots > 1 ? j0 : 0);
-      T* dst = static_cast<T*>(a.out_dense) + drow * R + roff;
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
-        if (rb < nrb) {
-#pragma unroll
-          for (int v = 0; v < 4; ++v) {
-            const int r = rank_of_row<T>(rb, 4 * g + v);
-            if (r < r_q) dst[r] = (T)h[rb][v];
-          }
-        }
-    }
+    contract_store<__bf16, RB>(a, q, lo, u, h);
   }
 }
 
@@ -254,6 +433,14 @@ hipError_t launch_contract_rb(const ContractArgs& a, long P, hipStream_t stream)
   constexpr int BM = 16 * CGeo<RB>::NRB;
   // tiles per bucket <= (all tiles) / kXcds + n_keys
   const long per_bucket = P > 0 ? ((P + BM - 1) / BM + a.keys.n_keys) / kXcds + a.keys.n_keys : 0;
+  if constexpr (std::is_same<T, __bf16>::value) {
+    // 64-row tiles
+    const long pb = P > 0 ? ((P + 63) / 64 + a.keys.n_keys) / kXcds + a.keys.n_keys : 0;
+    const long cap = (long)CDma<RB>::BLOCKS_PER_CU * device_cu_count() / kXcds;
+    const int grid = (int)(pb < cap ? pb : cap) * kXcds;
+    if (grid > 0) contract_dma_kernel<RB><<<grid, kThreads, 0, stream>>>(a);
+    return hipGetLastError();
+  }
   const long cap = 6L * device_cu_count() / kXcds;
   const int grid = (int)(per_bucket < cap ? per_bucket : cap) * kXcds;
   if (grid > 0) contract_kernel<T, RB><<<grid, kThreads, 0, stream>>>(a);

@@ -175,17 +175,8 @@ __device__ inline void finish_item(const GradArgs& a, const Item& it, int item,
 
 // ----------------------------------------------------------------- bf16 path
 
-// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
-// vmcnt bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8).
-template <int N>
-__device__ inline void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-
 typedef __attribute__((ext_vector_type(4))) short s16x4;
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
-typedef __attribute__((address_space(3))) void lds_void;
 
 template <int RB>
 struct DmaGeo {
@@ -201,18 +192,6 @@ struct DmaGeo {
 // 16-byte chunk position of chunk c of L row r (0..63) inside the LDS row:
 // spreads the 16 rows that one transposed read touches over the banks.
 __device__ inline int l_swz(int r) { return 2 * ((r & 3) | (((r >> 3) & 1) << 2)); }
-
-// 16-byte copy global -> LDS: lane l's bytes land at lds_base + 16 * l
-// (lds_base wave-uniform).  Issued as inline assembly so that the compiler does
-// not treat every later LDS read as dependent on it; completion is awaited
-// explicitly with wait_vmcnt before the barrier that publishes a stage.
-__device__ inline void dma16(const void* g, uint32_t lds_base) {
-  asm volatile("global_load_lds_dwordx4 %1, off" ::"{m0}"(lds_base), "v"(g) : "memory");
-}
-
-__device__ inline uint32_t lds_addr(const void* p) {
-  return (uint32_t)(uintptr_t)(const lds_void*)p;
-}
 
 template <int RB>
 struct DmaSmem {
