@@ -97,6 +97,10 @@ typedef enum {
  *
  * Rows are sorted by key, then token, then slot.  Row u serves token
  * row_token[u]; bit j of row_slots[u] is set for every slot j it serves.
+ * The routed pairs sorted by (key, token, slot) are listed in pair_list; the
+ * pairs of row u sit at positions row_pair[u] .. row_pair[u+1] (one per row
+ * except in ACE_ROWS_GROUP_DEDUP mode, where a row serves every slot of its
+ * token whose expert is in the group).
  * offsets[q] .. offsets[q+1] is key q's segment; offsets[n_keys] = U, the
  * number of rows (U <= P; in ACE_ROWS_GROUP_DEDUP mode U is the number of
  * distinct (token, group) pairs, Sec. 3.5).
@@ -108,6 +112,10 @@ typedef struct ace_routing {
   uint32_t* row_slots; /* device [P]         slot mask of each row                  */
   int32_t* pair_row;   /* device [P]         row that serves pair t*k+j, -1 if dropped */
   int32_t* n_dropped;  /* device [1]         pairs dropped for an id out of range   */
+  int32_t* row_pair;   /* device [P+1]       position of row u's first pair in pair
+                                             order (key, token, slot); [U] = number
+                                             of routed pairs                          */
+  int32_t* pair_list;  /* device [P]         pair t*k+j at each position in pair order */
   int32_t n_keys;      /* host: set by ace_group_permute                            */
   int32_t mode;        /* host: ace_row_mode used                                   */
   int32_t T, k;        /* host: problem size used                                   */

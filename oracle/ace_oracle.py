@@ -83,7 +83,9 @@ def permute(topk_ids: np.ndarray, E: int, expert_to_group: Optional[np.ndarray],
     GROUP_PAIRS / EXPERT: one row per routed pair (t, j), keyed by g(e_tj) or
       e_tj; mask = {j}.
     Rows are sorted by (key, token, slot).  Built by listing the rows and
-    sorting them, not by histogram/scan.
+    sorting them, not by histogram/scan.  Also lists the routed pairs in
+    (key, token, slot) order (pair_list) and the position of each row's first
+    pair in that list (row_pair, with row_pair[U] = number of pairs).
     """
     T, k = topk_ids.shape
     n_keys = E if mode == ROWS_EXPERT else G
@@ -121,8 +123,18 @@ def permute(topk_ids: np.ndarray, E: int, expert_to_group: Optional[np.ndarray],
                 pair_row[t * k + j] = u
     offsets = np.zeros(n_keys + 1, dtype=np.int64)
     offsets[1:] = np.cumsum(counts)
+    # The routed pairs themselves in (key, token, slot) order, listed and
+    # sorted on their own; row_pair[u] = position of row u's first pair.
+    pairs = sorted((int(keys[t, j]), t, j) for t in range(T) for j in range(k) if keys[t, j] >= 0)
+    pair_list = np.array([t * k + j for (_q, t, j) in pairs], dtype=np.int64)
+    position = {(q, t, j): i for i, (q, t, j) in enumerate(pairs)}
+    row_pair = np.zeros(U + 1, dtype=np.int64)
+    for u, (q, t, j0, _m) in enumerate(rows):
+        row_pair[u] = position[(q, t, j0)]
+    row_pair[U] = len(pairs)
     return {"counts": counts, "offsets": offsets, "row_token": row_token,
-            "row_slots": row_slots, "pair_row": pair_row, "U": U}
+            "row_slots": row_slots, "pair_row": pair_row, "U": U,
+            "row_pair": row_pair, "pair_list": pair_list}
 
 
 # ---------------------------------------------------------------------------

@@ -36,6 +36,7 @@ class AceRouting(ctypes.Structure):
     _fields_ = [("counts", ctypes.c_void_p), ("offsets", ctypes.c_void_p),
                 ("row_token", ctypes.c_void_p), ("row_slots", ctypes.c_void_p),
                 ("pair_row", ctypes.c_void_p), ("n_dropped", ctypes.c_void_p),
+                ("row_pair", ctypes.c_void_p), ("pair_list", ctypes.c_void_p),
                 ("n_keys", ctypes.c_int32), ("mode", ctypes.c_int32),
                 ("T", ctypes.c_int32), ("k", ctypes.c_int32)]
 
@@ -124,9 +125,12 @@ class Routing:
         self.row_slots = torch.zeros(P, **i32)
         self.pair_row = torch.zeros(P, **i32)
         self.n_dropped = torch.zeros(1, **i32)
+        self.row_pair = torch.zeros(P + 1, **i32)
+        self.pair_list = torch.zeros(P, **i32)
         self.c = AceRouting(self.counts.data_ptr(), self.offsets.data_ptr(),
                             self.row_token.data_ptr(), self.row_slots.data_ptr(),
-                            self.pair_row.data_ptr(), self.n_dropped.data_ptr(), n_keys, -1, T, k)
+                            self.pair_row.data_ptr(), self.n_dropped.data_ptr(),
+                            self.row_pair.data_ptr(), self.pair_list.data_ptr(), n_keys, -1, T, k)
 
     @property
     def n_keys(self) -> int:

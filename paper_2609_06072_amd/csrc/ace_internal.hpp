@@ -110,6 +110,7 @@ struct GradArgs {
 struct DxArgs {
   const void* dHf;            // [T][KR]
   const void* At;             // [d_in][R]
+  const void* A;              // [R][d_in]
   void* dx;                   // [T][d_in]
   int32_t T, d_in, R, KR;
 };

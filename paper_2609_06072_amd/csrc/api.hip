@@ -64,7 +64,7 @@ ace_status check_problem(Problem& p, ace_dtype dtype, ace_input_mode im, int32_t
   if (!std::isfinite(alpha)) return fail(ACE_ERR_INVALID_ARG, "alpha is not finite");
   if (!rt) return fail(ACE_ERR_INVALID_ARG, "routing is NULL");
   if (!rt->offsets || !rt->counts) return fail(ACE_ERR_INVALID_ARG, "routing arrays are NULL");
-  if (T > 0 && (!rt->row_token || !rt->row_slots))
+  if (T > 0 && (!rt->row_token || !rt->row_slots || !rt->row_pair || !rt->pair_list))
     return fail(ACE_ERR_INVALID_ARG, "routing arrays are NULL");
   if (rt->T != T || rt->k != k)
     return fail(ACE_ERR_INVALID_ARG, "routing was built for T=%d k=%d, call has T=%d k=%d", rt->T,
@@ -185,7 +185,8 @@ ace_status ace_group_permute(const int32_t* topk_ids, int32_t T, int32_t k, int3
   if (T > 0 && !topk_ids) return fail(ACE_ERR_INVALID_ARG, "topk_ids is NULL");
   if (!rt->counts || !rt->offsets || !rt->n_dropped)
     return fail(ACE_ERR_INVALID_ARG, "routing arrays are NULL");
-  if (T > 0 && (!rt->row_token || !rt->row_slots || !rt->pair_row))
+  if (T > 0 && (!rt->row_token || !rt->row_slots || !rt->pair_row || !rt->row_pair ||
+                 !rt->pair_list))
     return fail(ACE_ERR_INVALID_ARG, "routing arrays are NULL");
   const size_t need = permute_ws_bytes(T, k, n_keys);
   if (need > 0 && (!ws || ws_bytes < need))

@@ -8,9 +8,6 @@
 //   dx    += sum over the rows that read x of A_q^T dH_u
 //
 // Launches, all deterministic (each output is reduced in a fixed order):
-//   pairs     -- rows serving several slots only: the position of each row's
-//                first pair in pair order and the pair at each position (two
-//                small launches: per-tile counts, then positions).
 //   prep      -- A^T and B_q^T into the workspace (so every MFMA operand is
 //                contiguous along its contraction index); zeroes the dense
 //                per-token dH buffer used for dx.
@@ -37,10 +34,8 @@ constexpr int kMaxJobs = kMaxKeys + 2;
 size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 
 struct WsLayout {
-  size_t At, Bt, Ht, dHt, dHf, dHrow, part, ppos, plist, tsum, total;
+  size_t At, Bt, Ht, dHt, dHf, dHrow, part, total;
 };
-
-constexpr int kPairTile = 1024;   // rows per tile of the pair-position launches
 
 // Workspace regions for element size es: At [d_in][R], Bt [R][d_out],
 // Ht/dHt [R][ldh] (column = row index inside the key's segment), dense dH
@@ -61,75 +56,8 @@ WsLayout ws_layout(int T, int k, int d_in, int d_out, int n_keys, int R, int r_m
   w.dHf = o;   o += align256(es * P * R);
   w.dHrow = o; o += align256(es * P * rpad);
   w.part = o;  o += align256(grads_part_bytes(T, k, d_in, d_out, n_keys, r_max));
-  w.ppos = o;  o += align256(4 * (P + 1));
-  w.plist = o; o += align256(4 * P);
-  w.tsum = o;  o += align256(4 * ((P + kPairTile - 1) / kPairTile));
   w.total = o + 256;
   return w;
-}
-
-// ----------------------------------------------------------------- pairs
-
-// Sum of the slot counts of each tile of kPairTile rows.
-__global__ __launch_bounds__(kThreads) void pair_count_kernel(const int32_t* offsets, int n_keys,
-                                                              const uint32_t* row_slots,
-                                                              int32_t* tsum) {
-  __shared__ int red[kThreads];
-  const int U = offsets[n_keys];
-  const int u0 = blockIdx.x * kPairTile;
-  int c = 0;
-#pragma unroll
-  for (int i = 0; i < kPairTile / kThreads; ++i) {
-    const int u = u0 + threadIdx.x + i * kThreads;
-    const uint32_t sl = row_slots[min(u, max(U - 1, 0))];
-    c += u < U ? __builtin_popcount(sl) : 0;
-  }
-  int total;
-  block_exclusive_scan(c, red, &total);
-  if (threadIdx.x == 0) tsum[blockIdx.x] = total;
-}
-
-// ppos[u] = number of pairs served by rows before u (u <= U); plist[ppos[u] +
-// i] = t*k + (i-th slot of row u).  Pairs are thus ordered by key, token, slot.
-__global__ __launch_bounds__(kThreads) void pair_write_kernel(const int32_t* offsets, int n_keys,
-                                                              const int32_t* row_token,
-                                                              const uint32_t* row_slots, int k,
-                                                              const int32_t* tsum, int32_t* ppos,
-                                                              int32_t* plist) {
-  __shared__ int red[kThreads];
-  const int U = offsets[n_keys];
-  const int u0 = blockIdx.x * kPairTile;
-  if (u0 > U) return;
-  int before = 0;
-  for (int b = threadIdx.x; b < (int)blockIdx.x; b += kThreads) before += tsum[b];
-  int base;
-  block_exclusive_scan(before, red, &base);   // base = sum over the earlier tiles
-  constexpr int RPT = kPairTile / kThreads;   // consecutive rows per thread
-  const int ub = u0 + RPT * threadIdx.x;
-  uint32_t sl[RPT];
-  int tok[RPT];
-  int c = 0;
-#pragma unroll
-  for (int i = 0; i < RPT; ++i) {
-    const int u = min(ub + i, max(U - 1, 0));
-    sl[i] = row_slots[u];
-    tok[i] = row_token[u];
-  }
-#pragma unroll
-  for (int i = 0; i < RPT; ++i) {
-    if (ub + i >= U) sl[i] = 0u;
-    c += __builtin_popcount(sl[i]);
-  }
-  int total;
-  int pos = base + block_exclusive_scan(c, red, &total);
-#pragma unroll
-  for (int i = 0; i < RPT; ++i) {
-    const int u = ub + i;
-    if (u < U) ppos[u] = pos;
-    for (uint32_t mm = sl[i]; mm; mm &= mm - 1u) plist[pos++] = tok[i] * k + __builtin_ctz(mm);
-    if (u == U - 1) ppos[U] = pos;
-  }
-  if (U == 0 && blockIdx.x == 0 && threadIdx.x == 0) ppos[0] = 0;
 }
 
 // dH of a row serving several pairs: dH_u = sum_i w_{p_i} dHp[ppos[u] + i]
@@ -331,9 +259,12 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
   pa.n_jobs = n_keys + 2;
   long nb = 0;
   auto tiles = [](long x) { return (x + kTile - 1) / kTile; };
+  // A^T feeds the per-pair dx expand and the register dx GEMM; the bf16 dx
+  // GEMM reads A itself when the dense dH rows are 16-byte aligned
+  const bool need_At = p.per_pair || p.dtype != ACE_BF16 || (kslots * R) % 8 != 0;
   pa.job_start[0] = 0;
   pa.job_cols_tiles[0] = (int)tiles(p.d_in);
-  nb += tiles(R) * tiles(p.d_in);
+  nb += need_At ? tiles(R) * tiles(p.d_in) : 0;
   for (int q = 0; q < n_keys; ++q) {
     pa.job_start[q + 1] = (int)nb;
     pa.job_cols_tiles[q + 1] = (int)tiles(p.keys.rank[q]);
@@ -357,19 +288,10 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
   c.ldh = ldh;
   c.kslots = kslots;
   c.keys = p.keys;
-  // pair positions (rows that serve several slots)
+  // pair positions of rows that serve several slots (from the permutation)
   const bool multi = p.rt->mode == ACE_ROWS_GROUP_DEDUP;
-  int32_t* ppos = multi ? reinterpret_cast<int32_t*>(base + L.ppos) : nullptr;
-  int32_t* plist = multi ? reinterpret_cast<int32_t*>(base + L.plist) : nullptr;
-  if (multi && P > 0) {
-    const int tiles = (int)((P + kPairTile - 1) / kPairTile);
-    int32_t* tsum = reinterpret_cast<int32_t*>(base + L.tsum);
-    pair_count_kernel<<<tiles, kThreads, 0, stream>>>(p.rt->offsets, n_keys, p.rt->row_slots, tsum);
-    pair_write_kernel<<<tiles, kThreads, 0, stream>>>(p.rt->offsets, n_keys, p.rt->row_token,
-                                                      p.rt->row_slots, p.k, tsum, ppos, plist);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
+  const int32_t* ppos = multi ? p.rt->row_pair : nullptr;
+  const int32_t* plist = multi ? p.rt->pair_list : nullptr;
   // Hw = w s A x, per key and pair [r][pair position]
   c.src = p.x;
   c.W = p.A;
@@ -468,6 +390,7 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
   DxArgs d{};
   d.dHf = base + L.dHf;
   d.At = base + L.At;
+  d.A = p.A;
   d.dx = dx;
   d.T = p.T;
   d.d_in = p.d_in;

@@ -3,7 +3,7 @@
 // expert-wise and "shared adapter, per-pair" modes).
 //
 // A stable counting sort of the emitted rows by key, in three launches:
-//   count   -- each block owns a chunk of whole tokens (<= 1024 pairs).  The
+//   count   -- each block owns a chunk of whole tokens (<= 256 pairs).  The
 //              block's keys go to LDS; each emitted row sets the bit of its
 //              local pair index in a per-key bitmap (LDS, ds_or_b64), and the
 //              per-(key, block) population counts are written key-major.
@@ -12,6 +12,10 @@
 //   scatter -- rebuilds the bitmap; a row's rank inside its (key, block) cell
 //              is the popcount of the lower bits, so rows come out sorted by
 //              (key, token, slot) with no atomics on rows and no sort.
+// Pair positions (the routed pairs in (key, token, slot) order) follow the
+// same scheme: in ACE_ROWS_GROUP_DEDUP mode a second bitmap marks every pair
+// of a key and second cell table is scanned; in the other modes a row is a
+// pair and its position is its row.
 #include "ace_device.hpp"
 #include "ace_internal.hpp"
 
@@ -19,7 +23,7 @@ namespace ace {
 
 namespace {
 
-constexpr int kPairsPerBlock = 1024;
+constexpr int kPairsPerBlock = 256;
 constexpr int kWordsPerKey = kPairsPerBlock / 64;
 
 struct PermArgs {
@@ -28,6 +32,7 @@ struct PermArgs {
   int32_t T, k, E, G, mode, n_keys;
   int32_t tokens_per_block, nblk;
   int32_t* cell;       // [n_keys * nblk] counts, then (scan) first rows
+  int32_t* pcell;      // [n_keys * nblk] pair counts, then first pair positions (dedup)
   int32_t* drops;      // [nblk]
   int32_t* counts;
   int32_t* offsets;
@@ -35,15 +40,20 @@ struct PermArgs {
   uint32_t* row_slots;
   int32_t* pair_row;
   int32_t* n_dropped;
+  int32_t* row_pair;
+  int32_t* pair_list;
 };
 
 // Stage the block's pair keys (-1 = dropped) and mark emitted rows in the
 // per-key bitmaps.  Returns the number of dropped pairs seen by this thread.
+// In ACE_ROWS_GROUP_DEDUP mode pbits (right after bits) also marks every pair.
 __device__ int stage_and_mark(const PermArgs& a, int p0, int np, int* keys, uint32_t* masks,
                               unsigned long long* bits) {
   const int t = threadIdx.x;
   int drops = 0;
-  for (int i = t; i < a.n_keys * kWordsPerKey; i += kThreads) bits[i] = 0ull;
+  const bool dedup = a.mode == ACE_ROWS_GROUP_DEDUP;
+  unsigned long long* pbits = bits + a.n_keys * kWordsPerKey;
+  for (int i = t; i < a.n_keys * kWordsPerKey * (dedup ? 2 : 1); i += kThreads) bits[i] = 0ull;
   for (int lp = t; lp < np; lp += kThreads) {
     const int e = a.ids[p0 + lp];
     int q = -1;
@@ -76,6 +86,7 @@ __device__ int stage_and_mark(const PermArgs& a, int p0, int np, int* keys, uint
     }
     masks[lp] = emit ? m : 0u;
     if (emit) atomicOr(&bits[q * kWordsPerKey + (lp >> 6)], 1ull << (lp & 63));
+    if (dedup) atomicOr(&pbits[q * kWordsPerKey + (lp >> 6)], 1ull << (lp & 63));
   }
   __syncthreads();
   return drops;
@@ -90,53 +101,131 @@ __global__ __launch_bounds__(kThreads) void permute_count_kernel(PermArgs a) {
   const int p0 = b * a.tokens_per_block * a.k;
   const int np = min(a.tokens_per_block * a.k, a.T * a.k - p0);
   const int d = stage_and_mark(a, p0, np, keys, masks, bits);
+  const bool dedup = a.mode == ACE_ROWS_GROUP_DEDUP;
   for (int q = threadIdx.x; q < a.n_keys; q += kThreads) {
-    int c = 0;
+    int c = 0, pc = 0;
 #pragma unroll
-    for (int w = 0; w < kWordsPerKey; ++w) c += __popcll(bits[q * kWordsPerKey + w]);
+    for (int w = 0; w < kWordsPerKey; ++w) {
+      c += __popcll(bits[q * kWordsPerKey + w]);
+      if (dedup) pc += __popcll(bits[(a.n_keys + q) * kWordsPerKey + w]);
+    }
     a.cell[q * a.nblk + b] = c;
+    if (dedup) a.pcell[q * a.nblk + b] = pc;
   }
   int total;
   block_exclusive_scan(d, red, &total);
   if (threadIdx.x == 0) a.drops[b] = total;
 }
 
-// One block of 1024 threads: exclusive scan over n_keys * nblk cells.
-__global__ __launch_bounds__(1024) void permute_scan_kernel(PermArgs a) {
-  __shared__ int part[1024];
-  const int t = threadIdx.x;
-  const int N = a.n_keys * a.nblk;
+// Inclusive scan of one int per lane across a wave of 64.
+__device__ inline int wave_inclusive_scan(int v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int o = __shfl_up(v, off, 64);
+    if (lane >= off) v += o;
+  }
+  return v;
+}
+
+// Exclusive scans in place of v[0 .. N) and w[0 .. N) (w may be null) by one
+// block of 1024 threads (16 waves); returns the totals.
+__device__ int2 scan_cells(int32_t* v, int32_t* w, int N, int2* part) {
+  constexpr int MAXPER = 16;   // cells per thread held in registers (N <= 16384)
+  const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
   const int per = (N + 1023) / 1024;
   const int lo = min(N, t * per), hi = min(N, lo + per);
-  int s = 0;
-  for (int i = lo; i < hi; ++i) s += a.cell[i];
-  part[t] = s;
-  __syncthreads();
-  for (int off = 1; off < 1024; off <<= 1) {
-    const int add = t >= off ? part[t - off] : 0;
-    __syncthreads();
-    part[t] += add;
-    __syncthreads();
+  int sv = 0, sw = 0;
+  int rv_[MAXPER], rw_[MAXPER];
+  const bool regs = per <= MAXPER;
+  if (regs) {
+    // unconditional clamped loads, all in flight at once
+#pragma unroll
+    for (int i = 0; i < MAXPER; ++i) {
+      const int idx = min(lo + i, max(N - 1, 0));
+      rv_[i] = N > 0 ? v[idx] : 0;
+      rw_[i] = (N > 0 && w) ? w[idx] : 0;
+    }
+#pragma unroll
+    for (int i = 0; i < MAXPER; ++i) {
+      if (lo + i < hi) {
+        sv += rv_[i];
+        sw += rw_[i];
+      }
+    }
+  } else {
+    for (int i = lo; i < hi; ++i) {
+      sv += v[i];
+      if (w) sw += w[i];
+    }
   }
-  int run = part[t] - s;  // exclusive prefix of this thread's range
-  for (int i = lo; i < hi; ++i) {
-    const int c = a.cell[i];
-    a.cell[i] = run;
-    run += c;
+  const int iv = wave_inclusive_scan(sv), iw = wave_inclusive_scan(sw);
+  if (lane == 63) part[wv] = make_int2(iv, iw);
+  __syncthreads();
+  if (t < 64) {
+    int2 x = t < 16 ? part[t] : make_int2(0, 0);
+    const int a = wave_inclusive_scan(x.x), b = wave_inclusive_scan(x.y);
+    if (t < 16) part[16 + t] = make_int2(a, b);   // inclusive per-wave prefixes
   }
   __syncthreads();
-  const int U = part[1023];
+  const int2 before = wv > 0 ? part[16 + wv - 1] : make_int2(0, 0);
+  int rv = before.x + iv - sv, rw = before.y + iw - sw;   // exclusive prefixes of this thread
+  if (regs) {
+#pragma unroll
+    for (int i = 0; i < MAXPER; ++i) {
+      if (lo + i < hi) {
+        v[lo + i] = rv;
+        rv += rv_[i];
+        if (w) {
+          w[lo + i] = rw;
+          rw += rw_[i];
+        }
+      }
+    }
+  } else {
+    for (int i = lo; i < hi; ++i) {
+      const int c = v[i];
+      v[i] = rv;
+      rv += c;
+      if (w) {
+        const int d = w[i];
+        w[i] = rw;
+        rw += d;
+      }
+    }
+  }
+  const int2 total = part[16 + 15];
+  __syncthreads();
+  return total;
+}
+
+// One block of 1024 threads: exclusive scans over the n_keys * nblk cells.
+__global__ __launch_bounds__(1024) void permute_scan_kernel(PermArgs a) {
+  __shared__ int2 part[32];
+  __shared__ int dsum[16];
+  const int t = threadIdx.x;
+  const int N = a.n_keys * a.nblk;
+  const bool dedup = a.mode == ACE_ROWS_GROUP_DEDUP;
+  const int2 tot = scan_cells(a.cell, dedup ? a.pcell : nullptr, N, part);
+  const int U = tot.x;
+  const int npairs = dedup ? tot.y : U;
   for (int q = t; q < a.n_keys; q += 1024) {
     const int first = a.nblk > 0 ? a.cell[q * a.nblk] : 0;
     const int next = (q + 1 < a.n_keys && a.nblk > 0) ? a.cell[(q + 1) * a.nblk] : U;
     a.offsets[q] = first;
     a.counts[q] = next - first;
   }
+  int d = 0;
+  for (int b = t; b < a.nblk; b += 1024) d += a.drops[b];
+  d = wave_inclusive_scan(d);
+  if ((t & 63) == 63) dsum[t >> 6] = d;
+  __syncthreads();
   if (t == 0) {
+    int dt = 0;
+    for (int i = 0; i < 16; ++i) dt += dsum[i];
+    *a.n_dropped = dt;
     a.offsets[a.n_keys] = U;
-    int d = 0;
-    for (int b = 0; b < a.nblk; ++b) d += a.drops[b];
-    *a.n_dropped = d;
+    a.row_pair[U] = npairs;
   }
 }
 
@@ -165,7 +254,19 @@ __global__ __launch_bounds__(kThreads) void permute_scatter_kernel(PermArgs a) {
     const int tok = (p0 + lp) / k;
     a.row_token[row] = tok;
     a.row_slots[row] = m;
-    for (uint32_t mm = m; mm; mm &= mm - 1u) a.pair_row[tok * k + __builtin_ctz(mm)] = row;
+    int pos = row;
+    if (a.mode == ACE_ROWS_GROUP_DEDUP) {  // the row's first pair among the key's pairs
+      const unsigned long long* pb = bits + (a.n_keys + q) * kWordsPerKey;
+      int prank = __popcll(pb[w] & ((1ull << (lp & 63)) - 1ull));
+      for (int i = 0; i < w; ++i) prank += __popcll(pb[i]);
+      pos = a.pcell[q * a.nblk + b] + prank;
+    }
+    a.row_pair[row] = pos;
+    for (uint32_t mm = m; mm; mm &= mm - 1u) {
+      const int p = tok * k + __builtin_ctz(mm);
+      a.pair_row[p] = row;
+      a.pair_list[pos++] = p;
+    }
   }
 }
 
@@ -174,7 +275,7 @@ __global__ __launch_bounds__(kThreads) void permute_scatter_kernel(PermArgs a) {
 size_t permute_ws_bytes(int T, int k, int n_keys) {
   const int tpb = permute_tokens_per_block(k);
   const long nblk = T > 0 ? (T + tpb - 1) / tpb : 0;
-  return (size_t)(nblk * n_keys + nblk) * sizeof(int32_t);
+  return (size_t)(2 * nblk * n_keys + nblk) * sizeof(int32_t);
 }
 
 int permute_tokens_per_block(int k) { return k > 0 ? kPairsPerBlock / k : 1; }
@@ -194,14 +295,18 @@ hipError_t launch_permute(const int32_t* ids, int T, int k, int E, const int32_t
   a.tokens_per_block = permute_tokens_per_block(k);
   a.nblk = T > 0 ? (T + a.tokens_per_block - 1) / a.tokens_per_block : 0;
   a.cell = static_cast<int32_t*>(ws);
-  a.drops = a.cell + (size_t)a.nblk * n_keys;
+  a.pcell = a.cell + (size_t)a.nblk * n_keys;
+  a.drops = a.pcell + (size_t)a.nblk * n_keys;
   a.counts = rt->counts;
   a.offsets = rt->offsets;
   a.row_token = rt->row_token;
   a.row_slots = rt->row_slots;
   a.pair_row = rt->pair_row;
   a.n_dropped = rt->n_dropped;
-  const size_t lds = (size_t)n_keys * kWordsPerKey * sizeof(unsigned long long);
+  a.row_pair = rt->row_pair;
+  a.pair_list = rt->pair_list;
+  const size_t lds = (size_t)n_keys * kWordsPerKey * sizeof(unsigned long long) *
+                     (mode == ACE_ROWS_GROUP_DEDUP ? 2 : 1);
   if (a.nblk > 0) {
     permute_count_kernel<<<a.nblk, kThreads, lds, stream>>>(a);
   }

@@ -53,7 +53,8 @@ def test_workspace_bytes(ace):
 
 def _routing(ace, T=4, k=2, n_keys=2, mode=0):
     # fake (never dereferenced) device addresses: validation fails before use
-    r = ace.AceRouting(0x1000, 0x2000, 0x3000, 0x4000, 0x5000, 0x6000, n_keys, mode, T, k)
+    r = ace.AceRouting(0x1000, 0x2000, 0x3000, 0x4000, 0x5000, 0x6000, 0x7000, 0x8000, n_keys, mode,
+                       T, k)
     return r
 
 

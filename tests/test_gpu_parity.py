@@ -54,6 +54,11 @@ def _perm_check(ids, E, e2g, G, mode):
         assert np.array_equal(rt.row_token.cpu().numpy()[:U], ref["row_token"])
         assert np.array_equal(rt.row_slots.cpu().numpy().view(np.uint32)[:U], ref["row_slots"])
         assert np.array_equal(rt.pair_row.cpu().numpy(), ref["pair_row"])
+        npairs = int(ref["row_pair"][U])
+        assert np.array_equal(rt.row_pair.cpu().numpy()[:U + 1], ref["row_pair"])
+        assert np.array_equal(rt.pair_list.cpu().numpy()[:npairs], ref["pair_list"])
+    else:
+        assert int(rt.row_pair.cpu().numpy()[0]) == 0
     dropped = int(np.sum(ref["pair_row"] < 0)) if mode != ace.ACE_ROWS_GROUP_DEDUP else None
     n = ace.ace_routing_check(rt)
     valid_pairs = sum(bin(int(m)).count("1") for m in ref["row_slots"])
@@ -215,7 +220,7 @@ def test_deterministic(path):
     b = run_gpu(c)
     for key in ("y", "dx", "dA", "dB"):
         assert torch.equal(a[key], b[key]), key
-    for key in ("row_token", "row_slots", "pair_row", "offsets"):
+    for key in ("row_token", "row_slots", "pair_row", "offsets", "row_pair", "pair_list"):
         assert torch.equal(getattr(a["routing"], key), getattr(b["routing"], key))
 
 

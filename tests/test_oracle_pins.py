@@ -57,7 +57,7 @@ def test_hand_permutation(mode, name):
     rt = O.permute(_np(g["topk_ids"], np.int64), g["E"], _np(g["expert_to_group"], np.int64),
                    g["G"], mode)
     exp = g["permute"][name]
-    for key in ("counts", "offsets", "row_token", "row_slots", "pair_row"):
+    for key in ("counts", "offsets", "row_token", "row_slots", "pair_row", "row_pair", "pair_list"):
         assert list(rt[key]) == exp[key], key
 
 
@@ -309,6 +309,20 @@ def test_permutation_invariants(mode):
         assert U == exp_U
     else:
         assert U == cfg.P
+    # pair order: every routed pair once, sorted by (key, token, slot); a
+    # row's pairs are consecutive and start at row_pair[u]
+    rp, pl = res["row_pair"], res["pair_list"]
+    assert rp[U] == cfg.P and sorted(pl.tolist()) == list(range(cfg.P))
+    keyed = [(key(ids[p // cfg.k, p % cfg.k]), p // cfg.k, p % cfg.k) for p in pl]
+    assert keyed == sorted(keyed)
+    for u in range(U):
+        m = int(res["row_slots"][u])
+        slots = [j for j in range(cfg.k) if (m >> j) & 1]
+        assert rp[u + 1] - rp[u] == len(slots)
+        t = res["row_token"][u]
+        assert pl[rp[u]:rp[u + 1]].tolist() == [t * cfg.k + j for j in slots]
+    if mode != O.ROWS_GROUP_DEDUP:
+        assert np.array_equal(rp, np.arange(U + 1))
 
 
 def test_k1_dedup_is_pairs():
@@ -317,7 +331,7 @@ def test_k1_dedup_is_pairs():
     e2g = np.arange(8) // 2
     a = O.permute(ids, 8, e2g, 4, O.ROWS_GROUP_DEDUP)
     b = O.permute(ids, 8, e2g, 4, O.ROWS_GROUP_PAIRS)
-    for key in ("counts", "offsets", "row_token", "row_slots", "pair_row"):
+    for key in ("counts", "offsets", "row_token", "row_slots", "pair_row", "row_pair", "pair_list"):
         assert np.array_equal(a[key], b[key])
 
 
