@@ -60,17 +60,27 @@ class Path:
         self.ids = torch.from_numpy(rt.topk_ids).to(dev)
         self.e2g = torch.from_numpy(rt.expert_to_group).to(dev)
         self.G = rt.G
-        self.rt_e = ace.Routing(cfg.T, cfg.k, cfg.E)
-        self.rt_g = ace.Routing(cfg.T, cfg.k, rt.G) if kind == "ace" else None
+        # row mode of each projection: the shared-input projections (gate/up)
+        # and the per-pair one (down) per execution scheme
+        shared_mode, pair_mode = {
+            "ace": (ace.ACE_ROWS_GROUP_DEDUP, ace.ACE_ROWS_EXPERT),
+            "lora": (ace.ACE_ROWS_EXPERT, ace.ACE_ROWS_EXPERT),
+            "consolidated": (ace.ACE_ROWS_GROUP_PAIRS, ace.ACE_ROWS_EXPERT),
+            "consolidated_down": (ace.ACE_ROWS_GROUP_DEDUP, ace.ACE_ROWS_GROUP_PAIRS),
+        }[kind]
         self.projs = []
+        modes = set()
         for proj in cfg.projections:
             d_in, d_out, im = cfg.proj_dims(proj)
-            grouped = kind == "ace" and im == W.INPUT_SHARED
+            mode = shared_mode if im == W.INPUT_SHARED else pair_mode
+            modes.add(mode)
+            grouped = mode != ace.ACE_ROWS_EXPERT
             ranks = [int(r) for r in rt.group_rank] if grouped else [cfg.r_e] * cfg.E
             b = bufs[proj]
-            mode = ace.ACE_ROWS_GROUP_DEDUP if grouped else ace.ACE_ROWS_EXPERT
             self.projs.append(Proj(proj, mode, im, ranks, b["x"], b["A"], b["B"], b["dy"], b["y"],
                                    b["dx"], b["dA"], b["dB"]))
+        self.rts = {m: ace.Routing(cfg.T, cfg.k, cfg.E if m == ace.ACE_ROWS_EXPERT else rt.G)
+                    for m in sorted(modes)}
         self.timer = None   # (proj name, phase) -> list of (start, end) events
         self.marker = None  # callable(label) run before each phase (traffic pass)
 
@@ -78,20 +88,20 @@ class Path:
         a = self.ace
         if p.mode == a.ACE_ROWS_EXPERT:
             a.ace_expertwise_lora_fwd(p.x, p.A, p.B, self.cfg.E, self.cfg.r_e, self.cfg.alpha,
-                                      self.rt_e, p.y, input_mode=p.im)
+                                      self.rts[p.mode], p.y, input_mode=p.im)
         else:
-            a.ace_grouped_lora_fwd(p.x, p.A, p.B, p.ranks, self.cfg.alpha, self.rt_g, p.y,
+            a.ace_grouped_lora_fwd(p.x, p.A, p.B, p.ranks, self.cfg.alpha, self.rts[p.mode], p.y,
                                    input_mode=p.im)
 
     def _bwd(self, p):
         a = self.ace
         if p.mode == a.ACE_ROWS_EXPERT:
             a.ace_expertwise_lora_bwd(p.x, p.A, p.B, self.cfg.E, self.cfg.r_e, self.cfg.alpha,
-                                      self.rt_e, p.dy, p.dx, p.dA, p.dB, input_mode=p.im,
+                                      self.rts[p.mode], p.dy, p.dx, p.dA, p.dB, input_mode=p.im,
                                       ws=self.ws_bwd)
         else:
-            a.ace_grouped_lora_bwd(p.x, p.A, p.B, p.ranks, self.cfg.alpha, self.rt_g, p.dy, p.dx,
-                                   p.dA, p.dB, input_mode=p.im, ws=self.ws_bwd)
+            a.ace_grouped_lora_bwd(p.x, p.A, p.B, p.ranks, self.cfg.alpha, self.rts[p.mode], p.dy,
+                                   p.dx, p.dA, p.dB, input_mode=p.im, ws=self.ws_bwd)
 
     def _timed(self, key, fn, *args):
         import torch
@@ -107,16 +117,67 @@ class Path:
 
     def step(self):
         a = self.ace
-        if self.rt_g is not None:
-            self._timed(("permute", "group"), a.ace_group_permute, self.ids, self.cfg.E, self.e2g,
-                        self.G, a.ACE_ROWS_GROUP_DEDUP, self.rt_g, self.ws_perm)
-        if any(p.mode == a.ACE_ROWS_EXPERT for p in self.projs):
-            self._timed(("permute", "expert"), a.ace_group_permute, self.ids, self.cfg.E, None,
-                        self.cfg.E, a.ACE_ROWS_EXPERT, self.rt_e, self.ws_perm)
+        names = {a.ACE_ROWS_GROUP_DEDUP: "group", a.ACE_ROWS_GROUP_PAIRS: "group_pairs",
+                 a.ACE_ROWS_EXPERT: "expert"}
+        for m, rt in self.rts.items():
+            expert = m == a.ACE_ROWS_EXPERT
+            self._timed(("permute", names[m]), a.ace_group_permute, self.ids, self.cfg.E,
+                        None if expert else self.e2g, self.cfg.E if expert else self.G, m, rt,
+                        self.ws_perm)
         for p in self.projs:
             self._timed((p.name, "fwd"), self._fwd, p)
         for p in reversed(self.projs):
             self._timed((p.name, "bwd"), self._bwd, p)
+
+
+class PerExpertPath:
+    """Expert-wise LoRA launched once per expert, the execution pattern the
+    paper measures its baseline with (Sec. 3.1.3, App. L): per expert, a
+    one-key routing of that expert's pairs (other experts' pairs dropped) and
+    a forward/backward call on its own rank-r adapter block."""
+
+    def __init__(self, ace, cfg, rt, bufs):
+        import torch
+        self.ace, self.cfg = ace, cfg
+        dev = "cuda"
+        self.ids = torch.from_numpy(rt.topk_ids).to(dev)
+        self.maps = []
+        for e in range(cfg.E):
+            m = torch.full((cfg.E,), -1, dtype=torch.int32, device=dev)
+            m[e] = 0
+            self.maps.append(m)
+        self.rts = [ace.Routing(cfg.T, cfg.k, 1) for _ in range(cfg.E)]
+        self.ws_perm = torch.empty(max(256, ace.ace_workspace_bytes(ace.ACE_OP_PERMUTE, cfg.T, cfg.k,
+                                                                     0, 0, 1, 0)),
+                                   dtype=torch.uint8, device=dev)
+        need = 0
+        self.projs = []
+        r = cfg.r_e
+        for proj in cfg.projections:
+            d_in, d_out, im = cfg.proj_dims(proj)
+            need = max(need, ace.ace_workspace_bytes(ace.ACE_OP_BWD, cfg.T, cfg.k, d_in, d_out, 1, r))
+            b = bufs[proj]
+            self.projs.append((proj, im, d_in, d_out, b))
+        self.ws_bwd = torch.empty(need, dtype=torch.uint8, device=dev)
+        self.timer = None
+        self.marker = None
+
+    def step(self):
+        a, cfg, r = self.ace, self.cfg, self.cfg.r_e
+        for e in range(cfg.E):
+            a.ace_group_permute(self.ids, cfg.E, self.maps[e], 1, a.ACE_ROWS_GROUP_PAIRS, self.rts[e],
+                                self.ws_perm)
+        for proj, im, d_in, d_out, b in self.projs:
+            for e in range(cfg.E):
+                a.ace_grouped_lora_fwd(b["x"], b["A"][e * r:(e + 1) * r], b["B"][e * r * d_out:(e + 1) * r * d_out],
+                                       [r], cfg.alpha, self.rts[e], b["y"], input_mode=im)
+        for proj, im, d_in, d_out, b in reversed(self.projs):
+            for e in range(cfg.E):
+                a.ace_grouped_lora_bwd(b["x"], b["A"][e * r:(e + 1) * r],
+                                       b["B"][e * r * d_out:(e + 1) * r * d_out], [r], cfg.alpha,
+                                       self.rts[e], b["dy"], b["dx"], b["dA"][e * r:(e + 1) * r],
+                                       b["dB"][e * r * d_out:(e + 1) * r * d_out], input_mode=im,
+                                       ws=self.ws_bwd)
 
 
 def make_buffers(cfg, rt, seed=0):
@@ -361,7 +422,12 @@ def trace_summary(trace_dir, fetch_dir, labels_path, config, command):
     keys = [t[0] for t in trace]
     lines = [f"# kernel time per call, {config} (rocprofv3 kernel trace)", f"source_hash {source_hash()}",
              f"command {command}"]
-    for kind in ("ace", "lora"):
+    kinds = []
+    for lab in labels:
+        kd = lab.split(":")[0]
+        if kd != "calib" and kd not in kinds:
+            kinds.append(kd)
+    for kind in kinds:
         calls = [(lab, [n for n, _ in ph[lab]]) for lab in labels if lab.startswith(kind + ":")]
         sig = [n for _, ns in calls for n in ns]
         acc = {lab: [] for lab, _ in calls}
@@ -425,6 +491,8 @@ def main():
     ap.add_argument("--config", default="olmoe_bf16", choices=W.CONFIG_ORDER)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="time only the ace and expert-wise steps (not the ablation rows)")
     ap.add_argument("--traffic-pass", metavar="LABELS_OUT",
                     help="run one marked step of each path for rocprofv3 counter passes")
     ap.add_argument("--pmc-summary", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "LABELS"),
@@ -467,11 +535,18 @@ def main():
             need = max(need, ace.ace_workspace_bytes(ace.ACE_OP_BWD, cfg.T, cfg.k, d_in, d_out, nk, r))
     ws_bwd = torch.empty(need, dtype=torch.uint8, device="cuda")
 
-    paths = {kind: Path(ace, cfg, rt, kind, bufs, ws_perm, ws_bwd) for kind in ("ace", "lora")}
+    kinds = ("ace", "lora") if args.no_extras else ("ace", "lora", "consolidated", "consolidated_down")
+    paths = {kind: Path(ace, cfg, rt, kind, bufs, ws_perm, ws_bwd) for kind in kinds}
     if args.traffic_pass:
         traffic_pass(paths, args.traffic_pass)
         return
     res = {}
+    if not args.no_extras:
+        # launch-bound: a few steps suffice
+        pe = PerExpertPath(ace, cfg, rt, bufs)
+        per_step, _ = time_path(pe, max(2, args.steps // 20), 2, 2)
+        res["expertwise_per_expert_launch"] = dict(ms=statistics.median(per_step), ms_std=statistics.pstdev(per_step),
+                                                   ms_with_events=statistics.median(per_step), phases={})
     for kind, path in paths.items():
         per_step, phases = time_path(path, args.steps, args.warmup, args.repeats)
         plain = time_plain(path, args.steps, args.repeats)
@@ -537,9 +612,19 @@ def main():
                      "frac": achieved / HBM_PEAK_GBS, "traffic": dom_traffic,
                      "algorithmic_bytes": call_bytes[dom], "ms_per_call": dom_ms},
         "call_roofline_frac": call_roofline,
-        "phases_ms": {k: {"ace": res["ace"]["phases"].get(k), "lora": res["lora"]["phases"].get(k)}
-                      for k in sorted(set(res["ace"]["phases"]) | set(res["lora"]["phases"]))},
-        "ms_std": {"ace": res["ace"]["ms_std"], "lora": res["lora"]["ms_std"]},
+        "phases_ms": {k: {kind: res[kind]["phases"].get(k) for kind in res}
+                      for k in sorted(set().union(*(set(r["phases"]) for r in res.values())))},
+        "extra_rows": {
+            kind: {"ms_per_step": res[kind]["ms"], "value": P / (res[kind]["ms"] * 1e-3),
+                   "what": {"consolidated": "group-rank adapters on gate/up run per routed pair "
+                                            "(no compute-once), expert-wise down",
+                            "consolidated_down": "ace step with the down projection at group "
+                                                 "rank over pair rows",
+                            "expertwise_per_expert_launch": "expert-wise LoRA with one permutation "
+                                                            "and one fwd/bwd call per expert (the "
+                                                            "baseline's launch pattern)"}[kind]}
+            for kind in res if kind not in ("ace", "lora")},
+        "ms_std": {kind: res[kind]["ms_std"] for kind in res},
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(cfg, rt)
