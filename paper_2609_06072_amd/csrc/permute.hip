@@ -2,13 +2,17 @@
 // token, one row per (token, active group); or one row per routed pair for the
 // expert-wise and "shared adapter, per-pair" modes).
 //
-// A stable counting sort of the emitted rows by key, in three launches:
+// A stable counting sort of the emitted rows by key, in two or three launches:
 //   count   -- each block owns a chunk of whole tokens (<= 256 pairs).  The
 //              block's keys go to LDS; each emitted row sets the bit of its
 //              local pair index in a per-key bitmap (LDS, ds_or_b64), and the
 //              per-(key, block) population counts are written key-major.
 //   scan    -- one block: exclusive scan of the key-major counts gives each
 //              (key, block) its first row; counts/offsets/n_dropped written.
+//              Only for large cell tables: otherwise every scatter block
+//              derives the bases of its own cells from the count table
+//              (per-key totals and prefixes, exact integer sums) and block 0
+//              writes counts/offsets/n_dropped.
 //   scatter -- rebuilds the bitmap; a row's rank inside its (key, block) cell
 //              is the popcount of the lower bits, so rows come out sorted by
 //              (key, token, slot) with no atomics on rows and no sort.
@@ -31,6 +35,7 @@ struct PermArgs {
   const int32_t* e2g;  // null in expert mode
   int32_t T, k, E, G, mode, n_keys;
   int32_t tokens_per_block, nblk;
+  int32_t fold;        // the scatter derives the cell bases itself (no scan launch)
   int32_t* cell;       // [n_keys * nblk] counts, then (scan) first rows
   int32_t* pcell;      // [n_keys * nblk] pair counts, then first pair positions (dedup)
   int32_t* drops;      // [nblk]
@@ -229,14 +234,94 @@ __global__ __launch_bounds__(1024) void permute_scan_kernel(PermArgs a) {
   }
 }
 
+constexpr int kFoldCells = 16384;   // largest cell table the scatter scans itself
+
 __global__ __launch_bounds__(kThreads) void permute_scatter_kernel(PermArgs a) {
   extern __shared__ unsigned long long bits[];
   __shared__ int keys[kPairsPerBlock];
   __shared__ uint32_t masks[kPairsPerBlock];
+  __shared__ int tot[kMaxKeys], pre[kMaxKeys], ptot[kMaxKeys], ppre[kMaxKeys];
+  __shared__ int cbase[kMaxKeys], pbase[kMaxKeys];
+  __shared__ int red[kThreads];
   const int b = blockIdx.x;
   const int k = a.k;
   const int p0 = b * a.tokens_per_block * k;
   const int np = min(a.tokens_per_block * k, a.T * k - p0);
+  const bool dedup = a.mode == ACE_ROWS_GROUP_DEDUP;
+  if (a.fold) {
+    // per-key totals over all blocks and prefixes over the blocks before this one
+    const int t = threadIdx.x;
+    for (int q = t; q < a.n_keys; q += kThreads) tot[q] = pre[q] = ptot[q] = ppre[q] = 0;
+    __syncthreads();
+    // each thread sums a contiguous range of the key-major table (at most a
+    // few keys), then adds its per-key sums with one LDS atomic per key
+    const int N = a.n_keys * a.nblk;
+    const int per = (N + kThreads - 1) / kThreads;
+    const int lo = min(N, t * per), hi = min(N, lo + per);
+    int cq = lo < hi ? lo / a.nblk : 0;
+    int st = 0, sp = 0, pt = 0, pp = 0;
+    auto flush = [&]() {
+      if (st | sp | pt | pp) {
+        atomicAdd(&tot[cq], st);
+        atomicAdd(&pre[cq], sp);
+        atomicAdd(&ptot[cq], pt);
+        atomicAdd(&ppre[cq], pp);
+      }
+      st = sp = pt = pp = 0;
+    };
+    for (int i0 = lo; i0 < hi; i0 += 8) {
+      int cv[8], pv[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {   // unconditional clamped loads, all in flight
+        const int i = min(i0 + j, N - 1);
+        cv[j] = a.cell[i];
+        pv[j] = dedup ? a.pcell[i] : 0;
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int i = i0 + j;
+        if (i < hi) {
+          const int q = i / a.nblk, bb = i - q * a.nblk;
+          if (q != cq) {
+            flush();
+            cq = q;
+          }
+          st += cv[j];
+          pt += pv[j];
+          if (bb < b) {
+            sp += cv[j];
+            pp += pv[j];
+          }
+        }
+      }
+    }
+    flush();
+    __syncthreads();
+    const int q = t;   // n_keys <= kThreads
+    int U, npairs;
+    const int ks = block_exclusive_scan(q < a.n_keys ? tot[q] : 0, red, &U);
+    const int pks = block_exclusive_scan(q < a.n_keys && dedup ? ptot[q] : 0, red, &npairs);
+    if (q < a.n_keys) {
+      cbase[q] = ks + pre[q];
+      pbase[q] = pks + ppre[q];
+      if (b == 0) {
+        a.offsets[q] = ks;
+        a.counts[q] = tot[q];
+      }
+    }
+    if (b == 0) {
+      int d = 0;
+      for (int bb = t; bb < a.nblk; bb += kThreads) d += a.drops[bb];
+      int dt;
+      block_exclusive_scan(d, red, &dt);
+      if (t == 0) {
+        a.offsets[a.n_keys] = U;
+        a.row_pair[U] = dedup ? npairs : U;
+        *a.n_dropped = dt;
+      }
+    }
+    __syncthreads();
+  }
   stage_and_mark(a, p0, np, keys, masks, bits);
   for (int lp = threadIdx.x; lp < np; lp += kThreads) {
     const int q = keys[lp];
@@ -250,7 +335,7 @@ __global__ __launch_bounds__(kThreads) void permute_scatter_kernel(PermArgs a) {
     const int w = lp >> 6;
     int rank = __popcll(kb[w] & ((1ull << (lp & 63)) - 1ull));
     for (int i = 0; i < w; ++i) rank += __popcll(kb[i]);
-    const int row = a.cell[q * a.nblk + b] + rank;
+    const int row = (a.fold ? cbase[q] : a.cell[q * a.nblk + b]) + rank;
     const int tok = (p0 + lp) / k;
     a.row_token[row] = tok;
     a.row_slots[row] = m;
@@ -259,7 +344,7 @@ __global__ __launch_bounds__(kThreads) void permute_scatter_kernel(PermArgs a) {
       const unsigned long long* pb = bits + (a.n_keys + q) * kWordsPerKey;
       int prank = __popcll(pb[w] & ((1ull << (lp & 63)) - 1ull));
       for (int i = 0; i < w; ++i) prank += __popcll(pb[i]);
-      pos = a.pcell[q * a.nblk + b] + prank;
+      pos = (a.fold ? pbase[q] : a.pcell[q * a.nblk + b]) + prank;
     }
     a.row_pair[row] = pos;
     for (uint32_t mm = m; mm; mm &= mm - 1u) {
@@ -307,10 +392,11 @@ hipError_t launch_permute(const int32_t* ids, int T, int k, int E, const int32_t
   a.pair_list = rt->pair_list;
   const size_t lds = (size_t)n_keys * kWordsPerKey * sizeof(unsigned long long) *
                      (mode == ACE_ROWS_GROUP_DEDUP ? 2 : 1);
+  a.fold = a.nblk > 0 && (long)a.nblk * n_keys <= kFoldCells;
   if (a.nblk > 0) {
     permute_count_kernel<<<a.nblk, kThreads, lds, stream>>>(a);
   }
-  permute_scan_kernel<<<1, 1024, 0, stream>>>(a);
+  if (!a.fold) permute_scan_kernel<<<1, 1024, 0, stream>>>(a);
   if (a.nblk > 0) {
     permute_scatter_kernel<<<a.nblk, kThreads, lds, stream>>>(a);
   }
