@@ -47,6 +47,7 @@ class Proj:
     def __init__(self, name, mode, im, ranks, x, A, B, dy, y, dx, dA, dB):
         self.name, self.mode, self.im, self.ranks = name, mode, im, ranks
         self.x, self.A, self.B, self.dy, self.y, self.dx, self.dA, self.dB = x, A, B, dy, y, dx, dA, dB
+        self.ws_fwd = None  # the forward's workspace; the backward reads h from it
 
 
 class Path:
@@ -77,8 +78,12 @@ class Path:
             grouped = mode != ace.ACE_ROWS_EXPERT
             ranks = [int(r) for r in rt.group_rank] if grouped else [cfg.r_e] * cfg.E
             b = bufs[proj]
-            self.projs.append(Proj(proj, mode, im, ranks, b["x"], b["A"], b["B"], b["dy"], b["y"],
-                                   b["dx"], b["dA"], b["dB"]))
+            pj = Proj(proj, mode, im, ranks, b["x"], b["A"], b["B"], b["dy"], b["y"], b["dx"],
+                      b["dA"], b["dB"])
+            need = ace.ace_workspace_bytes(ace.ACE_OP_FWD, cfg.T, cfg.k, d_in, d_out, len(ranks),
+                                           max(ranks))
+            pj.ws_fwd = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+            self.projs.append(pj)
         self.rts = {m: ace.Routing(cfg.T, cfg.k, cfg.E if m == ace.ACE_ROWS_EXPERT else rt.G)
                     for m in sorted(modes)}
         self.timer = None   # (proj name, phase) -> list of (start, end) events
@@ -88,20 +93,21 @@ class Path:
         a = self.ace
         if p.mode == a.ACE_ROWS_EXPERT:
             a.ace_expertwise_lora_fwd(p.x, p.A, p.B, self.cfg.E, self.cfg.r_e, self.cfg.alpha,
-                                      self.rts[p.mode], p.y, input_mode=p.im)
+                                      self.rts[p.mode], p.y, input_mode=p.im, ws=p.ws_fwd)
         else:
             a.ace_grouped_lora_fwd(p.x, p.A, p.B, p.ranks, self.cfg.alpha, self.rts[p.mode], p.y,
-                                   input_mode=p.im)
+                                   input_mode=p.im, ws=p.ws_fwd)
 
     def _bwd(self, p):
         a = self.ace
         if p.mode == a.ACE_ROWS_EXPERT:
             a.ace_expertwise_lora_bwd(p.x, p.A, p.B, self.cfg.E, self.cfg.r_e, self.cfg.alpha,
                                       self.rts[p.mode], p.dy, p.dx, p.dA, p.dB, input_mode=p.im,
-                                      ws=self.ws_bwd)
+                                      ws=self.ws_bwd, h_fwd=p.ws_fwd)
         else:
             a.ace_grouped_lora_bwd(p.x, p.A, p.B, p.ranks, self.cfg.alpha, self.rts[p.mode], p.dy,
-                                   p.dx, p.dA, p.dB, input_mode=p.im, ws=self.ws_bwd)
+                                   p.dx, p.dA, p.dB, input_mode=p.im, ws=self.ws_bwd,
+                                   h_fwd=p.ws_fwd)
 
     def _timed(self, key, fn, *args):
         import torch
@@ -156,7 +162,10 @@ class PerExpertPath:
         for proj in cfg.projections:
             d_in, d_out, im = cfg.proj_dims(proj)
             need = max(need, ace.ace_workspace_bytes(ace.ACE_OP_BWD, cfg.T, cfg.k, d_in, d_out, 1, r))
-            b = bufs[proj]
+            b = dict(bufs[proj])
+            # one forward workspace per expert call; its backward reads h from it
+            nf = max(256, ace.ace_workspace_bytes(ace.ACE_OP_FWD, cfg.T, cfg.k, d_in, d_out, 1, r))
+            b["ws_fwd"] = [torch.empty(nf, dtype=torch.uint8, device=dev) for _ in range(cfg.E)]
             self.projs.append((proj, im, d_in, d_out, b))
         self.ws_bwd = torch.empty(need, dtype=torch.uint8, device=dev)
         self.timer = None
@@ -170,14 +179,15 @@ class PerExpertPath:
         for proj, im, d_in, d_out, b in self.projs:
             for e in range(cfg.E):
                 a.ace_grouped_lora_fwd(b["x"], b["A"][e * r:(e + 1) * r], b["B"][e * r * d_out:(e + 1) * r * d_out],
-                                       [r], cfg.alpha, self.rts[e], b["y"], input_mode=im)
+                                       [r], cfg.alpha, self.rts[e], b["y"], input_mode=im,
+                                       ws=b["ws_fwd"][e])
         for proj, im, d_in, d_out, b in reversed(self.projs):
             for e in range(cfg.E):
                 a.ace_grouped_lora_bwd(b["x"], b["A"][e * r:(e + 1) * r],
                                        b["B"][e * r * d_out:(e + 1) * r * d_out], [r], cfg.alpha,
                                        self.rts[e], b["dy"], b["dx"], b["dA"][e * r:(e + 1) * r],
                                        b["dB"][e * r * d_out:(e + 1) * r * d_out], input_mode=im,
-                                       ws=self.ws_bwd)
+                                       ws=self.ws_bwd, h_fwd=b["ws_fwd"][e])
 
 
 def make_buffers(cfg, rt, seed=0):

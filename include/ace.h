@@ -163,6 +163,10 @@ ace_status ace_grouped_lora_fwd(ace_dtype dtype, ace_input_mode input_mode, int3
 /*
  * Grouped LoRA backward: gradients of L = <dy, y_out> for the forward above
  * (Sec. 3.1.2 / 3.4: a shared adapter collects every routed pair of its group).
+ *   h_fwd       NULL, or the workspace of the forward call made with the same
+ *               arguments (it still holds h = (alpha/r_g) A_g x per row); the
+ *               backward then reads h from it instead of recomputing it.
+ *               Read only; must not be overwritten in between.
  *   dy          device [T*k, d_out], dtype.
  *   dx          device, shape of x, dtype: accumulated (+=).
  *   dA          device fp32 [R, d_in]: overwritten (a group with no rows gets 0).
@@ -176,8 +180,9 @@ ace_status ace_grouped_lora_bwd(ace_dtype dtype, ace_input_mode input_mode, int3
                                 int32_t k, int32_t d_in, int32_t d_out, int32_t G,
                                 const int32_t* group_rank, float alpha, const void* x,
                                 const void* A, const void* B, const float* pair_w,
-                                const ace_routing* rt, const void* dy, void* dx, float* dA,
-                                float* dB, void* ws, size_t ws_bytes, void* stream);
+                                const ace_routing* rt, const void* h_fwd, const void* dy,
+                                void* dx, float* dA, float* dB, void* ws, size_t ws_bytes,
+                                void* stream);
 
 /*
  * Expert-wise LoRA (Sec. 3.1), the baseline that grouped execution replaces:
@@ -195,8 +200,8 @@ ace_status ace_expertwise_lora_bwd(ace_dtype dtype, ace_input_mode input_mode, i
                                    int32_t k, int32_t d_in, int32_t d_out, int32_t E,
                                    int32_t rank, float alpha, const void* x, const void* A,
                                    const void* B, const float* pair_w, const ace_routing* rt,
-                                   const void* dy, void* dx, float* dA, float* dB, void* ws,
-                                   size_t ws_bytes, void* stream);
+                                   const void* h_fwd, const void* dy, void* dx, float* dA,
+                                   float* dB, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * Device scratch needed by an op (bytes, rounded up to 256).  n_keys and

@@ -47,7 +47,7 @@ _lib.ace_group_permute.argtypes = [_vp, _i32, _i32, _i32, _vp, _i32, _i32, _R, _
 _lib.ace_group_permute.restype = _i32
 _FWD = [_i32, _i32, _i32, _i32, _i32, _i32, _i32, _vp, _f32, _vp, _vp, _vp, _vp, _R, _vp, _vp, _sz, _vp]
 _BWD = [_i32, _i32, _i32, _i32, _i32, _i32, _i32, _vp, _f32, _vp, _vp, _vp, _vp, _R, _vp, _vp, _vp,
-        _vp, _vp, _sz, _vp]
+        _vp, _vp, _vp, _sz, _vp]
 _lib.ace_grouped_lora_fwd.argtypes = _FWD
 _lib.ace_grouped_lora_fwd.restype = _i32
 _lib.ace_grouped_lora_bwd.argtypes = _BWD
@@ -192,7 +192,9 @@ def ace_grouped_lora_fwd(x, A, B, group_rank: Sequence[int], alpha: float, routi
 
 def ace_grouped_lora_bwd(x, A, B, group_rank: Sequence[int], alpha: float, routing: Routing,
                          dy, dx, dA, dB, pair_w=None, input_mode: int = ACE_INPUT_SHARED,
-                         ws=None, stream=None) -> None:
+                         ws=None, stream=None, h_fwd=None) -> None:
+    """h_fwd: None, or the workspace of the forward call with the same arguments
+    (the backward then reuses the forward's h instead of recomputing it)."""
     T, k = routing.c.T, routing.c.k
     d_in, d_out = A.shape[1], dy.shape[1]
     ranks = _ranks_arg(group_rank)
@@ -201,8 +203,8 @@ def ace_grouped_lora_bwd(x, A, B, group_rank: Sequence[int], alpha: float, routi
         ws = torch.empty(max(need, 256), dtype=torch.uint8, device=A.device)
     _check(_lib.ace_grouped_lora_bwd(_dtype(A), input_mode, T, k, d_in, d_out, len(group_rank),
                                      ranks, alpha, _ptr(x), _ptr(A), _ptr(B), _ptr(pair_w),
-                                     ctypes.byref(routing.c), _ptr(dy), _ptr(dx), _ptr(dA),
-                                     _ptr(dB), _ptr(ws), ws.numel(), _stream(stream)),
+                                     ctypes.byref(routing.c), _ptr(h_fwd), _ptr(dy), _ptr(dx),
+                                     _ptr(dA), _ptr(dB), _ptr(ws), ws.numel(), _stream(stream)),
            "ace_grouped_lora_bwd")
 
 
@@ -221,7 +223,7 @@ def ace_expertwise_lora_fwd(x, A, B, E: int, rank: int, alpha: float, routing: R
 
 def ace_expertwise_lora_bwd(x, A, B, E: int, rank: int, alpha: float, routing: Routing, dy, dx,
                             dA, dB, pair_w=None, input_mode: int = ACE_INPUT_SHARED, ws=None,
-                            stream=None) -> None:
+                            stream=None, h_fwd=None) -> None:
     T, k = routing.c.T, routing.c.k
     d_in, d_out = A.shape[1], dy.shape[1]
     if ws is None:
@@ -229,8 +231,9 @@ def ace_expertwise_lora_bwd(x, A, B, E: int, rank: int, alpha: float, routing: R
         ws = torch.empty(max(need, 256), dtype=torch.uint8, device=A.device)
     _check(_lib.ace_expertwise_lora_bwd(_dtype(A), input_mode, T, k, d_in, d_out, E, rank, alpha,
                                         _ptr(x), _ptr(A), _ptr(B), _ptr(pair_w),
-                                        ctypes.byref(routing.c), _ptr(dy), _ptr(dx), _ptr(dA),
-                                        _ptr(dB), _ptr(ws), ws.numel(), _stream(stream)),
+                                        ctypes.byref(routing.c), _ptr(h_fwd), _ptr(dy), _ptr(dx),
+                                        _ptr(dA), _ptr(dB), _ptr(ws), ws.numel(),
+                                        _stream(stream)),
            "ace_expertwise_lora_bwd")
 
 

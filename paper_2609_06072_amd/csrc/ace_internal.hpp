@@ -23,6 +23,7 @@ struct Problem {
   const ace_routing* rt;
   KeyTable keys;   // ranks and rank offsets of the n_keys adapters
   int r_max;
+  const void* h_fwd = nullptr;  // backward: h per row from the forward workspace, or null
 };
 
 int permute_tokens_per_block(int k);

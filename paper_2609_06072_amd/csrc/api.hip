@@ -129,9 +129,12 @@ ace_status run_fwd(const Problem& p, void* y, void* ws, size_t ws_bytes, void* s
   return hip_status(launch_fwd(p, y, ws, static_cast<hipStream_t>(stream)), "forward launch");
 }
 
-ace_status run_bwd(const Problem& p, const void* dy, void* dx, float* dA, float* dB, void* ws,
-                   size_t ws_bytes, void* stream) {
+ace_status run_bwd(Problem& p, const void* h_fwd, const void* dy, void* dx, float* dA, float* dB,
+                   void* ws, size_t ws_bytes, void* stream) {
   if (p.T > 0 && (!dy || !dx)) return fail(ACE_ERR_INVALID_ARG, "dy or dx is NULL");
+  if (h_fwd && !aligned(h_fwd, 256))
+    return fail(ACE_ERR_INVALID_ARG, "h_fwd must be a forward workspace (256-byte aligned)");
+  p.h_fwd = h_fwd;
   if (!dA || !dB) return fail(ACE_ERR_INVALID_ARG, "dA or dB is NULL");
   if (!aligned(dy, 16) || !aligned(dx, 16))
     return fail(ACE_ERR_INVALID_ARG, "dy and dx must be 16-byte aligned");
@@ -219,13 +222,14 @@ ace_status ace_grouped_lora_bwd(ace_dtype dtype, ace_input_mode input_mode, int3
                                 int32_t k, int32_t d_in, int32_t d_out, int32_t G,
                                 const int32_t* group_rank, float alpha, const void* x,
                                 const void* A, const void* B, const float* pair_w,
-                                const ace_routing* rt, const void* dy, void* dx, float* dA,
-                                float* dB, void* ws, size_t ws_bytes, void* stream) {
+                                const ace_routing* rt, const void* h_fwd, const void* dy,
+                                void* dx, float* dA, float* dB, void* ws, size_t ws_bytes,
+                                void* stream) {
   Problem p;
   ace_status s = check_problem(p, dtype, input_mode, T, k, d_in, d_out, G, group_rank, 0, alpha,
                                x, A, B, pair_w, rt, false);
   if (s != ACE_OK) return s;
-  return run_bwd(p, dy, dx, dA, dB, ws, ws_bytes, stream);
+  return run_bwd(p, h_fwd, dy, dx, dA, dB, ws, ws_bytes, stream);
 }
 
 ace_status ace_expertwise_lora_fwd(ace_dtype dtype, ace_input_mode input_mode, int32_t T,
@@ -244,13 +248,13 @@ ace_status ace_expertwise_lora_bwd(ace_dtype dtype, ace_input_mode input_mode, i
                                    int32_t k, int32_t d_in, int32_t d_out, int32_t E,
                                    int32_t rank, float alpha, const void* x, const void* A,
                                    const void* B, const float* pair_w, const ace_routing* rt,
-                                   const void* dy, void* dx, float* dA, float* dB, void* ws,
-                                   size_t ws_bytes, void* stream) {
+                                   const void* h_fwd, const void* dy, void* dx, float* dA,
+                                   float* dB, void* ws, size_t ws_bytes, void* stream) {
   Problem p;
   ace_status s = check_problem(p, dtype, input_mode, T, k, d_in, d_out, E, nullptr, rank, alpha,
                                x, A, B, pair_w, rt, true);
   if (s != ACE_OK) return s;
-  return run_bwd(p, dy, dx, dA, dB, ws, ws_bytes, stream);
+  return run_bwd(p, h_fwd, dy, dx, dA, dB, ws, ws_bytes, stream);
 }
 
 size_t ace_workspace_bytes(ace_op op, int32_t T, int32_t k, int32_t d_in, int32_t d_out,

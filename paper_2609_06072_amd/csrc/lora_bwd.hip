@@ -12,7 +12,9 @@
 //                contiguous along its contraction index); zeroes the dense
 //                per-token dH buffer used for dx.
 //   contract  -- Hs per row (x against A), stored per key and per pair served
-//                as [r][pair position], times the pair's weight (Hw).
+//                as [r][pair position], times the pair's weight (Hw); when
+//                the forward's h is passed in, a copy kernel builds Hw from
+//                it instead.
 //   contract  -- dH per row (gathered G against B^T), stored per key as
 //                [r][u] and either as dense per-token rows (shared input) or
 //                row-major for the expand below (per-pair input).
@@ -130,6 +132,54 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
         dt[(size_t)(roff + r0 + e) * a.ldh + col] = v;
         df[r0 + e] = v;
       }
+  }
+}
+
+// Hw from the forward's h (h_u = s_q A_q x_u per row, row-major [U][rpad]):
+// Hw[roff + r][pair position - first pair of the key] = w_p h_u[r] for every
+// pair p the row serves -- what the Hs contract below would store.  Lane l of
+// wave w handles row 64b + l and the rank chunks w, w + 4, ...
+struct HwArgs {
+  const int32_t* offsets;
+  const int32_t* row_token;
+  const uint32_t* row_slots;
+  const int32_t* ppos;   // first pair position of each row, or null (one pair per row)
+  const float* pair_w;
+  const void* h;
+  int32_t rpad;
+  int32_t k;
+  void* Hw;
+  long ldh;
+  KeyTable keys;
+};
+
+template <typename T>
+__global__ __launch_bounds__(kThreads) void hw_from_h_kernel(HwArgs a) {
+  constexpr int PER = Tr<T>::PER;
+  __shared__ int seg[kMaxKeys + 1];
+  const int n_keys = a.keys.n_keys;
+  for (int i = threadIdx.x; i <= n_keys; i += kThreads) seg[i] = a.offsets[i];
+  __syncthreads();
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int u = blockIdx.x * 64 + lane;
+  if (u >= seg[n_keys]) return;
+  const int q = upper_index(seg, n_keys, u);
+  const int r_q = a.keys.rank[q], roff = a.keys.roff[q];
+  const int tok = a.row_token[u];
+  const uint32_t slots = a.row_slots[u];
+  const long col0 = a.ppos ? (long)a.ppos[u] - a.ppos[seg[q]] : (long)(u - seg[q]);
+  const T* src = static_cast<const T*>(a.h) + (size_t)u * a.rpad;
+  T* dst = static_cast<T*>(a.Hw);
+  for (int r0 = PER * wave; r0 < r_q; r0 += 4 * PER) {
+    float f[PER];
+    Tr<T>::to_f32(Tr<T>::load(src + r0), f);
+    long col = col0;
+    for (uint32_t mm = slots; mm; mm &= mm - 1u, ++col) {
+      const float w = a.pair_w ? a.pair_w[tok * a.k + __builtin_ctz(mm)] : 1.f;
+#pragma unroll
+      for (int e = 0; e < PER; ++e)
+        if (r0 + e < r_q) dst[(size_t)(roff + r0 + e) * a.ldh + col] = (T)(f[e] * w);
+    }
   }
 }
 
@@ -292,17 +342,36 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
   const bool multi = p.rt->mode == ACE_ROWS_GROUP_DEDUP;
   const int32_t* ppos = multi ? p.rt->row_pair : nullptr;
   const int32_t* plist = multi ? p.rt->pair_list : nullptr;
-  // Hw = w s A x, per key and pair [r][pair position]
-  c.src = p.x;
-  c.W = p.A;
-  c.ldw = p.d_in;
-  c.K = p.d_in;
-  c.src_mode = p.per_pair ? kSrcPerPair : kSrcShared;
+  // Hw = w s A x, per key and pair [r][pair position]: from the forward's h
+  // when the caller kept it, else recomputed
   c.pair_w = p.pair_w;
-  c.out_t = base + L.Ht;
-  c.out_t_pairs = 1;
-  c.ppos = ppos;
-  e = launch_contract(p.dtype, c, p.r_max, P, stream);
+  if (p.h_fwd) {
+    HwArgs hw{};
+    hw.offsets = p.rt->offsets;
+    hw.row_token = p.rt->row_token;
+    hw.row_slots = p.rt->row_slots;
+    hw.ppos = ppos;
+    hw.pair_w = p.pair_w;
+    hw.h = p.h_fwd;
+    hw.rpad = rpad;
+    hw.k = p.k;
+    hw.Hw = base + L.Ht;
+    hw.ldh = ldh;
+    hw.keys = p.keys;
+    const int blocks = (int)((P + 63) / 64);
+    if (blocks > 0) hw_from_h_kernel<T><<<blocks, kThreads, 0, stream>>>(hw);
+    e = hipGetLastError();
+  } else {
+    c.src = p.x;
+    c.W = p.A;
+    c.ldw = p.d_in;
+    c.K = p.d_in;
+    c.src_mode = p.per_pair ? kSrcPerPair : kSrcShared;
+    c.out_t = base + L.Ht;
+    c.out_t_pairs = 1;
+    c.ppos = ppos;
+    e = launch_contract(p.dtype, c, p.r_max, P, stream);
+  }
   if (e != hipSuccess) return e;
   // dH = s B^T G
   c.W = base + L.Bt;

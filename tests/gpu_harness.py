@@ -75,7 +75,10 @@ def make_case(cfg: W.MoEConfig, path: str, seed: int = 0, with_w: bool = False,
     return Case(cfg, rt, mode, im, ranks, e2g, n_keys, t.d_in, t.d_out, x, t.A, t.B, t.dy, pair_w)
 
 
-def run_gpu(c: Case, fwd: bool = True, bwd: bool = True, y_in=None, dx_in=None):
+def run_gpu(c: Case, fwd: bool = True, bwd: bool = True, y_in=None, dx_in=None,
+            reuse_h: bool = False):
+    """Forward and/or backward through the library; with reuse_h the
+    backward reads h from the forward's workspace (h_fwd)."""
     from paper_2609_06072_amd import ace
     dev = c.x.device
     ids = torch.from_numpy(c.rt.topk_ids).to(dev)
@@ -84,15 +87,20 @@ def run_gpu(c: Case, fwd: bool = True, bwd: bool = True, y_in=None, dx_in=None):
                                     c.rt.G, c.mode)
     out = {"routing": routing}
     P = c.cfg.P
+    fws = None
     if fwd:
         y = torch.zeros(P, c.d_out, dtype=c.x.dtype, device=dev) if y_in is None else y_in.clone()
+        need = ace.ace_workspace_bytes(ace.ACE_OP_FWD, c.cfg.T, c.cfg.k, c.d_in, c.d_out,
+                                       c.n_keys, max(c.ranks))
+        fws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
         if c.mode == W.ROWS_EXPERT:
             ace.ace_expertwise_lora_fwd(c.x, c.A, c.B, c.cfg.E, c.cfg.r_e, c.cfg.alpha, routing, y,
-                                        pair_w=c.pair_w, input_mode=c.input_mode)
+                                        pair_w=c.pair_w, input_mode=c.input_mode, ws=fws)
         else:
             ace.ace_grouped_lora_fwd(c.x, c.A, c.B, c.ranks, c.cfg.alpha, routing, y,
-                                     pair_w=c.pair_w, input_mode=c.input_mode)
+                                     pair_w=c.pair_w, input_mode=c.input_mode, ws=fws)
         out["y"] = y
+    h_fwd = fws if (reuse_h and fwd) else None
     if bwd:
         dx = torch.zeros_like(c.x) if dx_in is None else dx_in.clone()
         R = sum(c.ranks)
@@ -100,10 +108,11 @@ def run_gpu(c: Case, fwd: bool = True, bwd: bool = True, y_in=None, dx_in=None):
         dB = torch.full((R * c.d_out,), float("nan"), dtype=torch.float32, device=dev)
         if c.mode == W.ROWS_EXPERT:
             ace.ace_expertwise_lora_bwd(c.x, c.A, c.B, c.cfg.E, c.cfg.r_e, c.cfg.alpha, routing,
-                                        c.dy, dx, dA, dB, pair_w=c.pair_w, input_mode=c.input_mode)
+                                        c.dy, dx, dA, dB, pair_w=c.pair_w, input_mode=c.input_mode,
+                                        h_fwd=h_fwd)
         else:
             ace.ace_grouped_lora_bwd(c.x, c.A, c.B, c.ranks, c.cfg.alpha, routing, c.dy, dx, dA,
-                                     dB, pair_w=c.pair_w, input_mode=c.input_mode)
+                                     dB, pair_w=c.pair_w, input_mode=c.input_mode, h_fwd=h_fwd)
         out.update(dx=dx, dA=dA, dB=dB)
     torch.cuda.synchronize()
     return out

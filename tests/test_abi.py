@@ -123,8 +123,14 @@ def test_forward_backward_reject_bad_arguments(ace):
     assert st == ace.ACE_ERR_INVALID_ARG
     # backward: workspace checked before anything runs
     st = lib.ace_grouped_lora_bwd(ace.ACE_BF16, 0, 4, 2, 64, 32, 2, ranks, 16.0, p, p, p, None,
-                                  ctypes.byref(_routing(ace)), p, p, p, p, p, 16, None)
+                                  ctypes.byref(_routing(ace)), None, p, p, p, p, p, 16, None)
     assert st == ace.ACE_ERR_WORKSPACE
     st = lib.ace_grouped_lora_bwd(ace.ACE_BF16, 0, 4, 2, 64, 32, 2, ranks, 16.0, p, p, p, None,
-                                  ctypes.byref(_routing(ace)), p, p, None, p, p, 1 << 30, None)
+                                  ctypes.byref(_routing(ace)), None, p, p, None, p, p, 1 << 30,
+                                  None)
+    assert st == ace.ACE_ERR_INVALID_ARG
+    # h_fwd must be a forward workspace (256-byte aligned)
+    h_bad = ctypes.c_void_p(0x100010)
+    st = lib.ace_grouped_lora_bwd(ace.ACE_BF16, 0, 4, 2, 64, 32, 2, ranks, 16.0, p, p, p, None,
+                                  ctypes.byref(_routing(ace)), h_bad, p, p, p, p, p, 1 << 30, None)
     assert st == ace.ACE_ERR_INVALID_ARG

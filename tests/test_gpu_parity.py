@@ -123,6 +123,27 @@ def test_parity_small(name, path):
     check_rel("dB", f64(out["dB"]), dB, tol)
 
 
+@pytest.mark.parametrize("name", ["tiny_fp32", "olmoe_bf16", "mixtral_bf16"])
+@pytest.mark.parametrize("path", list(PATHS))
+def test_parity_small_h_reused(name, path):
+    """Backward that reads h from the forward's workspace: same gradients."""
+    cfg = SMALL[name]
+    c = make_case(cfg, path, seed=2, with_w=(path in ("grouped", "pairs_per_pair")))
+    say(f"parity (h reused) {name} {path} T={cfg.T} keys={c.n_keys}")
+    out = run_gpu(c, reuse_h=True)
+    tol = TOL[cfg.dtype]
+    dx, dA, dB = oracle_bwd(c)
+    check_rel("dx", f64(out["dx"]), dx, tol)
+    check_rel("dA", f64(out["dA"]), dA, tol)
+    check_rel("dB", f64(out["dB"]), dB, tol)
+    ref = run_gpu(c, fwd=False)
+    # only Hw differs (bf16: h rounded once more before the weight); dx and dA
+    # do not read it
+    assert torch.equal(out["dx"], ref["dx"]) and torch.equal(out["dA"], ref["dA"])
+    if cfg.dtype == "f32":
+        check_rel("dB vs recomputed h", f64(out["dB"]), f64(ref["dB"]), 1e-6)
+
+
 # ------------------------------------------------ full size, sampled checks
 
 def _sub_tokens(c, toks):
@@ -147,7 +168,7 @@ def test_parity_full_size_sampled(name, path):
         pytest.skip("this workload adapts the up projection only")
     c = make_case(cfg, path, seed=0)
     say(f"full-size {name} {path} T={cfg.T} d_in={c.d_in} d_out={c.d_out}")
-    out = run_gpu(c)
+    out = run_gpu(c, reuse_h=True)   # as timed: the backward reuses the forward's h
     tol = TOL[cfg.dtype]
     k = cfg.k
     rng = np.random.default_rng(123)
