@@ -20,6 +20,12 @@ What it follows (arXiv 2609.06072):
   * Appendix "Implementation Details": gate and up projections share the
     input x (grouped execution applies); the down projection takes the
     expert-specific h_e (one input row per routed pair).
+  * Down projection, pre-combined form: the layer output combines the expert
+    outputs linearly with p_e (Sec. 3.1), so the adapter part of the combined
+    output is sum_{g in A(t)} s_g B_g A_g (sum_{j: g(e_tj) = g} p_tj h_tj):
+    one input combination and one adapter evaluation per (token, active
+    group).  The paper keeps down expert-wise; this identity is a reading of
+    Sec. 3.1 and 3.5 together (its steps: precombined_delta).
 
 Readings where the paper is silent (each is restated in the design notes):
   * LoRA scale s = alpha / r for each adapter (alpha = 16, the paper's
@@ -47,6 +53,7 @@ ROWS_GROUP_PAIRS = 1
 ROWS_EXPERT = 2
 INPUT_SHARED = 0
 INPUT_PER_PAIR = 1
+INPUT_COMBINED = 2   # per-pair input, output combined per token: [T, d_out]
 
 
 # ---------------------------------------------------------------------------
@@ -183,7 +190,9 @@ def _inputs(x: np.ndarray, pairs: np.ndarray, k: int, input_mode: int) -> np.nda
 def lora_delta(x, A, B, ranks, alpha, topk_ids, E, expert_to_group, G,
                input_mode=INPUT_SHARED, pair_w=None) -> np.ndarray:
     """Delta[t*k + j] = w_tj * (alpha / r_q) * B_q (A_q xin(t, j)),  q = key of
-    the pair (g(e) for groups, e for experts).  Returns fp64 [T*k, d_out]."""
+    the pair (g(e) for groups, e for experts).  Returns fp64 [T*k, d_out]; with
+    INPUT_COMBINED (per-pair input) the per-token sum over the slots,
+    sum_j Delta[t*k + j], as fp64 [T, d_out]."""
     x = np.asarray(x, dtype=np.float64)
     T, k = topk_ids.shape
     n_keys = len(ranks)
@@ -200,6 +209,8 @@ def lora_delta(x, A, B, ranks, alpha, topk_ids, E, expert_to_group, G,
         h = xin @ As[q].T                 # h = A_q x          (Sec. 3.1.3)
         c = h @ Bs[q].T                   # Delta W_q x = B_q h
         out[pairs] = (w[pairs] * s)[:, None] * c
+    if input_mode == INPUT_COMBINED:
+        return out.reshape(T, k, d_out).sum(axis=1)
     return out
 
 
@@ -211,8 +222,9 @@ def lora_grads(x, A, B, ranks, alpha, topk_ids, E, expert_to_group, G, dy,
       dB_q  += c * dY h^T                 [d_out, r_q]
       dA_q  += c * (B_q^T dY) xin^T       [r_q, d_in]
       dxin  += c * A_q^T B_q^T dY         (shared input: summed over slots)
-    Only routed pairs contribute (Sec. 3.1.2).  Returns fp64 dx (shape of x),
-    dA [R, d_in] and dB packed like B.
+    Only routed pairs contribute (Sec. 3.1.2).  With INPUT_COMBINED, dY is the
+    gradient of the combined output [T, d_out], so every pair of token t sees
+    dY[t].  Returns fp64 dx (shape of x), dA [R, d_in] and dB packed like B.
     """
     x = np.asarray(x, dtype=np.float64)
     dy = np.asarray(dy, dtype=np.float64)
@@ -230,7 +242,8 @@ def lora_grads(x, A, B, ranks, alpha, topk_ids, E, expert_to_group, G, dy,
             continue
         c = (w[pairs] * (alpha / float(ranks[q])))[:, None]
         xin = _inputs(x, pairs, k, input_mode)
-        g = c * dy[pairs]                  # weighted output gradient per pair
+        dyp = dy[pairs // k] if input_mode == INPUT_COMBINED else dy[pairs]
+        g = c * dyp                        # weighted output gradient per pair
         h = xin @ As[q].T
         dBs[q] = g.T @ h
         dh = g @ Bs[q]
@@ -271,6 +284,31 @@ def grouped_execution_delta(x, A, B, ranks, alpha, topk_ids, E, expert_to_group,
     return out
 
 
+def precombined_delta(x, A, B, ranks, alpha, topk_ids, E, expert_to_group, G,
+                      pair_w=None) -> np.ndarray:
+    """Down projection with the combine moved in front of the adapter: for
+    every (token, active group) row, z = sum over its slots j of w_tj h_tj
+    (h = the per-pair input x[t*k + j]), then out[t] += s_g B_g (A_g z).
+    Returns fp64 [T, d_out]."""
+    x = np.asarray(x, dtype=np.float64)
+    T, k = topk_ids.shape
+    d_out = int(np.asarray(B).size // max(1, int(np.sum(ranks))))
+    As, Bs = unpack(A, B, ranks, d_out)
+    rt = permute(topk_ids, E, expert_to_group, G, ROWS_GROUP_DEDUP)
+    w = np.ones(T * k) if pair_w is None else np.asarray(pair_w, np.float64).reshape(-1)
+    out = np.zeros((T, d_out))
+    for g in range(G):
+        lo, hi = int(rt["offsets"][g]), int(rt["offsets"][g + 1])
+        for u in range(lo, hi):
+            t, m = int(rt["row_token"][u]), int(rt["row_slots"][u])
+            z = np.zeros(x.shape[1])
+            for j in range(k):
+                if (m >> j) & 1:
+                    z += w[t * k + j] * x[t * k + j]
+            out[t] += (alpha / float(ranks[g])) * (Bs[g] @ (As[g] @ z))
+    return out
+
+
 # ---------------------------------------------------------------------------
 # brute force: scalar Python loops straight from the definition (tiny inputs)
 # ---------------------------------------------------------------------------
@@ -284,7 +322,8 @@ def brute_delta(x, A, B, ranks, alpha, topk_ids, E, expert_to_group, G,
     off = [0]
     for r in ranks:
         off.append(off[-1] + int(r))
-    out = [[0.0] * d_out for _ in range(T * k)]
+    combined = input_mode == INPUT_COMBINED
+    out = [[0.0] * d_out for _ in range(T if combined else T * k)]
     for t in range(T):
         for j in range(k):
             e = int(topk_ids[t][j])
@@ -303,7 +342,10 @@ def brute_delta(x, A, B, ranks, alpha, topk_ids, E, expert_to_group, G,
                 acc = 0.0
                 for a in range(r):
                     acc += float(B[d_out * off[q] + n * r + a]) * h[a]
-                out[t * k + j][n] = w * s * acc
+                if combined:
+                    out[t][n] += w * s * acc
+                else:
+                    out[t * k + j][n] = w * s * acc
     return np.array(out, dtype=np.float64)
 
 
@@ -331,7 +373,7 @@ def brute_grads(x, A, B, ranks, alpha, topk_ids, E, expert_to_group, G, dy,
             xr = t if input_mode == INPUT_SHARED else t * k + j
             w = 1.0 if pair_w is None else float(pair_w[t][j])
             c = w * alpha / r
-            g = [float(v) for v in dy[t * k + j]]
+            g = [float(v) for v in dy[t if input_mode == INPUT_COMBINED else t * k + j]]
             h = [sum(float(A[off[q] + a][i]) * float(x[xr][i]) for i in range(d_in))
                  for a in range(r)]
             bg = [sum(float(B[d_out * off[q] + n * r + a]) * g[n] for n in range(d_out))

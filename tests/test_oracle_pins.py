@@ -95,7 +95,7 @@ def tiny_problem(seed, T=5, k=3, E=6, G=3, d_in=7, d_out=5, r_e=2, input_mode=O.
     x = rng.normal(size=(rows, d_in))
     A = rng.normal(size=(R, d_in))
     B = rng.normal(size=(d_out * R,))
-    dy = rng.normal(size=(T * k, d_out))
+    dy = rng.normal(size=(T if input_mode == O.INPUT_COMBINED else T * k, d_out))
     w = rng.uniform(0.1, 1.0, size=(T, k))
     return dict(x=x, A=A, B=B, ranks=ranks, ids=ids, E=E, e2g=e2g, n_keys=n_keys, dy=dy, w=w,
                 im=input_mode)
@@ -114,7 +114,7 @@ def grads(p, **kw):
 # ------------------------------------------------------------- brute force
 
 @pytest.mark.parametrize("seed", range(4))
-@pytest.mark.parametrize("im", [O.INPUT_SHARED, O.INPUT_PER_PAIR])
+@pytest.mark.parametrize("im", [O.INPUT_SHARED, O.INPUT_PER_PAIR, O.INPUT_COMBINED])
 @pytest.mark.parametrize("expert_keys", [False, True])
 def test_brute_force_matches(seed, im, expert_keys):
     p = tiny_problem(seed, input_mode=im, expert_keys=expert_keys, drop=(seed == 3))
@@ -137,6 +137,38 @@ def test_grouped_execution_equals_per_pair_definition(seed):
     a = (p["x"], p["A"], p["B"], p["ranks"], 16.0, p["ids"], p["E"], p["e2g"], p["n_keys"])
     for w in (None, p["w"]):
         assert O.rel_l2(O.grouped_execution_delta(*a, pair_w=w), fwd(p, pair_w=w)) < 1e-13
+
+
+def test_hand_combined():
+    """Pre-combined down projection, worked by hand (forward and backward)."""
+    g, c = GOLD["grouped"], GOLD["combined"]
+    ids = _np(g["topk_ids"], np.int64)
+    args = (_np(c["x"]), _np(g["A"]), _np(g["B"]), g["group_rank"], g["alpha"], ids,
+            g["E"], _np(g["expert_to_group"], np.int64), g["G"])
+    w = _np(c["pair_w"])
+    for d in (O.lora_delta(*args, input_mode=O.INPUT_COMBINED, pair_w=w),
+              O.precombined_delta(*args, pair_w=w),
+              O.brute_delta(*args, input_mode=O.INPUT_COMBINED, pair_w=w)):
+        assert np.array_equal(d, _np(c["out"]))
+    for fn in (O.lora_grads, O.brute_grads):
+        dx, dA, dB = fn(*args, _np(c["dy"]), input_mode=O.INPUT_COMBINED, pair_w=w)
+        assert np.array_equal(dx, _np(c["dx"]))
+        assert np.array_equal(dA, _np(c["dA"]))
+        assert np.array_equal(dB, _np(c["dB"]))
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_precombine_equals_per_pair_then_combine(seed):
+    """Combining the per-pair inputs before the group adapter (one evaluation
+    per active group) equals the per-pair down delta followed by the weighted
+    combine over the token's slots."""
+    p = tiny_problem(seed, T=9, k=4, E=8, G=3, input_mode=O.INPUT_PER_PAIR, drop=(seed == 2))
+    a = (p["x"], p["A"], p["B"], p["ranks"], 16.0, p["ids"], p["E"], p["e2g"], p["n_keys"])
+    T, k = p["ids"].shape
+    for w in (None, p["w"]):
+        per_pair = O.lora_delta(*a, input_mode=O.INPUT_PER_PAIR, pair_w=w)
+        combined = per_pair.reshape(T, k, -1).sum(axis=1)
+        assert O.rel_l2(O.precombined_delta(*a, pair_w=w), combined) < 1e-13
 
 
 # -------------------------------------------- G = E reduces to expert-wise
@@ -238,7 +270,7 @@ def test_concatenated_group_adapter_scale():
 
 # ------------------------------------------------ finite differences
 
-@pytest.mark.parametrize("im", [O.INPUT_SHARED, O.INPUT_PER_PAIR])
+@pytest.mark.parametrize("im", [O.INPUT_SHARED, O.INPUT_PER_PAIR, O.INPUT_COMBINED])
 def test_finite_differences(im):
     p = tiny_problem(4, T=4, k=2, E=4, G=2, d_in=3, d_out=4, r_e=1, input_mode=im)
     w = p["w"]
