@@ -48,6 +48,7 @@ class Proj:
         self.name, self.mode, self.im, self.ranks = name, mode, im, ranks
         self.x, self.A, self.B, self.dy, self.y, self.dx, self.dA, self.dB = x, A, B, dy, y, dx, dA, dB
         self.ws_fwd = None  # the forward's workspace; the backward reads h from it
+        self.pair_w = None  # routing weights (the pre-combined down projection sums with them)
 
 
 class Path:
@@ -68,7 +69,12 @@ class Path:
             "lora": (ace.ACE_ROWS_EXPERT, ace.ACE_ROWS_EXPERT),
             "consolidated": (ace.ACE_ROWS_GROUP_PAIRS, ace.ACE_ROWS_EXPERT),
             "consolidated_down": (ace.ACE_ROWS_GROUP_DEDUP, ace.ACE_ROWS_GROUP_PAIRS),
+            "combined_down": (ace.ACE_ROWS_GROUP_DEDUP, ace.ACE_ROWS_GROUP_DEDUP),
+            "combined_down_expertwise": (ace.ACE_ROWS_EXPERT, ace.ACE_ROWS_EXPERT),
         }[kind]
+        # the down projection with its output combined per token (per-pair
+        # input, y and dy [T, d_out]) in the combined_down rows
+        combine = kind.startswith("combined_down")
         self.projs = []
         modes = set()
         for proj in cfg.projections:
@@ -78,8 +84,14 @@ class Path:
             grouped = mode != ace.ACE_ROWS_EXPERT
             ranks = [int(r) for r in rt.group_rank] if grouped else [cfg.r_e] * cfg.E
             b = bufs[proj]
-            pj = Proj(proj, mode, im, ranks, b["x"], b["A"], b["B"], b["dy"], b["y"], b["dx"],
-                      b["dA"], b["dB"])
+            y, dy = b["y"], b["dy"]
+            if combine and im == W.INPUT_PER_PAIR:
+                im = W.INPUT_COMBINED
+                y, dy = b["y_tok"], b["dy"][:cfg.T]
+            pj = Proj(proj, mode, im, ranks, b["x"], b["A"], b["B"], dy, y, b["dx"], b["dA"],
+                      b["dB"])
+            if im == W.INPUT_COMBINED:
+                pj.pair_w = torch.from_numpy(rt.topk_w).to(dev)
             need = ace.ace_workspace_bytes(ace.ACE_OP_FWD, cfg.T, cfg.k, d_in, d_out, len(ranks),
                                            max(ranks))
             pj.ws_fwd = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
@@ -93,21 +105,22 @@ class Path:
         a = self.ace
         if p.mode == a.ACE_ROWS_EXPERT:
             a.ace_expertwise_lora_fwd(p.x, p.A, p.B, self.cfg.E, self.cfg.r_e, self.cfg.alpha,
-                                      self.rts[p.mode], p.y, input_mode=p.im, ws=p.ws_fwd)
+                                      self.rts[p.mode], p.y, pair_w=p.pair_w, input_mode=p.im,
+                                      ws=p.ws_fwd)
         else:
             a.ace_grouped_lora_fwd(p.x, p.A, p.B, p.ranks, self.cfg.alpha, self.rts[p.mode], p.y,
-                                   input_mode=p.im, ws=p.ws_fwd)
+                                   pair_w=p.pair_w, input_mode=p.im, ws=p.ws_fwd)
 
     def _bwd(self, p):
         a = self.ace
         if p.mode == a.ACE_ROWS_EXPERT:
             a.ace_expertwise_lora_bwd(p.x, p.A, p.B, self.cfg.E, self.cfg.r_e, self.cfg.alpha,
-                                      self.rts[p.mode], p.dy, p.dx, p.dA, p.dB, input_mode=p.im,
-                                      ws=self.ws_bwd, h_fwd=p.ws_fwd)
+                                      self.rts[p.mode], p.dy, p.dx, p.dA, p.dB, pair_w=p.pair_w,
+                                      input_mode=p.im, ws=self.ws_bwd, h_fwd=p.ws_fwd)
         else:
             a.ace_grouped_lora_bwd(p.x, p.A, p.B, p.ranks, self.cfg.alpha, self.rts[p.mode], p.dy,
-                                   p.dx, p.dA, p.dB, input_mode=p.im, ws=self.ws_bwd,
-                                   h_fwd=p.ws_fwd)
+                                   p.dx, p.dA, p.dB, pair_w=p.pair_w, input_mode=p.im,
+                                   ws=self.ws_bwd, h_fwd=p.ws_fwd)
 
     def _timed(self, key, fn, *args):
         import torch
@@ -206,6 +219,7 @@ def make_buffers(cfg, rt, seed=0):
             dx = torch.zeros_like(t.x)
         bufs[proj] = dict(x=t.x, A=t.A, B=t.B, dy=t.dy,
                           y=torch.zeros(cfg.P, t.d_out, dtype=dt, device="cuda"), dx=dx,
+                          y_tok=torch.zeros(cfg.T, t.d_out, dtype=dt, device="cuda"),
                           dA=torch.zeros(R, t.d_in, dtype=torch.float32, device="cuda"),
                           dB=torch.zeros(R * t.d_out, dtype=torch.float32, device="cuda"))
     # gate and up read the same token activations
@@ -545,7 +559,9 @@ def main():
             need = max(need, ace.ace_workspace_bytes(ace.ACE_OP_BWD, cfg.T, cfg.k, d_in, d_out, nk, r))
     ws_bwd = torch.empty(need, dtype=torch.uint8, device="cuda")
 
-    kinds = ("ace", "lora") if args.no_extras else ("ace", "lora", "consolidated", "consolidated_down")
+    kinds = ("ace", "lora") if args.no_extras else (
+        "ace", "lora", "consolidated", "consolidated_down", "combined_down",
+        "combined_down_expertwise")
     paths = {kind: Path(ace, cfg, rt, kind, bufs, ws_perm, ws_bwd) for kind in kinds}
     if args.traffic_pass:
         traffic_pass(paths, args.traffic_pass)
@@ -630,6 +646,12 @@ def main():
                                             "(no compute-once), expert-wise down",
                             "consolidated_down": "ace step with the down projection at group "
                                                  "rank over pair rows",
+                            "combined_down": "ace step with the down projection pre-combined: "
+                                             "output summed per token with the routing weights, "
+                                             "one group-rank row per (token, active group)",
+                            "combined_down_expertwise": "expert-wise step with the down "
+                                                        "projection's output summed per token "
+                                                        "(expert rows, expert rank)",
                             "expertwise_per_expert_launch": "expert-wise LoRA with one permutation "
                                                             "and one fwd/bwd call per expert (the "
                                                             "baseline's launch pattern)"}[kind]}

@@ -46,7 +46,8 @@
  *   y[t*k + j, :] += w[t, j] * s_q * B_q (A_q xin(t, j))   for every routed
  *   pair (t, j) with q = the key of expert topk_ids[t, j];
  *   xin(t, j) = x[t] (ACE_INPUT_SHARED) or x[t*k + j] (ACE_INPUT_PER_PAIR);
- *   w = 1 when pair_w is NULL.
+ *   w = 1 when pair_w is NULL.  With ACE_INPUT_COMBINED the same sum lands in
+ *   y[t, :] (input x[t*k + j]), see ace_input_mode.
  */
 #ifndef ACE_H_
 #define ACE_H_
@@ -80,7 +81,16 @@ typedef enum {
 
 typedef enum {
   ACE_INPUT_SHARED = 0,   /* x is [T, d_in]; every routed expert sees x[t]        */
-  ACE_INPUT_PER_PAIR = 1  /* x is [T*k, d_in]; pair (t,j) has its own row t*k+j   */
+  ACE_INPUT_PER_PAIR = 1, /* x is [T*k, d_in]; pair (t,j) has its own row t*k+j   */
+  /* x is [T*k, d_in] as for ACE_INPUT_PER_PAIR, but the output is combined per
+     token with the routing weights: y is [T, d_out] and
+       y[t] += sum_j w[t, j] * s_q * B_q (A_q x[t*k + j]).
+     This is the down projection of an MoE layer whose expert outputs are
+     summed with the weights p_e (Sec. 3.1): since that sum is linear, a
+     (token, group) row evaluates its adapter once on the weighted sum of its
+     pairs' inputs (Sec. 3.5 applied to the down projection).  dy and dx of
+     the backward are [T, d_out] and [T*k, d_in].                              */
+  ACE_INPUT_COMBINED = 2
 } ace_input_mode;
 
 typedef enum {
@@ -141,17 +151,22 @@ ace_status ace_group_permute(const int32_t* topk_ids, int32_t T, int32_t k, int3
  * Grouped LoRA forward (Sec. 3.4 output, Sec. 3.5 execution).
  *   group_rank  host int32 [G]: r_g, the consolidated rank of each group.
  *   alpha       LoRA scaling numerator (s_g = alpha / r_g).
- *   x           device [T, d_in] (shared) or [T*k, d_in] (per pair), dtype.
+ *   x           device [T, d_in] (shared) or [T*k, d_in] (per pair, combined), dtype.
  *   A, B        device, packed as described at the top, dtype.
  *   pair_w      device fp32 [T, k] or NULL (weight 1).
  *   rt          rows from ace_group_permute in ACE_ROWS_GROUP_DEDUP (requires
- *               ACE_INPUT_SHARED) or ACE_ROWS_GROUP_PAIRS mode, with n_keys == G.
- *   y           device [T*k, d_out], dtype: accumulated (+=).
+ *               ACE_INPUT_SHARED or ACE_INPUT_COMBINED) or ACE_ROWS_GROUP_PAIRS
+ *               mode, with n_keys == G.
+ *   y           device [T*k, d_out] ([T, d_out] for ACE_INPUT_COMBINED), dtype:
+ *               accumulated (+=).
  *   ws          device scratch of at least
  *               ace_workspace_bytes(ACE_OP_FWD, T, k, d_in, d_out, G, max r_g)
- *               (it holds h = (alpha/r_g) A_g x per row); no initialisation.
+ *               (it holds h = (alpha/r_g) A_g x per row, per routed pair for
+ *               ACE_INPUT_COMBINED); no initialisation.
  * Two launches: the shrink h once per row of the permutation, then the
- * expand B_g h added into every slot the row serves.
+ * expand B_g h added into every slot the row serves.  ACE_INPUT_COMBINED:
+ * h per routed pair, its weighted sum per row into dense per-token rows
+ * [T, R], and y += those rows times B^T (a GEMM over K = R).
  */
 ace_status ace_grouped_lora_fwd(ace_dtype dtype, ace_input_mode input_mode, int32_t T,
                                 int32_t k, int32_t d_in, int32_t d_out, int32_t G,
@@ -167,7 +182,7 @@ ace_status ace_grouped_lora_fwd(ace_dtype dtype, ace_input_mode input_mode, int3
  *               arguments (it still holds h = (alpha/r_g) A_g x per row); the
  *               backward then reads h from it instead of recomputing it.
  *               Read only; must not be overwritten in between.
- *   dy          device [T*k, d_out], dtype.
+ *   dy          device [T*k, d_out] ([T, d_out] for ACE_INPUT_COMBINED), dtype.
  *   dx          device, shape of x, dtype: accumulated (+=).
  *   dA          device fp32 [R, d_in]: overwritten (a group with no rows gets 0).
  *   dB          device fp32, layout of B: overwritten.

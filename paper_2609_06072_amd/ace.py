@@ -24,7 +24,7 @@ _lib = ctypes.CDLL(LIB_PATH)
 ACE_OK, ACE_ERR_INVALID_ARG, ACE_ERR_UNSUPPORTED, ACE_ERR_WORKSPACE, ACE_ERR_HIP = 0, -1, -2, -3, -4
 ACE_F32, ACE_BF16 = 0, 1
 ACE_ROWS_GROUP_DEDUP, ACE_ROWS_GROUP_PAIRS, ACE_ROWS_EXPERT = 0, 1, 2
-ACE_INPUT_SHARED, ACE_INPUT_PER_PAIR = 0, 1
+ACE_INPUT_SHARED, ACE_INPUT_PER_PAIR, ACE_INPUT_COMBINED = 0, 1, 2
 ACE_OP_PERMUTE, ACE_OP_FWD, ACE_OP_BWD = 0, 1, 2
 
 EXPORTS = ("ace_group_permute", "ace_grouped_lora_fwd", "ace_grouped_lora_bwd",

@@ -13,7 +13,8 @@ namespace ace {
 // One adapted projection as the kernels see it.
 struct Problem {
   int dtype;       // ACE_F32 / ACE_BF16
-  int per_pair;    // input mode
+  int per_pair;    // ACE_INPUT_PER_PAIR
+  int combined;    // ACE_INPUT_COMBINED: per-pair input, output combined per token
   int T, k, d_in, d_out;
   float alpha;
   const void* x;
@@ -85,6 +86,25 @@ hipError_t launch_expand(int dtype, const ExpandArgs& a, int r_max, long P, hipS
 size_t fwd_ws_bytes(int T, int k, int r_max);
 hipError_t launch_fwd(const Problem& p, void* y, void* ws, hipStream_t stream);
 
+// Backward helpers shared with the pre-combined mode.
+//   prep: A^T [d_in][R] into At and B_q^T rows [R][d_out] into Bt (each
+//         skipped when null), and zero_bytes of zeros at `zero` (16-byte
+//         multiple inside a 256-byte padded region).
+//   combine: h_u = sum over the pairs of row u of w_p hp[pos] (hp row-major
+//         [P][rpad] per pair position), written to Ht [R][ldh] (column
+//         u - offsets[q]) and/or Hd [T][R] (dense per token); either may be null.
+hipError_t launch_prep(const Problem& p, void* At, void* Bt, void* zero, long zero_bytes,
+                       hipStream_t stream);
+hipError_t launch_combine(const Problem& p, const void* hp, int rpad, void* Ht, long ldh,
+                          void* Hd, hipStream_t stream);
+
+// Pre-combined input mode (ACE_INPUT_COMBINED).
+size_t fwd_combined_ws_bytes(int T, int k, int d_out, int n_keys, int r_max);
+size_t bwd_combined_ws_bytes(int T, int k, int d_in, int d_out, int n_keys, int r_max);
+hipError_t launch_fwd_combined(const Problem& p, void* y, void* ws, hipStream_t stream);
+hipError_t launch_bwd_combined(const Problem& p, const void* dy, void* dx, float* dA, float* dB,
+                               void* ws, hipStream_t stream);
+
 // Weight gradients dB_q = sum_p dY[p] Hw_p^T over the pairs of key q and
 // dA_q = sum_u dH_u x_u^T over its rows (split over chunks, reduced in order).
 struct GradArgs {
@@ -103,6 +123,9 @@ struct GradArgs {
   const int32_t* ppos;        // [U+1] first pair position of each row, or null (one pair per row)
   const int32_t* plist;       // [P] pair (t*k + j) at each position, or null
   int32_t k, d_in, d_out, per_pair;
+  int32_t combined;           // pre-combined input mode: dB runs over the rows (dy row =
+                              //   token, Hw = h per row), dA over the pairs (x row = plist,
+                              //   dHt = w dH per pair position)
   int32_t nbB, nbA;           // column blocks of dB / dA (set by the launcher)
   KeyTable keys;
 };

@@ -47,7 +47,7 @@ ace_status check_problem(Problem& p, ace_dtype dtype, ace_input_mode im, int32_t
                          const void* B, const float* pair_w, const ace_routing* rt,
                          bool expertwise) {
   if (dtype != ACE_F32 && dtype != ACE_BF16) return fail(ACE_ERR_INVALID_ARG, "unknown dtype %d", (int)dtype);
-  if (im != ACE_INPUT_SHARED && im != ACE_INPUT_PER_PAIR)
+  if (im != ACE_INPUT_SHARED && im != ACE_INPUT_PER_PAIR && im != ACE_INPUT_COMBINED)
     return fail(ACE_ERR_INVALID_ARG, "unknown input mode %d", (int)im);
   if (T < 0) return fail(ACE_ERR_INVALID_ARG, "T = %d < 0", T);
   if (k < 1 || k > kMaxK) return fail(ACE_ERR_UNSUPPORTED, "k = %d outside [1, %d]", k, kMaxK);
@@ -76,8 +76,9 @@ ace_status check_problem(Problem& p, ace_dtype dtype, ace_input_mode im, int32_t
       return fail(ACE_ERR_INVALID_ARG, "expert-wise calls need ACE_ROWS_EXPERT routing");
   } else {
     if (rt->mode == ACE_ROWS_GROUP_DEDUP) {
-      if (im != ACE_INPUT_SHARED)
-        return fail(ACE_ERR_INVALID_ARG, "ACE_ROWS_GROUP_DEDUP needs ACE_INPUT_SHARED");
+      if (im == ACE_INPUT_PER_PAIR)
+        return fail(ACE_ERR_INVALID_ARG,
+                    "ACE_ROWS_GROUP_DEDUP needs ACE_INPUT_SHARED or ACE_INPUT_COMBINED");
     } else if (rt->mode != ACE_ROWS_GROUP_PAIRS) {
       return fail(ACE_ERR_INVALID_ARG, "grouped calls need group-keyed routing");
     }
@@ -104,6 +105,7 @@ ace_status check_problem(Problem& p, ace_dtype dtype, ace_input_mode im, int32_t
   p.r_max = rmax;
   p.dtype = dtype;
   p.per_pair = im == ACE_INPUT_PER_PAIR;
+  p.combined = im == ACE_INPUT_COMBINED;
   p.T = T;
   p.k = k;
   p.d_in = d_in;
@@ -120,13 +122,17 @@ ace_status check_problem(Problem& p, ace_dtype dtype, ace_input_mode im, int32_t
 ace_status run_fwd(const Problem& p, void* y, void* ws, size_t ws_bytes, void* stream) {
   if (p.T > 0 && !y) return fail(ACE_ERR_INVALID_ARG, "y is NULL");
   if (!aligned(y, 16)) return fail(ACE_ERR_INVALID_ARG, "y must be 16-byte aligned");
-  const size_t need = fwd_ws_bytes(p.T, p.k, p.r_max);
+  const size_t need = p.combined
+                          ? fwd_combined_ws_bytes(p.T, p.k, p.d_out, p.keys.n_keys, p.r_max)
+                          : fwd_ws_bytes(p.T, p.k, p.r_max);
   if (need > 0 && (!ws || ws_bytes < need))
     return fail(ACE_ERR_WORKSPACE, "forward needs %zu workspace bytes, got %zu", need,
                 ws ? ws_bytes : (size_t)0);
   if (!aligned(ws, 256)) return fail(ACE_ERR_WORKSPACE, "workspace must be 256-byte aligned");
   if (p.T == 0) return ok();
-  return hip_status(launch_fwd(p, y, ws, static_cast<hipStream_t>(stream)), "forward launch");
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  return hip_status(p.combined ? launch_fwd_combined(p, y, ws, st) : launch_fwd(p, y, ws, st),
+                    "forward launch");
 }
 
 ace_status run_bwd(Problem& p, const void* h_fwd, const void* dy, void* dx, float* dA, float* dB,
@@ -139,12 +145,16 @@ ace_status run_bwd(Problem& p, const void* h_fwd, const void* dy, void* dx, floa
   if (!aligned(dy, 16) || !aligned(dx, 16))
     return fail(ACE_ERR_INVALID_ARG, "dy and dx must be 16-byte aligned");
   if (!aligned(dA, 4) || !aligned(dB, 4)) return fail(ACE_ERR_INVALID_ARG, "dA/dB misaligned");
-  const size_t need = bwd_ws_bytes(p.T, p.k, p.d_in, p.d_out, p.keys.n_keys, p.keys.R, p.r_max);
+  const size_t need =
+      p.combined ? bwd_combined_ws_bytes(p.T, p.k, p.d_in, p.d_out, p.keys.n_keys, p.r_max)
+                 : bwd_ws_bytes(p.T, p.k, p.d_in, p.d_out, p.keys.n_keys, p.keys.R, p.r_max);
   if (!ws || ws_bytes < need)
     return fail(ACE_ERR_WORKSPACE, "backward needs %zu workspace bytes, got %zu", need,
                 ws ? ws_bytes : (size_t)0);
   if (!aligned(ws, 256)) return fail(ACE_ERR_WORKSPACE, "workspace must be 256-byte aligned");
-  return hip_status(launch_bwd(p, dy, dx, dA, dB, ws, static_cast<hipStream_t>(stream)),
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  return hip_status(p.combined ? launch_bwd_combined(p, dy, dx, dA, dB, ws, st)
+                               : launch_bwd(p, dy, dx, dA, dB, ws, st),
                     "backward launch");
 }
 
@@ -271,13 +281,22 @@ size_t ace_workspace_bytes(ace_op op, int32_t T, int32_t k, int32_t d_in, int32_
         fail(ACE_ERR_INVALID_ARG, "invalid workspace query");
         return (size_t)-1;
       }
-      return round256(fwd_ws_bytes(T, k, r_max));
+      {
+        // covers every input mode (the pre-combined one also needs d_out)
+        const size_t a = fwd_ws_bytes(T, k, r_max);
+        const size_t b = fwd_combined_ws_bytes(T, k, d_out > 0 ? d_out : 0, n_keys, r_max);
+        return round256(a > b ? a : b);
+      }
     case ACE_OP_BWD:
       if (d_in < 1 || d_out < 1 || r_max < 1 || r_max > kMaxRank) {
         fail(ACE_ERR_INVALID_ARG, "invalid workspace query");
         return (size_t)-1;
       }
-      return round256(bwd_ws_bytes(T, k, d_in, d_out, n_keys, n_keys * r_max, r_max));
+      {
+        const size_t a = bwd_ws_bytes(T, k, d_in, d_out, n_keys, n_keys * r_max, r_max);
+        const size_t b = bwd_combined_ws_bytes(T, k, d_in, d_out, n_keys, r_max);
+        return round256(a > b ? a : b);
+      }
   }
   fail(ACE_ERR_INVALID_ARG, "unknown op %d", (int)op);
   return (size_t)-1;

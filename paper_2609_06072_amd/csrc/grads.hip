@@ -6,6 +6,9 @@
 //                p, times the pair's weight)
 //   dA_q[r][c] = sum_u dH_u[r] x_u[c]      over the rows u of key q
 //   dx[t][c]  += sum_K dHdense[t][K] A^T[c][K mod R]   (shared input only)
+// In the pre-combined mode (per-pair input, output combined per token) the
+// roles swap: dB_q = sum_u dY[t_u] h_u^T over the rows (h_u = the row's
+// combined h) and dA_q = sum_p (w_p dH_{u(p)}) x_p^T over the pairs.
 // Both weight gradients are gathered-row GEMMs: a list of rows of a large
 // row-major operand L (dY or x) against a small operand S that is contiguous
 // along the contraction index (Hw or dH, stored per key as [r][position]).
@@ -35,13 +38,15 @@ namespace {
 constexpr int kColBlk = 128;     // gradient columns per item
 constexpr int kSplitRows = 1024; // contraction indices per item (split-K chunk)
 
-// Item table shared by the gradient kernels.  For key q: rows seg[q] ..
-// seg[q+1], pairs pseg[q] .. pseg[q+1] (positions in pair order; = rows when
-// every row serves one pair).  Items of q: nsB(q) * nbB dB items, then
-// nsA(q) * nbA dA items, ns = max(1, ceil(count / kSplitRows)).
+// Item table shared by the gradient kernels.  For key q the dB contraction
+// runs over bseg[q] .. bseg[q+1] and the dA contraction over aseg[q] ..
+// aseg[q+1]: pairs (positions in pair order; = rows when every row serves one
+// pair) and rows respectively, swapped in the pre-combined mode.  Items of q:
+// nsB(q) * nbB dB items, then nsA(q) * nbA dA items,
+// ns = max(1, ceil(count / kSplitRows)).
 struct GradTable {
-  int seg[kMaxKeys + 1];
-  int pseg[kMaxKeys + 1];
+  int bseg[kMaxKeys + 1];
+  int aseg[kMaxKeys + 1];
   int istart[kMaxKeys + 1];
 };
 
@@ -52,13 +57,14 @@ __device__ inline void build_grad_table(const GradArgs& a, GradTable& tb, int* s
   const int n_keys = a.keys.n_keys;
   for (int i = t; i <= n_keys; i += kThreads) {
     const int o = a.offsets[i];
-    tb.seg[i] = o;
-    tb.pseg[i] = a.ppos ? a.ppos[o] : o;
+    const int po = a.ppos ? a.ppos[o] : o;
+    tb.bseg[i] = a.combined ? o : po;
+    tb.aseg[i] = a.combined ? po : o;
   }
   __syncthreads();
   int items = 0;
   if (t < n_keys)
-    items = n_split(tb.pseg[t + 1] - tb.pseg[t]) * a.nbB + n_split(tb.seg[t + 1] - tb.seg[t]) * a.nbA;
+    items = n_split(tb.bseg[t + 1] - tb.bseg[t]) * a.nbB + n_split(tb.aseg[t + 1] - tb.aseg[t]) * a.nbA;
   int total;
   const int ex = block_exclusive_scan(items, scan_lds, &total);
   if (t < n_keys) tb.istart[t] = ex;
@@ -79,7 +85,7 @@ __device__ inline Item decode_item(const GradArgs& a, const GradTable& tb, int i
   const int n_keys = a.keys.n_keys;
   it.q = upper_index(tb.istart, n_keys, item);
   int local = item - tb.istart[it.q];
-  const int npB = tb.pseg[it.q + 1] - tb.pseg[it.q];
+  const int npB = tb.bseg[it.q + 1] - tb.bseg[it.q];
   const int nsB = n_split(npB);
   it.isB = local < nsB * a.nbB;
   int cnt;
@@ -87,15 +93,15 @@ __device__ inline Item decode_item(const GradArgs& a, const GradTable& tb, int i
     it.s = local / a.nbB;
     it.cb = local % a.nbB;
     it.ns = nsB;
-    it.kbase = tb.pseg[it.q];
+    it.kbase = tb.bseg[it.q];
     cnt = npB;
   } else {
     local -= nsB * a.nbB;
     it.s = local / a.nbA;
     it.cb = local % a.nbA;
-    cnt = tb.seg[it.q + 1] - tb.seg[it.q];
+    cnt = tb.aseg[it.q + 1] - tb.aseg[it.q];
     it.ns = n_split(cnt);
-    it.kbase = tb.seg[it.q];
+    it.kbase = tb.aseg[it.q];
   }
   it.k0 = it.s * kSplitRows;
   it.nk = max(0, min(cnt - it.k0, kSplitRows));
@@ -104,6 +110,7 @@ __device__ inline Item decode_item(const GradArgs& a, const GradTable& tb, int i
 
 // Row of the large operand for contraction index kabs of an item.
 __device__ inline int l_row(const GradArgs& a, bool isB, int kabs) {
+  if (a.combined) return isB ? a.row_token[kabs] : a.plist[kabs];
   if (isB) {
     if (a.plist) return a.plist[kabs];
     return a.row_token[kabs] * a.k + (__builtin_ctz(a.row_slots[kabs] | 0x80000000u) & 31);
@@ -210,7 +217,10 @@ __device__ inline void load_rows(const GradArgs& a, const Item& it, int* idx) {
 #pragma unroll
   for (int i = 0; i < MPT; ++i)
     kabs[i] = it.kbase + it.k0 + min((int)threadIdx.x + i * kThreads, it.nk - 1);
-  if (ISB && a.plist) {
+  if (a.combined) {   // dB rows: dY of the row's token; dA rows: x of the pair
+#pragma unroll
+    for (int i = 0; i < MPT; ++i) v[i] = ISB ? a.row_token[kabs[i]] : a.plist[kabs[i]];
+  } else if (ISB && a.plist) {
 #pragma unroll
     for (int i = 0; i < MPT; ++i) v[i] = a.plist[kabs[i]];
   } else {
@@ -394,7 +404,7 @@ __global__ __launch_bounds__(kThreads) void grad_reg_kernel(GradArgs a) {
     const int ncol = ldl;
     const float* S = static_cast<const float*>(it.isB ? a.Hw : a.dHt);
     const int col0 = it.cb * kColBlk;
-    const long scol0 = (long)it.kbase - (it.isB ? tb.pseg[q] : tb.seg[q]) + it.k0;
+    const long scol0 = it.k0;   // S columns count from the key's first index
     const long hmax = a.ldh - PER;
     const int nst = (it.nk + RPS - 1) / RPS;
 
@@ -482,8 +492,8 @@ __global__ __launch_bounds__(kThreads) void grad_reduce_kernel(GradArgs a) {
   const int q = blockIdx.x / nb, rem = blockIdx.x % nb;
   const bool isB = rem < a.nbB;
   const int cb = isB ? rem : rem - a.nbB;
-  const int nsB = n_split(tb.pseg[q + 1] - tb.pseg[q]);
-  const int ns = isB ? nsB : n_split(tb.seg[q + 1] - tb.seg[q]);
+  const int nsB = n_split(tb.bseg[q + 1] - tb.bseg[q]);
+  const int ns = isB ? nsB : n_split(tb.aseg[q + 1] - tb.aseg[q]);
   if (ns == 1) return;  // written directly by the gradient kernel
   const int first = tb.istart[q] + (isB ? cb : nsB * a.nbB + cb);
   const int step = isB ? a.nbB : a.nbA;

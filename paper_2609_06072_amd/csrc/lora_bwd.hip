@@ -62,10 +62,11 @@ WsLayout ws_layout(int T, int k, int d_in, int d_out, int n_keys, int R, int r_m
   return w;
 }
 
-// dH of a row serving several pairs: dH_u = sum_i w_{p_i} dHp[ppos[u] + i]
+// Sum over the pairs of a row: dH_u = sum_i w_{p_i} dHp[ppos[u] + i]
 // (dHp = s B^T dY per pair position, row-major [P][rpad]); written per key as
-// [r][u - offsets[q]] for the weight gradient and as dense per-token rows for
-// the dx GEMM.  One thread per row.
+// [r][u - offsets[q]] for the weight gradient and/or as dense per-token rows
+// for the dx GEMM (either output may be null).  The pre-combined mode uses
+// the same sum for h_u = sum_i w_{p_i} h_{p_i}.
 struct CombineArgs {
   const int32_t* offsets;
   const int32_t* row_token;
@@ -110,7 +111,7 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
   }
   const T* src = static_cast<const T*>(a.dHp);
   T* dt = static_cast<T*>(a.dHt);
-  T* df = static_cast<T*>(a.dHf) + (size_t)tok * R + roff;
+  T* df = a.dHf ? static_cast<T*>(a.dHf) + (size_t)tok * R + roff : nullptr;
   for (int r0 = PER * wave; r0 < r_q; r0 += 4 * PER) {
     float f0[PER], f1[PER];
     Tr<T>::to_f32(Tr<T>::load(src + (size_t)p0 * a.rpad + r0), f0);
@@ -129,8 +130,8 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
     for (int e = 0; e < PER; ++e)
       if (r0 + e < r_q) {
         const T v = (T)acc[e];
-        dt[(size_t)(roff + r0 + e) * a.ldh + col] = v;
-        df[r0 + e] = v;
+        if (dt) dt[(size_t)(roff + r0 + e) * a.ldh + col] = v;
+        if (df) df[r0 + e] = v;
       }
   }
 }
@@ -282,6 +283,62 @@ __global__ __launch_bounds__(kThreads) void bwd_prep_kernel(PrepArgs a) {
 }
 
 template <typename T>
+hipError_t launch_prep_t(const Problem& p, void* At, void* Bt, void* zero, long zero_bytes,
+                         hipStream_t stream) {
+  const int R = p.keys.R;
+  const int n_keys = p.keys.n_keys;
+  PrepArgs pa{};
+  pa.A = p.A;
+  pa.B = p.B;
+  pa.At = At;
+  pa.Bt = Bt;
+  pa.dHf = zero;
+  pa.d_in = p.d_in;
+  pa.d_out = p.d_out;
+  pa.R = R;
+  pa.dHf_vecs = (zero_bytes + 15) / 16;   // the region is 256-byte padded
+  pa.keys = p.keys;
+  pa.n_jobs = n_keys + 2;
+  long nb = 0;
+  auto tiles = [](long x) { return (x + kTile - 1) / kTile; };
+  pa.job_start[0] = 0;
+  pa.job_cols_tiles[0] = (int)tiles(p.d_in);
+  nb += At ? tiles(R) * tiles(p.d_in) : 0;
+  for (int q = 0; q < n_keys; ++q) {
+    pa.job_start[q + 1] = (int)nb;
+    pa.job_cols_tiles[q + 1] = (int)tiles(p.keys.rank[q]);
+    nb += Bt ? tiles(p.d_out) * tiles(p.keys.rank[q]) : 0;
+  }
+  pa.job_start[n_keys + 1] = (int)nb;
+  pa.job_cols_tiles[n_keys + 1] = 1;
+  nb += (pa.dHf_vecs + 4 * kThreads - 1) / (4 * kThreads);
+  pa.job_start[n_keys + 2] = (int)nb;
+  if (nb > 0) bwd_prep_kernel<T><<<(int)nb, kThreads, 0, stream>>>(pa);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_combine_t(const Problem& p, const void* hp, int rpad, void* Ht, long ldh,
+                            void* Hd, hipStream_t stream) {
+  CombineArgs cb{};
+  cb.offsets = p.rt->offsets;
+  cb.row_token = p.rt->row_token;
+  cb.ppos = p.rt->row_pair;
+  cb.plist = p.rt->pair_list;
+  cb.pair_w = p.pair_w;
+  cb.dHp = hp;
+  cb.rpad = rpad;
+  cb.dHt = Ht;
+  cb.ldh = ldh;
+  cb.dHf = Hd;
+  cb.keys = p.keys;
+  const long P = (long)p.T * p.k;
+  const int blocks = (int)((P + 63) / 64);
+  if (blocks > 0) combine_kernel<T><<<blocks, kThreads, 0, stream>>>(cb);
+  return hipGetLastError();
+}
+
+template <typename T>
 hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, float* dB,
                         void* ws, hipStream_t stream) {
   const int R = p.keys.R;
@@ -294,38 +351,12 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
   // kslots: rows of the dense dH buffer per token (1 when (token, key) is unique)
   const int kslots = (!p.per_pair && p.rt->mode == ACE_ROWS_GROUP_PAIRS) ? p.k : 1;
 
-  PrepArgs pa{};
-  pa.A = p.A;
-  pa.B = p.B;
-  pa.At = base + L.At;
-  pa.Bt = base + L.Bt;
-  pa.dHf = base + L.dHf;
-  pa.d_in = p.d_in;
-  pa.d_out = p.d_out;
-  pa.R = R;
   const long dHf_bytes = p.per_pair ? 0 : (long)p.T * kslots * R * (long)sizeof(T);
-  pa.dHf_vecs = (dHf_bytes + 15) / 16;   // the region is 256-byte padded
-  pa.keys = p.keys;
-  pa.n_jobs = n_keys + 2;
-  long nb = 0;
-  auto tiles = [](long x) { return (x + kTile - 1) / kTile; };
   // A^T feeds the per-pair dx expand and the register dx GEMM; the bf16 dx
   // GEMM reads A itself when the dense dH rows are 16-byte aligned
   const bool need_At = p.per_pair || p.dtype != ACE_BF16 || (kslots * R) % 8 != 0;
-  pa.job_start[0] = 0;
-  pa.job_cols_tiles[0] = (int)tiles(p.d_in);
-  nb += need_At ? tiles(R) * tiles(p.d_in) : 0;
-  for (int q = 0; q < n_keys; ++q) {
-    pa.job_start[q + 1] = (int)nb;
-    pa.job_cols_tiles[q + 1] = (int)tiles(p.keys.rank[q]);
-    nb += tiles(p.d_out) * tiles(p.keys.rank[q]);
-  }
-  pa.job_start[n_keys + 1] = (int)nb;
-  pa.job_cols_tiles[n_keys + 1] = 1;
-  nb += (pa.dHf_vecs + 4 * kThreads - 1) / (4 * kThreads);
-  pa.job_start[n_keys + 2] = (int)nb;
-  if (nb > 0) bwd_prep_kernel<T><<<(int)nb, kThreads, 0, stream>>>(pa);
-  hipError_t e = hipGetLastError();
+  hipError_t e = launch_prep_t<T>(p, need_At ? base + L.At : nullptr, base + L.Bt, base + L.dHf,
+                                  dHf_bytes, stream);
   if (e != hipSuccess) return e;
 
   ContractArgs c{};
@@ -391,21 +422,7 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
     c.out_row = base + L.dHrow;
     e = launch_contract(p.dtype, c, p.r_max, P, stream);
     if (e != hipSuccess) return e;
-    CombineArgs cb{};
-    cb.offsets = p.rt->offsets;
-    cb.row_token = p.rt->row_token;
-    cb.ppos = ppos;
-    cb.plist = plist;
-    cb.pair_w = p.pair_w;
-    cb.dHp = base + L.dHrow;
-    cb.rpad = rpad;
-    cb.dHt = base + L.dHt;
-    cb.ldh = ldh;
-    cb.dHf = base + L.dHf;
-    cb.keys = p.keys;
-    const int blocks = (int)((P + 63) / 64);
-    if (blocks > 0) combine_kernel<T><<<blocks, kThreads, 0, stream>>>(cb);
-    e = hipGetLastError();
+    e = launch_combine_t<T>(p, base + L.dHrow, rpad, base + L.dHt, ldh, base + L.dHf, stream);
   } else {
     c.src_mode = kSrcPerPair;
     c.out_w = 1;
@@ -472,6 +489,18 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
 
 size_t bwd_ws_bytes(int T, int k, int d_in, int d_out, int n_keys, int R, int r_max) {
   return ws_layout(T, k, d_in, d_out, n_keys, R, r_max, sizeof(float)).total;
+}
+
+hipError_t launch_prep(const Problem& p, void* At, void* Bt, void* zero, long zero_bytes,
+                       hipStream_t stream) {
+  if (p.dtype == ACE_BF16) return launch_prep_t<__bf16>(p, At, Bt, zero, zero_bytes, stream);
+  return launch_prep_t<float>(p, At, Bt, zero, zero_bytes, stream);
+}
+
+hipError_t launch_combine(const Problem& p, const void* hp, int rpad, void* Ht, long ldh,
+                          void* Hd, hipStream_t stream) {
+  if (p.dtype == ACE_BF16) return launch_combine_t<__bf16>(p, hp, rpad, Ht, ldh, Hd, stream);
+  return launch_combine_t<float>(p, hp, rpad, Ht, ldh, Hd, stream);
 }
 
 hipError_t launch_bwd(const Problem& p, const void* dy, void* dx, float* dA, float* dB, void* ws,

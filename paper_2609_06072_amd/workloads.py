@@ -38,10 +38,11 @@ ROWS_GROUP_PAIRS = 1
 ROWS_EXPERT = 2
 INPUT_SHARED = 0
 INPUT_PER_PAIR = 1
+INPUT_COMBINED = 2
 
 _STREAMS = ("router", "groups", "x", "h", "gate.A", "gate.B", "gate.dy",
             "up.A", "up.B", "up.dy", "down.A", "down.B", "down.dy", "y_in",
-            "dx_in", "extra")
+            "dx_in", "extra", "gate.dy_combined", "up.dy_combined", "down.dy_combined")
 
 
 @dataclasses.dataclass(frozen=True)

@@ -22,7 +22,11 @@ PATHS = {
     "down_expertwise": (W.ROWS_EXPERT, W.INPUT_PER_PAIR, "expert"),
     "pairs_shared": (W.ROWS_GROUP_PAIRS, W.INPUT_SHARED, "group"),
     "pairs_per_pair": (W.ROWS_GROUP_PAIRS, W.INPUT_PER_PAIR, "group"),
+    # down projection with the output combined per token (per-pair input)
+    "combined": (W.ROWS_GROUP_DEDUP, W.INPUT_COMBINED, "group"),
+    "combined_expertwise": (W.ROWS_EXPERT, W.INPUT_COMBINED, "expert"),
 }
+WEIGHTED = ("grouped", "pairs_per_pair", "combined", "combined_expertwise")
 
 
 def say(msg: str) -> None:
@@ -53,7 +57,7 @@ def make_case(cfg: W.MoEConfig, path: str, seed: int = 0, with_w: bool = False,
     mode, im, kind = PATHS[path]
     rt = W.make_routing(cfg, seed)
     if proj is None:
-        if im == W.INPUT_PER_PAIR:
+        if im in (W.INPUT_PER_PAIR, W.INPUT_COMBINED):
             proj = "down"
         else:
             proj = "gate" if "gate" in cfg.projections else cfg.projections[0]
@@ -66,13 +70,16 @@ def make_case(cfg: W.MoEConfig, path: str, seed: int = 0, with_w: bool = False,
         e2g = None
         n_keys = cfg.E
     t = W.make_proj(cfg, proj, ranks, seed=seed, device=device)
-    x = t.x
-    if t.input_mode != im:
+    x, dy = t.x, t.dy
+    x_mode = W.INPUT_PER_PAIR if im == W.INPUT_COMBINED else im
+    if t.input_mode != x_mode:
         rows = cfg.T if im == W.INPUT_SHARED else cfg.P
         x = W.draw_tensor((rows, t.d_in), 1.0, seed, "x" if im == W.INPUT_SHARED else "h",
                           cfg.dtype, device)
+    if im == W.INPUT_COMBINED:   # gradient of the combined output: one row per token
+        dy = W.draw_tensor((cfg.T, t.d_out), 1.0, seed, proj + ".dy_combined", cfg.dtype, device)
     pair_w = torch.from_numpy(rt.topk_w).to(device) if with_w else None
-    return Case(cfg, rt, mode, im, ranks, e2g, n_keys, t.d_in, t.d_out, x, t.A, t.B, t.dy, pair_w)
+    return Case(cfg, rt, mode, im, ranks, e2g, n_keys, t.d_in, t.d_out, x, t.A, t.B, dy, pair_w)
 
 
 def run_gpu(c: Case, fwd: bool = True, bwd: bool = True, y_in=None, dx_in=None,
@@ -89,7 +96,8 @@ def run_gpu(c: Case, fwd: bool = True, bwd: bool = True, y_in=None, dx_in=None,
     P = c.cfg.P
     fws = None
     if fwd:
-        y = torch.zeros(P, c.d_out, dtype=c.x.dtype, device=dev) if y_in is None else y_in.clone()
+        rows = c.cfg.T if c.input_mode == W.INPUT_COMBINED else P
+        y = torch.zeros(rows, c.d_out, dtype=c.x.dtype, device=dev) if y_in is None else y_in.clone()
         need = ace.ace_workspace_bytes(ace.ACE_OP_FWD, c.cfg.T, c.cfg.k, c.d_in, c.d_out,
                                        c.n_keys, max(c.ranks))
         fws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)

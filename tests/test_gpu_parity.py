@@ -12,8 +12,8 @@ import torch
 from oracle import ace_oracle as O
 from paper_2609_06072_amd import workloads as W
 
-from gpu_harness import (PATHS, TOL, check_rel, f64, make_case, oracle_args, oracle_bwd,
-                         oracle_fwd, run_gpu, say)
+from gpu_harness import (PATHS, TOL, WEIGHTED, check_rel, f64, make_case, oracle_args,
+                         oracle_bwd, oracle_fwd, run_gpu, say)
 
 pytestmark = pytest.mark.gpu
 
@@ -112,7 +112,7 @@ def test_permute_edge_cases():
 @pytest.mark.parametrize("path", list(PATHS))
 def test_parity_small(name, path):
     cfg = SMALL[name]
-    c = make_case(cfg, path, seed=1, with_w=(path in ("grouped", "pairs_per_pair")))
+    c = make_case(cfg, path, seed=1, with_w=(path in WEIGHTED))
     say(f"parity {name} {path} T={cfg.T} d_in={c.d_in} d_out={c.d_out} keys={c.n_keys}")
     out = run_gpu(c)
     tol = TOL[cfg.dtype]
@@ -128,7 +128,7 @@ def test_parity_small(name, path):
 def test_parity_small_h_reused(name, path):
     """Backward that reads h from the forward's workspace: same gradients."""
     cfg = SMALL[name]
-    c = make_case(cfg, path, seed=2, with_w=(path in ("grouped", "pairs_per_pair")))
+    c = make_case(cfg, path, seed=2, with_w=(path in WEIGHTED))
     say(f"parity (h reused) {name} {path} T={cfg.T} keys={c.n_keys}")
     out = run_gpu(c, reuse_h=True)
     tol = TOL[cfg.dtype]
@@ -161,12 +161,12 @@ def _sub_tokens(c, toks):
 
 
 @pytest.mark.parametrize("name", W.CONFIG_ORDER)
-@pytest.mark.parametrize("path", ["grouped", "expertwise", "down_expertwise"])
+@pytest.mark.parametrize("path", ["grouped", "expertwise", "down_expertwise", "combined"])
 def test_parity_full_size_sampled(name, path):
     cfg = W.CONFIGS[name]
-    if path == "down_expertwise" and "down" not in cfg.projections:
+    if path in ("down_expertwise", "combined") and "down" not in cfg.projections:
         pytest.skip("this workload adapts the up projection only")
-    c = make_case(cfg, path, seed=0)
+    c = make_case(cfg, path, seed=0, with_w=(path == "combined"))
     say(f"full-size {name} {path} T={cfg.T} d_in={c.d_in} d_out={c.d_out}")
     out = run_gpu(c, reuse_h=True)   # as timed: the backward reuses the forward's h
     tol = TOL[cfg.dtype]
@@ -177,8 +177,11 @@ def test_parity_full_size_sampled(name, path):
     a, _ = oracle_args(c, ids=ids, x=x)
     ref = O.lora_delta(*a, input_mode=c.input_mode, pair_w=w)
     rows = (toks[:, None] * k + np.arange(k)[None, :]).ravel()
-    check_rel("delta(sampled tokens)", f64(out["y"][torch.as_tensor(rows, device="cuda")]), ref, tol)
-    dy_sub = f64(c.dy[torch.as_tensor(rows, device="cuda")])
+    # output / output-gradient rows: per pair, or per token when combined
+    orows = toks if c.input_mode == W.INPUT_COMBINED else rows
+    check_rel("delta(sampled tokens)", f64(out["y"][torch.as_tensor(orows, device="cuda")]), ref,
+              tol)
+    dy_sub = f64(c.dy[torch.as_tensor(orows, device="cuda")])
     dx_ref, _, _ = O.lora_grads(*a, dy_sub, input_mode=c.input_mode, pair_w=w)
     if c.input_mode == W.INPUT_SHARED:
         got = f64(out["dx"][torch.as_tensor(toks, device="cuda")])
@@ -275,9 +278,11 @@ def test_empty_group_gets_exact_zero():
     check_rel("dA", f64(out["dA"]), dA, TOL["bf16"])
 
 
-def test_accumulates_into_existing_outputs():
-    c = make_case(SMALL["deepseek_bf16"], "grouped", seed=7)
-    y0 = W.draw_tensor((c.cfg.P, c.d_out), 1.0, 7, "y_in", "bf16", "cuda")
+@pytest.mark.parametrize("path", ["grouped", "combined"])
+def test_accumulates_into_existing_outputs(path):
+    c = make_case(SMALL["deepseek_bf16"], path, seed=7, with_w=(path == "combined"))
+    rows = c.cfg.T if path == "combined" else c.cfg.P
+    y0 = W.draw_tensor((rows, c.d_out), 1.0, 7, "y_in", "bf16", "cuda")
     dx0 = W.draw_tensor(tuple(c.x.shape), 1.0, 7, "dx_in", "bf16", "cuda")
     out = run_gpu(c, y_in=y0, dx_in=dx0)
     ref = f64(y0) + oracle_fwd(c)
@@ -286,9 +291,10 @@ def test_accumulates_into_existing_outputs():
     check_rel("dx_in + dx", f64(out["dx"]), f64(dx0) + dx, TOL["bf16"])
 
 
-def test_empty_input():
+@pytest.mark.parametrize("path", ["grouped", "combined"])
+def test_empty_input(path):
     cfg = SMALL["olmoe_bf16"].scaled(T=0)
-    c = make_case(cfg, "grouped", seed=0)
+    c = make_case(cfg, path, seed=0)
     out = run_gpu(c)
     assert out["y"].numel() == 0
     assert not out["dA"].isnan().any() and not out["dA"].any() and not out["dB"].any()
@@ -300,7 +306,7 @@ def test_small_and_odd_ranks(dtype, r_e):
     """The paper trains with expert rank 2; ranks that are not multiples of
     4 or 16 exercise the masked operand paths."""
     cfg = W.CONFIGS["olmoe_bf16"].scaled(T=200, d_model=128, d_ffn=96, dtype=dtype, r_e=r_e)
-    for path in ("grouped", "down_expertwise"):
+    for path in ("grouped", "down_expertwise", "combined"):
         c = make_case(cfg, path, seed=8, with_w=True)
         out = run_gpu(c)
         tol = TOL[dtype]
