@@ -244,7 +244,9 @@ def time_path(path, steps, warmup, repeats):
         e.record()
         torch.cuda.synchronize()
         per_step.append(s.elapsed_time(e) / steps)
-    phases = {f"{k[0]}.{k[1]}": statistics.mean(s.elapsed_time(e) for s, e in v)
+    # median over every timed call: a single clock hiccup must not move the
+    # choice of the dominant call
+    phases = {f"{k[0]}.{k[1]}": statistics.median(s.elapsed_time(e) for s, e in v)
               for k, v in path.timer.items()}
     path.timer = None
     return per_step, phases

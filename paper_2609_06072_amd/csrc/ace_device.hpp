@@ -195,6 +195,53 @@ __device__ inline void build_bucket_table(const int32_t* offsets, const int32_t*
   __syncthreads();
 }
 
+// Key q and row range of tile `tile` when every key's rows (segment
+// offsets[q] .. offsets[q+1]) are cut into tiles of BM rows, key-major.  Every
+// wave computes it on its own: lane l owns keys KPL*l .. KPL*l + KPL - 1, a
+// wave-level scan of the per-lane tile counts finds the owning lane, which
+// broadcasts the result (no LDS, no barrier).  Returns false (in every lane)
+// when the tile is past the last one.
+__device__ inline bool locate_tile(const int32_t* offsets, int n_keys, int BM, int tile, int* q_out,
+                                   int* u0_out, int* uend_out) {
+  constexpr int KPL = kMaxKeys / 64;
+  const int lane = threadIdx.x & 63;
+  int off[KPL + 1], tl[KPL];
+#pragma unroll
+  for (int i = 0; i <= KPL; ++i) off[i] = offsets[min(lane * KPL + i, n_keys)];
+  int cnt = 0;
+#pragma unroll
+  for (int i = 0; i < KPL; ++i) {
+    tl[i] = (off[i + 1] - off[i] + BM - 1) / BM;  // zero past n_keys (clamped offsets)
+    cnt += tl[i];
+  }
+  int incl = cnt;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int v = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += v;
+  }
+  const int excl = incl - cnt;
+  const unsigned long long hit = __ballot(tile >= excl && tile < incl);
+  if (hit == 0ull) return false;
+  const int owner = __builtin_ctzll(hit);
+  int t = tile - excl, q = 0, u0 = 0, ue = 0;
+  bool found = false;
+#pragma unroll
+  for (int i = 0; i < KPL; ++i) {
+    if (!found && t < tl[i]) {
+      q = lane * KPL + i;
+      u0 = off[i] + t * BM;
+      ue = off[i + 1];
+      found = true;
+    }
+    if (!found) t -= tl[i];
+  }
+  *q_out = __shfl(q, owner, 64);
+  *u0_out = __shfl(u0, owner, 64);
+  *uend_out = __shfl(ue, owner, 64);
+  return true;
+}
+
 // Largest q in [0, n) with arr[q] <= x, for a non-decreasing arr (uniform).
 __device__ inline int upper_index(const int* arr, int n, int x) {
   int lo = 0, hi = n;  // invariant: arr[lo] <= x < arr[hi] (arr[n] treated as +inf)
