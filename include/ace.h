@@ -96,7 +96,8 @@ typedef enum {
 typedef enum {
   ACE_OP_PERMUTE = 0,
   ACE_OP_FWD = 1,
-  ACE_OP_BWD = 2
+  ACE_OP_BWD = 2,
+  ACE_OP_CKA = 3   /* ace_pairwise_cka: T = probe rows N, k = 1, n_keys = E, r_max = rank */
 } ace_op;
 
 /*
@@ -217,6 +218,33 @@ ace_status ace_expertwise_lora_bwd(ace_dtype dtype, ace_input_mode input_mode, i
                                    const void* B, const float* pair_w, const ace_routing* rt,
                                    const void* h_fwd, const void* dy, void* dx, float* dA,
                                    float* dB, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Pairwise linear CKA of the expert adapters of one layer on a shared probe
+ * set (Sec. 3.3, rank consolidation): the similarity that groups experts.
+ * Every probe row goes through every adapter regardless of routing; with
+ * Z_e the N x d_out matrix of rows (B_e A_e x_n)^T, centred over the probe
+ * rows (Zc_e = H Z_e, H = I - 11^T/N),
+ *   S[i][j] = ||Zc_i^T Zc_j||_F^2 / (||Zc_i^T Zc_i||_F ||Zc_j^T Zc_j||_F).
+ * The LoRA scale is common to the experts of a layer and CKA is invariant to
+ * it, so B_e A_e is used unscaled.  An expert whose centred output is
+ * identically zero (B_e = 0, N < 2, ...) gets S = 0 in its row and column.
+ *   X       device [N, d_in], dtype: the probe hidden states.
+ *   A, B    device, the expert adapters in the packed layout at the top with
+ *           E keys of rank `rank` (1 <= rank <= 64), dtype.
+ *   S       device fp32 [E, E]: overwritten (symmetric, diagonal 1).
+ *   ws      device scratch of at least
+ *           ace_workspace_bytes(ACE_OP_CKA, N, 1, d_in, d_out, E, rank);
+ *           no initialisation.
+ * Evaluated through the rank-r identity
+ *   ||Zc_i^T Zc_j||_F^2 = <G_i M_ij, M_ij G_j>_F,  M = Pc^T Pc,
+ *   Pc = centred X A^T (N x E*rank),  G_e = B_e^T B_e,
+ * which is exact up to rounding: X A^T on the matrix cores (fp32
+ * accumulation), M in fp32, no N x d_out matrix formed.  Deterministic.
+ */
+ace_status ace_pairwise_cka(ace_dtype dtype, int32_t N, int32_t d_in, int32_t d_out, int32_t E,
+                            int32_t rank, const void* X, const void* A, const void* B, float* S,
+                            void* ws, size_t ws_bytes, void* stream);
 
 /*
  * Device scratch needed by an op (bytes, rounded up to 256).  n_keys and

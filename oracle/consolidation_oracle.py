@@ -77,10 +77,9 @@ def adapter_outputs(X: np.ndarray, A: np.ndarray, B: np.ndarray, E: int, r: int)
 
 
 def center(Z: np.ndarray) -> np.ndarray:
-    """H Z with H = I - 11^T / N: subtract the mean over the probe rows."""
-    N = Z.shape[0]
-    H = np.eye(N) - np.ones((N, N)) / N
-    return H @ Z
+    """H Z with H = I - 11^T / N, evaluated as Z - 1 (1^T Z / N): every row
+    minus the mean over the probe rows."""
+    return Z - Z.sum(axis=0, keepdims=True) / Z.shape[0]
 
 
 def cka_matrix(X: np.ndarray, A: np.ndarray, B: np.ndarray, E: int, r: int) -> np.ndarray:

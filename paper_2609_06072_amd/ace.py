@@ -25,11 +25,11 @@ ACE_OK, ACE_ERR_INVALID_ARG, ACE_ERR_UNSUPPORTED, ACE_ERR_WORKSPACE, ACE_ERR_HIP
 ACE_F32, ACE_BF16 = 0, 1
 ACE_ROWS_GROUP_DEDUP, ACE_ROWS_GROUP_PAIRS, ACE_ROWS_EXPERT = 0, 1, 2
 ACE_INPUT_SHARED, ACE_INPUT_PER_PAIR, ACE_INPUT_COMBINED = 0, 1, 2
-ACE_OP_PERMUTE, ACE_OP_FWD, ACE_OP_BWD = 0, 1, 2
+ACE_OP_PERMUTE, ACE_OP_FWD, ACE_OP_BWD, ACE_OP_CKA = 0, 1, 2, 3
 
 EXPORTS = ("ace_group_permute", "ace_grouped_lora_fwd", "ace_grouped_lora_bwd",
            "ace_expertwise_lora_fwd", "ace_expertwise_lora_bwd", "ace_workspace_bytes",
-           "ace_routing_check", "ace_last_error")
+           "ace_routing_check", "ace_last_error", "ace_pairwise_cka")
 
 
 class AceRouting(ctypes.Structure):
@@ -64,6 +64,9 @@ _lib.ace_workspace_bytes.argtypes = [_i32, _i32, _i32, _i32, _i32, _i32, _i32]
 _lib.ace_workspace_bytes.restype = _sz
 _lib.ace_routing_check.argtypes = [_R, ctypes.POINTER(ctypes.c_int32), _vp]
 _lib.ace_routing_check.restype = _i32
+_lib.ace_pairwise_cka.argtypes = [_i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _sz,
+                                  _vp]
+_lib.ace_pairwise_cka.restype = _i32
 _lib.ace_last_error.argtypes = []
 _lib.ace_last_error.restype = ctypes.c_char_p
 
@@ -235,6 +238,22 @@ def ace_expertwise_lora_bwd(x, A, B, E: int, rank: int, alpha: float, routing: R
                                         _ptr(dA), _ptr(dB), _ptr(ws), ws.numel(),
                                         _stream(stream)),
            "ace_expertwise_lora_bwd")
+
+
+def ace_pairwise_cka(X, A, B, E: int, rank: int, S=None, ws=None, stream=None) -> torch.Tensor:
+    """Pairwise linear CKA [E, E] (fp32) of the expert adapters A, B (packed,
+    E keys of rank `rank`) on the probe rows X [N, d_in]."""
+    N, d_in = X.shape
+    d_out = B.numel() // (E * rank)
+    if S is None:
+        S = torch.empty(E, E, dtype=torch.float32, device=A.device)
+    if ws is None:
+        need = ace_workspace_bytes(ACE_OP_CKA, N, 1, d_in, d_out, E, rank)
+        ws = torch.empty(max(need, 256), dtype=torch.uint8, device=A.device)
+    _check(_lib.ace_pairwise_cka(_dtype(A), N, d_in, d_out, E, rank, _ptr(X), _ptr(A), _ptr(B),
+                                 _ptr(S), _ptr(ws), ws.numel(), _stream(stream)),
+           "ace_pairwise_cka")
+    return S
 
 
 def raw_lib() -> ctypes.CDLL:

@@ -147,6 +147,18 @@ size_t bwd_ws_bytes(int T, int k, int d_in, int d_out, int n_keys, int R, int r_
 hipError_t launch_bwd(const Problem& p, const void* dy, void* dx, float* dA, float* dB, void* ws,
                       hipStream_t stream);
 
+// Pairwise linear CKA of expert adapters (ace_pairwise_cka).
+struct CkaProblem {
+  int dtype;
+  int N, d_in, d_out, E, r;
+  const void* X;   // [N][d_in]
+  const void* A;   // [E*r][d_in]
+  const void* B;   // expert e: [d_out][r] at d_out * r * e
+  float* S;        // [E][E]
+};
+size_t cka_ws_bytes(int N, int E, int r);
+hipError_t launch_cka(const CkaProblem& p, void* ws, hipStream_t stream);
+
 // Number of compute units of the current device (cached per device).
 int device_cu_count();
 

@@ -267,6 +267,37 @@ ace_status ace_expertwise_lora_bwd(ace_dtype dtype, ace_input_mode input_mode, i
   return run_bwd(p, h_fwd, dy, dx, dA, dB, ws, ws_bytes, stream);
 }
 
+ace_status ace_pairwise_cka(ace_dtype dtype, int32_t N, int32_t d_in, int32_t d_out, int32_t E,
+                            int32_t rank, const void* X, const void* A, const void* B, float* S,
+                            void* ws, size_t ws_bytes, void* stream) {
+  if (dtype != ACE_F32 && dtype != ACE_BF16) return fail(ACE_ERR_INVALID_ARG, "unknown dtype %d", (int)dtype);
+  if (N < 0) return fail(ACE_ERR_INVALID_ARG, "N = %d < 0", N);
+  const int vec = dtype == ACE_BF16 ? 8 : 4;
+  if (d_in < 1 || d_out < 1) return fail(ACE_ERR_INVALID_ARG, "d_in = %d, d_out = %d", d_in, d_out);
+  if (d_in % vec) return fail(ACE_ERR_UNSUPPORTED, "d_in (%d) must be a multiple of %d", d_in, vec);
+  if (E < 1 || E > kMaxKeys) return fail(ACE_ERR_UNSUPPORTED, "expert count %d outside [1, %d]", E, kMaxKeys);
+  if (rank < 1 || rank > 64) return fail(ACE_ERR_UNSUPPORTED, "rank %d outside [1, 64]", rank);
+  if ((int64_t)N * E * rank >= (int64_t)1 << 40) return fail(ACE_ERR_UNSUPPORTED, "probe too large");
+  if (!A || !B || !S || (N > 0 && !X)) return fail(ACE_ERR_INVALID_ARG, "NULL argument");
+  if (!aligned(X, 16) || !aligned(A, 16)) return fail(ACE_ERR_INVALID_ARG, "X and A must be 16-byte aligned");
+  if (!aligned(S, 4) || !aligned(B, dtype == ACE_BF16 ? 2 : 4)) return fail(ACE_ERR_INVALID_ARG, "B or S misaligned");
+  const size_t need = cka_ws_bytes(N, E, rank);
+  if (!ws || ws_bytes < need)
+    return fail(ACE_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", ws_bytes, need);
+  CkaProblem p{};
+  p.dtype = dtype;
+  p.N = N;
+  p.d_in = d_in;
+  p.d_out = d_out;
+  p.E = E;
+  p.r = rank;
+  p.X = X;
+  p.A = A;
+  p.B = B;
+  p.S = S;
+  return hip_status(launch_cka(p, ws, static_cast<hipStream_t>(stream)), "pairwise cka launch");
+}
+
 size_t ace_workspace_bytes(ace_op op, int32_t T, int32_t k, int32_t d_in, int32_t d_out,
                            int32_t n_keys, int32_t r_max) {
   if (T < 0 || k < 1 || k > kMaxK || n_keys < 1 || n_keys > kMaxKeys) {
@@ -297,6 +328,12 @@ size_t ace_workspace_bytes(ace_op op, int32_t T, int32_t k, int32_t d_in, int32_
         const size_t b = bwd_combined_ws_bytes(T, k, d_in, d_out, n_keys, r_max);
         return round256(a > b ? a : b);
       }
+    case ACE_OP_CKA:
+      if (d_in < 1 || d_out < 1 || r_max < 1 || r_max > 64) {
+        fail(ACE_ERR_INVALID_ARG, "invalid workspace query");
+        return (size_t)-1;
+      }
+      return round256(cka_ws_bytes(T, n_keys, r_max));
   }
   fail(ACE_ERR_INVALID_ARG, "unknown op %d", (int)op);
   return (size_t)-1;

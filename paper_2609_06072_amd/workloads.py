@@ -23,6 +23,14 @@ Recipe (every stream is an independent child of ``SeedSequence(seed)``):
                  Sec. 3.3 rank consolidation).
   * tensors   -- x ~ N(0,1), A ~ N(0, 1/d_in) (std d_in^-1/2), B ~ N(0, 0.02)
                  (std 0.02), dY ~ N(0,1); bf16 configs round with RNE.
+  * probe and expert adapters for the consolidation step (Sec. 3.3: N probe
+    hidden states go through every expert adapter of a layer; the paper uses
+    N = 10,000 training tokens after a warm-up of expert-wise LoRA) --
+    probe rows ~ N(mu, 1) with a per-feature offset mu ~ N(0, 1); the experts
+    fall into planted clusters (the config's group scheme), and expert e's
+    adapter is its cluster's base plus independent noise:
+    A_e = A_c + nu * N(0, 1/d_in), B_e = B_c + nu * N(0, 0.02^2), with
+    A_c ~ N(0, 1/d_in), B_c ~ N(0, 0.02^2); nu = 0.5 by default.
 """
 from __future__ import annotations
 
@@ -42,7 +50,9 @@ INPUT_COMBINED = 2
 
 _STREAMS = ("router", "groups", "x", "h", "gate.A", "gate.B", "gate.dy",
             "up.A", "up.B", "up.dy", "down.A", "down.B", "down.dy", "y_in",
-            "dx_in", "extra", "gate.dy_combined", "up.dy_combined", "down.dy_combined")
+            "dx_in", "extra", "gate.dy_combined", "up.dy_combined", "down.dy_combined",
+            "probe", "probe.mu", "cka.clusters", "cka.A", "cka.B", "cka.A_noise", "cka.B_noise",
+            "cka.A_init")
 
 
 @dataclasses.dataclass(frozen=True)
@@ -249,3 +259,39 @@ def describe(cfg: MoEConfig, rt: Routing) -> Dict[str, object]:
     ent = float(-(nz * np.log(nz)).sum() / math.log(cfg.E))
     return {"P": cfg.P, "E": cfg.E, "G": rt.G, "load_entropy": ent,
             "max_over_mean_load": float(load.max() / load.mean())}
+
+
+@dataclasses.dataclass
+class ProbeAdapters:
+    X: object          # torch [N, d_in]
+    A: object          # torch [E*r, d_in]
+    B: object          # torch flat: expert e's [d_out, r] block at d_out * r * e
+    clusters: np.ndarray  # int32 [E]: planted cluster of every expert
+    d_in: int
+    d_out: int
+    E: int
+    r: int
+
+
+def make_probe_adapters(cfg: MoEConfig, proj: str = "gate", N: int = 10000, noise: float = 0.5,
+                        seed: int = 0, device: str = "cpu") -> ProbeAdapters:
+    """Probe set and expert-wise adapters of one projection for the CKA step
+    (recipe in the module notes)."""
+    torch = _torch()
+    d_in, d_out, _ = cfg.proj_dims(proj)
+    E, r = cfg.E, cfg.r_e
+    clusters = draw_groups(E, cfg.groups, rng_for(seed, "cka.clusters"))
+    C = int(clusters.max()) + 1
+    idx = torch.from_numpy(clusters.astype(np.int64)).to(device)
+    X = draw_tensor((N, d_in), 1.0, seed, "probe", "f32", device)
+    X += draw_tensor((d_in,), 1.0, seed, "probe.mu", "f32", device)
+    Ac = draw_tensor((C, r, d_in), 1.0 / math.sqrt(d_in), seed, "cka.A", "f32", device)
+    An = draw_tensor((E, r, d_in), noise / math.sqrt(d_in), seed, "cka.A_noise", "f32", device)
+    Bc = draw_tensor((C, d_out, r), 0.02, seed, "cka.B", "f32", device)
+    Bn = draw_tensor((E, d_out, r), 0.02 * noise, seed, "cka.B_noise", "f32", device)
+    A = (Ac[idx] + An).reshape(E * r, d_in)
+    B = (Bc[idx] + Bn).reshape(-1)
+    dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    return ProbeAdapters(X.to(dt).contiguous(), A.to(dt).contiguous(), B.to(dt).contiguous(),
+                         clusters, d_in, d_out, E, r)
+

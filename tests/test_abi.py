@@ -134,3 +134,26 @@ def test_forward_backward_reject_bad_arguments(ace):
     st = lib.ace_grouped_lora_bwd(ace.ACE_BF16, 0, 4, 2, 64, 32, 2, ranks, 16.0, p, p, p, None,
                                   ctypes.byref(_routing(ace)), h_bad, p, p, p, p, p, 1 << 30, None)
     assert st == ace.ACE_ERR_INVALID_ARG
+
+
+def test_cka_rejects_bad_arguments(ace):
+    lib = ace.raw_lib()
+    ws = ctypes.c_void_p(0x10000)
+    X, A, B, S = (ctypes.c_void_p(a) for a in (0x1000, 0x2000, 0x3000, 0x4000))
+    ok_ws = ace.ace_workspace_bytes(ace.ACE_OP_CKA, 100, 1, 64, 32, 8, 4)
+    assert ok_ws > 0 and ok_ws % 256 == 0
+    cases = [
+        (7, 100, 64, 32, 8, 4, ok_ws),        # unknown dtype
+        (1, 100, 64, 32, 8, 65, ok_ws),       # rank above 64
+        (1, 100, 64, 32, 0, 4, ok_ws),        # no experts
+        (1, 100, 60, 32, 8, 4, ok_ws),        # d_in not a multiple of 8 (bf16)
+        (1, -1, 64, 32, 8, 4, ok_ws),         # negative probe size
+        (1, 100, 64, 32, 8, 4, ok_ws - 256),  # workspace too small
+    ]
+    for dt, N, d_in, d_out, E, r, wsb in cases:
+        st = lib.ace_pairwise_cka(dt, N, d_in, d_out, E, r, X, A, B, S, ws, wsb, None)
+        assert st < 0, (dt, N, d_in, d_out, E, r, wsb)
+        assert ace.ace_last_error()
+    with pytest.raises(ace.AceError):
+        ace.ace_workspace_bytes(ace.ACE_OP_CKA, 100, 1, 64, 32, 8, 65)
+
