@@ -40,6 +40,8 @@ Readings where the paper is silent (each is restated in the design notes):
     the communities then become super-nodes (numbered by their lowest
     member) and the next level starts; the algorithm ends at a level with no
     move.  Final groups are numbered in order of their lowest expert.
+    Degrees, 2m, k_i,in and the coarse weights are summed in index order
+    (the gain comparisons decide the partition, so the order is fixed).
   * The CKA centre of a group is the member with the largest sum of CKA
     similarities to the other members (ties to the lowest index).
   * The group adapter keeps the anchor's update exactly: rank rows 0 .. r-1 of
@@ -127,29 +129,46 @@ def modularity(W: np.ndarray, labels: Sequence[int], gamma: float) -> float:
     return float(((W - gamma * np.outer(k, k) / two_m) * same).sum() / two_m)
 
 
+def _degrees(W: np.ndarray) -> Tuple[List[float], float]:
+    """k_i = sum_j W_ij and 2m = sum_i k_i, each summed in index order."""
+    n = W.shape[0]
+    k = []
+    for i in range(n):
+        s = 0.0
+        for j in range(n):
+            s += float(W[i, j])
+        k.append(s)
+    two_m = 0.0
+    for i in range(n):
+        two_m += k[i]
+    return k, two_m
+
+
 def _local_moves(W: np.ndarray, gamma: float) -> Tuple[np.ndarray, bool]:
     """One level of greedy local moves from singletons (the reading of the
     visiting order in the module notes).  Returns community ids (not yet
     renumbered) and whether any node moved."""
     n = W.shape[0]
-    k = W.sum(axis=1)
-    two_m = W.sum()
+    k, two_m = _degrees(W)
     comm = np.arange(n)
-    tot = k.copy()                      # sum of degrees per community
+    tot = list(k)                       # sum of degrees per community
     moved_any = False
     if two_m <= 0.0:
         return comm, False
     while True:
         moved = False
         for i in range(n):
-            ci = comm[i]
+            ci = int(comm[i])
             tot[ci] -= k[i]             # remove i from its community
-            # k_i,in(C): weight from i to the members of C (self-loop excluded)
+            # k_i,in(C): weight from i to the members of C (self-loop excluded),
+            # summed in index order
             kin = {}
             for j in range(n):
                 if j != i and W[i, j] > 0.0:
-                    kin[comm[j]] = kin.get(comm[j], 0.0) + W[i, j]
+                    c = int(comm[j])
+                    kin[c] = kin.get(c, 0.0) + float(W[i, j])
             cands = set(kin) | {ci}
+
             def gain(c):
                 return kin.get(c, 0.0) - gamma * k[i] * tot[c] / two_m
             best = min(cands, key=lambda c: (-gain(c), c))
@@ -157,7 +176,7 @@ def _local_moves(W: np.ndarray, gamma: float) -> Tuple[np.ndarray, bool]:
                 comm[i] = best
                 moved = True
                 moved_any = True
-            tot[comm[i]] += k[i]
+            tot[int(comm[i])] += k[i]
         if not moved:
             break
     return comm, moved_any
@@ -187,10 +206,13 @@ def louvain(W: np.ndarray, gamma: float = 0.8) -> np.ndarray:
             break
         comm = _renumber(comm)
         nc = int(comm.max()) + 1
-        # coarsen: W'_ab = sum over members i of a and j of b of W_ij
-        onehot = np.zeros((Wl.shape[0], nc))
-        onehot[np.arange(Wl.shape[0]), comm] = 1.0
-        Wl = onehot.T @ Wl @ onehot
+        # coarsen: W'_ab = sum over members i of a and j of b of W_ij,
+        # accumulated with (i, j) in row-major order
+        Wc = np.zeros((nc, nc))
+        for i in range(Wl.shape[0]):
+            for j in range(Wl.shape[0]):
+                Wc[comm[i], comm[j]] += Wl[i, j]
+        Wl = Wc
         node_of = comm[node_of]
     return _renumber(node_of)
 
