@@ -247,6 +247,68 @@ ace_status ace_pairwise_cka(ace_dtype dtype, int32_t N, int32_t d_in, int32_t d_
                             void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * Expert grouping from the CKA matrix (appendices "Layer-wise graph
+ * construction" and "Layer-wise grouping with the Louvain method").  Host
+ * computations on host arrays; E <= 256.
+ *
+ * ace_similarity_graph: W[i][j] = max(0, (S[i][j] + S[j][i])/2 - b) for
+ *   i != j, W[i][i] = 0, with b the median of the off-diagonal entries of
+ *   (S + S^T)/2 (the mean of the two middle ones for an even count).
+ *   S host fp32 [E, E]; W host fp64 [E, E] (overwritten).
+ *
+ * ace_louvain: groups the nodes of W by greedy modularity optimisation,
+ *   Q = (1/2m) sum_ij (W_ij - gamma k_i k_j / 2m) [z_i == z_j]
+ *   (k_i = sum_j W_ij, 2m = sum_ij W_ij; the paper uses gamma = 0.8).  Node i,
+ *   in index order, leaves its community and joins the candidate (a community
+ *   holding one of its neighbours, or its own) with the largest gain
+ *   k_i,in(C) - gamma k_i tot(C) / 2m (ties to the lowest community id) when
+ *   that gain beats staying; sweeps repeat until none moves, the communities
+ *   become super-nodes and the next level starts; a level with no move ends
+ *   it.  Sums run in index order, so the result is reproducible bit for bit.
+ *   W host fp64 [E, E], symmetric, non-negative; groups host int32 [E]
+ *   (out): numbered in order of their lowest expert; *n_groups (out) = G.
+ *   A graph without edges leaves every expert alone (G = E).
+ *
+ * ace_group_anchors: the CKA centre of every group, the member with the
+ *   largest summed similarity S[i][j] to the other members (ties to the
+ *   lowest expert).  expert_to_group host int32 [E] with values in [0, G),
+ *   every group non-empty; anchors host int32 [G] (out).
+ */
+ace_status ace_similarity_graph(const float* S, int32_t E, double* W);
+ace_status ace_louvain(const double* W, int32_t E, double gamma, int32_t* groups,
+                       int32_t* n_groups);
+ace_status ace_group_anchors(const float* S, int32_t E, const int32_t* expert_to_group, int32_t G,
+                             int32_t* anchors);
+
+/*
+ * Consolidated group adapters from the expert adapters (Sec. 3.3 rank
+ * consolidation; group-anchor appendix).  Group g has rank
+ * r_g = |G_g| * rank (the budget is unchanged) and its adapter starts from
+ * its anchor expert a = anchors[g]:
+ *   A_g rows 0 .. rank-1     = A_a
+ *   A_g rows rank .. r_g-1   = the next r_g - rank rows of A_init (the
+ *                              standard LoRA draw of the extra rank, group
+ *                              by group in group order)
+ *   B_g columns 0 .. rank-1  = (r_g / rank) * B_a, so that the group adapter
+ *                              at scale alpha / r_g reproduces the anchor's
+ *                              update at alpha / rank
+ *   B_g other columns        = 0
+ *   A, B      device, expert adapters (E keys of rank `rank`, packed layout
+ *             above), dtype.
+ *   expert_to_group, anchors  host int32 [E], [G] (every group non-empty, its
+ *             anchor one of its members).
+ *   A_init    device [(E - G) * rank, d_in], dtype; may be NULL when G == E.
+ *   A_g, B_g  device, packed layout above with G keys of ranks r_g (the
+ *             group blocks in group order), dtype: overwritten.
+ * Asynchronous on `stream`; A_g and B_g must not overlap the inputs.
+ */
+ace_status ace_consolidate_adapters(ace_dtype dtype, int32_t d_in, int32_t d_out, int32_t E,
+                                    int32_t rank, const void* A, const void* B,
+                                    const int32_t* expert_to_group, int32_t G,
+                                    const int32_t* anchors, const void* A_init, void* A_g,
+                                    void* B_g, void* stream);
+
+/*
  * Device scratch needed by an op (bytes, rounded up to 256).  n_keys and
  * r_max bound the packed rank R <= n_keys * r_max; dtype-independent (sized
  * for fp32).  Pure host computation; (size_t)-1 for invalid arguments.

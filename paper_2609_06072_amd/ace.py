@@ -29,7 +29,8 @@ ACE_OP_PERMUTE, ACE_OP_FWD, ACE_OP_BWD, ACE_OP_CKA = 0, 1, 2, 3
 
 EXPORTS = ("ace_group_permute", "ace_grouped_lora_fwd", "ace_grouped_lora_bwd",
            "ace_expertwise_lora_fwd", "ace_expertwise_lora_bwd", "ace_workspace_bytes",
-           "ace_routing_check", "ace_last_error", "ace_pairwise_cka")
+           "ace_routing_check", "ace_last_error", "ace_pairwise_cka", "ace_similarity_graph",
+           "ace_louvain", "ace_group_anchors", "ace_consolidate_adapters")
 
 
 class AceRouting(ctypes.Structure):
@@ -67,6 +68,15 @@ _lib.ace_routing_check.restype = _i32
 _lib.ace_pairwise_cka.argtypes = [_i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _sz,
                                   _vp]
 _lib.ace_pairwise_cka.restype = _i32
+_lib.ace_similarity_graph.argtypes = [_vp, _i32, _vp]
+_lib.ace_similarity_graph.restype = _i32
+_lib.ace_louvain.argtypes = [_vp, _i32, ctypes.c_double, _vp, ctypes.POINTER(ctypes.c_int32)]
+_lib.ace_louvain.restype = _i32
+_lib.ace_group_anchors.argtypes = [_vp, _i32, _vp, _i32, _vp]
+_lib.ace_group_anchors.restype = _i32
+_lib.ace_consolidate_adapters.argtypes = [_i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _i32, _vp,
+                                          _vp, _vp, _vp, _vp]
+_lib.ace_consolidate_adapters.restype = _i32
 _lib.ace_last_error.argtypes = []
 _lib.ace_last_error.restype = ctypes.c_char_p
 
@@ -254,6 +264,65 @@ def ace_pairwise_cka(X, A, B, E: int, rank: int, S=None, ws=None, stream=None) -
                                  _ptr(S), _ptr(ws), ws.numel(), _stream(stream)),
            "ace_pairwise_cka")
     return S
+
+
+def _host(a, dtype):
+    import numpy as np
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def ace_similarity_graph(S):
+    """W [E, E] (float64, numpy) from the similarity matrix S [E, E] (host)."""
+    import numpy as np
+    S = _host(S, np.float32)
+    E = S.shape[0]
+    W = np.empty((E, E), dtype=np.float64)
+    _check(_lib.ace_similarity_graph(S.ctypes.data, E, W.ctypes.data), "ace_similarity_graph")
+    return W
+
+
+def ace_louvain(W, gamma: float = 0.8):
+    """(groups int32 [E], G) from the graph W [E, E] (host, float64)."""
+    import numpy as np
+    W = _host(W, np.float64)
+    E = W.shape[0]
+    groups = np.empty(E, dtype=np.int32)
+    G = ctypes.c_int32(0)
+    _check(_lib.ace_louvain(W.ctypes.data, E, float(gamma), groups.ctypes.data, ctypes.byref(G)),
+           "ace_louvain")
+    return groups, int(G.value)
+
+
+def ace_group_anchors(S, expert_to_group, G: int):
+    """CKA centre of every group (int32 [G])."""
+    import numpy as np
+    S = _host(S, np.float32)
+    e2g = _host(expert_to_group, np.int32)
+    anchors = np.empty(G, dtype=np.int32)
+    _check(_lib.ace_group_anchors(S.ctypes.data, S.shape[0], e2g.ctypes.data, G,
+                                  anchors.ctypes.data), "ace_group_anchors")
+    return anchors
+
+
+def ace_consolidate_adapters(A, B, E: int, rank: int, expert_to_group, G: int, anchors, A_init,
+                             A_g=None, B_g=None, stream=None):
+    """Group adapters (A_g, B_g, ranks) from the expert adapters A, B (device)."""
+    import numpy as np
+    e2g = _host(expert_to_group, np.int32)
+    anc = _host(anchors, np.int32)
+    ranks = [int(np.sum(e2g == g)) * rank for g in range(G)]
+    R = sum(ranks)
+    d_in = A.shape[1]
+    d_out = B.numel() // (E * rank)
+    if A_g is None:
+        A_g = torch.empty(R, d_in, dtype=A.dtype, device=A.device)
+    if B_g is None:
+        B_g = torch.empty(R * d_out, dtype=B.dtype, device=B.device)
+    _check(_lib.ace_consolidate_adapters(_dtype(A), d_in, d_out, E, rank, _ptr(A), _ptr(B),
+                                         e2g.ctypes.data, G, anc.ctypes.data, _ptr(A_init),
+                                         _ptr(A_g), _ptr(B_g), _stream(stream)),
+           "ace_consolidate_adapters")
+    return A_g, B_g, ranks
 
 
 def raw_lib() -> ctypes.CDLL:

@@ -159,6 +159,22 @@ struct CkaProblem {
 size_t cka_ws_bytes(int N, int E, int r);
 hipError_t launch_cka(const CkaProblem& p, void* ws, hipStream_t stream);
 
+// Expert grouping (host) and adapter consolidation (device).
+void similarity_graph(const float* S, int E, double* W);
+int louvain(const double* W, int E, double gamma, int32_t* groups);  // returns G
+void group_anchors(const float* S, int E, const int32_t* e2g, int G, int32_t* anchors);
+struct ConsolidateProblem {
+  int d_in, d_out, r;
+  const void* A;
+  const void* B;
+  const void* A_init;
+  void* Ag;
+  void* Bg;
+  KeyTable keys;            // group ranks r_g = |G_g| r and offsets
+  const int32_t* anchor;    // host [G]
+};
+hipError_t launch_consolidate(int dtype, const ConsolidateProblem& p, hipStream_t stream);
+
 // Number of compute units of the current device (cached per device).
 int device_cu_count();
 

@@ -7,6 +7,7 @@
 
 #include <cmath>
 #include <string>
+#include <vector>
 
 #include "ace_internal.hpp"
 
@@ -296,6 +297,96 @@ ace_status ace_pairwise_cka(ace_dtype dtype, int32_t N, int32_t d_in, int32_t d_
   p.B = B;
   p.S = S;
   return hip_status(launch_cka(p, ws, static_cast<hipStream_t>(stream)), "pairwise cka launch");
+}
+
+ace_status ace_similarity_graph(const float* S, int32_t E, double* W) {
+  if (E < 1 || E > kMaxKeys) return fail(ACE_ERR_UNSUPPORTED, "expert count %d outside [1, %d]", E, kMaxKeys);
+  if (!S || !W) return fail(ACE_ERR_INVALID_ARG, "NULL argument");
+  for (int64_t i = 0; i < (int64_t)E * E; ++i)
+    if (!std::isfinite(S[i])) return fail(ACE_ERR_INVALID_ARG, "S[%lld] is not finite", (long long)i);
+  similarity_graph(S, E, W);
+  return ok();
+}
+
+ace_status ace_louvain(const double* W, int32_t E, double gamma, int32_t* groups,
+                       int32_t* n_groups) {
+  if (E < 1 || E > kMaxKeys) return fail(ACE_ERR_UNSUPPORTED, "expert count %d outside [1, %d]", E, kMaxKeys);
+  if (!W || !groups || !n_groups) return fail(ACE_ERR_INVALID_ARG, "NULL argument");
+  if (!std::isfinite(gamma) || gamma < 0.0) return fail(ACE_ERR_INVALID_ARG, "gamma must be finite and >= 0");
+  for (int i = 0; i < E; ++i)
+    for (int j = 0; j < E; ++j) {
+      const double w = W[(size_t)i * E + j];
+      if (!std::isfinite(w) || w < 0.0 || w != W[(size_t)j * E + i])
+        return fail(ACE_ERR_INVALID_ARG, "W must be finite, non-negative and symmetric (entry %d,%d)", i, j);
+    }
+  *n_groups = louvain(W, E, gamma, groups);
+  return ok();
+}
+
+static ace_status check_groups(int32_t E, const int32_t* e2g, int32_t G) {
+  if (E < 1 || E > kMaxKeys) return fail(ACE_ERR_UNSUPPORTED, "expert count %d outside [1, %d]", E, kMaxKeys);
+  if (!e2g) return fail(ACE_ERR_INVALID_ARG, "expert_to_group is NULL");
+  if (G < 1 || G > E) return fail(ACE_ERR_INVALID_ARG, "group count %d outside [1, %d]", G, E);
+  std::vector<int> size(G, 0);
+  for (int e = 0; e < E; ++e) {
+    if (e2g[e] < 0 || e2g[e] >= G) return fail(ACE_ERR_INVALID_ARG, "group %d of expert %d outside [0, %d)", e2g[e], e, G);
+    ++size[e2g[e]];
+  }
+  for (int g = 0; g < G; ++g)
+    if (!size[g]) return fail(ACE_ERR_INVALID_ARG, "group %d has no expert", g);
+  return ok();
+}
+
+ace_status ace_group_anchors(const float* S, int32_t E, const int32_t* expert_to_group, int32_t G,
+                             int32_t* anchors) {
+  ace_status s = check_groups(E, expert_to_group, G);
+  if (s != ACE_OK) return s;
+  if (!S || !anchors) return fail(ACE_ERR_INVALID_ARG, "NULL argument");
+  group_anchors(S, E, expert_to_group, G, anchors);
+  return ok();
+}
+
+ace_status ace_consolidate_adapters(ace_dtype dtype, int32_t d_in, int32_t d_out, int32_t E,
+                                    int32_t rank, const void* A, const void* B,
+                                    const int32_t* expert_to_group, int32_t G,
+                                    const int32_t* anchors, const void* A_init, void* A_g,
+                                    void* B_g, void* stream) {
+  if (dtype != ACE_F32 && dtype != ACE_BF16) return fail(ACE_ERR_INVALID_ARG, "unknown dtype %d", (int)dtype);
+  ace_status s = check_groups(E, expert_to_group, G);
+  if (s != ACE_OK) return s;
+  const int vec = dtype == ACE_BF16 ? 8 : 4;
+  if (d_in < 1 || d_out < 1) return fail(ACE_ERR_INVALID_ARG, "d_in = %d, d_out = %d", d_in, d_out);
+  if (d_in % vec) return fail(ACE_ERR_UNSUPPORTED, "d_in (%d) must be a multiple of %d", d_in, vec);
+  if (rank < 1 || rank > kMaxRank) return fail(ACE_ERR_UNSUPPORTED, "rank %d outside [1, %d]", rank, kMaxRank);
+  if (!A || !B || !A_g || !B_g || !anchors || (G < E && !A_init))
+    return fail(ACE_ERR_INVALID_ARG, "NULL argument");
+  if (!aligned(A, 16) || !aligned(A_g, 16) || !aligned(A_init, 16))
+    return fail(ACE_ERR_INVALID_ARG, "A, A_init and A_g must be 16-byte aligned");
+  ConsolidateProblem p{};
+  p.d_in = d_in;
+  p.d_out = d_out;
+  p.r = rank;
+  p.A = A;
+  p.B = B;
+  p.A_init = A_init;
+  p.Ag = A_g;
+  p.Bg = B_g;
+  p.anchor = anchors;
+  p.keys.n_keys = G;
+  std::vector<int> size(G, 0);
+  for (int e = 0; e < E; ++e) ++size[expert_to_group[e]];
+  int R = 0;
+  for (int g = 0; g < G; ++g) {
+    if (anchors[g] < 0 || anchors[g] >= E || expert_to_group[anchors[g]] != g)
+      return fail(ACE_ERR_INVALID_ARG, "anchor %d of group %d is not one of its experts", anchors[g], g);
+    p.keys.rank[g] = size[g] * rank;
+    p.keys.roff[g] = R;
+    R += size[g] * rank;
+  }
+  p.keys.roff[G] = R;
+  p.keys.R = R;
+  return hip_status(launch_consolidate(dtype, p, static_cast<hipStream_t>(stream)),
+                    "consolidate launch");
 }
 
 size_t ace_workspace_bytes(ace_op op, int32_t T, int32_t k, int32_t d_in, int32_t d_out,

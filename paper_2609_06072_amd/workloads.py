@@ -295,3 +295,15 @@ def make_probe_adapters(cfg: MoEConfig, proj: str = "gate", N: int = 10000, nois
     return ProbeAdapters(X.to(dt).contiguous(), A.to(dt).contiguous(), B.to(dt).contiguous(),
                          clusters, d_in, d_out, E, r)
 
+
+def draw_lora_init_A(rows: int, d_in: int, seed: int = 0, dtype: str = "bf16", device: str = "cpu"):
+    """Standard LoRA initialisation of A rows (Kaiming-uniform with a = sqrt(5),
+    i.e. U(-1/sqrt(d_in), 1/sqrt(d_in))): the draw that fills the extra rank
+    rows of a consolidated group adapter.  torch [rows, d_in]."""
+    torch = _torch()
+    g = torch.Generator(device=device)
+    g.manual_seed(torch_seed_for(seed, "cka.A_init"))
+    t = (torch.rand(rows, d_in, generator=g, device=device, dtype=torch.float32) * 2 - 1)
+    t.mul_(1.0 / math.sqrt(d_in))
+    return t.to(torch.bfloat16 if dtype == "bf16" else torch.float32)
+
