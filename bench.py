@@ -318,6 +318,98 @@ def cpu_baseline(cfg, rt, budget_s=15.0):
                       f"({sum(times):.1f} s in total), {dt:.2f} s per run"}
 
 
+# ---------------------------------------------------------------- consolidation
+# The one-time consolidation step of Sec. 3.3 on one layer: pairwise CKA of
+# the expert adapters on the probe set (GPU), similarity graph + Louvain +
+# anchors (host), consolidated group adapters (GPU).
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+PAPER_CKA_S_PER_LAYER = 123.90 / 16   # OLMoE-1B-7B, 16 MoE layers, NVIDIA H200 (overhead table)
+
+
+def time_calls(fn, warmup=3, steps=20, repeats=5):
+    """Median ms per call over `repeats` runs of `steps` back-to-back calls
+    (HIP events on the current stream, which the library launches on)."""
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    out = []
+    for _ in range(repeats):
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        for _ in range(steps):
+            fn()
+        e.record()
+        torch.cuda.synchronize()
+        out.append(s.elapsed_time(e) / steps)
+    return statistics.median(out)
+
+
+def consolidation_bench(ace, cfg, seed, cpu=True, N=10000):
+    import torch
+    pa = W.make_probe_adapters(cfg, "gate", N=N, seed=seed, device="cuda")
+    E, r, d_in, d_out = pa.E, pa.r, pa.d_in, pa.d_out
+    R = E * r
+    S = torch.empty(E, E, dtype=torch.float32, device="cuda")
+    need = ace.ace_workspace_bytes(ace.ACE_OP_CKA, N, 1, d_in, d_out, E, r)
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    cka_ms = time_calls(lambda: ace.ace_pairwise_cka(pa.X, pa.A, pa.B, E, r, S=S, ws=ws))
+    torch.cuda.synchronize()
+    S_host = S.cpu().numpy()
+    t0 = time.perf_counter()
+    Wg = ace.ace_similarity_graph(S_host)
+    groups, G = ace.ace_louvain(Wg, 0.8)
+    anchors = ace.ace_group_anchors(S_host, groups, G)
+    host_ms = (time.perf_counter() - t0) * 1e3
+    A_init = W.draw_lora_init_A(max(1, (E - G) * r), d_in, seed=seed, dtype=cfg.dtype, device="cuda")
+    Ag, Bg, ranks = ace.ace_consolidate_adapters(pa.A, pa.B, E, r, groups, G, anchors, A_init)
+    cons_ms = time_calls(lambda: ace.ace_consolidate_adapters(pa.A, pa.B, E, r, groups, G, anchors,
+                                                             A_init, A_g=Ag, B_g=Bg))
+    # algorithmic work of one CKA call: X A^T on the storage type's matrix
+    # cores, the symmetric Gram of the centred projections in fp32
+    f_proj = 2.0 * N * d_in * R
+    f_gram = 1.0 * N * R * (R + 1)
+    t_min = f_proj / (MFMA_PEAK_TFLOPS[cfg.dtype] * 1e12) + f_gram / (MFMA_PEAK_TFLOPS["f32"] * 1e12)
+    pairs = E * (E + 1) // 2
+    planted = pa.clusters
+    out = {
+        "workload": f"{cfg.name} gate adapters: E={E} rank {r}, {d_in}->{d_out}, probe N={N}, "
+                    f"{cfg.dtype}; planted clusters {int(planted.max()) + 1}",
+        "cka_ms": cka_ms, "value": pairs / (cka_ms * 1e-3), "unit": "expert pairs/s",
+        "roofline": {"bound": "mfma", "algorithmic_flops": f_proj + f_gram,
+                     "achieved_tflops": (f_proj + f_gram) / (cka_ms * 1e-3) / 1e12,
+                     "ceiling_ms": t_min * 1e3, "frac": t_min / (cka_ms * 1e-3),
+                     "peaks_tflops": {"X A^T": MFMA_PEAK_TFLOPS[cfg.dtype],
+                                      "Gram": MFMA_PEAK_TFLOPS["f32"]}},
+        "grouping_host_ms": host_ms, "groups": G,
+        "groups_match_planted": bool(np.array_equal(planted[:, None] == planted[None, :],
+                                                    groups[:, None] == groups[None, :])),
+        "consolidate_ms": cons_ms,
+        "paper_cka_s_per_layer": {"value": PAPER_CKA_S_PER_LAYER, "hardware": "NVIDIA H200",
+                                  "note": "context: whole-pipeline CKA stage of the paper's overhead "
+                                          "table divided by OLMoE's 16 MoE layers; the paper's "
+                                          "implementation and probe precision are not given"},
+    }
+    if cpu:
+        from oracle import consolidation_oracle as C
+        X64 = pa.X.double().cpu().numpy()
+        A64 = pa.A.double().cpu().numpy()
+        B64 = pa.B.double().cpu().numpy()
+        sub_A = A64[:2 * r]
+        sub_B = B64[:2 * r * d_out]
+        times = []
+        while sum(times) < 10.0 and len(times) < 5:
+            t0 = time.perf_counter()
+            C.cka_matrix(X64, sub_A, sub_B, 2, r)
+            times.append(time.perf_counter() - t0)
+        dt = statistics.median(times)
+        out["cpu_baseline"] = {"value": 3 / dt, "unit": "expert pairs/s", "kind": "oracle",
+                               "sample": f"fp64 oracle (materialised Z_e) on experts 0 and 1 at the "
+                                         f"full probe (3 pairs incl. the diagonal); median of "
+                                         f"{len(times)} runs, {dt:.2f} s per run"}
+    return out
+
+
 # ---------------------------------------------------------------- HBM traffic
 # Traffic is taken from two rocprofv3 counter passes over `--traffic-pass`
 # (FETCH_SIZE, then WRITE_SIZE), summarised by `--pmc-summary` into
@@ -495,6 +587,27 @@ def trace_summary(trace_dir, fetch_dir, labels_path, config, command):
 kThreadsGuess = 256   # threads per workgroup of the library's kernels (grid printed in blocks)
 
 
+def stats_summary(trace_dir, name, command, keep=("cka_", "consolidate_")):
+    """profiles/kernels_<name>.txt from a rocprofv3 --stats kernel summary:
+    calls and average/min/max duration of the library's kernels."""
+    import csv
+    import glob
+    sf = glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True)
+    if not sf:
+        raise SystemExit(f"no kernel_stats.csv under {trace_dir}")
+    lines = [f"# kernel time, {name} (rocprofv3 --kernel-trace --stats)", f"source_hash {source_hash()}",
+             f"command {command}", "# kernel  calls  avg_us  min_us  max_us"]
+    for r in csv.DictReader(open(sf[0])):
+        k = short_kernel(r["Name"])
+        if any(t in r["Name"] for t in keep):
+            lines.append(f"{k} {r['Calls']} {float(r['AverageNs']) / 1e3:.2f} "
+                         f"{float(r['MinNs']) / 1e3:.2f} {float(r['MaxNs']) / 1e3:.2f}")
+    os.makedirs(PROFILES, exist_ok=True)
+    with open(os.path.join(PROFILES, f"kernels_{name}.txt"), "w") as out:
+        out.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def read_traffic(config: str):
     """{phase label: (fetch, write)} if the stored counters were taken on the
     current sources, else None."""
@@ -526,6 +639,12 @@ def main():
     ap.add_argument("--trace-summary", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "LABELS"),
                     help="write profiles/kernels_<config>.txt from a kernel trace of the bench")
     ap.add_argument("--pmc-command", default="", help="command recorded in the summary")
+    ap.add_argument("--stats-summary", nargs=2, metavar=("TRACE_DIR", "NAME"),
+                    help="write profiles/kernels_<NAME>.txt from a rocprofv3 --stats run")
+    ap.add_argument("--no-consolidation", action="store_true",
+                    help="skip the consolidation step (CKA, grouping, consolidated adapters)")
+    ap.add_argument("--consolidation-only", action="store_true",
+                    help="time only the consolidation step and print its object")
     args = ap.parse_args()
 
     if args.pmc_summary:
@@ -533,6 +652,9 @@ def main():
         return
     if args.trace_summary:
         trace_summary(*args.trace_summary, args.config, args.pmc_command)
+        return
+    if args.stats_summary:
+        stats_summary(*args.stats_summary, args.pmc_command)
         return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -545,8 +667,12 @@ def main():
     from paper_2609_06072_amd import ace
 
     cfg = W.CONFIGS[args.config]
-    rt = W.make_routing(cfg, args.seed)
     torch.cuda.set_device(0)
+    if args.consolidation_only:
+        print(json.dumps(consolidation_bench(ace, cfg, args.seed, cpu=not args.no_cpu_baseline)),
+              flush=True)
+        return
+    rt = W.make_routing(cfg, args.seed)
     bufs = make_buffers(cfg, rt, args.seed)
     b = 2 if cfg.dtype == "bf16" else 4
     r_max = max(int(rt.group_rank.max()), cfg.r_e)
@@ -662,6 +788,8 @@ def main():
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(cfg, rt)
+    if not args.no_consolidation and cfg.dtype == "bf16":
+        line["consolidation"] = consolidation_bench(ace, cfg, args.seed, cpu=not args.no_cpu_baseline)
     print(json.dumps(line), flush=True)
 
 

@@ -156,7 +156,7 @@ struct CkaProblem {
   const void* B;   // expert e: [d_out][r] at d_out * r * e
   float* S;        // [E][E]
 };
-size_t cka_ws_bytes(int N, int E, int r);
+size_t cka_ws_bytes(int N, int d_out, int E, int r);
 hipError_t launch_cka(const CkaProblem& p, void* ws, hipStream_t stream);
 
 // Expert grouping (host) and adapter consolidation (device).

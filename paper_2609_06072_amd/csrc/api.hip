@@ -282,7 +282,7 @@ ace_status ace_pairwise_cka(ace_dtype dtype, int32_t N, int32_t d_in, int32_t d_
   if (!A || !B || !S || (N > 0 && !X)) return fail(ACE_ERR_INVALID_ARG, "NULL argument");
   if (!aligned(X, 16) || !aligned(A, 16)) return fail(ACE_ERR_INVALID_ARG, "X and A must be 16-byte aligned");
   if (!aligned(S, 4) || !aligned(B, dtype == ACE_BF16 ? 2 : 4)) return fail(ACE_ERR_INVALID_ARG, "B or S misaligned");
-  const size_t need = cka_ws_bytes(N, E, rank);
+  const size_t need = cka_ws_bytes(N, d_out, E, rank);
   if (!ws || ws_bytes < need)
     return fail(ACE_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", ws_bytes, need);
   CkaProblem p{};
@@ -424,7 +424,7 @@ size_t ace_workspace_bytes(ace_op op, int32_t T, int32_t k, int32_t d_in, int32_
         fail(ACE_ERR_INVALID_ARG, "invalid workspace query");
         return (size_t)-1;
       }
-      return round256(cka_ws_bytes(T, n_keys, r_max));
+      return round256(cka_ws_bytes(T, d_out, n_keys, r_max));
   }
   fail(ACE_ERR_INVALID_ARG, "unknown op %d", (int)op);
   return (size_t)-1;

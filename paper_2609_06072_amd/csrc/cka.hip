@@ -12,12 +12,16 @@
 // exact up to rounding; no N x d_out matrix is ever formed.
 //
 // Launches (all deterministic):
-//   project -- Pt = A X^T, [R][ldp] fp32: a 128 x 128-tile MFMA GEMM over
+//   project -- Pt = A X^T, [R][ldp] fp32: a 64 x 128-tile MFMA GEMM over
 //              K = d_in, operands staged through LDS, double buffered
 //   mean    -- the probe mean of every row of Pt
 //   gram    -- partial M over chunks of the probe: upper-triangle 64 x 64
-//              tiles, centring on load, fp32 MFMA, one partial per chunk
-//   bgram   -- G_e = B_e^T B_e
+//              tiles, centring on load, one partial per chunk.  fp32
+//              inputs: fp32 MFMA.  bf16 inputs: the centred fp32 values are
+//              split as v = hi + lo (both bf16, |lo| <= 2^-9 |v|) and
+//              M = hi^T hi + hi^T lo + lo^T hi on the bf16 matrix cores
+//              (the dropped lo^T lo is below 2^-16 of |v_a v_b|)
+//   bgram   -- partial G_e = B_e^T B_e over chunks of 256 rows of B_e
 //   pairs   -- num_ij = <G_i M_ij, M_ij G_j> for i <= j (partials summed in
 //              chunk order)
 //   score   -- S_ij = num_ij / sqrt(num_ii num_jj); 0 when a norm is 0
@@ -28,35 +32,38 @@ namespace ace {
 
 namespace {
 
-constexpr int kPT = 128;   // projection tile edge (probe rows and adapter rows)
+constexpr int kPN = 64;    // projection tile: probe rows
+constexpr int kPC = 128;   // projection tile: adapter rows
 constexpr int kGT = 64;    // Gram tile edge
-constexpr int kGK = 1024;  // probe rows per Gram chunk (at least)
+constexpr int kGK = 512;   // probe rows per Gram chunk (at least)
+constexpr int kBO = 256;   // rows of B_e per B^T B chunk
 
 size_t a256(size_t b) { return (b + 255) & ~(size_t)255; }
 
 struct CkaLayout {
   size_t Pt, mean, part, Gb, num, total;
-  int ldp, splits, kchunk;
+  int ldp, splits, kchunk, nbo;
 };
 
-CkaLayout cka_layout(int N, int E, int r) {
+CkaLayout cka_layout(int N, int d_out, int E, int r) {
   CkaLayout L{};
   const size_t R = (size_t)E * r;
-  L.ldp = ((N > 0 ? N : 1) + 15) & ~15;
-  // chunks of the probe for the Gram: at least kGK rows each, at most 16
+  L.ldp = ((N > 0 ? N : 1) + 31) & ~31;
+  // chunks of the probe for the Gram: at least kGK rows each, at most 32
   // chunks, and at most 256 MB of partials
   int splits = (N + kGK - 1) / kGK;
   const size_t cap = (size_t)(256u << 20) / (R * R * 4 > 0 ? R * R * 4 : 1);
   if ((size_t)splits > cap) splits = (int)cap;
-  if (splits > 16) splits = 16;
+  if (splits > 32) splits = 32;
   if (splits < 1) splits = 1;
   L.splits = splits;
-  L.kchunk = (((N + splits - 1) / splits) + 15) & ~15;
+  L.kchunk = (((N + splits - 1) / splits) + 31) & ~31;
   size_t o = 0;
   L.Pt = o;   o += a256(R * L.ldp * 4);
   L.mean = o; o += a256(R * 4);
   L.part = o; o += a256((size_t)splits * R * R * 4);
-  L.Gb = o;   o += a256((size_t)E * r * r * 4);
+  L.nbo = (d_out + kBO - 1) / kBO;
+  L.Gb = o;   o += a256((size_t)E * L.nbo * r * r * 4);
   L.num = o;  o += a256((size_t)E * E * 4);
   L.total = o;
   return L;
@@ -69,10 +76,10 @@ struct CkaArgs {
   float* Pt;         // [R][ldp]
   float* mean;       // [R]
   float* part;       // [splits][R][R]
-  float* Gb;         // [E][r][r]
+  float* Gb;         // [E][nbo][r][r] partials of B_e^T B_e
   float* num;        // [E][E]
   float* S;          // [E][E]
-  int32_t N, d_in, d_out, E, r, R, ldp, splits, kchunk;
+  int32_t N, d_in, d_out, E, r, R, ldp, splits, kchunk, nbo;
 };
 
 // Upper-triangle index p -> (a, b), a <= b < n, row-major.
@@ -93,42 +100,46 @@ __global__ __launch_bounds__(kThreads) void cka_project_kernel(CkaArgs a) {
   using F = typename Tr<T>::frag;
   constexpr int PER = Tr<T>::PER, KB = Tr<T>::KB;
   constexpr int RS = KB + PER;  // LDS row stride in elements (80 bytes: conflict-free fragments)
-  __shared__ __attribute__((aligned(16))) T xs[2][kPT * RS];
-  __shared__ __attribute__((aligned(16))) T as[2][kPT * RS];
+  __shared__ __attribute__((aligned(16))) T xs[2][kPN * RS];
+  __shared__ __attribute__((aligned(16))) T as[2][kPC * RS];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int c16 = lane & 15, g = lane >> 4;
-  const int n0 = blockIdx.x * kPT, c0 = blockIdx.y * kPT;
-  const int wn = (wave & 1) * 64, wc = (wave >> 1) * 64;
+  const int n0 = blockIdx.x * kPN, c0 = blockIdx.y * kPC;
+  const int wn = (wave & 1) * 32, wc = (wave >> 1) * 64;   // wave: 32 probe rows x 64 adapter rows
   const T* X = static_cast<const T*>(a.X);
   const T* A = static_cast<const T*>(a.A);
   const int N = a.N, R = a.R, d_in = a.d_in;
 
-  // a stage is KB contraction indices (64 bytes) of 128 rows of each operand:
-  // 512 16-byte pieces per operand, two per thread
-  F xr[2], ar[2];
+  // a stage is KB contraction indices (64 bytes) of the tile's rows: 256
+  // 16-byte pieces of X (one per thread) and 512 of A (two per thread)
+  F xr, ar[2];
   auto load_stage = [&](int k0) {
+    {
+      const int row = tid >> 2, kk = k0 + (tid & 3) * PER;
+      const bool ok = kk < d_in;  // d_in is a multiple of PER: a piece is wholly in or out
+      const F v = Tr<T>::load(X + (size_t)min(n0 + row, N - 1) * d_in + (ok ? kk : 0));
+      xr = ok ? v : Tr<T>::zero();
+    }
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int id = tid + kThreads * i, row = id >> 2, kk = k0 + (id & 3) * PER;
-      const bool ok = kk < d_in;  // d_in is a multiple of PER: a piece is wholly in or out
-      const F xv = Tr<T>::load(X + (size_t)min(n0 + row, N - 1) * d_in + (ok ? kk : 0));
-      const F av = Tr<T>::load(A + (size_t)min(c0 + row, R - 1) * d_in + (ok ? kk : 0));
-      xr[i] = ok ? xv : Tr<T>::zero();
-      ar[i] = ok ? av : Tr<T>::zero();
+      const bool ok = kk < d_in;
+      const F v = Tr<T>::load(A + (size_t)min(c0 + row, R - 1) * d_in + (ok ? kk : 0));
+      ar[i] = ok ? v : Tr<T>::zero();
     }
   };
   auto store_stage = [&](int buf) {
+    *reinterpret_cast<F*>(&xs[buf][(tid >> 2) * RS + (tid & 3) * PER]) = xr;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      const int id = tid + kThreads * i, row = id >> 2, ch = id & 3;
-      *reinterpret_cast<F*>(&xs[buf][row * RS + ch * PER]) = xr[i];
-      *reinterpret_cast<F*>(&as[buf][row * RS + ch * PER]) = ar[i];
+      const int id = tid + kThreads * i;
+      *reinterpret_cast<F*>(&as[buf][(id >> 2) * RS + (id & 3) * PER]) = ar[i];
     }
   };
 
-  f32x4 acc[4][4];
+  f32x4 acc[2][4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
@@ -139,14 +150,15 @@ __global__ __launch_bounds__(kThreads) void cka_project_kernel(CkaArgs a) {
   for (int k0 = 0; k0 < d_in; k0 += KB) {
     const bool more = k0 + KB < d_in;
     if (more) load_stage(k0 + KB);
-    F xf[4], af[4];
+    F xf[2], af[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < 2; ++j)
       xf[j] = *reinterpret_cast<const F*>(&xs[buf][(wn + 16 * j + c16) * RS + g * PER]);
-      af[j] = *reinterpret_cast<const F*>(&as[buf][(wc + 16 * j + c16) * RS + g * PER]);
-    }
 #pragma unroll
-    for (int jn = 0; jn < 4; ++jn)
+    for (int j = 0; j < 4; ++j)
+      af[j] = *reinterpret_cast<const F*>(&as[buf][(wc + 16 * j + c16) * RS + g * PER]);
+#pragma unroll
+    for (int jn = 0; jn < 2; ++jn)
 #pragma unroll
       for (int jc = 0; jc < 4; ++jc) acc[jn][jc] = Tr<T>::mma(xf[jn], af[jc], acc[jn][jc]);
     if (more) store_stage(buf ^ 1);
@@ -156,7 +168,7 @@ __global__ __launch_bounds__(kThreads) void cka_project_kernel(CkaArgs a) {
   // acc[jn][jc] element v = P[n][c] with n = n0+wn+16jn+4g+v, c = c0+wc+16jc+c16:
   // four consecutive probe rows of Pt row c per lane
 #pragma unroll
-  for (int jn = 0; jn < 4; ++jn)
+  for (int jn = 0; jn < 2; ++jn)
 #pragma unroll
     for (int jc = 0; jc < 4; ++jc) {
       const int c = c0 + wc + 16 * jc + c16, n = n0 + wn + 16 * jn + 4 * g;
@@ -177,9 +189,16 @@ __global__ __launch_bounds__(kThreads) void cka_project_kernel(CkaArgs a) {
 
 __global__ __launch_bounds__(kThreads) void cka_mean_kernel(CkaArgs a) {
   __shared__ float red[kThreads];
-  const float* row = a.Pt + (size_t)blockIdx.x * a.ldp;
+  // ldp is a multiple of 16: whole 16-byte pieces, entries past N masked
+  const f32x4* row = reinterpret_cast<const f32x4*>(a.Pt + (size_t)blockIdx.x * a.ldp);
+  const int n4 = (a.N + 3) / 4;
   float s = 0.f;
-  for (int n = threadIdx.x; n < a.N; n += kThreads) s += row[n];
+#pragma unroll 4
+  for (int i = threadIdx.x; i < n4; i += kThreads) {
+    const f32x4 v = row[i];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) s += 4 * i + e < a.N ? v[e] : 0.f;
+  }
   red[threadIdx.x] = s;
   __syncthreads();
   for (int w = kThreads / 2; w > 0; w >>= 1) {
@@ -193,8 +212,13 @@ __global__ __launch_bounds__(kThreads) void cka_mean_kernel(CkaArgs a) {
 
 // Block (tile pair p, chunk s): the 64 x 64 tile (ta, tb), ta <= tb, of
 // sum over the chunk's probe rows of (Pt[a][n] - mean[a]) (Pt[b][n] - mean[b]).
-// Wave w owns a 32 x 32 quarter; fragments are 16-byte loads of Pt rows.
+// Wave w owns a 32 x 32 quarter; fragments are read straight from the Pt rows
+// (contiguous along the probe).  SPLIT: bf16 matrix cores on the hi/lo split
+// (K-blocks of 32), else fp32 matrix cores (K-blocks of 16).
+template <bool SPLIT>
 __global__ __launch_bounds__(kThreads) void cka_gram_kernel(CkaArgs a) {
+  constexpr int KS = SPLIT ? 32 : 16;      // probe rows per MFMA K-block
+  constexpr int PL = KS / 4;               // probe rows per lane per K-block
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int c16 = lane & 15, g = lane >> 4;
   const int R = a.R;
@@ -220,36 +244,62 @@ __global__ __launch_bounds__(kThreads) void cka_gram_kernel(CkaArgs a) {
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  constexpr int U = 4;  // 16-row steps loaded ahead of their MFMAs
-  for (int k = k_beg; k < k_end; k += 16 * U) {
-    f32x4 fa[U][2], fb[U][2];
+  constexpr int U = SPLIT ? 2 : 4;  // K-blocks loaded ahead of their MFMAs
+  for (int k = k_beg; k < k_end; k += KS * U) {
+    f32x4 fa[U][2][PL / 4], fb[U][2][PL / 4];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       // rows past k_end (the chunk end, <= ldp) are read but masked below;
-      // starts are multiples of 16 and ldp is too, so a fragment never
-      // crosses the end of its Pt row
-      const int kk = min(k + 16 * u, a.ldp - 16) + 4 * g;
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        fa[u][j] = *reinterpret_cast<const f32x4*>(pa[j] + kk);
-        fb[u][j] = *reinterpret_cast<const f32x4*>(pb[j] + kk);
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int kk = k + 16 * u + 4 * g;
+      // chunk starts are multiples of 32, ldp of 16 and the start is clamped
+      // so that a fragment never crosses the end of its Pt row
+      const int kk = min(k + KS * u, a.ldp - KS) + PL * g;
 #pragma unroll
       for (int j = 0; j < 2; ++j)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const bool ok = kk + e < k_end;
-          fa[u][j][e] = ok ? fa[u][j][e] - ma[j] : 0.f;
-          fb[u][j][e] = ok ? fb[u][j][e] - mb[j] : 0.f;
+        for (int h = 0; h < PL / 4; ++h) {
+          fa[u][j][h] = *reinterpret_cast<const f32x4*>(pa[j] + kk + 4 * h);
+          fb[u][j][h] = *reinterpret_cast<const f32x4*>(pb[j] + kk + 4 * h);
         }
+    }
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+    for (int u = 0; u < U; ++u) {
+      const int kk = k + KS * u + PL * g;
+      float va[2][PL], vb[2][PL];
 #pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = Tr<float>::mma(fa[u][i], fb[u][j], acc[i][j]);
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int e = 0; e < PL; ++e) {
+          const bool ok = kk + e < k_end;
+          va[j][e] = ok ? fa[u][j][e / 4][e % 4] - ma[j] : 0.f;
+          vb[j][e] = ok ? fb[u][j][e / 4][e % 4] - mb[j] : 0.f;
+        }
+      if constexpr (SPLIT) {
+        bf16x8 ha[2], la[2], hb[2], lb[2];
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            ha[j][e] = (__bf16)va[j][e];
+            la[j][e] = (__bf16)(va[j][e] - (float)ha[j][e]);
+            hb[j][e] = (__bf16)vb[j][e];
+            lb[j][e] = (__bf16)(vb[j][e] - (float)hb[j][e]);
+          }
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j) {
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(la[i], hb[j], acc[i][j], 0, 0, 0);
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ha[i], lb[j], acc[i][j], 0, 0, 0);
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ha[i], hb[j], acc[i][j], 0, 0, 0);
+          }
+      } else {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            acc[i][j] = Tr<float>::mma(f32x4{va[i][0], va[i][1], va[i][2], va[i][3]},
+                                       f32x4{vb[j][0], vb[j][1], vb[j][2], vb[j][3]}, acc[i][j]);
+      }
     }
   }
   float* out = a.part + (size_t)s * R * R;
@@ -268,35 +318,21 @@ __global__ __launch_bounds__(kThreads) void cka_gram_kernel(CkaArgs a) {
 
 // ---------------------------------------------------------------- B^T B
 
+// Block (e, c): partial G_e over rows c*kBO .. of B_e, all rows loaded at once.
 template <typename T>
 __global__ __launch_bounds__(kThreads) void cka_bgram_kernel(CkaArgs a) {
-  constexpr int CH = 64;                 // rows of B_e staged per step
-  __shared__ float bs[CH * 64];
-  const int e = blockIdx.x, r = a.r, rr = r * r;
-  const T* B = static_cast<const T*>(a.B) + (size_t)a.d_out * r * e;
-  float acc[16];
-#pragma unroll
-  for (int i = 0; i < 16; ++i) acc[i] = 0.f;
-  for (int o0 = 0; o0 < a.d_out; o0 += CH) {
-    const int rows = min(CH, a.d_out - o0);
-    __syncthreads();
-    for (int i = threadIdx.x; i < rows * r; i += kThreads) bs[i] = (float)B[(size_t)o0 * r + i];
-    __syncthreads();
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int pq = threadIdx.x + kThreads * i;
-      if (pq < rr) {
-        const int p = pq / r, q = pq % r;
-        float s = acc[i];
-        for (int o = 0; o < rows; ++o) s += bs[o * r + p] * bs[o * r + q];
-        acc[i] = s;
-      }
-    }
-  }
-#pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const int pq = threadIdx.x + kThreads * i;
-    if (pq < rr) a.Gb[(size_t)e * rr + pq] = acc[i];
+  __shared__ float bs[kBO * 64];
+  const int e = blockIdx.x, c = blockIdx.y, r = a.r, rr = r * r;
+  const int o0 = c * kBO, rows = min(kBO, a.d_out - o0);
+  const T* B = static_cast<const T*>(a.B) + (size_t)a.d_out * r * e + (size_t)o0 * r;
+#pragma unroll 8
+  for (int i = threadIdx.x; i < rows * r; i += kThreads) bs[i] = (float)B[i];
+  __syncthreads();
+  for (int pq = threadIdx.x; pq < rr; pq += kThreads) {
+    const int p = pq / r, q = pq % r;
+    float acc = 0.f;
+    for (int o = 0; o < rows; ++o) acc += bs[o * r + p] * bs[o * r + q];
+    a.Gb[((size_t)e * a.nbo + c) * rr + pq] = acc;
   }
 }
 
@@ -311,8 +347,13 @@ __global__ __launch_bounds__(kThreads) void cka_pairs_kernel(CkaArgs a) {
   upper_pair(blockIdx.x, a.E, &i, &j);
   const int r = a.r, rr = r * r, R = a.R;
   for (int t = threadIdx.x; t < rr; t += kThreads) {
-    Gi[t] = a.Gb[(size_t)i * rr + t];
-    Gj[t] = a.Gb[(size_t)j * rr + t];
+    float gi = 0.f, gj = 0.f;
+    for (int c = 0; c < a.nbo; ++c) {
+      gi += a.Gb[((size_t)i * a.nbo + c) * rr + t];
+      gj += a.Gb[((size_t)j * a.nbo + c) * rr + t];
+    }
+    Gi[t] = gi;
+    Gj[t] = gj;
     const int row = i * r + t / r, col = j * r + t % r;
     const size_t off = (size_t)min(row, col) * R + max(row, col);
     float m = 0.f;
@@ -354,7 +395,7 @@ __global__ __launch_bounds__(kThreads) void cka_score_kernel(CkaArgs a) {
 
 template <typename T>
 hipError_t launch_cka_t(const CkaProblem& p, void* ws, hipStream_t stream) {
-  const CkaLayout L = cka_layout(p.N, p.E, p.r);
+  const CkaLayout L = cka_layout(p.N, p.d_out, p.E, p.r);
   char* base = static_cast<char*>(ws);
   CkaArgs a{};
   a.X = p.X;
@@ -375,18 +416,22 @@ hipError_t launch_cka_t(const CkaProblem& p, void* ws, hipStream_t stream) {
   a.ldp = L.ldp;
   a.splits = L.splits;
   a.kchunk = L.kchunk;
+  a.nbo = L.nbo;
   const int R = a.R;
   if (p.N > 0) {
-    dim3 grid((p.N + kPT - 1) / kPT, (R + kPT - 1) / kPT);
+    dim3 grid((p.N + kPN - 1) / kPN, (R + kPC - 1) / kPC);
     cka_project_kernel<T><<<grid, kThreads, 0, stream>>>(a);
   }
   cka_mean_kernel<<<R, kThreads, 0, stream>>>(a);
   {
     const int nt = (R + kGT - 1) / kGT;
     dim3 grid(nt * (nt + 1) / 2, L.splits);
-    cka_gram_kernel<<<grid, kThreads, 0, stream>>>(a);
+    if (p.dtype == ACE_BF16)
+      cka_gram_kernel<true><<<grid, kThreads, 0, stream>>>(a);
+    else
+      cka_gram_kernel<false><<<grid, kThreads, 0, stream>>>(a);
   }
-  cka_bgram_kernel<T><<<p.E, kThreads, 0, stream>>>(a);
+  cka_bgram_kernel<T><<<dim3(p.E, L.nbo), kThreads, 0, stream>>>(a);
   cka_pairs_kernel<<<p.E * (p.E + 1) / 2, kThreads, 0, stream>>>(a);
   cka_score_kernel<<<(p.E * p.E + kThreads - 1) / kThreads, kThreads, 0, stream>>>(a);
   return hipGetLastError();
@@ -394,7 +439,7 @@ hipError_t launch_cka_t(const CkaProblem& p, void* ws, hipStream_t stream) {
 
 }  // namespace
 
-size_t cka_ws_bytes(int N, int E, int r) { return cka_layout(N, E, r).total; }
+size_t cka_ws_bytes(int N, int d_out, int E, int r) { return cka_layout(N, d_out, E, r).total; }
 
 hipError_t launch_cka(const CkaProblem& p, void* ws, hipStream_t stream) {
   if (p.dtype == ACE_BF16) return launch_cka_t<__bf16>(p, ws, stream);
