@@ -535,7 +535,8 @@ def trace_summary(trace_dir, fetch_dir, labels_path, config, command):
     ph = _split_phases(_pmc_by_dispatch(fetch_dir, "FETCH_SIZE", with_grid=True), labels)
     tf = glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True)[0]
     rows = sorted(csv.DictReader(open(tf)), key=lambda r: int(r["Dispatch_Id"]))
-    trace = [((r["Kernel_Name"], int(r["Grid_Size_X"])),
+    # the counter pass records the whole grid (x * y * z threads)
+    trace = [((r["Kernel_Name"], int(r["Grid_Size_X"]) * int(r["Grid_Size_Y"]) * int(r["Grid_Size_Z"])),
               (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3) for r in rows]
     keys = [t[0] for t in trace]
     lines = [f"# kernel time per call, {config} (rocprofv3 kernel trace)", f"source_hash {source_hash()}",
