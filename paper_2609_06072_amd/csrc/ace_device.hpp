@@ -276,4 +276,19 @@ __device__ inline void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
+// s_waitcnt vmcnt(n) for a wave-uniform 0 <= n <= N
+template <int N>
+__device__ inline void wait_vmcnt_upto(int n) {
+  if constexpr (N > 0) {
+    if (n >= N) {
+      wait_vmcnt<N>();
+      return;
+    }
+    wait_vmcnt_upto<N - 1>(n);
+  } else {
+    (void)n;
+    wait_vmcnt<0>();
+  }
+}
+
 }  // namespace ace

@@ -13,14 +13,15 @@
 //
 // Launches (all deterministic):
 //   project -- Pt = A X^T, [R][ldp] fp32: a 64 x 128-tile MFMA GEMM over
-//              K = d_in, operands staged through LDS, double buffered
-//   mean    -- the probe mean of every row of Pt
+//              K = d_in, operands copied global -> LDS directly, four
+//              stages in flight
+//   mean    -- the probe mean of every row of Pt; bf16 inputs: also the
+//              centred rows split as v = hi + lo (both bf16, |lo| <= 2^-9 |v|)
 //   gram    -- partial M over chunks of the probe: upper-triangle 64 x 64
-//              tiles, centring on load, one partial per chunk.  fp32
-//              inputs: fp32 MFMA.  bf16 inputs: the centred fp32 values are
-//              split as v = hi + lo (both bf16, |lo| <= 2^-9 |v|) and
-//              M = hi^T hi + hi^T lo + lo^T hi on the bf16 matrix cores
-//              (the dropped lo^T lo is below 2^-16 of |v_a v_b|)
+//              tiles, one partial per chunk.  bf16 inputs:
+//              M = hi^T hi + hi^T lo + lo^T hi on the bf16 matrix cores (the
+//              dropped lo^T lo is below 2^-16 of |v_a v_b|).  fp32 inputs:
+//              fp32 MFMA, centring on load.
 //   bgram   -- partial G_e = B_e^T B_e over chunks of 256 rows of B_e
 //   pairs   -- num_ij = <G_i M_ij, M_ij G_j> for i <= j (partials summed in
 //              chunk order)
@@ -41,7 +42,7 @@ constexpr int kBO = 256;   // rows of B_e per B^T B chunk
 size_t a256(size_t b) { return (b + 255) & ~(size_t)255; }
 
 struct CkaLayout {
-  size_t Pt, mean, part, Gb, num, total;
+  size_t Pt, mean, part, Gb, num, Phi, Plo, total;
   int ldp, splits, kchunk, nbo;
 };
 
@@ -65,6 +66,8 @@ CkaLayout cka_layout(int N, int d_out, int E, int r) {
   L.nbo = (d_out + kBO - 1) / kBO;
   L.Gb = o;   o += a256((size_t)E * L.nbo * r * r * 4);
   L.num = o;  o += a256((size_t)E * E * 4);
+  L.Phi = o;  o += a256(R * L.ldp * 2);
+  L.Plo = o;  o += a256(R * L.ldp * 2);
   L.total = o;
   return L;
 }
@@ -78,6 +81,8 @@ struct CkaArgs {
   float* part;       // [splits][R][R]
   float* Gb;         // [E][nbo][r][r] partials of B_e^T B_e
   float* num;        // [E][E]
+  __bf16* Phi;       // [R][ldp] centred Pt split as hi + lo (bf16 inputs; zero past N)
+  __bf16* Plo;
   float* S;          // [E][E]
   int32_t N, d_in, d_out, E, r, R, ldp, splits, kchunk, nbo;
 };
@@ -95,13 +100,24 @@ __device__ inline void upper_pair(int p, int n, int* a, int* b) {
 
 // ---------------------------------------------------------------- project
 
+// A block takes 64 probe rows x 128 adapter rows; wave (wn, wc) owns 32 x 64.
+// Stages of one K-block (64 bytes of every row) of both operands are copied
+// global -> LDS with global_load_lds_dwordx4, NBUF stages in flight (no
+// register staging).  A copy instruction moves 16 rows; lane l lands at row
+// l/4, position l%4 of the 64-byte LDS row and fetches the global 16-byte
+// chunk (l%4) ^ sw(row), sw(row) = (row >> 2) & 3, so that the 16 rows one
+// fragment read touches fall in distinct banks.  Chunks past d_in (a
+// multiple of 16 bytes) are fetched clamped and zeroed at the read.
+__device__ inline int cka_sw(int row) { return (row >> 2) & 3; }
+
 template <typename T>
 __global__ __launch_bounds__(kThreads) void cka_project_kernel(CkaArgs a) {
   using F = typename Tr<T>::frag;
-  constexpr int PER = Tr<T>::PER, KB = Tr<T>::KB;
-  constexpr int RS = KB + PER;  // LDS row stride in elements (80 bytes: conflict-free fragments)
-  __shared__ __attribute__((aligned(16))) T xs[2][kPN * RS];
-  __shared__ __attribute__((aligned(16))) T as[2][kPC * RS];
+  constexpr int PER = Tr<T>::PER, KB = Tr<T>::KB;   // KB * sizeof(T) = 64 bytes
+  constexpr int NBUF = 4;
+  constexpr int XB = kPN * 64, AB = kPC * 64;       // stage bytes of each operand
+  __shared__ __attribute__((aligned(16))) char xs[NBUF][XB];
+  __shared__ __attribute__((aligned(16))) char as[NBUF][AB];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int c16 = lane & 15, g = lane >> 4;
   const int n0 = blockIdx.x * kPN, c0 = blockIdx.y * kPC;
@@ -109,33 +125,35 @@ __global__ __launch_bounds__(kThreads) void cka_project_kernel(CkaArgs a) {
   const T* X = static_cast<const T*>(a.X);
   const T* A = static_cast<const T*>(a.A);
   const int N = a.N, R = a.R, d_in = a.d_in;
+  const int nst = (d_in + KB - 1) / KB;
 
-  // a stage is KB contraction indices (64 bytes) of the tile's rows: 256
-  // 16-byte pieces of X (one per thread) and 512 of A (two per thread)
-  F xr, ar[2];
-  auto load_stage = [&](int k0) {
-    {
-      const int row = tid >> 2, kk = k0 + (tid & 3) * PER;
-      const bool ok = kk < d_in;  // d_in is a multiple of PER: a piece is wholly in or out
-      const F v = Tr<T>::load(X + (size_t)min(n0 + row, N - 1) * d_in + (ok ? kk : 0));
-      xr = ok ? v : Tr<T>::zero();
-    }
+  // copy plan: X rows 16w .. 16w+15 (one instruction per wave), A rows
+  // 32w .. 32w+31 (two); lane l copies row (l >> 2) of its instruction
+  // (a chunk past d_in is fetched from column d_in - PER instead, inside the
+  // row, and zeroed at the read)
+  const int crow = lane >> 2, cpos = lane & 3;
+  const int xr = 16 * wave + crow;
+  const T* xsrc = X + (size_t)min(n0 + xr, N - 1) * d_in;
+  const int xch = PER * (cpos ^ cka_sw(xr));
+  const T* asrc[2];
+  int ach[2];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int id = tid + kThreads * i, row = id >> 2, kk = k0 + (id & 3) * PER;
-      const bool ok = kk < d_in;
-      const F v = Tr<T>::load(A + (size_t)min(c0 + row, R - 1) * d_in + (ok ? kk : 0));
-      ar[i] = ok ? v : Tr<T>::zero();
-    }
-  };
-  auto store_stage = [&](int buf) {
-    *reinterpret_cast<F*>(&xs[buf][(tid >> 2) * RS + (tid & 3) * PER]) = xr;
+  for (int i = 0; i < 2; ++i) {
+    const int ar = 32 * wave + 16 * i + crow;
+    asrc[i] = A + (size_t)min(c0 + ar, R - 1) * d_in;
+    ach[i] = PER * (cpos ^ cka_sw(ar));
+  }
+  auto issue = [&](int st) {
+    const int b = st % NBUF;
+    const int k0 = st * KB;
+    dma16(xsrc + min(k0 + xch, d_in - PER),
+          __builtin_amdgcn_readfirstlane(lds_addr(&xs[b][16 * wave * 64])));
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int id = tid + kThreads * i;
-      *reinterpret_cast<F*>(&as[buf][(id >> 2) * RS + (id & 3) * PER]) = ar[i];
-    }
+    for (int i = 0; i < 2; ++i)
+      dma16(asrc[i] + min(k0 + ach[i], d_in - PER),
+            __builtin_amdgcn_readfirstlane(lds_addr(&as[b][(32 * wave + 16 * i) * 64])));
   };
+  constexpr int PER_STAGE = 3;   // copies per wave per stage
 
   f32x4 acc[2][4];
 #pragma unroll
@@ -143,27 +161,35 @@ __global__ __launch_bounds__(kThreads) void cka_project_kernel(CkaArgs a) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  load_stage(0);
-  store_stage(0);
-  __syncthreads();
-  int buf = 0;
-  for (int k0 = 0; k0 < d_in; k0 += KB) {
-    const bool more = k0 + KB < d_in;
-    if (more) load_stage(k0 + KB);
+#pragma unroll
+  for (int p = 0; p < NBUF - 1; ++p)
+    if (p < nst) issue(p);
+  for (int st = 0; st < nst; ++st) {
+    // this wave's copies of stage st are done once at most those of the
+    // stages issued after it are outstanding; the barrier publishes them
+    wait_vmcnt_upto<(NBUF - 2) * PER_STAGE>(min(NBUF - 2, nst - 1 - st) * PER_STAGE);
+    __syncthreads();
+    if (st + NBUF - 1 < nst) issue(st + NBUF - 1);
+    const int b = st % NBUF;
+    // chunk g of this K-block holds k = st*KB + PER*g .. (a full chunk or none)
+    const bool kin = st * KB + PER * g < d_in;
     F xf[2], af[4];
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
-      xf[j] = *reinterpret_cast<const F*>(&xs[buf][(wn + 16 * j + c16) * RS + g * PER]);
+    for (int j = 0; j < 2; ++j) {
+      const int r = wn + 16 * j + c16;
+      const F v = *reinterpret_cast<const F*>(&xs[b][r * 64 + 16 * (g ^ cka_sw(r))]);
+      xf[j] = kin ? v : Tr<T>::zero();
+    }
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      af[j] = *reinterpret_cast<const F*>(&as[buf][(wc + 16 * j + c16) * RS + g * PER]);
+    for (int j = 0; j < 4; ++j) {
+      const int r = wc + 16 * j + c16;
+      const F v = *reinterpret_cast<const F*>(&as[b][r * 64 + 16 * (g ^ cka_sw(r))]);
+      af[j] = kin ? v : Tr<T>::zero();
+    }
 #pragma unroll
     for (int jn = 0; jn < 2; ++jn)
 #pragma unroll
       for (int jc = 0; jc < 4; ++jc) acc[jn][jc] = Tr<T>::mma(xf[jn], af[jc], acc[jn][jc]);
-    if (more) store_stage(buf ^ 1);
-    __syncthreads();
-    buf ^= 1;
   }
   // acc[jn][jc] element v = P[n][c] with n = n0+wn+16jn+4g+v, c = c0+wc+16jc+c16:
   // four consecutive probe rows of Pt row c per lane
@@ -187,9 +213,13 @@ __global__ __launch_bounds__(kThreads) void cka_project_kernel(CkaArgs a) {
 
 // ---------------------------------------------------------------- mean
 
+// Block c: the probe mean of Pt row c; with SPLIT, also the centred row split
+// as v = hi + lo in bf16 (hi = v rounded, lo = the remainder rounded), zero
+// from N up to ldp, so the Gram reads ready matrix-core operands.
+template <bool SPLIT>
 __global__ __launch_bounds__(kThreads) void cka_mean_kernel(CkaArgs a) {
   __shared__ float red[kThreads];
-  // ldp is a multiple of 16: whole 16-byte pieces, entries past N masked
+  // ldp is a multiple of 32: whole 16-byte pieces, entries past N masked
   const f32x4* row = reinterpret_cast<const f32x4*>(a.Pt + (size_t)blockIdx.x * a.ldp);
   const int n4 = (a.N + 3) / 4;
   float s = 0.f;
@@ -205,7 +235,25 @@ __global__ __launch_bounds__(kThreads) void cka_mean_kernel(CkaArgs a) {
     if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
     __syncthreads();
   }
-  if (threadIdx.x == 0) a.mean[blockIdx.x] = a.N > 0 ? red[0] / (float)a.N : 0.f;
+  const float mean = a.N > 0 ? red[0] / (float)a.N : 0.f;
+  if (threadIdx.x == 0) a.mean[blockIdx.x] = mean;
+  if constexpr (SPLIT) {
+    bf16x4* hi = reinterpret_cast<bf16x4*>(a.Phi + (size_t)blockIdx.x * a.ldp);
+    bf16x4* lo = reinterpret_cast<bf16x4*>(a.Plo + (size_t)blockIdx.x * a.ldp);
+#pragma unroll 4
+    for (int i = threadIdx.x; i < a.ldp / 4; i += kThreads) {
+      const f32x4 v = row[min(i, max(n4 - 1, 0))];
+      bf16x4 h, l;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float c = 4 * i + e < a.N ? v[e] - mean : 0.f;
+        h[e] = (__bf16)c;
+        l[e] = (__bf16)(c - (float)h[e]);
+      }
+      hi[i] = h;
+      lo[i] = l;
+    }
+  }
 }
 
 // ---------------------------------------------------------------- gram
@@ -216,7 +264,83 @@ __global__ __launch_bounds__(kThreads) void cka_mean_kernel(CkaArgs a) {
 // (contiguous along the probe).  SPLIT: bf16 matrix cores on the hi/lo split
 // (K-blocks of 32), else fp32 matrix cores (K-blocks of 16).
 template <bool SPLIT>
-__global__ __launch_bounds__(kThreads) void cka_gram_kernel(CkaArgs a) {
+__global__ __launch_bounds__(kThreads) void cka_gram_kernel(CkaArgs a);
+
+// bf16 inputs: hi/lo fragments straight from Phi/Plo (centred, zero past N);
+// a chunk is a whole number of 32-row K-blocks, so nothing is masked.
+template <>
+__global__ __launch_bounds__(kThreads) void cka_gram_kernel<true>(CkaArgs a) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int c16 = lane & 15, g = lane >> 4;
+  const int R = a.R;
+  const int nt = (R + kGT - 1) / kGT;
+  int ta, tb;
+  upper_pair(blockIdx.x, nt, &ta, &tb);
+  const int s = blockIdx.y;
+  const int abase = ta * kGT + (wave & 1) * 32, bbase = tb * kGT + (wave >> 1) * 32;
+  const int k_beg = s * a.kchunk;
+  const int k_end = min(((a.N + 31) & ~31), k_beg + a.kchunk);   // <= ldp
+  const __bf16* ph[2][2];   // [operand a/b][j]
+  const __bf16* pl[2][2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const size_t ra = (size_t)min(abase + 16 * j + c16, R - 1) * a.ldp;
+    const size_t rb = (size_t)min(bbase + 16 * j + c16, R - 1) * a.ldp;
+    ph[0][j] = a.Phi + ra + 8 * g;
+    pl[0][j] = a.Plo + ra + 8 * g;
+    ph[1][j] = a.Phi + rb + 8 * g;
+    pl[1][j] = a.Plo + rb + 8 * g;
+  }
+  f32x4 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  constexpr int U = 4;   // K-blocks loaded ahead of their MFMAs
+  for (int k = k_beg; k < k_end; k += 32 * U) {
+    bf16x8 fh[U][2][2], fl[U][2][2];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int kk = min(k + 32 * u, k_end - 32);   // past the chunk: re-read, not used
+#pragma unroll
+      for (int o = 0; o < 2; ++o)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          fh[u][o][j] = Tr<__bf16>::load(ph[o][j] + kk);
+          fl[u][o][j] = Tr<__bf16>::load(pl[o][j] + kk);
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (k + 32 * u >= k_end) break;
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fl[u][0][i], fh[u][1][j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh[u][0][i], fl[u][1][j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh[u][0][i], fh[u][1][j], acc[i][j], 0, 0, 0);
+        }
+    }
+  }
+  float* out = a.part + (size_t)s * R * R;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int col = bbase + 16 * j + c16;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int row = abase + 16 * i + 4 * g + v;
+        if (row < R && col < R) out[(size_t)row * R + col] = acc[i][j][v];
+      }
+    }
+}
+
+// fp32 inputs: fp32 matrix cores, centring and masking on load.
+template <>
+__global__ __launch_bounds__(kThreads) void cka_gram_kernel<false>(CkaArgs a) {
+  constexpr bool SPLIT = false;
   constexpr int KS = SPLIT ? 32 : 16;      // probe rows per MFMA K-block
   constexpr int PL = KS / 4;               // probe rows per lane per K-block
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -356,8 +480,17 @@ __global__ __launch_bounds__(kThreads) void cka_pairs_kernel(CkaArgs a) {
     Gj[t] = gj;
     const int row = i * r + t / r, col = j * r + t % r;
     const size_t off = (size_t)min(row, col) * R + max(row, col);
+    // eight chunks' loads in flight at a time; the sum keeps chunk order
     float m = 0.f;
-    for (int s = 0; s < a.splits; ++s) m += a.part[(size_t)s * R * R + off];
+    int s = 0;
+    for (; s + 8 <= a.splits; s += 8) {
+      float v[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = a.part[(size_t)(s + i) * R * R + off];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) m += v[i];
+    }
+    for (; s < a.splits; ++s) m += a.part[(size_t)s * R * R + off];
     Mij[t] = m;
   }
   __syncthreads();
@@ -417,12 +550,17 @@ hipError_t launch_cka_t(const CkaProblem& p, void* ws, hipStream_t stream) {
   a.splits = L.splits;
   a.kchunk = L.kchunk;
   a.nbo = L.nbo;
+  a.Phi = reinterpret_cast<__bf16*>(base + L.Phi);
+  a.Plo = reinterpret_cast<__bf16*>(base + L.Plo);
   const int R = a.R;
   if (p.N > 0) {
     dim3 grid((p.N + kPN - 1) / kPN, (R + kPC - 1) / kPC);
     cka_project_kernel<T><<<grid, kThreads, 0, stream>>>(a);
   }
-  cka_mean_kernel<<<R, kThreads, 0, stream>>>(a);
+  if (p.dtype == ACE_BF16)
+    cka_mean_kernel<true><<<R, kThreads, 0, stream>>>(a);
+  else
+    cka_mean_kernel<false><<<R, kThreads, 0, stream>>>(a);
   {
     const int nt = (R + kGT - 1) / kGT;
     dim3 grid(nt * (nt + 1) / 2, L.splits);

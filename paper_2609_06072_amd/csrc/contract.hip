@@ -287,21 +287,6 @@ struct CDma {
   static constexpr int BLOCKS_PER_CU = (160 * 1024) / (LDS + 4 * 1024 + 512) < 1 ? 1 : (160 * 1024) / (LDS + 4 * 1024 + 512);
 };
 
-// s_waitcnt vmcnt(n) for a wave-uniform 0 <= n <= N
-template <int N>
-__device__ inline void wait_vmcnt_upto(int n) {
-  if constexpr (N > 0) {
-    if (n >= N) {
-      wait_vmcnt<N>();
-      return;
-    }
-    wait_vmcnt_upto<N - 1>(n);
-  } else {
-    (void)n;
-    wait_vmcnt<0>();
-  }
-}
-
 template <int RB>
 __global__ __launch_bounds__(kThreads) void contract_dma_kernel(ContractArgs a) {
   using G = CDma<RB>;
