@@ -524,6 +524,59 @@ def pmc_summary(fetch_dir, write_dir, labels_path, config, command):
     print("\n".join(lines))
 
 
+SIMD_NUM = 1024   # 256 compute units x 4 SIMDs
+N_XCD = 8         # GRBM counters come summed over the XCDs; busy % uses the per-XCD count
+
+
+def mfma_summary(pmc_dir, labels_path, config, command):
+    """profiles/mfma_<config>.txt: matrix-core utilisation per call and kernel
+    from one counter pass: SQ_VALU_MFMA_BUSY_CYCLES (summed over the SIMDs)
+    against GRBM_GUI_ACTIVE / 8 (the active cycles of one XCD) x 1024 SIMDs,
+    and SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 = bf16 matrix flops over the
+    dispatch's duration (its timestamps in the same pass) against 2.5 PFLOP/s.
+    Without labels (a run that is not a marked bench pass) every dispatch of a
+    kernel is pooled."""
+    import csv
+    import glob
+    files = glob.glob(os.path.join(pmc_dir, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {pmc_dir}")
+    by = {}
+    for r in csv.DictReader(open(files[0])):
+        d = int(r["Dispatch_Id"])
+        e = by.setdefault(d, {"name": (r["Kernel_Name"], int(r["Grid_Size"])),
+                              "ns": int(r["End_Timestamp"]) - int(r["Start_Timestamp"])})
+        e[r["Counter_Name"]] = e.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    disp = [(by[d]["name"], (by[d].get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0), by[d].get("GRBM_GUI_ACTIVE", 0.0),
+                             by[d].get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0), float(by[d]["ns"])))
+            for d in sorted(by)]
+    lines = [f"# matrix-core utilisation per kernel, {config}", f"source_hash {source_hash()}",
+             f"command {command}",
+             "# phase  kernel(grid)  mfma_busy_%  bf16_mfma_gflop  kernel_us  bf16_tflops  %_of_2.5PF"]
+    if labels_path and os.path.exists(labels_path):
+        labels = [l.strip() for l in open(labels_path) if l.strip()]
+        phases = _split_phases(disp, labels)
+        groups = [(lab, phases[lab]) for lab in labels[1:]]
+    else:
+        pooled = {}
+        for n, v in disp:
+            pooled.setdefault(n, []).append(v)
+        groups = [("all", [(n, tuple(sum(x[i] for x in vs) for i in range(4))) for n, vs in pooled.items()])]
+    for lab, ds in groups:
+        for (name, grid), (b, a, m, ns) in ds:
+            if "FillFunctor" in name or not any(t in name for t in ("ace::", "_ZN3ace")):
+                continue
+            util = 100.0 * b / (a / N_XCD * SIMD_NUM) if a > 0 else 0.0
+            tf = m * 512 / (ns * 1e-9) / 1e12 if ns > 0 else 0.0
+            lines.append(f"{lab} {short_kernel(name)}({grid // kThreadsGuess}) {util:.2f} "
+                         f"{m * 512 / 1e9:.3f} {ns / 1e3:.1f} {tf:.1f} {100 * tf / 2500:.2f}")
+    name = config if labels_path else f"cka_{config}"   # an unmarked run is the consolidation step
+    os.makedirs(PROFILES, exist_ok=True)
+    with open(os.path.join(PROFILES, f"mfma_{name}.txt"), "w") as out:
+        out.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def trace_summary(trace_dir, fetch_dir, labels_path, config, command):
     """Per-call kernel time from a rocprofv3 kernel trace of the bench: the
     dispatch sequence of one step of each path (names and grid sizes, taken
@@ -640,6 +693,9 @@ def main():
     ap.add_argument("--trace-summary", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "LABELS"),
                     help="write profiles/kernels_<config>.txt from a kernel trace of the bench")
     ap.add_argument("--pmc-command", default="", help="command recorded in the summary")
+    ap.add_argument("--mfma-summary", nargs=2, metavar=("PMC_DIR", "LABELS"),
+                    help="write profiles/mfma_<config>.txt from a matrix-core counter pass "
+                         "(LABELS = - for a run without markers)")
     ap.add_argument("--stats-summary", nargs=2, metavar=("TRACE_DIR", "NAME"),
                     help="write profiles/kernels_<NAME>.txt from a rocprofv3 --stats run")
     ap.add_argument("--no-consolidation", action="store_true",
@@ -656,6 +712,10 @@ def main():
         return
     if args.stats_summary:
         stats_summary(*args.stats_summary, args.pmc_command)
+        return
+    if args.mfma_summary:
+        mfma_summary(args.mfma_summary[0], None if args.mfma_summary[1] == "-" else args.mfma_summary[1],
+                     args.config, args.pmc_command)
         return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
