@@ -273,8 +273,8 @@ __global__ __launch_bounds__(kThreads) void contract_kernel(ContractArgs a) {
 // (rounded up to a copy) are copied.
 template <int RB>
 struct CDma {
-  static constexpr int KC = 64;                  // contraction indices per stage
-  static constexpr int NBUF = 3;                 // at most 4 (see the waits)
+  static constexpr int KC = RB <= 4 ? 128 : 64;  // contraction indices per stage
+  static constexpr int NBUF = RB <= 4 ? 2 : 3;  // at most 4 (see the waits)
   static constexpr int CPR = KC / 8;             // 16-byte chunks per row piece
   static constexpr int RPI = 64 / CPR;           // row pieces per copy instruction
   static constexpr int SBYTES = 64 * KC * 2;     // 64 source rows x KC bf16
