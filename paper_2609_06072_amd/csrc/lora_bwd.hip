@@ -10,11 +10,11 @@
 // Launches, all deterministic (each output is reduced in a fixed order):
 //   prep      -- A^T and B_q^T into the workspace (so every MFMA operand is
 //                contiguous along its contraction index); zeroes the dense
-//                per-token dH buffer used for dx.
-//   contract  -- Hs per row (x against A), stored per key and per pair served
-//                as [r][pair position], times the pair's weight (Hw); when
-//                the forward's h is passed in, a copy kernel builds Hw from
-//                it instead.
+//                per-token dH buffer used for dx; when the forward's h is
+//                passed in, builds Hw (below) from it in the same launch.
+//   contract  -- without the forward's h: Hs per row (x against A), stored
+//                per key and per pair served as [r][pair position], times the
+//                pair's weight (Hw).
 //   contract  -- dH per row (gathered G against B^T), stored per key as
 //                [r][u] and either as dense per-token rows (shared input) or
 //                row-major for the expand below (per-pair input).
@@ -31,7 +31,7 @@ namespace ace {
 namespace {
 
 constexpr int kTile = 64;   // transpose tile / column block
-constexpr int kMaxJobs = kMaxKeys + 2;
+constexpr int kMaxJobs = kMaxKeys + 3;
 
 size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 
@@ -138,9 +138,10 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
 
 // Hw from the forward's h (h_u = s_q A_q x_u per row, row-major [U][rpad]):
 // Hw[roff + r][pair position - first pair of the key] = w_p h_u[r] for every
-// pair p the row serves -- what the Hs contract below would store.  Lane l of
-// wave w handles row 64b + l and the rank chunks w, w + 4, ...
-struct HwArgs {
+// pair p the row serves -- what the Hs contract below would store.  Runs as
+// blocks of the prep launch: lane l of wave w handles row 64 blk + l and the
+// rank chunks w, w + 4, ...
+struct HwJob {
   const int32_t* offsets;
   const int32_t* row_token;
   const uint32_t* row_slots;
@@ -151,21 +152,19 @@ struct HwArgs {
   int32_t k;
   void* Hw;
   long ldh;
-  KeyTable keys;
 };
 
 template <typename T>
-__global__ __launch_bounds__(kThreads) void hw_from_h_kernel(HwArgs a) {
+__device__ inline void hw_rows(const HwJob& a, const KeyTable& keys, int blk, int* seg) {
   constexpr int PER = Tr<T>::PER;
-  __shared__ int seg[kMaxKeys + 1];
-  const int n_keys = a.keys.n_keys;
+  const int n_keys = keys.n_keys;
   for (int i = threadIdx.x; i <= n_keys; i += kThreads) seg[i] = a.offsets[i];
   __syncthreads();
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int u = blockIdx.x * 64 + lane;
+  const int u = blk * 64 + lane;
   if (u >= seg[n_keys]) return;
   const int q = upper_index(seg, n_keys, u);
-  const int r_q = a.keys.rank[q], roff = a.keys.roff[q];
+  const int r_q = keys.rank[q], roff = keys.roff[q];
   const int tok = a.row_token[u];
   const uint32_t slots = a.row_slots[u];
   const long col0 = a.ppos ? (long)a.ppos[u] - a.ppos[seg[q]] : (long)(u - seg[q]);
@@ -195,18 +194,25 @@ struct PrepArgs {
   int32_t d_in, d_out, R;
   long dHf_vecs;                    // 16-byte vectors to zero
   int32_t n_jobs;
-  int32_t job_start[kMaxJobs + 1];  // block ranges: job 0 = A, 1..n_keys = B_q, last = zero
+  int32_t job_start[kMaxJobs + 1];  // block ranges: job 0 = A, 1..n_keys = B_q, n_keys + 1 =
+                                    //   zero, n_keys + 2 = Hw rows
   int32_t job_cols_tiles[kMaxJobs];
+  HwJob hw;
   KeyTable keys;
 };
 
 template <typename T>
 __global__ __launch_bounds__(kThreads) void bwd_prep_kernel(PrepArgs a) {
   __shared__ T tile[kTile][kTile + 1];
+  __shared__ int seg[kMaxKeys + 1];
   const int b = blockIdx.x;
   const int job = upper_index(a.job_start, a.n_jobs, b);
   const int tb = b - a.job_start[job];
   const int n_keys = a.keys.n_keys;
+  if (job == n_keys + 2) {  // Hw from the forward's h
+    hw_rows<T>(a.hw, a.keys, tb, seg);
+    return;
+  }
   if (job == n_keys + 1) {  // zero the dense dH buffer
     u32x4* d = static_cast<u32x4*>(a.dHf);
     const long base = (long)tb * kThreads * 4;
@@ -284,7 +290,7 @@ __global__ __launch_bounds__(kThreads) void bwd_prep_kernel(PrepArgs a) {
 
 template <typename T>
 hipError_t launch_prep_t(const Problem& p, void* At, void* Bt, void* zero, long zero_bytes,
-                         hipStream_t stream) {
+                         const HwJob* hw, hipStream_t stream) {
   const int R = p.keys.R;
   const int n_keys = p.keys.n_keys;
   PrepArgs pa{};
@@ -298,7 +304,7 @@ hipError_t launch_prep_t(const Problem& p, void* At, void* Bt, void* zero, long 
   pa.R = R;
   pa.dHf_vecs = (zero_bytes + 15) / 16;   // the region is 256-byte padded
   pa.keys = p.keys;
-  pa.n_jobs = n_keys + 2;
+  pa.n_jobs = n_keys + 3;
   long nb = 0;
   auto tiles = [](long x) { return (x + kTile - 1) / kTile; };
   pa.job_start[0] = 0;
@@ -313,6 +319,12 @@ hipError_t launch_prep_t(const Problem& p, void* At, void* Bt, void* zero, long 
   pa.job_cols_tiles[n_keys + 1] = 1;
   nb += (pa.dHf_vecs + 4 * kThreads - 1) / (4 * kThreads);
   pa.job_start[n_keys + 2] = (int)nb;
+  pa.job_cols_tiles[n_keys + 2] = 1;
+  if (hw) {
+    pa.hw = *hw;
+    nb += ((long)p.T * p.k + 63) / 64;
+  }
+  pa.job_start[n_keys + 3] = (int)nb;
   if (nb > 0) bwd_prep_kernel<T><<<(int)nb, kThreads, 0, stream>>>(pa);
   return hipGetLastError();
 }
@@ -355,8 +367,27 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
   // A^T feeds the per-pair dx expand and the register dx GEMM; the bf16 dx
   // GEMM reads A itself when the dense dH rows are 16-byte aligned
   const bool need_At = p.per_pair || p.dtype != ACE_BF16 || (kslots * R) % 8 != 0;
+  // pair positions of rows that serve several slots (from the permutation)
+  const bool multi = p.rt->mode == ACE_ROWS_GROUP_DEDUP;
+  const int32_t* ppos = multi ? p.rt->row_pair : nullptr;
+  const int32_t* plist = multi ? p.rt->pair_list : nullptr;
+  // Hw = w s A x, per key and pair [r][pair position]: from the forward's h
+  // (blocks of the prep launch) when the caller kept it, else recomputed
+  HwJob hw{};
+  if (p.h_fwd) {
+    hw.offsets = p.rt->offsets;
+    hw.row_token = p.rt->row_token;
+    hw.row_slots = p.rt->row_slots;
+    hw.ppos = ppos;
+    hw.pair_w = p.pair_w;
+    hw.h = p.h_fwd;
+    hw.rpad = rpad;
+    hw.k = p.k;
+    hw.Hw = base + L.Ht;
+    hw.ldh = ldh;
+  }
   hipError_t e = launch_prep_t<T>(p, need_At ? base + L.At : nullptr, base + L.Bt, base + L.dHf,
-                                  dHf_bytes, stream);
+                                  dHf_bytes, p.h_fwd ? &hw : nullptr, stream);
   if (e != hipSuccess) return e;
 
   ContractArgs c{};
@@ -369,30 +400,8 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
   c.ldh = ldh;
   c.kslots = kslots;
   c.keys = p.keys;
-  // pair positions of rows that serve several slots (from the permutation)
-  const bool multi = p.rt->mode == ACE_ROWS_GROUP_DEDUP;
-  const int32_t* ppos = multi ? p.rt->row_pair : nullptr;
-  const int32_t* plist = multi ? p.rt->pair_list : nullptr;
-  // Hw = w s A x, per key and pair [r][pair position]: from the forward's h
-  // when the caller kept it, else recomputed
   c.pair_w = p.pair_w;
-  if (p.h_fwd) {
-    HwArgs hw{};
-    hw.offsets = p.rt->offsets;
-    hw.row_token = p.rt->row_token;
-    hw.row_slots = p.rt->row_slots;
-    hw.ppos = ppos;
-    hw.pair_w = p.pair_w;
-    hw.h = p.h_fwd;
-    hw.rpad = rpad;
-    hw.k = p.k;
-    hw.Hw = base + L.Ht;
-    hw.ldh = ldh;
-    hw.keys = p.keys;
-    const int blocks = (int)((P + 63) / 64);
-    if (blocks > 0) hw_from_h_kernel<T><<<blocks, kThreads, 0, stream>>>(hw);
-    e = hipGetLastError();
-  } else {
+  if (!p.h_fwd) {
     c.src = p.x;
     c.W = p.A;
     c.ldw = p.d_in;
@@ -402,8 +411,8 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
     c.out_t_pairs = 1;
     c.ppos = ppos;
     e = launch_contract(p.dtype, c, p.r_max, P, stream);
+    if (e != hipSuccess) return e;
   }
-  if (e != hipSuccess) return e;
   // dH = s B^T G
   c.W = base + L.Bt;
   c.ldw = p.d_out;
@@ -493,8 +502,8 @@ size_t bwd_ws_bytes(int T, int k, int d_in, int d_out, int n_keys, int R, int r_
 
 hipError_t launch_prep(const Problem& p, void* At, void* Bt, void* zero, long zero_bytes,
                        hipStream_t stream) {
-  if (p.dtype == ACE_BF16) return launch_prep_t<__bf16>(p, At, Bt, zero, zero_bytes, stream);
-  return launch_prep_t<float>(p, At, Bt, zero, zero_bytes, stream);
+  if (p.dtype == ACE_BF16) return launch_prep_t<__bf16>(p, At, Bt, zero, zero_bytes, nullptr, stream);
+  return launch_prep_t<float>(p, At, Bt, zero, zero_bytes, nullptr, stream);
 }
 
 hipError_t launch_combine(const Problem& p, const void* hp, int rpad, void* Ht, long ldh,
