@@ -108,6 +108,39 @@ __device__ inline Item decode_item(const GradArgs& a, const GradTable& tb, int i
   return it;
 }
 
+// Segments of key q for the two contractions (see GradTable).
+__device__ inline void key_segments(const GradArgs& a, int q, int* b0, int* b1, int* a0, int* a1) {
+  const int o0 = a.offsets[q], o1 = a.offsets[q + 1];
+  const int p0 = a.ppos ? a.ppos[o0] : o0, p1 = a.ppos ? a.ppos[o1] : o1;
+  *b0 = a.combined ? o0 : p0;
+  *b1 = a.combined ? o1 : p1;
+  *a0 = a.combined ? p0 : o0;
+  *a1 = a.combined ? p1 : o1;
+}
+
+__device__ inline int key_items(const GradArgs& a, int b0, int b1, int a0, int a1) {
+  return n_split(b1 - b0) * a.nbB + n_split(a1 - a0) * a.nbA;
+}
+
+// First item of key q (a wave-level sum over the keys before it).
+__device__ inline int key_first_item(const GradArgs& a, int q) {
+  constexpr int KPL = kMaxKeys / 64;
+  const int lane = threadIdx.x & 63;
+  int s = 0;
+#pragma unroll
+  for (int i = 0; i < KPL; ++i) {
+    const int qq = lane * KPL + i;
+    if (qq < q) {
+      int b0, b1, a0, a1;
+      key_segments(a, qq, &b0, &b1, &a0, &a1);
+      s += key_items(a, b0, b1, a0, a1);
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
+  return s;
+}
+
 // Row of the large operand for contraction index kabs of an item.
 __device__ inline int l_row(const GradArgs& a, bool isB, int kabs) {
   if (a.combined) return isB ? a.row_token[kabs] : a.plist[kabs];
@@ -485,17 +518,16 @@ __global__ __launch_bounds__(kThreads) void grad_reg_kernel(GradArgs a) {
 // One block per (key, dB|dA column block): sums the chunk partials in order.
 template <int RB>
 __global__ __launch_bounds__(kThreads) void grad_reduce_kernel(GradArgs a) {
-  __shared__ GradTable tb;
-  __shared__ int scan[kThreads];
-  build_grad_table(a, tb, scan);
   const int nb = a.nbB + a.nbA;
   const int q = blockIdx.x / nb, rem = blockIdx.x % nb;
   const bool isB = rem < a.nbB;
   const int cb = isB ? rem : rem - a.nbB;
-  const int nsB = n_split(tb.bseg[q + 1] - tb.bseg[q]);
-  const int ns = isB ? nsB : n_split(tb.aseg[q + 1] - tb.aseg[q]);
+  int b0, b1, a0, a1;
+  key_segments(a, q, &b0, &b1, &a0, &a1);
+  const int nsB = n_split(b1 - b0);
+  const int ns = isB ? nsB : n_split(a1 - a0);
   if (ns == 1) return;  // written directly by the gradient kernel
-  const int first = tb.istart[q] + (isB ? cb : nsB * a.nbB + cb);
+  const int first = key_first_item(a, q) + (isB ? cb : nsB * a.nbB + cb);
   const int step = isB ? a.nbB : a.nbA;
   const int nrb = (a.keys.rank[q] + 15) >> 4;
   const f32x4* part = reinterpret_cast<const f32x4*>(a.part);
