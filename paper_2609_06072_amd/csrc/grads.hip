@@ -660,16 +660,21 @@ __global__ __launch_bounds__(kThreads) void dx_gemm_kernel(DxArgs a) {
   }
 }
 
-// bf16 dx GEMM with LDS staging: stages of 64 contraction indices of the
-// tile's 128 dHdense rows (128-byte row pieces) and of the matching rows of A
-// itself ([R][d_in], 256-byte row pieces read transposed with
-// ds_read_b64_tr_b16, so A^T is not needed), two stages in LDS.
-constexpr int kDxKC = 64;
-constexpr int kDxStage = 128 * kDxKC * 2 + kDxKC * kDxTile * 2;   // 16 KB + 16 KB
+// bf16 dx GEMM with LDS staging: stages of one K-block (32 contraction
+// indices) of the tile's 128 dHdense rows (64-byte row pieces) and of the
+// matching rows of A itself ([R][d_in], 256-byte row pieces read transposed
+// with ds_read_b64_tr_b16, so A^T is not needed), NBUF stages in LDS, all
+// copied global -> LDS directly.  dHdense rows keep 16-byte chunk c at
+// position c ^ ((row >> 2) & 3), so the 16 rows of one fragment read fall in
+// distinct banks.
+constexpr int kDxKC = 32;
+constexpr int kDxNbuf = 4;
+constexpr int kDxHBytes = 128 * kDxKC * 2;                // 8 KB
+constexpr int kDxStage = kDxHBytes + kDxKC * kDxTile * 2;  // 8 KB + 8 KB
 
 __global__ __launch_bounds__(kThreads) void dx_dma_kernel(DxArgs a) {
   constexpr int CST = kDxTile + 8;
-  __shared__ __attribute__((aligned(16))) char smem[2 * kDxStage];
+  __shared__ __attribute__((aligned(16))) char smem[kDxNbuf * kDxStage];
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int c16 = lane & 15, g = lane >> 4;
@@ -681,82 +686,84 @@ __global__ __launch_bounds__(kThreads) void dx_dma_kernel(DxArgs a) {
   __bf16* DX = static_cast<__bf16*>(a.dx);
   const int KR = a.KR, R = a.R, d_in = a.d_in;
   const int nst = (KR + kDxKC - 1) / kDxKC;
-  // dHdense copies: wave w copies tile rows 32w + 8i + (lane >> 3), chunk lane & 7
-  const int cpos = lane & 7, crow = lane >> 3;
-  const __bf16* hrow[4];
-  int hcol[4];
+  // dHdense copies: wave w copies tile rows 32w + 16i + (lane >> 2), chunk
+  // position lane & 3 (global chunk (lane & 3) ^ sw(row))
+  const int hpos = lane & 3, hrl = lane >> 2;
+  const __bf16* hrow[2];
+  int hcol[2];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int rl = 32 * wave + 8 * i + crow;
+  for (int i = 0; i < 2; ++i) {
+    const int rl = 32 * wave + 16 * i + hrl;
     hrow[i] = H + (size_t)min(t0 + rl, a.T - 1) * KR;
-    hcol[i] = 8 * (cpos ^ (rl & 7));
+    hcol[i] = 8 * (hpos ^ ((rl >> 2) & 3));
   }
-  // A copies: wave w copies K rows 16w + 4i + (lane >> 4), chunk (lane & 15) ^ swizzle
+  // A copies: wave w copies K rows 8w + 4i + (lane >> 4), chunk (lane & 15) ^ swizzle
   const int arow = lane >> 4, apos = lane & 15;
-  int acol[4];
+  int acol[2];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int kr = 16 * wave + 4 * i + arow;
+  for (int i = 0; i < 2; ++i) {
+    const int kr = 8 * wave + 4 * i + arow;
     acol[i] = min(c0 + 8 * (apos ^ l_swz(kr)), d_in - 8);
   }
   auto issue = [&](int st) {
-    char* Hs = smem + (st & 1) * kDxStage;
-    char* As = Hs + 128 * kDxKC * 2;
+    char* Hs = smem + (st % kDxNbuf) * kDxStage;
+    char* As = Hs + kDxHBytes;
     const int k0 = st * kDxKC;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 2; ++i)
       dma16(hrow[i] + min(k0 + hcol[i], KR - 8),
-            __builtin_amdgcn_readfirstlane(lds_addr(Hs + (32 * wave + 8 * i) * kDxKC * 2)));
+            __builtin_amdgcn_readfirstlane(lds_addr(Hs + (32 * wave + 16 * i) * kDxKC * 2)));
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int kr = 16 * wave + 4 * i + arow;
+    for (int i = 0; i < 2; ++i) {
+      const int kr = 8 * wave + 4 * i + arow;
       const int krow = min(k0 + kr, KR - 1) % R;
       dma16(Am + (size_t)krow * d_in + acol[i],
-            __builtin_amdgcn_readfirstlane(lds_addr(As + (16 * wave + 4 * i) * kDxTile * 2)));
+            __builtin_amdgcn_readfirstlane(lds_addr(As + (8 * wave + 4 * i) * kDxTile * 2)));
     }
   };
+  constexpr int PER_STAGE = 4;   // copies per wave per stage
   f32x4 acc[4][4];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  if (nst > 0) issue(0);
+#pragma unroll
+  for (int p = 0; p < kDxNbuf - 1; ++p)
+    if (p < nst) issue(p);
   for (int st = 0; st < nst; ++st) {
-    wait_vmcnt<0>();
-    __syncthreads();   // stage st is in LDS; every wave is done with stage st - 1
-    if (st + 1 < nst) issue(st + 1);
-    const char* Hs = smem + (st & 1) * kDxStage;
-    const char* As = Hs + 128 * kDxKC * 2;
+    // this wave's copies of stage st are done once at most those of the
+    // stages issued after it are outstanding; the barrier publishes them
+    wait_vmcnt_upto<(kDxNbuf - 2) * PER_STAGE>(min(kDxNbuf - 2, nst - 1 - st) * PER_STAGE);
+    __syncthreads();
+    if (st + kDxNbuf - 1 < nst) issue(st + kDxNbuf - 1);
+    const char* Hs = smem + (st % kDxNbuf) * kDxStage;
+    const char* As = Hs + kDxHBytes;
+    const int kk = st * kDxKC;
+    const int nv = KR - (kk + 8 * g);
+    bf16x8 hf[4];
 #pragma unroll
-    for (int kb = 0; kb < kDxKC / 32; ++kb) {
-      const int kk = st * kDxKC + kb * 32;
-      if (kk >= KR) break;
-      const int nv = KR - (kk + 8 * g);
-      bf16x8 hf[4];
+    for (int tb = 0; tb < 4; ++tb) {
+      const int rl = 64 * wy + 16 * tb + c16;
+      bf16x8 f = *reinterpret_cast<const bf16x8*>(Hs + rl * kDxKC * 2 + ((g ^ ((rl >> 2) & 3)) << 4));
 #pragma unroll
-      for (int tb = 0; tb < 4; ++tb) {
-        const int rl = 64 * wy + 16 * tb + c16;
-        bf16x8 f = *reinterpret_cast<const bf16x8*>(Hs + rl * kDxKC * 2 + (((kb * 4 + g) ^ (rl & 7)) << 4));
+      for (int e = 0; e < 8; ++e)
+        if (e >= nv) f[e] = (__bf16)0.f;
+      hf[tb] = f;
+    }
 #pragma unroll
-        for (int e = 0; e < 8; ++e)
-          if (e >= nv) f[e] = (__bf16)0.f;
-        hf[tb] = f;
+    for (int cb = 0; cb < 4; ++cb) {
+      const int n0 = 64 * wx + 16 * cb;
+      s16x4 h2[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int r = 8 * g + 4 * h + (c16 >> 2);
+        const int c = (n0 >> 3) + ((c16 & 3) >> 1);
+        const int off = r * kDxTile * 2 + ((c ^ l_swz(r)) << 4) + ((c16 & 1) << 3);
+        h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(As + off));
       }
+      const bf16x8 af = __builtin_bit_cast(bf16x8, __builtin_shufflevector(h2[0], h2[1], 0, 1, 2, 3, 4, 5, 6, 7));
 #pragma unroll
-      for (int cb = 0; cb < 4; ++cb) {
-        const int n0 = 64 * wx + 16 * cb;
-        s16x4 h2[2];
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int r = kb * 32 + 8 * g + 4 * h + (c16 >> 2);
-          const int c = (n0 >> 3) + ((c16 & 3) >> 1);
-          const int off = r * kDxTile * 2 + ((c ^ l_swz(r)) << 4) + ((c16 & 1) << 3);
-          h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(As + off));
-        }
-        const bf16x8 af = __builtin_bit_cast(bf16x8, __builtin_shufflevector(h2[0], h2[1], 0, 1, 2, 3, 4, 5, 6, 7));
-#pragma unroll
-        for (int tb = 0; tb < 4; ++tb) acc[cb][tb] = Tr<__bf16>::mma(af, hf[tb], acc[cb][tb]);  // D[c][t]
-      }
+      for (int tb = 0; tb < 4; ++tb) acc[cb][tb] = Tr<__bf16>::mma(af, hf[tb], acc[cb][tb]);  // D[c][t]
     }
   }
   // tile -> LDS as [t][c] (over the stage buffers), then a coalesced read-modify-write of dx
