@@ -220,6 +220,52 @@ ace_status ace_expertwise_lora_bwd(ace_dtype dtype, ace_input_mode input_mode, i
                                    float* dB, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * Adapted expert projection: the frozen expert GEMM of an MoE layer with the
+ * adapter update added in its epilogue (Sec. 3.1 base projection plus the
+ * Sec. 3.4 shared-adapter update, the adapter part evaluated as in Sec. 3.5):
+ *   y[t*k + j, :] = W_e xin(t, j) + s_q B_q (A_q xin(t, j))
+ * for every routed pair, e = topk_ids[t, j], q = expert_key[e], s_q =
+ * alpha / r_q, xin as for the LoRA calls.  No router weight (gate and up
+ * projections, and the down projection ahead of the weighted combine).
+ * y is written, not accumulated: the separate adapter forward's
+ * read-modify-write of y disappears.
+ *   input_mode  ACE_INPUT_SHARED (x [T, d_in]) or ACE_INPUT_PER_PAIR
+ *               (x [T*k, d_in]).
+ *   W           device [E, d_out, d_in], dtype: expert e's frozen weight.
+ *   expert_rt   rows from ace_group_permute in ACE_ROWS_EXPERT mode over E
+ *               experts: the GEMM's row tiles (one expert per tile).
+ *   n_keys      number of adapters; 0 runs the plain expert projection
+ *               y = W_e xin (key_rank, expert_key, A, B, adapter_rt and ws
+ *               are then ignored and may be NULL).
+ *   key_rank    host int32 [n_keys]: rank r_q of each adapter.
+ *   expert_key  host int32 [E]: adapter of each expert (its group g(e) for
+ *               consolidated adapters, e itself for expert-wise LoRA).
+ *   A, B        device, adapters in the packed layout at the top, dtype.
+ *   adapter_rt  rows of the adapter's shrink h = s_q A_q xin, from
+ *               ace_group_permute on the same topk_ids with expert_to_group
+ *               = expert_key: ACE_ROWS_GROUP_DEDUP (grouped execution, once
+ *               per (token, active group); needs ACE_INPUT_SHARED),
+ *               ACE_ROWS_GROUP_PAIRS, or ACE_ROWS_EXPERT (expert-wise; then
+ *               expert_key[e] == e; expert_rt itself may be passed).
+ *               n_keys == adapter_rt->n_keys.
+ *   y           device [T*k, d_out], dtype: the rows of routed pairs are
+ *               written; rows of dropped pairs are left untouched.
+ *   ws          device scratch of at least
+ *               ace_workspace_bytes(ACE_OP_FWD, T, k, d_in, d_out, n_keys,
+ *               max r_q) (h per adapter row); no initialisation.
+ * Two launches: the shrink once per adapter row, then the expert GEMM whose
+ * K loop runs over d_in (x against W_e) and then over r_q (h against B_q)
+ * into the same fp32 accumulators; each output element is rounded once.
+ * Deterministic.
+ */
+ace_status ace_moe_lora_fwd(ace_dtype dtype, ace_input_mode input_mode, int32_t T, int32_t k,
+                            int32_t d_in, int32_t d_out, int32_t E, const void* x, const void* W,
+                            const ace_routing* expert_rt, int32_t n_keys, const int32_t* key_rank,
+                            const int32_t* expert_key, float alpha, const void* A, const void* B,
+                            const ace_routing* adapter_rt, void* y, void* ws, size_t ws_bytes,
+                            void* stream);
+
+/*
  * Pairwise linear CKA of the expert adapters of one layer on a shared probe
  * set (Sec. 3.3, rank consolidation): the similarity that groups experts.
  * Every probe row goes through every adapter regardless of routing; with

@@ -310,6 +310,39 @@ def precombined_delta(x, A, B, ranks, alpha, topk_ids, E, expert_to_group, G,
 
 
 # ---------------------------------------------------------------------------
+# the adapted expert projection (Sec. 3.1): the frozen expert weight and the
+# adapter update applied to the same input, y = (W_e + s_q B_q A_q) xin
+# ---------------------------------------------------------------------------
+
+def expert_projection(x, W, topk_ids, E, input_mode=INPUT_SHARED) -> np.ndarray:
+    """Y[t*k + j] = W_e xin(t, j) with e = topk_ids[t, j] and W [E, d_out, d_in]
+    (the frozen per-expert projection of Sec. 3.1).  Rows of dropped pairs
+    (id outside [0, E)) are zero.  Returns fp64 [T*k, d_out]."""
+    x = np.asarray(x, dtype=np.float64)
+    W = np.asarray(W, dtype=np.float64)
+    T, k = topk_ids.shape
+    out = np.zeros((T * k, W.shape[1]))
+    ids = np.asarray(topk_ids).reshape(-1)
+    for e in range(E):
+        pairs = np.nonzero(ids == e)[0]
+        if pairs.size:
+            out[pairs] = _inputs(x, pairs, k, input_mode) @ W[e].T
+    return out
+
+
+def adapted_projection(x, W, A, B, ranks, alpha, topk_ids, E, expert_to_group, G,
+                       input_mode=INPUT_SHARED) -> np.ndarray:
+    """Y[t*k + j] = W_e xin(t, j) + (alpha / r_q) B_q (A_q xin(t, j)): the
+    expert's frozen projection plus its adapter update (the adapter of the
+    expert's group, or its own with expert keys), no router weight (gate and
+    up projections, and the down projection before the combine).  Rows of
+    dropped pairs are zero.  Returns fp64 [T*k, d_out]."""
+    base = expert_projection(x, W, topk_ids, E, input_mode)
+    return base + lora_delta(x, A, B, ranks, alpha, topk_ids, E, expert_to_group, G,
+                             input_mode=input_mode)
+
+
+# ---------------------------------------------------------------------------
 # brute force: scalar Python loops straight from the definition (tiny inputs)
 # ---------------------------------------------------------------------------
 
@@ -346,6 +379,37 @@ def brute_delta(x, A, B, ranks, alpha, topk_ids, E, expert_to_group, G,
                     out[t][n] += w * s * acc
                 else:
                     out[t * k + j][n] = w * s * acc
+    return np.array(out, dtype=np.float64)
+
+
+def brute_adapted_projection(x, W, A, B, ranks, alpha, topk_ids, E, expert_to_group, G,
+                             input_mode=INPUT_SHARED):
+    """Scalar loops over the merged weight: y[n] = sum_i (W_e[n][i] +
+    s_q sum_a B_q[n][a] A_q[a][i]) xin[i] (the adapter folded into the
+    expert weight, as LoRA is merged for inference)."""
+    T, k = topk_ids.shape
+    d_out, d_in = len(W[0]), len(W[0][0])
+    off = [0]
+    for r in ranks:
+        off.append(off[-1] + int(r))
+    out = [[0.0] * d_out for _ in range(T * k)]
+    for t in range(T):
+        for j in range(k):
+            e = int(topk_ids[t][j])
+            if not 0 <= e < E:
+                continue
+            q = e if expert_to_group is None else int(expert_to_group[e])
+            r = int(ranks[q])
+            s = alpha / r
+            xin = x[t] if input_mode == INPUT_SHARED else x[t * k + j]
+            for n in range(d_out):
+                acc = 0.0
+                for i in range(d_in):
+                    m = float(W[e][n][i])
+                    for a in range(r):
+                        m += s * float(B[d_out * off[q] + n * r + a]) * float(A[off[q] + a][i])
+                    acc += m * float(xin[i])
+                out[t * k + j][n] = acc
     return np.array(out, dtype=np.float64)
 
 

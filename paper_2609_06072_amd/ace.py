@@ -30,7 +30,7 @@ ACE_OP_PERMUTE, ACE_OP_FWD, ACE_OP_BWD, ACE_OP_CKA = 0, 1, 2, 3
 EXPORTS = ("ace_group_permute", "ace_grouped_lora_fwd", "ace_grouped_lora_bwd",
            "ace_expertwise_lora_fwd", "ace_expertwise_lora_bwd", "ace_workspace_bytes",
            "ace_routing_check", "ace_last_error", "ace_pairwise_cka", "ace_similarity_graph",
-           "ace_louvain", "ace_group_anchors", "ace_consolidate_adapters")
+           "ace_louvain", "ace_group_anchors", "ace_consolidate_adapters", "ace_moe_lora_fwd")
 
 
 class AceRouting(ctypes.Structure):
@@ -77,6 +77,9 @@ _lib.ace_group_anchors.restype = _i32
 _lib.ace_consolidate_adapters.argtypes = [_i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _i32, _vp,
                                           _vp, _vp, _vp, _vp]
 _lib.ace_consolidate_adapters.restype = _i32
+_lib.ace_moe_lora_fwd.argtypes = [_i32, _i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _R, _i32, _vp,
+                                  _vp, _f32, _vp, _vp, _R, _vp, _vp, _sz, _vp]
+_lib.ace_moe_lora_fwd.restype = _i32
 _lib.ace_last_error.argtypes = []
 _lib.ace_last_error.restype = ctypes.c_char_p
 
@@ -328,3 +331,25 @@ def ace_consolidate_adapters(A, B, E: int, rank: int, expert_to_group, G: int, a
 def raw_lib() -> ctypes.CDLL:
     """The loaded library (tests check exports and host-side validation)."""
     return _lib
+
+
+def ace_moe_lora_fwd(x, W, expert_routing: Routing, y, key_rank: Optional[Sequence[int]] = None,
+                     expert_key: Optional[Sequence[int]] = None, alpha: float = 16.0, A=None,
+                     B=None, adapter_routing: Optional[Routing] = None,
+                     input_mode: int = ACE_INPUT_SHARED, ws=None, stream=None) -> None:
+    """y[t*k + j] = W_e xin(t, j) + s_q B_q (A_q xin(t, j)) (include/ace.h).
+    key_rank None runs the plain expert projection."""
+    T, k = expert_routing.c.T, expert_routing.c.k
+    E, d_out, d_in = W.shape
+    n_keys = 0 if key_rank is None else len(key_rank)
+    ranks = _ranks_arg(key_rank) if n_keys else None
+    ekey = (ctypes.c_int32 * E)(*[int(v) for v in expert_key]) if n_keys else None
+    if n_keys:
+        ws = _fwd_ws(ws, T, k, d_in, d_out, n_keys, max(key_rank), x.device)
+    _check(_lib.ace_moe_lora_fwd(_dtype(x), input_mode, T, k, d_in, d_out, E, _ptr(x), _ptr(W),
+                                 ctypes.byref(expert_routing.c), n_keys, ranks, ekey, alpha,
+                                 _ptr(A), _ptr(B),
+                                 ctypes.byref(adapter_routing.c) if adapter_routing else None,
+                                 _ptr(y), _ptr(ws), 0 if ws is None else ws.numel(),
+                                 _stream(stream)),
+           "ace_moe_lora_fwd")

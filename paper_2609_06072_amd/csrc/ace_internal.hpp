@@ -86,6 +86,30 @@ hipError_t launch_expand(int dtype, const ExpandArgs& a, int r_max, long P, hipS
 size_t fwd_ws_bytes(int T, int k, int r_max);
 hipError_t launch_fwd(const Problem& p, void* y, void* ws, hipStream_t stream);
 
+// Shrink h = (alpha / r_q) A_q xin once per row of p.rt, into h [U][rpad]
+// (the first launch of the forward).
+hipError_t launch_shrink(const Problem& p, void* h, hipStream_t stream);
+
+// Expert projection with the adapter update in its epilogue:
+//   y[t*k + j] = W_e xin(t, j) + h[h_row[t*k + j]] B_q^T   (q = key_of[e])
+struct MoeArgs {
+  const void* x;              // [T][d_in] (shared) or [T*k][d_in] (per pair)
+  const void* W;              // [E][d_out][d_in]
+  const int32_t* offsets;     // expert routing (ACE_ROWS_EXPERT)
+  const int32_t* row_token;
+  const uint32_t* row_slots;
+  int32_t E, k, d_in, d_out, per_pair;
+  const void* H;              // [U'][rpad] scaled shrink per adapter row, or null (no adapter)
+  int32_t rpad;
+  const int32_t* h_row;       // adapter row of each pair (the adapter routing's pair_row)
+  const void* B;              // key q: [d_out][r_q] at d_out * roff_q
+  void* y;                    // [T*k][d_out], written
+  int32_t nt;                 // column tiles (set by the launcher)
+  KeyTable keys;              // adapter keys
+  uint8_t key_of[kMaxKeys];   // adapter key of each expert
+};
+hipError_t launch_moe_gemm(int dtype, const MoeArgs& a, long P, hipStream_t stream);
+
 // Backward helpers shared with the pre-combined mode.
 //   prep: A^T [d_in][R] into At and B_q^T rows [R][d_out] into Bt (each
 //         skipped when null), and zero_bytes of zeros at `zero` (16-byte

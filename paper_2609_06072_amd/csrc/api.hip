@@ -46,7 +46,7 @@ ace_status check_problem(Problem& p, ace_dtype dtype, ace_input_mode im, int32_t
                          int32_t d_in, int32_t d_out, int32_t n_keys, const int32_t* ranks,
                          int32_t uniform_rank, float alpha, const void* x, const void* A,
                          const void* B, const float* pair_w, const ace_routing* rt,
-                         bool expertwise) {
+                         bool expertwise, bool any_rows = false) {
   if (dtype != ACE_F32 && dtype != ACE_BF16) return fail(ACE_ERR_INVALID_ARG, "unknown dtype %d", (int)dtype);
   if (im != ACE_INPUT_SHARED && im != ACE_INPUT_PER_PAIR && im != ACE_INPUT_COMBINED)
     return fail(ACE_ERR_INVALID_ARG, "unknown input mode %d", (int)im);
@@ -72,7 +72,13 @@ ace_status check_problem(Problem& p, ace_dtype dtype, ace_input_mode im, int32_t
                 rt->k, T, k);
   if (rt->n_keys != n_keys)
     return fail(ACE_ERR_INVALID_ARG, "routing has %d keys, call has %d", rt->n_keys, n_keys);
-  if (expertwise) {
+  if (any_rows) {
+    if (rt->mode == ACE_ROWS_GROUP_DEDUP && im != ACE_INPUT_SHARED)
+      return fail(ACE_ERR_INVALID_ARG, "ACE_ROWS_GROUP_DEDUP adapter rows need ACE_INPUT_SHARED");
+    if (rt->mode != ACE_ROWS_GROUP_DEDUP && rt->mode != ACE_ROWS_GROUP_PAIRS &&
+        rt->mode != ACE_ROWS_EXPERT)
+      return fail(ACE_ERR_INVALID_ARG, "adapter routing has an unknown row mode %d", rt->mode);
+  } else if (expertwise) {
     if (rt->mode != ACE_ROWS_EXPERT)
       return fail(ACE_ERR_INVALID_ARG, "expert-wise calls need ACE_ROWS_EXPERT routing");
   } else {
@@ -159,6 +165,83 @@ ace_status run_bwd(Problem& p, const void* h_fwd, const void* dy, void* dx, floa
                     "backward launch");
 }
 
+ace_status run_moe_fwd(ace_dtype dtype, ace_input_mode im, int32_t T, int32_t k, int32_t d_in,
+                       int32_t d_out, int32_t E, const void* x, const void* W,
+                       const ace_routing* ert, int32_t n_keys, const int32_t* key_rank,
+                       const int32_t* expert_key, float alpha, const void* A, const void* B,
+                       const ace_routing* art, void* y, void* ws, size_t ws_bytes, void* stream) {
+  if (dtype != ACE_F32 && dtype != ACE_BF16) return fail(ACE_ERR_INVALID_ARG, "unknown dtype %d", (int)dtype);
+  if (im != ACE_INPUT_SHARED && im != ACE_INPUT_PER_PAIR)
+    return fail(ACE_ERR_INVALID_ARG, "input mode must be ACE_INPUT_SHARED or ACE_INPUT_PER_PAIR");
+  if (T < 0) return fail(ACE_ERR_INVALID_ARG, "T = %d < 0", T);
+  if (k < 1 || k > kMaxK) return fail(ACE_ERR_UNSUPPORTED, "k = %d outside [1, %d]", k, kMaxK);
+  if ((int64_t)T * k >= (int64_t)1 << 31) return fail(ACE_ERR_UNSUPPORTED, "T*k >= 2^31");
+  const int vec = dtype == ACE_BF16 ? 8 : 4;
+  if (d_in < 1 || d_out < 1) return fail(ACE_ERR_INVALID_ARG, "d_in = %d, d_out = %d", d_in, d_out);
+  if (d_in % vec || d_out % vec)
+    return fail(ACE_ERR_UNSUPPORTED, "d_in (%d) and d_out (%d) must be multiples of %d", d_in,
+                d_out, vec);
+  if (E < 1 || E > kMaxKeys) return fail(ACE_ERR_UNSUPPORTED, "E = %d outside [1, %d]", E, kMaxKeys);
+  if ((int64_t)E * d_out * d_in >= (int64_t)1 << 40)
+    return fail(ACE_ERR_UNSUPPORTED, "expert weights too large");
+  if (!ert || !ert->offsets || (T > 0 && (!ert->row_token || !ert->row_slots)))
+    return fail(ACE_ERR_INVALID_ARG, "expert routing is NULL");
+  if (ert->mode != ACE_ROWS_EXPERT || ert->n_keys != E)
+    return fail(ACE_ERR_INVALID_ARG, "expert_rt must be ACE_ROWS_EXPERT routing over %d experts", E);
+  if (ert->T != T || ert->k != k)
+    return fail(ACE_ERR_INVALID_ARG, "expert routing was built for T=%d k=%d, call has T=%d k=%d",
+                ert->T, ert->k, T, k);
+  if (T > 0 && (!x || !W || !y)) return fail(ACE_ERR_INVALID_ARG, "x, W or y is NULL");
+  if (!aligned(x, 16) || !aligned(W, 16) || !aligned(y, 16))
+    return fail(ACE_ERR_INVALID_ARG, "x, W and y must be 16-byte aligned");
+  if (n_keys < 0) return fail(ACE_ERR_INVALID_ARG, "n_keys = %d < 0", n_keys);
+  MoeArgs a{};
+  Problem p{};
+  if (n_keys > 0) {
+    if (!key_rank || !expert_key) return fail(ACE_ERR_INVALID_ARG, "key_rank or expert_key is NULL");
+    ace_status s = check_problem(p, dtype, im, T, k, d_in, d_out, n_keys, key_rank, 0, alpha, x,
+                                 A, B, nullptr, art, false, true);
+    if (s != ACE_OK) return s;
+    for (int e = 0; e < E; ++e) {
+      const int q = expert_key[e];
+      if (q < 0 || q >= n_keys)
+        return fail(ACE_ERR_INVALID_ARG, "expert_key[%d] = %d outside [0, %d)", e, q, n_keys);
+      if (art->mode == ACE_ROWS_EXPERT && q != e)
+        return fail(ACE_ERR_INVALID_ARG, "expert-keyed adapter rows need expert_key[e] == e");
+      a.key_of[e] = (uint8_t)q;
+    }
+    if (T > 0 && !art->pair_row) return fail(ACE_ERR_INVALID_ARG, "adapter routing arrays are NULL");
+    const size_t need = fwd_ws_bytes(T, k, p.r_max);
+    if (!ws || ws_bytes < need)
+      return fail(ACE_ERR_WORKSPACE, "forward needs %zu workspace bytes, got %zu", need,
+                  ws ? ws_bytes : (size_t)0);
+    if (!aligned(ws, 256)) return fail(ACE_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  }
+  if (T == 0) return ok();
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  a.x = x;
+  a.W = W;
+  a.offsets = ert->offsets;
+  a.row_token = ert->row_token;
+  a.row_slots = ert->row_slots;
+  a.E = E;
+  a.k = k;
+  a.d_in = d_in;
+  a.d_out = d_out;
+  a.per_pair = im == ACE_INPUT_PER_PAIR;
+  a.y = y;
+  if (n_keys > 0) {
+    hipError_t e = launch_shrink(p, ws, st);
+    if (e != hipSuccess) return hip_status(e, "shrink launch");
+    a.H = ws;
+    a.rpad = rank_pad(dtype, p.r_max);
+    a.h_row = art->pair_row;
+    a.B = B;
+    a.keys = p.keys;
+  }
+  return hip_status(launch_moe_gemm(dtype, a, (long)T * k, st), "expert GEMM launch");
+}
+
 }  // namespace
 
 int device_cu_count() {
@@ -227,6 +310,16 @@ ace_status ace_grouped_lora_fwd(ace_dtype dtype, ace_input_mode input_mode, int3
                                x, A, B, pair_w, rt, false);
   if (s != ACE_OK) return s;
   return run_fwd(p, y, ws, ws_bytes, stream);
+}
+
+ace_status ace_moe_lora_fwd(ace_dtype dtype, ace_input_mode input_mode, int32_t T, int32_t k,
+                            int32_t d_in, int32_t d_out, int32_t E, const void* x, const void* W,
+                            const ace_routing* expert_rt, int32_t n_keys, const int32_t* key_rank,
+                            const int32_t* expert_key, float alpha, const void* A, const void* B,
+                            const ace_routing* adapter_rt, void* y, void* ws, size_t ws_bytes,
+                            void* stream) {
+  return run_moe_fwd(dtype, input_mode, T, k, d_in, d_out, E, x, W, expert_rt, n_keys, key_rank,
+                     expert_key, alpha, A, B, adapter_rt, y, ws, ws_bytes, stream);
 }
 
 ace_status ace_grouped_lora_bwd(ace_dtype dtype, ace_input_mode input_mode, int32_t T,

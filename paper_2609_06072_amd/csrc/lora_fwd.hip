@@ -13,9 +13,7 @@ size_t fwd_ws_bytes(int T, int k, int r_max) {
   return (P * (size_t)rank_pad(ACE_F32, r_max) * sizeof(float) + 255) & ~(size_t)255;
 }
 
-hipError_t launch_fwd(const Problem& p, void* y, void* ws, hipStream_t stream) {
-  const long P = (long)p.T * p.k;
-  const int rpad = rank_pad(p.dtype, p.r_max);
+hipError_t launch_shrink(const Problem& p, void* h, hipStream_t stream) {
   ContractArgs c{};
   c.src = p.x;
   c.W = p.A;
@@ -28,10 +26,16 @@ hipError_t launch_fwd(const Problem& p, void* y, void* ws, hipStream_t stream) {
   c.offsets = p.rt->offsets;
   c.row_token = p.rt->row_token;
   c.row_slots = p.rt->row_slots;
-  c.out_row = ws;
-  c.rpad = rpad;
+  c.out_row = h;
+  c.rpad = rank_pad(p.dtype, p.r_max);
   c.keys = p.keys;
-  hipError_t e = launch_contract(p.dtype, c, p.r_max, P, stream);
+  return launch_contract(p.dtype, c, p.r_max, (long)p.T * p.k, stream);
+}
+
+hipError_t launch_fwd(const Problem& p, void* y, void* ws, hipStream_t stream) {
+  const long P = (long)p.T * p.k;
+  const int rpad = rank_pad(p.dtype, p.r_max);
+  hipError_t e = launch_shrink(p, ws, stream);
   if (e != hipSuccess) return e;
   ExpandArgs x{};
   x.H = ws;

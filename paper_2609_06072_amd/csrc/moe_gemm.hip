@@ -1,0 +1,252 @@
+// Adapted expert projection: the frozen expert GEMM of an MoE layer with the
+// adapter update added in its epilogue (Sec. 3.1 base projection W_e x plus
+// the Sec. 3.4 shared-adapter update, executed as in Sec. 3.5):
+//   y[t*k + j] = W_e xin(t, j) + B_q h_u,   e = topk_ids[t, j], q = key of e,
+// where h_u = (alpha / r_q) A_q xin is the shrink of the adapter row u that
+// serves the pair (one row per (token, active group) for grouped execution,
+// one per pair for expert-wise LoRA), computed beforehand by the contract
+// kernel.  y is written once: the adapter's read-modify-write of y is gone.
+//
+// Tiles.  The rows of the expert routing (sorted by expert, then token) are
+// cut into tiles of kGM rows of one expert; a block computes a kGM x kGN
+// output tile.  The contraction runs over d_in (x rows against W_e rows, both
+// K-contiguous) and then over the adapter rank (h rows against B_q rows, also
+// K-contiguous), all into the same fp32 accumulators.
+//
+// Data movement.  One K-block (64 bytes of every row: 32 bf16 or 16 fp32) per
+// stage; x and W_e pieces are copied global -> LDS directly
+// (global_load_lds_dwordx4), kGNbuf stages in flight.  Within a stage a row's
+// four 16-byte chunks sit XOR-swizzled by (row >> 2) & 3, so the fragment
+// reads of 16 consecutive rows hit distinct banks.  The adapter K-blocks (one
+// or two) are read straight into registers while the first stages are in
+// flight.
+//
+// Waves.  Four waves, 2 x 2 over the tile: wave (wy, wx) owns rows
+// 64*wy .. +64 and columns 128*wx .. +128, i.e. 4 x 8 blocks of 16 x 16.  The
+// weight rows are the first MFMA operand, so a lane's accumulator holds four
+// consecutive output columns of one row; the epilogue stages the tile in LDS
+// and writes y with 16-byte stores of whole row pieces.
+//
+// Block order.  Blocks are dealt to the 8 XCDs round-robin; block b takes
+// tile (b % 8) * ceil(n_tiles / 8) + b / 8, so each XCD walks a contiguous
+// run of tiles (expert-major): an expert's weight slices stay in one L2.
+#include "ace_device.hpp"
+#include "ace_internal.hpp"
+
+namespace ace {
+
+namespace {
+
+constexpr int kGM = 128;                 // rows (routed pairs) per tile
+constexpr int kGN = 256;                 // output columns per tile
+constexpr int kGNbuf = 3;                // stages in flight
+constexpr int kGRowBytes = 64;           // bytes of a row per stage
+constexpr int kGXBytes = kGM * kGRowBytes;
+constexpr int kGWBytes = kGN * kGRowBytes;
+constexpr int kGStage = kGXBytes + kGWBytes;  // 24 KB
+constexpr int kGCopies = (kGM + kGN) / 16 / 4; // 16-row copies per wave per stage
+
+__device__ inline int g_swz(int row) { return (row >> 2) & 3; }
+
+// Number of tiles of BM rows over the key segments offsets[0 .. n_keys]
+// (wave-level; every lane gets the total).
+__device__ inline int count_tiles(const int32_t* offsets, int n_keys, int BM) {
+  constexpr int KPL = kMaxKeys / 64;
+  const int lane = threadIdx.x & 63;
+  int cnt = 0;
+  int prev = offsets[min(lane * KPL, n_keys)];
+#pragma unroll
+  for (int i = 0; i < KPL; ++i) {
+    const int nxt = offsets[min(lane * KPL + i + 1, n_keys)];
+    cnt += (nxt - prev + BM - 1) / BM;
+    prev = nxt;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
+  return cnt;
+}
+
+template <typename T>
+__global__ __launch_bounds__(kThreads, 2) void moe_gemm_kernel(MoeArgs a) {
+  using F = typename Tr<T>::frag;
+  constexpr int PER = Tr<T>::PER, KB = Tr<T>::KB;
+  constexpr int NH = sizeof(T) / 2;            // epilogue passes (C tile halves for fp32)
+  constexpr int HC = kGN / NH;                 // columns per pass
+  constexpr int CST = HC + 16 / (int)sizeof(T);
+  static_assert(kGM * CST * (int)sizeof(T) <= kGNbuf * kGStage, "C tile exceeds the stage buffers");
+  __shared__ __attribute__((aligned(16))) char smem[kGNbuf * kGStage];
+  __shared__ int s_src[kGM];   // x row of each tile row (clamped into the segment)
+  __shared__ int s_out[kGM];   // y row, -1 past the segment
+  __shared__ int s_h[kGM];     // adapter row, -1 for none
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int c16 = lane & 15, g = lane >> 4;
+  const int wy = wave >> 1, wx = wave & 1;
+
+  // ---- which tile
+  const int n_mt = count_tiles(a.offsets, a.E, kGM);
+  const int n_tiles = n_mt * a.nt;
+  const int per_xcd = (n_tiles + kXcds - 1) / kXcds;
+  const int bi = blockIdx.x / kXcds;
+  const int tile = (blockIdx.x % kXcds) * per_xcd + bi;
+  if (bi >= per_xcd || tile >= n_tiles) return;
+  const int mt = tile / a.nt, n0 = (tile % a.nt) * kGN;
+  int e, u0, uend;
+  locate_tile(a.offsets, a.E, kGM, mt, &e, &u0, &uend);
+
+  if (tid < kGM) {
+    const int u = u0 + tid;
+    const int uc = min(u, uend - 1);
+    const int tok = a.row_token[uc];
+    const int j = __builtin_ctz(a.row_slots[uc] | 0x80000000u) & 31;
+    const int p = tok * a.k + j;
+    s_src[tid] = a.per_pair ? p : tok;
+    s_out[tid] = u < uend ? p : -1;
+    s_h[tid] = (u < uend && a.H) ? a.h_row[p] : -1;
+  }
+  __syncthreads();
+
+  const T* X = static_cast<const T*>(a.x);
+  const T* Wt = static_cast<const T*>(a.W) + (size_t)e * a.d_out * a.d_in;
+  const int d_in = a.d_in, d_out = a.d_out;
+  const int nst = (d_in + KB - 1) / KB;
+
+  // ---- copy assignment: lane covers row (lane >> 2) of each 16-row copy,
+  // chunk position lane & 3 (global chunk (lane & 3) ^ swizzle)
+  const int cpos = lane & 3, crl = lane >> 2;
+  const T* src[kGCopies];
+  uint32_t dst[kGCopies];
+  int coff[kGCopies];
+#pragma unroll
+  for (int i = 0; i < kGCopies; ++i) {
+    const int blk = wave * kGCopies + i;      // 16-row copy index over [x rows | W rows]
+    const int row = 16 * blk + crl;
+    coff[i] = PER * (cpos ^ g_swz(row));
+    if (16 * blk < kGM) {
+      src[i] = X + (size_t)s_src[row] * d_in;
+      dst[i] = 16 * blk * kGRowBytes;
+    } else {
+      const int wr = row - kGM;
+      src[i] = Wt + (size_t)min(n0 + wr, d_out - 1) * d_in;
+      dst[i] = kGXBytes + 16 * (blk - kGM / 16) * kGRowBytes;
+    }
+  }
+  const uint32_t sbase = lds_addr(smem);
+  auto issue = [&](int st) {
+    const uint32_t buf = sbase + (st % kGNbuf) * kGStage;
+    const int k0 = st * KB;
+#pragma unroll
+    for (int i = 0; i < kGCopies; ++i)
+      dma16(src[i] + min(k0 + coff[i], d_in - PER), __builtin_amdgcn_readfirstlane(buf + dst[i]));
+  };
+#pragma unroll
+  for (int s = 0; s < kGNbuf - 1; ++s)
+    if (s < nst) issue(s);
+
+  f32x4 acc[8][4];
+#pragma unroll
+  for (int nb = 0; nb < 8; ++nb)
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) acc[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // ---- adapter K-blocks: acc[n][m] += sum_rho B_q[n][rho] h_m[rho]
+  if (a.H) {
+    const int q = a.key_of[e];
+    const int r_q = a.keys.rank[q];
+    const T* Bq = static_cast<const T*>(a.B) + (size_t)d_out * a.keys.roff[q];
+    const T* Hm = static_cast<const T*>(a.H);
+    const bool bvec = (r_q % PER) == 0;
+    for (int kb = 0; kb * KB < r_q; ++kb) {
+      const int rho = kb * KB + PER * g;
+      F hf[4], bf[8];
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb) {
+        const int hr = s_h[64 * wy + 16 * mb + c16];
+        hf[mb] = hr >= 0 ? Tr<T>::load(Hm + (size_t)hr * a.rpad + rho) : Tr<T>::zero();
+      }
+#pragma unroll
+      for (int nb = 0; nb < 8; ++nb) {
+        const int n = min(n0 + 128 * wx + 16 * nb + c16, d_out - 1);
+        bf[nb] = load_frag<T>(Bq + (size_t)n * r_q + rho, r_q - rho, bvec);
+      }
+#pragma unroll
+      for (int nb = 0; nb < 8; ++nb)
+#pragma unroll
+        for (int mb = 0; mb < 4; ++mb) acc[nb][mb] = Tr<T>::mma(bf[nb], hf[mb], acc[nb][mb]);
+    }
+  }
+
+  // ---- main loop over d_in
+  for (int st = 0; st < nst; ++st) {
+    wait_vmcnt_upto<(kGNbuf - 2) * kGCopies>(min(kGNbuf - 2, nst - 1 - st) * kGCopies);
+    __syncthreads();
+    if (st + kGNbuf - 1 < nst) issue(st + kGNbuf - 1);
+    const char* Xs = smem + (st % kGNbuf) * kGStage;
+    const char* Ws = Xs + kGXBytes;
+    const bool kval = st * KB + PER * g < d_in;   // chunk g of this K-block inside d_in
+    F xf[4], wf[8];
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) {
+      const int rl = 64 * wy + 16 * mb + c16;
+      const F v = *reinterpret_cast<const F*>(Xs + rl * kGRowBytes + ((g ^ g_swz(rl)) << 4));
+      xf[mb] = kval ? v : Tr<T>::zero();
+    }
+#pragma unroll
+    for (int nb = 0; nb < 8; ++nb) {
+      const int rl = 128 * wx + 16 * nb + c16;
+      wf[nb] = *reinterpret_cast<const F*>(Ws + rl * kGRowBytes + ((g ^ g_swz(rl)) << 4));
+    }
+#pragma unroll
+    for (int nb = 0; nb < 8; ++nb)
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb) acc[nb][mb] = Tr<T>::mma(wf[nb], xf[mb], acc[nb][mb]);
+  }
+
+  // ---- epilogue: C tile -> LDS [m][n] (over the stage buffers), then whole
+  // 16-byte row pieces of y
+  T* Cs = reinterpret_cast<T*>(smem);
+  T* Y = static_cast<T*>(a.y);
+  constexpr int CPR = HC / PER;                 // 16-byte pieces per row and pass
+  constexpr int NP = kGM * CPR / kThreads;
+#pragma unroll
+  for (int h = 0; h < NH; ++h) {
+    __syncthreads();
+#pragma unroll
+    for (int nb = 0; nb < 8; ++nb) {
+      const int nl = 128 * wx + 16 * nb + 4 * g - h * HC;   // column inside this pass
+      if (nl >= 0 && nl < HC) {
+#pragma unroll
+        for (int mb = 0; mb < 4; ++mb) {
+          T* cp = Cs + (64 * wy + 16 * mb + c16) * CST + nl;
+#pragma unroll
+          for (int v = 0; v < 4; ++v) cp[v] = (T)acc[nb][mb][v];
+        }
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < NP; ++i) {
+      const int it = tid + i * kThreads;
+      const int m = it / CPR, pc = (it % CPR) * PER;
+      const int orow = s_out[m];
+      const int col = n0 + h * HC + pc;
+      if (orow >= 0 && col < d_out)
+        Tr<T>::store(Y + (size_t)orow * d_out + col, *reinterpret_cast<const F*>(Cs + m * CST + pc));
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_moe_gemm(int dtype, const MoeArgs& a0, long P, hipStream_t stream) {
+  MoeArgs a = a0;
+  a.nt = (a.d_out + kGN - 1) / kGN;
+  const long max_tiles = ((P + kGM - 1) / kGM + a.E) * a.nt;
+  const long grid = (max_tiles + kXcds - 1) / kXcds * kXcds;
+  if (grid <= 0) return hipSuccess;
+  if (dtype == ACE_BF16) moe_gemm_kernel<__bf16><<<(int)grid, kThreads, 0, stream>>>(a);
+  else moe_gemm_kernel<float><<<(int)grid, kThreads, 0, stream>>>(a);
+  return hipGetLastError();
+}
+
+}  // namespace ace

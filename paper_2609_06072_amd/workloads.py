@@ -23,6 +23,9 @@ Recipe (every stream is an independent child of ``SeedSequence(seed)``):
                  Sec. 3.3 rank consolidation).
   * tensors   -- x ~ N(0,1), A ~ N(0, 1/d_in) (std d_in^-1/2), B ~ N(0, 0.02)
                  (std 0.02), dY ~ N(0,1); bf16 configs round with RNE.
+  * frozen expert weights of a projection (the base GEMM that the adapter
+    update can be fused into) -- W_e ~ N(0, 1/d_in), one [d_out, d_in] matrix
+    per expert, stream "<proj>.W".
   * probe and expert adapters for the consolidation step (Sec. 3.3: N probe
     hidden states go through every expert adapter of a layer; the paper uses
     N = 10,000 training tokens after a warm-up of expert-wise LoRA) --
@@ -52,7 +55,7 @@ _STREAMS = ("router", "groups", "x", "h", "gate.A", "gate.B", "gate.dy",
             "up.A", "up.B", "up.dy", "down.A", "down.B", "down.dy", "y_in",
             "dx_in", "extra", "gate.dy_combined", "up.dy_combined", "down.dy_combined",
             "probe", "probe.mu", "cka.clusters", "cka.A", "cka.B", "cka.A_noise", "cka.B_noise",
-            "cka.A_init")
+            "cka.A_init", "gate.W", "up.W", "down.W")
 
 
 @dataclasses.dataclass(frozen=True)
@@ -307,3 +310,11 @@ def draw_lora_init_A(rows: int, d_in: int, seed: int = 0, dtype: str = "bf16", d
     t.mul_(1.0 / math.sqrt(d_in))
     return t.to(torch.bfloat16 if dtype == "bf16" else torch.float32)
 
+
+
+def draw_expert_weights(cfg: MoEConfig, proj: str, seed: int = 0, device: str = "cpu"):
+    """Frozen expert weights of one projection: torch [E, d_out, d_in],
+    N(0, 1/d_in), in the config's storage dtype."""
+    d_in, d_out, _ = cfg.proj_dims(proj)
+    return draw_tensor((cfg.E, d_out, d_in), 1.0 / math.sqrt(d_in), seed, proj + ".W", cfg.dtype,
+                       device)

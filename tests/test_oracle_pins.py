@@ -372,3 +372,59 @@ def test_rel_l2():
     assert O.rel_l2([0.0], [0.0]) == 0.0
     assert O.rel_l2([1e-30], [0.0]) == float("inf")
     assert abs(O.rel_l2([3.0, 4.0], [0.0, 4.0]) - 0.75) < 1e-15
+
+
+# ----------------------------- adapted expert projection (frozen W_e + adapter)
+
+def test_hand_adapted_projection():
+    g, a = GOLD["grouped"], GOLD["adapted"]
+    ids = _np(g["topk_ids"], np.int64)
+    Wb = _np(a["W"])
+    args = (_np(g["x"]), Wb, _np(g["A"]), _np(g["B"]), g["group_rank"], g["alpha"], ids,
+            g["E"], _np(g["expert_to_group"], np.int64), g["G"])
+    assert np.array_equal(O.expert_projection(_np(g["x"]), Wb, ids, g["E"]), _np(a["base"]))
+    assert np.array_equal(O.adapted_projection(*args), _np(a["y"]))
+    assert np.array_equal(O.brute_adapted_projection(*args), _np(a["y"]))
+
+
+@pytest.mark.parametrize("seed", range(3))
+@pytest.mark.parametrize("im", [O.INPUT_SHARED, O.INPUT_PER_PAIR])
+@pytest.mark.parametrize("expert_keys", [False, True])
+def test_adapted_projection_brute_force(seed, im, expert_keys):
+    p = tiny_problem(seed, input_mode=im, expert_keys=expert_keys, drop=(seed == 2))
+    rng = np.random.default_rng(100 + seed)
+    Wb = rng.normal(size=(p["E"], 5, 7))
+    a = (p["x"], Wb, p["A"], p["B"], p["ranks"], 16.0, p["ids"], p["E"], p["e2g"], p["n_keys"])
+    y0 = O.brute_adapted_projection(*a, input_mode=im)
+    y1 = O.adapted_projection(*a, input_mode=im)
+    assert O.rel_l2(y1, y0) < 1e-12
+    if seed == 2:   # the dropped pair's row stays zero
+        assert not y1[0].any()
+
+
+def test_adapted_projection_single_expert_is_merged_linear():
+    """One expert, k = 1: every token goes through W + s B A, a plain matmul
+    with the merged weight."""
+    rng = np.random.default_rng(11)
+    T, d_in, d_out, r = 9, 6, 4, 3
+    x = rng.normal(size=(T, d_in))
+    Wb = rng.normal(size=(1, d_out, d_in))
+    A = rng.normal(size=(r, d_in))
+    Bm = rng.normal(size=(d_out, r))
+    ids = np.zeros((T, 1), np.int64)
+    y = O.adapted_projection(x, Wb, A, Bm.reshape(-1), [r], 16.0, ids, 1, None, 1)
+    merged = Wb[0] + (16.0 / r) * np.matmul(Bm, A)
+    assert O.rel_l2(y, np.matmul(x, merged.T)) < 1e-14
+
+
+def test_adapted_projection_zero_adapter_is_base():
+    p = tiny_problem(1)
+    rng = np.random.default_rng(12)
+    Wb = rng.normal(size=(p["E"], 5, 7))
+    y = O.adapted_projection(p["x"], Wb, p["A"], np.zeros_like(p["B"]), p["ranks"], 16.0,
+                             p["ids"], p["E"], p["e2g"], p["n_keys"])
+    base = np.zeros((p["ids"].size, 5))
+    for t in range(p["ids"].shape[0]):          # per pair: x_t times W_e^T
+        for j in range(p["ids"].shape[1]):
+            base[t * p["ids"].shape[1] + j] = np.matmul(Wb[p["ids"][t, j]], p["x"][t])
+    assert O.rel_l2(y, base) < 1e-14
