@@ -410,6 +410,110 @@ def consolidation_bench(ace, cfg, seed, cpu=True, N=10000):
     return out
 
 
+def fused_projection_bench(ace, cfg, rt, seed, cpu=True):
+    """The adapted expert projection (frozen expert GEMM with the adapter
+    update in its epilogue, ace_moe_lora_fwd) for every projection of the
+    layer's forward, against the plain expert GEMM and against the GEMM
+    followed by the separate adapter forward (its read-modify-write of y)."""
+    import torch
+    dev = "cuda"
+    ids = torch.from_numpy(rt.topk_ids).to(dev)
+    e2g = torch.from_numpy(rt.expert_to_group).to(dev)
+    ert = ace.ace_group_permute(ids, cfg.E, None, rt.G, W.ROWS_EXPERT)
+    grt = ace.ace_group_permute(ids, cfg.E, e2g, rt.G, W.ROWS_GROUP_DEDUP)
+    granks = [int(r) for r in rt.group_rank]
+    eranks = [cfg.r_e] * cfg.E
+    ekey_g = [int(g) for g in rt.expert_to_group]
+    ekey_e = list(range(cfg.E))
+    P, b = cfg.P, (2 if cfg.dtype == "bf16" else 4)
+    per_proj, tot = {}, {}
+    gemm_flops = gemm_ms = 0.0
+    for proj in cfg.projections:
+        d_in, d_out, im = cfg.proj_dims(proj)
+        shared = im == W.INPUT_SHARED
+        tg = W.make_proj(cfg, proj, granks, seed=seed, device=dev)
+        te = W.make_proj(cfg, proj, eranks, seed=seed, device=dev)
+        Wt = W.draw_expert_weights(cfg, proj, seed=seed, device=dev)
+        y = torch.empty(P, d_out, dtype=tg.x.dtype, device=dev)
+        need = max(ace.ace_workspace_bytes(ace.ACE_OP_FWD, cfg.T, cfg.k, d_in, d_out, rt.G, max(granks)),
+                   ace.ace_workspace_bytes(ace.ACE_OP_FWD, cfg.T, cfg.k, d_in, d_out, cfg.E, cfg.r_e))
+        ws = torch.empty(need, dtype=torch.uint8, device=dev)
+
+        def base():
+            ace.ace_moe_lora_fwd(te.x, Wt, ert, y, input_mode=im)
+
+        def fused_ew():
+            ace.ace_moe_lora_fwd(te.x, Wt, ert, y, eranks, ekey_e, cfg.alpha, te.A, te.B, ert,
+                                 input_mode=im, ws=ws)
+
+        def unfused_ew():
+            base()
+            ace.ace_expertwise_lora_fwd(te.x, te.A, te.B, cfg.E, cfg.r_e, cfg.alpha, ert, y,
+                                        input_mode=im, ws=ws)
+
+        def fused_grp():
+            ace.ace_moe_lora_fwd(tg.x, Wt, ert, y, granks, ekey_g, cfg.alpha, tg.A, tg.B, grt,
+                                 input_mode=im, ws=ws)
+
+        def unfused_grp():
+            base()
+            ace.ace_grouped_lora_fwd(tg.x, tg.A, tg.B, granks, cfg.alpha, grt, y, input_mode=im,
+                                     ws=ws)
+
+        t = {"base": time_calls(base), "fused_expertwise": time_calls(fused_ew),
+             "unfused_expertwise": time_calls(unfused_ew)}
+        if shared:   # grouped execution on gate/up; down stays expert-wise in the ace path
+            t["fused_ace"], t["unfused_ace"] = time_calls(fused_grp), time_calls(unfused_grp)
+        else:
+            t["fused_ace"], t["unfused_ace"] = t["fused_expertwise"], t["unfused_expertwise"]
+        per_proj[proj] = t
+        for k, v in t.items():
+            tot[k] = tot.get(k, 0.0) + v
+        gemm_flops += 2.0 * P * d_in * d_out
+        gemm_ms += t["base"]
+        del Wt, y, ws, tg, te
+        torch.cuda.empty_cache()
+    achieved = gemm_flops / (gemm_ms * 1e-3) / 1e12
+    peak = MFMA_PEAK_TFLOPS[cfg.dtype]
+    out = {
+        "workload": f"{cfg.name} layer forward, projections {'/'.join(cfg.projections)}: "
+                    f"y = W_e x + s B A x per routed pair (P={P}), frozen W_e per expert, "
+                    f"adapters grouped on gate/up (ranks {sorted(set(granks))}) and expert-wise on down",
+        "ms_per_layer_fwd": tot,
+        "per_projection_ms": per_proj,
+        "value": P / (tot["fused_ace"] * 1e-3), "unit": "routed tokens/s (layer forward)",
+        "fusion_speedup_ace": tot["unfused_ace"] / tot["fused_ace"],
+        "fusion_speedup_expertwise": tot["unfused_expertwise"] / tot["fused_expertwise"],
+        "adapter_overhead_fused": tot["fused_ace"] / tot["base"] - 1.0,
+        "adapter_overhead_unfused": tot["unfused_ace"] / tot["base"] - 1.0,
+        "roofline": {"bound": "mfma", "kernel": "moe_gemm (expert GEMM, all projections)",
+                     "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
+                     "algorithmic_flops": gemm_flops, "ms": gemm_ms},
+    }
+    if cpu:
+        from oracle import ace_oracle as O
+        proj = cfg.projections[0]
+        d_in, d_out, im = cfg.proj_dims(proj)
+        tg = W.make_proj(cfg, proj, granks, seed=seed, device="cpu")
+        Wt = W.draw_expert_weights(cfg, proj, seed=seed, device="cpu")
+        args = (tg.x.double().numpy(), Wt.double().numpy(), tg.A.double().numpy(),
+                tg.B.double().numpy(), granks, cfg.alpha, rt.topk_ids.astype(np.int64), cfg.E,
+                rt.expert_to_group, rt.G)
+        times = []
+        while sum(times) < 10.0 and len(times) < 3:
+            t0 = time.perf_counter()
+            O.adapted_projection(*args, input_mode=im)
+            times.append(time.perf_counter() - t0)
+        dt = statistics.median(times)
+        out["cpu_baseline"] = {"value": P / dt, "unit": "routed tokens/s (one projection)",
+                               "kind": "oracle", "cores": torch.get_num_threads(),
+                               "sample": f"fp64 oracle adapted_projection over the whole {proj} "
+                                         f"projection ({P} routed pairs; inputs converted to fp64 "
+                                         f"once, not timed); median of {len(times)} runs, "
+                                         f"{dt:.2f} s per run"}
+    return out
+
+
 # ---------------------------------------------------------------- HBM traffic
 # Traffic is taken from two rocprofv3 counter passes over `--traffic-pass`
 # (FETCH_SIZE, then WRITE_SIZE), summarised by `--pmc-summary` into
@@ -528,7 +632,7 @@ SIMD_NUM = 1024   # 256 compute units x 4 SIMDs
 N_XCD = 8         # GRBM counters come summed over the XCDs; busy % uses the per-XCD count
 
 
-def mfma_summary(pmc_dir, labels_path, config, command):
+def mfma_summary(pmc_dir, labels_path, config, command, name=None):
     """profiles/mfma_<config>.txt: matrix-core utilisation per call and kernel
     from one counter pass: SQ_VALU_MFMA_BUSY_CYCLES (summed over the SIMDs)
     against GRBM_GUI_ACTIVE / 8 (the active cycles of one XCD) x 1024 SIMDs,
@@ -563,14 +667,15 @@ def mfma_summary(pmc_dir, labels_path, config, command):
             pooled.setdefault(n, []).append(v)
         groups = [("all", [(n, tuple(sum(x[i] for x in vs) for i in range(4))) for n, vs in pooled.items()])]
     for lab, ds in groups:
-        for (name, grid), (b, a, m, ns) in ds:
-            if "FillFunctor" in name or not any(t in name for t in ("ace::", "_ZN3ace")):
+        for (kname, grid), (b, a, m, ns) in ds:
+            if "FillFunctor" in kname or not any(t in kname for t in ("ace::", "_ZN3ace")):
                 continue
             util = 100.0 * b / (a / N_XCD * SIMD_NUM) if a > 0 else 0.0
             tf = m * 512 / (ns * 1e-9) / 1e12 if ns > 0 else 0.0
-            lines.append(f"{lab} {short_kernel(name)}({grid // kThreadsGuess}) {util:.2f} "
+            lines.append(f"{lab} {short_kernel(kname)}({grid // kThreadsGuess}) {util:.2f} "
                          f"{m * 512 / 1e9:.3f} {ns / 1e3:.1f} {tf:.1f} {100 * tf / 2500:.2f}")
-    name = config if labels_path else f"cka_{config}"   # an unmarked run is the consolidation step
+    if name is None:   # an unmarked run is the consolidation step unless named
+        name = config if labels_path else f"cka_{config}"
     os.makedirs(PROFILES, exist_ok=True)
     with open(os.path.join(PROFILES, f"mfma_{name}.txt"), "w") as out:
         out.write("\n".join(lines) + "\n")
@@ -641,7 +746,8 @@ def trace_summary(trace_dir, fetch_dir, labels_path, config, command):
 kThreadsGuess = 256   # threads per workgroup of the library's kernels (grid printed in blocks)
 
 
-def stats_summary(trace_dir, name, command, keep=("cka_", "consolidate_")):
+def stats_summary(trace_dir, name, command,
+                  keep=("cka_", "consolidate_", "moe_gemm", "contract", "expand", "permute")):
     """profiles/kernels_<name>.txt from a rocprofv3 --stats kernel summary:
     calls and average/min/max duration of the library's kernels."""
     import csv
@@ -702,6 +808,12 @@ def main():
                     help="skip the consolidation step (CKA, grouping, consolidated adapters)")
     ap.add_argument("--consolidation-only", action="store_true",
                     help="time only the consolidation step and print its object")
+    ap.add_argument("--summary-name", default=None,
+                    help="file name stem of an unlabeled --mfma-summary (profiles/mfma_<NAME>.txt)")
+    ap.add_argument("--no-fused", action="store_true",
+                    help="skip the adapted expert projection (expert GEMM with the adapter fused)")
+    ap.add_argument("--fused-only", action="store_true",
+                    help="time only the adapted expert projection and print its object")
     args = ap.parse_args()
 
     if args.pmc_summary:
@@ -715,7 +827,7 @@ def main():
         return
     if args.mfma_summary:
         mfma_summary(args.mfma_summary[0], None if args.mfma_summary[1] == "-" else args.mfma_summary[1],
-                     args.config, args.pmc_command)
+                     args.config, args.pmc_command, name=args.summary_name)
         return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -734,6 +846,10 @@ def main():
               flush=True)
         return
     rt = W.make_routing(cfg, args.seed)
+    if args.fused_only:
+        print(json.dumps(fused_projection_bench(ace, cfg, rt, args.seed,
+                                                cpu=not args.no_cpu_baseline)), flush=True)
+        return
     bufs = make_buffers(cfg, rt, args.seed)
     b = 2 if cfg.dtype == "bf16" else 4
     r_max = max(int(rt.group_rank.max()), cfg.r_e)
@@ -849,6 +965,9 @@ def main():
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(cfg, rt)
+    if not args.no_fused:
+        line["fused_projection"] = fused_projection_bench(ace, cfg, rt, args.seed,
+                                                          cpu=not args.no_cpu_baseline)
     if not args.no_consolidation and cfg.dtype == "bf16":
         line["consolidation"] = consolidation_bench(ace, cfg, args.seed, cpu=not args.no_cpu_baseline)
     print(json.dumps(line), flush=True)

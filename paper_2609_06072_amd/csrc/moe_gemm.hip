@@ -16,8 +16,8 @@
 // Data movement.  One K-block (64 bytes of every row: 32 bf16 or 16 fp32) per
 // stage; x and W_e pieces are copied global -> LDS directly
 // (global_load_lds_dwordx4), kGNbuf stages in flight.  Within a stage a row's
-// four 16-byte chunks sit XOR-swizzled by (row >> 2) & 3, so the fragment
-// reads of 16 consecutive rows hit distinct banks.  The adapter K-blocks (one
+// four 16-byte chunks sit XOR-swizzled (g_swz), so the fragment reads of 16
+// consecutive rows hit distinct banks.  The adapter K-blocks (one
 // or two) are read straight into registers while the first stages are in
 // flight.
 //
@@ -46,7 +46,12 @@ constexpr int kGWBytes = kGN * kGRowBytes;
 constexpr int kGStage = kGXBytes + kGWBytes;  // 24 KB
 constexpr int kGCopies = (kGM + kGN) / 16 / 4; // 16-row copies per wave per stage
 
-__device__ inline int g_swz(int row) { return (row >> 2) & 3; }
+// Chunk position of a row's 16-byte chunk 0.  Rows 64 bytes apart share a
+// bank line; the position differs for any two rows among 8 consecutive ones
+// with the same parity and among 16 consecutive ones with the same residue
+// mod 4, so a fragment read (16 rows, one chunk each) is free of bank
+// conflicts whether the LDS serves 8 or 16 lanes of a 16-byte read per cycle.
+__device__ inline int g_swz(int row) { return (((row >> 1) ^ (row >> 3)) & 1) | ((row >> 1) & 2); }
 
 // Number of tiles of BM rows over the key segments offsets[0 .. n_keys]
 // (wave-level; every lane gets the total).
@@ -79,7 +84,8 @@ __global__ __launch_bounds__(kThreads, 2) void moe_gemm_kernel(MoeArgs a) {
   __shared__ int s_out[kGM];   // y row, -1 past the segment
   __shared__ int s_h[kGM];     // adapter row, -1 for none
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int c16 = lane & 15, g = lane >> 4;
   const int wy = wave >> 1, wx = wave & 1;
 
@@ -112,35 +118,33 @@ __global__ __launch_bounds__(kThreads, 2) void moe_gemm_kernel(MoeArgs a) {
   const int nst = (d_in + KB - 1) / KB;
 
   // ---- copy assignment: lane covers row (lane >> 2) of each 16-row copy,
-  // chunk position lane & 3 (global chunk (lane & 3) ^ swizzle)
+  // chunk position lane & 3 (global chunk (lane & 3) ^ g_swz(row)).  The
+  // swizzle only sees bits 1..3 of the row, i.e. of lane >> 2, so one chunk
+  // offset serves every copy; rows are 32-bit element offsets from X or W_e.
   const int cpos = lane & 3, crl = lane >> 2;
-  const T* src[kGCopies];
-  uint32_t dst[kGCopies];
-  int coff[kGCopies];
+  const int coff = PER * (cpos ^ g_swz(crl));
+  uint32_t roff[kGCopies];
 #pragma unroll
   for (int i = 0; i < kGCopies; ++i) {
     const int blk = wave * kGCopies + i;      // 16-row copy index over [x rows | W rows]
     const int row = 16 * blk + crl;
-    coff[i] = PER * (cpos ^ g_swz(row));
-    if (16 * blk < kGM) {
-      src[i] = X + (size_t)s_src[row] * d_in;
-      dst[i] = 16 * blk * kGRowBytes;
-    } else {
-      const int wr = row - kGM;
-      src[i] = Wt + (size_t)min(n0 + wr, d_out - 1) * d_in;
-      dst[i] = kGXBytes + 16 * (blk - kGM / 16) * kGRowBytes;
-    }
+    roff[i] = 16 * blk < kGM ? (uint32_t)s_src[row] * (uint32_t)d_in
+                             : (uint32_t)min(n0 + row - kGM, d_out - 1) * (uint32_t)d_in;
   }
   const uint32_t sbase = lds_addr(smem);
   auto issue = [&](int st) {
     const uint32_t buf = sbase + (st % kGNbuf) * kGStage;
-    const int k0 = st * KB;
+    const uint32_t kk = (uint32_t)min(st * KB + coff, d_in - PER);
 #pragma unroll
-    for (int i = 0; i < kGCopies; ++i)
-      dma16(src[i] + min(k0 + coff[i], d_in - PER), __builtin_amdgcn_readfirstlane(buf + dst[i]));
+    for (int i = 0; i < kGCopies; ++i) {
+      const int blk = wave * kGCopies + i;
+      const bool xcopy = 16 * blk < kGM;
+      const uint32_t dst = xcopy ? 16 * blk * kGRowBytes : kGXBytes + 16 * (blk - kGM / 16) * kGRowBytes;
+      dma16((xcopy ? X : Wt) + (roff[i] + kk), __builtin_amdgcn_readfirstlane(buf + dst));
+    }
   };
 #pragma unroll
-  for (int s = 0; s < kGNbuf - 1; ++s)
+  for (int s = 0; s < kGNbuf; ++s)
     if (s < nst) issue(s);
 
   f32x4 acc[8][4];
@@ -176,30 +180,67 @@ __global__ __launch_bounds__(kThreads, 2) void moe_gemm_kernel(MoeArgs a) {
     }
   }
 
-  // ---- main loop over d_in
-  for (int st = 0; st < nst; ++st) {
-    wait_vmcnt_upto<(kGNbuf - 2) * kGCopies>(min(kGNbuf - 2, nst - 1 - st) * kGCopies);
-    __syncthreads();
-    if (st + kGNbuf - 1 < nst) issue(st + kGNbuf - 1);
-    const char* Xs = smem + (st % kGNbuf) * kGStage;
-    const char* Ws = Xs + kGXBytes;
-    const bool kval = st * KB + PER * g < d_in;   // chunk g of this K-block inside d_in
-    F xf[4], wf[8];
+  // ---- main loop over d_in, fragments double-buffered in registers: the
+  // LDS reads of K-block st + 1 are in flight while the matrix cores work on
+  // K-block st.
+  // fragment rows 64 wy + 16 mb + c16 (x) and 128 wx + 16 nb + c16 (W): the
+  // swizzle again depends on c16 only, so a read is a lane base plus an
+  // immediate offset
+  const int xl = (64 * wy + c16) * kGRowBytes + ((g ^ g_swz(c16)) << 4);
+  const int wl = kGXBytes + (128 * wx + c16) * kGRowBytes + ((g ^ g_swz(c16)) << 4);
+  auto read_frags = [&](int st, F (&xf)[4], F (&wf)[8]) {
+    const char* S = smem + (st % kGNbuf) * kGStage;
 #pragma unroll
-    for (int mb = 0; mb < 4; ++mb) {
-      const int rl = 64 * wy + 16 * mb + c16;
-      const F v = *reinterpret_cast<const F*>(Xs + rl * kGRowBytes + ((g ^ g_swz(rl)) << 4));
-      xf[mb] = kval ? v : Tr<T>::zero();
-    }
+    for (int mb = 0; mb < 4; ++mb) xf[mb] = *reinterpret_cast<const F*>(S + xl + mb * 16 * kGRowBytes);
 #pragma unroll
-    for (int nb = 0; nb < 8; ++nb) {
-      const int rl = 128 * wx + 16 * nb + c16;
-      wf[nb] = *reinterpret_cast<const F*>(Ws + rl * kGRowBytes + ((g ^ g_swz(rl)) << 4));
-    }
+    for (int nb = 0; nb < 8; ++nb)
+      wf[nb] = *reinterpret_cast<const F*>(S + wl + nb * 16 * kGRowBytes);
+  };
+  auto mma_all = [&](const F (&xf)[4], const F (&wf)[8]) {
 #pragma unroll
     for (int nb = 0; nb < 8; ++nb)
 #pragma unroll
       for (int mb = 0; mb < 4; ++mb) acc[nb][mb] = Tr<T>::mma(wf[nb], xf[mb], acc[nb][mb]);
+  };
+  // The last K-block may reach past d_in: once it has landed, its x chunks
+  // past d_in (copies of the clamped last chunk) are cleared in LDS, so no
+  // fragment read needs a mask.  Called with stage st landed and published
+  // (possibly twice for the last stage: clearing again changes nothing).
+  auto clear_tail = [&](int st) {
+    if (st != nst - 1 || d_in % KB == 0) return;
+    const int valid = (d_in - st * KB) / PER;   // chunks of this K-block inside d_in
+    char* S = smem + (st % kGNbuf) * kGStage;
+    for (int i = tid; i < kGM * 4; i += kThreads) {
+      const int row = i >> 2, pos = i & 3;
+      if ((pos ^ g_swz(row)) >= valid) *reinterpret_cast<u32x4*>(S + row * kGRowBytes + pos * 16) = u32x4{0u, 0u, 0u, 0u};
+    }
+    __syncthreads();
+  };
+  // Stage st lives in buffer st % kGNbuf.  Before K-block st + 1 is read, the
+  // barrier also tells that every wave holds K-block st in registers, so
+  // its buffer takes stage st + kGNbuf.
+  // Every half-step reads the next K-block unconditionally (clamped to the
+  // last one: a repeated read of a landed buffer is harmless), so the reads
+  // and the matrix work on the previous block share one basic block.
+  F xa[4], wa[8], xb[4], wb[8];
+  wait_vmcnt_upto<(kGNbuf - 1) * kGCopies>(min(kGNbuf - 1, nst - 1) * kGCopies);
+  __syncthreads();
+  clear_tail(0);
+  read_frags(0, xa, wa);
+  auto half = [&](int st, F (&xc)[4], F (&wc)[8], F (&xn)[4], F (&wn)[8]) {
+    // K-block st is in (xc, wc); K-block st + 1 lands in (xn, wn)
+    wait_vmcnt_upto<(kGNbuf - 2) * kGCopies>(min(kGNbuf - 2, nst - 2 - st) * kGCopies);
+    __syncthreads();
+    if (st + kGNbuf < nst) issue(st + kGNbuf);
+    const int sn = min(st + 1, nst - 1);
+    clear_tail(sn);
+    read_frags(sn, xn, wn);
+    mma_all(xc, wc);
+  };
+  for (int st = 0; st < nst; st += 2) {
+    half(st, xa, wa, xb, wb);
+    if (st + 1 >= nst) break;
+    half(st + 1, xb, wb, xa, wa);
   }
 
   // ---- epilogue: C tile -> LDS [m][n] (over the stage buffers), then whole
