@@ -160,6 +160,18 @@ def test_moe_max_rank_and_many_experts():
     check_rel("y", f64(run_moe(c, Wt)), oracle_y(c, Wt), TOL["bf16"])
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_moe_many_rows_per_expert(dtype):
+    """At >= 1024 routed rows per expert on average the launch switches to
+    256 x 256 tiles; ragged d_in, d_out and segment tails there too."""
+    cfg = W.CONFIGS["mixtral_bf16"].scaled(T=2600, k=1, E=2, d_model=264, d_ffn=136, dtype=dtype,
+                                           groups=("consecutive", 1))
+    assert cfg.P >= 1024 * cfg.E
+    for path in ("grouped", "down_expertwise"):
+        c, Wt = case_and_weights(cfg, path, seed=11)
+        check_rel("y", f64(run_moe(c, Wt)), oracle_y(c, Wt), TOL[dtype])
+
+
 def test_moe_deterministic():
     cfg = SMALL["qwen_bf16"]
     c, Wt = case_and_weights(cfg, "grouped", seed=7)
