@@ -441,25 +441,6 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
     e = launch_contract(p.dtype, c, p.r_max, P, stream);
   }
   if (e != hipSuccess) return e;
-  if (p.per_pair) {
-    ExpandArgs x{};
-    x.H = base + L.dHrow;
-    x.rpad = rpad;
-    x.W = base + L.At;
-    x.w_key_mul = 1;
-    x.w_stride_is_rank = 0;
-    x.offsets = p.rt->offsets;
-    x.row_token = p.rt->row_token;
-    x.row_slots = p.rt->row_slots;
-    x.k = p.k;
-    x.n_out = p.d_in;
-    x.out = dx;
-    x.pair_w = nullptr;
-    x.keys = p.keys;
-    e = launch_expand(p.dtype, x, p.r_max, P, stream);
-    if (e != hipSuccess) return e;
-  }
-
   GradArgs gr{};
   gr.x = p.x;
   gr.dy = dy;
@@ -480,7 +461,27 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
   gr.per_pair = p.per_pair;
   gr.keys = p.keys;
   e = launch_grads(p.dtype, gr, p.r_max, P, stream);
-  if (e != hipSuccess || p.per_pair) return e;
+  if (e != hipSuccess) return e;
+  if (p.per_pair) {
+    // dx = A^T dH per pair, after the weight gradients: they read dY again,
+    // which the contraction has just pulled through the caches, and dx's
+    // read-modify-write in between would push it out
+    ExpandArgs x{};
+    x.H = base + L.dHrow;
+    x.rpad = rpad;
+    x.W = base + L.At;
+    x.w_key_mul = 1;
+    x.w_stride_is_rank = 0;
+    x.offsets = p.rt->offsets;
+    x.row_token = p.rt->row_token;
+    x.row_slots = p.rt->row_slots;
+    x.k = p.k;
+    x.n_out = p.d_in;
+    x.out = dx;
+    x.pair_w = nullptr;
+    x.keys = p.keys;
+    return launch_expand(p.dtype, x, p.r_max, P, stream);
+  }
 
   DxArgs d{};
   d.dHf = base + L.dHf;
