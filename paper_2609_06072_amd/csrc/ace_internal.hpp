@@ -58,6 +58,11 @@ struct ContractArgs {
   const int32_t* ppos;        // [U+1] first pair position of each row, or null (one per row)
   void* out_dense;            // [T * kslots][R] or null
   int32_t kslots;
+  // row_sum (bf16, kSrcPairList): tiles hold whole rows; the results of a
+  // row's pairs, times their weights, are summed in the epilogue and stored
+  // per row (out_t column u - offsets[q], out_dense) -- dH_u = s B^T G_u
+  int32_t row_sum;
+  const int32_t* pair_row;    // row_sum: row serving each pair
   KeyTable keys;
 };
 

@@ -271,6 +271,12 @@ __global__ __launch_bounds__(kThreads) void contract_kernel(ContractArgs a) {
 // pieces with 16-byte chunks XOR-swizzled by row), NBUF stages in flight;
 // MFMA fragments are plain 16-byte LDS reads.  Only the weight rows below r_q
 // (rounded up to a copy) are copied.
+//
+// Row sums (row_sum, pair-position sources): a row serves up to k pairs, at
+// consecutive positions.  A tile then takes the rows whose first pair lies in
+// a window of 65 - k positions, so their pairs (at most 64) are all in the
+// tile; the per-pair results times the pair weights go to LDS in fp32 and
+// every row's sum (pairs in position order) is stored once.
 template <int RB>
 struct CDma {
   static constexpr int KC = RB <= 4 ? 128 : 64;  // contraction indices per stage
@@ -285,7 +291,77 @@ struct CDma {
   static constexpr int LDS = NBUF * (SBYTES + WBYTES);
   // LDS per CU is 160 KiB; the tile tables take about 4 KiB more per block
   static constexpr int BLOCKS_PER_CU = (160 * 1024) / (LDS + 4 * 1024 + 512) < 1 ? 1 : (160 * 1024) / (LDS + 4 * 1024 + 512);
+  // row sums: per-pair results [64][RPS] fp32 in the weight buffers
+  static constexpr int RPS = 16 * RB + 4;   // 16-byte skew between positions
+  static_assert(64 * RPS * 4 <= NBUF * WBYTES, "per-pair results exceed the weight buffers");
 };
+
+// Tile size in pair positions when rows are summed (every row's pairs lie in
+// the tile) or 64 rows otherwise.
+inline __host__ __device__ int contract_tile(int row_sum, int k) { return row_sum ? 65 - k : 64; }
+
+// Row sums of a tile whose pair positions p0 .. p1 - 1 hold rows ua .. ub - 1
+// (rstart = first position of this lane's row ua + lane, rtok its token):
+// the per-pair results, scaled and times the pair weights, go to LDS (fp32);
+// then lane l of wave w sums row ua + l over its pairs in position order for
+// the rank chunks 8w, 8w + 32, ... and stores the bf16 sum per key (column
+// u - rfirst) and/or per token.
+template <int RB>
+__device__ inline void row_sum_store(const ContractArgs& a, int q, const f32x4 (&acc)[RB], float s,
+                                     float pw, int ua, int ub, int p0, int p1, int rfirst,
+                                     int rstart, int rtok, float* hp) {
+  constexpr int RPS = CDma<RB>::RPS;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int c16 = lane & 15, g = lane >> 4;
+  const int r_q = a.keys.rank[q], roff = a.keys.roff[q], R = a.keys.R;
+  __syncthreads();   // every wave is done reading the staging buffers
+  {
+    float* dst = hp + (16 * wave + c16) * RPS;
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const int r0 = rank_of_row<__bf16>(rb, 4 * g);   // 4 consecutive ranks
+      f32x4 h = (acc[rb] * s) * pw;
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        if (r0 + v >= r_q) h[v] = 0.f;
+      *reinterpret_cast<f32x4*>(dst + r0) = h;
+    }
+  }
+  __syncthreads();
+  const int u = ua + lane;
+  int rend = __shfl_down(rstart, 1);
+  if (lane == 63 || u + 1 >= ub) rend = p1;
+  if (u >= ub) return;
+  const int b0 = rstart - p0, b1 = rend - p0;
+  __bf16* dt = static_cast<__bf16*>(a.out_t);
+  const long col = u - rfirst;
+  __bf16* df = a.out_dense ? static_cast<__bf16*>(a.out_dense) + (size_t)rtok * R + roff : nullptr;
+  for (int r0 = 8 * wave; r0 < r_q; r0 += 32) {
+    const float* src = hp + b0 * RPS + r0;
+    f32x4 lo = *reinterpret_cast<const f32x4*>(src), hi = *reinterpret_cast<const f32x4*>(src + 4);
+    for (int pos = b0 + 1; pos < b1; ++pos) {
+      src += RPS;
+      lo += *reinterpret_cast<const f32x4*>(src);
+      hi += *reinterpret_cast<const f32x4*>(src + 4);
+    }
+    const bf16x8 v = {(__bf16)lo[0], (__bf16)lo[1], (__bf16)lo[2], (__bf16)lo[3],
+                      (__bf16)hi[0], (__bf16)hi[1], (__bf16)hi[2], (__bf16)hi[3]};
+    if (dt) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (r0 + e < r_q) dt[(size_t)(roff + r0 + e) * a.ldh + col] = v[e];
+    }
+    if (df) {
+      if (r0 + 8 <= r_q && ((roff + r0) & 7) == 0) {
+        Tr<__bf16>::store(df + r0, v);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (r0 + e < r_q) df[r0 + e] = v[e];
+      }
+    }
+  }
+}
 
 template <int RB>
 __global__ __launch_bounds__(kThreads) void contract_dma_kernel(ContractArgs a) {
@@ -300,7 +376,10 @@ __global__ __launch_bounds__(kThreads) void contract_dma_kernel(ContractArgs a) 
   __shared__ int scan[kThreads];
   const int n_keys = a.keys.n_keys;
   const int bucket = blockIdx.x % kXcds;
-  build_bucket_table(a.offsets, a.src_mode == kSrcPairList ? a.ppos : nullptr, n_keys, 64, bucket,
+  const int K = a.K, k = a.k;
+  const bool rsum = a.row_sum != 0;   // implies kSrcPairList
+  const int TS = contract_tile(a.row_sum, k);
+  build_bucket_table(a.offsets, a.src_mode == kSrcPairList ? a.ppos : nullptr, n_keys, TS, bucket,
                      seg, bstart, bfirst, scan);
   const int total = bstart[n_keys];
   const int stride = gridDim.x / kXcds;  // the grid is a multiple of kXcds
@@ -308,16 +387,43 @@ __global__ __launch_bounds__(kThreads) void contract_dma_kernel(ContractArgs a) 
   const int c16 = lane & 15, g = lane >> 4;
   const __bf16* S = static_cast<const __bf16*>(a.src);
   const __bf16* W = static_cast<const __bf16*>(a.W);
-  const int K = a.K, k = a.k;
   const int nst = (K + KC - 1) / KC;
   const int cpos = lane & (CPR - 1), crow = lane / CPR;   // 16-byte position / row inside a copy
 
   for (int idx = blockIdx.x / kXcds; idx < total; idx += stride) {
     const int q = upper_index(bstart, n_keys, idx);
     const int lo = seg[q];
-    const int u0 = lo + (bfirst[q] + idx - bstart[q]) * 64;
-    const int u_end = seg[q + 1];
+    int u0 = lo + (bfirst[q] + idx - bstart[q]) * TS;
+    int u_end = seg[q + 1];
     const int r_q = a.keys.rank[q], roff = a.keys.roff[q];
+    // row sums: rows ua .. ub - 1 start inside the window [u0, u0 + TS); their
+    // pairs are positions ppos[ua] .. ppos[ub] - 1, which become u0 .. u_end
+    int ua = 0, ub = 0, rfirst = 0, rtok = 0, rstart = 0;
+    float pw = 1.f;
+    if (rsum) {
+      const int y = (lane & 1) ? min(u0 + TS, u_end) : u0;
+      int row, pos;
+      if (y < u_end) {   // first row starting at or after position y
+        const int r0 = a.pair_row[a.plist[y]];
+        const int s0 = a.ppos[r0], s1 = a.ppos[r0 + 1];
+        row = s0 == y ? r0 : r0 + 1;
+        pos = s0 == y ? s0 : s1;
+      } else {
+        row = a.offsets[q + 1];
+        pos = u_end;
+      }
+      ua = __shfl(row, 0);
+      ub = __shfl(row, 1);
+      u0 = __shfl(pos, 0);
+      u_end = __shfl(pos, 1);
+      if (ua >= ub) continue;   // block-uniform: no row starts in this window
+      rfirst = a.offsets[q];
+      if (ua + lane < ub) {     // this lane's row in the epilogue
+        rstart = a.ppos[ua + lane];
+        rtok = a.row_token[ua + lane];
+      }
+      if (a.pair_w) pw = a.pair_w[a.plist[min(u0 + 16 * wave + c16, u_end - 1)]];
+    }
     // weight copies this wave issues per stage (rows below r_q only)
     const int wcopies = (r_q + RPI - 1) / RPI;
     const int nw = min(G::NW, max(0, wcopies - wave * G::NW));
@@ -398,9 +504,14 @@ __global__ __launch_bounds__(kThreads) void contract_dma_kernel(ContractArgs a) 
       }
     }
 
+    const float s = a.alpha / (float)r_q;
+    if (rsum) {
+      row_sum_store<RB>(a, q, acc, s, pw, ua, ub, u0, u_end, rfirst, rstart, rtok,
+                        reinterpret_cast<float*>(&Wb[0][0]));
+      continue;
+    }
     const int u = u0 + 16 * wave + c16;
     if (u0 + 16 * wave >= u_end || u >= u_end) continue;
-    const float s = a.alpha / (float)r_q;
     f32x4 h[RB];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
@@ -419,8 +530,8 @@ hipError_t launch_contract_rb(const ContractArgs& a, long P, hipStream_t stream)
   // tiles per bucket <= (all tiles) / kXcds + n_keys
   const long per_bucket = P > 0 ? ((P + BM - 1) / BM + a.keys.n_keys) / kXcds + a.keys.n_keys : 0;
   if constexpr (std::is_same<T, __bf16>::value) {
-    // 64-row tiles
-    const long pb = P > 0 ? ((P + 63) / 64 + a.keys.n_keys) / kXcds + a.keys.n_keys : 0;
+    const int TS = contract_tile(a.row_sum, a.k);
+    const long pb = P > 0 ? ((P + TS - 1) / TS + a.keys.n_keys) / kXcds + a.keys.n_keys : 0;
     const long cap = (long)CDma<RB>::BLOCKS_PER_CU * device_cu_count() / kXcds;
     const int grid = (int)(pb < cap ? pb : cap) * kXcds;
     if (grid > 0) contract_dma_kernel<RB><<<grid, kThreads, 0, stream>>>(a);
@@ -447,6 +558,7 @@ int rank_pad(int dtype, int r_max) {
 
 hipError_t launch_contract(int dtype, const ContractArgs& a, int r_max, long P,
                            hipStream_t stream) {
+  if (a.row_sum && (dtype != ACE_BF16 || a.src_mode != kSrcPairList)) return hipErrorInvalidValue;
   const int rb = rank_blocks(r_max);
   if (dtype == ACE_BF16) {
     if (rb == 2) return launch_contract_rb<__bf16, 2>(a, P, stream);

@@ -17,7 +17,10 @@
 //                pair's weight (Hw).
 //   contract  -- dH per row (gathered G against B^T), stored per key as
 //                [r][u] and either as dense per-token rows (shared input) or
-//                row-major for the expand below (per-pair input).
+//                row-major for the expand below (per-pair input).  Rows that
+//                serve several pairs are contracted per pair and summed per
+//                row: in the contraction's epilogue (bf16) or by a combine
+//                launch (fp32).
 //   expand    -- per-pair input only: dx[t*k+j] += A_q^T dH_u (each row owns
 //                its input row).
 //   grads     -- dB_q over each key's pairs and dA_q over its rows (split into
@@ -420,7 +423,19 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
   c.src = dy;
   c.out_t_pairs = 0;
   c.ppos = nullptr;
-  if (multi) {
+  if (multi && p.dtype == ACE_BF16) {
+    // per pair position (single dY rows), summed per row in the epilogue
+    c.src_mode = kSrcPairList;
+    c.plist = plist;
+    c.ppos = ppos;
+    c.pair_row = p.rt->pair_row;
+    c.row_sum = 1;
+    c.out_w = 0;
+    c.out_t = base + L.dHt;
+    c.out_dense = base + L.dHf;
+    c.out_row = nullptr;
+    e = launch_contract(p.dtype, c, p.r_max, P, stream);
+  } else if (multi) {
     // per pair position (single dY rows), then summed per row
     c.src_mode = kSrcPairList;
     c.plist = plist;
