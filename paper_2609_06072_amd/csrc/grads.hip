@@ -209,7 +209,8 @@ __device__ inline void finish_item(const GradArgs& a, const Item& it, int item,
 #pragma unroll
     for (int cbi = 0; cbi < 2; ++cbi)
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb) part[((wave * 2 + cbi) * RB + rb) * 64 + lane] = acc[cbi][rb];
+      for (int rb = 0; rb < RB; ++rb)   // rank blocks past r_q are never read
+        if (rb < nrb) part[((wave * 2 + cbi) * RB + rb) * 64 + lane] = acc[cbi][rb];
   }
 }
 
@@ -515,11 +516,23 @@ __global__ __launch_bounds__(kThreads) void grad_reg_kernel(GradArgs a) {
   }
 }
 
-// One block per (key, dB|dA column block): sums the chunk partials in order.
+// Blocks of one (key, dB|dA column block) sum its chunk partials in chunk
+// order: Red::SPLIT blocks share an item's elements, four per thread, and the
+// partials of four chunks are loaded at once (clamped, masked in the sum).
+template <int RB>
+struct Red {
+  static constexpr int PER_ITEM = 4 * 2 * RB * 64;   // f32x4 elements of a partial
+  static constexpr int EPT = 4;                      // elements per thread
+  static constexpr int SPLIT = PER_ITEM / (kThreads * EPT);
+};
+
 template <int RB>
 __global__ __launch_bounds__(kThreads) void grad_reduce_kernel(GradArgs a) {
+  using G = Red<RB>;
+  constexpr int EPT = G::EPT, PER_ITEM = G::PER_ITEM, CB = 4;
   const int nb = a.nbB + a.nbA;
-  const int q = blockIdx.x / nb, rem = blockIdx.x % nb;
+  const int blk = blockIdx.x / G::SPLIT, sub = blockIdx.x % G::SPLIT;
+  const int q = blk / nb, rem = blk % nb;
   const bool isB = rem < a.nbB;
   const int cb = isB ? rem : rem - a.nbB;
   int b0, b1, a0, a1;
@@ -528,18 +541,39 @@ __global__ __launch_bounds__(kThreads) void grad_reduce_kernel(GradArgs a) {
   const int ns = isB ? nsB : n_split(a1 - a0);
   if (ns == 1) return;  // written directly by the gradient kernel
   const int first = key_first_item(a, q) + (isB ? cb : nsB * a.nbB + cb);
-  const int step = isB ? a.nbB : a.nbA;
+  const size_t cstride = (size_t)(isB ? a.nbB : a.nbA) * PER_ITEM;
   const int nrb = (a.keys.rank[q] + 15) >> 4;
-  const f32x4* part = reinterpret_cast<const f32x4*>(a.part);
-  constexpr int PER_ITEM = 4 * 2 * RB * 64;
-  for (int e = threadIdx.x; e < PER_ITEM; e += kThreads) {
-    const int lane = e & 63;
-    const int rb = (e >> 6) % RB;
-    const int wc = (e >> 6) / RB;  // wave * 2 + cbi
-    if (rb >= nrb) continue;
-    f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int c = 0; c < ns; ++c) s += part[(size_t)(first + c * step) * PER_ITEM + e];
-    store_grad(a, isB, q, cb * kColBlk, wc >> 1, wc & 1, rb, lane, s);
+  const f32x4* part = reinterpret_cast<const f32x4*>(a.part) + (size_t)first * PER_ITEM;
+  int e[EPT];
+  bool live[EPT];
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) {
+    e[i] = (sub * EPT + i) * kThreads + threadIdx.x;
+    live[i] = (e[i] >> 6) % RB < nrb;   // wave-uniform
+  }
+  f32x4 acc[EPT];
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int c0 = 0; c0 < ns; c0 += CB) {
+    f32x4 v[CB][EPT];
+#pragma unroll
+    for (int j = 0; j < CB; ++j) {
+      const size_t off = (size_t)min(c0 + j, ns - 1) * cstride;
+#pragma unroll
+      for (int i = 0; i < EPT; ++i) v[j][i] = live[i] ? part[off + e[i]] : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int j = 0; j < CB; ++j)
+      if (c0 + j < ns) {
+#pragma unroll
+        for (int i = 0; i < EPT; ++i) acc[i] += v[j][i];
+      }
+  }
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) {
+    if (!live[i]) continue;
+    const int lane = e[i] & 63, rb = (e[i] >> 6) % RB, wc = (e[i] >> 6) / RB;  // wc = wave * 2 + cbi
+    store_grad(a, isB, q, cb * kColBlk, wc >> 1, wc & 1, rb, lane, acc[i]);
   }
 }
 
@@ -815,7 +849,8 @@ hipError_t launch_grads_rb(int dtype, const GradArgs& g, long P, hipStream_t str
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (P > kSplitRows) grad_reduce_kernel<RB><<<g.keys.n_keys * nb, kThreads, 0, stream>>>(g);
+  if (P > kSplitRows)
+    grad_reduce_kernel<RB><<<g.keys.n_keys * nb * Red<RB>::SPLIT, kThreads, 0, stream>>>(g);
   return hipGetLastError();
 }
 
