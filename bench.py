@@ -138,11 +138,19 @@ class Path:
         a = self.ace
         names = {a.ACE_ROWS_GROUP_DEDUP: "group", a.ACE_ROWS_GROUP_PAIRS: "group_pairs",
                  a.ACE_ROWS_EXPERT: "expert"}
-        for m, rt in self.rts.items():
-            expert = m == a.ACE_ROWS_EXPERT
-            self._timed(("permute", names[m]), a.ace_group_permute, self.ids, self.cfg.E,
-                        None if expert else self.e2g, self.cfg.E if expert else self.G, m, rt,
+        group = [m for m in self.rts if m != a.ACE_ROWS_EXPERT]
+        if len(self.rts) == 2 and len(group) == 1:
+            # a group-keyed and the expert-keyed routing from one pass over the ids
+            g = group[0]
+            self._timed(("permute", names[g] + "+expert"), a.ace_group_expert_permute, self.ids,
+                        self.cfg.E, self.e2g, self.G, g, self.rts[g], self.rts[a.ACE_ROWS_EXPERT],
                         self.ws_perm)
+        else:
+            for m, rt in self.rts.items():
+                expert = m == a.ACE_ROWS_EXPERT
+                self._timed(("permute", names[m]), a.ace_group_permute, self.ids, self.cfg.E,
+                            None if expert else self.e2g, self.cfg.E if expert else self.G, m, rt,
+                            self.ws_perm)
         for p in self.projs:
             self._timed((p.name, "fwd"), self._fwd, p)
         for p in reversed(self.projs):
@@ -854,9 +862,12 @@ def main():
     b = 2 if cfg.dtype == "bf16" else 4
     r_max = max(int(rt.group_rank.max()), cfg.r_e)
     n_keys = max(cfg.E, rt.G)
+    # room for a group-keyed and an expert-keyed routing written by one call
     ws_perm = torch.empty(max(256, ace.ace_workspace_bytes(ace.ACE_OP_PERMUTE, cfg.T, cfg.k, 0, 0,
-                                                            n_keys, 0)), dtype=torch.uint8,
-                          device="cuda")
+                                                            rt.G, 0)
+                              + ace.ace_workspace_bytes(ace.ACE_OP_PERMUTE, cfg.T, cfg.k, 0, 0,
+                                                        n_keys, 0)),
+                          dtype=torch.uint8, device="cuda")
     need = 0
     for proj in cfg.projections:
         d_in, d_out, _ = cfg.proj_dims(proj)

@@ -149,6 +149,25 @@ ace_status ace_group_permute(const int32_t* topk_ids, int32_t T, int32_t k, int3
                              ace_routing* rt, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * Both routings an ACE layer needs from one top-k routing (Sec. 3.5 for the
+ * grouped gate/up projections; the down projection stays expert-wise, App. L):
+ * group_rt in group_mode (ACE_ROWS_GROUP_DEDUP or ACE_ROWS_GROUP_PAIRS,
+ * n_keys = G) and expert_rt in ACE_ROWS_EXPERT (n_keys = E), from one pass over
+ * topk_ids.  The outputs are bit-identical to two ace_group_permute calls.
+ *   group_rt, expert_rt  distinct structs with distinct device arrays.
+ *   ws, ws_bytes         device scratch, at least
+ *                        ace_workspace_bytes(ACE_OP_PERMUTE, T, k, 0, 0, G, 0) +
+ *                        ace_workspace_bytes(ACE_OP_PERMUTE, T, k, 0, 0, E, 0);
+ *                        4-byte aligned; needs no initialisation.
+ * Other arguments and errors as for ace_group_permute.
+ */
+ace_status ace_group_expert_permute(const int32_t* topk_ids, int32_t T, int32_t k, int32_t E,
+                                    const int32_t* expert_to_group, int32_t G,
+                                    ace_row_mode group_mode, ace_routing* group_rt,
+                                    ace_routing* expert_rt, void* ws, size_t ws_bytes,
+                                    void* stream);
+
+/*
  * Grouped LoRA forward (Sec. 3.4 output, Sec. 3.5 execution).
  *   group_rank  host int32 [G]: r_g, the consolidated rank of each group.
  *   alpha       LoRA scaling numerator (s_g = alpha / r_g).

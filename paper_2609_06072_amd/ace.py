@@ -27,7 +27,7 @@ ACE_ROWS_GROUP_DEDUP, ACE_ROWS_GROUP_PAIRS, ACE_ROWS_EXPERT = 0, 1, 2
 ACE_INPUT_SHARED, ACE_INPUT_PER_PAIR, ACE_INPUT_COMBINED = 0, 1, 2
 ACE_OP_PERMUTE, ACE_OP_FWD, ACE_OP_BWD, ACE_OP_CKA = 0, 1, 2, 3
 
-EXPORTS = ("ace_group_permute", "ace_grouped_lora_fwd", "ace_grouped_lora_bwd",
+EXPORTS = ("ace_group_permute", "ace_group_expert_permute", "ace_grouped_lora_fwd", "ace_grouped_lora_bwd",
            "ace_expertwise_lora_fwd", "ace_expertwise_lora_bwd", "ace_workspace_bytes",
            "ace_routing_check", "ace_last_error", "ace_pairwise_cka", "ace_similarity_graph",
            "ace_louvain", "ace_group_anchors", "ace_consolidate_adapters", "ace_moe_lora_fwd")
@@ -46,6 +46,9 @@ _i32, _f32, _vp, _sz = ctypes.c_int32, ctypes.c_float, ctypes.c_void_p, ctypes.c
 _R = ctypes.POINTER(AceRouting)
 _lib.ace_group_permute.argtypes = [_vp, _i32, _i32, _i32, _vp, _i32, _i32, _R, _vp, _sz, _vp]
 _lib.ace_group_permute.restype = _i32
+_lib.ace_group_expert_permute.argtypes = [_vp, _i32, _i32, _i32, _vp, _i32, _i32, _R, _R, _vp, _sz,
+                                          _vp]
+_lib.ace_group_expert_permute.restype = _i32
 _FWD = [_i32, _i32, _i32, _i32, _i32, _i32, _i32, _vp, _f32, _vp, _vp, _vp, _vp, _R, _vp, _vp, _sz, _vp]
 _BWD = [_i32, _i32, _i32, _i32, _i32, _i32, _i32, _vp, _f32, _vp, _vp, _vp, _vp, _R, _vp, _vp, _vp,
         _vp, _vp, _vp, _sz, _vp]
@@ -171,6 +174,29 @@ def ace_group_permute(topk_ids: torch.Tensor, E: int, expert_to_group: Optional[
                                   ctypes.byref(routing.c), _ptr(ws), ws.numel(), _stream(stream)),
            "ace_group_permute")
     return routing
+
+
+def ace_group_expert_permute(topk_ids: torch.Tensor, E: int, expert_to_group: torch.Tensor,
+                             G: int, group_mode: int = ACE_ROWS_GROUP_DEDUP,
+                             group_routing: Optional[Routing] = None,
+                             expert_routing: Optional[Routing] = None,
+                             ws: Optional[torch.Tensor] = None, stream=None):
+    """Group-keyed and expert-keyed routings from one pass over topk_ids."""
+    T, k = topk_ids.shape
+    if group_routing is None:
+        group_routing = Routing(T, k, G, device=topk_ids.device)
+    if expert_routing is None:
+        expert_routing = Routing(T, k, E, device=topk_ids.device)
+    need = (ace_workspace_bytes(ACE_OP_PERMUTE, T, k, 0, 0, G, 0)
+            + ace_workspace_bytes(ACE_OP_PERMUTE, T, k, 0, 0, E, 0))
+    if ws is None:
+        ws = torch.empty(max(need, 256), dtype=torch.uint8, device=topk_ids.device)
+    _check(_lib.ace_group_expert_permute(_ptr(topk_ids), T, k, E, _ptr(expert_to_group), G,
+                                         group_mode, ctypes.byref(group_routing.c),
+                                         ctypes.byref(expert_routing.c), _ptr(ws), ws.numel(),
+                                         _stream(stream)),
+           "ace_group_expert_permute")
+    return group_routing, expert_routing
 
 
 def ace_routing_check(routing: Routing, stream=None) -> int:

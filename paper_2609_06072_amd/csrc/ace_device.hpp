@@ -129,22 +129,29 @@ __device__ inline typename Tr<T>::frag load_frag(const T* p, int nvalid, bool ve
   return f;
 }
 
-// Exclusive block-wide scan of one int per thread (kThreads threads).
-__device__ inline int block_exclusive_scan(int v, int* lds /* kThreads ints */, int* total) {
-  const int t = threadIdx.x;
-  lds[t] = v;
-  __syncthreads();
+// Exclusive block-wide scan of one int per thread (kThreads threads): a
+// shuffle scan inside each wave, then the wave totals through LDS (two
+// barriers).  lds needs kThreads / 64 ints and is free again on return.
+__device__ inline int block_exclusive_scan(int v, int* lds, int* total) {
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  int incl = v;
 #pragma unroll
-  for (int off = 1; off < kThreads; off <<= 1) {
-    const int add = t >= off ? lds[t - off] : 0;
-    __syncthreads();
-    lds[t] += add;
-    __syncthreads();
+  for (int off = 1; off < 64; off <<= 1) {
+    const int o = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += o;
   }
-  const int incl = lds[t];
-  *total = lds[kThreads - 1];
+  if (lane == 63) lds[w] = incl;
   __syncthreads();
-  return incl - v;
+  int base = 0, tot = 0;
+#pragma unroll
+  for (int i = 0; i < kThreads / 64; ++i) {
+    const int s = lds[i];
+    if (i < w) base += s;
+    tot += s;
+  }
+  *total = tot;
+  __syncthreads();
+  return base + incl - v;
 }
 
 // Tile table of a launch over per-key row segments: tiles of BM rows,

@@ -29,9 +29,16 @@ struct Problem {
 
 int permute_tokens_per_block(int k);
 size_t permute_ws_bytes(int T, int k, int n_keys);
+// One routing written by a permutation launch sequence: its row mode, key
+// count, output arrays and workspace (permute_ws_bytes(T, k, n_keys)).
+struct PermuteOut {
+  int mode, n_keys;
+  const ace_routing* rt;
+  void* ws;
+};
+constexpr int kMaxPermPasses = 2;
 hipError_t launch_permute(const int32_t* ids, int T, int k, int E, const int32_t* e2g, int G,
-                          int mode, int n_keys, const ace_routing* rt, void* ws,
-                          hipStream_t stream);
+                          int npass, const PermuteOut* outs, hipStream_t stream);
 
 // Source of the rows of a rank contraction.
 constexpr int kSrcShared = 0;    // src[row_token[u]]

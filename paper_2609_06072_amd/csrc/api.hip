@@ -294,7 +294,53 @@ ace_status ace_group_permute(const int32_t* topk_ids, int32_t T, int32_t k, int3
   rt->mode = mode;
   rt->T = T;
   rt->k = k;
-  return hip_status(launch_permute(topk_ids, T, k, E, expert_to_group, G, mode, n_keys, rt, ws,
+  const PermuteOut out{(int)mode, n_keys, rt, ws};
+  return hip_status(launch_permute(topk_ids, T, k, E, expert_to_group, G, 1, &out,
+                                   static_cast<hipStream_t>(stream)),
+                    "permute launch");
+}
+
+ace_status ace_group_expert_permute(const int32_t* topk_ids, int32_t T, int32_t k, int32_t E,
+                                    const int32_t* expert_to_group, int32_t G,
+                                    ace_row_mode group_mode, ace_routing* group_rt,
+                                    ace_routing* expert_rt, void* ws, size_t ws_bytes,
+                                    void* stream) {
+  if (!group_rt || !expert_rt) return fail(ACE_ERR_INVALID_ARG, "routing is NULL");
+  if (group_rt == expert_rt) return fail(ACE_ERR_INVALID_ARG, "the two routings are the same struct");
+  if (group_mode != ACE_ROWS_GROUP_DEDUP && group_mode != ACE_ROWS_GROUP_PAIRS)
+    return fail(ACE_ERR_INVALID_ARG, "group mode %d is not a group-keyed mode", (int)group_mode);
+  if (T < 0) return fail(ACE_ERR_INVALID_ARG, "T = %d < 0", T);
+  if (k < 1 || k > kMaxK) return fail(ACE_ERR_UNSUPPORTED, "k = %d outside [1, %d]", k, kMaxK);
+  if ((int64_t)T * k >= (int64_t)1 << 31) return fail(ACE_ERR_UNSUPPORTED, "T*k >= 2^31");
+  if (E < 1 || E > kMaxKeys) return fail(ACE_ERR_UNSUPPORTED, "E = %d outside [1, %d]", E, kMaxKeys);
+  if (G < 1 || G > kMaxKeys) return fail(ACE_ERR_UNSUPPORTED, "G = %d outside [1, %d]", G, kMaxKeys);
+  if (!expert_to_group) return fail(ACE_ERR_INVALID_ARG, "expert_to_group is NULL");
+  if (T > 0 && !topk_ids) return fail(ACE_ERR_INVALID_ARG, "topk_ids is NULL");
+  for (const ace_routing* rt : {(const ace_routing*)group_rt, (const ace_routing*)expert_rt}) {
+    if (!rt->counts || !rt->offsets || !rt->n_dropped)
+      return fail(ACE_ERR_INVALID_ARG, "routing arrays are NULL");
+    if (T > 0 && (!rt->row_token || !rt->row_slots || !rt->pair_row || !rt->row_pair ||
+                   !rt->pair_list))
+      return fail(ACE_ERR_INVALID_ARG, "routing arrays are NULL");
+  }
+  // the group routing's cell tables first, the expert routing's after them
+  const size_t need_g = round256(permute_ws_bytes(T, k, G));
+  const size_t need = need_g + round256(permute_ws_bytes(T, k, E));
+  if (!ws || ws_bytes < need)
+    return fail(ACE_ERR_WORKSPACE, "permute needs %zu workspace bytes, got %zu", need,
+                ws ? ws_bytes : (size_t)0);
+  if (!aligned(ws, 4)) return fail(ACE_ERR_WORKSPACE, "workspace misaligned");
+  group_rt->n_keys = G;
+  group_rt->mode = group_mode;
+  expert_rt->n_keys = E;
+  expert_rt->mode = ACE_ROWS_EXPERT;
+  for (ace_routing* rt : {group_rt, expert_rt}) {
+    rt->T = T;
+    rt->k = k;
+  }
+  const PermuteOut outs[2] = {{(int)group_mode, G, group_rt, ws},
+                              {ACE_ROWS_EXPERT, E, expert_rt, static_cast<char*>(ws) + need_g}};
+  return hip_status(launch_permute(topk_ids, T, k, E, expert_to_group, G, 2, outs,
                                    static_cast<hipStream_t>(stream)),
                     "permute launch");
 }

@@ -7,10 +7,10 @@
 //              block's keys go to LDS; each emitted row sets the bit of its
 //              local pair index in a per-key bitmap (LDS, ds_or_b64), and the
 //              per-(key, block) population counts are written key-major.
-//   scan    -- one block: exclusive scan of the key-major counts gives each
-//              (key, block) its first row; counts/offsets/n_dropped written.
-//              Only for large cell tables: otherwise every scatter block
-//              derives the bases of its own cells from the count table
+//   scan    -- one block per routing: exclusive scan of the key-major counts
+//              gives each (key, block) its first row; counts/offsets/n_dropped
+//              written.  Only for large cell tables: otherwise every scatter
+//              block derives the bases of its own cells from the count table
 //              (per-key totals and prefixes, exact integer sums) and block 0
 //              writes counts/offsets/n_dropped.
 //   scatter -- rebuilds the bitmap; a row's rank inside its (key, block) cell
@@ -20,6 +20,12 @@
 // same scheme: in ACE_ROWS_GROUP_DEDUP mode a second bitmap marks every pair
 // of a key and second cell table is scanned; in the other modes a row is a
 // pair and its position is its row.
+//
+// One launch sequence can write two routings of the same top-k ids (a
+// group-keyed one and the expert-keyed one, as a layer with grouped gate/up
+// and expert-wise down projections needs): the ids and the expert -> group map
+// are read once per block, and each routing is a pass over the staged ids
+// with bitmaps and cell tables of its own.
 #include "ace_device.hpp"
 #include "ace_internal.hpp"
 
@@ -27,15 +33,16 @@ namespace ace {
 
 namespace {
 
-constexpr int kPairsPerBlock = 256;
+constexpr int kPairsPerBlock = 256;   // == kThreads: one pair per thread
 constexpr int kWordsPerKey = kPairsPerBlock / 64;
+// Largest cell tables (counts, plus pair counts in ACE_ROWS_GROUP_DEDUP mode)
+// the scatter folds itself: 32 KiB of LDS as 16-bit counts.
+constexpr int kFoldCells = 16384;
 
-struct PermArgs {
-  const int32_t* ids;
-  const int32_t* e2g;  // null in expert mode
-  int32_t T, k, E, G, mode, n_keys;
-  int32_t tokens_per_block, nblk;
+struct PermPass {
+  int32_t mode, n_keys;
   int32_t fold;        // the scatter derives the cell bases itself (no scan launch)
+  int32_t bits_off;    // first 64-bit word of this pass's bitmaps in LDS
   int32_t* cell;       // [n_keys * nblk] counts, then (scan) first rows
   int32_t* pcell;      // [n_keys * nblk] pair counts, then first pair positions (dedup)
   int32_t* drops;      // [nblk]
@@ -49,77 +56,120 @@ struct PermArgs {
   int32_t* pair_list;
 };
 
-// Stage the block's pair keys (-1 = dropped) and mark emitted rows in the
-// per-key bitmaps.  Returns the number of dropped pairs seen by this thread.
-// In ACE_ROWS_GROUP_DEDUP mode pbits (right after bits) also marks every pair.
-__device__ int stage_and_mark(const PermArgs& a, int p0, int np, int* keys, uint32_t* masks,
-                              unsigned long long* bits) {
+struct PermArgs {
+  const int32_t* ids;
+  const int32_t* e2g;  // null unless a pass is group-keyed
+  int32_t T, k, E, G;
+  int32_t tokens_per_block, nblk, npass, nwords;
+  PermPass pass[kMaxPermPasses];
+};
+
+__host__ __device__ inline int pass_words(int mode, int n_keys) {
+  return n_keys * kWordsPerKey * (mode == ACE_ROWS_GROUP_DEDUP ? 2 : 1);
+}
+
+// Pass i with a constant index for each branch (no dynamic indexing of the
+// kernel argument block).
+__device__ inline const PermPass& pass_of(const PermArgs& a, int i) {
+  return i == 0 ? a.pass[0] : a.pass[kMaxPermPasses - 1];
+}
+
+// The block's expert ids (one pair per thread; -1 when out of [0, E)) and the
+// map e -> g(e) (-1 when out of [0, G)), loaded together, plus cleared bitmaps.
+struct Staged {
+  int e, g;
+};
+
+__device__ inline Staged issue_ids(const PermArgs& a, int p0, int np) {
   const int t = threadIdx.x;
-  int drops = 0;
-  const bool dedup = a.mode == ACE_ROWS_GROUP_DEDUP;
-  unsigned long long* pbits = bits + a.n_keys * kWordsPerKey;
-  for (int i = t; i < a.n_keys * kWordsPerKey * (dedup ? 2 : 1); i += kThreads) bits[i] = 0ull;
-  for (int lp = t; lp < np; lp += kThreads) {
-    const int e = a.ids[p0 + lp];
-    int q = -1;
-    if (e >= 0 && e < a.E) {
-      if (a.mode == ACE_ROWS_EXPERT) {
-        q = e;
-      } else {
-        const int g = a.e2g[e];
-        q = (g >= 0 && g < a.G) ? g : -1;
-      }
-    }
-    drops += q < 0;
-    keys[lp] = q;
+  Staged s;
+  s.e = t < np ? a.ids[p0 + t] : -1;
+  s.g = (a.e2g && t < a.E) ? a.e2g[t] : -1;
+  return s;
+}
+
+__device__ inline void store_ids(const PermArgs& a, Staged s, int* eid, int* gmap,
+                                 unsigned long long* bits) {
+  const int t = threadIdx.x;
+  for (int i = t; i < a.nwords; i += kThreads) bits[i] = 0ull;
+  eid[t] = (s.e >= 0 && s.e < a.E) ? s.e : -1;
+  gmap[t] = (s.g >= 0 && s.g < a.G) ? s.g : -1;
+  __syncthreads();
+}
+
+// Keys of the block's pairs for pass P (-1 = dropped) and the emitted rows
+// marked in the pass's per-key bitmaps (in ACE_ROWS_GROUP_DEDUP mode a second
+// bitmap right after the first marks every pair).  Returns 1 when this
+// thread's pair is dropped.
+__device__ inline int mark_pass(const PermArgs& a, const PermPass& P, int np, const int* eid,
+                                const int* gmap, int* keys, uint32_t* masks,
+                                unsigned long long* bits) {
+  const int t = threadIdx.x;
+  const bool dedup = P.mode == ACE_ROWS_GROUP_DEDUP;
+  int q = -1;
+  if (t < np) {
+    const int e = eid[t];
+    q = e < 0 ? -1 : (P.mode == ACE_ROWS_EXPERT ? e : gmap[e]);
+    keys[t] = q;
   }
   __syncthreads();
-  const int k = a.k;
-  for (int lp = t; lp < np; lp += kThreads) {
-    const int q = keys[lp];
-    if (q < 0) { masks[lp] = 0u; continue; }
-    uint32_t m = 1u << (lp % k);
-    bool emit = true;
-    if (a.mode == ACE_ROWS_GROUP_DEDUP) {
-      // leader = first slot of the token with this group; mask = all of them
-      const int j = lp % k, tb = lp - j;
-      for (int jj = 0; jj < k; ++jj) {
-        if (keys[tb + jj] != q) continue;
-        if (jj < j) { emit = false; break; }
-        m |= 1u << jj;
+  if (t < np) {
+    if (q < 0) {
+      masks[t] = 0u;
+    } else {
+      const int k = a.k;
+      uint32_t m = 1u << (t % k);
+      bool emit = true;
+      if (dedup) {
+        // leader = first slot of the token with this group; mask = all of them
+        const int j = t % k, tb = t - j;
+        for (int jj = 0; jj < k; ++jj) {
+          if (keys[tb + jj] != q) continue;
+          if (jj < j) { emit = false; break; }
+          m |= 1u << jj;
+        }
       }
+      masks[t] = emit ? m : 0u;
+      if (emit) atomicOr(&bits[q * kWordsPerKey + (t >> 6)], 1ull << (t & 63));
+      if (dedup) atomicOr(&bits[(P.n_keys + q) * kWordsPerKey + (t >> 6)], 1ull << (t & 63));
     }
-    masks[lp] = emit ? m : 0u;
-    if (emit) atomicOr(&bits[q * kWordsPerKey + (lp >> 6)], 1ull << (lp & 63));
-    if (dedup) atomicOr(&pbits[q * kWordsPerKey + (lp >> 6)], 1ull << (lp & 63));
   }
   __syncthreads();
-  return drops;
+  return (t < np && q < 0) ? 1 : 0;
 }
 
 __global__ __launch_bounds__(kThreads) void permute_count_kernel(PermArgs a) {
-  extern __shared__ unsigned long long bits[];  // [n_keys * kWordsPerKey]
+  extern __shared__ unsigned long long bits[];  // every pass's bitmaps
+  __shared__ int eid[kPairsPerBlock];
+  __shared__ int gmap[kMaxKeys];
   __shared__ int keys[kPairsPerBlock];
   __shared__ uint32_t masks[kPairsPerBlock];
   __shared__ int red[kThreads];
   const int b = blockIdx.x;
   const int p0 = b * a.tokens_per_block * a.k;
   const int np = min(a.tokens_per_block * a.k, a.T * a.k - p0);
-  const int d = stage_and_mark(a, p0, np, keys, masks, bits);
-  const bool dedup = a.mode == ACE_ROWS_GROUP_DEDUP;
-  for (int q = threadIdx.x; q < a.n_keys; q += kThreads) {
-    int c = 0, pc = 0;
+  store_ids(a, issue_ids(a, p0, np), eid, gmap, bits);
 #pragma unroll
-    for (int w = 0; w < kWordsPerKey; ++w) {
-      c += __popcll(bits[q * kWordsPerKey + w]);
-      if (dedup) pc += __popcll(bits[(a.n_keys + q) * kWordsPerKey + w]);
+  for (int ps = 0; ps < kMaxPermPasses; ++ps) {
+    if (ps >= a.npass) break;
+    const PermPass& P = pass_of(a, ps);
+    unsigned long long* pb = bits + P.bits_off;
+    const int d = mark_pass(a, P, np, eid, gmap, keys, masks, pb);
+    const bool dedup = P.mode == ACE_ROWS_GROUP_DEDUP;
+    for (int q = threadIdx.x; q < P.n_keys; q += kThreads) {
+      int c = 0, pc = 0;
+#pragma unroll
+      for (int w = 0; w < kWordsPerKey; ++w) {
+        c += __popcll(pb[q * kWordsPerKey + w]);
+        if (dedup) pc += __popcll(pb[(P.n_keys + q) * kWordsPerKey + w]);
+      }
+      P.cell[q * a.nblk + b] = c;
+      if (dedup) P.pcell[q * a.nblk + b] = pc;
     }
-    a.cell[q * a.nblk + b] = c;
-    if (dedup) a.pcell[q * a.nblk + b] = pc;
+    int total;
+    block_exclusive_scan(d, red, &total);
+    if (threadIdx.x == 0) P.drops[b] = total;
   }
-  int total;
-  block_exclusive_scan(d, red, &total);
-  if (threadIdx.x == 0) a.drops[b] = total;
 }
 
 // Inclusive scan of one int per lane across a wave of 64.
@@ -204,153 +254,189 @@ __device__ int2 scan_cells(int32_t* v, int32_t* w, int N, int2* part) {
   return total;
 }
 
-// One block of 1024 threads: exclusive scans over the n_keys * nblk cells.
+// One block of 1024 threads per pass without a fold: exclusive scans over the
+// pass's n_keys * nblk cells.
 __global__ __launch_bounds__(1024) void permute_scan_kernel(PermArgs a) {
   __shared__ int2 part[32];
   __shared__ int dsum[16];
+  const PermPass& P = pass_of(a, blockIdx.x);
+  if (P.fold) return;
   const int t = threadIdx.x;
-  const int N = a.n_keys * a.nblk;
-  const bool dedup = a.mode == ACE_ROWS_GROUP_DEDUP;
-  const int2 tot = scan_cells(a.cell, dedup ? a.pcell : nullptr, N, part);
+  const int N = P.n_keys * a.nblk;
+  const bool dedup = P.mode == ACE_ROWS_GROUP_DEDUP;
+  const int2 tot = scan_cells(P.cell, dedup ? P.pcell : nullptr, N, part);
   const int U = tot.x;
   const int npairs = dedup ? tot.y : U;
-  for (int q = t; q < a.n_keys; q += 1024) {
-    const int first = a.nblk > 0 ? a.cell[q * a.nblk] : 0;
-    const int next = (q + 1 < a.n_keys && a.nblk > 0) ? a.cell[(q + 1) * a.nblk] : U;
-    a.offsets[q] = first;
-    a.counts[q] = next - first;
+  for (int q = t; q < P.n_keys; q += 1024) {
+    const int first = a.nblk > 0 ? P.cell[q * a.nblk] : 0;
+    const int next = (q + 1 < P.n_keys && a.nblk > 0) ? P.cell[(q + 1) * a.nblk] : U;
+    P.offsets[q] = first;
+    P.counts[q] = next - first;
   }
   int d = 0;
-  for (int b = t; b < a.nblk; b += 1024) d += a.drops[b];
+  for (int b = t; b < a.nblk; b += 1024) d += P.drops[b];
   d = wave_inclusive_scan(d);
   if ((t & 63) == 63) dsum[t >> 6] = d;
   __syncthreads();
   if (t == 0) {
     int dt = 0;
     for (int i = 0; i < 16; ++i) dt += dsum[i];
-    *a.n_dropped = dt;
-    a.offsets[a.n_keys] = U;
-    a.row_pair[U] = npairs;
+    *P.n_dropped = dt;
+    P.offsets[P.n_keys] = U;
+    P.row_pair[U] = npairs;
   }
 }
 
-constexpr int kFoldCells = 16384;   // largest cell table the scatter scans itself
+// Fold of pass P by scatter block b: per-key totals over all blocks and
+// prefixes over the blocks before b, summed from the key-major count tables
+// (exact integer sums); cbase/pbase = first row / pair position of b's cells.
+// Block 0 also writes counts, offsets, n_dropped and row_pair[U].
+// The tables are staged in LDS as 16-bit counts (a cell counts at most
+// kPairsPerBlock rows) by coalesced loads, all in flight at once; then
+// key q is summed by tpk threads of one wave (strided over the blocks) and a
+// butterfly over those lanes.
+__device__ inline void stage_counts(const int32_t* src, int N, uint16_t* dst) {
+  constexpr int B = 32;
+  const int t = threadIdx.x;
+  for (int i0 = 0; i0 < N; i0 += B * kThreads) {
+    int v[B];
+#pragma unroll
+    for (int j = 0; j < B; ++j)   // block-uniform guard; the last row clamped
+      if (i0 + j * kThreads < N) v[j] = src[min(i0 + j * kThreads + t, N - 1)];
+#pragma unroll
+    for (int j = 0; j < B; ++j) {
+      const int i = i0 + j * kThreads + t;
+      if (i0 + j * kThreads < N && i < N) dst[i] = (uint16_t)v[j];
+    }
+  }
+}
+
+__device__ void fold_pass(const PermArgs& a, const PermPass& P, int b, uint16_t* tab,
+                          int* tot, int* pre, int* ptot, int* ppre, int* cbase, int* pbase,
+                          int* red) {
+  const int t = threadIdx.x;
+  const bool dedup = P.mode == ACE_ROWS_GROUP_DEDUP;
+  const int nblk = a.nblk, n_keys = P.n_keys;
+  const int N = n_keys * nblk;
+  uint16_t* ptab = tab + N;
+  // block 0 sums the dropped counts: loads issued with the table's
+  int d = 0;
+  if (b == 0)
+    for (int bb = t; bb < nblk; bb += kThreads) d += P.drops[bb];
+  stage_counts(P.cell, N, tab);
+  if (dedup) stage_counts(P.pcell, N, ptab);
+  __syncthreads();
+  int tpk = 1;   // threads per key: a power of two, at most a wave
+  while (tpk < 64 && 2 * tpk * n_keys <= kThreads) tpk *= 2;
+  const int q = t / tpk, sub = t % tpk;
+  int st = 0, sp = 0, pt = 0, pp = 0;
+  if (q < n_keys) {
+    for (int bb = sub; bb < nblk; bb += tpk) {
+      const int c = tab[q * nblk + bb];
+      const int pc = dedup ? ptab[q * nblk + bb] : 0;
+      st += c;
+      pt += pc;
+      if (bb < b) {
+        sp += c;
+        pp += pc;
+      }
+    }
+  }
+  for (int o = tpk >> 1; o > 0; o >>= 1) {
+    st += __shfl_xor(st, o, 64);
+    sp += __shfl_xor(sp, o, 64);
+    pt += __shfl_xor(pt, o, 64);
+    pp += __shfl_xor(pp, o, 64);
+  }
+  if (sub == 0 && q < n_keys) {
+    tot[q] = st;
+    pre[q] = sp;
+    ptot[q] = pt;
+    ppre[q] = pp;
+  }
+  __syncthreads();
+  const int kq = t;   // n_keys <= kThreads
+  int U, npairs;
+  const int ks = block_exclusive_scan(kq < n_keys ? tot[kq] : 0, red, &U);
+  const int pks = block_exclusive_scan(kq < n_keys && dedup ? ptot[kq] : 0, red, &npairs);
+  if (kq < n_keys) {
+    cbase[kq] = ks + pre[kq];
+    pbase[kq] = pks + ppre[kq];
+    if (b == 0) {
+      P.offsets[kq] = ks;
+      P.counts[kq] = tot[kq];
+    }
+  }
+  if (b == 0) {
+    int dt;
+    block_exclusive_scan(d, red, &dt);
+    if (t == 0) {
+      P.offsets[n_keys] = U;
+      P.row_pair[U] = dedup ? npairs : U;
+      *P.n_dropped = dt;
+    }
+  }
+  __syncthreads();
+}
 
 __global__ __launch_bounds__(kThreads) void permute_scatter_kernel(PermArgs a) {
-  extern __shared__ unsigned long long bits[];
+  extern __shared__ unsigned long long bits[];   // bitmaps, then the staged count tables
+  __shared__ int eid[kPairsPerBlock];
+  __shared__ int gmap[kMaxKeys];
   __shared__ int keys[kPairsPerBlock];
   __shared__ uint32_t masks[kPairsPerBlock];
   __shared__ int tot[kMaxKeys], pre[kMaxKeys], ptot[kMaxKeys], ppre[kMaxKeys];
-  __shared__ int cbase[kMaxKeys], pbase[kMaxKeys];
+  __shared__ int cbase[kMaxPermPasses][kMaxKeys], pbase[kMaxPermPasses][kMaxKeys];
   __shared__ int red[kThreads];
   const int b = blockIdx.x;
   const int k = a.k;
   const int p0 = b * a.tokens_per_block * k;
   const int np = min(a.tokens_per_block * k, a.T * k - p0);
-  const bool dedup = a.mode == ACE_ROWS_GROUP_DEDUP;
-  if (a.fold) {
-    // per-key totals over all blocks and prefixes over the blocks before this one
-    const int t = threadIdx.x;
-    for (int q = t; q < a.n_keys; q += kThreads) tot[q] = pre[q] = ptot[q] = ppre[q] = 0;
-    __syncthreads();
-    // each thread sums a contiguous range of the key-major table (at most a
-    // few keys), then adds its per-key sums with one LDS atomic per key
-    const int N = a.n_keys * a.nblk;
-    const int per = (N + kThreads - 1) / kThreads;
-    const int lo = min(N, t * per), hi = min(N, lo + per);
-    int cq = lo < hi ? lo / a.nblk : 0;
-    int st = 0, sp = 0, pt = 0, pp = 0;
-    auto flush = [&]() {
-      if (st | sp | pt | pp) {
-        atomicAdd(&tot[cq], st);
-        atomicAdd(&pre[cq], sp);
-        atomicAdd(&ptot[cq], pt);
-        atomicAdd(&ppre[cq], pp);
-      }
-      st = sp = pt = pp = 0;
-    };
-    for (int i0 = lo; i0 < hi; i0 += 8) {
-      int cv[8], pv[8];
+  // the ids are in flight while the first cell table is staged
+  const Staged ids = issue_ids(a, p0, np);
+  uint16_t* tab = reinterpret_cast<uint16_t*>(bits + a.nwords);   // after the bitmaps
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {   // unconditional clamped loads, all in flight
-        const int i = min(i0 + j, N - 1);
-        cv[j] = a.cell[i];
-        pv[j] = dedup ? a.pcell[i] : 0;
-      }
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int i = i0 + j;
-        if (i < hi) {
-          const int q = i / a.nblk, bb = i - q * a.nblk;
-          if (q != cq) {
-            flush();
-            cq = q;
-          }
-          st += cv[j];
-          pt += pv[j];
-          if (bb < b) {
-            sp += cv[j];
-            pp += pv[j];
-          }
-        }
-      }
-    }
-    flush();
-    __syncthreads();
-    const int q = t;   // n_keys <= kThreads
-    int U, npairs;
-    const int ks = block_exclusive_scan(q < a.n_keys ? tot[q] : 0, red, &U);
-    const int pks = block_exclusive_scan(q < a.n_keys && dedup ? ptot[q] : 0, red, &npairs);
-    if (q < a.n_keys) {
-      cbase[q] = ks + pre[q];
-      pbase[q] = pks + ppre[q];
-      if (b == 0) {
-        a.offsets[q] = ks;
-        a.counts[q] = tot[q];
-      }
-    }
-    if (b == 0) {
-      int d = 0;
-      for (int bb = t; bb < a.nblk; bb += kThreads) d += a.drops[bb];
-      int dt;
-      block_exclusive_scan(d, red, &dt);
-      if (t == 0) {
-        a.offsets[a.n_keys] = U;
-        a.row_pair[U] = dedup ? npairs : U;
-        *a.n_dropped = dt;
-      }
-    }
-    __syncthreads();
+  for (int ps = 0; ps < kMaxPermPasses; ++ps) {
+    if (ps >= a.npass) break;
+    const PermPass& P = pass_of(a, ps);
+    if (P.fold) fold_pass(a, P, b, tab, tot, pre, ptot, ppre, cbase[ps], pbase[ps], red);
   }
-  stage_and_mark(a, p0, np, keys, masks, bits);
-  for (int lp = threadIdx.x; lp < np; lp += kThreads) {
+  store_ids(a, ids, eid, gmap, bits);
+#pragma unroll
+  for (int ps = 0; ps < kMaxPermPasses; ++ps) {
+    if (ps >= a.npass) break;
+    const PermPass& P = pass_of(a, ps);
+    unsigned long long* pbits = bits + P.bits_off;
+    mark_pass(a, P, np, eid, gmap, keys, masks, pbits);
+    const int lp = threadIdx.x;
+    if (lp >= np) continue;
     const int q = keys[lp];
     if (q < 0) {
-      a.pair_row[p0 + lp] = -1;
+      P.pair_row[p0 + lp] = -1;
       continue;
     }
     const uint32_t m = masks[lp];
     if (m == 0u) continue;  // served by its token's leader slot
-    const unsigned long long* kb = bits + q * kWordsPerKey;
+    const unsigned long long* kb = pbits + q * kWordsPerKey;
     const int w = lp >> 6;
     int rank = __popcll(kb[w] & ((1ull << (lp & 63)) - 1ull));
     for (int i = 0; i < w; ++i) rank += __popcll(kb[i]);
-    const int row = (a.fold ? cbase[q] : a.cell[q * a.nblk + b]) + rank;
+    const int row = (P.fold ? cbase[ps][q] : P.cell[q * a.nblk + b]) + rank;
     const int tok = (p0 + lp) / k;
-    a.row_token[row] = tok;
-    a.row_slots[row] = m;
+    P.row_token[row] = tok;
+    P.row_slots[row] = m;
     int pos = row;
-    if (a.mode == ACE_ROWS_GROUP_DEDUP) {  // the row's first pair among the key's pairs
-      const unsigned long long* pb = bits + (a.n_keys + q) * kWordsPerKey;
+    if (P.mode == ACE_ROWS_GROUP_DEDUP) {  // the row's first pair among the key's pairs
+      const unsigned long long* pb = pbits + (P.n_keys + q) * kWordsPerKey;
       int prank = __popcll(pb[w] & ((1ull << (lp & 63)) - 1ull));
       for (int i = 0; i < w; ++i) prank += __popcll(pb[i]);
-      pos = (a.fold ? pbase[q] : a.pcell[q * a.nblk + b]) + prank;
+      pos = (P.fold ? pbase[ps][q] : P.pcell[q * a.nblk + b]) + prank;
     }
-    a.row_pair[row] = pos;
+    P.row_pair[row] = pos;
     for (uint32_t mm = m; mm; mm &= mm - 1u) {
       const int p = tok * k + __builtin_ctz(mm);
-      a.pair_row[p] = row;
-      a.pair_list[pos++] = p;
+      P.pair_row[p] = row;
+      P.pair_list[pos++] = p;
     }
   }
 }
@@ -366,8 +452,8 @@ size_t permute_ws_bytes(int T, int k, int n_keys) {
 int permute_tokens_per_block(int k) { return k > 0 ? kPairsPerBlock / k : 1; }
 
 hipError_t launch_permute(const int32_t* ids, int T, int k, int E, const int32_t* e2g, int G,
-                          int mode, int n_keys, const ace_routing* rt, void* ws,
-                          hipStream_t stream) {
+                          int npass, const PermuteOut* outs, hipStream_t stream) {
+  if (npass < 1 || npass > kMaxPermPasses) return hipErrorInvalidValue;
   PermArgs a{};
   a.ids = ids;
   a.e2g = e2g;
@@ -375,31 +461,44 @@ hipError_t launch_permute(const int32_t* ids, int T, int k, int E, const int32_t
   a.k = k;
   a.E = E;
   a.G = G;
-  a.mode = mode;
-  a.n_keys = n_keys;
   a.tokens_per_block = permute_tokens_per_block(k);
   a.nblk = T > 0 ? (T + a.tokens_per_block - 1) / a.tokens_per_block : 0;
-  a.cell = static_cast<int32_t*>(ws);
-  a.pcell = a.cell + (size_t)a.nblk * n_keys;
-  a.drops = a.pcell + (size_t)a.nblk * n_keys;
-  a.counts = rt->counts;
-  a.offsets = rt->offsets;
-  a.row_token = rt->row_token;
-  a.row_slots = rt->row_slots;
-  a.pair_row = rt->pair_row;
-  a.n_dropped = rt->n_dropped;
-  a.row_pair = rt->row_pair;
-  a.pair_list = rt->pair_list;
-  const size_t lds = (size_t)n_keys * kWordsPerKey * sizeof(unsigned long long) *
-                     (mode == ACE_ROWS_GROUP_DEDUP ? 2 : 1);
-  a.fold = a.nblk > 0 && (long)a.nblk * n_keys <= kFoldCells;
-  if (a.nblk > 0) {
-    permute_count_kernel<<<a.nblk, kThreads, lds, stream>>>(a);
+  a.npass = npass;
+  bool scan = false;
+  int words = 0;
+  size_t tab_bytes = 0;   // largest staged count table pair of a folding pass
+  for (int i = 0; i < npass; ++i) {
+    const PermuteOut& o = outs[i];
+    PermPass& P = a.pass[i];
+    P.mode = o.mode;
+    P.n_keys = o.n_keys;
+    P.bits_off = words;
+    words += pass_words(o.mode, o.n_keys);
+    P.cell = static_cast<int32_t*>(o.ws);
+    P.pcell = P.cell + (size_t)a.nblk * o.n_keys;
+    P.drops = P.pcell + (size_t)a.nblk * o.n_keys;
+    P.counts = o.rt->counts;
+    P.offsets = o.rt->offsets;
+    P.row_token = o.rt->row_token;
+    P.row_slots = o.rt->row_slots;
+    P.pair_row = o.rt->pair_row;
+    P.n_dropped = o.rt->n_dropped;
+    P.row_pair = o.rt->row_pair;
+    P.pair_list = o.rt->pair_list;
+    P.fold = a.nblk > 0 &&
+             (long)a.nblk * o.n_keys * (o.mode == ACE_ROWS_GROUP_DEDUP ? 2 : 1) <= kFoldCells;
+    scan = scan || !P.fold;
+    if (P.fold) {
+      const size_t tb = (size_t)a.nblk * o.n_keys * sizeof(uint16_t) *
+                        (o.mode == ACE_ROWS_GROUP_DEDUP ? 2 : 1);
+      tab_bytes = tb > tab_bytes ? tb : tab_bytes;
+    }
   }
-  if (!a.fold) permute_scan_kernel<<<1, 1024, 0, stream>>>(a);
-  if (a.nblk > 0) {
-    permute_scatter_kernel<<<a.nblk, kThreads, lds, stream>>>(a);
-  }
+  a.nwords = words;
+  const size_t lds = (size_t)words * sizeof(unsigned long long);
+  if (a.nblk > 0) permute_count_kernel<<<a.nblk, kThreads, lds, stream>>>(a);
+  if (scan) permute_scan_kernel<<<npass, 1024, 0, stream>>>(a);
+  if (a.nblk > 0) permute_scatter_kernel<<<a.nblk, kThreads, lds + tab_bytes, stream>>>(a);
   return hipGetLastError();
 }
 

@@ -100,6 +100,40 @@ def test_permute_rejects_bad_arguments(ace, no_device):
     assert lib.ace_group_permute(ids, 4, 2, 8, e2g, 2, 0, None, ws, 1 << 20, None) == ace.ACE_ERR_INVALID_ARG
 
 
+def test_group_expert_permute_rejects_bad_arguments(ace, no_device):
+    lib = ace.raw_lib()
+    rg, re_ = _routing(ace), _routing(ace)
+    ws = ctypes.c_void_p(0x10000)
+    ids = ctypes.c_void_p(0x20000)
+    e2g = ctypes.c_void_p(0x30000)
+    need = (ace.ace_workspace_bytes(ace.ACE_OP_PERMUTE, 4, 2, 0, 0, 2, 0)
+            + ace.ace_workspace_bytes(ace.ACE_OP_PERMUTE, 4, 2, 0, 0, 8, 0))
+    cases = [
+        dict(k=0, status=ace.ACE_ERR_UNSUPPORTED),
+        dict(E=257, status=ace.ACE_ERR_UNSUPPORTED),
+        dict(G=0, status=ace.ACE_ERR_UNSUPPORTED),
+        dict(T=-1, status=ace.ACE_ERR_INVALID_ARG),
+        dict(mode=ace.ACE_ROWS_EXPERT, status=ace.ACE_ERR_INVALID_ARG),   # not a group mode
+        dict(mode=7, status=ace.ACE_ERR_INVALID_ARG),
+        dict(e2g=None, status=ace.ACE_ERR_INVALID_ARG),
+        dict(ids=None, status=ace.ACE_ERR_INVALID_ARG),
+        dict(same=True, status=ace.ACE_ERR_INVALID_ARG),
+        dict(ws_bytes=need - 4, status=ace.ACE_ERR_WORKSPACE),            # one routing's worth
+        dict(ws=None, status=ace.ACE_ERR_WORKSPACE),
+    ]
+    for c in cases:
+        a = dict(ids=ids, T=4, k=2, E=8, e2g=e2g, G=2, mode=0, ws=ws, ws_bytes=need, same=False)
+        a.update(c)
+        st = lib.ace_group_expert_permute(a["ids"], a["T"], a["k"], a["E"], a["e2g"], a["G"],
+                                          a["mode"], ctypes.byref(rg),
+                                          ctypes.byref(rg if a["same"] else re_), a["ws"],
+                                          a["ws_bytes"], None)
+        assert st == c["status"], (c, ace.ace_last_error())
+        assert ace.ace_last_error()
+    assert lib.ace_group_expert_permute(ids, 4, 2, 8, e2g, 2, 0, None, ctypes.byref(re_), ws, need,
+                                        None) == ace.ACE_ERR_INVALID_ARG
+
+
 def test_forward_backward_reject_bad_arguments(ace, no_device):
     lib = ace.raw_lib()
     ranks = (ctypes.c_int32 * 2)(16, 16)

@@ -40,11 +40,16 @@ SMALL = {
 
 def _perm_check(ids, E, e2g, G, mode):
     from paper_2609_06072_amd import ace
-    T, k = ids.shape
     dev = "cuda"
     rt = ace.ace_group_permute(torch.from_numpy(ids.astype(np.int32)).to(dev), E,
                                None if e2g is None else torch.from_numpy(e2g.astype(np.int32)).to(dev),
                                G, mode)
+    return _perm_compare(rt, ids, E, e2g, G, mode)
+
+
+def _perm_compare(rt, ids, E, e2g, G, mode):
+    from paper_2609_06072_amd import ace
+    T, k = ids.shape
     ref = O.permute(ids.astype(np.int64), E, None if mode == ace.ACE_ROWS_EXPERT else e2g, G, mode)
     U = ref["U"]
     torch.cuda.synchronize()
@@ -77,6 +82,46 @@ def test_permute_bitexact_full_size(name, mode):
     _perm_check(rt.topk_ids, cfg.E, rt.expert_to_group, rt.G, mode)
 
 
+def _dual_check(ids, E, e2g, G, mode):
+    """Both routings of one ace_group_expert_permute call against the oracle."""
+    from paper_2609_06072_amd import ace
+    dev = "cuda"
+    grt, ert = ace.ace_group_expert_permute(torch.from_numpy(ids.astype(np.int32)).to(dev), E,
+                                            torch.from_numpy(e2g.astype(np.int32)).to(dev), G,
+                                            mode)
+    assert (grt.c.mode, grt.c.n_keys, ert.c.mode, ert.c.n_keys) == (mode, G, ace.ACE_ROWS_EXPERT, E)
+    _perm_compare(grt, ids, E, e2g, G, mode)
+    _perm_compare(ert, ids, E, None, G, ace.ACE_ROWS_EXPERT)
+
+
+@pytest.mark.parametrize("name", W.CONFIG_ORDER)
+@pytest.mark.parametrize("mode", [0, 1])
+def test_group_expert_permute_bitexact_full_size(name, mode):
+    cfg = W.CONFIGS[name]
+    rt = W.make_routing(cfg)
+    say(f"group+expert permute {name} mode={mode}")
+    _dual_check(rt.topk_ids, cfg.E, rt.expert_to_group, rt.G, mode)
+
+
+def test_group_expert_permute_edge_cases():
+    rng = np.random.default_rng(5)
+    say("group+expert permute edges")
+    _dual_check(np.zeros((0, 4), np.int32), 8, np.arange(8) // 2, 4, 0)        # T = 0
+    ids = rng.integers(0, 10, size=(203, 4))                                     # dropped pairs
+    ids[::7, 1] = -1
+    ids[::11, 2] = 99
+    e2g = np.arange(10) // 3
+    e2g[9] = 17
+    _dual_check(ids, 10, e2g, 4, 0)
+    _dual_check(ids, 10, e2g, 4, 1)
+    ids = np.stack([rng.permutation(256)[:32] for _ in range(97)])              # k = 32, 256 keys
+    _dual_check(ids, 256, rng.permutation(256) // 2, 128, 0)
+    # a cell table too large for the scatter's own fold on the expert side
+    # (the scan launch) while the group side folds
+    ids = rng.integers(0, 64, size=(70001, 1))
+    _dual_check(ids, 64, rng.permutation(64) // 4, 16, 0)
+
+
 def test_permute_edge_cases():
     rng = np.random.default_rng(3)
     say("permute edges")
@@ -96,6 +141,9 @@ def test_permute_edge_cases():
     # every token on one expert / one group
     ids = np.stack([[5, 1] for _ in range(300)])
     _perm_check(ids, 8, np.arange(8) // 4, 2, 0)
+    # a cell table too large for the scatter's own fold (the scan launch)
+    ids = rng.integers(0, 64, size=(70001, 1))
+    _perm_check(ids, 64, None, 64, 2)
     # dropped pairs: out-of-range ids and a group id out of range
     ids = rng.integers(0, 10, size=(200, 4))
     ids[::7, 1] = -1
