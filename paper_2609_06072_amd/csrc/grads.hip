@@ -517,19 +517,20 @@ __global__ __launch_bounds__(kThreads) void grad_reg_kernel(GradArgs a) {
 }
 
 // Blocks of one (key, dB|dA column block) sum its chunk partials in chunk
-// order: Red::SPLIT blocks share an item's elements, four per thread, and the
-// partials of four chunks are loaded at once (clamped, masked in the sum).
+// order: Red::SPLIT blocks share an item's elements, two per thread, and the
+// partials of eight chunks are loaded at once (clamped, masked in the sum).
 template <int RB>
 struct Red {
   static constexpr int PER_ITEM = 4 * 2 * RB * 64;   // f32x4 elements of a partial
-  static constexpr int EPT = 4;                      // elements per thread
+  static constexpr int EPT = 2;                      // elements per thread
+  static constexpr int CB = 8;                       // chunks per batch of loads
   static constexpr int SPLIT = PER_ITEM / (kThreads * EPT);
 };
 
 template <int RB>
 __global__ __launch_bounds__(kThreads) void grad_reduce_kernel(GradArgs a) {
   using G = Red<RB>;
-  constexpr int EPT = G::EPT, PER_ITEM = G::PER_ITEM, CB = 4;
+  constexpr int EPT = G::EPT, PER_ITEM = G::PER_ITEM, CB = G::CB;
   const int nb = a.nbB + a.nbA;
   const int blk = blockIdx.x / G::SPLIT, sub = blockIdx.x % G::SPLIT;
   const int q = blk / nb, rem = blk % nb;

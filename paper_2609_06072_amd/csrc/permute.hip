@@ -23,9 +23,10 @@
 //
 // One launch sequence can write two routings of the same top-k ids (a
 // group-keyed one and the expert-keyed one, as a layer with grouped gate/up
-// and expert-wise down projections needs): the ids and the expert -> group map
-// are read once per block, and each routing is a pass over the staged ids
-// with bitmaps and cell tables of its own.
+// and expert-wise down projections needs): each routing is a pass with
+// bitmaps and cell tables of its own, and the blocks of both passes run side
+// by side in each launch (block i serves pass i / nblk, token chunk
+// i % nblk).
 #include "ace_device.hpp"
 #include "ace_internal.hpp"
 
@@ -42,7 +43,6 @@ constexpr int kFoldCells = 16384;
 struct PermPass {
   int32_t mode, n_keys;
   int32_t fold;        // the scatter derives the cell bases itself (no scan launch)
-  int32_t bits_off;    // first 64-bit word of this pass's bitmaps in LDS
   int32_t* cell;       // [n_keys * nblk] counts, then (scan) first rows
   int32_t* pcell;      // [n_keys * nblk] pair counts, then first pair positions (dedup)
   int32_t* drops;      // [nblk]
@@ -60,7 +60,8 @@ struct PermArgs {
   const int32_t* ids;
   const int32_t* e2g;  // null unless a pass is group-keyed
   int32_t T, k, E, G;
-  int32_t tokens_per_block, nblk, npass, nwords;
+  int32_t tokens_per_block, nblk, npass;
+  int32_t nwords;      // 64-bit words of bitmaps (the largest pass's)
   PermPass pass[kMaxPermPasses];
 };
 
@@ -139,37 +140,32 @@ __device__ inline int mark_pass(const PermArgs& a, const PermPass& P, int np, co
 }
 
 __global__ __launch_bounds__(kThreads) void permute_count_kernel(PermArgs a) {
-  extern __shared__ unsigned long long bits[];  // every pass's bitmaps
+  extern __shared__ unsigned long long bits[];  // the pass's bitmaps
   __shared__ int eid[kPairsPerBlock];
   __shared__ int gmap[kMaxKeys];
   __shared__ int keys[kPairsPerBlock];
   __shared__ uint32_t masks[kPairsPerBlock];
   __shared__ int red[kThreads];
-  const int b = blockIdx.x;
+  const int ps = blockIdx.x / a.nblk, b = blockIdx.x % a.nblk;
+  const PermPass& P = pass_of(a, ps);
   const int p0 = b * a.tokens_per_block * a.k;
   const int np = min(a.tokens_per_block * a.k, a.T * a.k - p0);
   store_ids(a, issue_ids(a, p0, np), eid, gmap, bits);
+  const int d = mark_pass(a, P, np, eid, gmap, keys, masks, bits);
+  const bool dedup = P.mode == ACE_ROWS_GROUP_DEDUP;
+  for (int q = threadIdx.x; q < P.n_keys; q += kThreads) {
+    int c = 0, pc = 0;
 #pragma unroll
-  for (int ps = 0; ps < kMaxPermPasses; ++ps) {
-    if (ps >= a.npass) break;
-    const PermPass& P = pass_of(a, ps);
-    unsigned long long* pb = bits + P.bits_off;
-    const int d = mark_pass(a, P, np, eid, gmap, keys, masks, pb);
-    const bool dedup = P.mode == ACE_ROWS_GROUP_DEDUP;
-    for (int q = threadIdx.x; q < P.n_keys; q += kThreads) {
-      int c = 0, pc = 0;
-#pragma unroll
-      for (int w = 0; w < kWordsPerKey; ++w) {
-        c += __popcll(pb[q * kWordsPerKey + w]);
-        if (dedup) pc += __popcll(pb[(P.n_keys + q) * kWordsPerKey + w]);
-      }
-      P.cell[q * a.nblk + b] = c;
-      if (dedup) P.pcell[q * a.nblk + b] = pc;
+    for (int w = 0; w < kWordsPerKey; ++w) {
+      c += __popcll(bits[q * kWordsPerKey + w]);
+      if (dedup) pc += __popcll(bits[(P.n_keys + q) * kWordsPerKey + w]);
     }
-    int total;
-    block_exclusive_scan(d, red, &total);
-    if (threadIdx.x == 0) P.drops[b] = total;
+    P.cell[q * a.nblk + b] = c;
+    if (dedup) P.pcell[q * a.nblk + b] = pc;
   }
+  int total;
+  block_exclusive_scan(d, red, &total);
+  if (threadIdx.x == 0) P.drops[b] = total;
 }
 
 // Inclusive scan of one int per lane across a wave of 64.
@@ -380,64 +376,55 @@ __device__ void fold_pass(const PermArgs& a, const PermPass& P, int b, uint16_t*
 }
 
 __global__ __launch_bounds__(kThreads) void permute_scatter_kernel(PermArgs a) {
-  extern __shared__ unsigned long long bits[];   // bitmaps, then the staged count tables
+  extern __shared__ unsigned long long bits[];   // the pass's bitmaps, then its count tables
   __shared__ int eid[kPairsPerBlock];
   __shared__ int gmap[kMaxKeys];
   __shared__ int keys[kPairsPerBlock];
   __shared__ uint32_t masks[kPairsPerBlock];
   __shared__ int tot[kMaxKeys], pre[kMaxKeys], ptot[kMaxKeys], ppre[kMaxKeys];
-  __shared__ int cbase[kMaxPermPasses][kMaxKeys], pbase[kMaxPermPasses][kMaxKeys];
+  __shared__ int cbase[kMaxKeys], pbase[kMaxKeys];
   __shared__ int red[kThreads];
-  const int b = blockIdx.x;
+  const int ps = blockIdx.x / a.nblk, b = blockIdx.x % a.nblk;
+  const PermPass& P = pass_of(a, ps);
   const int k = a.k;
   const int p0 = b * a.tokens_per_block * k;
   const int np = min(a.tokens_per_block * k, a.T * k - p0);
-  // the ids are in flight while the first cell table is staged
+  // the ids are in flight while the cell tables are staged
   const Staged ids = issue_ids(a, p0, np);
-  uint16_t* tab = reinterpret_cast<uint16_t*>(bits + a.nwords);   // after the bitmaps
-#pragma unroll
-  for (int ps = 0; ps < kMaxPermPasses; ++ps) {
-    if (ps >= a.npass) break;
-    const PermPass& P = pass_of(a, ps);
-    if (P.fold) fold_pass(a, P, b, tab, tot, pre, ptot, ppre, cbase[ps], pbase[ps], red);
-  }
+  if (P.fold)
+    fold_pass(a, P, b, reinterpret_cast<uint16_t*>(bits + a.nwords), tot, pre, ptot, ppre, cbase,
+              pbase, red);
   store_ids(a, ids, eid, gmap, bits);
-#pragma unroll
-  for (int ps = 0; ps < kMaxPermPasses; ++ps) {
-    if (ps >= a.npass) break;
-    const PermPass& P = pass_of(a, ps);
-    unsigned long long* pbits = bits + P.bits_off;
-    mark_pass(a, P, np, eid, gmap, keys, masks, pbits);
-    const int lp = threadIdx.x;
-    if (lp >= np) continue;
-    const int q = keys[lp];
-    if (q < 0) {
-      P.pair_row[p0 + lp] = -1;
-      continue;
-    }
-    const uint32_t m = masks[lp];
-    if (m == 0u) continue;  // served by its token's leader slot
-    const unsigned long long* kb = pbits + q * kWordsPerKey;
-    const int w = lp >> 6;
-    int rank = __popcll(kb[w] & ((1ull << (lp & 63)) - 1ull));
-    for (int i = 0; i < w; ++i) rank += __popcll(kb[i]);
-    const int row = (P.fold ? cbase[ps][q] : P.cell[q * a.nblk + b]) + rank;
-    const int tok = (p0 + lp) / k;
-    P.row_token[row] = tok;
-    P.row_slots[row] = m;
-    int pos = row;
-    if (P.mode == ACE_ROWS_GROUP_DEDUP) {  // the row's first pair among the key's pairs
-      const unsigned long long* pb = pbits + (P.n_keys + q) * kWordsPerKey;
-      int prank = __popcll(pb[w] & ((1ull << (lp & 63)) - 1ull));
-      for (int i = 0; i < w; ++i) prank += __popcll(pb[i]);
-      pos = (P.fold ? pbase[ps][q] : P.pcell[q * a.nblk + b]) + prank;
-    }
-    P.row_pair[row] = pos;
-    for (uint32_t mm = m; mm; mm &= mm - 1u) {
-      const int p = tok * k + __builtin_ctz(mm);
-      P.pair_row[p] = row;
-      P.pair_list[pos++] = p;
-    }
+  mark_pass(a, P, np, eid, gmap, keys, masks, bits);
+  const int lp = threadIdx.x;
+  if (lp >= np) return;
+  const int q = keys[lp];
+  if (q < 0) {
+    P.pair_row[p0 + lp] = -1;
+    return;
+  }
+  const uint32_t m = masks[lp];
+  if (m == 0u) return;  // served by its token's leader slot
+  const unsigned long long* kb = bits + q * kWordsPerKey;
+  const int w = lp >> 6;
+  int rank = __popcll(kb[w] & ((1ull << (lp & 63)) - 1ull));
+  for (int i = 0; i < w; ++i) rank += __popcll(kb[i]);
+  const int row = (P.fold ? cbase[q] : P.cell[q * a.nblk + b]) + rank;
+  const int tok = (p0 + lp) / k;
+  P.row_token[row] = tok;
+  P.row_slots[row] = m;
+  int pos = row;
+  if (P.mode == ACE_ROWS_GROUP_DEDUP) {  // the row's first pair among the key's pairs
+    const unsigned long long* pb = bits + (P.n_keys + q) * kWordsPerKey;
+    int prank = __popcll(pb[w] & ((1ull << (lp & 63)) - 1ull));
+    for (int i = 0; i < w; ++i) prank += __popcll(pb[i]);
+    pos = (P.fold ? pbase[q] : P.pcell[q * a.nblk + b]) + prank;
+  }
+  P.row_pair[row] = pos;
+  for (uint32_t mm = m; mm; mm &= mm - 1u) {
+    const int p = tok * k + __builtin_ctz(mm);
+    P.pair_row[p] = row;
+    P.pair_list[pos++] = p;
   }
 }
 
@@ -465,15 +452,14 @@ hipError_t launch_permute(const int32_t* ids, int T, int k, int E, const int32_t
   a.nblk = T > 0 ? (T + a.tokens_per_block - 1) / a.tokens_per_block : 0;
   a.npass = npass;
   bool scan = false;
-  int words = 0;
-  size_t tab_bytes = 0;   // largest staged count table pair of a folding pass
+  int words = 0;          // the largest pass's bitmaps
+  size_t tab_bytes = 0;   // the largest staged count tables of a folding pass
   for (int i = 0; i < npass; ++i) {
     const PermuteOut& o = outs[i];
     PermPass& P = a.pass[i];
     P.mode = o.mode;
     P.n_keys = o.n_keys;
-    P.bits_off = words;
-    words += pass_words(o.mode, o.n_keys);
+    words = pass_words(o.mode, o.n_keys) > words ? pass_words(o.mode, o.n_keys) : words;
     P.cell = static_cast<int32_t*>(o.ws);
     P.pcell = P.cell + (size_t)a.nblk * o.n_keys;
     P.drops = P.pcell + (size_t)a.nblk * o.n_keys;
@@ -496,9 +482,9 @@ hipError_t launch_permute(const int32_t* ids, int T, int k, int E, const int32_t
   }
   a.nwords = words;
   const size_t lds = (size_t)words * sizeof(unsigned long long);
-  if (a.nblk > 0) permute_count_kernel<<<a.nblk, kThreads, lds, stream>>>(a);
+  if (a.nblk > 0) permute_count_kernel<<<a.nblk * npass, kThreads, lds, stream>>>(a);
   if (scan) permute_scan_kernel<<<npass, 1024, 0, stream>>>(a);
-  if (a.nblk > 0) permute_scatter_kernel<<<a.nblk, kThreads, lds + tab_bytes, stream>>>(a);
+  if (a.nblk > 0) permute_scatter_kernel<<<a.nblk * npass, kThreads, lds + tab_bytes, stream>>>(a);
   return hipGetLastError();
 }
 
