@@ -163,6 +163,8 @@ struct GradArgs {
                               //   token, Hw = h per row), dA over the pairs (x row = plist,
                               //   dHt = w dH per pair position)
   int32_t nbB, nbA;           // column blocks of dB / dA (set by the launcher)
+  int32_t* itab;              // item table written by the gradient launch for the reduce
+                              //   (set by the launcher, after the partials)
   KeyTable keys;
 };
 

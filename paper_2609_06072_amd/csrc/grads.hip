@@ -52,6 +52,11 @@ struct GradTable {
 
 __device__ inline int n_split(int cnt) { return max(1, (cnt + kSplitRows - 1) / kSplitRows); }
 
+// Item table for the reduce: [0, n_keys] first item of each key, then at
+// kItabStride the dB chunk counts, at 2 kItabStride the dA chunk counts.
+constexpr int kItabStride = kMaxKeys + 1;
+constexpr int kItabInts = 3 * kItabStride;
+
 __device__ inline void build_grad_table(const GradArgs& a, GradTable& tb, int* scan_lds) {
   const int t = threadIdx.x;
   const int n_keys = a.keys.n_keys;
@@ -69,6 +74,11 @@ __device__ inline void build_grad_table(const GradArgs& a, GradTable& tb, int* s
   const int ex = block_exclusive_scan(items, scan_lds, &total);
   if (t < n_keys) tb.istart[t] = ex;
   if (t == 0) tb.istart[n_keys] = total;
+  if (blockIdx.x == 0 && t < n_keys) {   // for the reduce launch
+    a.itab[t] = ex;
+    a.itab[kItabStride + t] = n_split(tb.bseg[t + 1] - tb.bseg[t]);
+    a.itab[2 * kItabStride + t] = n_split(tb.aseg[t + 1] - tb.aseg[t]);
+  }
   __syncthreads();
 }
 
@@ -106,39 +116,6 @@ __device__ inline Item decode_item(const GradArgs& a, const GradTable& tb, int i
   it.k0 = it.s * kSplitRows;
   it.nk = max(0, min(cnt - it.k0, kSplitRows));
   return it;
-}
-
-// Segments of key q for the two contractions (see GradTable).
-__device__ inline void key_segments(const GradArgs& a, int q, int* b0, int* b1, int* a0, int* a1) {
-  const int o0 = a.offsets[q], o1 = a.offsets[q + 1];
-  const int p0 = a.ppos ? a.ppos[o0] : o0, p1 = a.ppos ? a.ppos[o1] : o1;
-  *b0 = a.combined ? o0 : p0;
-  *b1 = a.combined ? o1 : p1;
-  *a0 = a.combined ? p0 : o0;
-  *a1 = a.combined ? p1 : o1;
-}
-
-__device__ inline int key_items(const GradArgs& a, int b0, int b1, int a0, int a1) {
-  return n_split(b1 - b0) * a.nbB + n_split(a1 - a0) * a.nbA;
-}
-
-// First item of key q (a wave-level sum over the keys before it).
-__device__ inline int key_first_item(const GradArgs& a, int q) {
-  constexpr int KPL = kMaxKeys / 64;
-  const int lane = threadIdx.x & 63;
-  int s = 0;
-#pragma unroll
-  for (int i = 0; i < KPL; ++i) {
-    const int qq = lane * KPL + i;
-    if (qq < q) {
-      int b0, b1, a0, a1;
-      key_segments(a, qq, &b0, &b1, &a0, &a1);
-      s += key_items(a, b0, b1, a0, a1);
-    }
-  }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
-  return s;
 }
 
 // Row of the large operand for contraction index kabs of an item.
@@ -536,12 +513,10 @@ __global__ __launch_bounds__(kThreads) void grad_reduce_kernel(GradArgs a) {
   const int q = blk / nb, rem = blk % nb;
   const bool isB = rem < a.nbB;
   const int cb = isB ? rem : rem - a.nbB;
-  int b0, b1, a0, a1;
-  key_segments(a, q, &b0, &b1, &a0, &a1);
-  const int nsB = n_split(b1 - b0);
-  const int ns = isB ? nsB : n_split(a1 - a0);
+  const int nsB = a.itab[kItabStride + q];
+  const int ns = isB ? nsB : a.itab[2 * kItabStride + q];
   if (ns == 1) return;  // written directly by the gradient kernel
-  const int first = key_first_item(a, q) + (isB ? cb : nsB * a.nbB + cb);
+  const int first = a.itab[q] + (isB ? cb : nsB * a.nbB + cb);
   const size_t cstride = (size_t)(isB ? a.nbB : a.nbA) * PER_ITEM;
   const int nrb = (a.keys.rank[q] + 15) >> 4;
   const f32x4* part = reinterpret_cast<const f32x4*>(a.part) + (size_t)first * PER_ITEM;
@@ -838,10 +813,18 @@ __global__ __launch_bounds__(kThreads) void dx_dma_kernel(DxArgs a) {
   }
 }
 
+// Bytes of split partials (the item table follows them).
+size_t partial_bytes(long P, int n_keys, long nb, int rb) {
+  const long items = ((P + kSplitRows - 1) / kSplitRows + n_keys) * nb;
+  return (size_t)items * 4 * 2 * rb * 64 * sizeof(f32x4);
+}
+
 template <int RB>
-hipError_t launch_grads_rb(int dtype, const GradArgs& g, long P, hipStream_t stream) {
+hipError_t launch_grads_rb(int dtype, GradArgs g, long P, hipStream_t stream) {
   const int nb = g.nbB + g.nbA;
   const long items = ((P + kSplitRows - 1) / kSplitRows + g.keys.n_keys) * nb;
+  g.itab = reinterpret_cast<int32_t*>(static_cast<char*>(g.part) +
+                                      partial_bytes(P, g.keys.n_keys, nb, RB));
   const long cap = 8L * device_cu_count();
   const int grid = (int)(items < cap ? items : cap);
   if (grid > 0) {
@@ -860,8 +843,7 @@ hipError_t launch_grads_rb(int dtype, const GradArgs& g, long P, hipStream_t str
 size_t grads_part_bytes(int T, int k, int d_in, int d_out, int n_keys, int r_max) {
   const long P = (long)T * k;
   const long nb = (d_out + kColBlk - 1) / kColBlk + (d_in + kColBlk - 1) / kColBlk;
-  const long items = ((P + kSplitRows - 1) / kSplitRows + n_keys) * nb;
-  return (size_t)items * 4 * 2 * rank_blocks(r_max) * 64 * sizeof(f32x4);
+  return partial_bytes(P, n_keys, nb, rank_blocks(r_max)) + kItabInts * sizeof(int32_t);
 }
 
 hipError_t launch_grads(int dtype, GradArgs g, int r_max, long P, hipStream_t stream) {
