@@ -165,6 +165,41 @@ struct GradArgs {
   int32_t nbB, nbA;           // column blocks of dB / dA (set by the launcher)
   int32_t* itab;              // item table written by the gradient launch for the reduce
                               //   (set by the launcher, after the partials)
+  // phase 0: dB and dA items.  phase 1 (bf16, r_max <= 16): dB items only, each
+  // also contracting its dY columns against B^T into dHp; phase 2: dA items only
+  // (dH complete).  The split reduce runs after phases 0 and 2.
+  int32_t phase;
+  float* dHp;                 // phase 1: [nbB][npos][dhs] fp32, B_q^T dY per pair
+                              //   position, the 128 columns of one dB column block
+  long npos;
+  int32_t dhs;                // rank stride of dHp (8 or 16)
+  const void* Bt;             // phase 1: B^T [R][d_out], storage type
+  KeyTable keys;
+};
+
+// dH per row from the phase-1 partials (bf16):
+//   dH_u[r] = sum over the row's pairs p, in position order, of
+//             (s_q * sum_cb dHp[cb][p][r]) * w_p
+// stored per key as [r][u - offsets[q]] (dHt), and row-major [u][rpad] with
+// zeros past r_q (dHrow) or in dense per-token rows (dHf), either may be null.
+struct DhReduceArgs {
+  const float* dHp;
+  long npos;
+  int32_t dhs, nbB;
+  const int32_t* offsets;
+  const int32_t* row_token;
+  const uint32_t* row_slots;
+  const int32_t* ppos;        // [U+1] first pair position of each row, or null (position = row)
+  const int32_t* plist;       // pair at each position (weights of multi-pair rows)
+  const float* pair_w;
+  int32_t k;
+  float alpha;
+  void* dHt;
+  long ldh;
+  void* dHrow;
+  int32_t rpad;
+  void* dHf;                  // [T * kslots][R]: row tok * kslots + (kslots > 1 ? slot : 0)
+  int32_t kslots;
   KeyTable keys;
 };
 
@@ -179,6 +214,9 @@ struct DxArgs {
 
 size_t grads_part_bytes(int T, int k, int d_in, int d_out, int n_keys, int r_max);
 hipError_t launch_grads(int dtype, GradArgs g, int r_max, long P, hipStream_t stream);
+hipError_t launch_dh_reduce(const DhReduceArgs& d, long U, hipStream_t stream);
+// Columns per dB column block (the dH partials of phase 1 are per block).
+constexpr int kGradColBlk = 128;
 hipError_t launch_dx_gemm(int dtype, const DxArgs& d, hipStream_t stream);
 
 size_t bwd_ws_bytes(int T, int k, int d_in, int d_out, int n_keys, int R, int r_max);

@@ -35,7 +35,7 @@ namespace ace {
 
 namespace {
 
-constexpr int kColBlk = 128;     // gradient columns per item
+constexpr int kColBlk = kGradColBlk;   // gradient columns per item
 constexpr int kSplitRows = 1024; // contraction indices per item (split-K chunk)
 
 // Item table shared by the gradient kernels.  For key q the dB contraction
@@ -48,6 +48,7 @@ struct GradTable {
   int bseg[kMaxKeys + 1];
   int aseg[kMaxKeys + 1];
   int istart[kMaxKeys + 1];
+  int pstart[kMaxKeys + 1];   // first item of each key among the phase's items (phases 1, 2)
 };
 
 __device__ inline int n_split(int cnt) { return max(1, (cnt + kSplitRows - 1) / kSplitRows); }
@@ -67,13 +68,24 @@ __device__ inline void build_grad_table(const GradArgs& a, GradTable& tb, int* s
     tb.aseg[i] = a.combined ? po : o;
   }
   __syncthreads();
-  int items = 0;
-  if (t < n_keys)
-    items = n_split(tb.bseg[t + 1] - tb.bseg[t]) * a.nbB + n_split(tb.aseg[t + 1] - tb.aseg[t]) * a.nbA;
-  int total;
+  int items = 0, pitems = 0;
+  if (t < n_keys) {
+    const int ib = n_split(tb.bseg[t + 1] - tb.bseg[t]) * a.nbB;
+    const int ia = n_split(tb.aseg[t + 1] - tb.aseg[t]) * a.nbA;
+    items = ib + ia;
+    pitems = a.phase == 1 ? ib : ia;
+  }
+  int total, ptotal;
   const int ex = block_exclusive_scan(items, scan_lds, &total);
-  if (t < n_keys) tb.istart[t] = ex;
-  if (t == 0) tb.istart[n_keys] = total;
+  const int pex = block_exclusive_scan(pitems, scan_lds, &ptotal);
+  if (t < n_keys) {
+    tb.istart[t] = ex;
+    tb.pstart[t] = pex;
+  }
+  if (t == 0) {
+    tb.istart[n_keys] = total;
+    tb.pstart[n_keys] = ptotal;
+  }
   if (blockIdx.x == 0 && t < n_keys) {   // for the reduce launch
     a.itab[t] = ex;
     a.itab[kItabStride + t] = n_split(tb.bseg[t + 1] - tb.bseg[t]);
@@ -116,6 +128,15 @@ __device__ inline Item decode_item(const GradArgs& a, const GradTable& tb, int i
   it.k0 = it.s * kSplitRows;
   it.nk = max(0, min(cnt - it.k0, kSplitRows));
   return it;
+}
+
+// Global index of the i-th item of phase 1 (the dB items of every key) or
+// phase 2 (the dA items).
+__device__ inline int phase_item(const GradArgs& a, const GradTable& tb, int i) {
+  const int q = upper_index(tb.pstart, a.keys.n_keys, i);
+  const int local = i - tb.pstart[q];
+  if (a.phase == 1) return tb.istart[q] + local;
+  return tb.istart[q] + n_split(tb.bseg[q + 1] - tb.bseg[q]) * a.nbB + local;
 }
 
 // Row of the large operand for contraction index kabs of an item.
@@ -252,7 +273,7 @@ __device__ inline void load_rows(const GradArgs& a, const Item& it, int* idx) {
   for (int i = 0; i < MPT; ++i) idx[threadIdx.x + i * kThreads] = v[i];
 }
 
-template <int RB, bool ISB>
+template <int RB, bool ISB, bool DH>
 __device__ __forceinline__ void dma_item(const GradArgs& a, DmaSmem<RB>& sm, const Item& it,
                                          int item) {
   using G = DmaGeo<RB>;
@@ -304,6 +325,18 @@ __device__ __forceinline__ void dma_item(const GradArgs& a, DmaSmem<RB>& sm, con
   for (int cbi = 0; cbi < 2; ++cbi)
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) acc[cbi][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // phase 1: B_q^T fragments of the block's columns (rank c16 < 16, columns
+  // col0 + 32 kb + 8 g; zero past r_q and past d_out)
+  bf16x8 bfr[4];
+  if constexpr (DH) {
+    const __bf16* Btp = static_cast<const __bf16*>(a.Bt) + (size_t)(roff + min(c16, r_q - 1)) * a.d_out;
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      const int c = col0 + 32 * kb + 8 * g;
+      bfr[kb] = Tr<__bf16>::load(Btp + min(c, a.d_out - 8));
+      if (c >= a.d_out || c16 >= r_q) bfr[kb] = Tr<__bf16>::zero();
+    }
+  }
 
 #pragma unroll
   for (int p = 0; p < NBUF - 1; ++p)
@@ -351,6 +384,23 @@ __device__ __forceinline__ void dma_item(const GradArgs& a, DmaSmem<RB>& sm, con
         }
       }
     }
+    if constexpr (DH) {
+      // the stage's pairs against B_q^T over the block's 128 columns: wave w
+      // takes stage rows 16w .. 16w+15 (row c16 per lane), D[rank][pair]
+      const int r = 16 * wave + c16;
+      f32x4 h = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        const int c = kb * 4 + g;
+        const bf16x8 lf = *reinterpret_cast<const bf16x8*>(&sm.L[b][r * 256 + ((c ^ l_swz(r)) << 4)]);
+        h = Tr<__bf16>::mma(bfr[kb], lf, h);
+      }
+      const int kk = st * RS + r;   // chunk index of this lane's pair (rows past nk are copies)
+      if (kk < it.nk && 4 * g < a.dhs) {
+        const long pos = (long)it.kbase + it.k0 + kk;
+        *reinterpret_cast<f32x4*>(a.dHp + ((size_t)it.cb * a.npos + pos) * a.dhs + 4 * g) = h;
+      }
+    }
   }
   finish_item<RB>(a, it, item, acc);
 }
@@ -359,11 +409,85 @@ template <int RB>
 __global__ __launch_bounds__(kThreads) void grad_dma_kernel(GradArgs a) {
   __shared__ DmaSmem<RB> sm;
   build_grad_table(a, sm.tb, sm.idx);
-  const int total = sm.tb.istart[a.keys.n_keys];
-  for (int item = blockIdx.x; item < total; item += gridDim.x) {
+  const int n_keys = a.keys.n_keys;
+  const int total = a.phase == 0 ? sm.tb.istart[n_keys] : sm.tb.pstart[n_keys];
+  for (int i = blockIdx.x; i < total; i += gridDim.x) {
+    const int item = a.phase == 0 ? i : phase_item(a, sm.tb, i);
     const Item it = decode_item(a, sm.tb, item);
-    if (it.isB) dma_item<RB, true>(a, sm, it, item);
-    else dma_item<RB, false>(a, sm, it, item);
+    if (it.isB) {
+      if (a.phase == 1) dma_item<RB, true, true>(a, sm, it, item);
+      else dma_item<RB, true, false>(a, sm, it, item);
+    } else {
+      dma_item<RB, false, false>(a, sm, it, item);
+    }
+  }
+}
+
+// dH per row from the phase-1 partials.  Thread t takes row blk * (256 / nq)
+// + t / nq and rank quad t % nq (nq = dhs / 4); the partials of the nbB column
+// blocks are loaded eight at a time and summed in block order.
+__global__ __launch_bounds__(kThreads) void dh_reduce_kernel(DhReduceArgs a) {
+  __shared__ int seg[kMaxKeys + 1];
+  const int n_keys = a.keys.n_keys;
+  for (int i = threadIdx.x; i <= n_keys; i += kThreads) seg[i] = a.offsets[i];
+  __syncthreads();
+  const int nq = a.dhs / 4;
+  const int u = blockIdx.x * (kThreads / nq) + threadIdx.x / nq;
+  const int quad = threadIdx.x % nq;
+  if (u >= seg[n_keys]) return;
+  const int q = upper_index(seg, n_keys, u);
+  const int r_q = a.keys.rank[q], roff = a.keys.roff[q], R = a.keys.R;
+  const int r0 = 4 * quad;
+  const int p0 = a.ppos ? a.ppos[u] : u, p1 = a.ppos ? a.ppos[u + 1] : u + 1;
+  const int tok = a.row_token[u];
+  const float s = a.alpha / (float)r_q;
+  f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (r0 < r_q) {
+    for (int p = p0; p < p1; ++p) {
+      float w = 1.f;
+      if (a.pair_w)
+        w = a.pair_w[a.ppos ? a.plist[p] : tok * a.k + (__builtin_ctz(a.row_slots[u] | 0x80000000u) & 31)];
+      f32x4 v = f32x4{0.f, 0.f, 0.f, 0.f};
+      const f32x4* src = reinterpret_cast<const f32x4*>(a.dHp + (size_t)p * a.dhs + r0);
+      const size_t cstride = (size_t)a.npos * a.dhs / 4;
+      for (int c0 = 0; c0 < a.nbB; c0 += 8) {
+        f32x4 t[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) t[j] = src[(size_t)min(c0 + j, a.nbB - 1) * cstride];
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          if (c0 + j < a.nbB) v += t[j];
+      }
+      const f32x4 h = (v * s) * w;
+      if (p == p0) acc = h;
+      else acc += h;
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (r0 + e >= r_q) acc[e] = 0.f;
+  }
+  const __bf16 hv[4] = {(__bf16)acc[0], (__bf16)acc[1], (__bf16)acc[2], (__bf16)acc[3]};
+  if (a.dHt) {
+    __bf16* dt = static_cast<__bf16*>(a.dHt);
+    const long col = u - seg[q];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (r0 + e < r_q) dt[(size_t)(roff + r0 + e) * a.ldh + col] = hv[e];
+  }
+  if (a.dHrow) {   // zeros past r_q up to rpad
+    __bf16* dr = static_cast<__bf16*>(a.dHrow) + (size_t)u * a.rpad;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) dr[r0 + e] = hv[e];
+    if (quad == 0)
+      for (int r = a.dhs; r < a.rpad; ++r) dr[r] = (__bf16)0.f;
+  }
+  if (a.dHf) {
+    const int j0 = __builtin_ctz(a.row_slots[u] | 0x80000000u) & 31;
+    const size_t drow = (size_t)tok * a.kslots + (a.kslots > 1 ? j0 : 0);
+    __bf16* df = static_cast<__bf16*>(a.dHf) + drow * R + roff;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (r0 + e < r_q) df[r0 + e] = hv[e];
   }
 }
 
@@ -821,6 +945,7 @@ size_t partial_bytes(long P, int n_keys, long nb, int rb) {
 
 template <int RB>
 hipError_t launch_grads_rb(int dtype, GradArgs g, long P, hipStream_t stream) {
+  if (g.phase != 0 && dtype != ACE_BF16) return hipErrorInvalidValue;
   const int nb = g.nbB + g.nbA;
   const long items = ((P + kSplitRows - 1) / kSplitRows + g.keys.n_keys) * nb;
   g.itab = reinterpret_cast<int32_t*>(static_cast<char*>(g.part) +
@@ -833,7 +958,7 @@ hipError_t launch_grads_rb(int dtype, GradArgs g, long P, hipStream_t stream) {
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (P > kSplitRows)
+  if (P > kSplitRows && g.phase != 1)   // the dB partials of phase 1 are reduced after phase 2
     grad_reduce_kernel<RB><<<g.keys.n_keys * nb * Red<RB>::SPLIT, kThreads, 0, stream>>>(g);
   return hipGetLastError();
 }
@@ -854,6 +979,14 @@ hipError_t launch_grads(int dtype, GradArgs g, int r_max, long P, hipStream_t st
   if (rb == 4) return launch_grads_rb<4>(dtype, g, P, stream);
   if (rb == 8) return launch_grads_rb<8>(dtype, g, P, stream);
   return launch_grads_rb<16>(dtype, g, P, stream);
+}
+
+hipError_t launch_dh_reduce(const DhReduceArgs& d, long U, hipStream_t stream) {
+  if (d.dhs != 8 && d.dhs != 16) return hipErrorInvalidValue;
+  const int rows_per_block = kThreads / (d.dhs / 4);
+  const long blocks = (U + rows_per_block - 1) / rows_per_block;
+  if (blocks > 0) dh_reduce_kernel<<<(int)blocks, kThreads, 0, stream>>>(d);
+  return hipGetLastError();
 }
 
 hipError_t launch_dx_gemm(int dtype, const DxArgs& d, hipStream_t stream) {

@@ -39,8 +39,13 @@ constexpr int kMaxJobs = kMaxKeys + 3;
 size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 
 struct WsLayout {
-  size_t At, Bt, Ht, dHt, dHf, dHrow, part, total;
+  size_t At, Bt, Ht, dHt, dHf, dHrow, part, dHp, total;
 };
+
+// Ranks up to 16 take the backward in which the dB pass also contracts dY
+// against B^T (bf16): its fp32 partials per column block use this rank stride.
+constexpr int kFusedDhMaxRank = 16;
+int dh_stride(int r_max) { return r_max <= 8 ? 8 : 16; }
 
 // Workspace regions for element size es: At [d_in][R], Bt [R][d_out],
 // Ht/dHt [R][ldh] (column = row index inside the key's segment), dense dH
@@ -52,6 +57,7 @@ WsLayout ws_layout(int T, int k, int d_in, int d_out, int n_keys, int R, int r_m
   const int rpad = rank_pad(ACE_F32, r_max);
   const size_t P = (size_t)T * k;
   const size_t ldh = (P + 7) & ~(size_t)7;
+  const size_t nbB = (d_out + kGradColBlk - 1) / kGradColBlk;
   WsLayout w{};
   size_t o = 0;
   w.At = o;    o += align256(es * d_in * R);
@@ -61,6 +67,7 @@ WsLayout ws_layout(int T, int k, int d_in, int d_out, int n_keys, int R, int r_m
   w.dHf = o;   o += align256(es * P * R);
   w.dHrow = o; o += align256(es * P * rpad);
   w.part = o;  o += align256(grads_part_bytes(T, k, d_in, d_out, n_keys, r_max));
+  w.dHp = o;   o += r_max <= kFusedDhMaxRank ? align256(sizeof(float) * nbB * P * dh_stride(r_max)) : 0;   // per-pair input only
   w.total = o + 256;
   return w;
 }
@@ -416,46 +423,6 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
     e = launch_contract(p.dtype, c, p.r_max, P, stream);
     if (e != hipSuccess) return e;
   }
-  // dH = s B^T G
-  c.W = base + L.Bt;
-  c.ldw = p.d_out;
-  c.K = p.d_out;
-  c.src = dy;
-  c.out_t_pairs = 0;
-  c.ppos = nullptr;
-  if (multi && p.dtype == ACE_BF16) {
-    // per pair position (single dY rows), summed per row in the epilogue
-    c.src_mode = kSrcPairList;
-    c.plist = plist;
-    c.ppos = ppos;
-    c.pair_row = p.rt->pair_row;
-    c.row_sum = 1;
-    c.out_w = 0;
-    c.out_t = base + L.dHt;
-    c.out_dense = base + L.dHf;
-    c.out_row = nullptr;
-    e = launch_contract(p.dtype, c, p.r_max, P, stream);
-  } else if (multi) {
-    // per pair position (single dY rows), then summed per row
-    c.src_mode = kSrcPairList;
-    c.plist = plist;
-    c.ppos = ppos;
-    c.out_w = 0;
-    c.out_t = nullptr;
-    c.out_dense = nullptr;
-    c.out_row = base + L.dHrow;
-    e = launch_contract(p.dtype, c, p.r_max, P, stream);
-    if (e != hipSuccess) return e;
-    e = launch_combine_t<T>(p, base + L.dHrow, rpad, base + L.dHt, ldh, base + L.dHf, stream);
-  } else {
-    c.src_mode = kSrcPerPair;
-    c.out_w = 1;
-    c.out_t = base + L.dHt;
-    c.out_dense = p.per_pair ? nullptr : base + L.dHf;
-    c.out_row = p.per_pair ? base + L.dHrow : nullptr;
-    e = launch_contract(p.dtype, c, p.r_max, P, stream);
-  }
-  if (e != hipSuccess) return e;
   GradArgs gr{};
   gr.x = p.x;
   gr.dy = dy;
@@ -475,8 +442,90 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
   gr.d_out = p.d_out;
   gr.per_pair = p.per_pair;
   gr.keys = p.keys;
-  e = launch_grads(p.dtype, gr, p.r_max, P, stream);
-  if (e != hipSuccess) return e;
+  // Per-pair input at small ranks (bf16): the dB pass reads dY once and also
+  // contracts it against B^T per 128-column block (fp32 partials); dH per row
+  // is their sum, then the dA pass (x per pair from HBM).  Otherwise dH by a
+  // contraction over all of d_out before the weight gradients: per-block
+  // partials of more ranks would cost more than the second read of dY, and
+  // with shared input the dA items (x rows from the caches) run best mixed
+  // with the dB items (HBM-bound) in one launch.
+  if (p.dtype == ACE_BF16 && p.per_pair && p.r_max <= kFusedDhMaxRank) {
+    gr.phase = 1;
+    gr.dHp = reinterpret_cast<float*>(base + L.dHp);
+    gr.npos = P;
+    gr.dhs = dh_stride(p.r_max);
+    gr.Bt = base + L.Bt;
+    e = launch_grads(p.dtype, gr, p.r_max, P, stream);
+    if (e != hipSuccess) return e;
+    DhReduceArgs d{};
+    d.dHp = gr.dHp;
+    d.npos = P;
+    d.dhs = gr.dhs;
+    d.nbB = (p.d_out + kGradColBlk - 1) / kGradColBlk;
+    d.offsets = p.rt->offsets;
+    d.row_token = p.rt->row_token;
+    d.row_slots = p.rt->row_slots;
+    d.ppos = ppos;
+    d.plist = plist;
+    d.pair_w = p.pair_w;
+    d.k = p.k;
+    d.alpha = p.alpha;
+    d.dHt = base + L.dHt;
+    d.ldh = ldh;
+    d.dHrow = p.per_pair ? base + L.dHrow : nullptr;
+    d.rpad = rpad;
+    d.dHf = p.per_pair ? nullptr : base + L.dHf;
+    d.kslots = kslots;
+    d.keys = p.keys;
+    e = launch_dh_reduce(d, P, stream);
+    if (e != hipSuccess) return e;
+    gr.phase = 2;
+    e = launch_grads(p.dtype, gr, p.r_max, P, stream);
+    if (e != hipSuccess) return e;
+  } else {
+    // dH = s B^T G
+    c.W = base + L.Bt;
+    c.ldw = p.d_out;
+    c.K = p.d_out;
+    c.src = dy;
+    c.out_t_pairs = 0;
+    c.ppos = nullptr;
+    if (multi && p.dtype == ACE_BF16) {
+      // per pair position (single dY rows), summed per row in the epilogue
+      c.src_mode = kSrcPairList;
+      c.plist = plist;
+      c.ppos = ppos;
+      c.pair_row = p.rt->pair_row;
+      c.row_sum = 1;
+      c.out_w = 0;
+      c.out_t = base + L.dHt;
+      c.out_dense = base + L.dHf;
+      c.out_row = nullptr;
+      e = launch_contract(p.dtype, c, p.r_max, P, stream);
+    } else if (multi) {
+      // per pair position (single dY rows), then summed per row
+      c.src_mode = kSrcPairList;
+      c.plist = plist;
+      c.ppos = ppos;
+      c.out_w = 0;
+      c.out_t = nullptr;
+      c.out_dense = nullptr;
+      c.out_row = base + L.dHrow;
+      e = launch_contract(p.dtype, c, p.r_max, P, stream);
+      if (e != hipSuccess) return e;
+      e = launch_combine_t<T>(p, base + L.dHrow, rpad, base + L.dHt, ldh, base + L.dHf, stream);
+    } else {
+      c.src_mode = kSrcPerPair;
+      c.out_w = 1;
+      c.out_t = base + L.dHt;
+      c.out_dense = p.per_pair ? nullptr : base + L.dHf;
+      c.out_row = p.per_pair ? base + L.dHrow : nullptr;
+      e = launch_contract(p.dtype, c, p.r_max, P, stream);
+    }
+    if (e != hipSuccess) return e;
+    e = launch_grads(p.dtype, gr, p.r_max, P, stream);
+    if (e != hipSuccess) return e;
+  }
   if (p.per_pair) {
     // dx = A^T dH per pair, after the weight gradients: they read dY again,
     // which the contraction has just pulled through the caches, and dx's
