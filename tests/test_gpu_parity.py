@@ -365,6 +365,26 @@ def test_small_and_odd_ranks(dtype, r_e):
         check_rel("dB", f64(out["dB"]), dB, tol)
 
 
+@pytest.mark.parametrize("r_e", [4, 2])
+def test_per_pair_single_read_backward(r_e):
+    """Per-pair input at ranks <= 16 runs the backward whose dB pass also
+    forms dH from per-column-block partials: ragged column blocks (d_out = 296
+    gives blocks of 128, 128 and 40 columns), pair weights, expert keys at rank
+    r_e and group keys at rank 4 r_e (8 or 16 ranks per partial)."""
+    cfg = W.CONFIGS["olmoe_bf16"].scaled(T=301, d_model=296, d_ffn=104, r_e=r_e)
+    for path in ("down_expertwise", "pairs_per_pair"):
+        c = make_case(cfg, path, seed=10, with_w=True)
+        assert max(c.ranks) <= 16
+        say(f"single-read backward {path} r={max(c.ranks)} d_out={c.d_out}")
+        out = run_gpu(c, reuse_h=True)
+        tol = TOL["bf16"]
+        check_rel("delta", f64(out["y"]), oracle_fwd(c), tol)
+        dx, dA, dB = oracle_bwd(c)
+        check_rel("dx", f64(out["dx"]), dx, tol)
+        check_rel("dA", f64(out["dA"]), dA, tol)
+        check_rel("dB", f64(out["dB"]), dB, tol)
+
+
 def test_max_rank_and_many_groups():
     cfg = W.CONFIGS["olmoe_bf16"].scaled(T=150, d_model=128, d_ffn=64, r_e=64,
                                          groups=("consecutive", 4))
