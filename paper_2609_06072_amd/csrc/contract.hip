@@ -279,8 +279,11 @@ __global__ __launch_bounds__(kThreads) void contract_kernel(ContractArgs a) {
 // every row's sum (pairs in position order) is stored once.
 template <int RB>
 struct CDma {
-  static constexpr int KC = RB <= 4 ? 128 : 64;  // contraction indices per stage
-  static constexpr int NBUF = RB <= 4 ? 2 : 3;  // at most 4 (see the waits)
+  // contraction indices per stage and stages in LDS: ranks up to 32 take
+  // 128-column stages two deep (three blocks per CU); larger ranks, whose
+  // weight rows double the bytes of a stage, 64-column stages three deep
+  static constexpr int KC = RB <= 2 ? 128 : 64;
+  static constexpr int NBUF = RB <= 2 ? 2 : 3;  // at most 4 (see the waits)
   static constexpr int CPR = KC / 8;             // 16-byte chunks per row piece
   static constexpr int RPI = 64 / CPR;           // row pieces per copy instruction
   static constexpr int SBYTES = 64 * KC * 2;     // 64 source rows x KC bf16

@@ -18,6 +18,8 @@
 //     store.
 // Nothing is held in registers across the two phases, so many blocks fit on
 // a compute unit and their y loads overlap.
+#include <type_traits>
+
 #include "ace_device.hpp"
 #include "ace_internal.hpp"
 
@@ -38,6 +40,12 @@ __global__ __launch_bounds__(kThreads) void expand_kernel(ExpandArgs a) {
   constexpr int PPR = kChunk / PER;     // 16-byte pieces per pair per item
   constexpr int CST = kChunk + 16 / (int)sizeof(T);  // LDS row stride of C (elements)
   __shared__ __attribute__((aligned(16))) T Cs[kBM * CST];
+  // bf16 at 64 ranks or more: the tile's H rows are loaded once into LDS and
+  // every wave reads its fragments there (rows 16 bytes longer than the ranks,
+  // so the 16 rows of a fragment read spread over the banks)
+  constexpr bool HLDS = std::is_same<T, __bf16>::value && RB >= 4;
+  constexpr int HST = HLDS ? NM * KB + 8 : 8;   // LDS row stride of H (elements)
+  __shared__ __attribute__((aligned(16))) T Hs[HLDS ? kBM * HST : 8];
   __shared__ uint16_t plist[kBM * kMaxK];  // (row << 5) | slot
   __shared__ int toks[kBM];
   __shared__ int npairs_s;
@@ -74,16 +82,33 @@ __global__ __launch_bounds__(kThreads) void expand_kernel(ExpandArgs a) {
     if (lane == 63) npairs_s = incl;
   }
 
+  if constexpr (HLDS) {
+    // 64 rows x NM*KB ranks in 16-byte pieces (rows past the segment re-read
+    // the last row)
+    constexpr int PPRH = NM * KB / PER;
+#pragma unroll
+    for (int i = tid; i < kBM * PPRH; i += kThreads) {
+      const int rr = i / PPRH, pc = (i % PPRH) * PER;
+      const int u = min(u0 + rr, u_end - 1);
+      Tr<T>::store(&Hs[rr * HST + pc], Tr<T>::load(H + (size_t)u * a.rpad + pc));
+    }
+    __syncthreads();
+  }
   {
     // H fragments of the four row blocks (rows past the segment re-read the
     // last row; nothing is stored for them)
     F hf[4][NM];
 #pragma unroll
     for (int jb = 0; jb < 4; ++jb) {
-      const int u = min(u0 + 16 * jb + c16, u_end - 1);
-      const T* hr = H + (size_t)u * a.rpad + PER * g;
+      if constexpr (HLDS) {
 #pragma unroll
-      for (int m = 0; m < NM; ++m) hf[jb][m] = Tr<T>::load(hr + KB * m);
+        for (int m = 0; m < NM; ++m) hf[jb][m] = Tr<T>::load(&Hs[(16 * jb + c16) * HST + KB * m + PER * g]);
+      } else {
+        const int u = min(u0 + 16 * jb + c16, u_end - 1);
+        const T* hr = H + (size_t)u * a.rpad + PER * g;
+#pragma unroll
+        for (int m = 0; m < NM; ++m) hf[jb][m] = Tr<T>::load(hr + KB * m);
+      }
     }
     // W fragments of this wave's column blocks (rows past n_out re-read the
     // last row; rank columns past r_q meet zeros in H)
