@@ -36,14 +36,18 @@ namespace ace {
 namespace {
 
 constexpr int kColBlk = kGradColBlk;   // gradient columns per item
-constexpr int kSplitRows = 1024; // contraction indices per item (split-K chunk)
+// Contraction indices per item (split-K chunk): GradArgs::split, at least
+// kSplitRows (which bounds the item count and the partials) and at most
+// kMaxSplit (the LDS row-index table).
+constexpr int kSplitRows = 1024;
+constexpr int kMaxSplit = 2048;
 
 // Item table shared by the gradient kernels.  For key q the dB contraction
 // runs over bseg[q] .. bseg[q+1] and the dA contraction over aseg[q] ..
 // aseg[q+1]: pairs (positions in pair order; = rows when every row serves one
 // pair) and rows respectively, swapped in the pre-combined mode.  Items of q:
 // nsB(q) * nbB dB items, then nsA(q) * nbA dA items,
-// ns = max(1, ceil(count / kSplitRows)).
+// ns = max(1, ceil(count / split)).
 struct GradTable {
   int bseg[kMaxKeys + 1];
   int aseg[kMaxKeys + 1];
@@ -51,7 +55,7 @@ struct GradTable {
   int pstart[kMaxKeys + 1];   // first item of each key among the phase's items (phases 1, 2)
 };
 
-__device__ inline int n_split(int cnt) { return max(1, (cnt + kSplitRows - 1) / kSplitRows); }
+__device__ inline int n_split(int cnt, int split) { return max(1, (cnt + split - 1) / split); }
 
 // Item table for the reduce: [0, n_keys] first item of each key, then at
 // kItabStride the dB chunk counts, at 2 kItabStride the dA chunk counts.
@@ -70,8 +74,8 @@ __device__ inline void build_grad_table(const GradArgs& a, GradTable& tb, int* s
   __syncthreads();
   int items = 0, pitems = 0;
   if (t < n_keys) {
-    const int ib = n_split(tb.bseg[t + 1] - tb.bseg[t]) * a.nbB;
-    const int ia = n_split(tb.aseg[t + 1] - tb.aseg[t]) * a.nbA;
+    const int ib = n_split(tb.bseg[t + 1] - tb.bseg[t], a.split) * a.nbB;
+    const int ia = n_split(tb.aseg[t + 1] - tb.aseg[t], a.split) * a.nbA;
     items = ib + ia;
     pitems = a.phase == 1 ? ib : ia;
   }
@@ -88,8 +92,8 @@ __device__ inline void build_grad_table(const GradArgs& a, GradTable& tb, int* s
   }
   if (blockIdx.x == 0 && t < n_keys) {   // for the reduce launch
     a.itab[t] = ex;
-    a.itab[kItabStride + t] = n_split(tb.bseg[t + 1] - tb.bseg[t]);
-    a.itab[2 * kItabStride + t] = n_split(tb.aseg[t + 1] - tb.aseg[t]);
+    a.itab[kItabStride + t] = n_split(tb.bseg[t + 1] - tb.bseg[t], a.split);
+    a.itab[2 * kItabStride + t] = n_split(tb.aseg[t + 1] - tb.aseg[t], a.split);
   }
   __syncthreads();
 }
@@ -108,7 +112,7 @@ __device__ inline Item decode_item(const GradArgs& a, const GradTable& tb, int i
   it.q = upper_index(tb.istart, n_keys, item);
   int local = item - tb.istart[it.q];
   const int npB = tb.bseg[it.q + 1] - tb.bseg[it.q];
-  const int nsB = n_split(npB);
+  const int nsB = n_split(npB, a.split);
   it.isB = local < nsB * a.nbB;
   int cnt;
   if (it.isB) {
@@ -122,11 +126,11 @@ __device__ inline Item decode_item(const GradArgs& a, const GradTable& tb, int i
     it.s = local / a.nbA;
     it.cb = local % a.nbA;
     cnt = tb.aseg[it.q + 1] - tb.aseg[it.q];
-    it.ns = n_split(cnt);
+    it.ns = n_split(cnt, a.split);
     it.kbase = tb.aseg[it.q];
   }
-  it.k0 = it.s * kSplitRows;
-  it.nk = max(0, min(cnt - it.k0, kSplitRows));
+  it.k0 = it.s * a.split;
+  it.nk = max(0, min(cnt - it.k0, a.split));
   return it;
 }
 
@@ -136,7 +140,7 @@ __device__ inline int phase_item(const GradArgs& a, const GradTable& tb, int i) 
   const int q = upper_index(tb.pstart, a.keys.n_keys, i);
   const int local = i - tb.pstart[q];
   if (a.phase == 1) return tb.istart[q] + local;
-  return tb.istart[q] + n_split(tb.bseg[q + 1] - tb.bseg[q]) * a.nbB + local;
+  return tb.istart[q] + n_split(tb.bseg[q + 1] - tb.bseg[q], a.split) * a.nbB + local;
 }
 
 // Row of the large operand for contraction index kabs of an item.
@@ -150,11 +154,10 @@ __device__ inline int l_row(const GradArgs& a, bool isB, int kabs) {
   return a.per_pair ? tok * a.k + (__builtin_ctz(a.row_slots[kabs] | 0x80000000u) & 31) : tok;
 }
 
-// Loads the chunk's L row indices into idx[0 .. kSplitRows) (clamped to the
+// Loads the chunk's L row indices into idx[0 .. split) (clamped to the
 // chunk's last index; unused when the chunk is empty).
-__device__ inline void load_chunk_rows(const GradArgs& a, const Item& it, int* idx) {
-  if (it.nk <= 0) return;
-  constexpr int MPT = kSplitRows / kThreads;
+template <int MPT>
+__device__ inline void load_chunk_rows_n(const GradArgs& a, const Item& it, int* idx) {
   int v[MPT];
 #pragma unroll
   for (int i = 0; i < MPT; ++i) {
@@ -163,6 +166,12 @@ __device__ inline void load_chunk_rows(const GradArgs& a, const Item& it, int* i
   }
 #pragma unroll
   for (int i = 0; i < MPT; ++i) idx[threadIdx.x + i * kThreads] = v[i];
+}
+
+__device__ inline void load_chunk_rows(const GradArgs& a, const Item& it, int* idx) {
+  if (it.nk <= 0) return;
+  if (a.split > kSplitRows) load_chunk_rows_n<kMaxSplit / kThreads>(a, it, idx);
+  else load_chunk_rows_n<kSplitRows / kThreads>(a, it, idx);
 }
 
 // Writes one accumulator fragment of an item's gradient block: element v of
@@ -232,19 +241,18 @@ struct DmaGeo {
 // spreads the 16 rows that one transposed read touches over the banks.
 __device__ inline int l_swz(int r) { return 2 * ((r & 3) | (((r >> 3) & 1) << 2)); }
 
-template <int RB>
+template <int RB, int SPLIT>
 struct DmaSmem {
   __attribute__((aligned(16))) char L[DmaGeo<RB>::NBUF][DmaGeo<RB>::LBYTES];
   __attribute__((aligned(16))) char S[DmaGeo<RB>::NBUF][DmaGeo<RB>::SBYTES];
-  int idx[kSplitRows];
+  int idx[SPLIT];
   GradTable tb;
 };
 
-// Loads the chunk's L row indices into idx (clamped to the last index).
-template <bool ISB>
-__device__ inline void load_rows(const GradArgs& a, const Item& it, int* idx) {
-  if (it.nk <= 0) return;
-  constexpr int MPT = kSplitRows / kThreads;
+// Loads the chunk's L row indices into idx (clamped to the last index): MPT
+// per thread, all loads unconditional so that they are in flight together.
+template <bool ISB, int MPT>
+__device__ inline void load_rows_n(const GradArgs& a, const Item& it, int* idx) {
   int kabs[MPT], v[MPT];
 #pragma unroll
   for (int i = 0; i < MPT; ++i)
@@ -273,8 +281,14 @@ __device__ inline void load_rows(const GradArgs& a, const Item& it, int* idx) {
   for (int i = 0; i < MPT; ++i) idx[threadIdx.x + i * kThreads] = v[i];
 }
 
-template <int RB, bool ISB, bool DH>
-__device__ __forceinline__ void dma_item(const GradArgs& a, DmaSmem<RB>& sm, const Item& it,
+template <bool ISB, int SPLIT>
+__device__ inline void load_rows(const GradArgs& a, const Item& it, int* idx) {
+  if (it.nk <= 0) return;
+  load_rows_n<ISB, SPLIT / kThreads>(a, it, idx);
+}
+
+template <int RB, int SPLIT, bool ISB, bool DH>
+__device__ __forceinline__ void dma_item(const GradArgs& a, DmaSmem<RB, SPLIT>& sm, const Item& it,
                                          int item) {
   using G = DmaGeo<RB>;
   constexpr int RS = G::RS, NBUF = G::NBUF;
@@ -290,7 +304,7 @@ __device__ __forceinline__ void dma_item(const GradArgs& a, DmaSmem<RB>& sm, con
   const int nst = (it.nk + RS - 1) / RS;
 
   __syncthreads();  // the previous item is done with idx and the buffers
-  load_rows<ISB>(a, it, sm.idx);
+  load_rows<ISB, SPLIT>(a, it, sm.idx);
   __syncthreads();
 
   const int lrow_in = lane >> 4;   // row inside a 4-row copy
@@ -405,9 +419,10 @@ __device__ __forceinline__ void dma_item(const GradArgs& a, DmaSmem<RB>& sm, con
   finish_item<RB>(a, it, item, acc);
 }
 
-template <int RB>
+// SPLIT = a.split (contraction indices per item; sizes the row-index table)
+template <int RB, int SPLIT>
 __global__ __launch_bounds__(kThreads) void grad_dma_kernel(GradArgs a) {
-  __shared__ DmaSmem<RB> sm;
+  __shared__ DmaSmem<RB, SPLIT> sm;
   build_grad_table(a, sm.tb, sm.idx);
   const int n_keys = a.keys.n_keys;
   const int total = a.phase == 0 ? sm.tb.istart[n_keys] : sm.tb.pstart[n_keys];
@@ -415,10 +430,10 @@ __global__ __launch_bounds__(kThreads) void grad_dma_kernel(GradArgs a) {
     const int item = a.phase == 0 ? i : phase_item(a, sm.tb, i);
     const Item it = decode_item(a, sm.tb, item);
     if (it.isB) {
-      if (a.phase == 1) dma_item<RB, true, true>(a, sm, it, item);
-      else dma_item<RB, true, false>(a, sm, it, item);
+      if (a.phase == 1) dma_item<RB, SPLIT, true, true>(a, sm, it, item);
+      else dma_item<RB, SPLIT, true, false>(a, sm, it, item);
     } else {
-      dma_item<RB, false, false>(a, sm, it, item);
+      dma_item<RB, SPLIT, false, false>(a, sm, it, item);
     }
   }
 }
@@ -514,7 +529,7 @@ __global__ __launch_bounds__(kThreads) void grad_reg_kernel(GradArgs a) {
   constexpr int TI = NI / 8;
   constexpr int SLD = RPS + PER;              // LDS stride of a transposed column
   __shared__ __attribute__((aligned(16))) float Sl[kColBlk * SLD];
-  __shared__ int idx[kSplitRows];
+  __shared__ int idx[kMaxSplit];
   __shared__ GradTable tb;
   build_grad_table(a, tb, idx);
   const int total = tb.istart[a.keys.n_keys];
@@ -946,6 +961,8 @@ size_t partial_bytes(long P, int n_keys, long nb, int rb) {
 template <int RB>
 hipError_t launch_grads_rb(int dtype, GradArgs g, long P, hipStream_t stream) {
   if (g.phase != 0 && dtype != ACE_BF16) return hipErrorInvalidValue;
+  if (g.split == 0) g.split = kSplitRows;
+  if (g.split != kSplitRows && g.split != kMaxSplit) return hipErrorInvalidValue;
   const int nb = g.nbB + g.nbA;
   const long items = ((P + kSplitRows - 1) / kSplitRows + g.keys.n_keys) * nb;
   g.itab = reinterpret_cast<int32_t*>(static_cast<char*>(g.part) +
@@ -953,7 +970,10 @@ hipError_t launch_grads_rb(int dtype, GradArgs g, long P, hipStream_t stream) {
   const long cap = 8L * device_cu_count();
   const int grid = (int)(items < cap ? items : cap);
   if (grid > 0) {
-    if (dtype == ACE_BF16) grad_dma_kernel<RB><<<grid, kThreads, 0, stream>>>(g);
+    if (dtype == ACE_BF16) {
+      if (g.split == kMaxSplit) grad_dma_kernel<RB, kMaxSplit><<<grid, kThreads, 0, stream>>>(g);
+      else grad_dma_kernel<RB, kSplitRows><<<grid, kThreads, 0, stream>>>(g);
+    }
     else grad_reg_kernel<RB><<<grid, kThreads, 0, stream>>>(g);
   }
   hipError_t e = hipGetLastError();

@@ -442,6 +442,14 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
   gr.d_out = p.d_out;
   gr.per_pair = p.per_pair;
   gr.keys = p.keys;
+  // shared input at ranks up to 32 with long keys (bf16, at least 1024 pairs
+  // per key on average): 2048 contraction indices per item, so that most keys
+  // need no split reduction; otherwise 1024 (shorter keys balance better over
+  // more items, and higher ranks and the per-pair passes have more work per
+  // item)
+  const bool long_keys = (long)p.T * p.k >= 1024L * n_keys;
+  gr.split = (p.dtype == ACE_BF16 && !p.per_pair && rank_blocks(p.r_max) <= 2 && long_keys) ? 2048
+                                                                                            : 1024;
   // Per-pair input at small ranks (bf16): the dB pass reads dY once and also
   // contracts it against B^T per 128-column block (fp32 partials); dH per row
   // is their sum, then the dA pass (x per pair from HBM).  Otherwise dH by a
