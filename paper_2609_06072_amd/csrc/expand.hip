@@ -10,14 +10,17 @@
 // (a wave-level scan, no host sync); blocks past the last item exit at once.
 // Per item:
 //   - wave 0 lists the tile's (row, slot) pairs in LDS;
+//   - the threads issue the loads of the item's y pieces (16-byte pieces, 16
+//     consecutive threads per 256-byte row piece; up to kPrefetch per
+//     thread), which are in flight during the matrix work;
 //   - each wave multiplies its two 16-column blocks of W against the four
 //     16-row blocks of H on the matrix cores and writes C to LDS (in the
 //     output precision);
-//   - the threads then load every y piece of the item at once (16-byte
-//     pieces, 16 consecutive threads per 256-byte row piece), add w * C and
-//     store.
-// Nothing is held in registers across the two phases, so many blocks fit on
-// a compute unit and their y loads overlap.
+//   - the threads add w * C to their y pieces and store them (items with
+//     more pieces take further batches of loads).
+// The y pieces held across the matrix work cost a wave per SIMD of
+// occupancy (four instead of five at ranks up to 32) and save the latency of
+// a round trip to the memory per item.
 #include <type_traits>
 
 #include "ace_device.hpp"
@@ -81,6 +84,44 @@ __global__ __launch_bounds__(kThreads) void expand_kernel(ExpandArgs a) {
     for (uint32_t mm = sl; mm; mm &= mm - 1u) plist[e++] = (uint16_t)((lane << 5) | __builtin_ctz(mm));
     if (lane == 63) npairs_s = incl;
   }
+  __syncthreads();  // plist, toks published
+  const int nitems = npairs_s * PPR;
+  F yv[kPrefetch];
+  float wv[kPrefetch];
+  int po[kPrefetch], co[kPrefetch];
+  auto issue_batch = [&](int base) {
+#pragma unroll
+    for (int pf = 0; pf < kPrefetch; ++pf) {
+      if (base + pf * kThreads < nitems) {  // block-uniform
+        const int it = base + tid + pf * kThreads;
+        const bool ok = it < nitems;
+        const int e = (ok ? it : nitems - 1) / PPR;
+        const int pc = (it % PPR) * PER;
+        const int ent = plist[e];
+        const int p = toks[ent >> 5] * k + (ent & 31);
+        const bool cok = ok && n0 + pc < n_out;
+        po[pf] = cok ? p : -1;
+        co[pf] = (ent >> 5) * CST + pc;
+        yv[pf] = Tr<T>::load(O + (cok ? (size_t)p * n_out + n0 + pc : 0));  // clamped, unconditional
+        wv[pf] = a.pair_w ? a.pair_w[p] : 1.f;
+      }
+    }
+  };
+  auto finish_batch = [&](int base) {
+#pragma unroll
+    for (int pf = 0; pf < kPrefetch; ++pf) {
+      if (base + pf * kThreads < nitems && po[pf] >= 0) {
+        float o[PER], cv[PER];
+        Tr<T>::to_f32(yv[pf], o);
+        Tr<T>::to_f32(*reinterpret_cast<const F*>(&Cs[co[pf]]), cv);
+#pragma unroll
+        for (int e2 = 0; e2 < PER; ++e2) o[e2] += wv[pf] * cv[e2];
+        const int pc = ((base + tid + pf * kThreads) % PPR) * PER;
+        Tr<T>::store(O + (size_t)po[pf] * n_out + n0 + pc, Tr<T>::from_f32(o));
+      }
+    }
+  };
+  issue_batch(0);   // in flight during the matrix work
 
   if constexpr (HLDS) {
     // 64 rows x NM*KB ranks in 16-byte pieces (rows past the segment re-read
@@ -148,41 +189,11 @@ __global__ __launch_bounds__(kThreads) void expand_kernel(ExpandArgs a) {
       }
     }
   }
-  __syncthreads();  // plist, toks and C are published
-  const int nitems = npairs_s * PPR;
-
-  for (int base = 0; base < nitems; base += kPrefetch * kThreads) {
-    F yv[kPrefetch];
-    float wv[kPrefetch];
-    int po[kPrefetch], co[kPrefetch];
-#pragma unroll
-    for (int pf = 0; pf < kPrefetch; ++pf) {
-      if (base + pf * kThreads < nitems) {  // block-uniform
-        const int it = base + tid + pf * kThreads;
-        const bool ok = it < nitems;
-        const int e = (ok ? it : nitems - 1) / PPR;
-        const int pc = (it % PPR) * PER;
-        const int ent = plist[e];
-        const int p = toks[ent >> 5] * k + (ent & 31);
-        const bool cok = ok && n0 + pc < n_out;
-        po[pf] = cok ? p : -1;
-        co[pf] = (ent >> 5) * CST + pc;
-        yv[pf] = Tr<T>::load(O + (cok ? (size_t)p * n_out + n0 + pc : 0));  // clamped, unconditional
-        wv[pf] = a.pair_w ? a.pair_w[p] : 1.f;
-      }
-    }
-#pragma unroll
-    for (int pf = 0; pf < kPrefetch; ++pf) {
-      if (base + pf * kThreads < nitems && po[pf] >= 0) {
-        float o[PER], cv[PER];
-        Tr<T>::to_f32(yv[pf], o);
-        Tr<T>::to_f32(*reinterpret_cast<const F*>(&Cs[co[pf]]), cv);
-#pragma unroll
-        for (int e2 = 0; e2 < PER; ++e2) o[e2] += wv[pf] * cv[e2];
-        const int pc = ((base + tid + pf * kThreads) % PPR) * PER;
-        Tr<T>::store(O + (size_t)po[pf] * n_out + n0 + pc, Tr<T>::from_f32(o));
-      }
-    }
+  __syncthreads();  // C is published
+  finish_batch(0);
+  for (int base = kPrefetch * kThreads; base < nitems; base += kPrefetch * kThreads) {
+    issue_batch(base);
+    finish_batch(base);
   }
 }
 
