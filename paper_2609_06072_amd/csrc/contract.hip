@@ -493,10 +493,12 @@ __global__ __launch_bounds__(kThreads) void contract_dma_kernel(ContractArgs a) 
         const int chunk = kb * 4 + g;
         const int rl = 16 * wave + c16;
         bf16x8 sf = *reinterpret_cast<const bf16x8*>(&Sb[b][rl * KC * 2 + ((chunk ^ (rl & (CPR - 1))) << 4)]);
-        const int nv = K - (kk + 8 * g);
+        if (kk + KB > K) {   // block-uniform: only a ragged last K-block is masked
+          const int nv = K - (kk + 8 * g);
 #pragma unroll
-        for (int e = 0; e < 8; ++e)
-          if (e >= nv) sf[e] = (__bf16)0.f;
+          for (int e = 0; e < 8; ++e)
+            if (e >= nv) sf[e] = (__bf16)0.f;
+        }
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) {
           // weight rows at or past r_q were not copied: their results are zeroed below

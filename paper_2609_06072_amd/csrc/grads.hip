@@ -368,15 +368,18 @@ __device__ __forceinline__ void dma_item(const GradArgs& a, DmaSmem<RB, SPLIT>& 
       const int kk = st * RS + kb * 32;   // chunk-relative index of the K-block
       if (kk >= it.nk) break;
       const int nv = it.nk - (kk + 8 * g);
+      const bool ragged = kk + 32 > it.nk;   // block-uniform: only the item's last K-block
       bf16x8 sf[RB];
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
         const int rr = 16 * rb + c16;
         const int pos = (kb * 4 + g) ^ (rr & 7);
         bf16x8 f = *reinterpret_cast<const bf16x8*>(&sm.S[b][rr * RS * 2 + pos * 16]);
+        if (ragged) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e)
-          if (e >= nv) f[e] = (__bf16)0.f;
+          for (int e = 0; e < 8; ++e)
+            if (e >= nv) f[e] = (__bf16)0.f;
+        }
         sf[rb] = f;
       }
 #pragma unroll
@@ -888,15 +891,17 @@ __global__ __launch_bounds__(kThreads) void dx_dma_kernel(DxArgs a) {
     const char* Hs = smem + (st % kDxNbuf) * kDxStage;
     const char* As = Hs + kDxHBytes;
     const int kk = st * kDxKC;
-    const int nv = KR - (kk + 8 * g);
+    // KR is a multiple of 8, so a lane's 8 contraction indices are all below
+    // KR or all past it (those copies re-read the last valid chunk and are
+    // zeroed here); only a ragged last stage has such lanes
+    const bool ragged = kk + kDxKC > KR;   // block-uniform
+    const bool past = kk + 8 * g >= KR;
     bf16x8 hf[4];
 #pragma unroll
     for (int tb = 0; tb < 4; ++tb) {
       const int rl = 64 * wy + 16 * tb + c16;
       bf16x8 f = *reinterpret_cast<const bf16x8*>(Hs + rl * kDxKC * 2 + ((g ^ ((rl >> 2) & 3)) << 4));
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-        if (e >= nv) f[e] = (__bf16)0.f;
+      if (ragged && past) f = bf16x8{};
       hf[tb] = f;
     }
 #pragma unroll
