@@ -229,7 +229,10 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 template <int RB>
 struct DmaGeo {
   static constexpr int RS = 64;                     // contraction indices per stage
-  static constexpr int NBUF = RB <= 2 ? 3 : 2;      // stages in LDS
+  // stages in LDS: two (one in flight while the other is contracted); the
+  // smaller footprint fits more blocks per CU, which hides more of the gather
+  // latency than a third stage per block did
+  static constexpr int NBUF = 2;
   static constexpr int LBYTES = RS * 256;           // 64 rows x 128 bf16
   static constexpr int SROWS = 16 * RB;             // rank rows of the S slice
   static constexpr int SBYTES = SROWS * RS * 2;     // rank rows x 64 bf16
