@@ -63,6 +63,13 @@ struct Tr<float> {
   __device__ static inline frag zero() { return frag{0.f, 0.f, 0.f, 0.f}; }
   __device__ static inline frag load(const float* p) { return *reinterpret_cast<const f32x4*>(p); }
   __device__ static inline void store(float* p, frag v) { *reinterpret_cast<f32x4*>(p) = v; }
+  // streaming (non-temporal) variants for data touched once per call
+  __device__ static inline frag load_nt(const float* p) {
+    return __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
+  }
+  __device__ static inline void store_nt(float* p, frag v) {
+    __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(p));
+  }
   __device__ static inline f32x4 lo4(frag f) { return f; }
   __device__ static inline void to_f32(frag f, float* v) {
     v[0] = f[0]; v[1] = f[1]; v[2] = f[2]; v[3] = f[3];
@@ -90,6 +97,13 @@ struct Tr<__bf16> {
   }
   __device__ static inline void store(__bf16* p, frag v) {
     *reinterpret_cast<u32x4*>(p) = __builtin_bit_cast(u32x4, v);
+  }
+  // streaming (non-temporal) variants for data touched once per call
+  __device__ static inline frag load_nt(const __bf16* p) {
+    return __builtin_bit_cast(frag, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p)));
+  }
+  __device__ static inline void store_nt(__bf16* p, frag v) {
+    __builtin_nontemporal_store(__builtin_bit_cast(u32x4, v), reinterpret_cast<u32x4*>(p));
   }
   __device__ static inline void to_f32(frag f, float* v) {
 #pragma unroll
@@ -273,6 +287,10 @@ __device__ inline uint32_t lds_addr(const void* p) {
 // explicitly with wait_vmcnt before the barrier that publishes the data.
 __device__ inline void dma16(const void* g, uint32_t lds_base) {
   asm volatile("global_load_lds_dwordx4 %1, off" ::"{m0}"(lds_base), "v"(g) : "memory");
+}
+// The same copy with the non-temporal policy (data read once per call).
+__device__ inline void dma16_nt(const void* g, uint32_t lds_base) {
+  asm volatile("global_load_lds_dwordx4 %1, off nt" ::"{m0}"(lds_base), "v"(g) : "memory");
 }
 
 // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:

@@ -20,7 +20,9 @@
 //     more pieces take further batches of loads).
 // The y pieces held across the matrix work cost a wave per SIMD of
 // occupancy (four instead of five at ranks up to 32) and save the latency of
-// a round trip to the memory per item.
+// a round trip to the memory per item.  y is read and written once per call,
+// with non-temporal loads and stores, so that it does not displace from the
+// caches what the next launches read.
 #include <type_traits>
 
 #include "ace_device.hpp"
@@ -102,7 +104,7 @@ __global__ __launch_bounds__(kThreads) void expand_kernel(ExpandArgs a) {
         const bool cok = ok && n0 + pc < n_out;
         po[pf] = cok ? p : -1;
         co[pf] = (ent >> 5) * CST + pc;
-        yv[pf] = Tr<T>::load(O + (cok ? (size_t)p * n_out + n0 + pc : 0));  // clamped, unconditional
+        yv[pf] = Tr<T>::load_nt(O + (cok ? (size_t)p * n_out + n0 + pc : 0));  // clamped, unconditional
         wv[pf] = a.pair_w ? a.pair_w[p] : 1.f;
       }
     }
@@ -117,7 +119,7 @@ __global__ __launch_bounds__(kThreads) void expand_kernel(ExpandArgs a) {
 #pragma unroll
         for (int e2 = 0; e2 < PER; ++e2) o[e2] += wv[pf] * cv[e2];
         const int pc = ((base + tid + pf * kThreads) % PPR) * PER;
-        Tr<T>::store(O + (size_t)po[pf] * n_out + n0 + pc, Tr<T>::from_f32(o));
+        Tr<T>::store_nt(O + (size_t)po[pf] * n_out + n0 + pc, Tr<T>::from_f32(o));
       }
     }
   };

@@ -314,6 +314,10 @@ __device__ __forceinline__ void dma_item(const GradArgs& a, DmaSmem<RB, SPLIT>& 
   const int lpos = lane & 15;      // 16-byte position in the LDS row
   const int srow_in = lane >> 3;   // rank row inside an 8-row copy
   const int spos = lane & 7;
+  // rows that this launch reads for the last time are copied with the
+  // non-temporal policy: dY (its other reader, the dH contraction, runs
+  // before) and per-pair x; shared x rows are gathered again by other keys
+  const bool l_last = ISB || a.per_pair;   // block-uniform
   auto issue = [&](int st) {
     const int b = st % NBUF;
 #pragma unroll
@@ -323,8 +327,9 @@ __device__ __forceinline__ void dma_item(const GradArgs& a, DmaSmem<RB, SPLIT>& 
       const int row = sm.idx[min(st * RS + r, it.nk - 1)];
       const int c = lpos ^ l_swz(r);                    // chunk this lane copies
       const int col = min(col0 + 8 * c, ldl - 8);
-      dma16(L + (size_t)row * ldl + col,
-            __builtin_amdgcn_readfirstlane(lds_addr(&sm.L[b][r0 * 256])));
+      const uint32_t ldst = __builtin_amdgcn_readfirstlane(lds_addr(&sm.L[b][r0 * 256]));
+      if (l_last) dma16_nt(L + (size_t)row * ldl + col, ldst);
+      else dma16(L + (size_t)row * ldl + col, ldst);
     }
 #pragma unroll
     for (int i = 0; i < G::NS; ++i) {
