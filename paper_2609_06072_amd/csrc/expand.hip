@@ -18,9 +18,10 @@
 //     output precision);
 //   - the threads add w * C to their y pieces and store them (items with
 //     more pieces take further batches of loads).
-// The y pieces held across the matrix work cost a wave per SIMD of
-// occupancy (four instead of five at ranks up to 32) and save the latency of
-// a round trip to the memory per item.  y is read and written once per call,
+// The y pieces held across the matrix work cost occupancy and save the
+// latency of a round trip to the memory per item (six pieces per thread
+// measured best: 64-pair items of a 128-column chunk need four, rows that
+// serve several slots more).  y is read and written once per call,
 // with non-temporal loads and stores, so that it does not displace from the
 // caches what the next launches read.
 #include <type_traits>
@@ -34,7 +35,7 @@ namespace {
 
 constexpr int kBM = 64;                 // rows per tile
 constexpr int kChunk = 128;             // output columns per item
-constexpr int kPrefetch = 8;            // y pieces per thread in flight
+constexpr int kPrefetch = 6;            // y pieces per thread in flight
 constexpr int kBPW = kChunk / 16 / 4;   // 16-column blocks per wave
 
 template <typename T, int RB>
