@@ -122,7 +122,7 @@ typedef struct ace_routing {
   int32_t* row_token;  /* device [P]         token of each row (entries >= U unused)*/
   uint32_t* row_slots; /* device [P]         slot mask of each row                  */
   int32_t* pair_row;   /* device [P]         row that serves pair t*k+j, -1 if dropped */
-  int32_t* n_dropped;  /* device [1]         pairs dropped for an id out of range   */
+  int32_t* n_dropped;  /* device [1]         pairs dropped (id out of range or repeated) */
   int32_t* row_pair;   /* device [P+1]       position of row u's first pair in pair
                                              order (key, token, slot); [U] = number
                                              of routed pairs                          */
@@ -136,7 +136,10 @@ typedef struct ace_routing {
  * Route expansion and permutation (Sec. 3.5, the active group set A(x)).
  *   topk_ids        device int32 [T, k]: routed expert of slot j of token t.
  *                   An id outside [0, E), or whose group is outside [0, G),
- *                   drops the pair (counted in rt->n_dropped).
+ *                   drops the pair (counted in rt->n_dropped).  The routed
+ *                   experts of a token are a set (Sec. 3.1): an id equal to
+ *                   one at a lower slot of the same token drops the pair too
+ *                   (counted likewise), in every mode.
  *   expert_to_group device int32 [E]: g(e); may be NULL iff mode == ACE_ROWS_EXPERT.
  *   mode            row mode; n_keys = G for the group modes, E for ACE_ROWS_EXPERT.
  *   ws, ws_bytes    device scratch, at least
@@ -364,14 +367,18 @@ ace_status ace_group_anchors(const float* S, int32_t E, const int32_t* expert_to
  *             anchor one of its members).
  *   A_init    device [(E - G) * rank, d_in], dtype; may be NULL when G == E.
  *   A_g, B_g  device, packed layout above with G keys of ranks r_g (the
- *             group blocks in group order), dtype: overwritten.
+ *             group blocks in group order), dtype: overwritten.  Their total
+ *             rank is E * rank (the budget is unchanged).
+ *   group_rank host int32 [G] (out) or NULL: r_g of every group, the ranks
+ *             to pass to the grouped calls with A_g, B_g.
  * Asynchronous on `stream`; A_g and B_g must not overlap the inputs.
+ * group_rank is written before the call returns.
  */
 ace_status ace_consolidate_adapters(ace_dtype dtype, int32_t d_in, int32_t d_out, int32_t E,
                                     int32_t rank, const void* A, const void* B,
                                     const int32_t* expert_to_group, int32_t G,
                                     const int32_t* anchors, const void* A_init, void* A_g,
-                                    void* B_g, void* stream);
+                                    void* B_g, int32_t* group_rank, void* stream);
 
 /*
  * Device scratch needed by an op (bytes, rounded up to 256).  n_keys and

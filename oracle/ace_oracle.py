@@ -35,7 +35,9 @@ Readings where the paper is silent (each is restated in the design notes):
   * Backward is the derivative of L = <dY, Y_out>.  Y and dx accumulate,
     dA and dB are returned whole.
   * Row order of the permutation: by key, then token, then slot (ascending).
-  * Routed ids outside [0, E) (and group ids outside [0, G)) drop the pair.
+  * Routed ids outside [0, E) (and group ids outside [0, G)) drop the pair;
+    so does an id that repeats one at a lower slot of the same token (R(x)
+    is a set of experts).
 
 Parameter layout (shared with the C-ABI, a convention of this project):
   A: [R, d_in], key q's block is rows roff_q .. roff_q + r_q  (A_q).
@@ -61,16 +63,25 @@ INPUT_COMBINED = 2   # per-pair input, output combined per token: [T, d_out]
 # grouped execution (Sec. 3.5)
 # ---------------------------------------------------------------------------
 
+def repeated_id(topk_ids, t: int, j: int) -> bool:
+    """True when slot j of token t repeats an expert id listed at a lower
+    slot of the same token.  The routed experts R(x) of Sec. 3.1 are a set,
+    so such a pair is not part of the routing and is dropped."""
+    e = int(topk_ids[t][j])
+    return any(int(topk_ids[t][jj]) == e for jj in range(j))
+
+
 def pair_keys(topk_ids: np.ndarray, E: int, expert_to_group: Optional[np.ndarray],
               G: int) -> np.ndarray:
     """Adapter key of every routed pair: g(e) for group keys, e itself for
-    expert keys (expert_to_group None).  -1 marks a dropped pair."""
+    expert keys (expert_to_group None).  -1 marks a dropped pair (an id out
+    of range, a group out of range, or an id repeated within the token)."""
     T, k = topk_ids.shape
     keys = np.full((T, k), -1, dtype=np.int64)
     for t in range(T):
         for j in range(k):
             e = int(topk_ids[t, j])
-            if not 0 <= e < E:
+            if not 0 <= e < E or repeated_id(topk_ids, t, j):
                 continue
             if expert_to_group is None:
                 keys[t, j] = e
@@ -317,12 +328,16 @@ def precombined_delta(x, A, B, ranks, alpha, topk_ids, E, expert_to_group, G,
 def expert_projection(x, W, topk_ids, E, input_mode=INPUT_SHARED) -> np.ndarray:
     """Y[t*k + j] = W_e xin(t, j) with e = topk_ids[t, j] and W [E, d_out, d_in]
     (the frozen per-expert projection of Sec. 3.1).  Rows of dropped pairs
-    (id outside [0, E)) are zero.  Returns fp64 [T*k, d_out]."""
+    (id outside [0, E) or repeated within the token) are zero.  Returns fp64 [T*k, d_out]."""
     x = np.asarray(x, dtype=np.float64)
     W = np.asarray(W, dtype=np.float64)
     T, k = topk_ids.shape
     out = np.zeros((T * k, W.shape[1]))
-    ids = np.asarray(topk_ids).reshape(-1)
+    ids = np.asarray(topk_ids).astype(np.int64).reshape(-1).copy()
+    for t in range(T):
+        for j in range(k):
+            if repeated_id(topk_ids, t, j):
+                ids[t * k + j] = -1
     for e in range(E):
         pairs = np.nonzero(ids == e)[0]
         if pairs.size:
@@ -360,7 +375,7 @@ def brute_delta(x, A, B, ranks, alpha, topk_ids, E, expert_to_group, G,
     for t in range(T):
         for j in range(k):
             e = int(topk_ids[t][j])
-            if not 0 <= e < E:
+            if not 0 <= e < E or repeated_id(topk_ids, t, j):
                 continue
             q = e if expert_to_group is None else int(expert_to_group[e])
             if not 0 <= q < len(ranks):
@@ -396,7 +411,7 @@ def brute_adapted_projection(x, W, A, B, ranks, alpha, topk_ids, E, expert_to_gr
     for t in range(T):
         for j in range(k):
             e = int(topk_ids[t][j])
-            if not 0 <= e < E:
+            if not 0 <= e < E or repeated_id(topk_ids, t, j):
                 continue
             q = e if expert_to_group is None else int(expert_to_group[e])
             r = int(ranks[q])
@@ -428,7 +443,7 @@ def brute_grads(x, A, B, ranks, alpha, topk_ids, E, expert_to_group, G, dy,
     for t in range(T):
         for j in range(k):
             e = int(topk_ids[t][j])
-            if not 0 <= e < E:
+            if not 0 <= e < E or repeated_id(topk_ids, t, j):
                 continue
             q = e if expert_to_group is None else int(expert_to_group[e])
             if not 0 <= q < len(ranks):

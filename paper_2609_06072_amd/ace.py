@@ -78,7 +78,7 @@ _lib.ace_louvain.restype = _i32
 _lib.ace_group_anchors.argtypes = [_vp, _i32, _vp, _i32, _vp]
 _lib.ace_group_anchors.restype = _i32
 _lib.ace_consolidate_adapters.argtypes = [_i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _i32, _vp,
-                                          _vp, _vp, _vp, _vp]
+                                          _vp, _vp, _vp, _vp, _vp]
 _lib.ace_consolidate_adapters.restype = _i32
 _lib.ace_moe_lora_fwd.argtypes = [_i32, _i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _R, _i32, _vp,
                                   _vp, _f32, _vp, _vp, _R, _vp, _vp, _sz, _vp]
@@ -124,6 +124,46 @@ def _dtype(t: torch.Tensor) -> int:
     raise TypeError(f"unsupported dtype {t.dtype}")
 
 
+def _want(name: str, t, numel: Optional[int] = None, dtype=None, device=None,
+          optional: bool = False) -> None:
+    """Host-side shape/type check of one argument before the call (the
+    library sees only pointers): numel, dtype and device must match."""
+    if t is None:
+        if optional:
+            return
+        raise ValueError(f"{name} is required")
+    if numel is not None and t.numel() != numel:
+        raise ValueError(f"{name} has {t.numel()} elements, expected {numel}")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+
+
+def _check_lora_args(x, A, B, ranks: Sequence[int], routing: "Routing", d_out: int,
+                     input_mode: int, pair_w, y=None, dy=None, dx=None, dA=None, dB=None) -> None:
+    T, k = routing.c.T, routing.c.k
+    R = int(sum(int(r) for r in ranks))
+    dt, dev = A.dtype, A.device
+    if A.dim() != 2 or A.shape[0] != R:
+        raise ValueError(f"A must be [R={R}, d_in], got {tuple(A.shape)}")
+    d_in = A.shape[1]
+    rows_in = T if input_mode == ACE_INPUT_SHARED else T * k
+    rows_out = T if input_mode == ACE_INPUT_COMBINED else T * k
+    _want("x", x, rows_in * d_in, dt, dev)
+    _want("B", B, R * d_out, dt, dev)
+    _want("pair_w", pair_w, T * k, torch.float32, dev, optional=True)
+    if y is not None:
+        _want("y", y, rows_out * d_out, dt, dev)
+    if dy is not None:
+        _want("dy", dy, rows_out * d_out, dt, dev)
+        _want("dx", dx, rows_in * d_in, dt, dev)
+        _want("dA", dA, R * d_in, torch.float32, dev)
+        _want("dB", dB, R * d_out, torch.float32, dev)
+    if routing.n_keys != len(ranks):
+        raise ValueError(f"routing has {routing.n_keys} keys, the call has {len(ranks)}")
+
+
 def ace_workspace_bytes(op: int, T: int, k: int, d_in: int, d_out: int, n_keys: int,
                         r_max: int) -> int:
     n = _lib.ace_workspace_bytes(op, T, k, d_in, d_out, n_keys, r_max)
@@ -151,6 +191,14 @@ class Routing:
                             self.pair_row.data_ptr(), self.n_dropped.data_ptr(),
                             self.row_pair.data_ptr(), self.pair_list.data_ptr(), n_keys, -1, T, k)
 
+    def check_capacity(self, T: int, k: int, n_keys: int) -> None:
+        """The arrays must hold a permutation of T*k pairs over n_keys keys."""
+        P = max(1, T * k)
+        if self.row_token.numel() < P or self.row_pair.numel() < P + 1:
+            raise ValueError(f"routing holds {self.row_token.numel()} pairs, the call needs {P}")
+        if self.counts.numel() != n_keys:
+            raise ValueError(f"routing has room for {self.counts.numel()} keys, the call has {n_keys}")
+
     @property
     def n_keys(self) -> int:
         return self.c.n_keys
@@ -165,8 +213,11 @@ def ace_group_permute(topk_ids: torch.Tensor, E: int, expert_to_group: Optional[
                       ws: Optional[torch.Tensor] = None, stream=None) -> Routing:
     T, k = topk_ids.shape
     n_keys = E if mode == ACE_ROWS_EXPERT else G
+    _want("topk_ids", topk_ids, dtype=torch.int32)
+    _want("expert_to_group", expert_to_group, E, torch.int32, topk_ids.device, optional=True)
     if routing is None:
         routing = Routing(T, k, n_keys, device=topk_ids.device)
+    routing.check_capacity(T, k, n_keys)
     need = ace_workspace_bytes(ACE_OP_PERMUTE, T, k, 0, 0, n_keys, 0)
     if ws is None:
         ws = torch.empty(max(need, 256), dtype=torch.uint8, device=topk_ids.device)
@@ -183,10 +234,14 @@ def ace_group_expert_permute(topk_ids: torch.Tensor, E: int, expert_to_group: to
                              ws: Optional[torch.Tensor] = None, stream=None):
     """Group-keyed and expert-keyed routings from one pass over topk_ids."""
     T, k = topk_ids.shape
+    _want("topk_ids", topk_ids, dtype=torch.int32)
+    _want("expert_to_group", expert_to_group, E, torch.int32, topk_ids.device)
     if group_routing is None:
         group_routing = Routing(T, k, G, device=topk_ids.device)
     if expert_routing is None:
         expert_routing = Routing(T, k, E, device=topk_ids.device)
+    group_routing.check_capacity(T, k, G)
+    expert_routing.check_capacity(T, k, E)
     need = (ace_workspace_bytes(ACE_OP_PERMUTE, T, k, 0, 0, G, 0)
             + ace_workspace_bytes(ACE_OP_PERMUTE, T, k, 0, 0, E, 0))
     if ws is None:
@@ -223,6 +278,7 @@ def ace_grouped_lora_fwd(x, A, B, group_rank: Sequence[int], alpha: float, routi
                          stream=None) -> None:
     T, k = routing.c.T, routing.c.k
     d_in, d_out = A.shape[1], y.shape[1]
+    _check_lora_args(x, A, B, group_rank, routing, d_out, input_mode, pair_w, y=y)
     ranks = _ranks_arg(group_rank)
     ws = _fwd_ws(ws, T, k, d_in, d_out, len(group_rank), max(group_rank), A.device)
     _check(_lib.ace_grouped_lora_fwd(_dtype(x), input_mode, T, k, d_in, d_out, len(group_rank),
@@ -239,6 +295,8 @@ def ace_grouped_lora_bwd(x, A, B, group_rank: Sequence[int], alpha: float, routi
     (the backward then reuses the forward's h instead of recomputing it)."""
     T, k = routing.c.T, routing.c.k
     d_in, d_out = A.shape[1], dy.shape[1]
+    _check_lora_args(x, A, B, group_rank, routing, d_out, input_mode, pair_w, dy=dy, dx=dx,
+                     dA=dA, dB=dB)
     ranks = _ranks_arg(group_rank)
     if ws is None:
         need = ace_workspace_bytes(ACE_OP_BWD, T, k, d_in, d_out, len(group_rank), max(group_rank))
@@ -255,6 +313,7 @@ def ace_expertwise_lora_fwd(x, A, B, E: int, rank: int, alpha: float, routing: R
                             stream=None) -> None:
     T, k = routing.c.T, routing.c.k
     d_in, d_out = A.shape[1], y.shape[1]
+    _check_lora_args(x, A, B, [rank] * E, routing, d_out, input_mode, pair_w, y=y)
     ws = _fwd_ws(ws, T, k, d_in, d_out, E, rank, A.device)
     _check(_lib.ace_expertwise_lora_fwd(_dtype(x), input_mode, T, k, d_in, d_out, E, rank, alpha,
                                         _ptr(x), _ptr(A), _ptr(B), _ptr(pair_w),
@@ -268,6 +327,8 @@ def ace_expertwise_lora_bwd(x, A, B, E: int, rank: int, alpha: float, routing: R
                             stream=None, h_fwd=None) -> None:
     T, k = routing.c.T, routing.c.k
     d_in, d_out = A.shape[1], dy.shape[1]
+    _check_lora_args(x, A, B, [rank] * E, routing, d_out, input_mode, pair_w, dy=dy, dx=dx,
+                     dA=dA, dB=dB)
     if ws is None:
         need = ace_workspace_bytes(ACE_OP_BWD, T, k, d_in, d_out, E, rank)
         ws = torch.empty(max(need, 256), dtype=torch.uint8, device=A.device)
@@ -335,23 +396,28 @@ def ace_group_anchors(S, expert_to_group, G: int):
 
 def ace_consolidate_adapters(A, B, E: int, rank: int, expert_to_group, G: int, anchors, A_init,
                              A_g=None, B_g=None, stream=None):
-    """Group adapters (A_g, B_g, ranks) from the expert adapters A, B (device)."""
+    """Group adapters (A_g, B_g, group ranks) from the expert adapters A, B
+    (device); the library returns the group ranks.  A_g, B_g hold E * rank
+    ranks in total (the unchanged budget)."""
     import numpy as np
     e2g = _host(expert_to_group, np.int32)
     anc = _host(anchors, np.int32)
-    ranks = [int(np.sum(e2g == g)) * rank for g in range(G)]
-    R = sum(ranks)
     d_in = A.shape[1]
     d_out = B.numel() // (E * rank)
     if A_g is None:
-        A_g = torch.empty(R, d_in, dtype=A.dtype, device=A.device)
+        A_g = torch.empty(E * rank, d_in, dtype=A.dtype, device=A.device)
     if B_g is None:
-        B_g = torch.empty(R * d_out, dtype=B.dtype, device=B.device)
+        B_g = torch.empty(E * rank * d_out, dtype=B.dtype, device=B.device)
+    for t, n in ((A_g, E * rank * d_in), (B_g, E * rank * d_out)):
+        if t.numel() != n or t.dtype != A.dtype or t.device != A.device:
+            raise ValueError("A_g / B_g must hold E * rank ranks in A's dtype and device")
+    ranks = np.zeros(G, dtype=np.int32)
     _check(_lib.ace_consolidate_adapters(_dtype(A), d_in, d_out, E, rank, _ptr(A), _ptr(B),
                                          e2g.ctypes.data, G, anc.ctypes.data, _ptr(A_init),
-                                         _ptr(A_g), _ptr(B_g), _stream(stream)),
+                                         _ptr(A_g), _ptr(B_g), ranks.ctypes.data,
+                                         _stream(stream)),
            "ace_consolidate_adapters")
-    return A_g, B_g, ranks
+    return A_g, B_g, [int(r) for r in ranks]
 
 
 def raw_lib() -> ctypes.CDLL:

@@ -64,8 +64,10 @@ ace_status check_problem(Problem& p, ace_dtype dtype, ace_input_mode im, int32_t
   if (!expertwise && !ranks) return fail(ACE_ERR_INVALID_ARG, "group_rank is NULL");
   if (!std::isfinite(alpha)) return fail(ACE_ERR_INVALID_ARG, "alpha is not finite");
   if (!rt) return fail(ACE_ERR_INVALID_ARG, "routing is NULL");
-  if (!rt->offsets || !rt->counts) return fail(ACE_ERR_INVALID_ARG, "routing arrays are NULL");
-  if (T > 0 && (!rt->row_token || !rt->row_slots || !rt->row_pair || !rt->pair_list))
+  // row_pair has P + 1 entries: its last one (the pair count) exists at T = 0 too
+  if (!rt->offsets || !rt->counts || !rt->row_pair)
+    return fail(ACE_ERR_INVALID_ARG, "routing arrays are NULL");
+  if (T > 0 && (!rt->row_token || !rt->row_slots || !rt->pair_list))
     return fail(ACE_ERR_INVALID_ARG, "routing arrays are NULL");
   if (rt->T != T || rt->k != k)
     return fail(ACE_ERR_INVALID_ARG, "routing was built for T=%d k=%d, call has T=%d k=%d", rt->T,
@@ -280,10 +282,11 @@ ace_status ace_group_permute(const int32_t* topk_ids, int32_t T, int32_t k, int3
     n_keys = G;
   }
   if (T > 0 && !topk_ids) return fail(ACE_ERR_INVALID_ARG, "topk_ids is NULL");
-  if (!rt->counts || !rt->offsets || !rt->n_dropped)
+  // row_pair has P + 1 entries: the permutation writes its last one (the
+  // pair count) at T = 0 too
+  if (!rt->counts || !rt->offsets || !rt->n_dropped || !rt->row_pair)
     return fail(ACE_ERR_INVALID_ARG, "routing arrays are NULL");
-  if (T > 0 && (!rt->row_token || !rt->row_slots || !rt->pair_row || !rt->row_pair ||
-                 !rt->pair_list))
+  if (T > 0 && (!rt->row_token || !rt->row_slots || !rt->pair_row || !rt->pair_list))
     return fail(ACE_ERR_INVALID_ARG, "routing arrays are NULL");
   const size_t need = permute_ws_bytes(T, k, n_keys);
   if (need > 0 && (!ws || ws_bytes < need))
@@ -317,10 +320,9 @@ ace_status ace_group_expert_permute(const int32_t* topk_ids, int32_t T, int32_t 
   if (!expert_to_group) return fail(ACE_ERR_INVALID_ARG, "expert_to_group is NULL");
   if (T > 0 && !topk_ids) return fail(ACE_ERR_INVALID_ARG, "topk_ids is NULL");
   for (const ace_routing* rt : {(const ace_routing*)group_rt, (const ace_routing*)expert_rt}) {
-    if (!rt->counts || !rt->offsets || !rt->n_dropped)
+    if (!rt->counts || !rt->offsets || !rt->n_dropped || !rt->row_pair)
       return fail(ACE_ERR_INVALID_ARG, "routing arrays are NULL");
-    if (T > 0 && (!rt->row_token || !rt->row_slots || !rt->pair_row || !rt->row_pair ||
-                   !rt->pair_list))
+    if (T > 0 && (!rt->row_token || !rt->row_slots || !rt->pair_row || !rt->pair_list))
       return fail(ACE_ERR_INVALID_ARG, "routing arrays are NULL");
   }
   // the group routing's cell tables first, the expert routing's after them
@@ -489,7 +491,7 @@ ace_status ace_consolidate_adapters(ace_dtype dtype, int32_t d_in, int32_t d_out
                                     int32_t rank, const void* A, const void* B,
                                     const int32_t* expert_to_group, int32_t G,
                                     const int32_t* anchors, const void* A_init, void* A_g,
-                                    void* B_g, void* stream) {
+                                    void* B_g, int32_t* group_rank, void* stream) {
   if (dtype != ACE_F32 && dtype != ACE_BF16) return fail(ACE_ERR_INVALID_ARG, "unknown dtype %d", (int)dtype);
   ace_status s = check_groups(E, expert_to_group, G);
   if (s != ACE_OK) return s;
@@ -524,6 +526,8 @@ ace_status ace_consolidate_adapters(ace_dtype dtype, int32_t d_in, int32_t d_out
   }
   p.keys.roff[G] = R;
   p.keys.R = R;
+  if (group_rank)
+    for (int g = 0; g < G; ++g) group_rank[g] = p.keys.rank[g];
   return hip_status(launch_consolidate(dtype, p, static_cast<hipStream_t>(stream)),
                     "consolidate launch");
 }

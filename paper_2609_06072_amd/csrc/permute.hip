@@ -111,6 +111,11 @@ __device__ inline int mark_pass(const PermArgs& a, const PermPass& P, int np, co
   if (t < np) {
     const int e = eid[t];
     q = e < 0 ? -1 : (P.mode == ACE_ROWS_EXPERT ? e : gmap[e]);
+    // the routed experts of a token form a set: an id already listed at a
+    // lower slot of the same token drops this pair
+    const int j = t % a.k, tb = t - j;
+    for (int jj = 0; jj < j; ++jj)
+      if (eid[tb + jj] == e) q = -1;
     keys[t] = q;
   }
   __syncthreads();

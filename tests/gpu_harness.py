@@ -154,3 +154,52 @@ def check_rel(name: str, got, ref, tol: float) -> float:
     assert np.all(np.isfinite(np.asarray(got))), f"{name}: non-finite values"
     assert e <= tol, f"{name}: rel L2 {e:.3e} > {tol:.1e}"
     return e
+
+
+def check_rows(name: str, got, ref, tol: float, row_len: Optional[int] = None) -> float:
+    """Per-row companion of check_rel: every row's rel-L2 must be within tol,
+    and a row that is exactly zero in the reference (a dropped pair, a token
+    no pair reads, an empty key) must be exactly zero.  A whole-tensor norm
+    alone lets one wrong row in a few thousand pass; this catches an error
+    confined to a few rows or one column chunk.  Returns the worst row's
+    rel-L2."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert got.shape == ref.shape, f"{name}: shape {got.shape} != {ref.shape}"
+    if row_len is not None:
+        got, ref = got.reshape(-1, row_len), ref.reshape(-1, row_len)
+    elif got.ndim == 1:
+        got, ref = got[None, :], ref[None, :]
+    assert np.all(np.isfinite(got)), f"{name}: non-finite values"
+    rn = np.sqrt((ref * ref).sum(axis=1))
+    en = np.sqrt(((got - ref) ** 2).sum(axis=1))
+    zero = rn == 0.0
+    bad_zero = np.nonzero(zero & (np.abs(got).max(axis=1, initial=0.0) != 0.0))[0]
+    assert bad_zero.size == 0, f"{name}: rows {bad_zero[:8].tolist()} should be exactly zero"
+    rel = np.where(zero, 0.0, en / np.where(zero, 1.0, rn))
+    worst = int(np.argmax(rel)) if rel.size else 0
+    e = float(rel[worst]) if rel.size else 0.0
+    assert e <= tol, f"{name}: row {worst} rel L2 {e:.3e} > {tol:.1e}"
+    return e
+
+
+def check_dB_rows(name: str, got, ref, ranks: Sequence[int], d_out: int, tol: float) -> float:
+    """check_rows on dB per rank index: key q's block is [d_out, r_q]
+    row-major; each of its r_q columns (d_out values) is one row here."""
+    got = np.asarray(got, dtype=np.float64).reshape(-1)
+    ref = np.asarray(ref, dtype=np.float64).reshape(-1)
+    g_cols, r_cols = [], []
+    o = 0
+    for r in ranks:
+        n = d_out * int(r)
+        g_cols.append(got[o:o + n].reshape(d_out, int(r)).T)
+        r_cols.append(ref[o:o + n].reshape(d_out, int(r)).T)
+        o += n
+    return check_rows(name, np.concatenate(g_cols), np.concatenate(r_cols), tol)
+
+
+def check_all(name: str, got, ref, tol: float, row_len: Optional[int] = None) -> float:
+    """Whole-tensor rel-L2 (the contract) and the per-row check."""
+    e = check_rel(name, got, ref, tol)
+    check_rows(name, got, ref, tol, row_len)
+    return e

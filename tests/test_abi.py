@@ -248,3 +248,32 @@ def test_moe_fwd_rejects_bad_arguments(ace, no_device):
     st = lib.ace_moe_lora_fwd(1, 0, T, k, 64, 32, E, x, W, ctypes.byref(ert), E, r4, ekey, 16.0,
                               A, B, ctypes.byref(ert2), y, ws, need * 2, None)
     assert st == ace.ACE_ERR_INVALID_ARG
+
+
+def test_row_pair_required_at_every_size(ace, no_device):
+    """row_pair has P + 1 entries, so it exists at T = 0 too (the permutation
+    writes its last entry, the pair count): a NULL row_pair is rejected by
+    both permutation calls and by the forward even when T = 0."""
+    lib = ace.raw_lib()
+    ws = ctypes.c_void_p(0x10000)
+    ids = ctypes.c_void_p(0x20000)
+    e2g = ctypes.c_void_p(0x30000)
+
+    def no_row_pair(mode=0, n_keys=2):
+        return ace.AceRouting(0x1000, 0x2000, 0x3000, 0x4000, 0x5000, 0x6000, None, 0x8000,
+                              n_keys, mode, 0, 2)
+
+    st = lib.ace_group_permute(ids, 0, 2, 8, e2g, 2, 0, ctypes.byref(no_row_pair()), ws, 1 << 20,
+                               None)
+    assert st == ace.ACE_ERR_INVALID_ARG, ace.ace_last_error()
+    need = (ace.ace_workspace_bytes(ace.ACE_OP_PERMUTE, 0, 2, 0, 0, 2, 0)
+            + ace.ace_workspace_bytes(ace.ACE_OP_PERMUTE, 0, 2, 0, 0, 8, 0))
+    st = lib.ace_group_expert_permute(ids, 0, 2, 8, e2g, 2, 0, ctypes.byref(_routing(ace, T=0)),
+                                      ctypes.byref(no_row_pair(ace.ACE_ROWS_EXPERT, 8)), ws,
+                                      max(need, 256), None)
+    assert st == ace.ACE_ERR_INVALID_ARG, ace.ace_last_error()
+    ranks = (ctypes.c_int32 * 2)(16, 16)
+    p = ctypes.c_void_p(0x100000)
+    st = lib.ace_grouped_lora_fwd(ace.ACE_BF16, 0, 0, 2, 64, 32, 2, ranks, 16.0, p, p, p, None,
+                                  ctypes.byref(no_row_pair()), p, p, 1 << 20, None)
+    assert st == ace.ACE_ERR_INVALID_ARG, ace.ace_last_error()

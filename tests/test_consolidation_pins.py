@@ -177,6 +177,19 @@ def _same_partition(a, b):
     return np.array_equal(a[:, None] == a[None, :], b[:, None] == b[None, :])
 
 
+def test_modularity_hand_values():
+    """Q of fixed partitions of the 4-node example at gamma = 0.8 (and one at
+    gamma = 1), every value worked out by hand from the modularity formula of
+    the Louvain appendix.  A dropped gamma, a wrong 2m normaliser or a
+    missing degree term changes at least one of them.  The hand values are
+    decimal, so the comparison allows binary rounding (1e-12)."""
+    g = json.load(open(GOLDEN))["modularity"]
+    W = np.array(g["W"], dtype=np.float64)
+    for case in g["cases"]:
+        Q = C.modularity(W, case["labels"], case["gamma"])
+        assert abs(Q - case["Q"]) <= 1e-12, (case["labels"], case["gamma"], Q, case["Q"])
+
+
 def test_louvain_two_cliques():
     W = np.zeros((8, 8))
     for blk in ([0, 2, 4, 6], [1, 3, 5, 7]):

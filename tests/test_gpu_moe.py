@@ -13,7 +13,7 @@ import torch
 
 from oracle import ace_oracle as O
 from paper_2609_06072_amd import workloads as W
-from gpu_harness import TOL, check_rel, f64, make_case, say
+from gpu_harness import TOL, check_all, f64, make_case, say
 
 pytestmark = pytest.mark.gpu
 
@@ -87,7 +87,7 @@ def test_moe_parity_small(name, path):
     c, Wt = case_and_weights(cfg, path)
     say(f"moe small {name} {path} T={cfg.T} d_in={c.d_in} d_out={c.d_out}")
     y = run_moe(c, Wt)
-    check_rel("y", f64(y), oracle_y(c, Wt), TOL[cfg.dtype])
+    check_all("y", f64(y), oracle_y(c, Wt), TOL[cfg.dtype])
 
 
 @pytest.mark.parametrize("name", ["tiny_fp32", "olmoe_bf16", "mixtral_bf16"])
@@ -96,7 +96,7 @@ def test_moe_base_only(name):
     for path in ("expertwise", "down_expertwise"):
         c, Wt = case_and_weights(cfg, path, seed=1)
         y = run_moe(c, Wt, base_only=True)
-        check_rel("W_e x", f64(y), oracle_y(c, Wt, base_only=True), TOL[cfg.dtype])
+        check_all("W_e x", f64(y), oracle_y(c, Wt, base_only=True), TOL[cfg.dtype])
 
 
 @pytest.mark.parametrize("path", ["grouped", "down_expertwise", "pairs_per_pair"])
@@ -109,7 +109,7 @@ def test_moe_zero_base_is_the_adapter_update(path):
     ref = O.lora_delta(f64(c.x), f64(c.A), f64(c.B), c.ranks, cfg.alpha,
                        c.rt.topk_ids.astype(np.int64), cfg.E, c.e2g, c.n_keys,
                        input_mode=c.input_mode)
-    check_rel("adapter update", f64(y), ref, TOL["bf16"])
+    check_all("adapter update", f64(y), ref, TOL["bf16"])
 
 
 def test_moe_dropped_pairs_and_untouched_rows():
@@ -124,7 +124,7 @@ def test_moe_dropped_pairs_and_untouched_rows():
     yd = f64(y)
     assert np.all(yd[dropped] == 7.0)
     keep = np.setdiff1d(np.arange(cfg.P), dropped)
-    check_rel("y", yd[keep], oracle_y(c, Wt)[keep], TOL["bf16"])
+    check_all("y", yd[keep], oracle_y(c, Wt)[keep], TOL["bf16"])
 
 
 def test_moe_empty_input():
@@ -144,7 +144,7 @@ def test_moe_odd_ranks(dtype, r_e):
     cfg = W.CONFIGS["olmoe_bf16"].scaled(T=200, d_model=136, d_ffn=96, dtype=dtype, r_e=r_e)
     for path in ("grouped", "down_expertwise"):
         c, Wt = case_and_weights(cfg, path, seed=4)
-        check_rel("y", f64(run_moe(c, Wt)), oracle_y(c, Wt), TOL[dtype])
+        check_all("y", f64(run_moe(c, Wt)), oracle_y(c, Wt), TOL[dtype])
 
 
 def test_moe_max_rank_and_many_experts():
@@ -152,12 +152,12 @@ def test_moe_max_rank_and_many_experts():
                                          groups=("consecutive", 4))
     c, Wt = case_and_weights(cfg, "grouped", seed=5)
     assert max(c.ranks) == 256
-    check_rel("y", f64(run_moe(c, Wt)), oracle_y(c, Wt), TOL["bf16"])
+    check_all("y", f64(run_moe(c, Wt)), oracle_y(c, Wt), TOL["bf16"])
     cfg = W.CONFIGS["olmoe_bf16"].scaled(T=100, d_model=64, d_ffn=64, E=256, k=16, r_e=2,
                                          groups=("consecutive", 1))
     c, Wt = case_and_weights(cfg, "grouped", seed=6)
     assert c.n_keys == 256
-    check_rel("y", f64(run_moe(c, Wt)), oracle_y(c, Wt), TOL["bf16"])
+    check_all("y", f64(run_moe(c, Wt)), oracle_y(c, Wt), TOL["bf16"])
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
@@ -169,7 +169,7 @@ def test_moe_many_rows_per_expert(dtype):
     assert cfg.P >= 1024 * cfg.E
     for path in ("grouped", "down_expertwise"):
         c, Wt = case_and_weights(cfg, path, seed=11)
-        check_rel("y", f64(run_moe(c, Wt)), oracle_y(c, Wt), TOL[dtype])
+        check_all("y", f64(run_moe(c, Wt)), oracle_y(c, Wt), TOL[dtype])
 
 
 def test_moe_deterministic():
@@ -198,5 +198,5 @@ def test_moe_parity_full_size_sampled(name, path):
         x = f64(c.x[torch.as_tensor(pairs, device="cuda")])
     rows = (toks[:, None] * k + np.arange(k)[None, :]).ravel()
     ref = oracle_y(c, Wt, ids=ids, x=x)
-    check_rel("y(sampled tokens)", f64(y[torch.as_tensor(rows, device="cuda")]), ref,
+    check_all("y(sampled tokens)", f64(y[torch.as_tensor(rows, device="cuda")]), ref,
               TOL[cfg.dtype])

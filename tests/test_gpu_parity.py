@@ -12,8 +12,8 @@ import torch
 from oracle import ace_oracle as O
 from paper_2609_06072_amd import workloads as W
 
-from gpu_harness import (PATHS, TOL, WEIGHTED, check_rel, f64, make_case, oracle_args,
-                         oracle_bwd, oracle_fwd, run_gpu, say)
+from gpu_harness import (PATHS, TOL, WEIGHTED, check_all, check_dB_rows, check_rel, f64,
+                         make_case, oracle_args, oracle_bwd, oracle_fwd, run_gpu, say)
 
 pytestmark = pytest.mark.gpu
 
@@ -164,11 +164,12 @@ def test_parity_small(name, path):
     say(f"parity {name} {path} T={cfg.T} d_in={c.d_in} d_out={c.d_out} keys={c.n_keys}")
     out = run_gpu(c)
     tol = TOL[cfg.dtype]
-    check_rel("delta", f64(out["y"]), oracle_fwd(c), tol)
+    check_all("delta", f64(out["y"]), oracle_fwd(c), tol)
     dx, dA, dB = oracle_bwd(c)
-    check_rel("dx", f64(out["dx"]), dx, tol)
-    check_rel("dA", f64(out["dA"]), dA, tol)
+    check_all("dx", f64(out["dx"]), dx, tol)
+    check_all("dA", f64(out["dA"]), dA, tol)
     check_rel("dB", f64(out["dB"]), dB, tol)
+    check_dB_rows("dB", f64(out["dB"]), dB, c.ranks, c.d_out, tol)
 
 
 @pytest.mark.parametrize("name", ["tiny_fp32", "olmoe_bf16", "mixtral_bf16"])
@@ -209,12 +210,15 @@ def _sub_tokens(c, toks):
 
 
 @pytest.mark.parametrize("name", W.CONFIG_ORDER)
-@pytest.mark.parametrize("path", ["grouped", "expertwise", "down_expertwise", "combined"])
+@pytest.mark.parametrize("path", ["grouped", "expertwise", "down_expertwise", "combined",
+                                  "pairs_shared", "pairs_per_pair"])
 def test_parity_full_size_sampled(name, path):
     cfg = W.CONFIGS[name]
-    if path in ("down_expertwise", "combined") and "down" not in cfg.projections:
+    if path in ("down_expertwise", "combined", "pairs_per_pair") and "down" not in cfg.projections:
         pytest.skip("this workload adapts the up projection only")
-    c = make_case(cfg, path, seed=0, with_w=(path == "combined"))
+    # pair weights where the timed paths can carry them (per-row weights of
+    # multi-slot rows on the grouped path)
+    c = make_case(cfg, path, seed=0, with_w=(path in ("combined", "grouped", "pairs_per_pair")))
     say(f"full-size {name} {path} T={cfg.T} d_in={c.d_in} d_out={c.d_out}")
     out = run_gpu(c, reuse_h=True)   # as timed: the backward reuses the forward's h
     tol = TOL[cfg.dtype]
@@ -227,7 +231,7 @@ def test_parity_full_size_sampled(name, path):
     rows = (toks[:, None] * k + np.arange(k)[None, :]).ravel()
     # output / output-gradient rows: per pair, or per token when combined
     orows = toks if c.input_mode == W.INPUT_COMBINED else rows
-    check_rel("delta(sampled tokens)", f64(out["y"][torch.as_tensor(orows, device="cuda")]), ref,
+    check_all("delta(sampled tokens)", f64(out["y"][torch.as_tensor(orows, device="cuda")]), ref,
               tol)
     dy_sub = f64(c.dy[torch.as_tensor(orows, device="cuda")])
     dx_ref, _, _ = O.lora_grads(*a, dy_sub, input_mode=c.input_mode, pair_w=w)
@@ -235,7 +239,7 @@ def test_parity_full_size_sampled(name, path):
         got = f64(out["dx"][torch.as_tensor(toks, device="cuda")])
     else:
         got = f64(out["dx"][torch.as_tensor(rows, device="cuda")])
-    check_rel("dx(sampled tokens)", got, dx_ref, tol)
+    check_all("dx(sampled tokens)", got, dx_ref, tol)
     # dA/dB of the largest and the smallest non-empty key: every pair of the key
     keys = O.pair_keys(c.rt.topk_ids.astype(np.int64), cfg.E, c.e2g, c.n_keys)
     cnt = np.bincount(keys[keys >= 0].ravel(), minlength=c.n_keys)
@@ -247,9 +251,10 @@ def test_parity_full_size_sampled(name, path):
         a, w = oracle_args(c, ids=ids_q)
         _, dA, dB = O.lora_grads(*a, f64(c.dy), input_mode=c.input_mode, pair_w=w)
         lo, hi = off[q], off[q + 1]
-        check_rel(f"dA[key {q}]", f64(out["dA"][lo:hi]), dA[lo:hi], tol)
-        check_rel(f"dB[key {q}]", f64(out["dB"][c.d_out * lo: c.d_out * hi]),
-                  dB[c.d_out * lo: c.d_out * hi], tol)
+        check_all(f"dA[key {q}]", f64(out["dA"][lo:hi]), dA[lo:hi], tol)
+        got_B, ref_B = f64(out["dB"][c.d_out * lo: c.d_out * hi]), dB[c.d_out * lo: c.d_out * hi]
+        check_rel(f"dB[key {q}]", got_B, ref_B, tol)
+        check_dB_rows(f"dB[key {q}]", got_B, ref_B, [c.ranks[q]], c.d_out, tol)
 
 
 # ---------------------------------------------------------- invariants
@@ -283,6 +288,33 @@ def test_group_per_expert_is_bitwise_expertwise(permuted):
         check_rel("dx", f64(gr["dx"]), f64(ew["dx"]), 1e-2)
     else:
         assert torch.equal(gr["dx"], ew["dx"])
+
+
+@pytest.mark.parametrize("path", ["expertwise", "combined_expertwise", "grouped", "down_expertwise"])
+def test_repeated_ids_are_dropped(path):
+    """A token that lists an expert twice: the repeat is dropped (the routed
+    experts of a token are a set) on every path, including the shared-input
+    expert-wise backward, whose dense per-token dH rows would otherwise
+    collide, and the combined expert-wise down projection."""
+    from paper_2609_06072_amd import ace
+    cfg = SMALL["olmoe_bf16"]
+    c = make_case(cfg, path, seed=12, with_w=(path in WEIGHTED))
+    ids = c.rt.topk_ids.copy()
+    ids[::5, 1] = ids[::5, 0]
+    ids[::7, 3] = ids[::7, 2]
+    c.rt = W.Routing(ids.astype(np.int32), c.rt.topk_w, c.rt.expert_to_group, c.rt.group_rank,
+                     c.rt.expert_rank)
+    say(f"repeated ids {path}")
+    out = run_gpu(c)
+    n_rep = sum(1 for t in range(cfg.T) for j in range(cfg.k) if ids[t, j] in ids[t, :j])
+    assert n_rep > 0
+    assert ace.ace_routing_check(out["routing"]) == n_rep
+    tol = TOL[cfg.dtype]
+    check_all("delta", f64(out["y"]), oracle_fwd(c), tol)
+    dx, dA, dB = oracle_bwd(c)
+    check_all("dx", f64(out["dx"]), dx, tol)
+    check_all("dA", f64(out["dA"]), dA, tol)
+    check_dB_rows("dB", f64(out["dB"]), dB, c.ranks, c.d_out, tol)
 
 
 @pytest.mark.parametrize("path", ["grouped", "down_expertwise", "pairs_shared"])

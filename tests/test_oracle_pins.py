@@ -313,6 +313,46 @@ def test_empty_group_and_dropped_pairs():
     assert not d[4:6].any()
 
 
+def test_repeated_id_within_a_token_is_dropped():
+    """The routed experts R(x) of a token are a set (Sec. 3.1): a slot that
+    repeats an expert id listed at a lower slot of the same token is not a
+    routed pair.  Every oracle path treats it exactly like an id out of range."""
+    rng = np.random.default_rng(11)
+    T, k, E, G, d_in, d_out = 3, 3, 4, 2, 5, 4
+    e2g = np.array([0, 0, 1, 1])
+    ids = np.array([[2, 2, 0], [1, 3, 1], [0, 1, 2]])
+    gone = ids.copy()
+    gone[0, 1] = gone[1, 2] = -1              # the repeats, dropped by hand
+    x = rng.normal(size=(T, d_in))
+    xp = rng.normal(size=(T * k, d_in))
+    dy = rng.normal(size=(T * k, d_out))
+    for e2g_, n_keys, ranks in ((e2g, G, [4, 4]), (None, E, [2, 2, 2, 2])):
+        A = rng.normal(size=(sum(ranks), d_in))
+        B = rng.normal(size=(d_out * sum(ranks),))
+        for im, xin in ((O.INPUT_SHARED, x), (O.INPUT_PER_PAIR, xp)):
+            a = (xin, A, B, ranks, 16.0)
+            d = O.lora_delta(*a, ids, E, e2g_, n_keys, input_mode=im)
+            assert not d[1].any() and not d[5].any()
+            assert np.array_equal(d, O.lora_delta(*a, gone, E, e2g_, n_keys, input_mode=im))
+            assert np.allclose(O.brute_delta(*a, ids, E, e2g_, n_keys, input_mode=im), d,
+                               rtol=1e-12, atol=1e-12)
+            g1 = O.lora_grads(*a, ids, E, e2g_, n_keys, dy, input_mode=im)
+            g0 = O.lora_grads(*a, gone, E, e2g_, n_keys, dy, input_mode=im)
+            for u, v in zip(g1, g0):
+                assert np.array_equal(u, v)
+    for mode in (O.ROWS_GROUP_DEDUP, O.ROWS_GROUP_PAIRS, O.ROWS_EXPERT):
+        r1 = O.permute(ids, E, e2g, G, mode)
+        r0 = O.permute(gone, E, e2g, G, mode)
+        for key in ("counts", "offsets", "row_token", "row_slots", "pair_row", "row_pair",
+                    "pair_list"):
+            assert np.array_equal(r1[key], r0[key]), (mode, key)
+        assert r1["pair_row"][1] == -1 and r1["pair_row"][5] == -1
+    # token 0 in group mode: slots 0 and 2 (experts 2 and 0) are in different
+    # groups, so the repeat leaves one row per group with one slot each
+    r = O.permute(ids, E, e2g, G, O.ROWS_GROUP_DEDUP)
+    assert sorted(int(m) for m, t in zip(r["row_slots"], r["row_token"]) if t == 0) == [1, 4]
+
+
 # ---------------------------------------------- permutation invariants
 
 @pytest.mark.parametrize("mode", [O.ROWS_GROUP_DEDUP, O.ROWS_GROUP_PAIRS, O.ROWS_EXPERT])
