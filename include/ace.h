@@ -152,6 +152,27 @@ ace_status ace_group_permute(const int32_t* topk_ids, int32_t T, int32_t k, int3
                              ace_routing* rt, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * ace_group_permute for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): no workspace argument.  The permutation's scratch (its count
+ * tables, ace_workspace_bytes(ACE_OP_PERMUTE, T, k, 0, 0, n_keys, 0) bytes)
+ * is a static device array of ACE_PERMUTE_SCRATCH_BYTES in the library, one
+ * per GPU, held until the process ends; its address is looked up on the
+ * first call on each device.  Nothing is allocated and nothing needs
+ * clearing (the tables are fully written before they are read).
+ *   Arguments, outputs and errors as for ace_group_permute; a problem whose
+ *   scratch exceeds ACE_PERMUTE_SCRATCH_BYTES returns ACE_ERR_UNSUPPORTED
+ *   before anything is launched (4 MiB holds, e.g., T*k = 1M pairs over 64
+ *   keys or 500K pairs over 256 keys).
+ *   Calls on one GPU share its array: calls that overlap in time on the same
+ *   GPU (different streams or threads) race and must not be issued.
+ */
+#define ACE_PERMUTE_SCRATCH_BYTES (4u << 20)
+ace_status ace_group_permute_noalloc(const int32_t* topk_ids, int32_t T, int32_t k, int32_t E,
+                                     const int32_t* expert_to_group, int32_t G,
+                                     ace_row_mode mode, ace_routing* rt, void* stream);
+
+/*
  * Both routings an ACE layer needs from one top-k routing (Sec. 3.5 for the
  * grouped gate/up projections; the down projection stays expert-wise, App. L):
  * group_rt in group_mode (ACE_ROWS_GROUP_DEDUP or ACE_ROWS_GROUP_PAIRS,

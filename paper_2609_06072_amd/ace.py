@@ -30,7 +30,9 @@ ACE_OP_PERMUTE, ACE_OP_FWD, ACE_OP_BWD, ACE_OP_CKA = 0, 1, 2, 3
 EXPORTS = ("ace_group_permute", "ace_group_expert_permute", "ace_grouped_lora_fwd", "ace_grouped_lora_bwd",
            "ace_expertwise_lora_fwd", "ace_expertwise_lora_bwd", "ace_workspace_bytes",
            "ace_routing_check", "ace_last_error", "ace_pairwise_cka", "ace_similarity_graph",
-           "ace_louvain", "ace_group_anchors", "ace_consolidate_adapters", "ace_moe_lora_fwd")
+           "ace_louvain", "ace_group_anchors", "ace_consolidate_adapters", "ace_moe_lora_fwd",
+           "ace_group_permute_noalloc")
+ACE_PERMUTE_SCRATCH_BYTES = 4 << 20
 
 
 class AceRouting(ctypes.Structure):
@@ -46,6 +48,8 @@ _i32, _f32, _vp, _sz = ctypes.c_int32, ctypes.c_float, ctypes.c_void_p, ctypes.c
 _R = ctypes.POINTER(AceRouting)
 _lib.ace_group_permute.argtypes = [_vp, _i32, _i32, _i32, _vp, _i32, _i32, _R, _vp, _sz, _vp]
 _lib.ace_group_permute.restype = _i32
+_lib.ace_group_permute_noalloc.argtypes = [_vp, _i32, _i32, _i32, _vp, _i32, _i32, _R, _vp]
+_lib.ace_group_permute_noalloc.restype = _i32
 _lib.ace_group_expert_permute.argtypes = [_vp, _i32, _i32, _i32, _vp, _i32, _i32, _R, _R, _vp, _sz,
                                           _vp]
 _lib.ace_group_expert_permute.restype = _i32
@@ -224,6 +228,22 @@ def ace_group_permute(topk_ids: torch.Tensor, E: int, expert_to_group: Optional[
     _check(_lib.ace_group_permute(_ptr(topk_ids), T, k, E, _ptr(expert_to_group), G, mode,
                                   ctypes.byref(routing.c), _ptr(ws), ws.numel(), _stream(stream)),
            "ace_group_permute")
+    return routing
+
+
+def ace_group_permute_noalloc(topk_ids: torch.Tensor, E: int,
+                              expert_to_group: Optional[torch.Tensor], G: int, mode: int,
+                              routing: Routing, stream=None) -> Routing:
+    """ace_group_permute with the library's static scratch instead of a
+    workspace: allocates nothing (the caller passes the routing arrays)."""
+    T, k = topk_ids.shape
+    n_keys = E if mode == ACE_ROWS_EXPERT else G
+    _want("topk_ids", topk_ids, dtype=torch.int32)
+    _want("expert_to_group", expert_to_group, E, torch.int32, topk_ids.device, optional=True)
+    routing.check_capacity(T, k, n_keys)
+    _check(_lib.ace_group_permute_noalloc(_ptr(topk_ids), T, k, E, _ptr(expert_to_group), G,
+                                          mode, ctypes.byref(routing.c), _stream(stream)),
+           "ace_group_permute_noalloc")
     return routing
 
 

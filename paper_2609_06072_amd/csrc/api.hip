@@ -6,6 +6,7 @@
 #include <stdio.h>
 
 #include <cmath>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -40,6 +41,45 @@ ace_status hip_status(hipError_t e, const char* what) {
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
 size_t round256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+// Scratch of ace_group_permute_noalloc: the permutation's cell tables live in
+// this static device array instead of a caller workspace.  Every GPU the
+// library runs on holds its own copy until the process ends.  In host code
+// the name is only a stand-in: kernels get the device address obtained once
+// per device with hipGetSymbolAddress.
+constexpr size_t kNoAllocScratchBytes = (size_t)ACE_PERMUTE_SCRATCH_BYTES;
+static __device__ __align__(256) uint8_t scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's scratch array (nullptr and the
+// message set on failure).  Looked up once per device, with that device
+// current, and kept.
+void* device_scratch(ace_status* st) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) {
+    *st = fail(ACE_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+    return nullptr;
+  }
+  if (dev < 0 || dev >= kMaxDevices) {
+    *st = fail(ACE_ERR_UNSUPPORTED, "device %d outside [0, %d)", dev, kMaxDevices);
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) {
+      *st = fail(ACE_ERR_HIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+      return nullptr;
+    }
+    g_scratch_ptr[dev] = ptr;
+  }
+  return g_scratch_ptr[dev];
+}
 
 // Shared validation of the forward/backward calls; fills the Problem.
 ace_status check_problem(Problem& p, ace_dtype dtype, ace_input_mode im, int32_t T, int32_t k,
@@ -301,6 +341,28 @@ ace_status ace_group_permute(const int32_t* topk_ids, int32_t T, int32_t k, int3
   return hip_status(launch_permute(topk_ids, T, k, E, expert_to_group, G, 1, &out,
                                    static_cast<hipStream_t>(stream)),
                     "permute launch");
+}
+
+ace_status ace_group_permute_noalloc(const int32_t* topk_ids, int32_t T, int32_t k, int32_t E,
+                                     const int32_t* expert_to_group, int32_t G, ace_row_mode mode,
+                                     ace_routing* rt, void* stream) {
+  // size check first (host only); ace_group_permute validates the rest
+  if (T >= 0 && k >= 1 && k <= kMaxK && (int64_t)T * k < ((int64_t)1 << 31)) {
+    const int n_keys = mode == ACE_ROWS_EXPERT ? E : G;
+    if (n_keys >= 1 && n_keys <= kMaxKeys) {
+      const size_t need = permute_ws_bytes(T, k, n_keys);
+      if (need > kNoAllocScratchBytes)
+        return fail(ACE_ERR_UNSUPPORTED,
+                    "permutation of %d x %d pairs over %d keys needs %zu scratch bytes, the "
+                    "static scratch holds %zu",
+                    T, k, n_keys, need, kNoAllocScratchBytes);
+    }
+  }
+  ace_status st = ACE_OK;
+  void* ptr = device_scratch(&st);
+  if (!ptr) return st;
+  return ace_group_permute(topk_ids, T, k, E, expert_to_group, G, mode, rt, ptr,
+                           kNoAllocScratchBytes, stream);
 }
 
 ace_status ace_group_expert_permute(const int32_t* topk_ids, int32_t T, int32_t k, int32_t E,

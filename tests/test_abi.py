@@ -277,3 +277,16 @@ def test_row_pair_required_at_every_size(ace, no_device):
     st = lib.ace_grouped_lora_fwd(ace.ACE_BF16, 0, 0, 2, 64, 32, 2, ranks, 16.0, p, p, p, None,
                                   ctypes.byref(no_row_pair()), p, p, 1 << 20, None)
     assert st == ace.ACE_ERR_INVALID_ARG, ace.ace_last_error()
+
+
+def test_noalloc_permute_rejects_oversized_problem(ace, no_device):
+    """The no-allocation permutation refuses, before any HIP call, a problem
+    whose count tables exceed its static scratch."""
+    lib = ace.raw_lib()
+    T, k, E = 1 << 20, 8, 256
+    assert ace.ace_workspace_bytes(ace.ACE_OP_PERMUTE, T, k, 0, 0, E, 0) > ace.ACE_PERMUTE_SCRATCH_BYTES
+    r = _routing(ace, T=T, k=k, n_keys=E, mode=ace.ACE_ROWS_EXPERT)
+    st = lib.ace_group_permute_noalloc(ctypes.c_void_p(0x20000), T, k, E, None, E,
+                                       ace.ACE_ROWS_EXPERT, ctypes.byref(r), None)
+    assert st == ace.ACE_ERR_UNSUPPORTED, ace.ace_last_error()
+    assert "scratch" in ace.ace_last_error()
