@@ -11,7 +11,9 @@ routing, for both execution schemes on the same GPU:
 Metric: routed (token, expert) pairs per second of the ace step (fwd+bwd), the
 speedup over the lora step, and the HBM roofline fraction of the dominant
 call (the library call of the ace step that takes longest, all of its kernels).
-Prints one JSON line.
+The headline workload is the Mixtral-like layer (the largest of the suite that
+one GPU holds); `configs` repeats both steps on every workload of the suite in
+the same run.  Prints one JSON line.
 """
 from __future__ import annotations
 
@@ -319,11 +321,67 @@ def cpu_baseline(cfg, rt, budget_s=15.0):
     while sum(times) < budget_s and len(times) < 9:
         times.append(run(Tp))
     dt = statistics.median(times)
-    return {"value": Tp * cfg.k / dt, "unit": "routed tokens/s", "cores": int(threads),
-            "kind": "oracle",
-            "sample": f"first {Tp} of {cfg.T} tokens ({Tp * cfg.k} routed pairs), fwd+bwd of "
-                      f"{'/'.join(cfg.projections)} in fp64 numpy; median of {len(times)} runs "
-                      f"({sum(times):.1f} s in total), {dt:.2f} s per run"}
+    out = {"value": Tp * cfg.k / dt, "unit": "routed tokens/s", "cores": int(threads),
+           "kind": "oracle",
+           "sample": f"first {Tp} of {cfg.T} tokens ({Tp * cfg.k} routed pairs), fwd+bwd of "
+                     f"{'/'.join(cfg.projections)} in fp64 numpy; median of {len(times)} runs "
+                     f"({sum(times):.1f} s in total), {dt:.2f} s per run"}
+    out.update(host_facts())
+    out["blas_threads"] = int(threads)
+    # the same oracle on one thread, on a smaller sample (about a tenth of
+    # the tokens, so that it stays within a few seconds per run)
+    try:
+        from threadpoolctl import threadpool_limits
+        T1 = max(1, Tp // 10)
+        with threadpool_limits(limits=1):
+            run(T1)
+            d1 = [run(T1) for _ in range(2)]
+        out["single_thread"] = {"value": T1 * cfg.k / statistics.median(d1), "unit": "routed tokens/s",
+                                "cores": 1,
+                                "sample": f"first {T1} tokens ({T1 * cfg.k} routed pairs), BLAS "
+                                          f"limited to one thread; median of 2 runs"}
+    except Exception as e:  # pragma: no cover
+        out["single_thread"] = {"error": repr(e)}
+    return out
+
+
+def host_facts():
+    """CPU model, logical CPUs and the affinity mask of this process."""
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:  # pragma: no cover
+        pass
+    try:
+        aff = sorted(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        aff = []
+    return {"cpu_model": model, "os_cpu_count": os.cpu_count(), "affinity_cpus": len(aff)}
+
+
+def copy_peak_gbs(nbytes=1 << 30, reps=20):
+    """HBM bandwidth of a plain device copy (reads and writes nbytes each),
+    median of reps back-to-back copies timed with HIP events."""
+    import torch
+    src = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(reps):
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        dst.copy_(src)
+        e.record()
+        torch.cuda.synchronize()
+        ts.append(s.elapsed_time(e))
+    del src, dst
+    torch.cuda.empty_cache()
+    return 2.0 * nbytes / (statistics.median(ts) * 1e-3) / 1e9
 
 
 # ---------------------------------------------------------------- consolidation
@@ -810,7 +868,12 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--repeats", type=int, default=5)
-    ap.add_argument("--config", default="olmoe_bf16", choices=W.CONFIG_ORDER)
+    ap.add_argument("--config", default="mixtral_bf16", choices=W.CONFIG_ORDER,
+                    help="headline workload (default: Mixtral-like, the largest single-GPU one)")
+    ap.add_argument("--side-config", default="olmoe_bf16", choices=W.CONFIG_ORDER,
+                    help="workload of the consolidation step and the adapted projection")
+    ap.add_argument("--no-all-configs", action="store_true",
+                    help="skip the table of every workload (ace and expert-wise steps)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true",
@@ -864,67 +927,33 @@ def main():
 
     cfg = W.CONFIGS[args.config]
     torch.cuda.set_device(0)
+    # the consolidation step and the adapted projection are measured on the
+    # OLMoE-like layer (the paper's consolidation overheads are quoted on
+    # OLMoE) unless that section's own run names a configuration
+    side_cfg = W.CONFIGS[args.side_config]
     if args.consolidation_only:
         print(json.dumps(consolidation_bench(ace, cfg, args.seed, cpu=not args.no_cpu_baseline)),
               flush=True)
         return
-    rt = W.make_routing(cfg, args.seed)
     if args.fused_only:
+        rt = W.make_routing(cfg, args.seed)
         print(json.dumps(fused_projection_bench(ace, cfg, rt, args.seed,
                                                 cpu=not args.no_cpu_baseline)), flush=True)
         return
-    bufs = make_buffers(cfg, rt, args.seed)
-    b = 2 if cfg.dtype == "bf16" else 4
-    r_max = max(int(rt.group_rank.max()), cfg.r_e)
-    n_keys = max(cfg.E, rt.G)
-    # room for a group-keyed and an expert-keyed routing written by one call
-    ws_perm = torch.empty(max(256, ace.ace_workspace_bytes(ace.ACE_OP_PERMUTE, cfg.T, cfg.k, 0, 0,
-                                                            rt.G, 0)
-                              + ace.ace_workspace_bytes(ace.ACE_OP_PERMUTE, cfg.T, cfg.k, 0, 0,
-                                                        n_keys, 0)),
-                          dtype=torch.uint8, device="cuda")
-    need = 0
-    for proj in cfg.projections:
-        d_in, d_out, _ = cfg.proj_dims(proj)
-        for nk, r in ((rt.G, int(rt.group_rank.max())), (cfg.E, cfg.r_e)):
-            need = max(need, ace.ace_workspace_bytes(ace.ACE_OP_BWD, cfg.T, cfg.k, d_in, d_out, nk, r))
-    ws_bwd = torch.empty(need, dtype=torch.uint8, device="cuda")
-
-    kinds = ("ace", "lora") if args.no_extras else (
-        "ace", "lora", "consolidated", "consolidated_down", "combined_down",
-        "combined_down_expertwise")
-    paths = {kind: Path(ace, cfg, rt, kind, bufs, ws_perm, ws_bwd) for kind in kinds}
     if args.traffic_pass:
+        rt = W.make_routing(cfg, args.seed)
+        paths = build_paths(ace, cfg, rt, args.seed, extras=not args.no_extras)
+        paths.pop("_bufs")
         traffic_pass(paths, args.traffic_pass)
         return
-    res = {}
-    if not args.no_extras:
-        # launch-bound: a few steps suffice
-        pe = PerExpertPath(ace, cfg, rt, bufs)
-        per_step, _ = time_path(pe, max(2, args.steps // 20), 2, 2)
-        res["expertwise_per_expert_launch"] = dict(ms=statistics.median(per_step), ms_std=statistics.pstdev(per_step),
-                                                   ms_with_events=statistics.median(per_step), phases={})
-    for kind, path in paths.items():
-        per_step, phases = time_path(path, args.steps, args.warmup, args.repeats)
-        plain = time_plain(path, args.steps, args.repeats)
-        res[kind] = dict(ms=statistics.median(plain), ms_std=statistics.pstdev(plain),
-                         ms_with_events=statistics.median(per_step), phases=phases)
 
-    # algorithmic bytes of a step and of each call (proj.fwd / proj.bwd)
-    T, P = cfg.T, cfg.P
-    step_bytes = 0
-    call_bytes = {}
-    for proj in cfg.projections:
-        d_in, d_out, im = cfg.proj_dims(proj)
-        f, bb = algo_bytes(im == W.INPUT_SHARED, T, P, d_in, d_out, cfg.E * cfg.r_e, b)
-        step_bytes += f + bb
-        call_bytes[f"{proj}.fwd"], call_bytes[f"{proj}.bwd"] = f, bb
-    ace_ms = res["ace"]["ms"]
-    lora_ms = res["lora"]["ms"]
-    call_roofline = {
-        kind: {k: call_bytes[k] / (res[kind]["phases"][k] * 1e-3) / (HBM_PEAK_GBS * 1e9)
-               for k in call_bytes}
-        for kind in ("ace", "lora")}
+    copy_gbs = copy_peak_gbs()
+    m = measure_config(ace, cfg, args.seed, args.steps, args.warmup, args.repeats,
+                       extras=not args.no_extras)
+    res, rt = m["res"], m["rt"]
+    P = cfg.P
+    ace_ms, lora_ms = res["ace"]["ms"], res["lora"]["ms"]
+    call_bytes = m["call_bytes"]
     # the dominant call of the ace step: the one that takes longest
     dom = max(call_bytes, key=lambda k: res["ace"]["phases"][k])
     dom_ms = res["ace"]["phases"][dom]
@@ -952,41 +981,28 @@ def main():
         "dtype": cfg.dtype,
         "data": "synthetic",
         "config": {
-            "workload": f"{cfg.name}: T={cfg.T} d_model={cfg.d_model} d_ffn={cfg.d_ffn} "
-                        f"E={cfg.E} top-{cfg.k} routing={cfg.routing[0]}({cfg.routing[1]}) "
-                        f"G={rt.G} expert rank {cfg.r_e} -> group ranks "
-                        f"{sorted(set(int(r) for r in rt.group_rank))}; "
-                        f"LoRA on {'/'.join(cfg.projections)}; grouped gate/up, expert-wise down",
-            "routed_pairs": P, "tokens": T, "parallelism": "single GPU",
+            "workload": workload_name(cfg, rt),
+            "routed_pairs": P, "tokens": cfg.T, "parallelism": "single GPU",
         },
         "speedup_vs_expertwise": lora_ms / ace_ms,
         "expertwise": {"value": P / (lora_ms * 1e-3), "ms_per_step": lora_ms},
         "paper_speedup": PAPER_SPEEDUP,
-        "step_roofline": {"bound": "hbm", "algorithmic_bytes": step_bytes,
-                          "frac_ace": step_bytes / (ace_ms * 1e-3) / (HBM_PEAK_GBS * 1e9),
-                          "frac_expertwise": step_bytes / (lora_ms * 1e-3) / (HBM_PEAK_GBS * 1e9)},
+        "step_roofline": {"bound": "hbm", "algorithmic_bytes": m["step_bytes"],
+                          "frac_ace": m["step_bytes"] / (ace_ms * 1e-3) / (HBM_PEAK_GBS * 1e9),
+                          "frac_expertwise": m["step_bytes"] / (lora_ms * 1e-3) / (HBM_PEAK_GBS * 1e9),
+                          "measured_copy_GBps": copy_gbs,
+                          "frac_ace_of_copy": m["step_bytes"] / (ace_ms * 1e-3) / (copy_gbs * 1e9)},
         "roofline": {"bound": "hbm", "kernel": f"{entry} ({proj}): all kernels of one call",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": dom_traffic,
-                     "algorithmic_bytes": call_bytes[dom], "ms_per_call": dom_ms},
-        "call_roofline_frac": call_roofline,
+                     "algorithmic_bytes": call_bytes[dom], "ms_per_call": dom_ms,
+                     "measured_copy_GBps": copy_gbs, "frac_of_copy": achieved / copy_gbs},
+        "call_roofline_frac": m["call_roofline"],
         "phases_ms": {k: {kind: res[kind]["phases"].get(k) for kind in res}
                       for k in sorted(set().union(*(set(r["phases"]) for r in res.values())))},
         "extra_rows": {
             kind: {"ms_per_step": res[kind]["ms"], "value": P / (res[kind]["ms"] * 1e-3),
-                   "what": {"consolidated": "group-rank adapters on gate/up run per routed pair "
-                                            "(no compute-once), expert-wise down",
-                            "consolidated_down": "ace step with the down projection at group "
-                                                 "rank over pair rows",
-                            "combined_down": "ace step with the down projection pre-combined: "
-                                             "output summed per token with the routing weights, "
-                                             "one group-rank row per (token, active group)",
-                            "combined_down_expertwise": "expert-wise step with the down "
-                                                        "projection's output summed per token "
-                                                        "(expert rows, expert rank)",
-                            "expertwise_per_expert_launch": "expert-wise LoRA with one permutation "
-                                                            "and one fwd/bwd call per expert (the "
-                                                            "baseline's launch pattern)"}[kind]}
+                   "what": EXTRA_WHAT[kind]}
             for kind in res if kind not in ("ace", "lora")},
         "ms_std": {kind: res[kind]["ms_std"] for kind in res},
     }
@@ -994,14 +1010,138 @@ def main():
         # against the launch pattern of the paper's baseline (one call per expert)
         line["speedup_vs_expertwise_per_expert_launch"] = (
             res["expertwise_per_expert_launch"]["ms"] / ace_ms)
+    del m
+    torch.cuda.empty_cache()
+    if not args.no_all_configs:
+        # every workload of the suite, both steps on the same GPU in the same run
+        allc = {}
+        for name in W.CONFIG_ORDER:
+            if name == cfg.name:
+                allc[name] = config_row(cfg, rt, res, None)
+                continue
+            c2 = W.CONFIGS[name]
+            m2 = measure_config(ace, c2, args.seed, max(10, args.steps // 3), max(5, args.warmup // 2),
+                                3, extras=False)
+            allc[name] = config_row(c2, m2["rt"], m2["res"], m2["step_bytes"])
+            del m2
+            torch.cuda.empty_cache()
+        line["configs"] = allc
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(cfg, rt)
     if not args.no_fused:
-        line["fused_projection"] = fused_projection_bench(ace, cfg, rt, args.seed,
-                                                          cpu=not args.no_cpu_baseline)
-    if not args.no_consolidation and cfg.dtype == "bf16":
-        line["consolidation"] = consolidation_bench(ace, cfg, args.seed, cpu=not args.no_cpu_baseline)
+        line["fused_projection"] = fused_projection_bench(ace, side_cfg,
+                                                          W.make_routing(side_cfg, args.seed),
+                                                          args.seed, cpu=not args.no_cpu_baseline)
+    if not args.no_consolidation and side_cfg.dtype == "bf16":
+        line["consolidation"] = consolidation_bench(ace, side_cfg, args.seed,
+                                                    cpu=not args.no_cpu_baseline)
     print(json.dumps(line), flush=True)
+
+
+EXTRA_WHAT = {
+    "consolidated": "group-rank adapters on gate/up run per routed pair (no compute-once), "
+                    "expert-wise down",
+    "consolidated_down": "ace step with the down projection at group rank over pair rows",
+    "combined_down": "ace step with the down projection pre-combined: output summed per token "
+                     "with the routing weights, one group-rank row per (token, active group)",
+    "combined_down_expertwise": "expert-wise step with the down projection's output summed per "
+                                "token (expert rows, expert rank)",
+    "expertwise_per_expert_launch": "expert-wise LoRA with one permutation and one fwd/bwd call "
+                                    "per expert (the baseline's launch pattern)",
+}
+
+
+def workload_name(cfg, rt):
+    return (f"{cfg.name}: T={cfg.T} d_model={cfg.d_model} d_ffn={cfg.d_ffn} "
+            f"E={cfg.E} top-{cfg.k} routing={cfg.routing[0]}({cfg.routing[1]}) "
+            f"G={rt.G} expert rank {cfg.r_e} -> group ranks "
+            f"{sorted(set(int(r) for r in rt.group_rank))}; "
+            f"LoRA on {'/'.join(cfg.projections)}; grouped gate/up, expert-wise down")
+
+
+def build_paths(ace, cfg, rt, seed, extras):
+    """Buffers and the Path objects of one workload (ace and lora, plus the
+    labelled extra rows)."""
+    import torch
+    bufs = make_buffers(cfg, rt, seed)
+    n_keys = max(cfg.E, rt.G)
+    # room for a group-keyed and an expert-keyed routing written by one call
+    ws_perm = torch.empty(max(256, ace.ace_workspace_bytes(ace.ACE_OP_PERMUTE, cfg.T, cfg.k, 0, 0,
+                                                            rt.G, 0)
+                              + ace.ace_workspace_bytes(ace.ACE_OP_PERMUTE, cfg.T, cfg.k, 0, 0,
+                                                        n_keys, 0)),
+                          dtype=torch.uint8, device="cuda")
+    need = 0
+    for proj in cfg.projections:
+        d_in, d_out, _ = cfg.proj_dims(proj)
+        for nk, r in ((rt.G, int(rt.group_rank.max())), (cfg.E, cfg.r_e)):
+            need = max(need, ace.ace_workspace_bytes(ace.ACE_OP_BWD, cfg.T, cfg.k, d_in, d_out, nk, r))
+    ws_bwd = torch.empty(need, dtype=torch.uint8, device="cuda")
+    kinds = ("ace", "lora") if not extras else (
+        "ace", "lora", "consolidated", "consolidated_down", "combined_down",
+        "combined_down_expertwise")
+    paths = {kind: Path(ace, cfg, rt, kind, bufs, ws_perm, ws_bwd) for kind in kinds}
+    paths["_bufs"] = bufs
+    return paths
+
+
+def measure_config(ace, cfg, seed, steps, warmup, repeats, extras):
+    """Times the ace and lora steps of one workload (and the extra rows):
+    per-step medians without events, per-call medians with events."""
+    rt = W.make_routing(cfg, seed)
+    paths = build_paths(ace, cfg, rt, seed, extras)
+    bufs = paths.pop("_bufs")
+    res = {}
+    if extras:
+        # launch-bound: a few steps suffice
+        pe = PerExpertPath(ace, cfg, rt, bufs)
+        per_step, _ = time_path(pe, max(2, steps // 20), 2, 2)
+        res["expertwise_per_expert_launch"] = dict(ms=statistics.median(per_step),
+                                                   ms_std=statistics.pstdev(per_step),
+                                                   ms_with_events=statistics.median(per_step),
+                                                   phases={})
+        del pe
+    for kind, path in paths.items():
+        per_step, phases = time_path(path, steps, warmup, repeats)
+        plain = time_plain(path, steps, repeats)
+        res[kind] = dict(ms=statistics.median(plain), ms_std=statistics.pstdev(plain),
+                         ms_with_events=statistics.median(per_step), phases=phases)
+    # algorithmic bytes of a step and of each call (proj.fwd / proj.bwd)
+    b = 2 if cfg.dtype == "bf16" else 4
+    step_bytes = 0
+    call_bytes = {}
+    for proj in cfg.projections:
+        d_in, d_out, im = cfg.proj_dims(proj)
+        f, bb = algo_bytes(im == W.INPUT_SHARED, cfg.T, cfg.P, d_in, d_out, cfg.E * cfg.r_e, b)
+        step_bytes += f + bb
+        call_bytes[f"{proj}.fwd"], call_bytes[f"{proj}.bwd"] = f, bb
+    call_roofline = {
+        kind: {k: call_bytes[k] / (res[kind]["phases"][k] * 1e-3) / (HBM_PEAK_GBS * 1e9)
+               for k in call_bytes}
+        for kind in ("ace", "lora")}
+    return {"rt": rt, "res": res, "step_bytes": step_bytes, "call_bytes": call_bytes,
+            "call_roofline": call_roofline}
+
+
+def config_row(cfg, rt, res, step_bytes):
+    """One workload's entry of the all-configurations table."""
+    if step_bytes is None:
+        b = 2 if cfg.dtype == "bf16" else 4
+        step_bytes = 0
+        for proj in cfg.projections:
+            d_in, d_out, im = cfg.proj_dims(proj)
+            f, bb = algo_bytes(im == W.INPUT_SHARED, cfg.T, cfg.P, d_in, d_out, cfg.E * cfg.r_e, b)
+            step_bytes += f + bb
+    a, l = res["ace"]["ms"], res["lora"]["ms"]
+    peak = HBM_PEAK_GBS * 1e9
+    return {"workload": workload_name(cfg, rt), "ace_ms": a, "expertwise_ms": l,
+            "speedup_vs_expertwise": l / a, "value": cfg.P / (a * 1e-3),
+            "expertwise_value": cfg.P / (l * 1e-3), "unit": "routed tokens/s",
+            "step_roofline_frac_ace": step_bytes / (a * 1e-3) / peak,
+            "step_roofline_frac_expertwise": step_bytes / (l * 1e-3) / peak,
+            "algorithmic_bytes": step_bytes,
+            "phases_ms": {k: {"ace": res["ace"]["phases"].get(k), "lora": res["lora"]["phases"].get(k)}
+                          for k in sorted(set(res["ace"]["phases"]) | set(res["lora"]["phases"]))}}
 
 
 if __name__ == "__main__":
