@@ -14,10 +14,10 @@
 //     consecutive threads per 256-byte row piece; up to kPrefetch per
 //     thread), which are in flight during the matrix work;
 //   - each wave multiplies its two 16-column blocks of W against the four
-//     16-row blocks of H on the matrix cores and writes C to LDS (in the
-//     output precision);
-//   - the threads add w * C to their y pieces and store them (items with
-//     more pieces take further batches of loads).
+//     16-row blocks of H on the matrix cores and writes C to LDS in fp32;
+//   - the threads add w * C to their y pieces and store them, so y is
+//     rounded once per call (items with more pieces take further batches of
+//     loads).
 // The y pieces held across the matrix work cost occupancy and save the
 // latency of a round trip to the memory per item (six pieces per thread
 // measured best: 64-pair items of a 128-column chunk need four, rows that
@@ -44,14 +44,16 @@ __global__ __launch_bounds__(kThreads) void expand_kernel(ExpandArgs a) {
   constexpr int PER = Tr<T>::PER, KB = Tr<T>::KB, APF = Tr<T>::APF;
   constexpr int NM = RB / APF;
   constexpr int PPR = kChunk / PER;     // 16-byte pieces per pair per item
-  constexpr int CST = kChunk + 16 / (int)sizeof(T);  // LDS row stride of C (elements)
-  __shared__ __attribute__((aligned(16))) T Cs[kBM * CST];
+  constexpr int CST = kChunk + 4;       // LDS row stride of C (fp32)
   // bf16 at 64 ranks or more: the tile's H rows are loaded once into LDS and
   // every wave reads its fragments there (rows 16 bytes longer than the ranks,
-  // so the 16 rows of a fragment read spread over the banks)
+  // so the 16 rows of a fragment read spread over the banks); H is read into
+  // registers before C is written, so both share one buffer
   constexpr bool HLDS = std::is_same<T, __bf16>::value && RB >= 4;
   constexpr int HST = HLDS ? NM * KB + 8 : 8;   // LDS row stride of H (elements)
-  __shared__ __attribute__((aligned(16))) T Hs[HLDS ? kBM * HST : 8];
+  static_assert(kBM * HST * sizeof(T) <= kBM * CST * sizeof(float), "H staging exceeds the C buffer");
+  __shared__ __attribute__((aligned(16))) float Cs[kBM * CST];
+  T* const Hs = reinterpret_cast<T*>(Cs);
   __shared__ uint16_t plist[kBM * kMaxK];  // (row << 5) | slot
   __shared__ int toks[kBM];
   __shared__ int npairs_s;
@@ -114,11 +116,15 @@ __global__ __launch_bounds__(kThreads) void expand_kernel(ExpandArgs a) {
 #pragma unroll
     for (int pf = 0; pf < kPrefetch; ++pf) {
       if (base + pf * kThreads < nitems && po[pf] >= 0) {
-        float o[PER], cv[PER];
+        float o[PER];
         Tr<T>::to_f32(yv[pf], o);
-        Tr<T>::to_f32(*reinterpret_cast<const F*>(&Cs[co[pf]]), cv);
+        const float* cp = &Cs[co[pf]];
 #pragma unroll
-        for (int e2 = 0; e2 < PER; ++e2) o[e2] += wv[pf] * cv[e2];
+        for (int e2 = 0; e2 < PER; e2 += 4) {
+          const f32x4 cv = *reinterpret_cast<const f32x4*>(cp + e2);
+#pragma unroll
+          for (int v = 0; v < 4; ++v) o[e2 + v] += wv[pf] * cv[v];
+        }
         const int pc = ((base + tid + pf * kThreads) % PPR) * PER;
         Tr<T>::store_nt(O + (size_t)po[pf] * n_out + n0 + pc, Tr<T>::from_f32(o));
       }
@@ -177,6 +183,7 @@ __global__ __launch_bounds__(kThreads) void expand_kernel(ExpandArgs a) {
         }
       }
     }
+    if constexpr (HLDS) __syncthreads();  // every wave holds its H fragments; C reuses the buffer
 #pragma unroll
     for (int bi = 0; bi < kBPW; ++bi) {
       const int b = wave * kBPW + bi;
@@ -186,9 +193,7 @@ __global__ __launch_bounds__(kThreads) void expand_kernel(ExpandArgs a) {
 #pragma unroll
         for (int m = 0; m < NM; ++m)
           if (m < nmb) c = Tr<T>::mma(wf[bi][m], hf[jb][m], c);  // C[u][n0+16b+4g+v]
-        T* cp = &Cs[(16 * jb + c16) * CST + 16 * b + 4 * g];
-#pragma unroll
-        for (int v = 0; v < 4; ++v) cp[v] = (T)c[v];
+        *reinterpret_cast<f32x4*>(&Cs[(16 * jb + c16) * CST + 16 * b + 4 * g]) = c;
       }
     }
   }

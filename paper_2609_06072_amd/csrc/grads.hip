@@ -40,7 +40,8 @@ constexpr int kColBlk = kGradColBlk;   // gradient columns per item
 // kSplitRows (which bounds the item count and the partials) and at most
 // kMaxSplit (the LDS row-index table).
 constexpr int kSplitRows = 1024;
-constexpr int kMaxSplit = 2048;
+constexpr int kMaxSplit = 2048;   // the fp32 path's row-index table
+constexpr int kSplit4 = 4096;     // bf16 path only (its row-index table is per instantiation)
 
 // Item table shared by the gradient kernels.  For key q the dB contraction
 // runs over bseg[q] .. bseg[q+1] and the dA contraction over aseg[q] ..
@@ -975,7 +976,8 @@ template <int RB>
 hipError_t launch_grads_rb(int dtype, GradArgs g, long P, hipStream_t stream) {
   if (g.phase != 0 && dtype != ACE_BF16) return hipErrorInvalidValue;
   if (g.split == 0) g.split = kSplitRows;
-  if (g.split != kSplitRows && g.split != kMaxSplit) return hipErrorInvalidValue;
+  if (g.split != kSplitRows && g.split != kMaxSplit && !(g.split == kSplit4 && dtype == ACE_BF16))
+    return hipErrorInvalidValue;
   const int nb = g.nbB + g.nbA;
   const long items = ((P + kSplitRows - 1) / kSplitRows + g.keys.n_keys) * nb;
   g.itab = reinterpret_cast<int32_t*>(static_cast<char*>(g.part) +
@@ -984,7 +986,8 @@ hipError_t launch_grads_rb(int dtype, GradArgs g, long P, hipStream_t stream) {
   const int grid = (int)(items < cap ? items : cap);
   if (grid > 0) {
     if (dtype == ACE_BF16) {
-      if (g.split == kMaxSplit) grad_dma_kernel<RB, kMaxSplit><<<grid, kThreads, 0, stream>>>(g);
+      if (g.split == kSplit4) grad_dma_kernel<RB, kSplit4><<<grid, kThreads, 0, stream>>>(g);
+      else if (g.split == kMaxSplit) grad_dma_kernel<RB, kMaxSplit><<<grid, kThreads, 0, stream>>>(g);
       else grad_dma_kernel<RB, kSplitRows><<<grid, kThreads, 0, stream>>>(g);
     }
     else grad_reg_kernel<RB><<<grid, kThreads, 0, stream>>>(g);

@@ -450,6 +450,20 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
   const bool long_keys = (long)p.T * p.k >= 1024L * n_keys;
   gr.split = (p.dtype == ACE_BF16 && !p.per_pair && rank_blocks(p.r_max) <= 2 && long_keys) ? 2048
                                                                                             : 1024;
+  // Shared input at ranks above 32 with many gradient column blocks (wide
+  // projections): the split partials grow with the rank and the number of
+  // chunks, so take the longest chunks that still leave at least four items
+  // per CU (at these ranks the block's LDS already allows two per CU, so the
+  // larger row-index table costs no occupancy)
+  if (p.dtype == ACE_BF16 && !p.per_pair && rank_blocks(p.r_max) == 4) {
+    const long nb = (p.d_out + kGradColBlk - 1) / kGradColBlk + (p.d_in + kGradColBlk - 1) / kGradColBlk;
+    const long want = 4L * device_cu_count();
+    for (int sp : {4096, 2048})
+      if ((long)p.T * p.k / sp * nb >= want) {
+        gr.split = sp;
+        break;
+      }
+  }
   // Per-pair input at small ranks (bf16): the dB pass reads dY once and also
   // contracts it against B^T per 128-column block (fp32 partials); dH per row
   // is their sum, then the dA pass (x per pair from HBM).  Otherwise dH by a

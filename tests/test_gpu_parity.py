@@ -371,6 +371,34 @@ def test_accumulates_into_existing_outputs(path):
     check_rel("dx_in + dx", f64(out["dx"]), f64(dx0) + dx, TOL["bf16"])
 
 
+@pytest.mark.parametrize("name", ["mixtral_bf16", "qwen_bf16"])
+def test_accumulates_full_size_weighted(name):
+    """Full-size grouped forward with pair weights into y_in ~ N(0, 1) (rows
+    that serve several slots add w * C once per slot).  Every sampled element
+    of y_out must lie within half a bf16 ulp of fp64(y_in) + delta (the one
+    rounding of the sum), plus 2% of the row's largest |delta| (the bf16
+    rounding of h between the two contractions), and every row must pass the
+    relative-L2 bound."""
+    cfg = W.CONFIGS[name]
+    c = make_case(cfg, "grouped", seed=3, with_w=True)
+    y0 = W.draw_tensor((cfg.P, c.d_out), 1.0, 3, "y_in", "bf16", "cuda")
+    say(f"full-size accumulate {name} T={cfg.T} d_out={c.d_out}")
+    out = run_gpu(c, bwd=False, y_in=y0)
+    rng = np.random.default_rng(5)
+    toks = np.sort(rng.choice(cfg.T, size=32, replace=False))
+    ids, x, w = _sub_tokens(c, toks)
+    a, _ = oracle_args(c, ids=ids, x=x)
+    delta = O.lora_delta(*a, input_mode=c.input_mode, pair_w=w)
+    rows = torch.as_tensor((toks[:, None] * cfg.k + np.arange(cfg.k)[None, :]).ravel(), device="cuda")
+    ref = f64(y0[rows]) + delta
+    got = f64(out["y"][rows])
+    check_all("y_in + delta (sampled tokens)", got, ref, TOL["bf16"])
+    ulp = np.exp2(np.floor(np.log2(np.maximum(np.abs(ref), 1e-30))) - 7)
+    bound = 0.5 * ulp + 0.02 * np.abs(delta).max(axis=1, keepdims=True) + 1e-7
+    worst = float(np.max(np.abs(got - ref) / bound))
+    assert worst <= 1.0, f"an element is {worst:.2f}x the rounding bound"
+
+
 @pytest.mark.parametrize("path", ["grouped", "combined"])
 def test_empty_input(path):
     cfg = SMALL["olmoe_bf16"].scaled(T=0)
