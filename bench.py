@@ -384,6 +384,28 @@ def copy_peak_gbs(nbytes=1 << 30, reps=20):
     return 2.0 * nbytes / (statistics.median(ts) * 1e-3) / 1e9
 
 
+def rmw_peak_gbs(nbytes=1 << 30, reps=20):
+    """HBM bandwidth of an in-place read-modify-write (x += 1 over nbytes of
+    bf16, the access pattern of y += delta), median of reps, bytes read plus
+    bytes written."""
+    import torch
+    x = torch.zeros(nbytes // 2, dtype=torch.bfloat16, device="cuda")
+    for _ in range(3):
+        x.add_(1.0)
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(reps):
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        x.add_(1.0)
+        e.record()
+        torch.cuda.synchronize()
+        ts.append(s.elapsed_time(e))
+    del x
+    torch.cuda.empty_cache()
+    return 2.0 * nbytes / (statistics.median(ts) * 1e-3) / 1e9
+
+
 # ---------------------------------------------------------------- consolidation
 # The one-time consolidation step of Sec. 3.3 on one layer: pairwise CKA of
 # the expert adapters on the probe set (GPU), similarity graph + Louvain +
@@ -698,11 +720,16 @@ def pmc_summary(fetch_dir, write_dir, labels_path, config, command):
              f"calibration copy of {CALIB_BYTES} B: FETCH_SIZE {cal_f:.0f} B, WRITE_SIZE {cal_w:.0f} B"
              f" -> scale fetch {kf:.4f}, write {kw:.4f}",
              "# phase  fetch_bytes  write_bytes  (scaled)  kernels"]
+    per_kernel = []
     for lab in labels[1:]:
         fb = sum(v for _, v in f[lab]) * 1024 * kf
         wb = sum(v for _, v in w[lab]) * 1024 * kw
         names = ",".join(short_kernel(n) for n, _ in f[lab])
         lines.append(f"{lab} {fb:.0f} {wb:.0f} {names}")
+        for (n, fv), (_, wv) in zip(f[lab], w[lab]):
+            per_kernel.append(f"k {lab} {short_kernel(n)} {fv * 1024 * kf:.0f} {wv * 1024 * kw:.0f}")
+    lines.append("# per kernel, in launch order:  k  phase  kernel  fetch_bytes  write_bytes  (scaled)")
+    lines += per_kernel
     os.makedirs(PROFILES, exist_ok=True)
     with open(traffic_file(config), "w") as out:
         out.write("\n".join(lines) + "\n")
@@ -849,6 +876,30 @@ def stats_summary(trace_dir, name, command,
     print("\n".join(lines))
 
 
+def configs_summary(json_path: str, command: str):
+    """profiles/bench_all_configs.txt from one bench line (the `configs` object:
+    every workload's ACE and expert-wise steps, measured in the same run)."""
+    d = json.loads([l for l in open(json_path) if l.strip().startswith("{")][-1])
+    lines = ["# bench line per configuration (ACE step vs expert-wise step, same GPU, same run)",
+             f"source_hash {source_hash()}", f"command {command}",
+             f"# measured references: plain copy {d['step_roofline'].get('measured_copy_GBps', 0):.0f} GB/s, "
+             f"in-place read-modify-write {d['step_roofline'].get('measured_rmw_GBps', 0):.0f} GB/s",
+             "# config  ace_ms  expertwise_ms  speedup  ace_pairs_per_s  step_frac_ace  step_frac_expertwise"]
+    for name, c in d["configs"].items():
+        lines.append(f"{name} {c['ace_ms']:.4f} {c['expertwise_ms']:.4f} {c['speedup_vs_expertwise']:.3f} "
+                     f"{c['value']:.4g} {c['step_roofline_frac_ace']:.3f} "
+                     f"{c['step_roofline_frac_expertwise']:.3f}")
+    lines.append("# phases (ms per call): config phase ace expertwise")
+    for name, c in d["configs"].items():
+        for ph, v in sorted(c["phases_ms"].items()):
+            a, l = v.get("ace"), v.get("lora")
+            lines.append(f"{name} {ph} {'-' if a is None else f'{a:.4f}'} {'-' if l is None else f'{l:.4f}'}")
+    os.makedirs(PROFILES, exist_ok=True)
+    with open(os.path.join(PROFILES, "bench_all_configs.txt"), "w") as out:
+        out.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def read_traffic(config: str):
     """{phase label: (fetch, write)} if the stored counters were taken on the
     current sources, else None."""
@@ -894,6 +945,8 @@ def main():
                     help="skip the consolidation step (CKA, grouping, consolidated adapters)")
     ap.add_argument("--consolidation-only", action="store_true",
                     help="time only the consolidation step and print its object")
+    ap.add_argument("--configs-summary", metavar="BENCH_JSON",
+                    help="write profiles/bench_all_configs.txt from a bench line and exit")
     ap.add_argument("--summary-name", default=None,
                     help="file name stem of an unlabeled --mfma-summary (profiles/mfma_<NAME>.txt)")
     ap.add_argument("--no-fused", action="store_true",
@@ -907,6 +960,9 @@ def main():
         return
     if args.trace_summary:
         trace_summary(*args.trace_summary, args.config, args.pmc_command)
+        return
+    if args.configs_summary:
+        configs_summary(args.configs_summary, args.pmc_command)
         return
     if args.stats_summary:
         stats_summary(*args.stats_summary, args.pmc_command)
@@ -948,6 +1004,7 @@ def main():
         return
 
     copy_gbs = copy_peak_gbs()
+    rmw_gbs = rmw_peak_gbs()
     m = measure_config(ace, cfg, args.seed, args.steps, args.warmup, args.repeats,
                        extras=not args.no_extras)
     res, rt = m["res"], m["rt"]
@@ -991,12 +1048,15 @@ def main():
                           "frac_ace": m["step_bytes"] / (ace_ms * 1e-3) / (HBM_PEAK_GBS * 1e9),
                           "frac_expertwise": m["step_bytes"] / (lora_ms * 1e-3) / (HBM_PEAK_GBS * 1e9),
                           "measured_copy_GBps": copy_gbs,
-                          "frac_ace_of_copy": m["step_bytes"] / (ace_ms * 1e-3) / (copy_gbs * 1e9)},
+                          "frac_ace_of_copy": m["step_bytes"] / (ace_ms * 1e-3) / (copy_gbs * 1e9),
+                          "measured_rmw_GBps": rmw_gbs,
+                          "frac_ace_of_rmw": m["step_bytes"] / (ace_ms * 1e-3) / (rmw_gbs * 1e9)},
         "roofline": {"bound": "hbm", "kernel": f"{entry} ({proj}): all kernels of one call",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": dom_traffic,
                      "algorithmic_bytes": call_bytes[dom], "ms_per_call": dom_ms,
-                     "measured_copy_GBps": copy_gbs, "frac_of_copy": achieved / copy_gbs},
+                     "measured_copy_GBps": copy_gbs, "frac_of_copy": achieved / copy_gbs,
+                     "measured_rmw_GBps": rmw_gbs, "frac_of_rmw": achieved / rmw_gbs},
         "call_roofline_frac": m["call_roofline"],
         "phases_ms": {k: {kind: res[kind]["phases"].get(k) for kind in res}
                       for k in sorted(set().union(*(set(r["phases"]) for r in res.values())))},
