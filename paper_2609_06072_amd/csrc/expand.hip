@@ -91,23 +91,34 @@ __global__ __launch_bounds__(kThreads) void expand_kernel(ExpandArgs a) {
   }
   __syncthreads();  // plist, toks published
   const int nitems = npairs_s * PPR;
+  if (nitems == 0) return;  // block-uniform (a row serves at least one slot)
   F yv[kPrefetch];
   float wv[kPrefetch];
   int po[kPrefetch], co[kPrefetch];
-  auto issue_batch = [&](int base) {
+  // Slot pf of the batch at base: piece base + tid + pf * kThreads (pieces past
+  // the item re-read the item's last piece, pieces past n_out read y[0]; po =
+  // -1 marks both as not stored).  Returns the pair.
+  auto locate = [&](int base, int pf) {
+    const int it = base + tid + pf * kThreads;
+    const bool ok = it < nitems;
+    const int itc = ok ? it : nitems - 1;
+    const int pc = (itc % PPR) * PER;
+    const int ent = plist[itc / PPR];
+    const int p = toks[ent >> 5] * k + (ent & 31);
+    po[pf] = ok && n0 + pc < n_out ? p : -1;
+    co[pf] = (ent >> 5) * CST + pc;
+    return p;
+  };
+  auto y_at = [&](int base, int pf) {
+    const int pc = ((base + tid + pf * kThreads) % PPR) * PER;
+    return O + (po[pf] >= 0 ? (size_t)po[pf] * n_out + n0 + pc : 0);
+  };
+  auto issue_batch = [&](int base) {   // later batches (items with many pairs)
 #pragma unroll
     for (int pf = 0; pf < kPrefetch; ++pf) {
       if (base + pf * kThreads < nitems) {  // block-uniform
-        const int it = base + tid + pf * kThreads;
-        const bool ok = it < nitems;
-        const int e = (ok ? it : nitems - 1) / PPR;
-        const int pc = (it % PPR) * PER;
-        const int ent = plist[e];
-        const int p = toks[ent >> 5] * k + (ent & 31);
-        const bool cok = ok && n0 + pc < n_out;
-        po[pf] = cok ? p : -1;
-        co[pf] = (ent >> 5) * CST + pc;
-        yv[pf] = Tr<T>::load_nt(O + (cok ? (size_t)p * n_out + n0 + pc : 0));  // clamped, unconditional
+        const int p = locate(base, pf);
+        yv[pf] = Tr<T>::load_nt(y_at(base, pf));
         wv[pf] = a.pair_w ? a.pair_w[p] : 1.f;
       }
     }
@@ -125,76 +136,102 @@ __global__ __launch_bounds__(kThreads) void expand_kernel(ExpandArgs a) {
 #pragma unroll
           for (int v = 0; v < 4; ++v) o[e2 + v] += wv[pf] * cv[v];
         }
-        const int pc = ((base + tid + pf * kThreads) % PPR) * PER;
-        Tr<T>::store_nt(O + (size_t)po[pf] * n_out + n0 + pc, Tr<T>::from_f32(o));
+        Tr<T>::store_nt(y_at(base, pf), Tr<T>::from_f32(o));
       }
     }
   };
-  issue_batch(0);   // in flight during the matrix work
 
+  // First batch.  Loads return in order, so the small operands (pair
+  // weights, H, W: cache hits) are issued before the y pieces (HBM): the
+  // matrix work then runs while the y pieces are in flight.  Every load of
+  // this batch is unconditional, so that the waits for H and W count exactly
+  // the y loads behind them.
+  {
+    int pp[kPrefetch];
+#pragma unroll
+    for (int pf = 0; pf < kPrefetch; ++pf) pp[pf] = locate(0, pf);
+    if (a.pair_w) {  // block-uniform, before H and W
+#pragma unroll
+      for (int pf = 0; pf < kPrefetch; ++pf) wv[pf] = a.pair_w[pp[pf]];
+    } else {
+#pragma unroll
+      for (int pf = 0; pf < kPrefetch; ++pf) wv[pf] = 1.f;
+    }
+  }
+  constexpr int PPRH = NM * KB / PER;   // 16-byte pieces per H row
+  constexpr int HN = HLDS ? kBM * PPRH / kThreads : 1;
+  static_assert(!HLDS || (kBM * PPRH) % kThreads == 0, "H pieces per thread");
+  F hv[HN];
+  F hf[4][NM];
   if constexpr (HLDS) {
     // 64 rows x NM*KB ranks in 16-byte pieces (rows past the segment re-read
     // the last row)
-    constexpr int PPRH = NM * KB / PER;
 #pragma unroll
-    for (int i = tid; i < kBM * PPRH; i += kThreads) {
-      const int rr = i / PPRH, pc = (i % PPRH) * PER;
-      const int u = min(u0 + rr, u_end - 1);
-      Tr<T>::store(&Hs[rr * HST + pc], Tr<T>::load(H + (size_t)u * a.rpad + pc));
+    for (int i = 0; i < HN; ++i) {
+      const int j = tid + i * kThreads;
+      const int u = min(u0 + j / PPRH, u_end - 1);
+      hv[i] = Tr<T>::load(H + (size_t)u * a.rpad + (j % PPRH) * PER);
     }
-    __syncthreads();
-  }
-  {
+  } else {
     // H fragments of the four row blocks (rows past the segment re-read the
     // last row; nothing is stored for them)
-    F hf[4][NM];
 #pragma unroll
     for (int jb = 0; jb < 4; ++jb) {
-      if constexpr (HLDS) {
+      const int u = min(u0 + 16 * jb + c16, u_end - 1);
+      const T* hr = H + (size_t)u * a.rpad + PER * g;
 #pragma unroll
-        for (int m = 0; m < NM; ++m) hf[jb][m] = Tr<T>::load(&Hs[(16 * jb + c16) * HST + KB * m + PER * g]);
+      for (int m = 0; m < NM; ++m) hf[jb][m] = Tr<T>::load(hr + KB * m);
+    }
+  }
+  // W fragments of this wave's column blocks (rows past n_out re-read the
+  // last row; rank columns past r_q meet zeros in H)
+  const T* Wq = W + (size_t)a.w_key_mul * roff;
+  const int ldw = a.w_stride_is_rank ? r_q : R;
+  // 16-byte loads need aligned rows; clamping a fragment that starts past
+  // r_q back to r_q - PER only keeps every valid rank in place when r_q is a
+  // multiple of PER
+  const bool vec = (ldw % PER) == 0 && ((size_t)a.w_key_mul * roff) % PER == 0 && (r_q % PER) == 0;
+  F wf[kBPW][NM];
+#pragma unroll
+  for (int bi = 0; bi < kBPW; ++bi) {
+    const int nrow = min(n0 + 16 * (wave * kBPW + bi) + c16, n_out - 1);
+    const T* wr = Wq + (size_t)nrow * ldw;
+#pragma unroll
+    for (int m = 0; m < NM; ++m) {
+      const int r0 = KB * m + PER * g;
+      if (vec) {
+        wf[bi][m] = Tr<T>::load(wr + min(r0, r_q - PER));
       } else {
-        const int u = min(u0 + 16 * jb + c16, u_end - 1);
-        const T* hr = H + (size_t)u * a.rpad + PER * g;
-#pragma unroll
-        for (int m = 0; m < NM; ++m) hf[jb][m] = Tr<T>::load(hr + KB * m);
+        wf[bi][m] = (m < nmb && r0 < r_q) ? load_frag<T>(wr + r0, r_q - r0, false) : Tr<T>::zero();
       }
     }
-    // W fragments of this wave's column blocks (rows past n_out re-read the
-    // last row; rank columns past r_q meet zeros in H)
-    const T* Wq = W + (size_t)a.w_key_mul * roff;
-    const int ldw = a.w_stride_is_rank ? r_q : R;
-    // 16-byte loads need aligned rows; clamping a fragment that starts past
-    // r_q back to r_q - PER only keeps every valid rank in place when r_q is a
-    // multiple of PER
-    const bool vec = (ldw % PER) == 0 && ((size_t)a.w_key_mul * roff) % PER == 0 && (r_q % PER) == 0;
-    F wf[kBPW][NM];
+  }
 #pragma unroll
-    for (int bi = 0; bi < kBPW; ++bi) {
-      const int nrow = min(n0 + 16 * (wave * kBPW + bi) + c16, n_out - 1);
-      const T* wr = Wq + (size_t)nrow * ldw;
+  for (int pf = 0; pf < kPrefetch; ++pf) yv[pf] = Tr<T>::load_nt(y_at(0, pf));
+
+  if constexpr (HLDS) {
 #pragma unroll
-      for (int m = 0; m < NM; ++m) {
-        const int r0 = KB * m + PER * g;
-        if (vec) {
-          wf[bi][m] = Tr<T>::load(wr + min(r0, r_q - PER));
-        } else {
-          wf[bi][m] = (m < nmb && r0 < r_q) ? load_frag<T>(wr + r0, r_q - r0, false) : Tr<T>::zero();
-        }
-      }
+    for (int i = 0; i < HN; ++i) {
+      const int j = tid + i * kThreads;
+      Tr<T>::store(&Hs[(j / PPRH) * HST + (j % PPRH) * PER], hv[i]);
     }
-    if constexpr (HLDS) __syncthreads();  // every wave holds its H fragments; C reuses the buffer
+    __syncthreads();
 #pragma unroll
-    for (int bi = 0; bi < kBPW; ++bi) {
-      const int b = wave * kBPW + bi;
+    for (int jb = 0; jb < 4; ++jb)
 #pragma unroll
-      for (int jb = 0; jb < 4; ++jb) {
-        f32x4 c = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int m = 0; m < NM; ++m) hf[jb][m] = Tr<T>::load(&Hs[(16 * jb + c16) * HST + KB * m + PER * g]);
+    __syncthreads();  // every wave holds its H fragments; C reuses the buffer
+  }
 #pragma unroll
-        for (int m = 0; m < NM; ++m)
-          if (m < nmb) c = Tr<T>::mma(wf[bi][m], hf[jb][m], c);  // C[u][n0+16b+4g+v]
-        *reinterpret_cast<f32x4*>(&Cs[(16 * jb + c16) * CST + 16 * b + 4 * g]) = c;
-      }
+  for (int bi = 0; bi < kBPW; ++bi) {
+    const int b = wave * kBPW + bi;
+#pragma unroll
+    for (int jb = 0; jb < 4; ++jb) {
+      f32x4 c = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int m = 0; m < NM; ++m)
+        if (m < nmb) c = Tr<T>::mma(wf[bi][m], hf[jb][m], c);  // C[u][n0+16b+4g+v]
+      *reinterpret_cast<f32x4*>(&Cs[(16 * jb + c16) * CST + 16 * b + 4 * g]) = c;
     }
   }
   __syncthreads();  // C is published

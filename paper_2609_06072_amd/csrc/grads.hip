@@ -19,9 +19,10 @@
 // directly, otherwise every chunk writes a partial and grad_reduce_kernel sums
 // them in chunk order (deterministic).
 //
-// bf16 (grad_dma_kernel): the chunk's row indices go to LDS; every stage of 64
-// L rows x 128 columns and the matching S slice are copied global -> LDS with
-// global_load_lds_dwordx4 (no register staging), NBUF stages in flight.  L is
+// bf16 (grad_dma_kernel): every stage of 64 L rows x 128 columns and the
+// matching S slice are copied global -> LDS with global_load_lds_dwordx4 (no
+// register staging), two stages in LDS; the L row indices are fetched one
+// stage ahead into registers (no row-index table in LDS).  L is
 // kept row-major in LDS (16-byte chunks XOR-swizzled by row) and read as MFMA
 // fragments along the contraction index with ds_read_b64_tr_b16: within each
 // 16-lane group, lane i receives element (i & 3) of the 8-byte reads of lanes
@@ -36,12 +37,11 @@ namespace ace {
 namespace {
 
 constexpr int kColBlk = kGradColBlk;   // gradient columns per item
-// Contraction indices per item (split-K chunk): GradArgs::split, at least
-// kSplitRows (which bounds the item count and the partials) and at most
-// kMaxSplit (the LDS row-index table).
+// Contraction indices per item (split-K chunk): GradArgs::split, kSplitRows
+// (which bounds the item count and the partials) or kMaxSplit (the fp32
+// path's LDS row-index table).
 constexpr int kSplitRows = 1024;
-constexpr int kMaxSplit = 2048;   // the fp32 path's row-index table
-constexpr int kSplit4 = 4096;     // bf16 path only (its row-index table is per instantiation)
+constexpr int kMaxSplit = 2048;
 
 // Item table shared by the gradient kernels.  For key q the dB contraction
 // runs over bseg[q] .. bseg[q+1] and the dA contraction over aseg[q] ..
@@ -245,54 +245,42 @@ struct DmaGeo {
 // spreads the 16 rows that one transposed read touches over the banks.
 __device__ inline int l_swz(int r) { return 2 * ((r & 3) | (((r >> 3) & 1) << 2)); }
 
-template <int RB, int SPLIT>
+template <int RB>
 struct DmaSmem {
   __attribute__((aligned(16))) char L[DmaGeo<RB>::NBUF][DmaGeo<RB>::LBYTES];
   __attribute__((aligned(16))) char S[DmaGeo<RB>::NBUF][DmaGeo<RB>::SBYTES];
-  int idx[SPLIT];
   GradTable tb;
+  int scan[kThreads / 64];
 };
 
-// Loads the chunk's L row indices into idx (clamped to the last index): MPT
-// per thread, all loads unconditional so that they are in flight together.
-template <bool ISB, int MPT>
-__device__ inline void load_rows_n(const GradArgs& a, const Item& it, int* idx) {
-  int kabs[MPT], v[MPT];
-#pragma unroll
-  for (int i = 0; i < MPT; ++i)
-    kabs[i] = it.kbase + it.k0 + min((int)threadIdx.x + i * kThreads, it.nk - 1);
+// Where the L row of a contraction index comes from: src0[kabs], or, when
+// slots is set, src0[kabs] * k + (first slot of src1[kabs]) (a row's first
+// pair).  src1 aliases src0 when it is not needed (the load is then unused).
+struct RowSrc {
+  const int32_t* src0;
+  const uint32_t* src1;
+  bool slots;
+};
+
+template <bool ISB>
+__device__ inline RowSrc row_src(const GradArgs& a) {
+  RowSrc r;
   if (a.combined) {   // dB rows: dY of the row's token; dA rows: x of the pair
-#pragma unroll
-    for (int i = 0; i < MPT; ++i) v[i] = ISB ? a.row_token[kabs[i]] : a.plist[kabs[i]];
+    r.src0 = ISB ? a.row_token : a.plist;
+    r.slots = false;
   } else if (ISB && a.plist) {
-#pragma unroll
-    for (int i = 0; i < MPT; ++i) v[i] = a.plist[kabs[i]];
+    r.src0 = a.plist;
+    r.slots = false;
   } else {
-    int tok[MPT];
-    uint32_t sl[MPT];
-#pragma unroll
-    for (int i = 0; i < MPT; ++i) {
-      tok[i] = a.row_token[kabs[i]];
-      sl[i] = a.row_slots[kabs[i]];
-    }
-#pragma unroll
-    for (int i = 0; i < MPT; ++i) {
-      const int p = tok[i] * a.k + (__builtin_ctz(sl[i] | 0x80000000u) & 31);
-      v[i] = (ISB || a.per_pair) ? p : tok[i];
-    }
+    r.src0 = a.row_token;
+    r.slots = ISB || a.per_pair;
   }
-#pragma unroll
-  for (int i = 0; i < MPT; ++i) idx[threadIdx.x + i * kThreads] = v[i];
+  r.src1 = r.slots ? a.row_slots : reinterpret_cast<const uint32_t*>(r.src0);
+  return r;
 }
 
-template <bool ISB, int SPLIT>
-__device__ inline void load_rows(const GradArgs& a, const Item& it, int* idx) {
-  if (it.nk <= 0) return;
-  load_rows_n<ISB, SPLIT / kThreads>(a, it, idx);
-}
-
-template <int RB, int SPLIT, bool ISB, bool DH>
-__device__ __forceinline__ void dma_item(const GradArgs& a, DmaSmem<RB, SPLIT>& sm, const Item& it,
+template <int RB, bool ISB, bool DH>
+__device__ __forceinline__ void dma_item(const GradArgs& a, DmaSmem<RB>& sm, const Item& it,
                                          int item) {
   using G = DmaGeo<RB>;
   constexpr int RS = G::RS, NBUF = G::NBUF;
@@ -307,9 +295,7 @@ __device__ __forceinline__ void dma_item(const GradArgs& a, DmaSmem<RB, SPLIT>& 
   const int col0 = it.cb * kColBlk;
   const int nst = (it.nk + RS - 1) / RS;
 
-  __syncthreads();  // the previous item is done with idx and the buffers
-  load_rows<ISB, SPLIT>(a, it, sm.idx);
-  __syncthreads();
+  __syncthreads();  // the previous item is done with the buffers
 
   const int lrow_in = lane >> 4;   // row inside a 4-row copy
   const int lpos = lane & 15;      // 16-byte position in the LDS row
@@ -319,13 +305,32 @@ __device__ __forceinline__ void dma_item(const GradArgs& a, DmaSmem<RB, SPLIT>& 
   // non-temporal policy: dY (its other reader, the dH contraction, runs
   // before) and per-pair x; shared x rows are gathered again by other keys
   const bool l_last = ISB || a.per_pair;   // block-uniform
+  // Wave w copies stage rows 16w .. 16w+15.  Lane j of the wave loads the row
+  // metadata of stage row 16w + (j & 15) one stage ahead (two loads, kept raw
+  // across the stage so that nothing waits on them early); the row itself is
+  // formed when the copies are issued and handed to the lanes that copy it by
+  // shuffles.  No row-index table in LDS.
+  const RowSrc rs = row_src<ISB>(a);
+  const int kfirst = it.kbase + it.k0;
+  int raw0 = 0;
+  uint32_t raw1 = 0u;
+  auto fetch = [&](int st) {
+    const int kabs = kfirst + min(st * RS + 16 * wave + (lane & 15), it.nk - 1);
+    raw0 = rs.src0[kabs];
+    raw1 = rs.src1[kabs];
+  };
   auto issue = [&](int st) {
     const int b = st % NBUF;
+    const int myrow = rs.slots ? raw0 * a.k + (__builtin_ctz(raw1 | 0x80000000u) & 31) : raw0;
+    int rows[G::NL];
+#pragma unroll
+    for (int i = 0; i < G::NL; ++i) rows[i] = __shfl(myrow, 4 * i + lrow_in, 64);
+    if (st + 1 < nst) fetch(st + 1);   // block-uniform
 #pragma unroll
     for (int i = 0; i < G::NL; ++i) {
       const int r0 = 16 * wave + 4 * i;
       const int r = r0 + lrow_in;                       // row of the stage
-      const int row = sm.idx[min(st * RS + r, it.nk - 1)];
+      const int row = rows[i];
       const int c = lpos ^ l_swz(r);                    // chunk this lane copies
       const int col = min(col0 + 8 * c, ldl - 8);
       const uint32_t ldst = __builtin_amdgcn_readfirstlane(lds_addr(&sm.L[b][r0 * 256]));
@@ -361,14 +366,15 @@ __device__ __forceinline__ void dma_item(const GradArgs& a, DmaSmem<RB, SPLIT>& 
     }
   }
 
-#pragma unroll
-  for (int p = 0; p < NBUF - 1; ++p)
-    if (p < nst) issue(p);
+  static_assert(NBUF == 2, "the row metadata is fetched one stage ahead");
+  if (nst > 0) {
+    fetch(0);
+    issue(0);
+  }
   for (int st = 0; st < nst; ++st) {
-    // this wave's copies of stage st are done once at most the later stages'
-    // copies are outstanding; the barrier then publishes every wave's copies
-    if (NBUF == 3 && st + 1 < nst) wait_vmcnt<G::NL + G::NS>();
-    else wait_vmcnt<0>();
+    // this wave's copies of stage st (and the row metadata of stage st + 1)
+    // are done; the barrier then publishes every wave's copies
+    wait_vmcnt<0>();
     __syncthreads();
     if (st + NBUF - 1 < nst) issue(st + NBUF - 1);
     const int b = st % NBUF;
@@ -431,21 +437,20 @@ __device__ __forceinline__ void dma_item(const GradArgs& a, DmaSmem<RB, SPLIT>& 
   finish_item<RB>(a, it, item, acc);
 }
 
-// SPLIT = a.split (contraction indices per item; sizes the row-index table)
-template <int RB, int SPLIT>
-__global__ __launch_bounds__(kThreads) void grad_dma_kernel(GradArgs a) {
-  __shared__ DmaSmem<RB, SPLIT> sm;
-  build_grad_table(a, sm.tb, sm.idx);
+template <int RB>
+__global__ __launch_bounds__(kThreads, RB <= 4 ? 3 : 1) void grad_dma_kernel(GradArgs a) {
+  __shared__ DmaSmem<RB> sm;
+  build_grad_table(a, sm.tb, sm.scan);
   const int n_keys = a.keys.n_keys;
   const int total = a.phase == 0 ? sm.tb.istart[n_keys] : sm.tb.pstart[n_keys];
   for (int i = blockIdx.x; i < total; i += gridDim.x) {
     const int item = a.phase == 0 ? i : phase_item(a, sm.tb, i);
     const Item it = decode_item(a, sm.tb, item);
     if (it.isB) {
-      if (a.phase == 1) dma_item<RB, SPLIT, true, true>(a, sm, it, item);
-      else dma_item<RB, SPLIT, true, false>(a, sm, it, item);
+      if (a.phase == 1) dma_item<RB, true, true>(a, sm, it, item);
+      else dma_item<RB, true, false>(a, sm, it, item);
     } else {
-      dma_item<RB, SPLIT, false, false>(a, sm, it, item);
+      dma_item<RB, false, false>(a, sm, it, item);
     }
   }
 }
@@ -976,8 +981,7 @@ template <int RB>
 hipError_t launch_grads_rb(int dtype, GradArgs g, long P, hipStream_t stream) {
   if (g.phase != 0 && dtype != ACE_BF16) return hipErrorInvalidValue;
   if (g.split == 0) g.split = kSplitRows;
-  if (g.split != kSplitRows && g.split != kMaxSplit && !(g.split == kSplit4 && dtype == ACE_BF16))
-    return hipErrorInvalidValue;
+  if (g.split != kSplitRows && g.split != kMaxSplit) return hipErrorInvalidValue;
   const int nb = g.nbB + g.nbA;
   const long items = ((P + kSplitRows - 1) / kSplitRows + g.keys.n_keys) * nb;
   g.itab = reinterpret_cast<int32_t*>(static_cast<char*>(g.part) +
@@ -986,9 +990,7 @@ hipError_t launch_grads_rb(int dtype, GradArgs g, long P, hipStream_t stream) {
   const int grid = (int)(items < cap ? items : cap);
   if (grid > 0) {
     if (dtype == ACE_BF16) {
-      if (g.split == kSplit4) grad_dma_kernel<RB, kSplit4><<<grid, kThreads, 0, stream>>>(g);
-      else if (g.split == kMaxSplit) grad_dma_kernel<RB, kMaxSplit><<<grid, kThreads, 0, stream>>>(g);
-      else grad_dma_kernel<RB, kSplitRows><<<grid, kThreads, 0, stream>>>(g);
+      grad_dma_kernel<RB><<<grid, kThreads, 0, stream>>>(g);
     }
     else grad_reg_kernel<RB><<<grid, kThreads, 0, stream>>>(g);
   }

@@ -452,17 +452,12 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
                                                                                             : 1024;
   // Shared input at ranks above 32 with many gradient column blocks (wide
   // projections): the split partials grow with the rank and the number of
-  // chunks, so take the longest chunks that still leave at least four items
-  // per CU (at these ranks the block's LDS already allows two per CU, so the
-  // larger row-index table costs no occupancy)
+  // chunks, so take chunks of 2048 when that still leaves at least four items
+  // per CU (three blocks per CU are resident; 4096 left the last round of
+  // items a third full and measured slower)
   if (p.dtype == ACE_BF16 && !p.per_pair && rank_blocks(p.r_max) == 4) {
     const long nb = (p.d_out + kGradColBlk - 1) / kGradColBlk + (p.d_in + kGradColBlk - 1) / kGradColBlk;
-    const long want = 4L * device_cu_count();
-    for (int sp : {4096, 2048})
-      if ((long)p.T * p.k / sp * nb >= want) {
-        gr.split = sp;
-        break;
-      }
+    if ((long)p.T * p.k / 2048 * nb >= 4L * device_cu_count()) gr.split = 2048;
   }
   // Per-pair input at small ranks (bf16): the dB pass reads dY once and also
   // contracts it against B^T per 128-column block (fp32 partials); dH per row
