@@ -386,7 +386,8 @@ __global__ __launch_bounds__(kThreads) void contract_dma_kernel(ContractArgs a) 
                      seg, bstart, bfirst, scan);
   const int total = bstart[n_keys];
   const int stride = gridDim.x / kXcds;  // the grid is a multiple of kXcds
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // wave-uniform values kept in scalar registers (uniform branches, no exec masks)
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int c16 = lane & 15, g = lane >> 4;
   const __bf16* S = static_cast<const __bf16*>(a.src);
   const __bf16* W = static_cast<const __bf16*>(a.W);
@@ -479,33 +480,49 @@ __global__ __launch_bounds__(kThreads) void contract_dma_kernel(ContractArgs a) 
 #pragma unroll
     for (int p = 0; p < NBUF - 1; ++p)
       if (p < nst) issue(p);
-    for (int st = 0; st < nst; ++st) {
-      // this wave's copies of stage st are done once at most those of the
-      // stages issued after it are outstanding; the barrier publishes them
+    // this wave's copies of stage st are done once at most those of the
+    // stages issued after it are outstanding; the barrier publishes them
+    auto begin_stage = [&](int st) {
       wait_vmcnt_upto<(NBUF - 2) * (G::NS + G::NW)>(min(NBUF - 2, nst - 1 - st) * per_stage);
       __syncthreads();
       if (st + NBUF - 1 < nst) issue(st + NBUF - 1);
+    };
+    // K-block kb of stage st; the ragged form masks the indices past K
+    auto kblock = [&](int st, int kb, bool ragged) {
       const int b = st % NBUF;
+      const int kk = st * KC + kb * KB;
+      const int chunk = kb * 4 + g;
+      const int rl = 16 * wave + c16;
+      bf16x8 sf = *reinterpret_cast<const bf16x8*>(&Sb[b][rl * KC * 2 + ((chunk ^ (rl & (CPR - 1))) << 4)]);
+      if (ragged) {
+        const int nv = K - (kk + 8 * g);
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (e >= nv) sf[e] = (__bf16)0.f;
+      }
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        // weight rows at or past r_q were not copied: their results are zeroed below
+        const int wr = rank_of_row<__bf16>(rb, c16);
+        const bf16x8 wf = *reinterpret_cast<const bf16x8*>(&Wb[b][wr * KC * 2 + ((chunk ^ (wr & (CPR - 1))) << 4)]);
+        acc[rb] = Tr<__bf16>::mma(wf, sf, acc[rb]);   // D[rank][row]
+      }
+    };
+    // full stages: a loop with no branch around the matrix work (a branch
+    // there made the compiler copy the accumulators every stage)
+    const int nst_full = K / KC;
+    for (int st = 0; st < nst_full; ++st) {
+      begin_stage(st);
+#pragma unroll
+      for (int kb = 0; kb < KC / KB; ++kb) kblock(st, kb, false);
+    }
+    if (nst_full < nst) {   // block-uniform: the last, partial stage
+      const int st = nst_full;
+      begin_stage(st);
 #pragma unroll
       for (int kb = 0; kb < KC / KB; ++kb) {
         const int kk = st * KC + kb * KB;
-        if (kk >= K) break;
-        const int chunk = kb * 4 + g;
-        const int rl = 16 * wave + c16;
-        bf16x8 sf = *reinterpret_cast<const bf16x8*>(&Sb[b][rl * KC * 2 + ((chunk ^ (rl & (CPR - 1))) << 4)]);
-        if (kk + KB > K) {   // block-uniform: only a ragged last K-block is masked
-          const int nv = K - (kk + 8 * g);
-#pragma unroll
-          for (int e = 0; e < 8; ++e)
-            if (e >= nv) sf[e] = (__bf16)0.f;
-        }
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) {
-          // weight rows at or past r_q were not copied: their results are zeroed below
-          const int wr = rank_of_row<__bf16>(rb, c16);
-          const bf16x8 wf = *reinterpret_cast<const bf16x8*>(&Wb[b][wr * KC * 2 + ((chunk ^ (wr & (CPR - 1))) << 4)]);
-          acc[rb] = Tr<__bf16>::mma(wf, sf, acc[rb]);   // D[rank][row]
-        }
+        if (kk < K) kblock(st, kb, kk + KB > K);
       }
     }
 

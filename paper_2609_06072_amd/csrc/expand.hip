@@ -10,18 +10,20 @@
 // (a wave-level scan, no host sync); blocks past the last item exit at once.
 // Per item:
 //   - wave 0 lists the tile's (row, slot) pairs in LDS;
-//   - the threads issue the loads of the item's y pieces (16-byte pieces, 16
+//   - the threads issue the loads of the pair weights, of H and of W (cache
+//     hits), then those of the item's y pieces (16-byte pieces, 16
 //     consecutive threads per 256-byte row piece; up to kPrefetch per
-//     thread), which are in flight during the matrix work;
+//     thread), which are in flight during the matrix work (loads return in
+//     order, so the small operands arrive first);
 //   - each wave multiplies its two 16-column blocks of W against the four
 //     16-row blocks of H on the matrix cores and writes C to LDS in fp32;
 //   - the threads add w * C to their y pieces and store them, so y is
 //     rounded once per call (items with more pieces take further batches of
 //     loads).
-// The y pieces held across the matrix work cost occupancy and save the
-// latency of a round trip to the memory per item (six pieces per thread
+// The y pieces held across the matrix work cost registers and save the
+// latency of a round trip to the memory per item (eight pieces per thread
 // measured best: 64-pair items of a 128-column chunk need four, rows that
-// serve several slots more).  y is read and written once per call,
+// serve several slots up to k times as many).  y is read and written once per call,
 // with non-temporal loads and stores, so that it does not displace from the
 // caches what the next launches read.
 #include <type_traits>
@@ -35,7 +37,7 @@ namespace {
 
 constexpr int kBM = 64;                 // rows per tile
 constexpr int kChunk = 128;             // output columns per item
-constexpr int kPrefetch = 6;            // y pieces per thread in flight
+constexpr int kPrefetch = 8;            // y pieces per thread in flight
 constexpr int kBPW = kChunk / 16 / 4;   // 16-column blocks per wave
 
 template <typename T, int RB>
