@@ -285,7 +285,7 @@ __device__ __forceinline__ void dma_item(const GradArgs& a, DmaSmem<RB>& sm, con
   using G = DmaGeo<RB>;
   constexpr int RS = G::RS, NBUF = G::NBUF;
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform, scalar
   const int c16 = lane & 15, g = lane >> 4;
   const int q = it.q;
   const int r_q = a.keys.rank[q], roff = a.keys.roff[q];
@@ -371,68 +371,86 @@ __device__ __forceinline__ void dma_item(const GradArgs& a, DmaSmem<RB>& sm, con
     fetch(0);
     issue(0);
   }
-  for (int st = 0; st < nst; ++st) {
-    // this wave's copies of stage st (and the row metadata of stage st + 1)
-    // are done; the barrier then publishes every wave's copies
+  // K-block kb of stage st (buffer b); the ragged form zeroes the
+  // contraction indices past the chunk
+  auto kblock = [&](int st, int b, int kb, bool ragged) {
+    const int kk = st * RS + kb * 32;   // chunk-relative index of the K-block
+    const int nv = it.nk - (kk + 8 * g);
+    bf16x8 sf[RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const int rr = 16 * rb + c16;
+      const int pos = (kb * 4 + g) ^ (rr & 7);
+      bf16x8 f = *reinterpret_cast<const bf16x8*>(&sm.S[b][rr * RS * 2 + pos * 16]);
+      if (ragged) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (e >= nv) f[e] = (__bf16)0.f;
+      }
+      sf[rb] = f;
+    }
+#pragma unroll
+    for (int cbi = 0; cbi < 2; ++cbi) {
+      const int n0 = 32 * wave + 16 * cbi;
+      s16x4 h2[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int r = kb * 32 + 8 * g + 4 * h + (c16 >> 2);
+        const int c = (n0 >> 3) + ((c16 & 3) >> 1);
+        const int off = r * 256 + ((c ^ l_swz(r)) << 4) + ((c16 & 1) << 3);
+        h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)&sm.L[b][off]);
+      }
+      const bf16x8 lf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(h2[0], h2[1], 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        if (ISB) acc[cbi][rb] = Tr<__bf16>::mma(lf, sf[rb], acc[cbi][rb]);   // D[n][r]
+        else acc[cbi][rb] = Tr<__bf16>::mma(sf[rb], lf, acc[cbi][rb]);       // D[r][c]
+      }
+    }
+  };
+  // the stage's pairs against B_q^T over the block's 128 columns: wave w
+  // takes stage rows 16w .. 16w+15 (row c16 per lane), D[rank][pair]
+  auto dh_part = [&](int st, int b) {
+    const int r = 16 * wave + c16;
+    f32x4 h = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      const int c = kb * 4 + g;
+      const bf16x8 lf = *reinterpret_cast<const bf16x8*>(&sm.L[b][r * 256 + ((c ^ l_swz(r)) << 4)]);
+      h = Tr<__bf16>::mma(bfr[kb], lf, h);
+    }
+    const int kk = st * RS + r;   // chunk index of this lane's pair (rows past nk are copies)
+    if (kk < it.nk && 4 * g < a.dhs) {
+      const long pos = (long)it.kbase + it.k0 + kk;
+      *reinterpret_cast<f32x4*>(a.dHp + ((size_t)it.cb * a.npos + pos) * a.dhs + 4 * g) = h;
+    }
+  };
+  // this wave's copies of stage st (and the row metadata of stage st + 1)
+  // are done; the barrier then publishes every wave's copies
+  auto begin_stage = [&](int st) {
     wait_vmcnt<0>();
     __syncthreads();
     if (st + NBUF - 1 < nst) issue(st + NBUF - 1);
+  };
+  // full stages: no test around the matrix work; then the last, partial one
+  const int nst_full = it.nk / RS;
+  for (int st = 0; st < nst_full; ++st) {
+    begin_stage(st);
+    const int b = st % NBUF;
+#pragma unroll
+    for (int kb = 0; kb < RS / 32; ++kb) kblock(st, b, kb, false);
+    if constexpr (DH) dh_part(st, b);
+  }
+  if (nst_full < nst) {   // block-uniform
+    const int st = nst_full;
+    begin_stage(st);
     const int b = st % NBUF;
 #pragma unroll
     for (int kb = 0; kb < RS / 32; ++kb) {
-      const int kk = st * RS + kb * 32;   // chunk-relative index of the K-block
-      if (kk >= it.nk) break;
-      const int nv = it.nk - (kk + 8 * g);
-      const bool ragged = kk + 32 > it.nk;   // block-uniform: only the item's last K-block
-      bf16x8 sf[RB];
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        const int rr = 16 * rb + c16;
-        const int pos = (kb * 4 + g) ^ (rr & 7);
-        bf16x8 f = *reinterpret_cast<const bf16x8*>(&sm.S[b][rr * RS * 2 + pos * 16]);
-        if (ragged) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e)
-            if (e >= nv) f[e] = (__bf16)0.f;
-        }
-        sf[rb] = f;
-      }
-#pragma unroll
-      for (int cbi = 0; cbi < 2; ++cbi) {
-        const int n0 = 32 * wave + 16 * cbi;
-        s16x4 h2[2];
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int r = kb * 32 + 8 * g + 4 * h + (c16 >> 2);
-          const int c = (n0 >> 3) + ((c16 & 3) >> 1);
-          const int off = r * 256 + ((c ^ l_swz(r)) << 4) + ((c16 & 1) << 3);
-          h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)&sm.L[b][off]);
-        }
-        const bf16x8 lf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(h2[0], h2[1], 0, 1, 2, 3, 4, 5, 6, 7));
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) {
-          if (ISB) acc[cbi][rb] = Tr<__bf16>::mma(lf, sf[rb], acc[cbi][rb]);   // D[n][r]
-          else acc[cbi][rb] = Tr<__bf16>::mma(sf[rb], lf, acc[cbi][rb]);       // D[r][c]
-        }
-      }
+      const int kk = st * RS + kb * 32;
+      if (kk < it.nk) kblock(st, b, kb, kk + 32 > it.nk);
     }
-    if constexpr (DH) {
-      // the stage's pairs against B_q^T over the block's 128 columns: wave w
-      // takes stage rows 16w .. 16w+15 (row c16 per lane), D[rank][pair]
-      const int r = 16 * wave + c16;
-      f32x4 h = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        const int c = kb * 4 + g;
-        const bf16x8 lf = *reinterpret_cast<const bf16x8*>(&sm.L[b][r * 256 + ((c ^ l_swz(r)) << 4)]);
-        h = Tr<__bf16>::mma(bfr[kb], lf, h);
-      }
-      const int kk = st * RS + r;   // chunk index of this lane's pair (rows past nk are copies)
-      if (kk < it.nk && 4 * g < a.dhs) {
-        const long pos = (long)it.kbase + it.k0 + kk;
-        *reinterpret_cast<f32x4*>(a.dHp + ((size_t)it.cb * a.npos + pos) * a.dhs + 4 * g) = h;
-      }
-    }
+    if constexpr (DH) dh_part(st, b);
   }
   finish_item<RB>(a, it, item, acc);
 }
