@@ -277,43 +277,58 @@ __global__ __launch_bounds__(kThreads) void contract_kernel(ContractArgs a) {
 // a window of 65 - k positions, so their pairs (at most 64) are all in the
 // tile; the per-pair results times the pair weights go to LDS in fp32 and
 // every row's sum (pairs in position order) is stored once.
-template <int RB>
+template <int RB, int NWV>
 struct CDma {
   // contraction indices per stage and stages in LDS: ranks up to 32 take
   // 128-column stages two deep (three blocks per CU); larger ranks, whose
   // weight rows double the bytes of a stage, 64-column stages three deep
   static constexpr int KC = RB <= 2 ? 128 : 64;
   static constexpr int NBUF = RB <= 2 ? 2 : 3;  // at most 4 (see the waits)
+  static constexpr int THREADS = 64 * NWV;       // NWV waves of 16 tile rows each
+  static constexpr int ROWS = 16 * NWV;          // tile rows
   static constexpr int CPR = KC / 8;             // 16-byte chunks per row piece
   static constexpr int RPI = 64 / CPR;           // row pieces per copy instruction
-  static constexpr int SBYTES = 64 * KC * 2;     // 64 source rows x KC bf16
+  static constexpr int SBYTES = ROWS * KC * 2;   // tile source rows x KC bf16
   static constexpr int WROWS = 16 * RB;
   static constexpr int WBYTES = WROWS * KC * 2;  // weight rows x KC bf16
   static constexpr int NS = 16 / RPI;            // source copies per wave per stage
-  static constexpr int NW = WROWS / RPI / 4;     // weight copies per wave per stage (at most)
+  static constexpr int NW = (WROWS / RPI + NWV - 1) / NWV;   // weight copies per wave per stage (at most)
   static constexpr int LDS = NBUF * (SBYTES + WBYTES);
   // LDS per CU is 160 KiB; the tile tables take about 4 KiB more per block
   static constexpr int BLOCKS_PER_CU = (160 * 1024) / (LDS + 4 * 1024 + 512) < 1 ? 1 : (160 * 1024) / (LDS + 4 * 1024 + 512);
-  // row sums: per-pair results [64][RPS] fp32 in the weight buffers
+  // row sums: per-pair results [ROWS][RPS] fp32 over the stage buffers
   static constexpr int RPS = 16 * RB + 4;   // 16-byte skew between positions
-  static_assert(64 * RPS * 4 <= NBUF * WBYTES, "per-pair results exceed the weight buffers");
+  static_assert(ROWS * RPS * 4 <= LDS, "per-pair results exceed the stage buffers");
+  static_assert(WROWS / RPI <= NWV * NW, "weight copies");
 };
 
+// Waves per block of the bf16 contraction (16 tile rows each).  At ranks
+// 33..64 the weight rows of a stage are as many as the source rows of a
+// 64-row tile; tiles of 128 rows (eight waves) stage each weight row once per
+// 128 source rows, which pays when there are tiles enough for about two
+// blocks per CU (at one per CU the 64-row tiles are faster).  Only the
+// pair-position contraction knows its tile count on the host (its positions
+// are the P pairs; a row count is known on the device only).
+constexpr int kWideTileMinPerCu2 = 3;   // 128-row tiles when tiles >= 1.5 x CUs
+
 // Tile size in pair positions when rows are summed (every row's pairs lie in
-// the tile) or 64 rows otherwise.
-inline __host__ __device__ int contract_tile(int row_sum, int k) { return row_sum ? 65 - k : 64; }
+// the tile) or rows otherwise, for tiles of `rows` rows.
+inline __host__ __device__ int contract_tile(int row_sum, int k, int rows) {
+  return row_sum ? rows + 1 - k : rows;
+}
 
 // Row sums of a tile whose pair positions p0 .. p1 - 1 hold rows ua .. ub - 1
-// (rstart = first position of this lane's row ua + lane, rtok its token):
-// the per-pair results, scaled and times the pair weights, go to LDS (fp32);
-// then lane l of wave w sums row ua + l over its pairs in position order for
-// the rank chunks 8w, 8w + 32, ... and stores the bf16 sum per key (column
-// u - rfirst) and/or per token.
-template <int RB>
+// (rstart = first position of this lane's row ua + 64 (wave / 4) + lane, rend
+// the next row's, rtok its token): the per-pair results, scaled and times the
+// pair weights, go to LDS (fp32); then lane l of wave w sums row ua + 64 (w /
+// 4) + l over its pairs in position order for the rank chunks 8 (w % 4),
+// 8 (w % 4) + 32, ... and stores the bf16 sum per key (column u - rfirst)
+// and/or per token.
+template <int RB, int NWV>
 __device__ inline void row_sum_store(const ContractArgs& a, int q, const f32x4 (&acc)[RB], float s,
-                                     float pw, int ua, int ub, int p0, int p1, int rfirst,
-                                     int rstart, int rtok, float* hp) {
-  constexpr int RPS = CDma<RB>::RPS;
+                                     float pw, int ua, int ub, int p0, int rfirst, int rstart,
+                                     int rend, int rtok, float* hp) {
+  constexpr int RPS = CDma<RB, NWV>::RPS;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int c16 = lane & 15, g = lane >> 4;
   const int r_q = a.keys.rank[q], roff = a.keys.roff[q], R = a.keys.R;
@@ -331,15 +346,13 @@ __device__ inline void row_sum_store(const ContractArgs& a, int q, const f32x4 (
     }
   }
   __syncthreads();
-  const int u = ua + lane;
-  int rend = __shfl_down(rstart, 1);
-  if (lane == 63 || u + 1 >= ub) rend = p1;
+  const int u = ua + 64 * (wave / 4) + lane;
   if (u >= ub) return;
   const int b0 = rstart - p0, b1 = rend - p0;
   __bf16* dt = static_cast<__bf16*>(a.out_t);
   const long col = u - rfirst;
   __bf16* df = a.out_dense ? static_cast<__bf16*>(a.out_dense) + (size_t)rtok * R + roff : nullptr;
-  for (int r0 = 8 * wave; r0 < r_q; r0 += 32) {
+  for (int r0 = 8 * (wave % 4); r0 < r_q; r0 += 32) {
     const float* src = hp + b0 * RPS + r0;
     f32x4 lo = *reinterpret_cast<const f32x4*>(src), hi = *reinterpret_cast<const f32x4*>(src + 4);
     for (int pos = b0 + 1; pos < b1; ++pos) {
@@ -366,22 +379,26 @@ __device__ inline void row_sum_store(const ContractArgs& a, int q, const f32x4 (
   }
 }
 
-template <int RB>
-__global__ __launch_bounds__(kThreads) void contract_dma_kernel(ContractArgs a) {
-  using G = CDma<RB>;
+template <int RB, int NWV>
+__global__ __launch_bounds__(64 * NWV, NWV == 8 ? 4 : 1) void contract_dma_kernel(ContractArgs a) {
+  using G = CDma<RB, NWV>;
   constexpr int KC = G::KC, NBUF = G::NBUF, KB = Tr<__bf16>::KB;
   constexpr int CPR = G::CPR, RPI = G::RPI;
-  __shared__ __attribute__((aligned(16))) char Sb[NBUF][G::SBYTES];
-  __shared__ __attribute__((aligned(16))) char Wb[NBUF][G::WBYTES];
+  // stage buffers: NBUF source stages, then NBUF weight stages; the row sums
+  // reuse the whole area for the per-pair results
+  __shared__ __attribute__((aligned(16))) char smem[G::LDS];
+  char (*Sb)[G::SBYTES] = reinterpret_cast<char (*)[G::SBYTES]>(smem);
+  char (*Wb)[G::WBYTES] = reinterpret_cast<char (*)[G::WBYTES]>(smem + NBUF * G::SBYTES);
   __shared__ int seg[kMaxKeys + 1];
   __shared__ int bstart[kMaxKeys + 1];
   __shared__ int bfirst[kMaxKeys];
-  __shared__ int scan[kThreads];
+  __shared__ int scan[kThreads];   // block_exclusive_scan reads the first kThreads / 64
+  static_assert(G::THREADS >= kMaxKeys, "one thread per key in the tile tables");
   const int n_keys = a.keys.n_keys;
   const int bucket = blockIdx.x % kXcds;
   const int K = a.K, k = a.k;
   const bool rsum = a.row_sum != 0;   // implies kSrcPairList
-  const int TS = contract_tile(a.row_sum, k);
+  const int TS = contract_tile(a.row_sum, k, G::ROWS);
   build_bucket_table(a.offsets, a.src_mode == kSrcPairList ? a.ppos : nullptr, n_keys, TS, bucket,
                      seg, bstart, bfirst, scan);
   const int total = bstart[n_keys];
@@ -402,7 +419,7 @@ __global__ __launch_bounds__(kThreads) void contract_dma_kernel(ContractArgs a) 
     const int r_q = a.keys.rank[q], roff = a.keys.roff[q];
     // row sums: rows ua .. ub - 1 start inside the window [u0, u0 + TS); their
     // pairs are positions ppos[ua] .. ppos[ub] - 1, which become u0 .. u_end
-    int ua = 0, ub = 0, rfirst = 0, rtok = 0, rstart = 0;
+    int ua = 0, ub = 0, rfirst = 0, rtok = 0, rstart = 0, rend = 0;
     float pw = 1.f;
     if (rsum) {
       const int y = (lane & 1) ? min(u0 + TS, u_end) : u0;
@@ -422,9 +439,11 @@ __global__ __launch_bounds__(kThreads) void contract_dma_kernel(ContractArgs a) 
       u_end = __shfl(pos, 1);
       if (ua >= ub) continue;   // block-uniform: no row starts in this window
       rfirst = a.offsets[q];
-      if (ua + lane < ub) {     // this lane's row in the epilogue
-        rstart = a.ppos[ua + lane];
-        rtok = a.row_token[ua + lane];
+      const int er = ua + 64 * (wave / 4) + lane;   // this lane's row in the epilogue
+      if (er < ub) {
+        rstart = a.ppos[er];
+        rend = er + 1 < ub ? a.ppos[er + 1] : u_end;
+        rtok = a.row_token[er];
       }
       if (a.pair_w) pw = a.pair_w[a.plist[min(u0 + 16 * wave + c16, u_end - 1)]];
     }
@@ -528,8 +547,8 @@ __global__ __launch_bounds__(kThreads) void contract_dma_kernel(ContractArgs a) 
 
     const float s = a.alpha / (float)r_q;
     if (rsum) {
-      row_sum_store<RB>(a, q, acc, s, pw, ua, ub, u0, u_end, rfirst, rstart, rtok,
-                        reinterpret_cast<float*>(&Wb[0][0]));
+      row_sum_store<RB, NWV>(a, q, acc, s, pw, ua, ub, u0, rfirst, rstart, rend, rtok,
+                             reinterpret_cast<float*>(smem));
       continue;
     }
     const int u = u0 + 16 * wave + c16;
@@ -546,18 +565,30 @@ __global__ __launch_bounds__(kThreads) void contract_dma_kernel(ContractArgs a) 
   }
 }
 
+template <int RB, int NWV>
+hipError_t launch_contract_dma(const ContractArgs& a, long P, hipStream_t stream) {
+  using G = CDma<RB, NWV>;
+  const int TS = contract_tile(a.row_sum, a.k, G::ROWS);
+  // tiles per bucket <= (all tiles) / kXcds + n_keys
+  const long pb = P > 0 ? ((P + TS - 1) / TS + a.keys.n_keys) / kXcds + a.keys.n_keys : 0;
+  const long cap = (long)G::BLOCKS_PER_CU * device_cu_count() / kXcds;
+  const int grid = (int)(pb < cap ? pb : cap) * kXcds;
+  if (grid > 0) contract_dma_kernel<RB, NWV><<<grid, G::THREADS, 0, stream>>>(a);
+  return hipGetLastError();
+}
+
 template <typename T, int RB>
 hipError_t launch_contract_rb(const ContractArgs& a, long P, hipStream_t stream) {
   constexpr int BM = 16 * CGeo<RB>::NRB;
   // tiles per bucket <= (all tiles) / kXcds + n_keys
   const long per_bucket = P > 0 ? ((P + BM - 1) / BM + a.keys.n_keys) / kXcds + a.keys.n_keys : 0;
   if constexpr (std::is_same<T, __bf16>::value) {
-    const int TS = contract_tile(a.row_sum, a.k);
-    const long pb = P > 0 ? ((P + TS - 1) / TS + a.keys.n_keys) / kXcds + a.keys.n_keys : 0;
-    const long cap = (long)CDma<RB>::BLOCKS_PER_CU * device_cu_count() / kXcds;
-    const int grid = (int)(pb < cap ? pb : cap) * kXcds;
-    if (grid > 0) contract_dma_kernel<RB><<<grid, kThreads, 0, stream>>>(a);
-    return hipGetLastError();
+    if constexpr (RB == 4) {
+      const int TS8 = contract_tile(a.row_sum, a.k, CDma<RB, 8>::ROWS);
+      if (a.src_mode == kSrcPairList && 2 * (P / TS8) >= (long)kWideTileMinPerCu2 * device_cu_count())
+        return launch_contract_dma<RB, 8>(a, P, stream);
+    }
+    return launch_contract_dma<RB, 4>(a, P, stream);
   }
   const long cap = 6L * device_cu_count() / kXcds;
   const int grid = (int)(per_bucket < cap ? per_bucket : cap) * kXcds;
