@@ -12,9 +12,9 @@
 // exact up to rounding; no N x d_out matrix is ever formed.
 //
 // Launches (all deterministic):
-//   project -- Pt = A X^T, [R][ldp] fp32: a 64 x 128-tile MFMA GEMM over
-//              K = d_in, operands copied global -> LDS directly, four
-//              stages in flight
+//   project -- Pt = A X^T, [R][ldp] fp32: a 64 x 256-tile MFMA GEMM over
+//              K = d_in (eight waves), operands copied global -> LDS
+//              directly, four stages in flight
 //   mean    -- the probe mean of every row of Pt; bf16 inputs: also the
 //              centred rows split as v = hi + lo (both bf16, |lo| <= 2^-9 |v|)
 //   gram    -- partial M over chunks of the probe: upper-triangle 64 x 64
@@ -34,7 +34,8 @@ namespace ace {
 namespace {
 
 constexpr int kPN = 64;    // projection tile: probe rows
-constexpr int kPC = 128;   // projection tile: adapter rows
+constexpr int kPC = 256;   // projection tile: adapter rows (eight waves)
+constexpr int kPThreads = 2 * kPC;
 constexpr int kGT = 64;    // Gram tile edge
 constexpr int kGK = 512;   // probe rows per Gram chunk (at least)
 constexpr int kBO = 256;   // rows of B_e per B^T B chunk
@@ -100,7 +101,8 @@ __device__ inline void upper_pair(int p, int n, int* a, int* b) {
 
 // ---------------------------------------------------------------- project
 
-// A block takes 64 probe rows x 128 adapter rows; wave (wn, wc) owns 32 x 64.
+// A block takes 64 probe rows x 256 adapter rows (eight waves, so that X is
+// staged once per 256 adapter rows); wave (wn, wc) owns 32 x 64.
 // Stages of one K-block (64 bytes of every row) of both operands are copied
 // global -> LDS with global_load_lds_dwordx4, NBUF stages in flight (no
 // register staging).  A copy instruction moves 16 rows; lane l lands at row
@@ -111,14 +113,14 @@ __device__ inline void upper_pair(int p, int n, int* a, int* b) {
 __device__ inline int cka_sw(int row) { return (row >> 2) & 3; }
 
 template <typename T>
-__global__ __launch_bounds__(kThreads) void cka_project_kernel(CkaArgs a) {
+__global__ __launch_bounds__(kPThreads) void cka_project_kernel(CkaArgs a) {
   using F = typename Tr<T>::frag;
   constexpr int PER = Tr<T>::PER, KB = Tr<T>::KB;   // KB * sizeof(T) = 64 bytes
   constexpr int NBUF = 4;
   constexpr int XB = kPN * 64, AB = kPC * 64;       // stage bytes of each operand
   __shared__ __attribute__((aligned(16))) char xs[NBUF][XB];
   __shared__ __attribute__((aligned(16))) char as[NBUF][AB];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int c16 = lane & 15, g = lane >> 4;
   const int n0 = blockIdx.x * kPN, c0 = blockIdx.y * kPC;
   const int wn = (wave & 1) * 32, wc = (wave >> 1) * 64;   // wave: 32 probe rows x 64 adapter rows
@@ -127,12 +129,14 @@ __global__ __launch_bounds__(kThreads) void cka_project_kernel(CkaArgs a) {
   const int N = a.N, R = a.R, d_in = a.d_in;
   const int nst = (d_in + KB - 1) / KB;
 
-  // copy plan: X rows 16w .. 16w+15 (one instruction per wave), A rows
-  // 32w .. 32w+31 (two); lane l copies row (l >> 2) of its instruction
-  // (a chunk past d_in is fetched from column d_in - PER instead, inside the
-  // row, and zeroed at the read)
+  // copy plan: X rows 16w .. 16w+15 (one instruction for each of waves
+  // 0..3), A rows 32w .. 32w+31 (two); lane l copies row (l >> 2) of its
+  // instruction (a chunk past d_in is fetched from column d_in - PER instead,
+  // inside the row, and zeroed at the read)
+  static_assert(kPN / 16 <= kPThreads / 64 && kPC == 32 * (kPThreads / 64), "copy plan");
+  const bool xcopy = 16 * wave < kPN;   // wave-uniform
   const int crow = lane >> 2, cpos = lane & 3;
-  const int xr = 16 * wave + crow;
+  const int xr = min(16 * wave, kPN - 16) + crow;
   const T* xsrc = X + (size_t)min(n0 + xr, N - 1) * d_in;
   const int xch = PER * (cpos ^ cka_sw(xr));
   const T* asrc[2];
@@ -146,14 +150,15 @@ __global__ __launch_bounds__(kThreads) void cka_project_kernel(CkaArgs a) {
   auto issue = [&](int st) {
     const int b = st % NBUF;
     const int k0 = st * KB;
-    dma16(xsrc + min(k0 + xch, d_in - PER),
-          __builtin_amdgcn_readfirstlane(lds_addr(&xs[b][16 * wave * 64])));
+    if (xcopy)
+      dma16(xsrc + min(k0 + xch, d_in - PER),
+            __builtin_amdgcn_readfirstlane(lds_addr(&xs[b][16 * wave * 64])));
 #pragma unroll
     for (int i = 0; i < 2; ++i)
       dma16(asrc[i] + min(k0 + ach[i], d_in - PER),
             __builtin_amdgcn_readfirstlane(lds_addr(&as[b][(32 * wave + 16 * i) * 64])));
   };
-  constexpr int PER_STAGE = 3;   // copies per wave per stage
+  const int per_stage = xcopy ? 3 : 2;   // copies per wave per stage
 
   f32x4 acc[2][4];
 #pragma unroll
@@ -167,7 +172,7 @@ __global__ __launch_bounds__(kThreads) void cka_project_kernel(CkaArgs a) {
   for (int st = 0; st < nst; ++st) {
     // this wave's copies of stage st are done once at most those of the
     // stages issued after it are outstanding; the barrier publishes them
-    wait_vmcnt_upto<(NBUF - 2) * PER_STAGE>(min(NBUF - 2, nst - 1 - st) * PER_STAGE);
+    wait_vmcnt_upto<(NBUF - 2) * 3>(min(NBUF - 2, nst - 1 - st) * per_stage);
     __syncthreads();
     if (st + NBUF - 1 < nst) issue(st + NBUF - 1);
     const int b = st % NBUF;
@@ -555,7 +560,7 @@ hipError_t launch_cka_t(const CkaProblem& p, void* ws, hipStream_t stream) {
   const int R = a.R;
   if (p.N > 0) {
     dim3 grid((p.N + kPN - 1) / kPN, (R + kPC - 1) / kPC);
-    cka_project_kernel<T><<<grid, kThreads, 0, stream>>>(a);
+    cka_project_kernel<T><<<grid, kPThreads, 0, stream>>>(a);
   }
   if (p.dtype == ACE_BF16)
     cka_mean_kernel<true><<<R, kThreads, 0, stream>>>(a);
