@@ -311,6 +311,15 @@ struct CDma {
 // are the P pairs; a row count is known on the device only).
 constexpr int kWideTileMinPerCu2 = 3;   // 128-row tiles when tiles >= 1.5 x CUs
 
+// Chunk swizzle of weight row w (CPR 16-byte chunks per staged row).  A
+// fragment read touches the rows rank_of_row(rb, i), i = 0..15: w & 3 = i & 3,
+// bit 2 of w = rb & 1 and bits 3.. = i >> 2, so w & (CPR - 1) alone would give
+// only four distinct chunk positions among the first eight lanes at 8 chunks
+// per row (two-way bank conflicts); folding bit 3 into bit 2 spreads them
+// over eight (and the 16 rows over 16 positions at 16 chunks per row).
+template <int CPR>
+__device__ inline int w_swz(int w) { return (w ^ ((w >> 3) << 2)) & (CPR - 1); }
+
 // Tile size in pair positions when rows are summed (every row's pairs lie in
 // the tile) or rows otherwise, for tiles of `rows` rows.
 inline __host__ __device__ int contract_tile(int row_sum, int k, int rows) {
@@ -380,7 +389,7 @@ __device__ inline void row_sum_store(const ContractArgs& a, int q, const f32x4 (
 }
 
 template <int RB, int NWV>
-__global__ __launch_bounds__(64 * NWV, NWV == 8 ? 4 : 1) void contract_dma_kernel(ContractArgs a) {
+__global__ __launch_bounds__(64 * NWV, NWV == 8 ? 4 : (RB == 8 ? 2 : 1)) void contract_dma_kernel(ContractArgs a) {
   using G = CDma<RB, NWV>;
   constexpr int KC = G::KC, NBUF = G::NBUF, KB = Tr<__bf16>::KB;
   constexpr int CPR = G::CPR, RPI = G::RPI;
@@ -474,7 +483,7 @@ __global__ __launch_bounds__(64 * NWV, NWV == 8 ? 4 : 1) void contract_dma_kerne
     for (int i = 0; i < G::NW; ++i) {
       const int rl = RPI * (wave * G::NW + i) + crow;  // weight row of the tile (rank)
       wptr[i] = W + (size_t)(roff + min(rl, r_q - 1)) * a.ldw;
-      wcol[i] = 8 * (cpos ^ (rl & (CPR - 1)));
+      wcol[i] = 8 * (cpos ^ w_swz<CPR>(rl));
     }
     // copies of stage st (columns past K are clamped; masked at the reads)
     auto issue = [&](int st) {
@@ -523,7 +532,7 @@ __global__ __launch_bounds__(64 * NWV, NWV == 8 ? 4 : 1) void contract_dma_kerne
       for (int rb = 0; rb < RB; ++rb) {
         // weight rows at or past r_q were not copied: their results are zeroed below
         const int wr = rank_of_row<__bf16>(rb, c16);
-        const bf16x8 wf = *reinterpret_cast<const bf16x8*>(&Wb[b][wr * KC * 2 + ((chunk ^ (wr & (CPR - 1))) << 4)]);
+        const bf16x8 wf = *reinterpret_cast<const bf16x8*>(&Wb[b][wr * KC * 2 + ((chunk ^ w_swz<CPR>(wr)) << 4)]);
         acc[rb] = Tr<__bf16>::mma(wf, sf, acc[rb]);   // D[rank][row]
       }
     };
