@@ -37,12 +37,13 @@ namespace ace {
 namespace {
 
 constexpr int kBM = 64;                 // rows per tile
+constexpr int kBM48 = 48;               // rows per tile, bf16 rank 64 with two chunks
 constexpr int kChunk = 128;             // output columns per chunk
 constexpr int kBPW = kChunk / 16 / 4;   // 16-column blocks per wave
 constexpr int kWideOut = 4096;          // outputs at least this wide take two chunks per item
 
-// NC chunks per item (1 or 2)
-template <typename T, int RB, int NC>
+// NC chunks per item (1 or 2), BM rows per tile (a multiple of 16, <= 64)
+template <typename T, int RB, int NC, int BM>
 __global__ __launch_bounds__(kThreads, (std::is_same<T, __bf16>::value && RB <= 4) ? 4 : 1) void expand_kernel(ExpandArgs a) {
   using F = typename Tr<T>::frag;
   constexpr int PER = Tr<T>::PER, KB = Tr<T>::KB, APF = Tr<T>::APF;
@@ -56,14 +57,16 @@ __global__ __launch_bounds__(kThreads, (std::is_same<T, __bf16>::value && RB <= 
   // registers before C is written, so both share one buffer
   constexpr bool HLDS = std::is_same<T, __bf16>::value && RB >= 4;
   constexpr int HST = HLDS ? NM * KB + 8 : 8;   // LDS row stride of H (elements)
-  static_assert(kBM * HST * sizeof(T) <= kBM * CST * sizeof(float), "H staging exceeds the C buffer");
+  constexpr int NJB = BM / 16;          // 16-row blocks per tile
+  static_assert(BM % 16 == 0 && BM <= 64, "tile rows");
+  static_assert(HST * sizeof(T) <= CST * sizeof(float), "H staging exceeds the C buffer");
   // the second chunk's W fragments are loaded with the first chunk's while
   // they are few; at higher ranks after the first chunk is done
   constexpr bool WB_EARLY = RB <= 2;
-  __shared__ __attribute__((aligned(16))) float Cs[kBM * CST];
+  __shared__ __attribute__((aligned(16))) float Cs[BM * CST];
   T* const Hs = reinterpret_cast<T*>(Cs);
-  __shared__ uint16_t plist[kBM * kMaxK];  // (row << 5) | slot
-  __shared__ int toks[kBM];
+  __shared__ uint16_t plist[BM * kMaxK];  // (row << 5) | slot
+  __shared__ int toks[BM];
   __shared__ int npairs_s;
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -71,7 +74,7 @@ __global__ __launch_bounds__(kThreads, (std::is_same<T, __bf16>::value && RB <= 
   const int tile = blockIdx.x / a.nch;
   const int n0 = (blockIdx.x - tile * a.nch) * (NC * kChunk);
   int q, u0, u_end;
-  if (!locate_tile(a.offsets, a.keys.n_keys, kBM, tile, &q, &u0, &u_end)) return;  // block-uniform
+  if (!locate_tile(a.offsets, a.keys.n_keys, BM, tile, &q, &u0, &u_end)) return;  // block-uniform
   const T* H = static_cast<const T*>(a.H);
   const T* W = static_cast<const T*>(a.W);
   T* O = static_cast<T*>(a.out);
@@ -85,8 +88,8 @@ __global__ __launch_bounds__(kThreads, (std::is_same<T, __bf16>::value && RB <= 
     const int uc = min(u, u_end - 1);  // unconditional loads
     const int tok = a.row_token[uc];
     uint32_t sl = a.row_slots[uc];
-    if (u >= u_end) sl = 0u;
-    toks[lane] = tok;
+    if (u >= u_end || lane >= BM) sl = 0u;
+    if (lane < BM) toks[lane] = tok;
     const int cnt = __builtin_popcount(sl);
     int incl = cnt;
 #pragma unroll
@@ -174,16 +177,16 @@ __global__ __launch_bounds__(kThreads, (std::is_same<T, __bf16>::value && RB <= 
     }
   }
   constexpr int PPRH = NM * KB / PER;   // 16-byte pieces per H row
-  constexpr int HN = HLDS ? kBM * PPRH / kThreads : 1;
-  static_assert(!HLDS || (kBM * PPRH) % kThreads == 0, "H pieces per thread");
+  constexpr int HN = HLDS ? (BM * PPRH + kThreads - 1) / kThreads : 1;
   F hv[HN];
-  F hf[4][NM];
+  F hf[NJB][NM];
   if constexpr (HLDS) {
-    // 64 rows x NM*KB ranks in 16-byte pieces (rows past the segment re-read
-    // the last row)
+    // BM rows x NM*KB ranks in 16-byte pieces (rows past the segment re-read
+    // the last row; pieces past the tile re-read its last piece and are not
+    // stored)
 #pragma unroll
     for (int i = 0; i < HN; ++i) {
-      const int j = tid + i * kThreads;
+      const int j = min(tid + i * kThreads, BM * PPRH - 1);
       const int u = min(u0 + j / PPRH, u_end - 1);
       hv[i] = Tr<T>::load(H + (size_t)u * a.rpad + (j % PPRH) * PER);
     }
@@ -191,7 +194,7 @@ __global__ __launch_bounds__(kThreads, (std::is_same<T, __bf16>::value && RB <= 
     // H fragments of the four row blocks (rows past the segment re-read the
     // last row; nothing is stored for them)
 #pragma unroll
-    for (int jb = 0; jb < 4; ++jb) {
+    for (int jb = 0; jb < NJB; ++jb) {
       const int u = min(u0 + 16 * jb + c16, u_end - 1);
       const T* hr = H + (size_t)u * a.rpad + PER * g;
 #pragma unroll
@@ -228,7 +231,7 @@ __global__ __launch_bounds__(kThreads, (std::is_same<T, __bf16>::value && RB <= 
     for (int bi = 0; bi < kBPW; ++bi) {
       const int b = wave * kBPW + bi;
 #pragma unroll
-      for (int jb = 0; jb < 4; ++jb) {
+      for (int jb = 0; jb < NJB; ++jb) {
         f32x4 c = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int m = 0; m < NM; ++m)
@@ -252,11 +255,11 @@ __global__ __launch_bounds__(kThreads, (std::is_same<T, __bf16>::value && RB <= 
 #pragma unroll
     for (int i = 0; i < HN; ++i) {
       const int j = tid + i * kThreads;
-      Tr<T>::store(&Hs[(j / PPRH) * HST + (j % PPRH) * PER], hv[i]);
+      if (j < BM * PPRH) Tr<T>::store(&Hs[(j / PPRH) * HST + (j % PPRH) * PER], hv[i]);
     }
     __syncthreads();
 #pragma unroll
-    for (int jb = 0; jb < 4; ++jb)
+    for (int jb = 0; jb < NJB; ++jb)
 #pragma unroll
       for (int m = 0; m < NM; ++m) hf[jb][m] = Tr<T>::load(&Hs[(16 * jb + c16) * HST + KB * m + PER * g]);
     __syncthreads();  // every wave holds its H fragments; C reuses the buffer
@@ -290,13 +293,23 @@ hipError_t launch_expand_rb(ExpandArgs a, long P, hipStream_t stream) {
   // the first chunk is done, costs more than the shared set-up saves
   const int nc = (RB <= 2 || a.n_out >= kWideOut) ? 2 : 1;
   a.nch = (a.n_out + nc * kChunk - 1) / (nc * kChunk);   // items per tile
-  // tiles are bounded by P / kBM plus one ragged tile per key; U itself stays
+  // bf16 at 64 ranks with two chunks: four y pieces per thread and chunk
+  // cover 64 pairs, so tiles of 48 rows keep rows serving two slots within
+  // one batch of loads (a second batch costs a round trip to the memory)
+  const int bm = (std::is_same<T, __bf16>::value && RB == 4 && nc == 2) ? kBM48 : kBM;
+  // tiles are bounded by P / bm plus one ragged tile per key; U itself stays
   // on the device
-  const long grid = P > 0 ? ((P + kBM - 1) / kBM + a.keys.n_keys) * a.nch : 0;
+  const long grid = P > 0 ? ((P + bm - 1) / bm + a.keys.n_keys) * a.nch : 0;
   if (grid > 0x7fffffffL) return hipErrorInvalidConfiguration;
   if (grid > 0) {
-    if (nc == 2) expand_kernel<T, RB, 2><<<(int)grid, kThreads, 0, stream>>>(a);
-    else expand_kernel<T, RB, 1><<<(int)grid, kThreads, 0, stream>>>(a);
+    if constexpr (std::is_same<T, __bf16>::value && RB == 4) {
+      if (nc == 2) {
+        expand_kernel<T, RB, 2, kBM48><<<(int)grid, kThreads, 0, stream>>>(a);
+        return hipGetLastError();
+      }
+    }
+    if (nc == 2) expand_kernel<T, RB, 2, kBM><<<(int)grid, kThreads, 0, stream>>>(a);
+    else expand_kernel<T, RB, 1, kBM><<<(int)grid, kThreads, 0, stream>>>(a);
   }
   return hipGetLastError();
 }
