@@ -85,6 +85,7 @@ struct ExpandArgs {
   int32_t k, n_out;
   void* out;                  // [T*k][n_out], accumulated
   const float* pair_w;        // or null (weight 1)
+  int32_t multi_slot;         // rows may serve several slots (row-deduplicated grouping)
   int32_t nch;                // set by the launcher
   KeyTable keys;
 };

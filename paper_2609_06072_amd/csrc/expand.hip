@@ -37,7 +37,7 @@ namespace ace {
 namespace {
 
 constexpr int kBM = 64;                 // rows per tile
-constexpr int kBM48 = 48;               // rows per tile, bf16 rank 64 with two chunks
+constexpr int kBM48 = 48;               // rows per tile, bf16 rows serving several slots, two chunks
 constexpr int kChunk = 128;             // output columns per chunk
 constexpr int kBPW = kChunk / 16 / 4;   // 16-column blocks per wave
 constexpr int kWideOut = 4096;          // outputs at least this wide take two chunks per item
@@ -293,17 +293,17 @@ hipError_t launch_expand_rb(ExpandArgs a, long P, hipStream_t stream) {
   // the first chunk is done, costs more than the shared set-up saves
   const int nc = (RB <= 2 || a.n_out >= kWideOut) ? 2 : 1;
   a.nch = (a.n_out + nc * kChunk - 1) / (nc * kChunk);   // items per tile
-  // bf16 at 64 ranks with two chunks: four y pieces per thread and chunk
-  // cover 64 pairs, so tiles of 48 rows keep rows serving two slots within
+  // bf16 with two chunks: four y pieces per thread and chunk cover 64 pairs,
+  // so where rows serve several slots, tiles of 48 rows keep most tiles within
   // one batch of loads (a second batch costs a round trip to the memory)
-  const int bm = (std::is_same<T, __bf16>::value && RB == 4 && nc == 2) ? kBM48 : kBM;
+  const int bm = (std::is_same<T, __bf16>::value && a.multi_slot && nc == 2) ? kBM48 : kBM;
   // tiles are bounded by P / bm plus one ragged tile per key; U itself stays
   // on the device
   const long grid = P > 0 ? ((P + bm - 1) / bm + a.keys.n_keys) * a.nch : 0;
   if (grid > 0x7fffffffL) return hipErrorInvalidConfiguration;
   if (grid > 0) {
-    if constexpr (std::is_same<T, __bf16>::value && RB == 4) {
-      if (nc == 2) {
+    if constexpr (std::is_same<T, __bf16>::value) {
+      if (bm == kBM48) {
         expand_kernel<T, RB, 2, kBM48><<<(int)grid, kThreads, 0, stream>>>(a);
         return hipGetLastError();
       }

@@ -561,6 +561,7 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
     x.out = dx;
     x.pair_w = nullptr;
     x.keys = p.keys;
+    x.multi_slot = p.rt->mode == ACE_ROWS_GROUP_DEDUP;
     return launch_expand(p.dtype, x, p.r_max, P, stream);
   }
 

@@ -218,6 +218,7 @@ hipError_t launch_bwd_combined(const Problem& p, const void* dy, void* dx, float
   x.out = dx;
   x.pair_w = p.pair_w;
   x.keys = p.keys;
+  x.multi_slot = p.rt->mode == ACE_ROWS_GROUP_DEDUP;
   e = launch_expand(p.dtype, x, p.r_max, P, stream);
   if (e != hipSuccess) return e;
   GradArgs gr{};

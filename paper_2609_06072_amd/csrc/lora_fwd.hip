@@ -51,6 +51,7 @@ hipError_t launch_fwd(const Problem& p, void* y, void* ws, hipStream_t stream) {
   x.out = y;
   x.pair_w = p.pair_w;
   x.keys = p.keys;
+  x.multi_slot = p.rt->mode == ACE_ROWS_GROUP_DEDUP;
   return launch_expand(p.dtype, x, p.r_max, P, stream);
 }
 
