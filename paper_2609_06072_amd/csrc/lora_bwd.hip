@@ -39,7 +39,7 @@ constexpr int kMaxJobs = kMaxKeys + 3;
 size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 
 struct WsLayout {
-  size_t At, Bt, Ht, dHt, dHf, dHrow, part, dHp, total;
+  size_t At, Bt, Ht, dHt, dHf, dHrow, part, dHp, cpart, total;
 };
 
 // Ranks up to 16 take the backward in which the dB pass also contracts dY
@@ -68,6 +68,8 @@ WsLayout ws_layout(int T, int k, int d_in, int d_out, int n_keys, int R, int r_m
   w.dHrow = o; o += align256(es * P * rpad);
   w.part = o;  o += align256(grads_part_bytes(T, k, d_in, d_out, n_keys, r_max));
   w.dHp = o;   o += r_max <= kFusedDhMaxRank ? align256(sizeof(float) * nbB * P * dh_stride(r_max)) : 0;   // per-pair input only
+  // K-split partials of the rank contraction (ranks 33..64, bf16)
+  w.cpart = o; o += rank_blocks(r_max) == 4 ? align256(sizeof(float) * kContractKSplit * P * 64) : 0;
   w.total = o + 256;
   return w;
 }
@@ -514,6 +516,7 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
       c.ppos = ppos;
       c.pair_row = p.rt->pair_row;
       c.row_sum = 1;
+      c.kpart = rank_blocks(p.r_max) == 4 ? reinterpret_cast<float*>(base + L.cpart) : nullptr;
       c.out_w = 0;
       c.out_t = base + L.dHt;
       c.out_dense = base + L.dHf;

@@ -445,6 +445,27 @@ def test_per_pair_single_read_backward(r_e):
         check_rel("dB", f64(out["dB"]), dB, tol)
 
 
+@pytest.mark.parametrize("d_ffn", [4136, 6152])
+def test_split_rank_contraction(d_ffn):
+    """Rank-64 group keys whose rows serve several slots, with a long output
+    dimension and few pair positions: the backward's rank contraction over
+    d_ffn runs in two K ranges (fp32 partials per position) and a finishing
+    pass that sums them and forms the row sums.  d_ffn is ragged against the
+    range length and the 64-column stages."""
+    cfg = W.CONFIGS["mixtral_bf16"].scaled(T=700, d_model=136, d_ffn=d_ffn)
+    c = make_case(cfg, "grouped", seed=12, with_w=True)
+    assert max(c.ranks) == 64 and c.d_out == d_ffn
+    say(f"split rank contraction T={cfg.T} d_out={c.d_out}")
+    out = run_gpu(c, reuse_h=True)
+    tol = TOL["bf16"]
+    check_rel("delta", f64(out["y"]), oracle_fwd(c), tol)
+    dx, dA, dB = oracle_bwd(c)
+    check_all("dx", f64(out["dx"]), dx, tol)
+    check_all("dA", f64(out["dA"]), dA, tol)
+    check_rel("dB", f64(out["dB"]), dB, tol)
+    check_dB_rows("dB", f64(out["dB"]), dB, c.ranks, c.d_out, tol)
+
+
 def test_max_rank_and_many_groups():
     cfg = W.CONFIGS["olmoe_bf16"].scaled(T=150, d_model=128, d_ffn=64, r_e=64,
                                          groups=("consecutive", 4))
