@@ -1024,6 +1024,17 @@ def main():
     if traffic is not None and f"ace:{dom}" in traffic:
         fb, wb = traffic[f"ace:{dom}"]
         dom_traffic = fb + wb
+    # the whole step's measured HBM traffic (FETCH_SIZE + WRITE_SIZE of every
+    # call, from the stored counter passes) against its time: how close the
+    # step runs to the rates a copy and a read-modify-write reach
+    step_traffic = {}
+    if traffic is not None:
+        for kind, pre in (("ace", "ace:"), ("expertwise", "lora:")):
+            tb = sum(f + w for k, (f, w) in traffic.items() if k.startswith(pre))
+            ms = ace_ms if kind == "ace" else lora_ms
+            step_traffic[f"measured_traffic_{kind}"] = tb
+            step_traffic[f"measured_GBps_{kind}"] = tb / (ms * 1e-3) / 1e9
+            step_traffic[f"measured_frac_{kind}_of_rmw"] = tb / (ms * 1e-3) / (rmw_gbs * 1e9)
     line = {
         "metric": METRIC,
         "value": P / (ace_ms * 1e-3),
@@ -1050,7 +1061,8 @@ def main():
                           "measured_copy_GBps": copy_gbs,
                           "frac_ace_of_copy": m["step_bytes"] / (ace_ms * 1e-3) / (copy_gbs * 1e9),
                           "measured_rmw_GBps": rmw_gbs,
-                          "frac_ace_of_rmw": m["step_bytes"] / (ace_ms * 1e-3) / (rmw_gbs * 1e9)},
+                          "frac_ace_of_rmw": m["step_bytes"] / (ace_ms * 1e-3) / (rmw_gbs * 1e9),
+                          **step_traffic},
         "roofline": {"bound": "hbm", "kernel": f"{entry} ({proj}): all kernels of one call",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": dom_traffic,
