@@ -15,7 +15,7 @@
 //
 // Items are (key, chunk of <= 1024 contraction indices, 128 gradient columns,
 // dB or dA), enumerated on the device from the segment offsets, so a skewed key
-// is split over several blocks; a key of one chunk writes its gradient
+// is split over several blocks (chunks of one key about equally long); a key of one chunk writes its gradient
 // directly, otherwise every chunk writes a partial and grad_reduce_kernel sums
 // them in chunk order (deterministic).
 //
@@ -130,8 +130,11 @@ __device__ inline Item decode_item(const GradArgs& a, const GradTable& tb, int i
     it.ns = n_split(cnt, a.split);
     it.kbase = tb.aseg[it.q];
   }
-  it.k0 = it.s * a.split;
-  it.nk = max(0, min(cnt - it.k0, a.split));
+  // the key's ns chunks share its indices evenly (in whole 64-index stages),
+  // so that no chunk is much shorter than the others
+  const int clen = min(a.split, ((cnt + it.ns - 1) / it.ns + 63) & ~63);
+  it.k0 = it.s * clen;
+  it.nk = max(0, min(cnt - it.k0, clen));
   return it;
 }
 
