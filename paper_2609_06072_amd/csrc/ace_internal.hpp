@@ -182,8 +182,9 @@ struct GradArgs {
   int32_t phase;
   float* dHp;                 // phase 1: [nbB][npos][dhs] fp32, B_q^T dY per pair
                               //   position, the 128 columns of one dB column block
+                              //   (wide items: [nbW][npos][64], 512 columns)
   long npos;
-  int32_t dhs;                // rank stride of dHp (8 or 16)
+  int32_t dhs;                // rank stride of dHp (8 or 16; 64 for wide items)
   const void* Bt;             // phase 1: B^T [R][d_out], storage type
   KeyTable keys;
 };
@@ -228,6 +229,12 @@ hipError_t launch_grads(int dtype, GradArgs g, int r_max, long P, hipStream_t st
 hipError_t launch_dh_reduce(const DhReduceArgs& d, long U, hipStream_t stream);
 // Columns per dB column block (the dH partials of phase 1 are per block).
 constexpr int kGradColBlk = 128;
+// Phase 1 at ranks 33..64 with shared input and wide outputs (bf16): dB items
+// of kWideCols dY columns whose dH partials ([nbW][npos][64] fp32, nbW =
+// ceil(d_out / kWideCols)) replace the dH contraction; phase 2 and the
+// split reduce as usual.
+constexpr int kWideCols = 512;
+hipError_t launch_grads_wide(GradArgs g, long P, hipStream_t stream);
 hipError_t launch_dx_gemm(int dtype, const DxArgs& d, hipStream_t stream);
 
 size_t bwd_ws_bytes(int T, int k, int d_in, int d_out, int n_keys, int R, int r_max);

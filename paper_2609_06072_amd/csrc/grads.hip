@@ -58,6 +58,13 @@ struct GradTable {
 
 __device__ inline int n_split(int cnt, int split) { return max(1, (cnt + split - 1) / split); }
 
+// Indices per chunk when a key's cnt indices form ns chunks: shared evenly,
+// in whole 64-index stages, so that no chunk is much shorter than the others
+// (at most split, so the last chunk is never empty).
+__device__ inline int chunk_len(int cnt, int ns, int split) {
+  return min(split, ((cnt + ns - 1) / ns + 63) & ~63);
+}
+
 // Item table for the reduce: [0, n_keys] first item of each key, then at
 // kItabStride the dB chunk counts, at 2 kItabStride the dA chunk counts.
 constexpr int kItabStride = kMaxKeys + 1;
@@ -130,9 +137,7 @@ __device__ inline Item decode_item(const GradArgs& a, const GradTable& tb, int i
     it.ns = n_split(cnt, a.split);
     it.kbase = tb.aseg[it.q];
   }
-  // the key's ns chunks share its indices evenly (in whole 64-index stages),
-  // so that no chunk is much shorter than the others
-  const int clen = min(a.split, ((cnt + it.ns - 1) / it.ns + 63) & ~63);
+  const int clen = chunk_len(cnt, it.ns, a.split);
   it.k0 = it.s * clen;
   it.nk = max(0, min(cnt - it.k0, clen));
   return it;
@@ -473,6 +478,264 @@ __global__ __launch_bounds__(kThreads, RB <= 4 ? 3 : 1) void grad_dma_kernel(Gra
     } else {
       dma_item<RB, false, false>(a, sm, it, item);
     }
+  }
+}
+
+// ------------------------------------------- wide dB items with dH partials
+// Shared input at ranks 33..64 with wide outputs (bf16): dY is read once per
+// call.  A dB item takes 512 dY columns (four 128-column sub-tiles, each laid
+// out like the L tile above) of a chunk of the key's pairs; from the same
+// stage in LDS it also contracts every pair's 512 columns against B_q^T into
+// an fp32 dH partial per pair position and 512-column block (rank stride 64),
+// which dh_reduce sums per row.  The dH contraction over all of d_out before
+// the weight gradients, and its second read of dY, are not run.
+// Eight waves: wave w accumulates dB of the item's columns 64w .. 64w+63 and
+// computes dH of rank block w % 4 for the pair blocks w / 4 and w / 4 + 2 of
+// every stage, with its B_q^T fragments over the item's 512 columns held in
+// registers for the whole item.  The dB results go out in the layout of the
+// four 128-column items they cover (direct stores or split partials), so the
+// split reduce after the dA items is the usual one.
+constexpr int kWideWaves = 8;
+constexpr int kWideThreads = 64 * kWideWaves;
+
+struct WideGeo {
+  static constexpr int RB = 4;                          // ranks up to 64
+  static constexpr int RS = 64;                         // pairs per stage
+  static constexpr int SUB = kWideCols / kColBlk;       // 128-column sub-tiles
+  static constexpr int SUBBYTES = RS * 256;             // 64 rows x 128 bf16
+  static constexpr int LBYTES = SUB * SUBBYTES;         // 64 KB
+  static constexpr int SROWS = 16 * RB;                 // rank rows of the Hw slice
+  static constexpr int SBYTES = SROWS * RS * 2;         // 8 KB
+  static constexpr int NL = SUB * RS / 4 / kWideWaves;  // 4-row dY copies per wave and stage
+  static_assert(SROWS == 8 * kWideWaves, "one 8-row Hw copy per wave and stage");
+  static_assert(NL == 2 * SUB, "wave w copies stage rows 8w .. 8w+7 of every sub-tile");
+};
+
+struct WideSmem {
+  __attribute__((aligned(16))) char L[2][WideGeo::LBYTES];
+  __attribute__((aligned(16))) char S[2][WideGeo::SBYTES];
+  GradTable tb;                 // the 128-column items (partial positions, chunks)
+  int wstart[kMaxKeys + 1];     // first wide item of each key
+  int scan[kWideWaves];
+};
+
+__device__ __forceinline__ void wide_item(const GradArgs& a, WideSmem& sm, int q, int s, int cbw,
+                                          int ns, int k0, int nk) {
+  using G = WideGeo;
+  constexpr int RB = G::RB, RS = G::RS, SUB = G::SUB;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int c16 = lane & 15, g = lane >> 4;
+  const int r_q = a.keys.rank[q], roff = a.keys.roff[q];
+  const int kbase = sm.tb.bseg[q];
+  const __bf16* L = static_cast<const __bf16*>(a.dy);
+  const int ldl = a.d_out;
+  const __bf16* S = static_cast<const __bf16*>(a.Hw);
+  const int col0 = cbw * kWideCols;
+  const int nst = (nk + RS - 1) / RS;
+
+  __syncthreads();  // the previous item is done with the buffers
+
+  const int lrow_in = lane >> 4;   // row inside a 4-row copy
+  const int lpos = lane & 15;      // 16-byte position in the sub-tile row
+  const int srow_in = lane >> 3;   // rank row inside the 8-row Hw copy
+  const int spos = lane & 7;
+  // Lane j of wave w loads the row metadata of stage row 8w + (j & 7) one
+  // stage ahead; the copying lanes get their rows by shuffles.
+  const RowSrc rs = row_src<true>(a);
+  const int kfirst = kbase + k0;
+  int raw0 = 0;
+  uint32_t raw1 = 0u;
+  auto fetch = [&](int st) {
+    const int kabs = kfirst + min(st * RS + 8 * wave + (lane & 7), nk - 1);
+    raw0 = rs.src0[kabs];
+    raw1 = rs.src1[kabs];
+  };
+  auto issue = [&](int st) {
+    const int b = st & 1;
+    const int myrow = rs.slots ? raw0 * a.k + (__builtin_ctz(raw1 | 0x80000000u) & 31) : raw0;
+    int rows[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) rows[h] = __shfl(myrow, 4 * h + lrow_in, 64);
+    if (st + 1 < nst) fetch(st + 1);   // block-uniform
+#pragma unroll
+    for (int i = 0; i < G::NL; ++i) {
+      const int sub = i >> 1, h = i & 1;
+      const int r0 = 8 * wave + 4 * h;
+      const int r = r0 + lrow_in;                       // row of the stage
+      const int c = lpos ^ l_swz(r);                    // chunk this lane copies
+      const int col = min(col0 + kColBlk * sub + 8 * c, ldl - 8);
+      dma16_nt(L + (size_t)rows[h] * ldl + col,
+               __builtin_amdgcn_readfirstlane(lds_addr(&sm.L[b][sub * G::SUBBYTES + r0 * 256])));
+    }
+    const int rr0 = 8 * wave;
+    const int rr = rr0 + srow_in;                       // rank row of the slice
+    const int c = spos ^ (rr & 7);
+    const long col = min((long)k0 + st * RS + 8 * c, a.ldh - 8);
+    dma16(S + (size_t)(roff + min(rr, r_q - 1)) * a.ldh + col,
+          __builtin_amdgcn_readfirstlane(lds_addr(&sm.S[b][rr0 * RS * 2])));
+  };
+
+  // B_q^T fragments of this wave's rank block over the item's columns (zero
+  // past r_q and past d_out)
+  const int rbw = wave & 3;
+  bf16x8 bt[kWideCols / 32];
+  {
+    const int rr = 16 * rbw + c16;
+    const __bf16* Btp = static_cast<const __bf16*>(a.Bt) + (size_t)(roff + min(rr, r_q - 1)) * a.d_out;
+#pragma unroll
+    for (int kb = 0; kb < kWideCols / 32; ++kb) {
+      const int c = col0 + 32 * kb + 8 * g;
+      bt[kb] = Tr<__bf16>::load(Btp + min(c, a.d_out - 8));
+      if (c >= a.d_out || rr >= r_q) bt[kb] = Tr<__bf16>::zero();
+    }
+  }
+  f32x4 acc[4][RB];
+#pragma unroll
+  for (int cbi = 0; cbi < 4; ++cbi)
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) acc[cbi][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  if (nst > 0) {
+    fetch(0);
+    issue(0);
+  }
+  const int sub_b = wave >> 1;                 // this wave's dB sub-tile
+  const int nb0 = 64 * (wave & 1);             // and its first column there
+  // dB K-block kb of stage st (buffer b); the ragged form zeroes the pairs
+  // past the chunk
+  auto kblock = [&](int st, int b, int kb, bool ragged) {
+    const int kk = st * RS + kb * 32;
+    const int nv = nk - (kk + 8 * g);
+    bf16x8 sf[RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const int rr = 16 * rb + c16;
+      const int pos = (kb * 4 + g) ^ (rr & 7);
+      bf16x8 f = *reinterpret_cast<const bf16x8*>(&sm.S[b][rr * RS * 2 + pos * 16]);
+      if (ragged) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (e >= nv) f[e] = (__bf16)0.f;
+      }
+      sf[rb] = f;
+    }
+    const char* Lb = &sm.L[b][sub_b * G::SUBBYTES];
+#pragma unroll
+    for (int cbi = 0; cbi < 4; ++cbi) {
+      const int n0 = nb0 + 16 * cbi;
+      s16x4 h2[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int r = kb * 32 + 8 * g + 4 * h + (c16 >> 2);
+        const int c = (n0 >> 3) + ((c16 & 3) >> 1);
+        const int off = r * 256 + ((c ^ l_swz(r)) << 4) + ((c16 & 1) << 3);
+        h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(Lb + off));
+      }
+      const bf16x8 lf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(h2[0], h2[1], 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) acc[cbi][rb] = Tr<__bf16>::mma(lf, sf[rb], acc[cbi][rb]);   // D[n][r]
+    }
+  };
+  // dH of rank block rbw for pair blocks pb0 and pb0 + 2 of stage st over the
+  // item's 512 columns: D[rank][pair], stored per pair position
+  const int pb0 = wave >> 2;
+  auto dh_part = [&](int st, int b) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int r = 16 * (pb0 + 2 * j) + c16;   // stage row (pair) of this lane
+      f32x4 h = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kb = 0; kb < kWideCols / 32; ++kb) {
+        const int c = (kb & 3) * 4 + g;
+        const bf16x8 lf = *reinterpret_cast<const bf16x8*>(
+            &sm.L[b][(kb >> 2) * G::SUBBYTES + r * 256 + ((c ^ l_swz(r)) << 4)]);
+        h = Tr<__bf16>::mma(bt[kb], lf, h);
+      }
+      const int kk = st * RS + r;   // chunk index of this lane's pair (rows past nk are copies)
+      if (kk < nk) {
+        const long pos = (long)kfirst + kk;
+        *reinterpret_cast<f32x4*>(a.dHp + ((size_t)cbw * a.npos + pos) * (16 * RB) + 16 * rbw + 4 * g) = h;
+      }
+    }
+  };
+  // this wave's copies of stage st (and the row metadata of stage st + 1)
+  // are done; the barrier then publishes every wave's copies
+  auto begin_stage = [&](int st) {
+    wait_vmcnt<0>();
+    __syncthreads();
+    if (st + 1 < nst) issue(st + 1);
+  };
+  const int nst_full = nk / RS;
+  for (int st = 0; st < nst_full; ++st) {
+    begin_stage(st);
+    const int b = st & 1;
+#pragma unroll
+    for (int kb = 0; kb < RS / 32; ++kb) kblock(st, b, kb, false);
+    dh_part(st, b);
+  }
+  if (nst_full < nst) {   // block-uniform: the last, partial stage
+    const int st = nst_full;
+    begin_stage(st);
+    const int b = st & 1;
+#pragma unroll
+    for (int kb = 0; kb < RS / 32; ++kb) {
+      const int kk = st * RS + kb * 32;
+      if (kk < nk) kblock(st, b, kb, kk + 32 > nk);
+    }
+    dh_part(st, b);
+  }
+
+  // dB: columns col0 + 128 sub_b + nb0 + 16 cbi of the 128-column item
+  // (q, s, 4 cbw + sub_b), i.e. its wave 2 (w & 1) + cbi / 2, block cbi % 2
+  const int cb = SUB * cbw + sub_b;
+  if (cb >= a.nbB) return;   // wave-uniform: a sub-tile past d_out
+  const int nrb = (r_q + 15) >> 4;
+  if (ns == 1) {
+#pragma unroll
+    for (int cbi = 0; cbi < 4; ++cbi)
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+        if (rb < nrb)
+          store_grad(a, true, q, cb * kColBlk, 2 * (wave & 1) + (cbi >> 1), cbi & 1, rb, lane,
+                     acc[cbi][rb]);
+  } else {
+    const int item = sm.tb.istart[q] + s * a.nbB + cb;
+    f32x4* part = reinterpret_cast<f32x4*>(a.part) + (size_t)item * (4 * 2 * RB * 64);
+#pragma unroll
+    for (int cbi = 0; cbi < 4; ++cbi)
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+        if (rb < nrb)
+          part[(((2 * (wave & 1) + (cbi >> 1)) * 2 + (cbi & 1)) * RB + rb) * 64 + lane] = acc[cbi][rb];
+  }
+}
+
+__global__ __launch_bounds__(kWideThreads, 2) void grad_wide_kernel(GradArgs a) {
+  __shared__ WideSmem sm;
+  build_grad_table(a, sm.tb, sm.scan);
+  const int n_keys = a.keys.n_keys;
+  const int nbW = (a.d_out + kWideCols - 1) / kWideCols;
+  {
+    // wide items of key q: nsB(q) * nbW, key-major
+    const int t = threadIdx.x;
+    const int cnt = t < n_keys ? n_split(sm.tb.bseg[t + 1] - sm.tb.bseg[t], a.split) * nbW : 0;
+    int total;
+    const int ex = block_exclusive_scan(cnt, sm.scan, &total);
+    if (t < n_keys) sm.wstart[t] = ex;
+    if (t == 0) sm.wstart[n_keys] = total;
+    __syncthreads();
+  }
+  const int total = sm.wstart[n_keys];
+  for (int i = blockIdx.x; i < total; i += gridDim.x) {
+    const int q = upper_index(sm.wstart, n_keys, i);
+    const int local = i - sm.wstart[q];
+    const int s = local / nbW, cbw = local - s * nbW;
+    const int cnt = sm.tb.bseg[q + 1] - sm.tb.bseg[q];
+    const int ns = n_split(cnt, a.split);
+    const int clen = chunk_len(cnt, ns, a.split);
+    const int k0 = s * clen;
+    wide_item(a, sm, q, s, cbw, ns, k0, max(0, min(cnt - k0, clen)));
   }
 }
 
@@ -1040,8 +1303,24 @@ hipError_t launch_grads(int dtype, GradArgs g, int r_max, long P, hipStream_t st
   return launch_grads_rb<16>(dtype, g, P, stream);
 }
 
+hipError_t launch_grads_wide(GradArgs g, long P, hipStream_t stream) {
+  g.nbB = (g.d_out + kColBlk - 1) / kColBlk;
+  g.nbA = (g.d_in + kColBlk - 1) / kColBlk;
+  if (g.split == 0) g.split = kSplitRows;
+  if (g.split != kSplitRows && g.split != kMaxSplit) return hipErrorInvalidValue;
+  const int nb = g.nbB + g.nbA;
+  g.itab = reinterpret_cast<int32_t*>(static_cast<char*>(g.part) +
+                                      partial_bytes(P, g.keys.n_keys, nb, WideGeo::RB));
+  const long nbW = (g.d_out + kWideCols - 1) / kWideCols;
+  const long items = ((P + kSplitRows - 1) / kSplitRows + g.keys.n_keys) * nbW;
+  const long cap = device_cu_count();
+  const int grid = (int)(items < cap ? items : cap);
+  if (grid > 0) grad_wide_kernel<<<grid, kWideThreads, 0, stream>>>(g);
+  return hipGetLastError();
+}
+
 hipError_t launch_dh_reduce(const DhReduceArgs& d, long U, hipStream_t stream) {
-  if (d.dhs != 8 && d.dhs != 16) return hipErrorInvalidValue;
+  if (d.dhs != 8 && d.dhs != 16 && d.dhs != 64) return hipErrorInvalidValue;
   const int rows_per_block = kThreads / (d.dhs / 4);
   const long blocks = (U + rows_per_block - 1) / rows_per_block;
   if (blocks > 0) dh_reduce_kernel<<<(int)blocks, kThreads, 0, stream>>>(d);

@@ -46,6 +46,15 @@ struct WsLayout {
 // against B^T (bf16): its fp32 partials per column block use this rank stride.
 constexpr int kFusedDhMaxRank = 16;
 int dh_stride(int r_max) { return r_max <= 8 ? 8 : 16; }
+// With shared input the dB pass forms the dH partials only for outputs of at
+// least this many columns: below it the second read of dY is cheap and the
+// dA items overlap best with the dB items in one launch.
+constexpr int kSharedDhMinOut = 1280;
+// Ranks 33..64 (bf16, shared input): dB items of kWideCols columns form the
+// dH partials for outputs of at least this many columns (a contraction over
+// all of d_out, re-reading dY, otherwise).
+constexpr int kWideDhMinOut = 4096;
+bool wide_dh(int r_max, int d_out) { return rank_blocks(r_max) == 4 && d_out >= kWideDhMinOut; }
 
 // Workspace regions for element size es: At [d_in][R], Bt [R][d_out],
 // Ht/dHt [R][ldh] (column = row index inside the key's segment), dense dH
@@ -67,7 +76,9 @@ WsLayout ws_layout(int T, int k, int d_in, int d_out, int n_keys, int R, int r_m
   w.dHf = o;   o += align256(es * P * R);
   w.dHrow = o; o += align256(es * P * rpad);
   w.part = o;  o += align256(grads_part_bytes(T, k, d_in, d_out, n_keys, r_max));
-  w.dHp = o;   o += r_max <= kFusedDhMaxRank ? align256(sizeof(float) * nbB * P * dh_stride(r_max)) : 0;   // per-pair input only
+  const size_t nbW = (d_out + kWideCols - 1) / kWideCols;
+  w.dHp = o;   o += r_max <= kFusedDhMaxRank ? align256(sizeof(float) * nbB * P * dh_stride(r_max))
+                    : wide_dh(r_max, d_out) ? align256(sizeof(float) * nbW * P * 64) : 0;
   // K-split partials of the rank contraction (ranks 33..64, bf16)
   w.cpart = o; o += rank_blocks(r_max) == 4 ? align256(sizeof(float) * kContractKSplit * P * 64) : 0;
   w.total = o + 256;
@@ -461,26 +472,30 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
     const long nb = (p.d_out + kGradColBlk - 1) / kGradColBlk + (p.d_in + kGradColBlk - 1) / kGradColBlk;
     if ((long)p.T * p.k / 2048 * nb >= 4L * device_cu_count()) gr.split = 2048;
   }
-  // Per-pair input at small ranks (bf16): the dB pass reads dY once and also
-  // contracts it against B^T per 128-column block (fp32 partials); dH per row
-  // is their sum, then the dA pass (x per pair from HBM).  Otherwise dH by a
-  // contraction over all of d_out before the weight gradients: per-block
-  // partials of more ranks would cost more than the second read of dY, and
-  // with shared input the dA items (x rows from the caches) run best mixed
-  // with the dB items (HBM-bound) in one launch.
-  if (p.dtype == ACE_BF16 && p.per_pair && p.r_max <= kFusedDhMaxRank) {
+  // Ranks up to 16 (bf16) with per-pair input, or with shared input and
+  // outputs of at least kSharedDhMinOut columns: the dB pass reads dY once and
+  // also contracts it against B^T per 128-column block (fp32 partials); dH per
+  // row is their sum, then the dA pass.  Ranks 33..64 with shared input and
+  // wide outputs: the same with dB items of kWideCols columns (partials of 64
+  // ranks per 512 columns).  Otherwise dH by a contraction over all of d_out
+  // before the weight gradients: per-block partials of more ranks would cost
+  // more than the second read of dY, and for narrow outputs the dA items (x
+  // rows from the caches) run best mixed with the dB items in one launch.
+  const bool wide = p.dtype == ACE_BF16 && !p.per_pair && wide_dh(p.r_max, p.d_out);
+  if ((p.dtype == ACE_BF16 && (p.per_pair || p.d_out >= kSharedDhMinOut) && p.r_max <= kFusedDhMaxRank) ||
+      wide) {
     gr.phase = 1;
     gr.dHp = reinterpret_cast<float*>(base + L.dHp);
     gr.npos = P;
-    gr.dhs = dh_stride(p.r_max);
+    gr.dhs = wide ? 64 : dh_stride(p.r_max);
     gr.Bt = base + L.Bt;
-    e = launch_grads(p.dtype, gr, p.r_max, P, stream);
+    e = wide ? launch_grads_wide(gr, P, stream) : launch_grads(p.dtype, gr, p.r_max, P, stream);
     if (e != hipSuccess) return e;
     DhReduceArgs d{};
     d.dHp = gr.dHp;
     d.npos = P;
     d.dhs = gr.dhs;
-    d.nbB = (p.d_out + kGradColBlk - 1) / kGradColBlk;
+    d.nbB = wide ? (p.d_out + kWideCols - 1) / kWideCols : (p.d_out + kGradColBlk - 1) / kGradColBlk;
     d.offsets = p.rt->offsets;
     d.row_token = p.rt->row_token;
     d.row_slots = p.rt->row_slots;

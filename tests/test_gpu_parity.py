@@ -425,6 +425,28 @@ def test_small_and_odd_ranks(dtype, r_e):
         check_rel("dB", f64(out["dB"]), dB, tol)
 
 
+@pytest.mark.parametrize("path", ["expertwise", "grouped"])
+def test_shared_single_read_backward(path):
+    """Shared input at ranks up to 16 with an output of at least 1280
+    columns: the dB pass forms the dH partials per 128-column block (dY read
+    once).  d_out = 1320 leaves a 40-column last block; expert keys at rank 8
+    and group keys at rank 16 (two experts per group, rows serving two
+    slots), pair weights."""
+    cfg = W.CONFIGS["olmoe_bf16"].scaled(T=300, d_model=136, d_ffn=1320, r_e=8,
+                                         groups=("consecutive", 2))
+    c = make_case(cfg, path, seed=14, with_w=True)
+    assert max(c.ranks) <= 16 and c.d_out == 1320
+    say(f"shared single-read backward {path} r={max(c.ranks)} d_out={c.d_out}")
+    out = run_gpu(c, reuse_h=True)
+    tol = TOL["bf16"]
+    check_rel("delta", f64(out["y"]), oracle_fwd(c), tol)
+    dx, dA, dB = oracle_bwd(c)
+    check_all("dx", f64(out["dx"]), dx, tol)
+    check_all("dA", f64(out["dA"]), dA, tol)
+    check_rel("dB", f64(out["dB"]), dB, tol)
+    check_dB_rows("dB", f64(out["dB"]), dB, c.ranks, c.d_out, tol)
+
+
 @pytest.mark.parametrize("r_e", [4, 2])
 def test_per_pair_single_read_backward(r_e):
     """Per-pair input at ranks <= 16 runs the backward whose dB pass also
@@ -445,17 +467,19 @@ def test_per_pair_single_read_backward(r_e):
         check_rel("dB", f64(out["dB"]), dB, tol)
 
 
+@pytest.mark.parametrize("path", ["grouped", "pairs_shared"])
 @pytest.mark.parametrize("d_ffn", [4136, 6152])
-def test_split_rank_contraction(d_ffn):
-    """Rank-64 group keys whose rows serve several slots, with a long output
-    dimension and few pair positions: the backward's rank contraction over
-    d_ffn runs in two K ranges (fp32 partials per position) and a finishing
-    pass that sums them and forms the row sums.  d_ffn is ragged against the
-    range length and the 64-column stages."""
-    cfg = W.CONFIGS["mixtral_bf16"].scaled(T=700, d_model=136, d_ffn=d_ffn)
-    c = make_case(cfg, "grouped", seed=12, with_w=True)
+def test_wide_single_read_backward(d_ffn, path):
+    """Rank-64 group keys with shared input and a wide output: the dB items
+    take 512 dY columns and also form the dH partials per 512-column block
+    (dY read once), which are summed per row (rows serving several slots on
+    the grouped path, pair weights).  d_ffn is ragged against the 512-column
+    blocks, the 128-column sub-tiles and the 64-pair stages; T gives a few
+    split chunks per key."""
+    cfg = W.CONFIGS["mixtral_bf16"].scaled(T=1500, d_model=136, d_ffn=d_ffn)
+    c = make_case(cfg, path, seed=12, with_w=True)
     assert max(c.ranks) == 64 and c.d_out == d_ffn
-    say(f"split rank contraction T={cfg.T} d_out={c.d_out}")
+    say(f"wide single-read backward {path} T={cfg.T} d_out={c.d_out}")
     out = run_gpu(c, reuse_h=True)
     tol = TOL["bf16"]
     check_rel("delta", f64(out["y"]), oracle_fwd(c), tol)
