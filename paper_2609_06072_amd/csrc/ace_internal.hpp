@@ -70,17 +70,8 @@ struct ContractArgs {
   // per row (out_t column u - offsets[q], out_dense) -- dH_u = s B^T G_u
   int32_t row_sum;
   const int32_t* pair_row;    // row_sum: row serving each pair
-  // K split (bf16, kSrcPairList, ranks 33..64, set by the launcher): the
-  // partial launch writes raw fp32 results per pair position and K range to
-  // kpart [ksplit][npos][64]; the finish launch sums them in split order and
-  // runs the epilogue.  kpart null: no split.
-  float* kpart;
-  long npos;
-  int32_t ksplit, kchunk;
   KeyTable keys;
 };
-// K ranges of a split rank contraction (kpart holds kContractKSplit x P x 64 fp32)
-constexpr int kContractKSplit = 2;
 
 struct ExpandArgs {
   const void* H;              // [U][rpad], scaled, zero beyond r_q

@@ -302,16 +302,6 @@ struct CDma {
   static_assert(WROWS / RPI <= NWV * NW, "weight copies");
 };
 
-// Waves per block of the bf16 contraction (16 tile rows each).  At ranks
-// 33..64 the weight rows of a stage are as many as the source rows of a
-// 64-row tile; tiles of 128 rows (eight waves) stage each weight row once per
-// 128 source rows, which pays when there are tiles enough for about two
-// blocks per CU (at one per CU the 64-row tiles are faster).  Only the
-// pair-position contraction knows its tile count on the host (its positions
-// are the P pairs; a row count is known on the device only).
-constexpr int kWideTileMinPerCu2 = 3;   // 128-row tiles when tiles >= 1.5 x CUs
-constexpr int kSplitMinK = 4096;        // K split only for contractions at least this long
-
 // Chunk swizzle of weight row w (CPR 16-byte chunks per staged row).  A
 // fragment read touches the rows rank_of_row(rb, i), i = 0..15: w & 3 = i & 3,
 // bit 2 of w = rb & 1 and bits 3.. = i >> 2, so w & (CPR - 1) alone would give
@@ -389,13 +379,8 @@ __device__ inline void row_sum_store(const ContractArgs& a, int q, const f32x4 (
   }
 }
 
-// MODE: kModeFull (the whole contraction and the epilogue), kModePart (one K
-// range of a split contraction, raw fp32 results out), kModeFinish (the
-// split ranges summed, then the epilogue)
-constexpr int kModeFull = 0, kModePart = 1, kModeFinish = 2;
-
-template <int RB, int NWV, int MODE>
-__global__ __launch_bounds__(64 * NWV, NWV == 8 ? 4 : (RB == 8 ? 2 : 1)) void contract_dma_kernel(ContractArgs a) {
+template <int RB, int NWV>
+__global__ __launch_bounds__(64 * NWV, RB == 8 ? 2 : 1) void contract_dma_kernel(ContractArgs a) {
   using G = CDma<RB, NWV>;
   constexpr int KC = G::KC, NBUF = G::NBUF, KB = Tr<__bf16>::KB;
   constexpr int CPR = G::CPR, RPI = G::RPI;
@@ -412,17 +397,11 @@ __global__ __launch_bounds__(64 * NWV, NWV == 8 ? 4 : (RB == 8 ? 2 : 1)) void co
   const int n_keys = a.keys.n_keys;
   const int bucket = blockIdx.x % kXcds;
   const int K = a.K, k = a.k;
-  // K split: the partial launch (ksplit > 1, not finish) takes tiles of
-  // ROWS pair positions, each against K range ks of the tile, and writes raw
-  // fp32 results per position; the finish launch sums them in split order and
-  // runs the epilogue on its usual tiles
-  constexpr bool part = MODE == kModePart, finish = MODE == kModeFinish;
-  const int nsplit = part ? a.ksplit : 1;
-  const bool rsum = a.row_sum != 0 && !part;   // implies kSrcPairList
-  const int TS = part ? G::ROWS : contract_tile(a.row_sum, k, G::ROWS);
+  const bool rsum = a.row_sum != 0;   // implies kSrcPairList
+  const int TS = contract_tile(a.row_sum, k, G::ROWS);
   build_bucket_table(a.offsets, a.src_mode == kSrcPairList ? a.ppos : nullptr, n_keys, TS, bucket,
                      seg, bstart, bfirst, scan);
-  const int total = bstart[n_keys] * nsplit;
+  const int total = bstart[n_keys];
   const int stride = gridDim.x / kXcds;  // the grid is a multiple of kXcds
   // wave-uniform values kept in scalar registers (uniform branches, no exec masks)
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -432,14 +411,10 @@ __global__ __launch_bounds__(64 * NWV, NWV == 8 ? 4 : (RB == 8 ? 2 : 1)) void co
   const int cpos = lane & (CPR - 1), crow = lane / CPR;   // 16-byte position / row inside a copy
 
   for (int idx = blockIdx.x / kXcds; idx < total; idx += stride) {
-    const int ti = idx / nsplit, ks = idx - ti * nsplit;   // tile of the bucket, K range
-    const int q = upper_index(bstart, n_keys, ti);
+    const int q = upper_index(bstart, n_keys, idx);
     const int lo = seg[q];
-    int u0 = lo + (bfirst[q] + ti - bstart[q]) * TS;
-    // contraction indices k_lo .. k_lo + Kr of this block (relative below)
-    const int k_lo = part ? ks * a.kchunk : 0;
-    const int Kr = part ? min(K - k_lo, a.kchunk) : K;
-    const int nst = finish ? 0 : (Kr + KC - 1) / KC;   // finish: no stages
+    int u0 = lo + (bfirst[q] + idx - bstart[q]) * TS;
+    const int nst = (K + KC - 1) / KC;
     int u_end = seg[q + 1];
     const int r_q = a.keys.rank[q], roff = a.keys.roff[q];
     // row sums: rows ua .. ub - 1 start inside the window [u0, u0 + TS); their
@@ -504,7 +479,7 @@ __global__ __launch_bounds__(64 * NWV, NWV == 8 ? 4 : (RB == 8 ? 2 : 1)) void co
     // copies of stage st (columns past K are clamped; masked at the reads)
     auto issue = [&](int st) {
       const int b = st % NBUF;
-      const int k0 = k_lo + st * KC;
+      const int k0 = st * KC;
 #pragma unroll
       for (int i = 0; i < G::NS; ++i)
         dma16(sptr[i] + min(k0 + scol[i], K - 8),
@@ -540,7 +515,7 @@ __global__ __launch_bounds__(64 * NWV, NWV == 8 ? 4 : (RB == 8 ? 2 : 1)) void co
       const int rl = 16 * wave + c16;
       bf16x8 sf = *reinterpret_cast<const bf16x8*>(&Sb[b][rl * KC * 2 + ((chunk ^ (rl & (CPR - 1))) << 4)]);
       if (ragged) {
-        const int nv = Kr - (kk + 8 * g);
+        const int nv = K - (kk + 8 * g);
 #pragma unroll
         for (int e = 0; e < 8; ++e)
           if (e >= nv) sf[e] = (__bf16)0.f;
@@ -553,44 +528,22 @@ __global__ __launch_bounds__(64 * NWV, NWV == 8 ? 4 : (RB == 8 ? 2 : 1)) void co
         acc[rb] = Tr<__bf16>::mma(wf, sf, acc[rb]);   // D[rank][row]
       }
     };
-    if constexpr (finish) {
-      // the K-split partials of this lane's position, summed in split order
-      // (positions past the tile re-read the last one; never stored)
-      const int pos = min(u0 + 16 * wave + c16, u_end - 1);
+    // full stages: a loop with no branch around the matrix work (a branch
+    // there made the compiler copy the accumulators every stage)
+    const int nst_full = K / KC;
+    for (int st = 0; st < nst_full; ++st) {
+      begin_stage(st);
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
-        for (int sp = 0; sp < a.ksplit; ++sp)
-          acc[rb] += *reinterpret_cast<const f32x4*>(
-              a.kpart + ((size_t)sp * a.npos + pos) * (16 * RB) + rank_of_row<__bf16>(rb, 4 * g));
-    } else {
-      // full stages: a loop with no branch around the matrix work (a branch
-      // there made the compiler copy the accumulators every stage)
-      const int nst_full = Kr / KC;
-      for (int st = 0; st < nst_full; ++st) {
-        begin_stage(st);
-#pragma unroll
-        for (int kb = 0; kb < KC / KB; ++kb) kblock(st, kb, false);
-      }
-      if (nst_full < nst) {   // block-uniform: the last, partial stage
-        const int st = nst_full;
-        begin_stage(st);
-#pragma unroll
-        for (int kb = 0; kb < KC / KB; ++kb) {
-          const int kk = st * KC + kb * KB;
-          if (kk < Kr) kblock(st, kb, kk + KB > Kr);
-        }
-      }
+      for (int kb = 0; kb < KC / KB; ++kb) kblock(st, kb, false);
     }
-    if constexpr (part) {
-      // raw results of this K range per position, [split][position][rank]
-      const int u = u0 + 16 * wave + c16;
-      if (u < u_end) {
+    if (nst_full < nst) {   // block-uniform: the last, partial stage
+      const int st = nst_full;
+      begin_stage(st);
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
-          *reinterpret_cast<f32x4*>(a.kpart + ((size_t)ks * a.npos + u) * (16 * RB) +
-                                    rank_of_row<__bf16>(rb, 4 * g)) = acc[rb];
+      for (int kb = 0; kb < KC / KB; ++kb) {
+        const int kk = st * KC + kb * KB;
+        if (kk < K) kblock(st, kb, kk + KB > K);
       }
-      continue;
     }
 
     const float s = a.alpha / (float)r_q;
@@ -613,16 +566,15 @@ __global__ __launch_bounds__(64 * NWV, NWV == 8 ? 4 : (RB == 8 ? 2 : 1)) void co
   }
 }
 
-template <int RB, int NWV, int MODE = kModeFull>
+template <int RB, int NWV>
 hipError_t launch_contract_dma(const ContractArgs& a, long P, hipStream_t stream) {
   using G = CDma<RB, NWV>;
-  constexpr bool part = MODE == kModePart;
-  const int TS = part ? G::ROWS : contract_tile(a.row_sum, a.k, G::ROWS);
-  // tiles per bucket <= (all tiles) / kXcds + n_keys, times the K ranges
-  const long pb = P > 0 ? (((P + TS - 1) / TS + a.keys.n_keys) / kXcds + a.keys.n_keys) * (part ? a.ksplit : 1) : 0;
+  const int TS = contract_tile(a.row_sum, a.k, G::ROWS);
+  // tiles per bucket <= (all tiles) / kXcds + n_keys
+  const long pb = P > 0 ? ((P + TS - 1) / TS + a.keys.n_keys) / kXcds + a.keys.n_keys : 0;
   const long cap = (long)G::BLOCKS_PER_CU * device_cu_count() / kXcds;
   const int grid = (int)(pb < cap ? pb : cap) * kXcds;
-  if (grid > 0) contract_dma_kernel<RB, NWV, MODE><<<grid, G::THREADS, 0, stream>>>(a);
+  if (grid > 0) contract_dma_kernel<RB, NWV><<<grid, G::THREADS, 0, stream>>>(a);
   return hipGetLastError();
 }
 
@@ -632,25 +584,6 @@ hipError_t launch_contract_rb(const ContractArgs& a, long P, hipStream_t stream)
   // tiles per bucket <= (all tiles) / kXcds + n_keys
   const long per_bucket = P > 0 ? ((P + BM - 1) / BM + a.keys.n_keys) / kXcds + a.keys.n_keys : 0;
   if constexpr (std::is_same<T, __bf16>::value) {
-    if constexpr (RB == 4) {
-      if (a.src_mode == kSrcPairList) {
-        const int TS8 = contract_tile(a.row_sum, a.k, CDma<RB, 8>::ROWS);
-        if (2 * (P / TS8) >= (long)kWideTileMinPerCu2 * device_cu_count())
-          return launch_contract_dma<RB, 8>(a, P, stream);
-        // too few 128-row tiles for the GPU: with a long contraction, split
-        // it in kContractKSplit ranges (fp32 partials per position), so that
-        // the 128-row tiles fill the GPU, then sum and finish on 64-row tiles
-        if (a.kpart && a.row_sum && a.K >= kSplitMinK) {
-          ContractArgs b = a;
-          b.ksplit = kContractKSplit;
-          b.kchunk = ((a.K + kContractKSplit - 1) / kContractKSplit + 63) / 64 * 64;
-          b.npos = P;
-          hipError_t e = launch_contract_dma<RB, 8, kModePart>(b, P, stream);
-          if (e != hipSuccess) return e;
-          return launch_contract_dma<RB, 4, kModeFinish>(b, P, stream);
-        }
-      }
-    }
     return launch_contract_dma<RB, 4>(a, P, stream);
   }
   const long cap = 6L * device_cu_count() / kXcds;

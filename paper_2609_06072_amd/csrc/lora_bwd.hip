@@ -39,7 +39,7 @@ constexpr int kMaxJobs = kMaxKeys + 3;
 size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 
 struct WsLayout {
-  size_t At, Bt, Ht, dHt, dHf, dHrow, part, dHp, cpart, total;
+  size_t At, Bt, Ht, dHt, dHf, dHrow, part, dHp, total;
 };
 
 // Ranks up to 16 take the backward in which the dB pass also contracts dY
@@ -50,11 +50,10 @@ int dh_stride(int r_max) { return r_max <= 8 ? 8 : 16; }
 // least this many columns: below it the second read of dY is cheap and the
 // dA items overlap best with the dB items in one launch.
 constexpr int kSharedDhMinOut = 1280;
-// Ranks 33..64 (bf16, shared input): dB items of kWideCols columns form the
-// dH partials for outputs of at least this many columns (a contraction over
-// all of d_out, re-reading dY, otherwise).
-constexpr int kWideDhMinOut = 4096;
-bool wide_dh(int r_max, int d_out) { return rank_blocks(r_max) == 4 && d_out >= kWideDhMinOut; }
+// Ranks 33..64 (bf16, shared input, outputs of at least kSharedDhMinOut
+// columns): dB items of kWideCols columns form the dH partials (a
+// contraction over all of d_out, re-reading dY, otherwise).
+bool wide_dh(int r_max, int d_out) { return rank_blocks(r_max) == 4 && d_out >= kSharedDhMinOut; }
 
 // Workspace regions for element size es: At [d_in][R], Bt [R][d_out],
 // Ht/dHt [R][ldh] (column = row index inside the key's segment), dense dH
@@ -79,8 +78,6 @@ WsLayout ws_layout(int T, int k, int d_in, int d_out, int n_keys, int R, int r_m
   const size_t nbW = (d_out + kWideCols - 1) / kWideCols;
   w.dHp = o;   o += r_max <= kFusedDhMaxRank ? align256(sizeof(float) * nbB * P * dh_stride(r_max))
                     : wide_dh(r_max, d_out) ? align256(sizeof(float) * nbW * P * 64) : 0;
-  // K-split partials of the rank contraction (ranks 33..64, bf16)
-  w.cpart = o; o += rank_blocks(r_max) == 4 ? align256(sizeof(float) * kContractKSplit * P * 64) : 0;
   w.total = o + 256;
   return w;
 }
@@ -531,7 +528,6 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
       c.ppos = ppos;
       c.pair_row = p.rt->pair_row;
       c.row_sum = 1;
-      c.kpart = rank_blocks(p.r_max) == 4 ? reinterpret_cast<float*>(base + L.cpart) : nullptr;
       c.out_w = 0;
       c.out_t = base + L.dHt;
       c.out_dense = base + L.dHf;
