@@ -741,7 +741,8 @@ __global__ __launch_bounds__(kWideThreads, 2) void grad_wide_kernel(GradArgs a) 
 
 // dH per row from the phase-1 partials.  Thread t takes row blk * (256 / nq)
 // + t / nq and rank quad t % nq (nq = dhs / 4); the partials of the nbB column
-// blocks are loaded eight at a time and summed in block order.
+// blocks are loaded NL at a time and summed in block order.
+template <int NL>
 __global__ __launch_bounds__(kThreads) void dh_reduce_kernel(DhReduceArgs a) {
   __shared__ int seg[kMaxKeys + 1];
   const int n_keys = a.keys.n_keys;
@@ -766,12 +767,12 @@ __global__ __launch_bounds__(kThreads) void dh_reduce_kernel(DhReduceArgs a) {
       f32x4 v = f32x4{0.f, 0.f, 0.f, 0.f};
       const f32x4* src = reinterpret_cast<const f32x4*>(a.dHp + (size_t)p * a.dhs + r0);
       const size_t cstride = (size_t)a.npos * a.dhs / 4;
-      for (int c0 = 0; c0 < a.nbB; c0 += 8) {
-        f32x4 t[8];
+      for (int c0 = 0; c0 < a.nbB; c0 += NL) {
+        f32x4 t[NL];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) t[j] = src[(size_t)min(c0 + j, a.nbB - 1) * cstride];
+        for (int j = 0; j < NL; ++j) t[j] = src[(size_t)min(c0 + j, a.nbB - 1) * cstride];
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
+        for (int j = 0; j < NL; ++j)
           if (c0 + j < a.nbB) v += t[j];
       }
       const f32x4 h = (v * s) * w;
@@ -1323,7 +1324,13 @@ hipError_t launch_dh_reduce(const DhReduceArgs& d, long U, hipStream_t stream) {
   if (d.dhs != 8 && d.dhs != 16 && d.dhs != 64) return hipErrorInvalidValue;
   const int rows_per_block = kThreads / (d.dhs / 4);
   const long blocks = (U + rows_per_block - 1) / rows_per_block;
-  if (blocks > 0) dh_reduce_kernel<<<(int)blocks, kThreads, 0, stream>>>(d);
+  if (blocks > 0) {
+    // loads in flight per thread: at most the column blocks (more would
+    // re-read the last one)
+    if (d.nbB >= 16) dh_reduce_kernel<16><<<(int)blocks, kThreads, 0, stream>>>(d);
+    else if (d.nbB >= 8) dh_reduce_kernel<8><<<(int)blocks, kThreads, 0, stream>>>(d);
+    else dh_reduce_kernel<4><<<(int)blocks, kThreads, 0, stream>>>(d);
+  }
   return hipGetLastError();
 }
 
