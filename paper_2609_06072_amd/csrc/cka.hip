@@ -14,7 +14,7 @@
 // Launches (all deterministic):
 //   project -- Pt = A X^T, [R][ldp] fp32: a 64 x 256-tile MFMA GEMM over
 //              K = d_in (eight waves), operands copied global -> LDS
-//              directly, four stages in flight
+//              directly, two stages in LDS (three blocks per CU)
 //   mean    -- the probe mean of every row of Pt; bf16 inputs: also the
 //              centred rows split as v = hi + lo (both bf16, |lo| <= 2^-9 |v|)
 //   gram    -- partial M over chunks of the probe: upper-triangle 64 x 64
@@ -22,9 +22,10 @@
 //              M = hi^T hi + hi^T lo + lo^T hi on the bf16 matrix cores (the
 //              dropped lo^T lo is below 2^-16 of |v_a v_b|).  fp32 inputs:
 //              fp32 MFMA, centring on load.
+//   msum    -- M: the Gram partials summed in chunk order (upper-triangle
+//              tiles), every element with all its chunks' loads in flight
 //   bgram   -- partial G_e = B_e^T B_e over chunks of 256 rows of B_e
-//   pairs   -- num_ij = <G_i M_ij, M_ij G_j> for i <= j (partials summed in
-//              chunk order)
+//   pairs   -- num_ij = <G_i M_ij, M_ij G_j> for i <= j
 //   score   -- S_ij = num_ij / sqrt(num_ii num_jj); 0 when a norm is 0
 #include "ace_device.hpp"
 #include "ace_internal.hpp"
@@ -43,7 +44,7 @@ constexpr int kBO = 256;   // rows of B_e per B^T B chunk
 size_t a256(size_t b) { return (b + 255) & ~(size_t)255; }
 
 struct CkaLayout {
-  size_t Pt, mean, part, Gb, num, Phi, Plo, total;
+  size_t Pt, mean, part, M, Gb, num, Phi, Plo, total;
   int ldp, splits, kchunk, nbo;
 };
 
@@ -64,6 +65,7 @@ CkaLayout cka_layout(int N, int d_out, int E, int r) {
   L.Pt = o;   o += a256(R * L.ldp * 4);
   L.mean = o; o += a256(R * 4);
   L.part = o; o += a256((size_t)splits * R * R * 4);
+  L.M = o;    o += a256(R * R * 4);
   L.nbo = (d_out + kBO - 1) / kBO;
   L.Gb = o;   o += a256((size_t)E * L.nbo * r * r * 4);
   L.num = o;  o += a256((size_t)E * E * 4);
@@ -80,6 +82,7 @@ struct CkaArgs {
   float* Pt;         // [R][ldp]
   float* mean;       // [R]
   float* part;       // [splits][R][R]
+  float* M;          // [R][R], upper-triangle tiles
   float* Gb;         // [E][nbo][r][r] partials of B_e^T B_e
   float* num;        // [E][E]
   __bf16* Phi;       // [R][ldp] centred Pt split as hi + lo (bf16 inputs; zero past N)
@@ -116,7 +119,9 @@ template <typename T>
 __global__ __launch_bounds__(kPThreads) void cka_project_kernel(CkaArgs a) {
   using F = typename Tr<T>::frag;
   constexpr int PER = Tr<T>::PER, KB = Tr<T>::KB;   // KB * sizeof(T) = 64 bytes
-  constexpr int NBUF = 4;
+  // two stages (40 KB): three blocks per CU, so that the 64-row tiles of a
+  // 10,000-row probe all run at once (four stages fit two blocks per CU)
+  constexpr int NBUF = 2;
   constexpr int XB = kPN * 64, AB = kPC * 64;       // stage bytes of each operand
   __shared__ __attribute__((aligned(16))) char xs[NBUF][XB];
   __shared__ __attribute__((aligned(16))) char as[NBUF][AB];
@@ -445,6 +450,30 @@ __global__ __launch_bounds__(kThreads) void cka_gram_kernel<false>(CkaArgs a) {
     }
 }
 
+// ---------------------------------------------------------------- M
+
+// Block (tile pair p, part h): the elements h * 256 + t of the 64 x 64 tile
+// (ta, tb) of M, each the sum of its chunks' partials in chunk order.
+__global__ __launch_bounds__(kThreads) void cka_msum_kernel(CkaArgs a) {
+  const int R = a.R, nt = (R + kGT - 1) / kGT;
+  int ta, tb;
+  upper_pair(blockIdx.x, nt, &ta, &tb);
+  const int e = blockIdx.y * kThreads + threadIdx.x;
+  const int row = ta * kGT + e / kGT, col = tb * kGT + e % kGT;
+  if (row >= R || col >= R) return;
+  const size_t off = (size_t)row * R + col, cs = (size_t)R * R;
+  float m = 0.f;
+  for (int s = 0; s < a.splits; s += 8) {
+    float v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = a.part[(size_t)min(s + i, a.splits - 1) * cs + off];
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      if (s + i < a.splits) m += v[i];
+  }
+  a.M[off] = m;
+}
+
 // ---------------------------------------------------------------- B^T B
 
 // Block (e, c): partial G_e over rows c*kBO .. of B_e, all rows loaded at once.
@@ -467,8 +496,8 @@ __global__ __launch_bounds__(kThreads) void cka_bgram_kernel(CkaArgs a) {
 
 // ---------------------------------------------------------------- pairs
 
-// Block per expert pair i <= j: M_ij (partials summed in chunk order, read
-// from the upper triangle of the symmetric M), then <G_i M_ij, M_ij G_j>.
+// Block per expert pair i <= j: M_ij (read from the upper triangle of the
+// symmetric M), then <G_i M_ij, M_ij G_j>.
 __global__ __launch_bounds__(kThreads) void cka_pairs_kernel(CkaArgs a) {
   __shared__ float Gi[64 * 64], Gj[64 * 64], Mij[64 * 64];
   __shared__ float red[kThreads];
@@ -484,19 +513,7 @@ __global__ __launch_bounds__(kThreads) void cka_pairs_kernel(CkaArgs a) {
     Gi[t] = gi;
     Gj[t] = gj;
     const int row = i * r + t / r, col = j * r + t % r;
-    const size_t off = (size_t)min(row, col) * R + max(row, col);
-    // eight chunks' loads in flight at a time; the sum keeps chunk order
-    float m = 0.f;
-    int s = 0;
-    for (; s + 8 <= a.splits; s += 8) {
-      float v[8];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) v[i] = a.part[(size_t)(s + i) * R * R + off];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) m += v[i];
-    }
-    for (; s < a.splits; ++s) m += a.part[(size_t)s * R * R + off];
-    Mij[t] = m;
+    Mij[t] = a.M[(size_t)min(row, col) * R + max(row, col)];
   }
   __syncthreads();
   float acc = 0.f;
@@ -542,6 +559,7 @@ hipError_t launch_cka_t(const CkaProblem& p, void* ws, hipStream_t stream) {
   a.Pt = reinterpret_cast<float*>(base + L.Pt);
   a.mean = reinterpret_cast<float*>(base + L.mean);
   a.part = reinterpret_cast<float*>(base + L.part);
+  a.M = reinterpret_cast<float*>(base + L.M);
   a.Gb = reinterpret_cast<float*>(base + L.Gb);
   a.num = reinterpret_cast<float*>(base + L.num);
   a.S = p.S;
@@ -573,6 +591,10 @@ hipError_t launch_cka_t(const CkaProblem& p, void* ws, hipStream_t stream) {
       cka_gram_kernel<true><<<grid, kThreads, 0, stream>>>(a);
     else
       cka_gram_kernel<false><<<grid, kThreads, 0, stream>>>(a);
+  }
+  {
+    const int nt = (R + kGT - 1) / kGT;
+    cka_msum_kernel<<<dim3(nt * (nt + 1) / 2, kGT * kGT / kThreads), kThreads, 0, stream>>>(a);
   }
   cka_bgram_kernel<T><<<dim3(p.E, L.nbo), kThreads, 0, stream>>>(a);
   cka_pairs_kernel<<<p.E * (p.E + 1) / 2, kThreads, 0, stream>>>(a);
