@@ -490,6 +490,31 @@ def test_wide_single_read_backward(d_ffn, path):
     check_dB_rows("dB", f64(out["dB"]), dB, c.ranks, c.d_out, tol)
 
 
+def test_wide_single_read_empty_group():
+    """The single-read backward at rank 64 (shared input, 1352 output
+    columns) when one group has no pairs: its dA and dB are exactly zero,
+    and every token's two experts share the other group, so every row
+    serves two slots."""
+    cfg = W.CONFIGS["mixtral_bf16"].scaled(T=300, d_model=136, d_ffn=1352)
+    c = make_case(cfg, "grouped", seed=16, with_w=True)
+    e2g = c.rt.expert_to_group
+    keep = [e for e in range(cfg.E) if e2g[e] == 0]
+    rng = np.random.default_rng(16)
+    ids = np.stack([rng.permutation(keep)[:cfg.k] for _ in range(cfg.T)]).astype(np.int32)
+    c.rt = W.Routing(ids, c.rt.topk_w, e2g, c.rt.group_rank, c.rt.expert_rank)
+    assert max(c.ranks) == 64 and c.d_out == 1352
+    say(f"wide single-read backward, empty group T={cfg.T} d_out={c.d_out}")
+    out = run_gpu(c, reuse_h=True)
+    off = np.concatenate([[0], np.cumsum(c.ranks)])
+    lo, hi = off[1], off[2]
+    assert not out["dA"][lo:hi].any() and not out["dB"][c.d_out * lo: c.d_out * hi].any()
+    tol = TOL["bf16"]
+    dx, dA, dB = oracle_bwd(c)
+    check_all("dx", f64(out["dx"]), dx, tol)
+    check_rel("dA", f64(out["dA"]), dA, tol)
+    check_rel("dB", f64(out["dB"]), dB, tol)
+
+
 def test_max_rank_and_many_groups():
     cfg = W.CONFIGS["olmoe_bf16"].scaled(T=150, d_model=128, d_ffn=64, r_e=64,
                                          groups=("consecutive", 4))
