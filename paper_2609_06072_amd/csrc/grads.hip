@@ -489,12 +489,14 @@ __global__ __launch_bounds__(kThreads, RB <= 4 ? 3 : 1) void grad_dma_kernel(Gra
 // an fp32 dH partial per pair position and 512-column block (rank stride 64),
 // which dh_reduce sums per row.  The dH contraction over all of d_out before
 // the weight gradients, and its second read of dY, are not run.
-// Eight waves: wave w accumulates dB of the item's columns 64w .. 64w+63 and
-// computes dH of rank block w % 4 for the pair blocks w / 4 and w / 4 + 2 of
-// every stage, with its B_q^T fragments over the item's 512 columns held in
-// registers for the whole item.  The dB results go out in the layout of the
-// four 128-column items they cover (direct stores or split partials), so the
-// split reduce after the dA items is the usual one.
+// Eight waves in two roles: waves 0-3 accumulate dB of one 128-column
+// sub-tile each for all 64 ranks; waves 4-7 compute dH, each for two rank
+// blocks and two pair blocks of every stage, with their B_q^T fragments over
+// the item's 512 columns held in registers for the whole item (so every dY
+// fragment a dH wave reads from LDS feeds two rank blocks).  The dB results
+// go out in the layout of the four 128-column items they cover (direct
+// stores or split partials), so the split reduce after the dA items is the
+// usual one.
 constexpr int kWideWaves = 8;
 constexpr int kWideThreads = 64 * kWideWaves;
 
@@ -576,89 +578,10 @@ __device__ __forceinline__ void wide_item(const GradArgs& a, WideSmem& sm, int q
           __builtin_amdgcn_readfirstlane(lds_addr(&sm.S[b][rr0 * RS * 2])));
   };
 
-  // B_q^T fragments of this wave's rank block over the item's columns (zero
-  // past r_q and past d_out)
-  const int rbw = wave & 3;
-  bf16x8 bt[kWideCols / 32];
-  {
-    const int rr = 16 * rbw + c16;
-    const __bf16* Btp = static_cast<const __bf16*>(a.Bt) + (size_t)(roff + min(rr, r_q - 1)) * a.d_out;
-#pragma unroll
-    for (int kb = 0; kb < kWideCols / 32; ++kb) {
-      const int c = col0 + 32 * kb + 8 * g;
-      bt[kb] = Tr<__bf16>::load(Btp + min(c, a.d_out - 8));
-      if (c >= a.d_out || rr >= r_q) bt[kb] = Tr<__bf16>::zero();
-    }
-  }
-  f32x4 acc[4][RB];
-#pragma unroll
-  for (int cbi = 0; cbi < 4; ++cbi)
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) acc[cbi][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
-
   if (nst > 0) {
     fetch(0);
     issue(0);
   }
-  const int sub_b = wave >> 1;                 // this wave's dB sub-tile
-  const int nb0 = 64 * (wave & 1);             // and its first column there
-  // dB K-block kb of stage st (buffer b); the ragged form zeroes the pairs
-  // past the chunk
-  auto kblock = [&](int st, int b, int kb, bool ragged) {
-    const int kk = st * RS + kb * 32;
-    const int nv = nk - (kk + 8 * g);
-    bf16x8 sf[RB];
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      const int rr = 16 * rb + c16;
-      const int pos = (kb * 4 + g) ^ (rr & 7);
-      bf16x8 f = *reinterpret_cast<const bf16x8*>(&sm.S[b][rr * RS * 2 + pos * 16]);
-      if (ragged) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-          if (e >= nv) f[e] = (__bf16)0.f;
-      }
-      sf[rb] = f;
-    }
-    const char* Lb = &sm.L[b][sub_b * G::SUBBYTES];
-#pragma unroll
-    for (int cbi = 0; cbi < 4; ++cbi) {
-      const int n0 = nb0 + 16 * cbi;
-      s16x4 h2[2];
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int r = kb * 32 + 8 * g + 4 * h + (c16 >> 2);
-        const int c = (n0 >> 3) + ((c16 & 3) >> 1);
-        const int off = r * 256 + ((c ^ l_swz(r)) << 4) + ((c16 & 1) << 3);
-        h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(Lb + off));
-      }
-      const bf16x8 lf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(h2[0], h2[1], 0, 1, 2, 3, 4, 5, 6, 7));
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) acc[cbi][rb] = Tr<__bf16>::mma(lf, sf[rb], acc[cbi][rb]);   // D[n][r]
-    }
-  };
-  // dH of rank block rbw for pair blocks pb0 and pb0 + 2 of stage st over the
-  // item's 512 columns: D[rank][pair], stored per pair position
-  const int pb0 = wave >> 2;
-  auto dh_part = [&](int st, int b) {
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int r = 16 * (pb0 + 2 * j) + c16;   // stage row (pair) of this lane
-      f32x4 h = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int kb = 0; kb < kWideCols / 32; ++kb) {
-        const int c = (kb & 3) * 4 + g;
-        const bf16x8 lf = *reinterpret_cast<const bf16x8*>(
-            &sm.L[b][(kb >> 2) * G::SUBBYTES + r * 256 + ((c ^ l_swz(r)) << 4)]);
-        h = Tr<__bf16>::mma(bt[kb], lf, h);
-      }
-      const int kk = st * RS + r;   // chunk index of this lane's pair (rows past nk are copies)
-      if (kk < nk) {
-        const long pos = (long)kfirst + kk;
-        *reinterpret_cast<f32x4*>(a.dHp + ((size_t)cbw * a.npos + pos) * (16 * RB) + 16 * rbw + 4 * g) = h;
-      }
-    }
-  };
   // this wave's copies of stage st (and the row metadata of stage st + 1)
   // are done; the barrier then publishes every wave's copies
   auto begin_stage = [&](int st) {
@@ -667,47 +590,135 @@ __device__ __forceinline__ void wide_item(const GradArgs& a, WideSmem& sm, int q
     if (st + 1 < nst) issue(st + 1);
   };
   const int nst_full = nk / RS;
-  for (int st = 0; st < nst_full; ++st) {
-    begin_stage(st);
-    const int b = st & 1;
-#pragma unroll
-    for (int kb = 0; kb < RS / 32; ++kb) kblock(st, b, kb, false);
-    dh_part(st, b);
-  }
-  if (nst_full < nst) {   // block-uniform: the last, partial stage
-    const int st = nst_full;
-    begin_stage(st);
-    const int b = st & 1;
-#pragma unroll
-    for (int kb = 0; kb < RS / 32; ++kb) {
-      const int kk = st * RS + kb * 32;
-      if (kk < nk) kblock(st, b, kb, kk + 32 > nk);
-    }
-    dh_part(st, b);
-  }
 
-  // dB: columns col0 + 128 sub_b + nb0 + 16 cbi of the 128-column item
-  // (q, s, 4 cbw + sub_b), i.e. its wave 2 (w & 1) + cbi / 2, block cbi % 2
-  const int cb = SUB * cbw + sub_b;
-  if (cb >= a.nbB) return;   // wave-uniform: a sub-tile past d_out
-  const int nrb = (r_q + 15) >> 4;
-  if (ns == 1) {
+  if (wave < kWideWaves / 2) {
+    // ---- dB waves: wave d accumulates the item's sub-tile d (128 columns)
+    // for all ranks, D[n][r]
+    const int sub_b = wave;
+    f32x4 acc[8][RB];
 #pragma unroll
-    for (int cbi = 0; cbi < 4; ++cbi)
+    for (int cbi = 0; cbi < 8; ++cbi)
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
-        if (rb < nrb)
-          store_grad(a, true, q, cb * kColBlk, 2 * (wave & 1) + (cbi >> 1), cbi & 1, rb, lane,
-                     acc[cbi][rb]);
+      for (int rb = 0; rb < RB; ++rb) acc[cbi][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // K-block kb of stage st (buffer b); the ragged form zeroes the pairs
+    // past the chunk
+    auto kblock = [&](int st, int b, int kb, bool ragged) {
+      const int nv = nk - (st * RS + kb * 32 + 8 * g);
+      bf16x8 sf[RB];
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        const int rr = 16 * rb + c16;
+        const int pos = (kb * 4 + g) ^ (rr & 7);
+        bf16x8 f = *reinterpret_cast<const bf16x8*>(&sm.S[b][rr * RS * 2 + pos * 16]);
+        if (ragged) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (e >= nv) f[e] = (__bf16)0.f;
+        }
+        sf[rb] = f;
+      }
+      const char* Lb = &sm.L[b][sub_b * G::SUBBYTES];
+#pragma unroll
+      for (int cbi = 0; cbi < 8; ++cbi) {
+        const int n0 = 16 * cbi;
+        s16x4 h2[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int r = kb * 32 + 8 * g + 4 * h + (c16 >> 2);
+          const int c = (n0 >> 3) + ((c16 & 3) >> 1);
+          const int off = r * 256 + ((c ^ l_swz(r)) << 4) + ((c16 & 1) << 3);
+          h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(Lb + off));
+        }
+        const bf16x8 lf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(h2[0], h2[1], 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) acc[cbi][rb] = Tr<__bf16>::mma(lf, sf[rb], acc[cbi][rb]);
+      }
+    };
+    for (int st = 0; st < nst_full; ++st) {
+      begin_stage(st);
+#pragma unroll
+      for (int kb = 0; kb < RS / 32; ++kb) kblock(st, st & 1, kb, false);
+    }
+    if (nst_full < nst) {   // block-uniform: the last, partial stage
+      const int st = nst_full;
+      begin_stage(st);
+#pragma unroll
+      for (int kb = 0; kb < RS / 32; ++kb) {
+        const int kk = st * RS + kb * 32;
+        if (kk < nk) kblock(st, st & 1, kb, kk + 32 > nk);
+      }
+    }
+    // columns 16 cbi of the 128-column item (q, s, 4 cbw + d), i.e. its wave
+    // cbi / 2, block cbi % 2
+    const int cb = SUB * cbw + sub_b;
+    if (cb >= a.nbB) return;   // wave-uniform: a sub-tile past d_out
+    const int nrb = (r_q + 15) >> 4;
+    if (ns == 1) {
+#pragma unroll
+      for (int cbi = 0; cbi < 8; ++cbi)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+          if (rb < nrb) store_grad(a, true, q, cb * kColBlk, cbi >> 1, cbi & 1, rb, lane, acc[cbi][rb]);
+    } else {
+      const int item = sm.tb.istart[q] + s * a.nbB + cb;
+      f32x4* part = reinterpret_cast<f32x4*>(a.part) + (size_t)item * (4 * 2 * RB * 64);
+#pragma unroll
+      for (int cbi = 0; cbi < 8; ++cbi)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+          if (rb < nrb) part[(cbi * RB + rb) * 64 + lane] = acc[cbi][rb];
+    }
   } else {
-    const int item = sm.tb.istart[q] + s * a.nbB + cb;
-    f32x4* part = reinterpret_cast<f32x4*>(a.part) + (size_t)item * (4 * 2 * RB * 64);
+    // ---- dH waves: wave 4 + h takes rank blocks 2 (h & 1) and 2 (h & 1) + 1
+    // and pair blocks h >> 1 and (h >> 1) + 2 of every stage, so that each
+    // dY fragment read from LDS feeds two rank blocks; B_q^T fragments of its
+    // two rank blocks over the item's columns (zero past r_q and past d_out)
+    // stay in registers for the whole item.  D[rank][pair], stored per
+    // pair position.
+    const int h = wave - kWideWaves / 2;
+    const int rb0 = 2 * (h & 1), pb0 = h >> 1;
+    bf16x8 bt[2][kWideCols / 32];
 #pragma unroll
-    for (int cbi = 0; cbi < 4; ++cbi)
+    for (int i = 0; i < 2; ++i) {
+      const int rr = 16 * (rb0 + i) + c16;
+      const __bf16* Btp = static_cast<const __bf16*>(a.Bt) + (size_t)(roff + min(rr, r_q - 1)) * a.d_out;
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
-        if (rb < nrb)
-          part[(((2 * (wave & 1) + (cbi >> 1)) * 2 + (cbi & 1)) * RB + rb) * 64 + lane] = acc[cbi][rb];
+      for (int kb = 0; kb < kWideCols / 32; ++kb) {
+        const int c = col0 + 32 * kb + 8 * g;
+        bt[i][kb] = Tr<__bf16>::load(Btp + min(c, a.d_out - 8));
+        if (c >= a.d_out || rr >= r_q) bt[i][kb] = Tr<__bf16>::zero();
+      }
+    }
+    auto dh_part = [&](int st, int b) {
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int r = 16 * (pb0 + 2 * j) + c16;   // stage row (pair) of this lane
+        f32x4 hv[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+        for (int kb = 0; kb < kWideCols / 32; ++kb) {
+          const int c = (kb & 3) * 4 + g;
+          const bf16x8 lf = *reinterpret_cast<const bf16x8*>(
+              &sm.L[b][(kb >> 2) * G::SUBBYTES + r * 256 + ((c ^ l_swz(r)) << 4)]);
+#pragma unroll
+          for (int i = 0; i < 2; ++i) hv[i] = Tr<__bf16>::mma(bt[i][kb], lf, hv[i]);
+        }
+        const int kk = st * RS + r;   // chunk index of this lane's pair (rows past nk are copies)
+        if (kk < nk) {
+          float* dst = a.dHp + ((size_t)cbw * a.npos + kfirst + kk) * (16 * RB) + 16 * rb0 + 4 * g;
+#pragma unroll
+          for (int i = 0; i < 2; ++i) *reinterpret_cast<f32x4*>(dst + 16 * i) = hv[i];
+        }
+      }
+    };
+    for (int st = 0; st < nst_full; ++st) {
+      begin_stage(st);
+      dh_part(st, st & 1);
+    }
+    if (nst_full < nst) {
+      const int st = nst_full;
+      begin_stage(st);
+      dh_part(st, st & 1);
+    }
   }
 }
 
