@@ -42,13 +42,14 @@ constexpr int kColBlk = kGradColBlk;   // gradient columns per item
 // path's LDS row-index table).
 constexpr int kSplitRows = 1024;
 constexpr int kMaxSplit = 2048;
+constexpr int kMinSplit = 512;    // dB items of the wide single read at narrow outputs
 
 // Item table shared by the gradient kernels.  For key q the dB contraction
 // runs over bseg[q] .. bseg[q+1] and the dA contraction over aseg[q] ..
 // aseg[q+1]: pairs (positions in pair order; = rows when every row serves one
 // pair) and rows respectively, swapped in the pre-combined mode.  Items of q:
 // nsB(q) * nbB dB items, then nsA(q) * nbA dA items,
-// ns = max(1, ceil(count / split)).
+// ns = max(1, ceil(count / split)) (split_b for the dB items).
 struct GradTable {
   int bseg[kMaxKeys + 1];
   int aseg[kMaxKeys + 1];
@@ -82,7 +83,7 @@ __device__ inline void build_grad_table(const GradArgs& a, GradTable& tb, int* s
   __syncthreads();
   int items = 0, pitems = 0;
   if (t < n_keys) {
-    const int ib = n_split(tb.bseg[t + 1] - tb.bseg[t], a.split) * a.nbB;
+    const int ib = n_split(tb.bseg[t + 1] - tb.bseg[t], a.split_b) * a.nbB;
     const int ia = n_split(tb.aseg[t + 1] - tb.aseg[t], a.split) * a.nbA;
     items = ib + ia;
     pitems = a.phase == 1 ? ib : ia;
@@ -100,7 +101,7 @@ __device__ inline void build_grad_table(const GradArgs& a, GradTable& tb, int* s
   }
   if (blockIdx.x == 0 && t < n_keys) {   // for the reduce launch
     a.itab[t] = ex;
-    a.itab[kItabStride + t] = n_split(tb.bseg[t + 1] - tb.bseg[t], a.split);
+    a.itab[kItabStride + t] = n_split(tb.bseg[t + 1] - tb.bseg[t], a.split_b);
     a.itab[2 * kItabStride + t] = n_split(tb.aseg[t + 1] - tb.aseg[t], a.split);
   }
   __syncthreads();
@@ -120,7 +121,7 @@ __device__ inline Item decode_item(const GradArgs& a, const GradTable& tb, int i
   it.q = upper_index(tb.istart, n_keys, item);
   int local = item - tb.istart[it.q];
   const int npB = tb.bseg[it.q + 1] - tb.bseg[it.q];
-  const int nsB = n_split(npB, a.split);
+  const int nsB = n_split(npB, a.split_b);
   it.isB = local < nsB * a.nbB;
   int cnt;
   if (it.isB) {
@@ -137,7 +138,7 @@ __device__ inline Item decode_item(const GradArgs& a, const GradTable& tb, int i
     it.ns = n_split(cnt, a.split);
     it.kbase = tb.aseg[it.q];
   }
-  const int clen = chunk_len(cnt, it.ns, a.split);
+  const int clen = chunk_len(cnt, it.ns, it.isB ? a.split_b : a.split);
   it.k0 = it.s * clen;
   it.nk = max(0, min(cnt - it.k0, clen));
   return it;
@@ -149,7 +150,7 @@ __device__ inline int phase_item(const GradArgs& a, const GradTable& tb, int i) 
   const int q = upper_index(tb.pstart, a.keys.n_keys, i);
   const int local = i - tb.pstart[q];
   if (a.phase == 1) return tb.istart[q] + local;
-  return tb.istart[q] + n_split(tb.bseg[q + 1] - tb.bseg[q], a.split) * a.nbB + local;
+  return tb.istart[q] + n_split(tb.bseg[q + 1] - tb.bseg[q], a.split_b) * a.nbB + local;
 }
 
 // Row of the large operand for contraction index kabs of an item.
@@ -179,7 +180,7 @@ __device__ inline void load_chunk_rows_n(const GradArgs& a, const Item& it, int*
 
 __device__ inline void load_chunk_rows(const GradArgs& a, const Item& it, int* idx) {
   if (it.nk <= 0) return;
-  if (a.split > kSplitRows) load_chunk_rows_n<kMaxSplit / kThreads>(a, it, idx);
+  if ((it.isB ? a.split_b : a.split) > kSplitRows) load_chunk_rows_n<kMaxSplit / kThreads>(a, it, idx);
   else load_chunk_rows_n<kSplitRows / kThreads>(a, it, idx);
 }
 
@@ -730,7 +731,7 @@ __global__ __launch_bounds__(kWideThreads, 2) void grad_wide_kernel(GradArgs a) 
   {
     // wide items of key q: nsB(q) * nbW, key-major
     const int t = threadIdx.x;
-    const int cnt = t < n_keys ? n_split(sm.tb.bseg[t + 1] - sm.tb.bseg[t], a.split) * nbW : 0;
+    const int cnt = t < n_keys ? n_split(sm.tb.bseg[t + 1] - sm.tb.bseg[t], a.split_b) * nbW : 0;
     int total;
     const int ex = block_exclusive_scan(cnt, sm.scan, &total);
     if (t < n_keys) sm.wstart[t] = ex;
@@ -743,8 +744,8 @@ __global__ __launch_bounds__(kWideThreads, 2) void grad_wide_kernel(GradArgs a) 
     const int local = i - sm.wstart[q];
     const int s = local / nbW, cbw = local - s * nbW;
     const int cnt = sm.tb.bseg[q + 1] - sm.tb.bseg[q];
-    const int ns = n_split(cnt, a.split);
-    const int clen = chunk_len(cnt, ns, a.split);
+    const int ns = n_split(cnt, a.split_b);
+    const int clen = chunk_len(cnt, ns, a.split_b);
     const int k0 = s * clen;
     wide_item(a, sm, q, s, cbw, ns, k0, max(0, min(cnt - k0, clen)));
   }
@@ -1267,19 +1268,29 @@ __global__ __launch_bounds__(kThreads) void dx_dma_kernel(DxArgs a) {
   }
 }
 
-// Bytes of split partials (the item table follows them).
+// split 0 means kSplitRows, split_b 0 means split; the dA items take 1024 or
+// 2048 indices, the dB items also 512.
+bool normalize_splits(GradArgs& g) {
+  if (g.split == 0) g.split = kSplitRows;
+  if (g.split_b == 0) g.split_b = g.split;
+  return (g.split == kSplitRows || g.split == kMaxSplit) &&
+         (g.split_b == kMinSplit || g.split_b == kSplitRows || g.split_b == kMaxSplit);
+}
+
+// Bytes of split partials (the item table follows them): bounded for the
+// shortest chunks.
 size_t partial_bytes(long P, int n_keys, long nb, int rb) {
-  const long items = ((P + kSplitRows - 1) / kSplitRows + n_keys) * nb;
+  const long items = ((P + kMinSplit - 1) / kMinSplit + n_keys) * nb;
   return (size_t)items * 4 * 2 * rb * 64 * sizeof(f32x4);
 }
 
 template <int RB>
 hipError_t launch_grads_rb(int dtype, GradArgs g, long P, hipStream_t stream) {
   if (g.phase != 0 && dtype != ACE_BF16) return hipErrorInvalidValue;
-  if (g.split == 0) g.split = kSplitRows;
-  if (g.split != kSplitRows && g.split != kMaxSplit) return hipErrorInvalidValue;
+  if (!normalize_splits(g)) return hipErrorInvalidValue;
   const int nb = g.nbB + g.nbA;
-  const long items = ((P + kSplitRows - 1) / kSplitRows + g.keys.n_keys) * nb;
+  const int smin = g.split < g.split_b ? g.split : g.split_b;
+  const long items = ((P + smin - 1) / smin + g.keys.n_keys) * nb;
   g.itab = reinterpret_cast<int32_t*>(static_cast<char*>(g.part) +
                                       partial_bytes(P, g.keys.n_keys, nb, RB));
   const long cap = 8L * device_cu_count();
@@ -1292,7 +1303,7 @@ hipError_t launch_grads_rb(int dtype, GradArgs g, long P, hipStream_t stream) {
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (P > kSplitRows && g.phase != 1)   // the dB partials of phase 1 are reduced after phase 2
+  if (P > smin && g.phase != 1)   // the dB partials of phase 1 are reduced after phase 2
     grad_reduce_kernel<RB><<<g.keys.n_keys * nb * Red<RB>::SPLIT, kThreads, 0, stream>>>(g);
   return hipGetLastError();
 }
@@ -1318,13 +1329,12 @@ hipError_t launch_grads(int dtype, GradArgs g, int r_max, long P, hipStream_t st
 hipError_t launch_grads_wide(GradArgs g, long P, hipStream_t stream) {
   g.nbB = (g.d_out + kColBlk - 1) / kColBlk;
   g.nbA = (g.d_in + kColBlk - 1) / kColBlk;
-  if (g.split == 0) g.split = kSplitRows;
-  if (g.split != kSplitRows && g.split != kMaxSplit) return hipErrorInvalidValue;
+  if (!normalize_splits(g)) return hipErrorInvalidValue;
   const int nb = g.nbB + g.nbA;
   g.itab = reinterpret_cast<int32_t*>(static_cast<char*>(g.part) +
                                       partial_bytes(P, g.keys.n_keys, nb, WideGeo::RB));
   const long nbW = (g.d_out + kWideCols - 1) / kWideCols;
-  const long items = ((P + kSplitRows - 1) / kSplitRows + g.keys.n_keys) * nbW;
+  const long items = ((P + g.split_b - 1) / g.split_b + g.keys.n_keys) * nbW;
   const long cap = device_cu_count();
   const int grid = (int)(items < cap ? items : cap);
   if (grid > 0) grad_wide_kernel<<<grid, kWideThreads, 0, stream>>>(g);

@@ -54,6 +54,8 @@ constexpr int kSharedDhMinOut = 1280;
 // columns): dB items of kWideCols columns form the dH partials (a
 // contraction over all of d_out, re-reading dY, otherwise).
 bool wide_dh(int r_max, int d_out) { return rank_blocks(r_max) == 4 && d_out >= kSharedDhMinOut; }
+// outputs below this many columns take dB items of 512 pairs on the wide path
+constexpr int kWideLongOut = 4096;
 
 // Workspace regions for element size es: At [d_in][R], Bt [R][d_out],
 // Ht/dHt [R][ldh] (column = row index inside the key's segment), dense dH
@@ -479,6 +481,13 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
   // more than the second read of dY, and for narrow outputs the dA items (x
   // rows from the caches) run best mixed with the dB items in one launch.
   const bool wide = p.dtype == ACE_BF16 && !p.per_pair && wide_dh(p.r_max, p.d_out);
+  // narrow outputs give the 512-column items few column blocks: chunks of
+  // 512 pairs keep more CUs busy (one block per CU) when that still leaves at
+  // most one item per CU (the dA items keep their chunks)
+  if (wide && p.d_out < kWideLongOut) {
+    const long nbW = (p.d_out + kWideCols - 1) / kWideCols;
+    if (((long)p.T * p.k / 512 + n_keys) * nbW <= device_cu_count()) gr.split_b = 512;
+  }
   if ((p.dtype == ACE_BF16 && (p.per_pair || p.d_out >= kSharedDhMinOut) && p.r_max <= kFusedDhMaxRank) ||
       wide) {
     gr.phase = 1;
