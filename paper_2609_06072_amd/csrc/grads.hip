@@ -1269,12 +1269,12 @@ __global__ __launch_bounds__(kThreads) void dx_dma_kernel(DxArgs a) {
 }
 
 // split 0 means kSplitRows, split_b 0 means split; the dA items take 1024 or
-// 2048 indices, the dB items also 512.
+// 2048 indices, the dB items any multiple of 64 from 512 to 2048.
 bool normalize_splits(GradArgs& g) {
   if (g.split == 0) g.split = kSplitRows;
   if (g.split_b == 0) g.split_b = g.split;
-  return (g.split == kSplitRows || g.split == kMaxSplit) &&
-         (g.split_b == kMinSplit || g.split_b == kSplitRows || g.split_b == kMaxSplit);
+  return (g.split == kSplitRows || g.split == kMaxSplit) && g.split_b >= kMinSplit &&
+         g.split_b <= kMaxSplit && g.split_b % 64 == 0;
 }
 
 // Bytes of split partials (the item table follows them): bounded for the

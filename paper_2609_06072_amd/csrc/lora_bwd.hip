@@ -481,12 +481,16 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
   // more than the second read of dY, and for narrow outputs the dA items (x
   // rows from the caches) run best mixed with the dB items in one launch.
   const bool wide = p.dtype == ACE_BF16 && !p.per_pair && wide_dh(p.r_max, p.d_out);
-  // narrow outputs give the 512-column items few column blocks: chunks of
-  // 512 pairs keep more CUs busy (one block per CU) when that still leaves at
-  // most one item per CU (the dA items keep their chunks)
+  // narrow outputs give the 512-column items few column blocks: the shortest
+  // pair chunks (512 or 768) that still leave at most one item per CU keep
+  // more CUs busy (one block per CU; the dA items keep their chunks)
   if (wide && p.d_out < kWideLongOut) {
     const long nbW = (p.d_out + kWideCols - 1) / kWideCols;
-    if (((long)p.T * p.k / 512 + n_keys) * nbW <= device_cu_count()) gr.split_b = 512;
+    for (int sb = 512; sb <= 768; sb += 256)
+      if (((long)p.T * p.k / sb + n_keys) * nbW <= device_cu_count()) {
+        gr.split_b = sb;
+        break;
+      }
   }
   if ((p.dtype == ACE_BF16 && (p.per_pair || p.d_out >= kSharedDhMinOut) && p.r_max <= kFusedDhMaxRank) ||
       wide) {
