@@ -17,13 +17,14 @@
 //              directly, two stages in LDS (three blocks per CU)
 //   mean    -- the probe mean of every row of Pt; bf16 inputs: also the
 //              centred rows split as v = hi + lo (both bf16, |lo| <= 2^-9 |v|)
-//   gram    -- partial M over chunks of the probe: upper-triangle 64 x 64
-//              tiles, one partial per chunk.  bf16 inputs:
+//   gram    -- partial M over chunks of the probe: upper-triangle tiles
+//              (128 x 128 staged through LDS for bf16 inputs, 64 x 64 for
+//              fp32), one partial per chunk.  bf16 inputs:
 //              M = hi^T hi + hi^T lo + lo^T hi on the bf16 matrix cores (the
 //              dropped lo^T lo is below 2^-16 of |v_a v_b|).  fp32 inputs:
 //              fp32 MFMA, centring on load.
-//   msum    -- M: the Gram partials summed in chunk order (upper-triangle
-//              tiles), every element with all its chunks' loads in flight
+//   msum    -- M: the Gram partials summed in chunk order (elements on or
+//              above the diagonal), eight chunks' loads in flight
 //   bgram   -- partial G_e = B_e^T B_e over chunks of 256 rows of B_e
 //   pairs   -- num_ij = <G_i M_ij, M_ij G_j> for i <= j
 //   score   -- S_ij = num_ij / sqrt(num_ii num_jj); 0 when a norm is 0
@@ -37,8 +38,10 @@ namespace {
 constexpr int kPN = 64;    // projection tile: probe rows
 constexpr int kPC = 256;   // projection tile: adapter rows (eight waves)
 constexpr int kPThreads = 2 * kPC;
-constexpr int kGT = 64;    // Gram tile edge
-constexpr int kGK = 512;   // probe rows per Gram chunk (at least)
+constexpr int kGT = 64;    // Gram tile edge (fp32 inputs)
+constexpr int kGT2 = 128;  // Gram tile edge (bf16 inputs, staged through LDS)
+constexpr int kGK = 256;   // probe rows per Gram chunk (at least)
+constexpr int kMaxSplits = 64;
 constexpr int kBO = 256;   // rows of B_e per B^T B chunk
 
 size_t a256(size_t b) { return (b + 255) & ~(size_t)255; }
@@ -52,12 +55,12 @@ CkaLayout cka_layout(int N, int d_out, int E, int r) {
   CkaLayout L{};
   const size_t R = (size_t)E * r;
   L.ldp = ((N > 0 ? N : 1) + 31) & ~31;
-  // chunks of the probe for the Gram: at least kGK rows each, at most 32
-  // chunks, and at most 256 MB of partials
+  // chunks of the probe for the Gram: at least kGK rows each, at most
+  // kMaxSplits chunks, and at most 256 MB of partials
   int splits = (N + kGK - 1) / kGK;
   const size_t cap = (size_t)(256u << 20) / (R * R * 4 > 0 ? R * R * 4 : 1);
   if ((size_t)splits > cap) splits = (int)cap;
-  if (splits > 32) splits = 32;
+  if (splits > kMaxSplits) splits = kMaxSplits;
   if (splits < 1) splits = 1;
   L.splits = splits;
   L.kchunk = (((N + splits - 1) / splits) + 31) & ~31;
@@ -276,72 +279,91 @@ __global__ __launch_bounds__(kThreads) void cka_mean_kernel(CkaArgs a) {
 template <bool SPLIT>
 __global__ __launch_bounds__(kThreads) void cka_gram_kernel(CkaArgs a);
 
-// bf16 inputs: hi/lo fragments straight from Phi/Plo (centred, zero past N);
-// a chunk is a whole number of 32-row K-blocks, so nothing is masked.
+// bf16 inputs: block (tile pair p, chunk s) takes the 128 x 128 tile (ta, tb)
+// of M; wave (w & 1, w >> 1) owns a 64 x 64 quarter (4 x 4 MFMA tiles).  Per
+// stage, 32 probe rows of the hi and lo splits of the tile's 128 a rows and
+// 128 b rows (centred, zero past N) are copied global -> LDS with
+// global_load_lds_dwordx4 (64-byte rows, chunk l % 4 of a 16-row copy at
+// position (l % 4) ^ sw(row)), two stages in LDS; every fragment read from
+// LDS feeds four MFMA tiles.  A chunk is a whole number of 32-row K-blocks,
+// so nothing is masked.
 template <>
-__global__ __launch_bounds__(kThreads) void cka_gram_kernel<true>(CkaArgs a) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+__global__ __launch_bounds__(kThreads, 2) void cka_gram_kernel<true>(CkaArgs a) {
+  constexpr int NBUF = 2;
+  constexpr int ROWS = kGT2;                  // rows of each operand tile
+  constexpr int OB = ROWS * 64;               // bytes of one operand array per stage
+  constexpr int STAGE = 4 * OB;               // a hi, a lo, b hi, b lo
+  __shared__ __attribute__((aligned(16))) char sm[NBUF * STAGE];
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int c16 = lane & 15, g = lane >> 4;
   const int R = a.R;
-  const int nt = (R + kGT - 1) / kGT;
+  const int nt = (R + kGT2 - 1) / kGT2;
   int ta, tb;
   upper_pair(blockIdx.x, nt, &ta, &tb);
   const int s = blockIdx.y;
-  const int abase = ta * kGT + (wave & 1) * 32, bbase = tb * kGT + (wave >> 1) * 32;
   const int k_beg = s * a.kchunk;
   const int k_end = min(((a.N + 31) & ~31), k_beg + a.kchunk);   // <= ldp
-  const __bf16* ph[2][2];   // [operand a/b][j]
-  const __bf16* pl[2][2];
+  const int nst = max(0, (k_end - k_beg) / 32);
+  // copy plan: 4 arrays x 128 rows = 32 copies of 16 rows per stage, eight
+  // per wave: wave w copies rows 32 (w & 3) .. + 31 of every array
+  const int crow = lane >> 2, cpos = lane & 3;
+  const __bf16* src[8];
+  int dst[8];
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const size_t ra = (size_t)min(abase + 16 * j + c16, R - 1) * a.ldp;
-    const size_t rb = (size_t)min(bbase + 16 * j + c16, R - 1) * a.ldp;
-    ph[0][j] = a.Phi + ra + 8 * g;
-    pl[0][j] = a.Plo + ra + 8 * g;
-    ph[1][j] = a.Phi + rb + 8 * g;
-    pl[1][j] = a.Plo + rb + 8 * g;
+  for (int i = 0; i < 8; ++i) {
+    const int arr = i >> 1;                            // 0 a hi, 1 a lo, 2 b hi, 3 b lo
+    const int r0 = 32 * wave + 16 * (i & 1);           // first row of the copy
+    const int r = r0 + crow;
+    const int grow = min((arr < 2 ? ta : tb) * kGT2 + r, R - 1);
+    src[i] = ((arr & 1) ? a.Plo : a.Phi) + (size_t)grow * a.ldp + 8 * (cpos ^ cka_sw(r));
+    dst[i] = arr * OB + r0 * 64;
   }
-  f32x4 acc[2][2];
+  const uint32_t sbase = lds_addr(sm);
+  auto issue = [&](int st) {
+    const int k0 = k_beg + 32 * st;
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < 8; ++i)
+      dma16(src[i] + k0, __builtin_amdgcn_readfirstlane(sbase + (st % NBUF) * STAGE + dst[i]));
+  };
+  const int ar0 = 64 * (wave & 1), br0 = 64 * (wave >> 1);
+  f32x4 acc[4][4];
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  constexpr int U = 4;   // K-blocks loaded ahead of their MFMAs
-  for (int k = k_beg; k < k_end; k += 32 * U) {
-    bf16x8 fh[U][2][2], fl[U][2][2];
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int kk = min(k + 32 * u, k_end - 32);   // past the chunk: re-read, not used
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (nst > 0) issue(0);
+  for (int st = 0; st < nst; ++st) {
+    wait_vmcnt<0>();
+    __syncthreads();   // stage st landed everywhere; stage st - 1 is no longer read
+    if (st + 1 < nst) issue(st + 1);
+    const char* S = sm + (st % NBUF) * STAGE;
+    bf16x8 ah[4], al[4], bh[4], bl[4];
 #pragma unroll
-      for (int o = 0; o < 2; ++o)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          fh[u][o][j] = Tr<__bf16>::load(ph[o][j] + kk);
-          fl[u][o][j] = Tr<__bf16>::load(pl[o][j] + kk);
-        }
+    for (int i = 0; i < 4; ++i) {
+      const int ra = ar0 + 16 * i + c16, rb = br0 + 16 * i + c16;
+      ah[i] = *reinterpret_cast<const bf16x8*>(S + 0 * OB + ra * 64 + 16 * (g ^ cka_sw(ra)));
+      al[i] = *reinterpret_cast<const bf16x8*>(S + 1 * OB + ra * 64 + 16 * (g ^ cka_sw(ra)));
+      bh[i] = *reinterpret_cast<const bf16x8*>(S + 2 * OB + rb * 64 + 16 * (g ^ cka_sw(rb)));
+      bl[i] = *reinterpret_cast<const bf16x8*>(S + 3 * OB + rb * 64 + 16 * (g ^ cka_sw(rb)));
     }
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      if (k + 32 * u >= k_end) break;
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fl[u][0][i], fh[u][1][j], acc[i][j], 0, 0, 0);
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh[u][0][i], fl[u][1][j], acc[i][j], 0, 0, 0);
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh[u][0][i], fh[u][1][j], acc[i][j], 0, 0, 0);
-        }
-    }
+      for (int j = 0; j < 4; ++j) {
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[i], bh[j], acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[i], bl[j], acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[i], bh[j], acc[i][j], 0, 0, 0);
+      }
   }
   float* out = a.part + (size_t)s * R * R;
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int col = bbase + 16 * j + c16;
+    for (int j = 0; j < 4; ++j) {
+      const int col = tb * kGT2 + br0 + 16 * j + c16;
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        const int row = abase + 16 * i + 4 * g + v;
+        const int row = ta * kGT2 + ar0 + 16 * i + 4 * g + v;
         if (row < R && col < R) out[(size_t)row * R + col] = acc[i][j][v];
       }
     }
@@ -452,16 +474,16 @@ __global__ __launch_bounds__(kThreads) void cka_gram_kernel<false>(CkaArgs a) {
 
 // ---------------------------------------------------------------- M
 
-// Block (tile pair p, part h): the elements h * 256 + t of the 64 x 64 tile
-// (ta, tb) of M, each the sum of its chunks' partials in chunk order.
+// Thread e: element (e / R, e % R) of M when it lies on or above the
+// diagonal (the Gram writes every such element), the sum of its chunks'
+// partials in chunk order.
 __global__ __launch_bounds__(kThreads) void cka_msum_kernel(CkaArgs a) {
-  const int R = a.R, nt = (R + kGT - 1) / kGT;
-  int ta, tb;
-  upper_pair(blockIdx.x, nt, &ta, &tb);
-  const int e = blockIdx.y * kThreads + threadIdx.x;
-  const int row = ta * kGT + e / kGT, col = tb * kGT + e % kGT;
-  if (row >= R || col >= R) return;
-  const size_t off = (size_t)row * R + col, cs = (size_t)R * R;
+  const int R = a.R;
+  const long e = (long)blockIdx.x * kThreads + threadIdx.x;
+  if (e >= (long)R * R) return;
+  const int row = (int)(e / R), col = (int)(e % R);
+  if (row > col) return;
+  const size_t off = (size_t)e, cs = (size_t)R * R;
   float m = 0.f;
   for (int s = 0; s < a.splits; s += 8) {
     float v[8];
@@ -584,18 +606,14 @@ hipError_t launch_cka_t(const CkaProblem& p, void* ws, hipStream_t stream) {
     cka_mean_kernel<true><<<R, kThreads, 0, stream>>>(a);
   else
     cka_mean_kernel<false><<<R, kThreads, 0, stream>>>(a);
-  {
+  if (p.dtype == ACE_BF16) {
+    const int nt = (R + kGT2 - 1) / kGT2;
+    cka_gram_kernel<true><<<dim3(nt * (nt + 1) / 2, L.splits), kThreads, 0, stream>>>(a);
+  } else {
     const int nt = (R + kGT - 1) / kGT;
-    dim3 grid(nt * (nt + 1) / 2, L.splits);
-    if (p.dtype == ACE_BF16)
-      cka_gram_kernel<true><<<grid, kThreads, 0, stream>>>(a);
-    else
-      cka_gram_kernel<false><<<grid, kThreads, 0, stream>>>(a);
+    cka_gram_kernel<false><<<dim3(nt * (nt + 1) / 2, L.splits), kThreads, 0, stream>>>(a);
   }
-  {
-    const int nt = (R + kGT - 1) / kGT;
-    cka_msum_kernel<<<dim3(nt * (nt + 1) / 2, kGT * kGT / kThreads), kThreads, 0, stream>>>(a);
-  }
+  cka_msum_kernel<<<(int)(((long)R * R + kThreads - 1) / kThreads), kThreads, 0, stream>>>(a);
   cka_bgram_kernel<T><<<dim3(p.E, L.nbo), kThreads, 0, stream>>>(a);
   cka_pairs_kernel<<<p.E * (p.E + 1) / 2, kThreads, 0, stream>>>(a);
   cka_score_kernel<<<(p.E * p.E + kThreads - 1) / kThreads, kThreads, 0, stream>>>(a);
