@@ -26,7 +26,8 @@
 //   msum    -- M: the Gram partials summed in chunk order (elements on or
 //              above the diagonal), eight chunks' loads in flight
 //   bgram   -- partial G_e = B_e^T B_e over chunks of 256 rows of B_e
-//   pairs   -- num_ij = <G_i M_ij, M_ij G_j> for i <= j
+//   pairs   -- num_ij = <G_i M_ij, M_ij G_j> for i <= j (one wave per pair
+//              at ranks up to 8, one block otherwise)
 //   score   -- S_ij = num_ij / sqrt(num_ii num_jj); 0 when a norm is 0
 #include "ace_device.hpp"
 #include "ace_internal.hpp"
@@ -560,6 +561,47 @@ __global__ __launch_bounds__(kThreads) void cka_pairs_kernel(CkaArgs a) {
   }
 }
 
+// Ranks up to 8: one wave per expert pair i <= j, four pairs per block; lane
+// t < r * r holds element t of G_i, G_j and M_ij (wave-private LDS rows),
+// then the lanes' products are summed by shuffles.
+__global__ __launch_bounds__(kThreads) void cka_pairs8_kernel(CkaArgs a) {
+  __shared__ float Gi[kThreads / 64][64], Gj[kThreads / 64][64], Mij[kThreads / 64][64];
+  const int wave = threadIdx.x >> 6, t = threadIdx.x & 63;
+  const int pidx = blockIdx.x * (kThreads / 64) + wave;
+  const bool live = pidx < a.E * (a.E + 1) / 2;   // wave-uniform
+  const int r = a.r, rr = r * r, R = a.R;
+  int i = 0, j = 0;
+  if (live) upper_pair(pidx, a.E, &i, &j);
+  if (live && t < rr) {
+    float gi = 0.f, gj = 0.f;
+    for (int c = 0; c < a.nbo; ++c) {
+      gi += a.Gb[((size_t)i * a.nbo + c) * rr + t];
+      gj += a.Gb[((size_t)j * a.nbo + c) * rr + t];
+    }
+    Gi[wave][t] = gi;
+    Gj[wave][t] = gj;
+    const int row = i * r + t / r, col = j * r + t % r;
+    Mij[wave][t] = a.M[(size_t)min(row, col) * R + max(row, col)];
+  }
+  __syncthreads();
+  float acc = 0.f;
+  if (live && t < rr) {
+    const int p = t / r, q = t % r;
+    float t1 = 0.f, t2 = 0.f;
+    for (int u = 0; u < r; ++u) {
+      t1 += Gi[wave][p * r + u] * Mij[wave][u * r + q];   // (G_i M_ij)[p][q]
+      t2 += Mij[wave][p * r + u] * Gj[wave][u * r + q];   // (M_ij G_j)[p][q]
+    }
+    acc = t1 * t2;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 64);
+  if (live && t == 0) {
+    a.num[(size_t)i * a.E + j] = acc;
+    a.num[(size_t)j * a.E + i] = acc;
+  }
+}
+
 __global__ __launch_bounds__(kThreads) void cka_score_kernel(CkaArgs a) {
   const int t = blockIdx.x * kThreads + threadIdx.x;
   const int E = a.E;
@@ -615,7 +657,10 @@ hipError_t launch_cka_t(const CkaProblem& p, void* ws, hipStream_t stream) {
   }
   cka_msum_kernel<<<(int)(((long)R * R + kThreads - 1) / kThreads), kThreads, 0, stream>>>(a);
   cka_bgram_kernel<T><<<dim3(p.E, L.nbo), kThreads, 0, stream>>>(a);
-  cka_pairs_kernel<<<p.E * (p.E + 1) / 2, kThreads, 0, stream>>>(a);
+  if (p.r <= 8)
+    cka_pairs8_kernel<<<(p.E * (p.E + 1) / 2 + kThreads / 64 - 1) / (kThreads / 64), kThreads, 0, stream>>>(a);
+  else
+    cka_pairs_kernel<<<p.E * (p.E + 1) / 2, kThreads, 0, stream>>>(a);
   cka_score_kernel<<<(p.E * p.E + kThreads - 1) / kThreads, kThreads, 0, stream>>>(a);
   return hipGetLastError();
 }

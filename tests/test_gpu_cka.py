@@ -44,8 +44,10 @@ def _gpu_cka(pa):
     return _f64(S)
 
 
-SMALL = [  # N, d_in, d_out, E, r: ragged against the 128-row projection tile,
-           # the 64-row Gram tile and the 1024-row probe chunks
+SMALL = [  # N, d_in, d_out, E, r: ragged against the projection tiles (64 probe
+           # rows x 256 adapter rows), the Gram tiles (128 for bf16, 64 for
+           # fp32) and the probe chunks (256 rows or more); ranks up to 8
+           # take the one-wave pair kernel, larger ranks the block one
     (300, 40, 24, 6, 3),
     (1500, 136, 72, 9, 8),
     (130, 64, 16, 20, 16),
