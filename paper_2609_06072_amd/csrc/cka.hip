@@ -14,7 +14,7 @@
 // Launches (all deterministic):
 //   project -- Pt = A X^T, [R][ldp] fp32: a 64 x 256-tile MFMA GEMM over
 //              K = d_in (eight waves), operands copied global -> LDS
-//              directly, two stages in LDS (three blocks per CU)
+//              directly, two stages of 128 bytes per row in LDS
 //   mean    -- the probe mean of every row of Pt; bf16 inputs: also the
 //              centred rows split as v = hi + lo (both bf16, |lo| <= 2^-9 |v|)
 //   gram    -- partial M over chunks of the probe: upper-triangle tiles
@@ -110,23 +110,27 @@ __device__ inline void upper_pair(int p, int n, int* a, int* b) {
 
 // A block takes 64 probe rows x 256 adapter rows (eight waves, so that X is
 // staged once per 256 adapter rows); wave (wn, wc) owns 32 x 64.
-// Stages of one K-block (64 bytes of every row) of both operands are copied
-// global -> LDS with global_load_lds_dwordx4, NBUF stages in flight (no
-// register staging).  A copy instruction moves 16 rows; lane l lands at row
-// l/4, position l%4 of the 64-byte LDS row and fetches the global 16-byte
-// chunk (l%4) ^ sw(row), sw(row) = (row >> 2) & 3, so that the 16 rows one
-// fragment read touches fall in distinct banks.  Chunks past d_in (a
-// multiple of 16 bytes) are fetched clamped and zeroed at the read.
-__device__ inline int cka_sw(int row) { return (row >> 2) & 3; }
+// Stages of two K-blocks (128 bytes of every row) of both operands are
+// copied global -> LDS with global_load_lds_dwordx4, two stages in LDS (no
+// register staging), so that a barrier is paid per 16 matrix instructions of
+// a wave.  A copy instruction moves 8 rows; lane l lands at row l/8,
+// position l%8 of the 128-byte LDS row and fetches the global 16-byte chunk
+// (l%8) ^ sw(row), sw(row) = (row >> 1) & 7, so that the 16 rows one fragment
+// read touches (two per 256-byte bank line) fall in distinct banks.  Chunks
+// past d_in (a multiple of 16 bytes) are fetched clamped and zeroed at the
+// read.
+__device__ inline int cka_sw(int row) { return (row >> 1) & 7; }
+// The same for 64-byte rows (four chunks; the Gram's stages): (row >> 2) & 3.
+__device__ inline int cka_sw4(int row) { return (row >> 2) & 3; }
 
 template <typename T>
 __global__ __launch_bounds__(kPThreads) void cka_project_kernel(CkaArgs a) {
   using F = typename Tr<T>::frag;
   constexpr int PER = Tr<T>::PER, KB = Tr<T>::KB;   // KB * sizeof(T) = 64 bytes
-  // two stages (40 KB): three blocks per CU, so that the 64-row tiles of a
-  // 10,000-row probe all run at once (four stages fit two blocks per CU)
-  constexpr int NBUF = 2;
-  constexpr int XB = kPN * 64, AB = kPC * 64;       // stage bytes of each operand
+  constexpr int KS = 2 * KB;                        // contraction indices per stage (128 bytes)
+  constexpr int RB = 128;                           // bytes of a row per stage
+  constexpr int NBUF = 2;                           // 80 KB: two blocks per CU
+  constexpr int XB = kPN * RB, AB = kPC * RB;       // stage bytes of each operand
   __shared__ __attribute__((aligned(16))) char xs[NBUF][XB];
   __shared__ __attribute__((aligned(16))) char as[NBUF][AB];
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -136,38 +140,35 @@ __global__ __launch_bounds__(kPThreads) void cka_project_kernel(CkaArgs a) {
   const T* X = static_cast<const T*>(a.X);
   const T* A = static_cast<const T*>(a.A);
   const int N = a.N, R = a.R, d_in = a.d_in;
-  const int nst = (d_in + KB - 1) / KB;
+  const int nst = (d_in + KS - 1) / KS;
 
-  // copy plan: X rows 16w .. 16w+15 (one instruction for each of waves
-  // 0..3), A rows 32w .. 32w+31 (two); lane l copies row (l >> 2) of its
-  // instruction (a chunk past d_in is fetched from column d_in - PER instead,
-  // inside the row, and zeroed at the read)
-  static_assert(kPN / 16 <= kPThreads / 64 && kPC == 32 * (kPThreads / 64), "copy plan");
-  const bool xcopy = 16 * wave < kPN;   // wave-uniform
-  const int crow = lane >> 2, cpos = lane & 3;
-  const int xr = min(16 * wave, kPN - 16) + crow;
+  // copy plan: X rows 8w .. 8w+7 (one instruction per wave), A rows
+  // 32w .. 32w+31 (four); lane l copies row (l >> 3) of its instruction (a
+  // chunk past d_in is fetched from column d_in - PER instead, inside the
+  // row, and zeroed at the read)
+  static_assert(kPN == 8 * (kPThreads / 64) && kPC == 32 * (kPThreads / 64), "copy plan");
+  const int crow = lane >> 3, cpos = lane & 7;
+  const int xr = 8 * wave + crow;
   const T* xsrc = X + (size_t)min(n0 + xr, N - 1) * d_in;
   const int xch = PER * (cpos ^ cka_sw(xr));
-  const T* asrc[2];
-  int ach[2];
+  const T* asrc[4];
+  int ach[4];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int ar = 32 * wave + 16 * i + crow;
+  for (int i = 0; i < 4; ++i) {
+    const int ar = 32 * wave + 8 * i + crow;
     asrc[i] = A + (size_t)min(c0 + ar, R - 1) * d_in;
     ach[i] = PER * (cpos ^ cka_sw(ar));
   }
   auto issue = [&](int st) {
     const int b = st % NBUF;
-    const int k0 = st * KB;
-    if (xcopy)
-      dma16(xsrc + min(k0 + xch, d_in - PER),
-            __builtin_amdgcn_readfirstlane(lds_addr(&xs[b][16 * wave * 64])));
+    const int k0 = st * KS;
+    dma16(xsrc + min(k0 + xch, d_in - PER),
+          __builtin_amdgcn_readfirstlane(lds_addr(&xs[b][8 * wave * RB])));
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < 4; ++i)
       dma16(asrc[i] + min(k0 + ach[i], d_in - PER),
-            __builtin_amdgcn_readfirstlane(lds_addr(&as[b][(32 * wave + 16 * i) * 64])));
+            __builtin_amdgcn_readfirstlane(lds_addr(&as[b][(32 * wave + 8 * i) * RB])));
   };
-  const int per_stage = xcopy ? 3 : 2;   // copies per wave per stage
 
   f32x4 acc[2][4];
 #pragma unroll
@@ -175,35 +176,38 @@ __global__ __launch_bounds__(kPThreads) void cka_project_kernel(CkaArgs a) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-#pragma unroll
-  for (int p = 0; p < NBUF - 1; ++p)
-    if (p < nst) issue(p);
+  if (nst > 0) issue(0);
   for (int st = 0; st < nst; ++st) {
-    // this wave's copies of stage st are done once at most those of the
-    // stages issued after it are outstanding; the barrier publishes them
-    wait_vmcnt_upto<(NBUF - 2) * 3>(min(NBUF - 2, nst - 1 - st) * per_stage);
+    // this wave's copies of stage st are done; the barrier publishes them and
+    // tells that stage st - 1's buffer is no longer read
+    wait_vmcnt<0>();
     __syncthreads();
-    if (st + NBUF - 1 < nst) issue(st + NBUF - 1);
+    if (st + 1 < nst) issue(st + 1);
     const int b = st % NBUF;
-    // chunk g of this K-block holds k = st*KB + PER*g .. (a full chunk or none)
-    const bool kin = st * KB + PER * g < d_in;
-    F xf[2], af[4];
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int r = wn + 16 * j + c16;
-      const F v = *reinterpret_cast<const F*>(&xs[b][r * 64 + 16 * (g ^ cka_sw(r))]);
-      xf[j] = kin ? v : Tr<T>::zero();
+    for (int kb = 0; kb < 2; ++kb) {
+      // chunk 4 kb + g of this stage holds k = st*KS + KB*kb + PER*g .. (a
+      // full chunk or none)
+      const int cc = 4 * kb + g;
+      const bool kin = st * KS + PER * cc < d_in;
+      F xf[2], af[4];
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int r = wn + 16 * j + c16;
+        const F v = *reinterpret_cast<const F*>(&xs[b][r * RB + 16 * (cc ^ cka_sw(r))]);
+        xf[j] = kin ? v : Tr<T>::zero();
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = wc + 16 * j + c16;
+        const F v = *reinterpret_cast<const F*>(&as[b][r * RB + 16 * (cc ^ cka_sw(r))]);
+        af[j] = kin ? v : Tr<T>::zero();
+      }
+#pragma unroll
+      for (int jn = 0; jn < 2; ++jn)
+#pragma unroll
+        for (int jc = 0; jc < 4; ++jc) acc[jn][jc] = Tr<T>::mma(xf[jn], af[jc], acc[jn][jc]);
     }
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int r = wc + 16 * j + c16;
-      const F v = *reinterpret_cast<const F*>(&as[b][r * 64 + 16 * (g ^ cka_sw(r))]);
-      af[j] = kin ? v : Tr<T>::zero();
-    }
-#pragma unroll
-    for (int jn = 0; jn < 2; ++jn)
-#pragma unroll
-      for (int jc = 0; jc < 4; ++jc) acc[jn][jc] = Tr<T>::mma(xf[jn], af[jc], acc[jn][jc]);
   }
   // acc[jn][jc] element v = P[n][c] with n = n0+wn+16jn+4g+v, c = c0+wc+16jc+c16:
   // four consecutive probe rows of Pt row c per lane
@@ -285,7 +289,7 @@ __global__ __launch_bounds__(kThreads) void cka_gram_kernel(CkaArgs a);
 // stage, 32 probe rows of the hi and lo splits of the tile's 128 a rows and
 // 128 b rows (centred, zero past N) are copied global -> LDS with
 // global_load_lds_dwordx4 (64-byte rows, chunk l % 4 of a 16-row copy at
-// position (l % 4) ^ sw(row)), two stages in LDS; every fragment read from
+// position (l % 4) ^ sw4(row)), two stages in LDS; every fragment read from
 // LDS feeds four MFMA tiles.  A chunk is a whole number of 32-row K-blocks,
 // so nothing is masked.
 template <>
@@ -316,7 +320,7 @@ __global__ __launch_bounds__(kThreads, 2) void cka_gram_kernel<true>(CkaArgs a) 
     const int r0 = 32 * wave + 16 * (i & 1);           // first row of the copy
     const int r = r0 + crow;
     const int grow = min((arr < 2 ? ta : tb) * kGT2 + r, R - 1);
-    src[i] = ((arr & 1) ? a.Plo : a.Phi) + (size_t)grow * a.ldp + 8 * (cpos ^ cka_sw(r));
+    src[i] = ((arr & 1) ? a.Plo : a.Phi) + (size_t)grow * a.ldp + 8 * (cpos ^ cka_sw4(r));
     dst[i] = arr * OB + r0 * 64;
   }
   const uint32_t sbase = lds_addr(sm);
@@ -342,10 +346,10 @@ __global__ __launch_bounds__(kThreads, 2) void cka_gram_kernel<true>(CkaArgs a) 
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int ra = ar0 + 16 * i + c16, rb = br0 + 16 * i + c16;
-      ah[i] = *reinterpret_cast<const bf16x8*>(S + 0 * OB + ra * 64 + 16 * (g ^ cka_sw(ra)));
-      al[i] = *reinterpret_cast<const bf16x8*>(S + 1 * OB + ra * 64 + 16 * (g ^ cka_sw(ra)));
-      bh[i] = *reinterpret_cast<const bf16x8*>(S + 2 * OB + rb * 64 + 16 * (g ^ cka_sw(rb)));
-      bl[i] = *reinterpret_cast<const bf16x8*>(S + 3 * OB + rb * 64 + 16 * (g ^ cka_sw(rb)));
+      ah[i] = *reinterpret_cast<const bf16x8*>(S + 0 * OB + ra * 64 + 16 * (g ^ cka_sw4(ra)));
+      al[i] = *reinterpret_cast<const bf16x8*>(S + 1 * OB + ra * 64 + 16 * (g ^ cka_sw4(ra)));
+      bh[i] = *reinterpret_cast<const bf16x8*>(S + 2 * OB + rb * 64 + 16 * (g ^ cka_sw4(rb)));
+      bl[i] = *reinterpret_cast<const bf16x8*>(S + 3 * OB + rb * 64 + 16 * (g ^ cka_sw4(rb)));
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i)
