@@ -175,7 +175,7 @@ struct GradArgs {
   int32_t phase;
   float* dHp;                 // phase 1: [nbB][npos][dhs] fp32, B_q^T dY per pair
                               //   position, the 128 columns of one dB column block
-                              //   (wide items: [nbW][npos][64], 512 columns)
+                              //   (wide items: [npos][nbW][64], 512 columns)
   long npos;
   int32_t dhs;                // rank stride of dHp (8 or 16; 64 for wide items)
   const void* Bt;             // phase 1: B^T [R][d_out], storage type
@@ -188,9 +188,10 @@ struct GradArgs {
 // stored per key as [r][u - offsets[q]] (dHt), and row-major [u][rpad] with
 // zeros past r_q (dHrow) or in dense per-token rows (dHf), either may be null.
 struct DhReduceArgs {
-  const float* dHp;
+  const float* dHp;           // [nbB][npos][dhs], or [npos][nbB][64] with pos_major
   long npos;
   int32_t dhs, nbB;
+  int32_t pos_major;          // partials of the wide items (pair-major runs)
   const int32_t* offsets;
   const int32_t* row_token;
   const uint32_t* row_slots;

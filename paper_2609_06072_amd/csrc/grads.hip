@@ -487,8 +487,9 @@ __global__ __launch_bounds__(kThreads, RB <= 4 ? 3 : 1) void grad_dma_kernel(Gra
 // call.  A dB item takes 512 dY columns (four 128-column sub-tiles, each laid
 // out like the L tile above) of a chunk of the key's pairs; from the same
 // stage in LDS it also contracts every pair's 512 columns against B_q^T into
-// an fp32 dH partial per pair position and 512-column block (rank stride 64),
-// which dh_reduce sums per row.  The dH contraction over all of d_out before
+// an fp32 dH partial per pair position and 512-column block, laid out pair
+// by pair ([npos][nbW][64]: a row's partials are one contiguous run), which
+// dh_reduce_wide sums per row.  The dH contraction over all of d_out before
 // the weight gradients, and its second read of dY, are not run.
 // Eight waves in two roles: waves 0-3 accumulate dB of one 128-column
 // sub-tile each for all 64 ranks; waves 4-7 compute dH, each for two rank
@@ -678,6 +679,7 @@ __device__ __forceinline__ void wide_item(const GradArgs& a, WideSmem& sm, int q
     // pair position.
     const int h = wave - kWideWaves / 2;
     const int rb0 = 2 * (h & 1), pb0 = h >> 1;
+    const int nbW = (a.d_out + kWideCols - 1) / kWideCols;
     bf16x8 bt[2][kWideCols / 32];
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
@@ -705,7 +707,7 @@ __device__ __forceinline__ void wide_item(const GradArgs& a, WideSmem& sm, int q
         }
         const int kk = st * RS + r;   // chunk index of this lane's pair (rows past nk are copies)
         if (kk < nk) {
-          float* dst = a.dHp + ((size_t)cbw * a.npos + kfirst + kk) * (16 * RB) + 16 * rb0 + 4 * g;
+          float* dst = a.dHp + ((size_t)(kfirst + kk) * nbW + cbw) * (16 * RB) + 16 * rb0 + 4 * g;
 #pragma unroll
           for (int i = 0; i < 2; ++i) *reinterpret_cast<f32x4*>(dst + 16 * i) = hv[i];
         }
@@ -817,6 +819,104 @@ __global__ __launch_bounds__(kThreads) void dh_reduce_kernel(DhReduceArgs a) {
 #pragma unroll
     for (int e = 0; e < 4; ++e)
       if (r0 + e < r_q) df[r0 + e] = hv[e];
+  }
+}
+
+// dH per row from the partials of the wide items ([npos][nbW][64] fp32, so a
+// row's pairs and their column blocks form one contiguous run of pieces of
+// 64 ranks).  Thread t takes row blockIdx.x * kWRows + t / 16 and ranks
+// 4 (t % 16) .. +3; it sums the run's pieces NL at a time (weighted per pair
+// when pair weights are given).  The block's dH pass through LDS so that dHt
+// ([r][u - offsets[q]] per key) is written in runs of kWRows columns.  Blocks
+// of 512 threads: 256 (more, smaller blocks) and 1024 (fewer blocks resident
+// per CU) measured slower at the Mixtral-like shape.
+constexpr int kWThreads = 512;
+constexpr int kWRows = kWThreads / 16;
+
+template <int NL>
+__global__ __launch_bounds__(kWThreads) void dh_reduce_wide_kernel(DhReduceArgs a) {
+  __shared__ int seg[kMaxKeys + 1];
+  __shared__ float sh[kWRows][65];
+  __shared__ int sq[kWRows];
+  const int n_keys = a.keys.n_keys;
+  for (int i = threadIdx.x; i <= n_keys; i += kWThreads) seg[i] = a.offsets[i];
+  __syncthreads();
+  const int U = seg[n_keys];
+  const int u0 = blockIdx.x * kWRows;
+  if (u0 >= U) return;   // block-uniform
+  const int lr = threadIdx.x >> 4, quad = threadIdx.x & 15;
+  const int r0 = 4 * quad;
+  const int nbW = a.nbB;
+  const int u = u0 + lr;
+  if (u < U) {
+    const int q = upper_index(seg, n_keys, u);
+    const int p0 = a.ppos ? a.ppos[u] : u, p1 = a.ppos ? a.ppos[u + 1] : u + 1;
+    const f32x4* src = reinterpret_cast<const f32x4*>(a.dHp + (size_t)p0 * nbW * 64) + quad;
+    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (!a.pair_w) {
+      const int n = (p1 - p0) * nbW;   // pieces of the row's run
+      for (int c0 = 0; c0 < n; c0 += NL) {
+        f32x4 t[NL];
+#pragma unroll
+        for (int j = 0; j < NL; ++j) t[j] = src[(size_t)min(c0 + j, n - 1) * 16];
+#pragma unroll
+        for (int j = 0; j < NL; ++j)
+          if (c0 + j < n) acc += t[j];
+      }
+    } else {
+      const int tok = a.row_token[u];
+      for (int p = p0; p < p1; ++p) {
+        const float w = a.pair_w[a.ppos ? a.plist[p] : tok * a.k + (__builtin_ctz(a.row_slots[u] | 0x80000000u) & 31)];
+        const f32x4* sp = src + (size_t)(p - p0) * nbW * 16;
+        f32x4 v = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int c0 = 0; c0 < nbW; c0 += NL) {
+          f32x4 t[NL];
+#pragma unroll
+          for (int j = 0; j < NL; ++j) t[j] = sp[(size_t)min(c0 + j, nbW - 1) * 16];
+#pragma unroll
+          for (int j = 0; j < NL; ++j)
+            if (c0 + j < nbW) v += t[j];
+        }
+        acc += v * w;
+      }
+    }
+    const int r_q = a.keys.rank[q], roff = a.keys.roff[q];
+    const float s = a.alpha / (float)r_q;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc[e] = r0 + e < r_q ? acc[e] * s : 0.f;
+    const __bf16 hv[4] = {(__bf16)acc[0], (__bf16)acc[1], (__bf16)acc[2], (__bf16)acc[3]};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) sh[lr][r0 + e] = acc[e];
+    if (quad == 0) sq[lr] = q;
+    if (a.dHrow) {   // zeros past r_q up to rpad
+      __bf16* dr = static_cast<__bf16*>(a.dHrow) + (size_t)u * a.rpad;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) dr[r0 + e] = hv[e];
+      if (quad == 0)
+        for (int r = 64; r < a.rpad; ++r) dr[r] = (__bf16)0.f;
+    }
+    if (a.dHf) {
+      const int tok = a.row_token[u];
+      const int j0 = __builtin_ctz(a.row_slots[u] | 0x80000000u) & 31;
+      const size_t drow = (size_t)tok * a.kslots + (a.kslots > 1 ? j0 : 0);
+      __bf16* df = static_cast<__bf16*>(a.dHf) + drow * a.keys.R + roff;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (r0 + e < r_q) df[r0 + e] = hv[e];
+    }
+  }
+  if (!a.dHt) return;   // block-uniform
+  __syncthreads();
+  __bf16* dt = static_cast<__bf16*>(a.dHt);
+#pragma unroll
+  for (int i = 0; i < 64 * kWRows / kWThreads; ++i) {
+    const int idx = threadIdx.x + i * kWThreads;
+    const int r = idx / kWRows, c = idx % kWRows;
+    const int uc = u0 + c;
+    if (uc >= U) continue;
+    const int q = sq[c];
+    if (r < a.keys.rank[q])
+      dt[(size_t)(a.keys.roff[q] + r) * a.ldh + (uc - seg[q])] = (__bf16)sh[c][r];
   }
 }
 
@@ -1343,6 +1443,16 @@ hipError_t launch_grads_wide(GradArgs g, long P, hipStream_t stream) {
 
 hipError_t launch_dh_reduce(const DhReduceArgs& d, long U, hipStream_t stream) {
   if (d.dhs != 8 && d.dhs != 16 && d.dhs != 64) return hipErrorInvalidValue;
+  if (d.pos_major) {
+    if (d.dhs != 64) return hipErrorInvalidValue;
+    const long blocks = (U + kWRows - 1) / kWRows;
+    if (blocks <= 0) return hipSuccess;
+    // loads in flight per thread: at most a pair's column blocks
+    if (d.nbB >= 16) dh_reduce_wide_kernel<8><<<(int)blocks, kWThreads, 0, stream>>>(d);
+    else if (d.nbB >= 8) dh_reduce_wide_kernel<8><<<(int)blocks, kWThreads, 0, stream>>>(d);
+    else dh_reduce_wide_kernel<4><<<(int)blocks, kWThreads, 0, stream>>>(d);
+    return hipGetLastError();
+  }
   const int rows_per_block = kThreads / (d.dhs / 4);
   const long blocks = (U + rows_per_block - 1) / rows_per_block;
   if (blocks > 0) {

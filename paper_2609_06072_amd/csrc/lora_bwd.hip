@@ -505,6 +505,7 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
     d.dHp = gr.dHp;
     d.npos = P;
     d.dhs = gr.dhs;
+    d.pos_major = wide ? 1 : 0;
     d.nbB = wide ? (p.d_out + kWideCols - 1) / kWideCols : (p.d_out + kGradColBlk - 1) / kGradColBlk;
     d.offsets = p.rt->offsets;
     d.row_token = p.rt->row_token;
