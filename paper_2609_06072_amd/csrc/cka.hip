@@ -14,7 +14,8 @@
 // Launches (all deterministic):
 //   project -- Pt = A X^T, [R][ldp] fp32: a 64 x 256-tile MFMA GEMM over
 //              K = d_in (eight waves), operands copied global -> LDS
-//              directly, two stages of 128 bytes per row in LDS
+//              directly, two stages of 128 bytes per row in LDS (128 x 256
+//              tiles with two or three stages measured no faster)
 //   mean    -- the probe mean of every row of Pt; bf16 inputs: also the
 //              centred rows split as v = hi + lo (both bf16, |lo| <= 2^-9 |v|)
 //   gram    -- partial M over chunks of the probe: upper-triangle tiles
@@ -24,10 +25,12 @@
 //              dropped lo^T lo is below 2^-16 of |v_a v_b|).  fp32 inputs:
 //              fp32 MFMA, centring on load.
 //   msum    -- M: the Gram partials summed in chunk order (elements on or
-//              above the diagonal), eight chunks' loads in flight
-//   bgram   -- partial G_e = B_e^T B_e over chunks of 256 rows of B_e
-//   pairs   -- num_ij = <G_i M_ij, M_ij G_j> for i <= j (one wave per pair
-//              at ranks up to 8, one block otherwise)
+//              above the diagonal), eight chunks' loads in flight; at ranks up
+//              to 8 the same launch also forms the partials of B_e^T B_e
+//   bgram   -- (ranks above 8) partial G_e over chunks of 256 rows of B_e
+//   pairs   -- num_ij = <G_i M_ij, M_ij G_j> for i <= j; at ranks up to 8 one
+//              wave per pair, which also forms num_ii and num_jj and writes
+//              S_ij directly; otherwise one block per pair, then
 //   score   -- S_ij = num_ij / sqrt(num_ii num_jj); 0 when a norm is 0
 #include "ace_device.hpp"
 #include "ace_internal.hpp"
@@ -37,6 +40,7 @@ namespace ace {
 namespace {
 
 constexpr int kPN = 64;    // projection tile: probe rows
+constexpr int kPBuf = 2;   // projection stages in LDS (80 KB: two blocks per CU)
 constexpr int kPC = 256;   // projection tile: adapter rows (eight waves)
 constexpr int kPThreads = 2 * kPC;
 constexpr int kGT = 64;    // Gram tile edge (fp32 inputs)
@@ -93,6 +97,7 @@ struct CkaArgs {
   __bf16* Plo;
   float* S;          // [E][E]
   int32_t N, d_in, d_out, E, r, R, ldp, splits, kchunk, nbo;
+  int32_t bf16;      // storage type of X, A and B
 };
 
 // Upper-triangle index p -> (a, b), a <= b < n, row-major.
@@ -108,53 +113,62 @@ __device__ inline void upper_pair(int p, int n, int* a, int* b) {
 
 // ---------------------------------------------------------------- project
 
-// A block takes 64 probe rows x 256 adapter rows (eight waves, so that X is
-// staged once per 256 adapter rows); wave (wn, wc) owns 32 x 64.
+// A block takes PN probe rows x 256 adapter rows (eight waves, so that X is
+// staged once per 256 adapter rows); wave (wn, wc) owns PN / 2 x 64.
 // Stages of two K-blocks (128 bytes of every row) of both operands are
-// copied global -> LDS with global_load_lds_dwordx4, two stages in LDS (no
-// register staging), so that a barrier is paid per 16 matrix instructions of
-// a wave.  A copy instruction moves 8 rows; lane l lands at row l/8,
-// position l%8 of the 128-byte LDS row and fetches the global 16-byte chunk
-// (l%8) ^ sw(row), sw(row) = (row >> 1) & 7, so that the 16 rows one fragment
-// read touches (two per 256-byte bank line) fall in distinct banks.  Chunks
-// past d_in (a multiple of 16 bytes) are fetched clamped and zeroed at the
-// read.
+// copied global -> LDS with global_load_lds_dwordx4, NBUF stages in LDS (no
+// register staging; NBUF - 1 stages in flight while one is read), so that a
+// barrier is paid per 8 PN / 32 matrix instructions of a wave.  A copy
+// instruction moves 8 rows; lane l lands at row l/8, position l%8 of the
+// 128-byte LDS row and fetches the global 16-byte chunk (l%8) ^ sw(row),
+// sw(row) = (row >> 1) & 7, so that the 16 rows one fragment read touches
+// (two per 256-byte bank line) fall in distinct banks.  Chunks past d_in (a
+// multiple of 16 bytes) are fetched clamped and zeroed at the read.
 __device__ inline int cka_sw(int row) { return (row >> 1) & 7; }
 // The same for 64-byte rows (four chunks; the Gram's stages): (row >> 2) & 3.
 __device__ inline int cka_sw4(int row) { return (row >> 2) & 3; }
 
-template <typename T>
+template <typename T, int PN, int NBUF>
 __global__ __launch_bounds__(kPThreads) void cka_project_kernel(CkaArgs a) {
   using F = typename Tr<T>::frag;
   constexpr int PER = Tr<T>::PER, KB = Tr<T>::KB;   // KB * sizeof(T) = 64 bytes
   constexpr int KS = 2 * KB;                        // contraction indices per stage (128 bytes)
   constexpr int RB = 128;                           // bytes of a row per stage
-  constexpr int NBUF = 2;                           // 80 KB: two blocks per CU
-  constexpr int XB = kPN * RB, AB = kPC * RB;       // stage bytes of each operand
+  constexpr int XB = PN * RB, AB = kPC * RB;        // stage bytes of each operand
+  constexpr int NW = kPThreads / 64;
+  constexpr int XC = PN / 8 / NW;                   // X copies per wave and stage
+  constexpr int AC = kPC / 8 / NW;                  // A copies per wave and stage
+  constexpr int CP = XC + AC;
+  constexpr int JN = PN / 32;                       // 16-row probe blocks per wave
+  static_assert(PN % (8 * NW) == 0 && kPC == 32 * NW && NBUF >= 2 && NBUF <= 4, "copy plan");
   __shared__ __attribute__((aligned(16))) char xs[NBUF][XB];
   __shared__ __attribute__((aligned(16))) char as[NBUF][AB];
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int c16 = lane & 15, g = lane >> 4;
-  const int n0 = blockIdx.x * kPN, c0 = blockIdx.y * kPC;
-  const int wn = (wave & 1) * 32, wc = (wave >> 1) * 64;   // wave: 32 probe rows x 64 adapter rows
+  const int n0 = blockIdx.x * PN, c0 = blockIdx.y * kPC;
+  const int wn = (wave & 1) * (PN / 2), wc = (wave >> 1) * 64;   // wave: PN/2 probe rows x 64 adapter rows
   const T* X = static_cast<const T*>(a.X);
   const T* A = static_cast<const T*>(a.A);
   const int N = a.N, R = a.R, d_in = a.d_in;
   const int nst = (d_in + KS - 1) / KS;
 
-  // copy plan: X rows 8w .. 8w+7 (one instruction per wave), A rows
+  // copy plan: X rows 8 (XC w + i) .. +7 (XC instructions per wave), A rows
   // 32w .. 32w+31 (four); lane l copies row (l >> 3) of its instruction (a
   // chunk past d_in is fetched from column d_in - PER instead, inside the
   // row, and zeroed at the read)
-  static_assert(kPN == 8 * (kPThreads / 64) && kPC == 32 * (kPThreads / 64), "copy plan");
   const int crow = lane >> 3, cpos = lane & 7;
-  const int xr = 8 * wave + crow;
-  const T* xsrc = X + (size_t)min(n0 + xr, N - 1) * d_in;
-  const int xch = PER * (cpos ^ cka_sw(xr));
-  const T* asrc[4];
-  int ach[4];
+  const T* xsrc[XC];
+  int xch[XC];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < XC; ++i) {
+    const int xr = 8 * (XC * wave + i) + crow;
+    xsrc[i] = X + (size_t)min(n0 + xr, N - 1) * d_in;
+    xch[i] = PER * (cpos ^ cka_sw(xr));
+  }
+  const T* asrc[AC];
+  int ach[AC];
+#pragma unroll
+  for (int i = 0; i < AC; ++i) {
     const int ar = 32 * wave + 8 * i + crow;
     asrc[i] = A + (size_t)min(c0 + ar, R - 1) * d_in;
     ach[i] = PER * (cpos ^ cka_sw(ar));
@@ -162,57 +176,82 @@ __global__ __launch_bounds__(kPThreads) void cka_project_kernel(CkaArgs a) {
   auto issue = [&](int st) {
     const int b = st % NBUF;
     const int k0 = st * KS;
-    dma16(xsrc + min(k0 + xch, d_in - PER),
-          __builtin_amdgcn_readfirstlane(lds_addr(&xs[b][8 * wave * RB])));
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < XC; ++i)
+      dma16(xsrc[i] + min(k0 + xch[i], d_in - PER),
+            __builtin_amdgcn_readfirstlane(lds_addr(&xs[b][8 * (XC * wave + i) * RB])));
+#pragma unroll
+    for (int i = 0; i < AC; ++i)
       dma16(asrc[i] + min(k0 + ach[i], d_in - PER),
             __builtin_amdgcn_readfirstlane(lds_addr(&as[b][(32 * wave + 8 * i) * RB])));
   };
 
-  f32x4 acc[2][4];
+  f32x4 acc[JN][4];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < JN; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  if (nst > 0) issue(0);
-  for (int st = 0; st < nst; ++st) {
-    // this wave's copies of stage st are done; the barrier publishes them and
-    // tells that stage st - 1's buffer is no longer read
-    wait_vmcnt<0>();
+#pragma unroll
+  for (int s = 0; s < NBUF - 1; ++s)
+    if (s < nst) issue(s);
+  // this wave's copies of stage st are done once at most those of the stages
+  // issued after it are outstanding; the barrier publishes every wave's
+  // copies and tells that stage st - 1's buffer is no longer read
+  auto begin_stage = [&](int st) {
+    wait_vmcnt_upto<(NBUF - 2) * CP>(min(NBUF - 2, nst - 1 - st) * CP);
     __syncthreads();
-    if (st + 1 < nst) issue(st + 1);
+    if (st + NBUF - 1 < nst) issue(st + NBUF - 1);
+  };
+  // fragments of K-block kb (chunks 4 kb + g) of stage st; with MASK the
+  // chunks past d_in (copies of the last one) read as zero
+  auto read_kb = [&](int st, int kb, bool mask, F (&xf)[JN], F (&af)[4]) {
     const int b = st % NBUF;
+    const int cc = 4 * kb + g;
+    const bool kin = !mask || st * KS + PER * cc < d_in;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      // chunk 4 kb + g of this stage holds k = st*KS + KB*kb + PER*g .. (a
-      // full chunk or none)
-      const int cc = 4 * kb + g;
-      const bool kin = st * KS + PER * cc < d_in;
-      F xf[2], af[4];
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int r = wn + 16 * j + c16;
-        const F v = *reinterpret_cast<const F*>(&xs[b][r * RB + 16 * (cc ^ cka_sw(r))]);
-        xf[j] = kin ? v : Tr<T>::zero();
-      }
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int r = wc + 16 * j + c16;
-        const F v = *reinterpret_cast<const F*>(&as[b][r * RB + 16 * (cc ^ cka_sw(r))]);
-        af[j] = kin ? v : Tr<T>::zero();
-      }
-#pragma unroll
-      for (int jn = 0; jn < 2; ++jn)
-#pragma unroll
-        for (int jc = 0; jc < 4; ++jc) acc[jn][jc] = Tr<T>::mma(xf[jn], af[jc], acc[jn][jc]);
+    for (int j = 0; j < JN; ++j) {
+      const int r = wn + 16 * j + c16;
+      xf[j] = *reinterpret_cast<const F*>(&xs[b][r * RB + 16 * (cc ^ cka_sw(r))]);
+      if (mask && !kin) xf[j] = Tr<T>::zero();
     }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = wc + 16 * j + c16;
+      af[j] = *reinterpret_cast<const F*>(&as[b][r * RB + 16 * (cc ^ cka_sw(r))]);
+      if (mask && !kin) af[j] = Tr<T>::zero();
+    }
+  };
+  auto mma_kb = [&](const F (&xf)[JN], const F (&af)[4]) {
+#pragma unroll
+    for (int jn = 0; jn < JN; ++jn)
+#pragma unroll
+      for (int jc = 0; jc < 4; ++jc) acc[jn][jc] = Tr<T>::mma(xf[jn], af[jc], acc[jn][jc]);
+  };
+  // whole stages: both K-blocks' fragments are read before the matrix work,
+  // with no masks (no branches around the reads)
+  const int nst_full = d_in / KS;
+  for (int st = 0; st < nst_full; ++st) {
+    begin_stage(st);
+    F x0[JN], a0[4], x1[JN], a1[4];
+    read_kb(st, 0, false, x0, a0);
+    read_kb(st, 1, false, x1, a1);
+    mma_kb(x0, a0);
+    mma_kb(x1, a1);
+  }
+  if (nst_full < nst) {   // the last stage reaches past d_in
+    const int st = nst_full;
+    begin_stage(st);
+    F x0[JN], a0[4], x1[JN], a1[4];
+    read_kb(st, 0, true, x0, a0);
+    read_kb(st, 1, true, x1, a1);
+    mma_kb(x0, a0);
+    mma_kb(x1, a1);
   }
   // acc[jn][jc] element v = P[n][c] with n = n0+wn+16jn+4g+v, c = c0+wc+16jc+c16:
   // four consecutive probe rows of Pt row c per lane
 #pragma unroll
-  for (int jn = 0; jn < 2; ++jn)
+  for (int jn = 0; jn < JN; ++jn)
 #pragma unroll
     for (int jc = 0; jc < 4; ++jc) {
       const int c = c0 + wc + 16 * jc + c16, n = n0 + wn + 16 * jn + 4 * g;
@@ -481,9 +520,19 @@ __global__ __launch_bounds__(kThreads) void cka_gram_kernel<false>(CkaArgs a) {
 
 // Thread e: element (e / R, e % R) of M when it lies on or above the
 // diagonal (the Gram writes every such element), the sum of its chunks'
-// partials in chunk order.
+// partials in chunk order.  With GB, the last E x nbo blocks of the grid
+// form the partials of G_e = B_e^T B_e for ranks up to 8 instead (see
+// bgram_small), so that the two small passes share one launch.
+__device__ void bgram_small(const CkaArgs& a, int e);
+
+template <bool GB>
 __global__ __launch_bounds__(kThreads) void cka_msum_kernel(CkaArgs a) {
   const int R = a.R;
+  const int mblocks = (int)(((long)R * R + kThreads - 1) / kThreads);
+  if (GB && (int)blockIdx.x >= mblocks) {
+    bgram_small(a, (int)blockIdx.x - mblocks);
+    return;
+  }
   const long e = (long)blockIdx.x * kThreads + threadIdx.x;
   if (e >= (long)R * R) return;
   const int row = (int)(e / R), col = (int)(e % R);
@@ -518,6 +567,38 @@ __global__ __launch_bounds__(kThreads) void cka_bgram_kernel(CkaArgs a) {
     float acc = 0.f;
     for (int o = 0; o < rows; ++o) acc += bs[o * r + p] * bs[o * r + q];
     a.Gb[((size_t)e * a.nbo + c) * rr + pq] = acc;
+  }
+}
+
+// Ranks up to 8: block (e, c) of the msum launch forms the partial G_e over
+// rows c*kBO .. of B_e (like cka_bgram).  The chunk is staged in LDS as fp32;
+// lane t of wave w sums B[o][p] B[o][q], (p, q) = (t / r, t % r), over the
+// chunk rows o = w, w + 4, ... in order, and the four waves' sums are added in
+// wave order (deterministic).
+template <typename T>
+__device__ void bgram_small_t(const CkaArgs& a, int blk) {
+  __shared__ float bs[kBO * 8];
+  __shared__ float wsum[kThreads / 64][64];
+  const int e = blk / a.nbo, c = blk % a.nbo;
+  const int r = a.r, rr = r * r;
+  const int o0 = c * kBO, rows = min(kBO, a.d_out - o0);
+  const T* B = static_cast<const T*>(a.B) + (size_t)a.d_out * r * e + (size_t)o0 * r;
+  for (int i = threadIdx.x; i < rows * r; i += kThreads) bs[i] = (float)B[i];
+  __syncthreads();
+  const int t = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  float acc = 0.f;
+  if (t < rr) {
+    const int p = t / r, q = t % r;
+#pragma unroll 8
+    for (int o = wave; o < rows; o += kThreads / 64) acc += bs[o * r + p] * bs[o * r + q];
+  }
+  wsum[wave][t] = acc;
+  __syncthreads();
+  if (threadIdx.x < rr) {
+    float g = 0.f;
+#pragma unroll
+    for (int w = 0; w < kThreads / 64; ++w) g += wsum[w][threadIdx.x];
+    a.Gb[((size_t)e * a.nbo + c) * rr + threadIdx.x] = g;
   }
 }
 
@@ -566,10 +647,36 @@ __global__ __launch_bounds__(kThreads) void cka_pairs_kernel(CkaArgs a) {
 }
 
 // Ranks up to 8: one wave per expert pair i <= j, four pairs per block; lane
-// t < r * r holds element t of G_i, G_j and M_ij (wave-private LDS rows),
-// then the lanes' products are summed by shuffles.
+// t < r * r holds element t of G_i, G_j (chunk partials summed in order) and
+// of M_ij, M_ii, M_jj (wave-private LDS rows); the lanes' products are summed
+// by shuffles into num_ij, num_ii and num_jj, and the wave writes S_ij = S_ji
+// directly (num_ii is formed by the same code from the same operands in
+// every wave that needs it, so the diagonal agrees everywhere).
+__device__ inline float pair_num8(const float* Ga, const float* Mab, const float* Gb, int r, int t) {
+  float acc = 0.f;
+  if (t < r * r) {
+    const int p = t / r, q = t % r;
+    float t1 = 0.f, t2 = 0.f;
+    for (int u = 0; u < r; ++u) {
+      t1 += Ga[p * r + u] * Mab[u * r + q];   // (G_a M_ab)[p][q]
+      t2 += Mab[p * r + u] * Gb[u * r + q];   // (M_ab G_b)[p][q]
+    }
+    acc = t1 * t2;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 64);
+  return acc;
+}
+
+__device__ inline float cka_score(float nij, float nii, float njj) {
+  const float den = sqrtf(nii) * sqrtf(njj);
+  const float v = den > 0.f ? nij / den : 0.f;
+  return isfinite(v) ? v : 0.f;
+}
+
 __global__ __launch_bounds__(kThreads) void cka_pairs8_kernel(CkaArgs a) {
-  __shared__ float Gi[kThreads / 64][64], Gj[kThreads / 64][64], Mij[kThreads / 64][64];
+  __shared__ float Gi[kThreads / 64][64], Gj[kThreads / 64][64];
+  __shared__ float Mij[kThreads / 64][64], Mii[kThreads / 64][64], Mjj[kThreads / 64][64];
   const int wave = threadIdx.x >> 6, t = threadIdx.x & 63;
   const int pidx = blockIdx.x * (kThreads / 64) + wave;
   const bool live = pidx < a.E * (a.E + 1) / 2;   // wave-uniform
@@ -584,25 +691,21 @@ __global__ __launch_bounds__(kThreads) void cka_pairs8_kernel(CkaArgs a) {
     }
     Gi[wave][t] = gi;
     Gj[wave][t] = gj;
-    const int row = i * r + t / r, col = j * r + t % r;
+    const int p = t / r, q = t % r;
+    const int row = i * r + p, col = j * r + q;
     Mij[wave][t] = a.M[(size_t)min(row, col) * R + max(row, col)];
+    Mii[wave][t] = a.M[(size_t)(i * r + min(p, q)) * R + i * r + max(p, q)];
+    Mjj[wave][t] = a.M[(size_t)(j * r + min(p, q)) * R + j * r + max(p, q)];
   }
   __syncthreads();
-  float acc = 0.f;
-  if (live && t < rr) {
-    const int p = t / r, q = t % r;
-    float t1 = 0.f, t2 = 0.f;
-    for (int u = 0; u < r; ++u) {
-      t1 += Gi[wave][p * r + u] * Mij[wave][u * r + q];   // (G_i M_ij)[p][q]
-      t2 += Mij[wave][p * r + u] * Gj[wave][u * r + q];   // (M_ij G_j)[p][q]
-    }
-    acc = t1 * t2;
-  }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 64);
-  if (live && t == 0) {
-    a.num[(size_t)i * a.E + j] = acc;
-    a.num[(size_t)j * a.E + i] = acc;
+  if (!live) return;   // wave-uniform
+  const float nij = pair_num8(Gi[wave], Mij[wave], Gj[wave], r, t);
+  const float nii = pair_num8(Gi[wave], Mii[wave], Gi[wave], r, t);
+  const float njj = pair_num8(Gj[wave], Mjj[wave], Gj[wave], r, t);
+  if (t == 0) {
+    const float v = cka_score(nij, nii, njj);
+    a.S[(size_t)i * a.E + j] = v;
+    a.S[(size_t)j * a.E + i] = v;
   }
 }
 
@@ -611,9 +714,12 @@ __global__ __launch_bounds__(kThreads) void cka_score_kernel(CkaArgs a) {
   const int E = a.E;
   if (t >= E * E) return;
   const int i = t / E, j = t % E;
-  const float den = sqrtf(a.num[(size_t)i * E + i]) * sqrtf(a.num[(size_t)j * E + j]);
-  const float v = den > 0.f ? a.num[t] / den : 0.f;
-  a.S[t] = isfinite(v) ? v : 0.f;
+  a.S[t] = cka_score(a.num[t], a.num[(size_t)i * E + i], a.num[(size_t)j * E + j]);
+}
+
+__device__ void bgram_small(const CkaArgs& a, int e) {
+  if (a.bf16) bgram_small_t<__bf16>(a, e);
+  else bgram_small_t<float>(a, e);
 }
 
 template <typename T>
@@ -643,10 +749,11 @@ hipError_t launch_cka_t(const CkaProblem& p, void* ws, hipStream_t stream) {
   a.nbo = L.nbo;
   a.Phi = reinterpret_cast<__bf16*>(base + L.Phi);
   a.Plo = reinterpret_cast<__bf16*>(base + L.Plo);
+  a.bf16 = p.dtype == ACE_BF16 ? 1 : 0;
   const int R = a.R;
   if (p.N > 0) {
     dim3 grid((p.N + kPN - 1) / kPN, (R + kPC - 1) / kPC);
-    cka_project_kernel<T><<<grid, kPThreads, 0, stream>>>(a);
+    cka_project_kernel<T, kPN, kPBuf><<<grid, kPThreads, 0, stream>>>(a);
   }
   if (p.dtype == ACE_BF16)
     cka_mean_kernel<true><<<R, kThreads, 0, stream>>>(a);
@@ -659,13 +766,18 @@ hipError_t launch_cka_t(const CkaProblem& p, void* ws, hipStream_t stream) {
     const int nt = (R + kGT - 1) / kGT;
     cka_gram_kernel<false><<<dim3(nt * (nt + 1) / 2, L.splits), kThreads, 0, stream>>>(a);
   }
-  cka_msum_kernel<<<(int)(((long)R * R + kThreads - 1) / kThreads), kThreads, 0, stream>>>(a);
-  cka_bgram_kernel<T><<<dim3(p.E, L.nbo), kThreads, 0, stream>>>(a);
-  if (p.r <= 8)
+  const int mblocks = (int)(((long)R * R + kThreads - 1) / kThreads);
+  if (p.r <= 8) {
+    // B^T B partials in the msum launch, then one wave per pair writing the
+    // scores
+    cka_msum_kernel<true><<<mblocks + p.E * L.nbo, kThreads, 0, stream>>>(a);
     cka_pairs8_kernel<<<(p.E * (p.E + 1) / 2 + kThreads / 64 - 1) / (kThreads / 64), kThreads, 0, stream>>>(a);
-  else
+  } else {
+    cka_msum_kernel<false><<<mblocks, kThreads, 0, stream>>>(a);
+    cka_bgram_kernel<T><<<dim3(p.E, L.nbo), kThreads, 0, stream>>>(a);
     cka_pairs_kernel<<<p.E * (p.E + 1) / 2, kThreads, 0, stream>>>(a);
-  cka_score_kernel<<<(p.E * p.E + kThreads - 1) / kThreads, kThreads, 0, stream>>>(a);
+    cka_score_kernel<<<(p.E * p.E + kThreads - 1) / kThreads, kThreads, 0, stream>>>(a);
+  }
   return hipGetLastError();
 }
 
