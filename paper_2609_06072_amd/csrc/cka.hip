@@ -18,7 +18,7 @@
 //              tiles with two or three stages measured no faster)
 //   mean    -- the probe mean of every row of Pt; bf16 inputs: also the
 //              centred rows split as v = hi + lo (both bf16, |lo| <= 2^-9 |v|)
-//   gram    -- partial M over chunks of the probe: upper-triangle tiles
+//   gram    -- partial M over chunks of the probe (at least kGK rows): upper-triangle tiles
 //              (128 x 128 staged through LDS for bf16 inputs, 64 x 64 for
 //              fp32), one partial per chunk.  bf16 inputs:
 //              M = hi^T hi + hi^T lo + lo^T hi on the bf16 matrix cores (the
@@ -45,7 +45,8 @@ constexpr int kPC = 256;   // projection tile: adapter rows (eight waves)
 constexpr int kPThreads = 2 * kPC;
 constexpr int kGT = 64;    // Gram tile edge (fp32 inputs)
 constexpr int kGT2 = 128;  // Gram tile edge (bf16 inputs, staged through LDS)
-constexpr int kGK = 256;   // probe rows per Gram chunk (at least)
+constexpr int kGK = 400;   // probe rows per Gram chunk (at least)
+constexpr int kGBuf = 3;   // Gram stages in LDS (bf16 inputs; 96 KB: one block per CU)
 constexpr int kMaxSplits = 64;
 constexpr int kBO = 256;   // rows of B_e per B^T B chunk
 
@@ -328,12 +329,15 @@ __global__ __launch_bounds__(kThreads) void cka_gram_kernel(CkaArgs a);
 // stage, 32 probe rows of the hi and lo splits of the tile's 128 a rows and
 // 128 b rows (centred, zero past N) are copied global -> LDS with
 // global_load_lds_dwordx4 (64-byte rows, chunk l % 4 of a 16-row copy at
-// position (l % 4) ^ sw4(row)), two stages in LDS; every fragment read from
-// LDS feeds four MFMA tiles.  A chunk is a whole number of 32-row K-blocks,
+// position (l % 4) ^ sw4(row)), kGBuf stages in LDS (two in flight while one
+// is read); every fragment read from LDS feeds four MFMA tiles.  Chunks of
+// about 400 probe rows give 250 blocks at N = 10,000, one per CU (chunks of
+// 256 rows with two blocks per CU and two stages: 21 against 19 us).  A chunk is a whole number of 32-row K-blocks,
 // so nothing is masked.
 template <>
-__global__ __launch_bounds__(kThreads, 2) void cka_gram_kernel<true>(CkaArgs a) {
-  constexpr int NBUF = 2;
+__global__ __launch_bounds__(kThreads, kGBuf <= 2 ? 2 : 1) void cka_gram_kernel<true>(CkaArgs a) {
+  constexpr int NBUF = kGBuf;
+  static_assert(NBUF >= 2 && NBUF <= 4, "stages in LDS");
   constexpr int ROWS = kGT2;                  // rows of each operand tile
   constexpr int OB = ROWS * 64;               // bytes of one operand array per stage
   constexpr int STAGE = 4 * OB;               // a hi, a lo, b hi, b lo
@@ -375,11 +379,15 @@ __global__ __launch_bounds__(kThreads, 2) void cka_gram_kernel<true>(CkaArgs a) 
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  if (nst > 0) issue(0);
+#pragma unroll
+  for (int p = 0; p < NBUF - 1; ++p)
+    if (p < nst) issue(p);
   for (int st = 0; st < nst; ++st) {
-    wait_vmcnt<0>();
+    // this wave's copies of stage st are done once at most those of the
+    // stages issued after it are outstanding (eight per stage)
+    wait_vmcnt_upto<(NBUF - 2) * 8>(min(NBUF - 2, nst - 1 - st) * 8);
     __syncthreads();   // stage st landed everywhere; stage st - 1 is no longer read
-    if (st + 1 < nst) issue(st + 1);
+    if (st + NBUF - 1 < nst) issue(st + NBUF - 1);
     const char* S = sm + (st % NBUF) * STAGE;
     bf16x8 ah[4], al[4], bh[4], bl[4];
 #pragma unroll

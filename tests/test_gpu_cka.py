@@ -46,9 +46,11 @@ def _gpu_cka(pa):
 
 SMALL = [  # N, d_in, d_out, E, r: ragged against the projection tiles (64 probe
            # rows x 256 adapter rows), the Gram tiles (128 for bf16, 64 for
-           # fp32) and the probe chunks (256 rows or more); ranks up to 8
-           # take the one-wave pair kernel, larger ranks the block one
+           # fp32), the probe chunks (400 rows or more) and the 256-row chunks
+           # of B^T B; ranks up to 8 take the one-wave pair kernel (B^T B
+           # partials formed in the msum launch), larger ranks the block one
     (300, 40, 24, 6, 3),
+    (700, 72, 600, 7, 5),
     (1500, 136, 72, 9, 8),
     (130, 64, 16, 20, 16),
     (2100, 96, 40, 4, 64),
