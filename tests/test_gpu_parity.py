@@ -490,6 +490,26 @@ def test_wide_single_read_backward(d_ffn, path):
     check_dB_rows("dB", f64(out["dB"]), dB, c.ranks, c.d_out, tol)
 
 
+def test_wide_single_read_unweighted():
+    """The wide single-read backward on the grouped path without pair
+    weights, as the gate/up projections are timed: each row's partials (one
+    run over its pairs and 512-column blocks) are summed without per-pair
+    factors; rows serving two slots."""
+    cfg = W.CONFIGS["mixtral_bf16"].scaled(T=1500, d_model=136, d_ffn=4136)
+    c = make_case(cfg, "grouped", seed=13, with_w=False)
+    assert max(c.ranks) == 64 and c.pair_w is None
+    grp = c.rt.expert_to_group[c.rt.topk_ids]
+    assert (grp[:, 0] == grp[:, 1]).any()   # some rows serve both slots of a token
+    say(f"wide single-read backward, no pair weights T={cfg.T} d_out={c.d_out}")
+    out = run_gpu(c, reuse_h=True)
+    tol = TOL["bf16"]
+    dx, dA, dB = oracle_bwd(c)
+    check_all("dx", f64(out["dx"]), dx, tol)
+    check_all("dA", f64(out["dA"]), dA, tol)
+    check_rel("dB", f64(out["dB"]), dB, tol)
+    check_dB_rows("dB", f64(out["dB"]), dB, c.ranks, c.d_out, tol)
+
+
 def test_wide_single_read_empty_group():
     """The single-read backward at rank 64 (shared input, 1352 output
     columns) when one group has no pairs: its dA and dB are exactly zero,
