@@ -671,7 +671,7 @@ def traffic_pass(paths, labels_out: str):
 
 def short_kernel(name: str) -> str:
     import re
-    m = re.search(r"([a-z_]+_kernel)", name)
+    m = re.search(r"([a-z][a-z0-9_]*_kernel)", name)
     return m.group(1) if m else name.split("(")[0][:40]
 
 
