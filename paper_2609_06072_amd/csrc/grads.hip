@@ -680,6 +680,7 @@ __device__ __forceinline__ void wide_item(const GradArgs& a, WideSmem& sm, int q
     const int h = wave - kWideWaves / 2;
     const int rb0 = 2 * (h & 1), pb0 = h >> 1;
     const int nbW = (a.d_out + kWideCols - 1) / kWideCols;
+    const bool live0 = 16 * rb0 < r_q, live1 = 16 * (rb0 + 1) < r_q;   // wave-uniform
     bf16x8 bt[2][kWideCols / 32];
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
@@ -708,19 +709,22 @@ __device__ __forceinline__ void wide_item(const GradArgs& a, WideSmem& sm, int q
         const int kk = st * RS + r;   // chunk index of this lane's pair (rows past nk are copies)
         if (kk < nk) {
           float* dst = a.dHp + ((size_t)(kfirst + kk) * nbW + cbw) * (16 * RB) + 16 * rb0 + 4 * g;
-#pragma unroll
-          for (int i = 0; i < 2; ++i) *reinterpret_cast<f32x4*>(dst + 16 * i) = hv[i];
+          *reinterpret_cast<f32x4*>(dst) = hv[0];
+          if (live1) *reinterpret_cast<f32x4*>(dst + 16) = hv[1];
         }
       }
     };
+    // rank blocks at or past r_q are neither formed nor stored (the reduce
+    // reads no rank at or past r_q): a key of rank 16 or 32 writes a quarter
+    // or a half of the 64-rank partials
     for (int st = 0; st < nst_full; ++st) {
       begin_stage(st);
-      dh_part(st, st & 1);
+      if (live0) dh_part(st, st & 1);
     }
     if (nst_full < nst) {
       const int st = nst_full;
       begin_stage(st);
-      dh_part(st, st & 1);
+      if (live0) dh_part(st, st & 1);
     }
   }
 }
@@ -852,8 +856,11 @@ __global__ __launch_bounds__(kWThreads) void dh_reduce_wide_kernel(DhReduceArgs 
     const int q = upper_index(seg, n_keys, u);
     const int p0 = a.ppos ? a.ppos[u] : u, p1 = a.ppos ? a.ppos[u + 1] : u + 1;
     const f32x4* src = reinterpret_cast<const f32x4*>(a.dHp + (size_t)p0 * nbW * 64) + quad;
+    const int r_q = a.keys.rank[q], roff = a.keys.roff[q];
     f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (!a.pair_w) {
+    if (r0 >= r_q) {
+      // ranks past r_q: the wide items wrote no partials there
+    } else if (!a.pair_w) {
       const int n = (p1 - p0) * nbW;   // pieces of the row's run
       for (int c0 = 0; c0 < n; c0 += NL) {
         f32x4 t[NL];
@@ -880,7 +887,6 @@ __global__ __launch_bounds__(kWThreads) void dh_reduce_wide_kernel(DhReduceArgs 
         acc += v * w;
       }
     }
-    const int r_q = a.keys.rank[q], roff = a.keys.roff[q];
     const float s = a.alpha / (float)r_q;
 #pragma unroll
     for (int e = 0; e < 4; ++e) acc[e] = r0 + e < r_q ? acc[e] * s : 0.f;

@@ -490,6 +490,24 @@ def test_wide_single_read_backward(d_ffn, path):
     check_dB_rows("dB", f64(out["dB"]), dB, c.ranks, c.d_out, tol)
 
 
+@pytest.mark.parametrize("with_w", [True, False])
+def test_wide_single_read_mixed_ranks(with_w):
+    """The wide single-read backward with group ranks 16, 32 and 64 in one
+    call (uneven groups): partials past a key's rank are neither written nor
+    read, and every row's dH, dA and dB still match."""
+    cfg = W.CONFIGS["deepseek_bf16"].scaled(T=400, d_model=136, d_ffn=1352)
+    c = make_case(cfg, "grouped", seed=17, with_w=with_w)
+    assert max(c.ranks) == 64 and min(c.ranks) < 64 and c.d_out == 1352
+    say(f"wide single-read backward, ranks {sorted(set(c.ranks))} d_out={c.d_out} w={with_w}")
+    out = run_gpu(c, reuse_h=True)
+    tol = TOL["bf16"]
+    dx, dA, dB = oracle_bwd(c)
+    check_all("dx", f64(out["dx"]), dx, tol)
+    check_all("dA", f64(out["dA"]), dA, tol)
+    check_rel("dB", f64(out["dB"]), dB, tol)
+    check_dB_rows("dB", f64(out["dB"]), dB, c.ranks, c.d_out, tol)
+
+
 def test_wide_single_read_unweighted():
     """The wide single-read backward on the grouped path without pair
     weights, as the gate/up projections are timed: each row's partials (one
