@@ -166,7 +166,7 @@ struct GradArgs {
   int32_t nbB, nbA;           // column blocks of dB / dA (set by the launcher)
   int32_t split;              // contraction indices per item: 0 (1024), 1024 or 2048
   int32_t split_b;            // the same for the dB items: 0 (= split), or a multiple of 64
-                              //   from 512 to 2048
+                              //   from 512 to 4096
   int32_t* itab;              // item table written by the gradient launch for the reduce
                               //   (set by the launcher, after the partials)
   // phase 0: dB and dA items.  phase 1 (bf16, r_max <= 16): dB items only, each

@@ -43,6 +43,7 @@ constexpr int kColBlk = kGradColBlk;   // gradient columns per item
 constexpr int kSplitRows = 1024;
 constexpr int kMaxSplit = 2048;
 constexpr int kMinSplit = 512;    // dB items of the wide single read at narrow outputs
+constexpr int kMaxSplitB = 4096;  // dB items of the wide single read at wide outputs
 
 // Item table shared by the gradient kernels.  For key q the dB contraction
 // runs over bseg[q] .. bseg[q+1] and the dA contraction over aseg[q] ..
@@ -1380,7 +1381,7 @@ bool normalize_splits(GradArgs& g) {
   if (g.split == 0) g.split = kSplitRows;
   if (g.split_b == 0) g.split_b = g.split;
   return (g.split == kSplitRows || g.split == kMaxSplit) && g.split_b >= kMinSplit &&
-         g.split_b <= kMaxSplit && g.split_b % 64 == 0;
+         g.split_b <= kMaxSplitB && g.split_b % 64 == 0;
 }
 
 // Bytes of split partials (the item table follows them): bounded for the

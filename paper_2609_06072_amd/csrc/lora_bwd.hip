@@ -56,6 +56,7 @@ constexpr int kSharedDhMinOut = 1280;
 bool wide_dh(int r_max, int d_out) { return rank_blocks(r_max) == 4 && d_out >= kSharedDhMinOut; }
 // outputs below this many columns take dB items of 512 pairs on the wide path
 constexpr int kWideLongOut = 4096;
+constexpr int kWideSplitB = 4096;   // dB chunk of the wide items from kWideLongOut columns
 
 // Workspace regions for element size es: At [d_in][R], Bt [R][d_out],
 // Ht/dHt [R][ldh] (column = row index inside the key's segment), dense dH
@@ -491,6 +492,12 @@ hipError_t launch_bwd_t(const Problem& p, const void* dy, void* dx, float* dA, f
         gr.split_b = sb;
         break;
       }
+  } else if (wide) {
+    // wide outputs: chunks of up to 4096 pairs halve the dB partials against
+    // 2048; the items' critical path is the same, since at 2048 most blocks
+    // take two items (Mixtral-like: 224 items of 4096 pairs, one per CU,
+    // against 448 of 2048)
+    gr.split_b = kWideSplitB;
   }
   if ((p.dtype == ACE_BF16 && (p.per_pair || p.d_out >= kSharedDhMinOut) && p.r_max <= kFusedDhMaxRank) ||
       wide) {
