@@ -508,6 +508,23 @@ def test_wide_single_read_mixed_ranks(with_w):
     check_dB_rows("dB", f64(out["dB"]), dB, c.ranks, c.d_out, tol)
 
 
+def test_wide_single_read_long_chunks():
+    """From 4096 output columns the dB items take chunks of up to 4096 pairs:
+    with about 4600 pairs per group key each key splits into two chunks
+    whose partials are summed by the reduce (every element checked)."""
+    cfg = W.CONFIGS["mixtral_bf16"].scaled(T=4600, d_model=136, d_ffn=4136)
+    c = make_case(cfg, "grouped", seed=18, with_w=True)
+    assert max(c.ranks) == 64 and c.d_out >= 4096
+    say(f"wide single-read backward, long chunks T={cfg.T} d_out={c.d_out}")
+    out = run_gpu(c, reuse_h=True)
+    tol = TOL["bf16"]
+    dx, dA, dB = oracle_bwd(c)
+    check_all("dx", f64(out["dx"]), dx, tol)
+    check_all("dA", f64(out["dA"]), dA, tol)
+    check_rel("dB", f64(out["dB"]), dB, tol)
+    check_dB_rows("dB", f64(out["dB"]), dB, c.ranks, c.d_out, tol)
+
+
 def test_wide_single_read_unweighted():
     """The wide single-read backward on the grouped path without pair
     weights, as the gate/up projections are timed: each row's partials (one
